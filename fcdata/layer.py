@@ -1,0 +1,101 @@
+"""Seeded decoder-layer inputs: bf16 weights, hidden states, cache contents, masks.
+
+bf16 values are carried as raw uint16 bit patterns so both sides see exactly the
+same numbers (the oracle upcasts them to float32 exactly).  The weight layout is
+row-major [out, in], like torch.nn.Linear.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class LayerShape:
+    d: int          # hidden size
+    n_heads: int    # query heads
+    n_kv: int       # key/value heads
+    hd: int         # head dim
+    ffn: int        # SwiGLU intermediate size
+    eps: float = 1e-6
+    theta: float = 1e6
+
+    @property
+    def qkv(self) -> int:
+        return (self.n_heads + 2 * self.n_kv) * self.hd
+
+
+# Toy block (4 heads x 64, MHA) and the Qwen2.5-VL-7B LLM block shape.
+TINY_LAYER = LayerShape(d=256, n_heads=4, n_kv=4, hd=64, ffn=1024)
+QWEN_LAYER = LayerShape(d=3584, n_heads=28, n_kv=4, hd=128, ffn=18944)
+
+
+def bf16_round(a: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = ((u >> 16) & 1) + np.uint32(0x7FFF)
+    return ((u + r) >> 16).astype(np.uint16)
+
+
+def bf16_to_f32(u: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> float32 (exact)."""
+    return (np.asarray(u, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def _normal_bf16(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    return bf16_round(rng.standard_normal(shape, dtype=np.float32) * np.float32(std))
+
+
+def layer_weights(seed: int, shape: LayerShape, std: float = 0.02) -> dict:
+    """Random-init weights of one pre-norm SwiGLU decoder block, bf16 bit patterns.
+
+    Linear weights and the q/k/v biases are N(0, std); RMSNorm gains are 1.
+    Keys: w_qkv [qkv, d] (rows q | k | v), b_qkv [qkv], w_o [d, n_heads*hd],
+    w_gate [ffn, d], w_up [ffn, d], w_down [d, ffn], g_attn [d], g_mlp [d].
+    """
+    rng = np.random.default_rng(seed)
+    one = bf16_round(np.ones(shape.d, np.float32))
+    return dict(
+        w_qkv=_normal_bf16(rng, (shape.qkv, shape.d), std),
+        b_qkv=_normal_bf16(rng, (shape.qkv,), std),
+        w_o=_normal_bf16(rng, (shape.d, shape.n_heads * shape.hd), std),
+        w_gate=_normal_bf16(rng, (shape.ffn, shape.d), std),
+        w_up=_normal_bf16(rng, (shape.ffn, shape.d), std),
+        w_down=_normal_bf16(rng, (shape.d, shape.ffn), std),
+        g_attn=one.copy(),
+        g_mlp=one.copy(),
+    )
+
+
+def layer_state(seed: int, shape: LayerShape, n_prefix: int, n_frame: int,
+                delta: float = 0.1) -> dict:
+    """Hidden states for one layer call: prefix rows (text + history frames) and the
+    current frame at the previous step, both N(0, 1); the current frame now is
+    x_prev + delta * N(0, 1).  All bf16 bit patterns, [rows, d].
+    """
+    rng = np.random.default_rng(seed)
+    prefix = rng.standard_normal((n_prefix, shape.d), dtype=np.float32)
+    x_prev = rng.standard_normal((n_frame, shape.d), dtype=np.float32)
+    x_cur = x_prev + np.float32(delta) * rng.standard_normal((n_frame, shape.d), dtype=np.float32)
+    return dict(prefix=bf16_round(prefix), x_prev=bf16_round(x_prev), x_cur=bf16_round(x_cur))
+
+
+def text_kv(seed: int, shape: LayerShape, rows: int, std: float = 1.0):
+    """Seeded K/V cache contents (bf16 bit patterns, [rows, n_kv, hd] each), used as
+    the prompt/pre-history state of an episode's caches."""
+    rng = np.random.default_rng(seed)
+    k = _normal_bf16(rng, (rows, shape.n_kv, shape.hd), std)
+    v = _normal_bf16(rng, (rows, shape.n_kv, shape.hd), std)
+    return k, v
+
+
+def random_reuse_ids(seed: int, n_tokens: int, reuse_percent: int) -> np.ndarray:
+    """Recompute ids (int32, ascending) for a random mask that reuses
+    floor(reuse_percent * n_tokens / 100) tokens drawn from a seeded permutation."""
+    rng = np.random.default_rng(seed)
+    k = (reuse_percent * n_tokens) // 100
+    perm = rng.permutation(n_tokens)
+    reused = np.zeros(n_tokens, bool)
+    reused[perm[:k]] = True
+    return np.flatnonzero(~reused).astype(np.int32)

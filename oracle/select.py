@@ -1,0 +1,347 @@
+"""FreqCache cacheable-token selection -- CPU oracle, float64.
+
+TEST INFRASTRUCTURE ONLY.  This module is the plain, slow reference that the
+HIP path is checked against.  Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import it; the product path never does.  It
+shares no code, tables or constants with the HIP sources.
+
+Every transform is written as its textbook definition (matrix DFT, matrix
+DCT-II), not as a fast algorithm.  Step names (O1..O19) follow the order in
+which the paper computes things:
+
+  Module I   (Sec. 4.1, Eqs. 3-2, 3-3, 4-1, 4-2): amplitude spectra, global
+             spectral similarity and the migration gate, phase correlation for
+             the displacement, alignment mask;
+  Module II  (Sec. 4.2, Eqs. 3-4, 3-5, 4-3): block DCT, high-pass energy, the
+             mean + lambda * std refresh rule;
+  Module III (Sec. 4.3, Eqs. 3-6, 4-4): spectral entropy and adaptive budget;
+  Fusion     (Sec. 4.4, Algorithm 1): candidates, ascending-energy top-K.
+
+Readings where the paper is silent or garbled (each is listed in the design doc):
+  * colour -> one channel: BT.601 luma of the [0,1] RGB frame;
+  * DFT unnormalised; DCT-II orthonormal;
+  * "feature maps" of Modules I/III: the token-grid map of mean luma;
+  * the entropy formula missing from Eq. 3-6: Shannon entropy of the
+    normalised power, divided by ln(M) (M = grid bins) when entropy_norm;
+  * std is the population std; E below 1e-8 * m^2 is snapped to exactly 0;
+  * phase-correlation guard |X| <= 1e-9 max|X| -> 0, real part, first
+    (lowest row-major) index on ties, signed wrap keeping +G/2 positive;
+  * a missing previous frame is treated as an all-zero previous frame.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+@dataclass
+class SelectParams:
+    """Selection hyper-parameters.  Defaults are the paper's chosen values
+    (Sec. 6.4: tau_mig = 0.12, lambda = 0.25, alpha_max = 0.5, alpha_min = 0.08)."""
+    patch: int = 14
+    merge: int = 1
+    tau_mig: float = 0.12
+    lam: float = 0.25
+    alpha_min: float = 0.08
+    alpha_max: float = 0.5
+    adaptive: bool = True          # False: fixed reuse ratio alpha_fixed (ablation "w/o III")
+    alpha_fixed: float = 0.5
+    entropy_norm: bool = True
+    tau_sim: float = 0.0           # per-token similarity floor; 0 is exact Algorithm 1
+
+
+# ---------------------------------------------------------------- O1, O2: luma and tiling
+def luma(frame: np.ndarray) -> np.ndarray:
+    """O1: BT.601 luma of a [3, H, W] RGB frame, float64."""
+    f = np.asarray(frame, dtype=np.float64)
+    return 0.299 * f[0] + 0.587 * f[1] + 0.114 * f[2]
+
+
+def patches(y: np.ndarray, p: int) -> np.ndarray:
+    """O2: non-overlapping P x P patches p_(i,j) of an [H, W] map -> [H/P, W/P, P, P]
+    (grid partition of Sec. 3.2)."""
+    h, w = y.shape
+    return y.reshape(h // p, p, w // p, p).transpose(0, 2, 1, 3)
+
+
+# ---------------------------------------------------------------- transforms (definitions)
+def dft_matrix(n: int) -> np.ndarray:
+    """W[u, y] = exp(-2 pi i u y / n), the 1-D DFT as a matrix (exact phase index)."""
+    k = np.arange(n)
+    ang = 2.0 * np.pi * ((k[:, None] * k[None, :]) % n) / n
+    return np.cos(ang) - 1j * np.sin(ang)
+
+
+def dft2(x: np.ndarray) -> np.ndarray:
+    """2-D DFT of the last two axes, X(u,v) = sum_{y,x} x(y,x) e^{-2 pi i (uy/H + vx/W)}."""
+    wh = dft_matrix(x.shape[-2])
+    ww = dft_matrix(x.shape[-1])
+    return wh @ x @ ww.T
+
+
+def idft2(x: np.ndarray) -> np.ndarray:
+    """Inverse 2-D DFT (with the 1/(H W) factor)."""
+    h, w = x.shape[-2:]
+    wh = np.conj(dft_matrix(h))
+    ww = np.conj(dft_matrix(w))
+    return (wh @ x @ ww.T) / (h * w)
+
+
+def dct_matrix(n: int) -> np.ndarray:
+    """Orthonormal DCT-II: C[k, j] = s_k cos(pi (2j + 1) k / (2n)), s_0 = sqrt(1/n),
+    s_k = sqrt(2/n)."""
+    k = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    c = np.cos(np.pi * (2 * j + 1) * k / (2 * n))
+    s = np.full((n, 1), np.sqrt(2.0 / n))
+    s[0, 0] = np.sqrt(1.0 / n)
+    return s * c
+
+
+def high_pass(p: int) -> np.ndarray:
+    """Eq. 3-4: H(u,v) = 0 iff u < c and v < c, c = max(1, floor(P/4)); else 1."""
+    c = max(1, p // 4)
+    h = np.ones((p, p))
+    h[:c, :c] = 0.0
+    return h
+
+
+# ---------------------------------------------------------------- per-patch quantities
+def patch_amplitude(pt: np.ndarray) -> np.ndarray:
+    """O3, Eq. 3-2: amplitude spectrum A = sqrt(R^2 + I^2) of each patch's 2-D DFT."""
+    return np.abs(dft2(pt))
+
+
+def patch_energy(pt: np.ndarray) -> np.ndarray:
+    """O14-O15, Eqs. 3-4/3-5: E = sum_{u,v} (H(u,v) D(u,v))^2 with D the patch's
+    2-D DCT-II."""
+    p = pt.shape[-1]
+    c = dct_matrix(p)
+    d = c @ pt @ c.T
+    return np.sum((high_pass(p) * d) ** 2, axis=(-1, -2))
+
+
+def token_view(a: np.ndarray, m: int) -> np.ndarray:
+    """Group a per-patch array [Gp_h, Gp_w, ...] into tokens of m x m patches:
+    -> [Gp_h/m, Gp_w/m, m*m, ...] with the m*m sub-patches in row-major order."""
+    gh, gw = a.shape[:2]
+    rest = a.shape[2:]
+    t = a.reshape(gh // m, m, gw // m, m, *rest)
+    t = np.moveaxis(t, 2, 1)           # [I, J, a, b, ...]
+    return t.reshape(gh // m, gw // m, m * m, *rest)
+
+
+# ---------------------------------------------------------------- Module III
+def spectral_entropy(f_cur: np.ndarray, normalise: bool) -> float:
+    """O9, Eq. 3-6: P = |F|^2 / sum |F|^2 and Psi = -sum P ln P (0 ln 0 = 0),
+    divided by ln(M) when `normalise` (M = number of bins)."""
+    pw = np.abs(f_cur) ** 2
+    tot = pw.sum()
+    if tot <= 0.0:
+        return 0.0
+    pr = (pw / tot).ravel()
+    nz = pr[pr > 0]
+    psi = float(-np.sum(nz * np.log(nz)))
+    if normalise:
+        m = pr.size
+        psi = psi / np.log(m) if m > 1 else 0.0
+    return psi
+
+
+def reuse_budget(psi: float, n_tokens: int, prm: SelectParams):
+    """O10, Eq. 4-4: alpha_t = a_min + (a_max - a_min) e^{-Psi}; K_reuse = floor(alpha_t N)."""
+    if prm.adaptive:
+        alpha = prm.alpha_min + (prm.alpha_max - prm.alpha_min) * np.exp(-psi)
+    else:
+        alpha = prm.alpha_fixed
+    return float(alpha), int(np.floor(alpha * n_tokens))
+
+
+# ---------------------------------------------------------------- Module I
+def global_similarity(f_cur: np.ndarray, f_prev: np.ndarray) -> float:
+    """O7, Eq. 3-3 on the global spectra: cosine of the amplitude spectra
+    (all bins, DC included); 0 if either spectrum is zero."""
+    a = np.abs(f_cur).ravel()
+    b = np.abs(f_prev).ravel()
+    na, nb = np.sqrt(np.sum(a * a)), np.sqrt(np.sum(b * b))
+    if na == 0.0 or nb == 0.0:
+        return 0.0
+    return float(np.sum(a * b) / (na * nb))
+
+
+def phase_correlation(f_prev: np.ndarray, f_cur: np.ndarray):
+    """O11, Eq. 4-1: C = X / |X| with X = F(F_{t-1}) . conj(F(F_t)); the displacement
+    is the argmax of Re F^{-1}(C), wrapped to signed offsets.
+
+    Returns ((di, dj), response) where response is the real inverse transform.
+    """
+    x = f_prev * np.conj(f_cur)
+    mag = np.abs(x)
+    mx = mag.max()
+    c = np.zeros_like(x)
+    if mx > 0.0:
+        keep = mag > 1e-9 * mx
+        c[keep] = x[keep] / mag[keep]
+    r = np.real(idft2(c))
+    k = int(np.argmax(r))          # first maximum in row-major order
+    gh, gw = r.shape
+    ki, kj = divmod(k, gw)
+    di = ki if ki <= gh // 2 else ki - gh
+    dj = kj if kj <= gw // 2 else kj - gw
+    return (di, dj), r
+
+
+def align_mask(gh: int, gw: int, di: int, dj: int) -> np.ndarray:
+    """O12, Eq. 4-2: token (I, J) is aligned iff its source (I + di, J + dj) lies in
+    the previous token grid."""
+    i = np.arange(gh)[:, None] + di
+    j = np.arange(gw)[None, :] + dj
+    return ((i >= 0) & (i < gh) & (j >= 0) & (j < gw))
+
+
+def token_similarity(a_cur: np.ndarray, a_prev: np.ndarray, di: int, dj: int,
+                     aligned: np.ndarray) -> np.ndarray:
+    """O13: per-token Eq. 3-3 -- cosine between the current token's amplitude vector and
+    that of its source token in the previous frame; 0 when not aligned.  Both norms
+    zero -> 1, exactly one zero -> 0.  a_*: [Gh, Gw, L] token amplitude vectors."""
+    gh, gw = aligned.shape
+    sim = np.zeros((gh, gw))
+    for i in range(gh):
+        for j in range(gw):
+            if not aligned[i, j]:
+                continue
+            u = a_cur[i, j]
+            v = a_prev[i + di, j + dj]
+            nu, nv = np.sqrt(np.sum(u * u)), np.sqrt(np.sum(v * v))
+            if nu == 0.0 and nv == 0.0:
+                sim[i, j] = 1.0
+            elif nu == 0.0 or nv == 0.0:
+                sim[i, j] = 0.0
+            else:
+                sim[i, j] = np.sum(u * v) / (nu * nv)
+    return sim
+
+
+# ---------------------------------------------------------------- Module II
+def refresh_mask(e_tok: np.ndarray, lam: float):
+    """O16, Eq. 4-3: Mask_fresh = 1(E > mu_E + lambda sigma_E), population statistics
+    over all N tokens."""
+    mu = float(np.mean(e_tok))
+    sd = float(np.sqrt(np.mean((e_tok - mu) ** 2)))
+    thr = mu + lam * sd
+    return e_tok > thr, mu, sd, thr
+
+
+# ---------------------------------------------------------------- Fusion (Algorithm 1)
+def topk_ascending(cand: np.ndarray, key: np.ndarray, k: int) -> np.ndarray:
+    """O18: the k candidates with the smallest key, ties to the lower token id."""
+    ids = np.flatnonzero(cand)
+    order = sorted(ids.tolist(), key=lambda t: (key[t], t))
+    return np.asarray(order[:k], dtype=np.int64)
+
+
+@dataclass
+class SelectResult:
+    reuse_mask: np.ndarray        # [N] uint8, 1 = reuse cached token
+    recompute_idx: np.ndarray     # [N - K_final] int32, ascending
+    shift: tuple                  # (di, dj): token (I,J) reuses source (I+di, J+dj)
+    sim: np.ndarray               # [N] per-token aligned spectral similarity
+    energy: np.ndarray            # [N] token high-frequency energy
+    aligned: np.ndarray           # [N] bool
+    fresh: np.ndarray             # [N] bool
+    cand: np.ndarray              # [N] bool
+    sim_freq: float
+    psi: float
+    alpha: float
+    mu: float
+    sigma: float
+    thr: float
+    k_reuse: int
+    k_cand: int
+    k_final: int
+    flushed: bool
+    response: np.ndarray = field(repr=False, default=None)   # phase-correlation surface
+
+    @property
+    def n_recompute(self) -> int:
+        return int(self.recompute_idx.size)
+
+
+def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> SelectResult:
+    """Algorithm 1 for one frame pair ([3, H, W] each; prev may be None)."""
+    p, m = prm.patch, prm.merge
+    y_cur = luma(cur)
+    y_prev = luma(prev) if prev is not None else np.zeros_like(y_cur)
+    h, w = y_cur.shape
+    if h % (p * m) or w % (p * m):
+        raise ValueError("frame size must be a multiple of patch * merge")
+    pc, pp = patches(y_cur, p), patches(y_prev, p)
+    # O3/O4: per-patch amplitude spectra, grouped into token vectors
+    a_cur = token_view(patch_amplitude(pc), m)
+    a_prev = token_view(patch_amplitude(pp), m)
+    gh, gw = a_cur.shape[:2]
+    n = gh * gw
+    a_cur = a_cur.reshape(gh, gw, -1)
+    a_prev = a_prev.reshape(gh, gw, -1)
+    # O5/O6: token-grid mean-luma maps and their spectra
+    g_cur = token_view(pc.mean(axis=(-1, -2)), m).mean(axis=-1)
+    g_prev = token_view(pp.mean(axis=(-1, -2)), m).mean(axis=-1)
+    f_cur, f_prev = dft2(g_cur), dft2(g_prev)
+    # Module I
+    sim_freq = global_similarity(f_cur, f_prev)
+    flushed = sim_freq < prm.tau_mig
+    (di, dj), resp = phase_correlation(f_prev, f_cur)
+    aligned = align_mask(gh, gw, di, dj)
+    sim = token_similarity(a_cur, a_prev, di, dj, aligned)
+    # Module II
+    e_tok = token_view(patch_energy(pc), m).sum(axis=-1)
+    e_tok = np.where(e_tok < 1e-8 * m * m, 0.0, e_tok)
+    fresh, mu, sd, thr = refresh_mask(e_tok, prm.lam)
+    # Module III
+    psi = spectral_entropy(f_cur, prm.entropy_norm)
+    alpha, k_reuse = reuse_budget(psi, n, prm)
+    # Fusion
+    e_flat = e_tok.ravel()
+    cand = (aligned & ~fresh & (sim >= prm.tau_sim)).ravel()
+    k_cand = int(cand.sum())
+    reuse = np.zeros(n, np.uint8)
+    k_final = 0
+    if not flushed:
+        k_final = min(k_reuse, k_cand)
+        reuse[topk_ascending(cand, e_flat, k_final)] = 1
+    return SelectResult(
+        reuse_mask=reuse, recompute_idx=np.flatnonzero(reuse == 0).astype(np.int32),
+        shift=(int(di), int(dj)), sim=sim.ravel(), energy=e_flat, aligned=aligned.ravel(),
+        fresh=fresh.ravel(), cand=cand, sim_freq=sim_freq, psi=psi, alpha=alpha, mu=mu,
+        sigma=sd, thr=thr, k_reuse=k_reuse, k_cand=k_cand, k_final=k_final,
+        flushed=bool(flushed), response=resp)
+
+
+def select_batch(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> list:
+    """select_item over a [B, 3, H, W] batch."""
+    return [select_item(None if prev is None else prev[b], cur[b], prm)
+            for b in range(cur.shape[0])]
+
+
+def decision_margins(res: SelectResult, prm: SelectParams) -> dict:
+    """How close each of the oracle's decisions came to flipping (relative), for
+    auditing any mismatch against the GPU: a mismatch is tolerated only where the
+    oracle's own margin is below 1e-5."""
+    n = res.energy.size
+    thr = res.thr
+    thr_m = np.abs(res.energy - thr) / max(abs(thr), 1e-300)
+    ids = np.flatnonzero(res.cand)
+    keys = np.sort(res.energy[ids])
+    if 0 < res.k_final < keys.size:
+        a, b = keys[res.k_final - 1], keys[res.k_final]
+        topk_m = (b - a) / max(abs(b), 1e-300)
+    else:
+        topk_m = np.inf
+    an = res.alpha * n
+    budget_m = abs(an - np.round(an)) / max(an, 1e-300) if prm.adaptive else np.inf
+    gate_m = abs(res.sim_freq - prm.tau_mig) / prm.tau_mig
+    r = np.sort(res.response.ravel())
+    shift_m = (r[-1] - r[-2]) / max(abs(r[-1]), 1e-300) if r.size > 1 else np.inf
+    return dict(threshold=thr_m, topk=float(topk_m), budget=float(budget_m),
+                gate=float(gate_m), shift=float(shift_m))
