@@ -1,0 +1,199 @@
+/*
+ * freqcache.h -- C ABI of the FreqCache per-step hot path on AMD Instinct MI355X (gfx950).
+ *
+ * FreqCache (arXiv 2604.24391) decides, at every navigation step, which visual
+ * tokens of the current camera frame may reuse cached model results, and the
+ * model then recomputes only the others.  This library implements that step:
+ *
+ *   fc_select        frequency-guided cacheable-token selection (Sec. 4.1-4.4,
+ *                    Algorithm 1): per-patch DFT amplitude spectra of both
+ *                    frames, global spectral similarity and migration gate,
+ *                    phase-correlation displacement and alignment mask,
+ *                    block-DCT high-frequency energy and refresh mask,
+ *                    spectral-entropy reuse budget, ascending-energy top-K.
+ *   fc_cache_update  token-cache preparation for the new step: each reused
+ *                    token takes the cached rows of its aligned source token
+ *                    in the previous frame (Sec. 4.1, Eq. 4-2).
+ *   fc_layer_forward the partial-recompute decoder layer: only non-reused
+ *                    tokens are gathered through RMSNorm, QKV, attention over
+ *                    the full cached K/V, O-projection and the SwiGLU MLP, and
+ *                    scattered back into the token cache (Sec. 1, 2.2, 5.2).
+ *
+ * Conventions for every call:
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller allocates
+ *     and owns every buffer; the library never frees or keeps caller pointers
+ *     past the call.  A context owns only its workspace and constant tables,
+ *     sized once by fc_create, so no call allocates device memory.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the
+ *     default stream); results are valid once the stream reaches the call.
+ *     Nothing is read back to the host: counts produced by fc_select stay on
+ *     the device and fc_layer_forward reads them there.
+ *   - Argument and shape checks are synchronous and launch nothing.  Every call
+ *     returns an fc_status; on failure fc_last_error() describes it.  A launch
+ *     failure returns FC_ERR_HIP.  The library never aborts or exits.
+ *   - Identical inputs give byte-identical outputs (no floating-point atomics).
+ *   - A context must not be used from two host threads at once; calls on one
+ *     context that overlap on different streams race on its workspace.
+ *   - bf16 values are raw uint16_t bit patterns.  Matrices are row-major;
+ *     weights are [out][in] like torch.nn.Linear.
+ */
+#ifndef FREQCACHE_H
+#define FREQCACHE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct fc_ctx fc_ctx;
+
+typedef enum {
+  FC_OK = 0,
+  FC_ERR_INVALID_ARG = 1,   /* null pointer, out-of-range parameter        */
+  FC_ERR_SHAPE = 2,         /* sizes inconsistent with each other           */
+  FC_ERR_CAPACITY = 3,      /* sizes above what the context was created for */
+  FC_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed   */
+  FC_ERR_NO_DEVICE = 5,     /* no usable GPU                                */
+  FC_ERR_UNSUPPORTED = 6    /* a valid request this build does not handle   */
+} fc_status;
+
+/* Upper bounds fixed at context creation; they size the workspace.  (host) */
+typedef struct {
+  int32_t max_batch;        /* frame pairs / episodes per call                    */
+  int32_t max_height;       /* frame height in pixels                             */
+  int32_t max_width;        /* frame width in pixels                              */
+  int32_t max_tokens;       /* visual tokens per frame N (<= 1024)                */
+  int32_t max_seq;          /* cached sequence length S = T + W * N               */
+  int32_t max_d_model;      /* hidden size                                        */
+  int32_t max_ffn;          /* SwiGLU intermediate size                           */
+  int32_t max_qkv;          /* (n_heads + 2 n_kv_heads) * head_dim                */
+} fc_caps;
+
+/* Selection hyper-parameters.  (host; copied at call time)
+ * Defaults from the paper (Sec. 6.4): tau_mig 0.12, lambda 0.25, alpha_min 0.08,
+ * alpha_max 0.5. */
+typedef struct {
+  int32_t patch;            /* P, pixels per patch side (14); 2..32                         */
+  int32_t merge;            /* m, patches per token side (1 or 2)                           */
+  double tau_mig;           /* flush when Sim_freq < tau_mig (Sec. 4.1)                    */
+  double lambda_;           /* refresh when E > mu_E + lambda sigma_E (Eq. 4-3)            */
+  double alpha_min;         /* reuse-ratio bounds of Eq. 4-4                               */
+  double alpha_max;
+  int32_t adaptive;         /* 1: alpha from spectral entropy (Eq. 4-4); 0: alpha_fixed    */
+  double alpha_fixed;       /* fixed reuse ratio (the "w/o Module III" ablation, Table 3)  */
+  int32_t entropy_norm;     /* 1: entropy divided by ln(grid bins), so Psi is in [0, 1]    */
+  double tau_sim;           /* extra per-token similarity floor; 0 = exact Algorithm 1     */
+} fc_select_params;
+
+enum { FC_SCALAR_SIM_FREQ = 0, FC_SCALAR_PSI, FC_SCALAR_ALPHA, FC_SCALAR_MU,
+       FC_SCALAR_SIGMA, FC_SCALAR_THR, FC_NSCALARS };
+enum { FC_COUNT_K_REUSE = 0, FC_COUNT_K_CAND, FC_COUNT_K_FINAL, FC_COUNT_FLUSHED,
+       FC_NCOUNTS };
+enum { FC_FLAG_ALIGNED = 1, FC_FLAG_FRESH = 2, FC_FLAG_CAND = 4 };
+
+/* Outputs of fc_select; caller-allocated device buffers.  N = tokens per frame
+ * = (H / (P m)) * (W / (P m)); token ids are row-major on the token grid. */
+typedef struct {
+  float *sim;               /* [B][N] aligned per-token spectral similarity (Eq. 3-3 per token; 0 if unaligned) */
+  double *energy;           /* [B][N] token high-frequency energy (Eqs. 3-4/3-5; sum over the m*m patches)      */
+  uint8_t *reuse_mask;      /* [B][N] 1 = the token reuses its cached results (P_final of Algorithm 1)          */
+  int32_t *recompute_idx;   /* [B][N] ascending ids of recomputed tokens; the first n_recompute[b] are valid    */
+  int32_t *n_recompute;     /* [B]    N - K_final                                                               */
+  int32_t *shift;           /* [B][2] (di, dj): token (I, J) reuses source token (I + di, J + dj) (Eq. 4-1)     */
+  double *scalars;          /* [B][FC_NSCALARS] Sim_freq, Psi, alpha_t, mu_E, sigma_E, mu_E + lambda sigma_E    */
+  int32_t *counts;          /* [B][FC_NCOUNTS] K_reuse, K_candidate, K_final, flushed                          */
+  uint8_t *flags;           /* [B][N] optional (may be NULL): FC_FLAG_* bits of Mask_align, Mask_fresh, C       */
+} fc_select_out;
+
+/* One decoder block (pre-norm RMSNorm, q/k/v bias, rotate-half RoPE, GQA, SwiGLU).
+ * (host struct; the weight pointers are device pointers, bf16) */
+typedef struct {
+  int32_t d_model, n_heads, n_kv_heads, head_dim, d_ffn;
+  float rms_eps;            /* 1e-6 */
+  double rope_theta;        /* 1e6  */
+  const uint16_t *w_qkv;    /* [(n_heads + 2 n_kv_heads) head_dim][d_model], rows q | k | v */
+  const uint16_t *b_qkv;    /* [(n_heads + 2 n_kv_heads) head_dim]                          */
+  const uint16_t *w_o;      /* [d_model][n_heads head_dim]                                  */
+  const uint16_t *w_gate;   /* [d_ffn][d_model]                                             */
+  const uint16_t *w_up;     /* [d_ffn][d_model]                                             */
+  const uint16_t *w_down;   /* [d_model][d_ffn]                                             */
+  const uint16_t *g_attn;   /* [d_model] RMSNorm gain before attention                      */
+  const uint16_t *g_mlp;    /* [d_model] RMSNorm gain before the MLP                        */
+} fc_layer_desc;
+
+/* One layer's token cache.  Sequence layout: [T text tokens][W frame slots of N
+ * tokens].  The frame slots are a ring: physical slot p holds the frame with
+ * logical index (p - head) mod W (0 = oldest, W - 1 = current).  A key sits at
+ * position T + logical * N + token (text: its index), i.e. at its place in the
+ * current step's prompt.  K holds raw (pre-RoPE) keys; rotation happens on use,
+ * so advancing the window (head = (head + 1) mod W) moves no data.  (host struct) */
+typedef struct {
+  uint16_t *k;              /* [B][S][n_kv_heads][head_dim] bf16, S = T + W N */
+  uint16_t *v;              /* [B][S][n_kv_heads][head_dim] bf16              */
+  int32_t text_tokens;      /* T */
+  int32_t frame_tokens;     /* N */
+  int32_t window;           /* W >= 1 (frames kept, including the current one) */
+  int32_t head;             /* 0 <= head < W */
+} fc_kv_cache;
+
+/* Library version string. */
+const char *fc_version(void);
+
+/* Text of the last non-OK status returned on this host thread ("" if none). */
+const char *fc_last_error(void);
+
+/* Create a context on `device`, sizing its workspace for `caps` (host).
+ * Returns FC_ERR_NO_DEVICE when no GPU is visible. */
+fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps);
+fc_status fc_destroy(fc_ctx *ctx);
+
+/* Cacheable-token selection for B frame pairs (Algorithm 1 per pair).
+ *   frames_prev: [B][3][H][W] float32 RGB in [0, 1], or NULL (no previous frame:
+ *                treated as an all-zero frame, so the step is flushed, Sec. 4.1);
+ *   frames_cur:  [B][3][H][W] float32.
+ * H and W must be multiples of P m; N = (H/(P m)) (W/(P m)) <= 1024 and <= caps.
+ * Every field of `out` except `flags` must be non-NULL. */
+fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frames_prev,
+                    const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                    const fc_select_out *out, void *stream);
+
+/* Token-cache preparation for one layer at a new step.  The caller has already
+ * advanced kv->head, so the current frame lives in slot (head + W - 1) mod W and
+ * the previous frame in slot (head + W - 2) mod W (the same slot when W = 1).  For
+ * every token t with reuse_mask[b][t] = 1, the K/V rows of the current slot and
+ * y_cur[b][t] are copied from source token s = (I + di) grid_w + (J + dj) of the
+ * previous frame (K/V) and of y_prev.  Other rows are left untouched (the layer
+ * call rewrites them).
+ *   y_prev, y_cur: [B][N][d_model] bf16, distinct buffers;
+ *   shift [B][2], reuse_mask [B][N]: from fc_select; grid_w: token-grid width. */
+fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                          const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                          const uint8_t *reuse_mask, int32_t grid_w, int32_t B, void *stream);
+
+/* The partial-recompute decoder layer for B batch items.
+ *   x_cur:         [B][N][d_model] bf16 layer input of the current frame's tokens;
+ *                  only rows listed in recompute_idx are read;
+ *   recompute_idx: [B][N] ascending token ids, n_recompute: [B] (from fc_select);
+ *   kv:            this layer's cache; the K/V rows of recomputed tokens in the
+ *                  current slot are written, every row is attended;
+ *   y_cur:         [B][N][d_model] bf16 output cache; only recomputed rows are written.
+ * Queries attend causally by position; QKV of all recomputed tokens is written
+ * before any attention, so they see each other's new keys. */
+fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                           const uint16_t *x_cur, const int32_t *recompute_idx,
+                           const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
+                           void *stream);
+
+/* Kernel timing with HIP events recorded on the launch stream around every
+ * kernel the context launches (off by default). */
+fc_status fc_profile_enable(fc_ctx *ctx, int32_t on);
+/* Wait for the recorded events and return the summed duration and launch count
+ * of kernel `name` (host string) since the last reset; reset=1 clears all records. */
+fc_status fc_profile_read(fc_ctx *ctx, const char *name, double *total_ms, int64_t *launches,
+                          int32_t reset);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FREQCACHE_H */

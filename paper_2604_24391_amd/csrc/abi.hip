@@ -1,0 +1,315 @@
+// C ABI of the FreqCache hot path: argument validation, context and workspace,
+// error reporting and event-based kernel timing.  The kernels live in select.hip
+// and layer.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "fc_internal.h"
+
+namespace fc {
+
+static thread_local char g_err[1024] = "";
+
+void set_error(const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+fc_status fail(fc_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+ProfScope::ProfScope(fc_ctx *c, hipStream_t s, const char *name) : ctx(c), st(s) {
+  if (!ctx->prof) return;
+  hipEvent_t a, b;
+  if (ctx->pool.size() >= 2) {
+    a = ctx->pool.back();
+    ctx->pool.pop_back();
+    b = ctx->pool.back();
+    ctx->pool.pop_back();
+  } else {
+    if (hipEventCreate(&a) != hipSuccess) return;
+    if (hipEventCreate(&b) != hipSuccess) {
+      hipEventDestroy(a);
+      return;
+    }
+  }
+  hipEventRecord(a, st);
+  ctx->recs.push_back(ProfRec{name, a, b});
+  stop = b;
+}
+
+ProfScope::~ProfScope() {
+  if (stop) hipEventRecord(stop, st);
+}
+
+}  // namespace fc
+
+using fc::fail;
+
+namespace {
+
+const char *kVersion = "freqcache-mi355x 0.1 (gfx950)";
+
+template <typename T>
+fc_status dev_alloc(T **p, size_t count, const char *what) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  hipError_t e = hipMalloc(reinterpret_cast<void **>(p), count * sizeof(T));
+  if (e != hipSuccess)
+    return fail(FC_ERR_HIP, "hipMalloc(%s, %zu bytes): %s", what, count * sizeof(T),
+                hipGetErrorString(e));
+  return FC_OK;
+}
+
+void free_ws(fc_ctx *c) {
+  void *ptrs[] = {c->amp, c->pmean, c->penergy, c->aligned, c->qbuf, c->attn,
+                  c->h1,  c->inv2,  c->act,     c->part,    c->rope, c->stage};
+  for (void *p : ptrs)
+    if (p) hipFree(p);
+  for (auto &r : c->recs) {
+    hipEventDestroy(r.start);
+    hipEventDestroy(r.stop);
+  }
+  for (auto e : c->pool) hipEventDestroy(e);
+  c->recs.clear();
+  c->pool.clear();
+}
+
+fc_status use_device(fc_ctx *ctx) {
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return fail(FC_ERR_HIP, "hipSetDevice(%d): %s", ctx->device, hipGetErrorString(e));
+  return FC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fc_version(void) { return kVersion; }
+
+const char *fc_last_error(void) { return fc::g_err; }
+
+fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
+  if (!out || !caps) return fail(FC_ERR_INVALID_ARG, "fc_create: null out or caps");
+  *out = nullptr;
+  const fc_caps &c = *caps;
+  if (c.max_batch < 1 || c.max_height < 1 || c.max_width < 1 || c.max_tokens < 1 ||
+      c.max_seq < 1 || c.max_d_model < 1 || c.max_ffn < 1 || c.max_qkv < 1)
+    return fail(FC_ERR_INVALID_ARG, "fc_create: every cap must be >= 1");
+  if (c.max_tokens > fc::kMaxTokens)
+    return fail(FC_ERR_UNSUPPORTED, "fc_create: max_tokens %d > %d", c.max_tokens, fc::kMaxTokens);
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n < 1)
+    return fail(FC_ERR_NO_DEVICE, "fc_create: no HIP device (%s)",
+                e != hipSuccess ? hipGetErrorString(e) : "count 0");
+  if (device < 0 || device >= n)
+    return fail(FC_ERR_INVALID_ARG, "fc_create: device %d of %d", device, n);
+  e = hipSetDevice(device);
+  if (e != hipSuccess) return fail(FC_ERR_HIP, "hipSetDevice: %s", hipGetErrorString(e));
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return fail(FC_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(FC_ERR_UNSUPPORTED, "fc_create: device is %s, this build targets gfx950",
+                prop.gcnArchName);
+
+  fc_ctx *ctx = new (std::nothrow) fc_ctx();
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_create: out of host memory");
+  ctx->device = device;
+  ctx->caps = c;
+  ctx->num_cus = prop.multiProcessorCount;
+
+  const size_t B = c.max_batch;
+  const size_t np = (size_t)(c.max_height / fc::kPatch) * (c.max_width / fc::kPatch);
+  const size_t rows = B * c.max_tokens;
+  const size_t wide = std::max(c.max_qkv, c.max_d_model) + 64;
+  const size_t base = rows * wide;
+  const size_t cap = (size_t)96 << 20;
+  ctx->part_elems = base * std::min<size_t>(fc::kMaxSplits, std::max<size_t>(1, cap / base));
+  ctx->stage_elems = B * c.max_tokens * (size_t)c.max_qkv;
+  fc_status st = FC_OK;
+  if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np, "amp")) != FC_OK ||
+      (st = dev_alloc(&ctx->pmean, B * 2 * np, "pmean")) != FC_OK ||
+      (st = dev_alloc(&ctx->penergy, B * np, "penergy")) != FC_OK ||
+      (st = dev_alloc(&ctx->aligned, B * c.max_tokens, "aligned")) != FC_OK ||
+      (st = dev_alloc(&ctx->qbuf, rows * c.max_qkv, "q")) != FC_OK ||
+      (st = dev_alloc(&ctx->attn, rows * c.max_qkv, "attn")) != FC_OK ||
+      (st = dev_alloc(&ctx->h1, rows * c.max_d_model, "h1")) != FC_OK ||
+      (st = dev_alloc(&ctx->inv2, rows, "inv2")) != FC_OK ||
+      (st = dev_alloc(&ctx->act, rows * c.max_ffn, "act")) != FC_OK ||
+      (st = dev_alloc(&ctx->part, ctx->part_elems, "partials")) != FC_OK ||
+      (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||
+      (st = dev_alloc(&ctx->stage, ctx->stage_elems, "stage")) != FC_OK ||
+      (st = fc::upload_select_tables()) != FC_OK) {
+    free_ws(ctx);
+    delete ctx;
+    return st;
+  }
+  *out = ctx;
+  return FC_OK;
+}
+
+fc_status fc_destroy(fc_ctx *ctx) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_destroy: null context");
+  hipSetDevice(ctx->device);
+  hipDeviceSynchronize();
+  free_ws(ctx);
+  delete ctx;
+  return FC_OK;
+}
+
+fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frames_prev,
+                    const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                    const fc_select_out *out, void *stream) {
+  if (!ctx || !prm || !frames_cur || !out)
+    return fail(FC_ERR_INVALID_ARG, "fc_select: null context, params, current frames or outputs");
+  if (!out->sim || !out->energy || !out->reuse_mask || !out->recompute_idx || !out->n_recompute ||
+      !out->shift || !out->scalars || !out->counts)
+    return fail(FC_ERR_INVALID_ARG, "fc_select: an output buffer is null");
+  const fc_select_params &p = *prm;
+  if (p.patch != fc::kPatch)
+    return fail(FC_ERR_UNSUPPORTED, "fc_select: patch %d (this build implements P = 14)", p.patch);
+  if (p.merge < 1 || p.merge > 4) return fail(FC_ERR_INVALID_ARG, "fc_select: merge %d", p.merge);
+  if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
+      !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
+      !std::isfinite(p.tau_sim))
+    return fail(FC_ERR_INVALID_ARG, "fc_select: hyper-parameter out of range");
+  if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "fc_select: B=%d H=%d W=%d", B, H, W);
+  const int tp = p.patch * p.merge;
+  if (H % tp || W % tp)
+    return fail(FC_ERR_SHAPE, "fc_select: H=%d, W=%d not multiples of patch*merge=%d", H, W, tp);
+  const int M = (H / tp) * (W / tp);
+  if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width ||
+      M > ctx->caps.max_tokens)
+    return fail(FC_ERR_CAPACITY, "fc_select: B=%d H=%d W=%d N=%d exceed the context caps", B, H, W, M);
+  if (M > fc::kMaxTokens)
+    return fail(FC_ERR_UNSUPPORTED, "fc_select: %d tokens per frame > %d", M, fc::kMaxTokens);
+  fc_status st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_select(ctx, p, frames_prev, frames_cur, B, H, W, *out,
+                           reinterpret_cast<hipStream_t>(stream));
+}
+
+static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_cache *kv, int B,
+                             const char *who) {
+  if (!L || !kv) return fail(FC_ERR_INVALID_ARG, "%s: null layer or cache descriptor", who);
+  if (L->d_model < 1 || L->n_heads < 1 || L->n_kv_heads < 1 || L->head_dim < 1 || L->d_ffn < 1)
+    return fail(FC_ERR_INVALID_ARG, "%s: non-positive layer dimension", who);
+  if (L->n_heads % L->n_kv_heads)
+    return fail(FC_ERR_SHAPE, "%s: n_kv_heads %d does not divide n_heads %d", who, L->n_kv_heads,
+                L->n_heads);
+  if (L->d_model % fc::kGemmBK || L->d_ffn % fc::kGemmBK || (L->n_heads * L->head_dim) % fc::kGemmBK)
+    return fail(FC_ERR_SHAPE, "%s: d_model, d_ffn and n_heads*head_dim must be multiples of %d", who,
+                fc::kGemmBK);
+  if (!(L->rms_eps > 0) || !(L->rope_theta > 1))
+    return fail(FC_ERR_INVALID_ARG, "%s: rms_eps must be > 0 and rope_theta > 1", who);
+  if (!kv->k || !kv->v) return fail(FC_ERR_INVALID_ARG, "%s: null K or V cache", who);
+  if (kv->text_tokens < 0 || kv->frame_tokens < 1 || kv->window < 1 || kv->head < 0 ||
+      kv->head >= kv->window)
+    return fail(FC_ERR_INVALID_ARG, "%s: bad cache layout T=%d N=%d W=%d head=%d", who,
+                kv->text_tokens, kv->frame_tokens, kv->window, kv->head);
+  const long S = (long)kv->text_tokens + (long)kv->window * kv->frame_tokens;
+  const int qkv = (L->n_heads + 2 * L->n_kv_heads) * L->head_dim;
+  const fc_caps &c = ctx->caps;
+  if (B < 1) return fail(FC_ERR_SHAPE, "%s: B=%d", who, B);
+  if (B > c.max_batch || kv->frame_tokens > c.max_tokens || S > c.max_seq || L->d_model > c.max_d_model ||
+      L->d_ffn > c.max_ffn || qkv > c.max_qkv)
+    return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%d exceed the context caps",
+                who, B, kv->frame_tokens, S, L->d_model, L->d_ffn, qkv);
+  return FC_OK;
+}
+
+fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                           const uint16_t *x_cur, const int32_t *recompute_idx,
+                           const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
+                           void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_layer_forward: null context");
+  fc_status st = check_layer(ctx, layer, kv, B, "fc_layer_forward");
+  if (st != FC_OK) return st;
+  const fc_layer_desc &L = *layer;
+  if (!x_cur || !recompute_idx || !n_recompute || !y_cur)
+    return fail(FC_ERR_INVALID_ARG, "fc_layer_forward: null activation or index buffer");
+  if (!L.w_qkv || !L.b_qkv || !L.w_o || !L.w_gate || !L.w_up || !L.w_down || !L.g_attn || !L.g_mlp)
+    return fail(FC_ERR_INVALID_ARG, "fc_layer_forward: null weight pointer");
+  if (!((L.head_dim == 128 && (L.n_heads / L.n_kv_heads == 7 || L.n_heads / L.n_kv_heads == 1 ||
+                               L.n_heads / L.n_kv_heads == 4)) ||
+        (L.head_dim == 64 && (L.n_heads / L.n_kv_heads == 1 || L.n_heads / L.n_kv_heads == 2))))
+    return fail(FC_ERR_UNSUPPORTED, "fc_layer_forward: head_dim %d with %d query heads per kv head",
+                L.head_dim, L.n_heads / L.n_kv_heads);
+  if ((long)kv->text_tokens + (long)kv->window * kv->frame_tokens > (long)ctx->caps.max_seq)
+    return fail(FC_ERR_CAPACITY, "fc_layer_forward: sequence exceeds max_seq");
+  st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_layer(ctx, L, *kv, x_cur, recompute_idx, n_recompute, y_cur, B,
+                          reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                          const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                          const uint8_t *reuse_mask, int32_t grid_w, int32_t B, void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_cache_update: null context");
+  fc_status st = check_layer(ctx, layer, kv, B, "fc_cache_update");
+  if (st != FC_OK) return st;
+  if (!y_prev || !y_cur || !shift || !reuse_mask)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update: null buffer");
+  if (y_prev == y_cur) return fail(FC_ERR_INVALID_ARG, "fc_cache_update: y_prev and y_cur alias");
+  if (grid_w < 1 || kv->frame_tokens % grid_w)
+    return fail(FC_ERR_SHAPE, "fc_cache_update: grid_w %d does not divide N=%d", grid_w,
+                kv->frame_tokens);
+  if ((layer->n_kv_heads * layer->head_dim) % 8 || layer->d_model % 8)
+    return fail(FC_ERR_SHAPE, "fc_cache_update: row sizes must be multiples of 8 elements");
+  st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_cache_update(ctx, *layer, *kv, y_prev, y_cur, shift, reuse_mask, grid_w, B,
+                                 reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_profile_enable(fc_ctx *ctx, int32_t on) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_profile_enable: null context");
+  ctx->prof = on != 0;
+  return FC_OK;
+}
+
+fc_status fc_profile_read(fc_ctx *ctx, const char *name, double *total_ms, int64_t *launches,
+                          int32_t reset) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_profile_read: null context");
+  double tot = 0.0;
+  int64_t cnt = 0;
+  for (auto &r : ctx->recs) {
+    if (name && std::strcmp(name, r.name) != 0) continue;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e != hipSuccess) return fail(FC_ERR_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return fail(FC_ERR_HIP, "hipEventElapsedTime: %s", hipGetErrorString(e));
+    tot += ms;
+    ++cnt;
+  }
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = cnt;
+  if (reset) {
+    for (auto &r : ctx->recs) {
+      hipEventSynchronize(r.stop);
+      ctx->pool.push_back(r.start);
+      ctx->pool.push_back(r.stop);
+    }
+    ctx->recs.clear();
+  }
+  return FC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// Internal declarations shared by the FreqCache HIP translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/freqcache.h"
+
+namespace fc {
+
+// ----------------------------------------------------------------------------- errors
+void set_error(const char *fmt, ...);
+fc_status fail(fc_status st, const char *fmt, ...);
+
+#define FC_HIP_TRY(expr)                                                                  \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess)                                                                 \
+      return ::fc::fail(FC_ERR_HIP, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(_e), \
+                        __FILE__, __LINE__);                                              \
+  } while (0)
+
+// ----------------------------------------------------------------------------- sizes
+constexpr int kPatch = 14;          // the transform kernels are specialised for P = 14
+constexpr int kBins = 100;          // unique DFT amplitude bins of a real 14x14 patch
+constexpr int kMaxTokens = 1024;    // token-grid / top-K kernels hold one frame in LDS
+constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 32;
+constexpr int kMaxSplits = 8;
+
+// ----------------------------------------------------------------------------- context
+struct ProfRec {
+  const char *name;
+  hipEvent_t start, stop;
+};
+
+}  // namespace fc
+
+struct fc_ctx {
+  int device = 0;
+  fc_caps caps{};
+  int num_cus = 0;
+  // selection workspace
+  float *amp = nullptr;        // [B][2][kBins][Np] per-patch DFT amplitude (prev, cur)
+  double *pmean = nullptr;     // [B][2][Np] per-patch mean luma
+  double *penergy = nullptr;   // [B][Np] per-patch high-pass DCT energy (current frame)
+  uint8_t *aligned = nullptr;  // [B][N] alignment mask
+  // layer workspace
+  uint16_t *qbuf = nullptr;    // [rows][qkv-wide] pre-RoPE queries, bf16
+  uint16_t *attn = nullptr;    // [rows][n_heads*hd] attention output, bf16
+  float *h1 = nullptr;         // [rows][d] post-attention residual stream
+  float *inv2 = nullptr;       // [rows] 1/rms of h1
+  uint16_t *act = nullptr;     // [rows][ffn] SwiGLU activation, bf16
+  float *part = nullptr;       // split-K / split-KV partial sums
+  size_t part_elems = 0;
+  float2 *rope = nullptr;      // [max_seq][64] (cos, sin)
+  int rope_hd = 0, rope_seq = 0;
+  double rope_theta = 0.0;
+  uint16_t *stage = nullptr;   // [B][N][kv row] staging copy for the W == 1 remap
+  size_t stage_elems = 0;
+  // kernel timing
+  bool prof = false;
+  std::vector<fc::ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+namespace fc {
+
+// Event bracket around one launch when profiling is on.
+struct ProfScope {
+  fc_ctx *ctx;
+  hipStream_t st;
+  hipEvent_t stop = nullptr;
+  ProfScope(fc_ctx *c, hipStream_t s, const char *name);
+  ~ProfScope();
+};
+
+// ----------------------------------------------------------------------------- launchers
+fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *prev,
+                        const float *cur, int B, int H, int W, const fc_select_out &out,
+                        hipStream_t st);
+
+fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
+                       const uint16_t *x_cur, const int32_t *idx, const int32_t *nrec,
+                       uint16_t *y_cur, int B, hipStream_t st);
+
+fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
+                              const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                              const uint8_t *reuse, int grid_w, int B, hipStream_t st);
+
+fc_status upload_select_tables();
+
+}  // namespace fc

@@ -1,0 +1,376 @@
+"""ctypes binding of libfreqcache (include/freqcache.h).
+
+Argument marshalling only: every computation runs in the HIP library.  Tensors
+are torch tensors on the GPU; the binding checks their device, dtype,
+contiguity and size against what the call will touch (the C ABI receives bare
+pointers and cannot), then passes data pointers and torch's current stream.
+The library must be built (paper_2604_24391_amd.build); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import torch  # imported before the library so both share torch's HIP runtime
+
+from .build import LIB
+
+c_int32, c_int64, c_double, c_float, c_void_p, c_char_p = (
+    ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_float, ctypes.c_void_p,
+    ctypes.c_char_p)
+
+FC_OK = 0
+STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID_ARG", 2: "FC_ERR_SHAPE", 3: "FC_ERR_CAPACITY",
+          4: "FC_ERR_HIP", 5: "FC_ERR_NO_DEVICE", 6: "FC_ERR_UNSUPPORTED"}
+NSCALARS, NCOUNTS = 6, 4
+SCALARS = ("sim_freq", "psi", "alpha", "mu", "sigma", "thr")
+COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
+FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
+
+EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
+           "fc_cache_update", "fc_layer_forward", "fc_profile_enable", "fc_profile_read")
+
+
+class FcError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class fc_caps(ctypes.Structure):
+    _fields_ = [("max_batch", c_int32), ("max_height", c_int32), ("max_width", c_int32),
+                ("max_tokens", c_int32), ("max_seq", c_int32), ("max_d_model", c_int32),
+                ("max_ffn", c_int32), ("max_qkv", c_int32)]
+
+
+class fc_select_params(ctypes.Structure):
+    _fields_ = [("patch", c_int32), ("merge", c_int32), ("tau_mig", c_double),
+                ("lambda_", c_double), ("alpha_min", c_double), ("alpha_max", c_double),
+                ("adaptive", c_int32), ("alpha_fixed", c_double), ("entropy_norm", c_int32),
+                ("tau_sim", c_double)]
+
+
+class fc_select_out(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("sim", "energy", "reuse_mask", "recompute_idx",
+                                        "n_recompute", "shift", "scalars", "counts", "flags")]
+
+
+class fc_layer_desc(ctypes.Structure):
+    _fields_ = [("d_model", c_int32), ("n_heads", c_int32), ("n_kv_heads", c_int32),
+                ("head_dim", c_int32), ("d_ffn", c_int32), ("rms_eps", c_float),
+                ("rope_theta", c_double)] + [
+        (n, c_void_p) for n in ("w_qkv", "b_qkv", "w_o", "w_gate", "w_up", "w_down", "g_attn",
+                                "g_mlp")]
+
+
+class fc_kv_cache(ctypes.Structure):
+    _fields_ = [("k", c_void_p), ("v", c_void_p), ("text_tokens", c_int32),
+                ("frame_tokens", c_int32), ("window", c_int32), ("head", c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libfreqcache.so (fails loudly when it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise FcError(6, f"{LIB} is missing: build it with "
+                             "`python -m paper_2604_24391_amd.build` (there is no fallback)")
+        L = ctypes.CDLL(LIB)
+        L.fc_version.restype = c_char_p
+        L.fc_last_error.restype = c_char_p
+        L.fc_create.argtypes = [ctypes.POINTER(c_void_p), c_int32, ctypes.POINTER(fc_caps)]
+        L.fc_destroy.argtypes = [c_void_p]
+        L.fc_select.argtypes = [c_void_p, ctypes.POINTER(fc_select_params), c_void_p, c_void_p,
+                                c_int32, c_int32, c_int32, ctypes.POINTER(fc_select_out),
+                                c_void_p]
+        L.fc_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
+                                      ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
+                                      c_void_p, c_int32, c_int32, c_void_p]
+        L.fc_layer_forward.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
+                                       ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_int32, c_void_p]
+        L.fc_profile_enable.argtypes = [c_void_p, c_int32]
+        L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
+                                      ctypes.POINTER(c_int64), c_int32]
+        for n in ("fc_create", "fc_destroy", "fc_select", "fc_cache_update", "fc_layer_forward",
+                  "fc_profile_enable", "fc_profile_read"):
+            getattr(L, n).restype = c_int32
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != FC_OK:
+        raise FcError(status, lib().fc_last_error().decode())
+
+
+def fc_version() -> str:
+    return lib().fc_version().decode()
+
+
+def fc_last_error() -> str:
+    return lib().fc_last_error().decode()
+
+
+def _stream(stream):
+    if stream is None:
+        return c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return c_void_p(stream.cuda_stream)
+    return c_void_p(int(stream))
+
+
+def _ptr(t: torch.Tensor, dtype, numel: int, name: str):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, the call touches {numel}")
+    if t.data_ptr() % 16:
+        raise ValueError(f"{name} must be 16-byte aligned")
+    return c_void_p(t.data_ptr())
+
+
+# ------------------------------------------------------------------------------ context
+@dataclass
+class Caps:
+    max_batch: int = 1
+    max_height: int = 448
+    max_width: int = 448
+    max_tokens: int = 1024
+    max_seq: int = 2176
+    max_d_model: int = 3584
+    max_ffn: int = 18944
+    max_qkv: int = 4608
+
+    def c(self) -> fc_caps:
+        return fc_caps(*(int(getattr(self, f[0])) for f in fc_caps._fields_))
+
+
+class Context:
+    """An fc_ctx on one GPU (owns the library workspace)."""
+
+    def __init__(self, caps: Caps, device: int = 0):
+        self.caps = caps
+        self.device = device
+        h = c_void_p()
+        cc = caps.c()
+        _check(lib().fc_create(ctypes.byref(h), device, ctypes.byref(cc)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None) and self.handle.value:
+            lib().fc_destroy(self.handle)
+            self.handle = c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def fc_create(caps: Caps, device: int = 0) -> Context:
+    return Context(caps, device)
+
+
+def fc_destroy(ctx: Context):
+    ctx.close()
+
+
+# ------------------------------------------------------------------------------ selection
+@dataclass
+class SelectParams:
+    """Selection hyper-parameters; defaults are the paper's (Sec. 6.4)."""
+    patch: int = 14
+    merge: int = 1
+    tau_mig: float = 0.12
+    lam: float = 0.25
+    alpha_min: float = 0.08
+    alpha_max: float = 0.5
+    adaptive: bool = True
+    alpha_fixed: float = 0.5
+    entropy_norm: bool = True
+    tau_sim: float = 0.0
+
+    def c(self) -> fc_select_params:
+        return fc_select_params(self.patch, self.merge, self.tau_mig, self.lam, self.alpha_min,
+                                self.alpha_max, int(self.adaptive), self.alpha_fixed,
+                                int(self.entropy_norm), self.tau_sim)
+
+
+@dataclass
+class SelectOut:
+    sim: torch.Tensor
+    energy: torch.Tensor
+    reuse_mask: torch.Tensor
+    recompute_idx: torch.Tensor
+    n_recompute: torch.Tensor
+    shift: torch.Tensor
+    scalars: torch.Tensor
+    counts: torch.Tensor
+    flags: torch.Tensor | None = None
+
+    @staticmethod
+    def alloc(B: int, N: int, device="cuda", flags: bool = True) -> "SelectOut":
+        kw = dict(device=device)
+        return SelectOut(
+            sim=torch.empty(B, N, dtype=torch.float32, **kw),
+            energy=torch.empty(B, N, dtype=torch.float64, **kw),
+            reuse_mask=torch.empty(B, N, dtype=torch.uint8, **kw),
+            recompute_idx=torch.empty(B, N, dtype=torch.int32, **kw),
+            n_recompute=torch.empty(B, dtype=torch.int32, **kw),
+            shift=torch.empty(B, 2, dtype=torch.int32, **kw),
+            scalars=torch.empty(B, NSCALARS, dtype=torch.float64, **kw),
+            counts=torch.empty(B, NCOUNTS, dtype=torch.int32, **kw),
+            flags=torch.empty(B, N, dtype=torch.uint8, **kw) if flags else None)
+
+    def c(self, B: int, N: int) -> fc_select_out:
+        return fc_select_out(
+            _ptr(self.sim, torch.float32, B * N, "sim"),
+            _ptr(self.energy, torch.float64, B * N, "energy"),
+            _ptr(self.reuse_mask, torch.uint8, B * N, "reuse_mask"),
+            _ptr(self.recompute_idx, torch.int32, B * N, "recompute_idx"),
+            _ptr(self.n_recompute, torch.int32, B, "n_recompute"),
+            _ptr(self.shift, torch.int32, 2 * B, "shift"),
+            _ptr(self.scalars, torch.float64, NSCALARS * B, "scalars"),
+            _ptr(self.counts, torch.int32, NCOUNTS * B, "counts"),
+            _ptr(self.flags, torch.uint8, B * N, "flags") if self.flags is not None
+            else c_void_p(0))
+
+
+def token_grid(H: int, W: int, prm: SelectParams):
+    tp = prm.patch * prm.merge
+    return H // tp, W // tp
+
+
+def fc_select(ctx: Context, prm: SelectParams, prev: torch.Tensor | None, cur: torch.Tensor,
+              out: SelectOut, stream=None):
+    """Algorithm 1 for a [B, 3, H, W] float32 batch of frame pairs (prev may be None)."""
+    if cur.dim() != 4 or cur.shape[1] != 3:
+        raise ValueError("cur must be [B, 3, H, W]")
+    B, _, H, W = cur.shape
+    gh, gw = token_grid(H, W, prm)
+    N = gh * gw
+    pc = _ptr(cur, torch.float32, B * 3 * H * W, "cur")
+    if prev is not None:
+        if tuple(prev.shape) != tuple(cur.shape):
+            raise ValueError("prev and cur shapes differ")
+        pp = _ptr(prev, torch.float32, B * 3 * H * W, "prev")
+    else:
+        pp = c_void_p(0)
+    co = out.c(B, N)
+    cp = prm.c()
+    _check(lib().fc_select(ctx.handle, ctypes.byref(cp), pp, pc, B, H, W, ctypes.byref(co),
+                           _stream(stream)))
+
+
+# ------------------------------------------------------------------------------ layer
+@dataclass
+class LayerDesc:
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ffn: int
+    weights: dict = field(repr=False)   # name -> bf16 GPU tensor
+    rms_eps: float = 1e-6
+    rope_theta: float = 1e6
+
+    @property
+    def qkv(self) -> int:
+        return (self.n_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    def c(self) -> fc_layer_desc:
+        d, f, q, o = self.d_model, self.d_ffn, self.qkv, self.n_heads * self.head_dim
+        w = self.weights
+        sizes = dict(w_qkv=q * d, b_qkv=q, w_o=d * o, w_gate=f * d, w_up=f * d, w_down=d * f,
+                     g_attn=d, g_mlp=d)
+        ptrs = [_ptr(w[n], torch.bfloat16, sizes[n], n) for n in
+                ("w_qkv", "b_qkv", "w_o", "w_gate", "w_up", "w_down", "g_attn", "g_mlp")]
+        return fc_layer_desc(d, self.n_heads, self.n_kv_heads, self.head_dim, f, self.rms_eps,
+                             self.rope_theta, *ptrs)
+
+
+@dataclass
+class KVCache:
+    """One layer's token cache: k, v [B, S, n_kv, hd] bf16, S = T + W N; ring head."""
+    k: torch.Tensor
+    v: torch.Tensor
+    text_tokens: int
+    frame_tokens: int
+    window: int
+    head: int = 0
+
+    @property
+    def S(self) -> int:
+        return self.text_tokens + self.window * self.frame_tokens
+
+    def advance(self):
+        """Move to the next step: the oldest frame's slot becomes the current one."""
+        self.head = (self.head + 1) % self.window
+
+    def c(self, B: int, kvw: int) -> fc_kv_cache:
+        n = B * self.S * kvw
+        return fc_kv_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
+                           self.text_tokens, self.frame_tokens, self.window, self.head)
+
+
+def fc_layer_forward(ctx: Context, layer: LayerDesc, kv: KVCache, x_cur: torch.Tensor,
+                     recompute_idx: torch.Tensor, n_recompute: torch.Tensor, y_cur: torch.Tensor,
+                     stream=None):
+    """Partial-recompute decoder layer over B items (x_cur, y_cur: [B, N, d] bf16)."""
+    B = x_cur.shape[0]
+    N, d = kv.frame_tokens, layer.d_model
+    cl = layer.c()
+    ck = kv.c(B, layer.n_kv_heads * layer.head_dim)
+    _check(lib().fc_layer_forward(
+        ctx.handle, ctypes.byref(cl), ctypes.byref(ck),
+        _ptr(x_cur, torch.bfloat16, B * N * d, "x_cur"),
+        _ptr(recompute_idx, torch.int32, B * N, "recompute_idx"),
+        _ptr(n_recompute, torch.int32, B, "n_recompute"),
+        _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur"), B, _stream(stream)))
+
+
+def fc_cache_update(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev: torch.Tensor,
+                    y_cur: torch.Tensor, shift: torch.Tensor, reuse_mask: torch.Tensor,
+                    grid_w: int, stream=None):
+    """Copy each reused token's cached K/V and output rows from its aligned source."""
+    B = y_cur.shape[0]
+    N, d = kv.frame_tokens, layer.d_model
+    cl = layer.c()
+    ck = kv.c(B, layer.n_kv_heads * layer.head_dim)
+    _check(lib().fc_cache_update(
+        ctx.handle, ctypes.byref(cl), ctypes.byref(ck),
+        _ptr(y_prev, torch.bfloat16, B * N * d, "y_prev"),
+        _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur"),
+        _ptr(shift, torch.int32, 2 * B, "shift"),
+        _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
+
+
+# ------------------------------------------------------------------------------ timing
+def fc_profile_enable(ctx: Context, on: bool = True):
+    _check(lib().fc_profile_enable(ctx.handle, int(on)))
+
+
+def fc_profile_read(ctx: Context, name: str | None = None, reset: bool = False):
+    """(total milliseconds, launches) of kernel `name` (all kernels when None)."""
+    ms, n = c_double(), c_int64()
+    _check(lib().fc_profile_read(ctx.handle, name.encode() if name else None, ctypes.byref(ms),
+                                 ctypes.byref(n), int(reset)))
+    return ms.value, n.value

@@ -1,0 +1,86 @@
+"""The C-ABI library loads and exports every entry point declared in
+include/freqcache.h, and argument errors come back as status codes without any
+device work (these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "freqcache.h")
+
+
+def declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(fc_[a-z_]+)\s*\(", txt)))
+
+
+@pytest.fixture(scope="module")
+def fc():
+    import paper_2604_24391_amd as fc
+    fc.lib()
+    return fc
+
+
+def test_header_declares_the_three_calls():
+    names = declared()
+    for n in ("fc_select", "fc_layer_forward", "fc_cache_update", "fc_create", "fc_destroy",
+              "fc_last_error"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(fc):
+    lib = fc.lib()
+    missing = [n for n in declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(fc.EXPORTS) == declared()
+
+
+def test_version_and_error_text(fc):
+    assert "gfx950" in fc.fc_version()
+    assert isinstance(fc.fc_last_error(), str)
+
+
+def test_null_arguments_are_rejected_without_a_device(fc):
+    lib = fc.lib()
+    assert lib.fc_create(None, 0, None) == 1
+    assert lib.fc_select(None, None, None, None, 1, 224, 224, None, None) == 1
+    assert "null" in fc.fc_last_error()
+    assert lib.fc_layer_forward(None, None, None, None, None, None, None, 1, None) == 1
+    assert lib.fc_cache_update(None, None, None, None, None, None, None, 16, 1, None) == 1
+    assert lib.fc_profile_enable(None, 1) == 1
+    assert lib.fc_destroy(None) == 1
+
+
+def test_create_without_gpu_reports_no_device(fc):
+    """On a machine without a GPU, fc_create fails with FC_ERR_NO_DEVICE (on a GPU
+    box it succeeds)."""
+    caps = fc.Caps(max_batch=1, max_height=224, max_width=224, max_tokens=256, max_seq=288,
+                   max_d_model=256, max_ffn=1024, max_qkv=768)
+    try:
+        ctx = fc.Context(caps)
+    except fc.FcError as e:
+        assert e.status == 5
+    else:
+        ctx.close()
+
+
+def test_bad_caps_rejected(fc):
+    caps = fc.Caps(max_batch=0)
+    with pytest.raises(fc.FcError) as e:
+        fc.Context(caps)
+    assert e.value.status == 1
+    with pytest.raises(fc.FcError) as e:
+        fc.Context(fc.Caps(max_tokens=4096))
+    assert e.value.status == 6
+
+
+def test_struct_layouts_match_the_header(fc):
+    """ctypes mirrors of the C structs have the sizes the C compiler gives them."""
+    assert ctypes.sizeof(fc.freqcache.fc_caps) == 8 * 4
+    assert ctypes.sizeof(fc.freqcache.fc_select_params) == 72
+    assert ctypes.sizeof(fc.freqcache.fc_select_out) == 9 * 8
+    assert ctypes.sizeof(fc.freqcache.fc_kv_cache) == 32
+    assert ctypes.sizeof(fc.freqcache.fc_layer_desc) == 5 * 4 + 4 + 8 + 8 * 8

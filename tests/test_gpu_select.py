@@ -1,0 +1,166 @@
+"""GPU parity of fc_select against the float64 oracle (called through the C ABI).
+
+Masks, ids, shifts and counts must match bit for bit (an exception is allowed
+only where the oracle's own decision margin is below 1e-5, and the GPU result
+must then still be a valid selection); similarities, energies and scalars
+within 1e-5 relative.
+"""
+import numpy as np
+import pytest
+import torch
+
+import fcdata
+from oracle import select as osel
+from tests import fcutil
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fc():
+    import paper_2604_24391_amd as fc
+    return fc
+
+
+@pytest.fixture(scope="module")
+def ctx(fc):
+    c = fc.Context(fc.Caps(max_batch=64, max_height=448, max_width=448, max_tokens=1024,
+                           max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+    yield c
+    c.close()
+
+
+def run_select(fc, ctx, prm, prev, cur):
+    B, _, H, W = cur.shape
+    gh, gw = fc.token_grid(H, W, prm)
+    out = fc.SelectOut.alloc(B, gh * gw)
+    p = None if prev is None else torch.from_numpy(np.ascontiguousarray(prev)).cuda()
+    c = torch.from_numpy(np.ascontiguousarray(cur)).cuda()
+    fc.fc_select(ctx, prm, p, c, out)
+    torch.cuda.synchronize()
+    return fcutil.select_out_np(out)
+
+
+def compare(fc, ctx, prm, prev, cur, items=None):
+    o = run_select(fc, ctx, prm, prev, cur)
+    op = fcutil.oracle_select_params(prm)
+    items = range(cur.shape[0]) if items is None else items
+    margins = []
+    for b in items:
+        res = osel.select_item(None if prev is None else prev[b], cur[b], op)
+        margins.append(fcutil.check_select(o, res, op, b))
+    return o, margins
+
+
+def test_tiny_pair_fixed_budget(fc, ctx):
+    """224x224 pair, 256 patches, fixed 50 % budget (K_reuse = 128)."""
+    prev, cur, _ = fcdata.tiny_pair(0)
+    prm = fc.SelectParams(adaptive=False, alpha_fixed=0.5)
+    o, _ = compare(fc, ctx, prm, prev, cur)
+    assert int(o["counts"][0][0]) == 128
+
+
+def test_tiny_pair_adaptive(fc, ctx):
+    prev, cur, _ = fcdata.tiny_pair(3)
+    compare(fc, ctx, fc.SelectParams(), prev, cur)
+
+
+def test_selection_at_scale_sampled(fc, ctx):
+    """64 pairs at 448x448 (1024 patches each), adaptive budget: the launch the
+    benchmark times; the oracle checks a spread sample of 8 pairs."""
+    prev, cur, _ = fcdata.sel_pairs(1)
+    o, margins = compare(fc, ctx, fc.SelectParams(), prev, cur, items=range(0, 64, 8))
+    print("min top-K margin", min(m["topk"] for m in margins))
+
+
+def test_flush_without_previous_frame(fc, ctx):
+    """No previous frame: flushed, K_final = 0, every token recomputed (Sec. 4.1)."""
+    _, cur, _ = fcdata.tiny_pair(5)
+    o, _ = compare(fc, ctx, fc.SelectParams(), None, cur)
+    assert int(o["counts"][0][3]) == 1 and int(o["n_recompute"][0]) == 256
+    np.testing.assert_array_equal(o["recompute_idx"][0], np.arange(256))
+
+
+def test_zero_previous_frame_flushes(fc, ctx):
+    prev, cur, _ = fcdata.tiny_pair(6)
+    o, _ = compare(fc, ctx, fc.SelectParams(), np.zeros_like(prev), cur)
+    assert int(o["counts"][0][3]) == 1
+
+
+def test_identical_and_rolled_frames(fc, ctx):
+    """Identical frames: Delta = 0, all aligned, similarity 1.  Frames rolled by one
+    token: Delta = -1 on both axes, first row and column unaligned."""
+    rng = np.random.default_rng(7)
+    fr = rng.uniform(size=(1, 3, 224, 224)).astype(np.float32)
+    o, _ = compare(fc, ctx, fc.SelectParams(), fr, fr)
+    assert tuple(o["shift"][0]) == (0, 0)
+    np.testing.assert_allclose(o["sim"][0], 1.0, atol=1e-6)
+    rolled = np.roll(fr, (14, 14), (2, 3))
+    o, _ = compare(fc, ctx, fc.SelectParams(), fr, rolled)
+    assert tuple(o["shift"][0]) == (-1, -1)
+
+
+def test_flat_frames_tie_to_lowest_ids(fc, ctx):
+    """Flat content has energy exactly 0 on both sides, so the ascending top-K takes
+    the lowest token ids (ties broken by id)."""
+    fr = np.full((1, 3, 224, 224), 0.4, np.float32)
+    fr[:, :, 100:, 150:] = 0.9
+    o, _ = compare(fc, ctx, fc.SelectParams(adaptive=False, alpha_fixed=0.25), fr, fr)
+    assert int(o["counts"][0][2]) == 64
+
+
+def test_merge2_episode_frames(fc, ctx):
+    """448x448 camera frames with 2x2 token merge (256 tokens), consecutive steps."""
+    fr = fcdata.episode_frames(11, n_frames=4)
+    prm = fc.SelectParams(merge=2)
+    compare(fc, ctx, prm, fr[:3], fr[1:4])
+
+
+@pytest.mark.parametrize("hw", [(154, 154), (168, 252), (196, 112), (42, 70)])
+def test_ragged_frame_sizes(fc, ctx, hw):
+    """Patch rows that do not fill a 16-patch workgroup and widths that are not a
+    multiple of 4 floats (scalar load path)."""
+    h, w = hw
+    rng = np.random.default_rng(h * 1000 + w)
+    cv = fcdata.canvas(rng, h + 16, w + 16)
+    prev = cv[None, :, 8:8 + h, 8:8 + w].astype(np.float32)
+    cur = np.clip(cv[None, :, 5:5 + h, 10:10 + w] + rng.normal(0, 0.01, (1, 3, h, w)), 0, 1)
+    compare(fc, ctx, fc.SelectParams(), prev, cur.astype(np.float32))
+
+
+def test_batch_items_are_independent(fc, ctx):
+    """Item b of a batch equals the same pair run alone."""
+    prev, cur, _ = fcdata.sel_pairs(9, batch=3, size=224)
+    prm = fc.SelectParams()
+    ob = run_select(fc, ctx, prm, prev, cur)
+    for b in range(3):
+        o1 = run_select(fc, ctx, prm, prev[b:b + 1], cur[b:b + 1])
+        for k in ("sim", "energy", "reuse_mask", "recompute_idx", "shift", "scalars", "counts"):
+            np.testing.assert_array_equal(ob[k][b], o1[k][0], err_msg=k)
+
+
+def test_deterministic(fc, ctx):
+    """Two runs on the same inputs are byte-identical."""
+    prev, cur, _ = fcdata.sel_pairs(4, batch=8)
+    prm = fc.SelectParams()
+    a = run_select(fc, ctx, prm, prev, cur)
+    b = run_select(fc, ctx, prm, prev, cur)
+    for k, v in a.items():
+        np.testing.assert_array_equal(v, b[k], err_msg=k)
+
+
+def test_boundary_errors(fc, ctx):
+    """Shape and capacity errors come back as status codes and launch nothing."""
+    prm = fc.SelectParams()
+    out = fc.SelectOut.alloc(1, 256)
+    bad = torch.zeros(1, 3, 100, 224, device="cuda")
+    with pytest.raises(fc.FcError) as e:
+        fc.fc_select(ctx, prm, None, bad, out)
+    assert e.value.status == 2
+    big = torch.zeros(1, 3, 896, 896, device="cuda")
+    with pytest.raises(fc.FcError) as e:
+        fc.fc_select(ctx, prm, None, big, fc.SelectOut.alloc(1, 4096))
+    assert e.value.status in (3, 6)
+    with pytest.raises(fc.FcError) as e:
+        fc.fc_select(ctx, fc.SelectParams(patch=16), None, torch.zeros(1, 3, 224, 224, device="cuda"), out)
+    assert e.value.status == 6
