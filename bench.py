@@ -1,0 +1,298 @@
+"""Benchmark of the FreqCache per-step hot path on one MI355X.
+
+A step is one navigation step of a 32-step camera episode at batch 1:
+  fc_select on the (previous, current) 448x448 frame pair (14-px patches, 2x2
+  merge -> 256 visual tokens, adaptive budget), then for each of 28
+  Qwen2.5-VL-7B-shaped bf16 decoder layers (128 text + 8 frames x 256 tokens =
+  2176 cached positions) the window advance, fc_cache_update and
+  fc_layer_forward on the tokens the selection left for recompute.
+Inputs (frames, token embeddings, weights, caches) are resident in HBM before
+the timed region.  value = steps/s = frames/s at batch 1.
+
+Also reported, each measured in the same run:
+  roofline      the dominant kernel (gate/up GEMM, weight-streaming) against HBM
+                peak, its duration from HIP events on its launch stream;
+  cpu_baseline  the CPU oracle on a bounded sample of the same step;
+  select_batch  fc_select on 64 pairs of 448x448 frames, GB/s of frame input;
+  layer_ratios  one layer at reuse 0/25/50/75/90 %, time, MFMA utilisation.
+
+    python bench.py [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--layers", type=int, default=28)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the per-step path has no cross-GPU work "
+              "(episodes shard over GPUs with zero communication); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import fcdata
+    import paper_2604_24391_amd as fc
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    shape = fcdata.QWEN_LAYER
+    L = args.layers
+    T, N, Wn, size, m = 128, 256, 8, 448, 2
+    S = T + Wn * N
+    gw = size // (14 * m)
+
+    # ------------------------------------------------------------------ inputs
+    t0 = time.time()
+    n_frames = fcdata.EPISODE["warmup"] + fcdata.EPISODE["steps"]
+    frames_np = fcdata.episode_frames(2024, size=size, n_frames=n_frames)
+    frames = torch.from_numpy(frames_np).to(dev)                       # [F, 3, H, W]
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+
+    def randn(*shp, std=0.02):
+        return (torch.randn(*shp, device=dev, generator=g) * std).to(torch.bfloat16)
+
+    # token-embedding stand-in for the vision tower (not part of the timed step):
+    # a fixed linear map of each token's 28x28x3 pixels to d_model
+    proj = randn(3 * 28 * 28, shape.d, std=0.02)
+    tok_px = frames.unfold(2, 28, 28).unfold(3, 28, 28)               # [F,3,16,16,28,28]
+    tok_px = tok_px.permute(0, 2, 3, 1, 4, 5).reshape(n_frames, N, 3 * 28 * 28)
+    emb = (tok_px.to(torch.bfloat16) @ proj).contiguous()             # [F, N, d]
+    del tok_px
+    layers = []
+    for li in range(L):
+        w = dict(w_qkv=randn(shape.qkv, shape.d), b_qkv=randn(shape.qkv),
+                 w_o=randn(shape.d, shape.n_heads * shape.hd),
+                 w_gate=randn(shape.ffn, shape.d), w_up=randn(shape.ffn, shape.d),
+                 w_down=randn(shape.d, shape.ffn),
+                 g_attn=torch.ones(shape.d, device=dev, dtype=torch.bfloat16),
+                 g_mlp=torch.ones(shape.d, device=dev, dtype=torch.bfloat16))
+        desc = fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w)
+        kv = fc.KVCache(randn(1, S, shape.n_kv, shape.hd, std=1.0),
+                        randn(1, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0)
+        ys = [randn(1, N, shape.d, std=1.0), randn(1, N, shape.d, std=1.0)]
+        layers.append(dict(desc=desc, kv=kv, y=ys))
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.time() - t0:.1f}s ({L} layers, {n_frames} frames)")
+
+    ctx = fc.Context(fc.Caps(max_batch=64, max_height=size, max_width=size, max_tokens=1024,
+                             max_seq=S, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    prm = fc.SelectParams(merge=m)
+    sel = fc.SelectOut.alloc(1, N)
+    cur_y = 0
+
+    def step(s):
+        nonlocal cur_y
+        fi = s % n_frames
+        prev = None if fi == 0 else frames[fi - 1:fi]
+        fc.fc_select(ctx, prm, prev, frames[fi:fi + 1], sel)
+        x = emb[fi:fi + 1]
+        nxt = 1 - cur_y
+        for lay in layers:
+            lay["kv"].advance()
+            fc.fc_cache_update(ctx, lay["desc"], lay["kv"], lay["y"][cur_y], lay["y"][nxt],
+                               sel.shift, sel.reuse_mask, gw)
+            fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, sel.recompute_idx,
+                                sel.n_recompute, lay["y"][nxt])
+            x = lay["y"][nxt]
+        cur_y = nxt
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    n_hist = torch.zeros(args.steps, dtype=torch.int32, device=dev)
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k)
+        n_hist[k:k + 1].copy_(sel.n_recompute)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t1
+    fc.fc_profile_enable(ctx, False)
+    ms_step = el * 1e3 / args.steps
+    n_mean = float(n_hist.float().mean())
+    log(f"{args.steps} steps in {el:.3f}s: {ms_step:.3f} ms/step, mean recomputed tokens {n_mean:.1f}")
+
+    kern = {}
+    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk", "fc_cache_update",
+                 "fc_gemm_qkv", "fc_red_qkv", "fc_attn", "fc_attn_combine", "fc_gemm_o",
+                 "fc_red_o", "fc_gemm_gateup", "fc_gemm_down", "fc_red_down"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        if cnt:
+            kern[name] = dict(avg_us=round(tot * 1e3 / cnt, 3), launches=cnt,
+                              share=round(tot / (el * 1e3), 4))
+    fc.fc_profile_read(ctx, None, reset=True)
+    gu = kern["fc_gemm_gateup"]
+    d, f = shape.d, shape.ffn
+    gu_bytes = 2 * f * d * 2 + n_mean * d * 4 + n_mean * f * 2
+    achieved = gu_bytes / (gu["avg_us"] * 1e-6) / 1e9
+    roofline = dict(bound="hbm", kernel="fc_gemm_gateup", achieved=round(achieved, 1),
+                    peak=HBM_PEAK_GBS, unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
+                    traffic=None, bytes_per_launch=round(gu_bytes),
+                    avg_us=gu["avg_us"])
+
+    result = dict(
+        metric="frames/s per-step (select+cached layer); select HBM GB/s; layer MFMA util",
+        value=round(args.steps / el, 3), unit="frames/s", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(ms_step, 4), higher_is_better=True,
+        scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+        config=dict(workload="episode step: 448x448 frame-pair selection (14-px patches, 2x2 "
+                    "merge, 256 tokens, adaptive budget) + window advance + cache remap + "
+                    f"{L} Qwen2.5-VL-7B-shaped bf16 decoder layers over 2176 cached "
+                    "positions, batch 1", frame=size, tokens=N, layers=L, seq=S, batch=1,
+                    mean_recomputed_tokens=round(n_mean, 1)),
+        roofline=roofline, kernels=kern,
+        context="paper (Table 2): 637 -> 401 ms/step, 1.59x, InternVLA-N1 on R2R-CE, one "
+                "NVIDIA A100 40GB, precision not stated; a different (whole-model) workload")
+
+    if not args.no_extras:
+        result["select_batch"] = bench_select_batch(fc, ctx, torch)
+        result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
+                                              T, N, Wn, L, gw)
+    ctx.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_select_batch(fc, ctx, torch):
+    """fc_select on 64 independent 448x448 pairs (the selection-only workload)."""
+    import fcdata
+    t0 = time.time()
+    prev_np, cur_np, _ = fcdata.sel_pairs(1)
+    prev, cur = torch.from_numpy(prev_np).cuda(), torch.from_numpy(cur_np).cuda()
+    log(f"selection pairs ready in {time.time() - t0:.1f}s")
+    B, H, W = 64, 448, 448
+    out = fc.SelectOut.alloc(B, 1024)
+    prm = fc.SelectParams()
+    for _ in range(3):
+        fc.fc_select(ctx, prm, prev, cur, out)
+    torch.cuda.synchronize()
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fc.fc_select(ctx, prm, prev, cur, out)
+    e1.record()
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
+    call_us = e0.elapsed_time(e1) * 1e3 / reps
+    frame_bytes = 2 * B * 3 * H * W * 4
+    out_bytes = B * 1024 * (4 + 8 + 1 + 4 + 1)
+    kern = {}
+    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        kern[name] = round(tot * 1e3 / cnt, 3)
+    fc.fc_profile_read(ctx, None, reset=True)
+    gbs = (frame_bytes + out_bytes) / (call_us * 1e-6) / 1e9
+    spectra_gbs = frame_bytes / (kern["fc_spectra"] * 1e-6) / 1e9
+    return dict(workload="64 pairs 448x448, 14-px patches, 1024 patches/frame, adaptive",
+                call_us=round(call_us, 2), algorithmic_bytes=frame_bytes + out_bytes,
+                gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
+                spectra_gbs=round(spectra_gbs, 1), kernel_avg_us=kern)
+
+
+def bench_layer_ratios(fc, ctx, torch, lay, shape):
+    """One layer call at fixed random reuse ratios (0/25/50/75/90 %), B = 1."""
+    import fcdata
+    out = {}
+    N = lay["kv"].frame_tokens
+    d, f, qkv, o = shape.d, shape.ffn, shape.qkv, shape.n_heads * shape.hd
+    wbytes = 2 * (qkv * d + d * o + 2 * f * d + d * f)
+    x = lay["y"][0].clone()
+    y = lay["y"][1].clone()
+    for r in (0, 25, 50, 75, 90):
+        ids = fcdata.random_reuse_ids(100 + r, N, r)
+        n = len(ids)
+        idx = torch.full((1, N), -1, dtype=torch.int32)
+        idx[0, :n] = torch.from_numpy(ids)
+        idx = idx.cuda()
+        nrec = torch.tensor([n], dtype=torch.int32, device="cuda")
+        for _ in range(3):
+            fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, idx, nrec, y)
+        torch.cuda.synchronize()
+        reps = 20
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, idx, nrec, y)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        S = lay["kv"].S
+        flops = 2.0 * n * (qkv * d + o * d + 2 * f * d + f * d) + 4.0 * n * shape.n_heads * shape.hd * (S - N / 2)
+        tf = flops / (us * 1e-6) / 1e12
+        gbs = wbytes / (us * 1e-6) / 1e9
+        out[f"reuse{r}"] = dict(n=n, us=round(us, 2), tflops=round(tf, 1),
+                                mfma_util=round(tf / BF16_PEAK_TFLOPS, 4),
+                                weight_gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4))
+    return out
+
+
+def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
+    """The oracle as it stands on a bounded sample of the same step: selection of one
+    frame pair and two of the 28 layer calls at this step's mask, extrapolated to a
+    whole step (select + 28 layers)."""
+    from oracle import layer as ol
+    from oracle import select as osel
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    op = osel.SelectParams(merge=prm.merge)
+    t0 = time.perf_counter()
+    res = osel.select_item(frames_np[10], frames_np[11], op)
+    t_sel = time.perf_counter() - t0
+
+    def u16(t):
+        return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    wt = {k: u16(v) for k, v in lay["desc"].weights.items()}
+    kc, vc = u16(lay["kv"].k[0]), u16(lay["kv"].v[0])
+    y_prev = u16(lay["y"][0][0])
+    x = u16(lay["y"][1][0])
+    lay_o = ol.Layout(T=T, N=N, W=Wn, head=lay["kv"].head)
+    reps = 2
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        ol.layer_partial(x, res.recompute_idx, kc, vc, y_prev, lay_o, wt, shape)
+    t_layer = (time.perf_counter() - t0) / reps
+    t_step = t_sel + L * t_layer
+    return dict(value=round(1.0 / t_step, 5), unit="frames/s", cores=int(cores), kind="oracle",
+                sample=f"oracle selection of one 448x448 pair ({t_sel:.2f}s) + {reps} oracle "
+                       f"layer calls at n={res.n_recompute} ({t_layer:.2f}s each), extrapolated "
+                       f"to select + {L} layers = {t_step:.1f}s/step")
+
+
+if __name__ == "__main__":
+    main()

@@ -76,7 +76,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->amp, c->pmean, c->penergy, c->aligned, c->qbuf, c->attn,
-                  c->h1,  c->inv2,  c->act,     c->part,    c->rope, c->stage};
+                  c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -149,7 +149,8 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
       (st = dev_alloc(&ctx->qbuf, rows * c.max_qkv, "q")) != FC_OK ||
       (st = dev_alloc(&ctx->attn, rows * c.max_qkv, "attn")) != FC_OK ||
       (st = dev_alloc(&ctx->h1, rows * c.max_d_model, "h1")) != FC_OK ||
-      (st = dev_alloc(&ctx->inv2, rows, "inv2")) != FC_OK ||
+      (st = dev_alloc(&ctx->hb, rows * c.max_d_model, "hb")) != FC_OK ||
+      (st = dev_alloc(&ctx->ssq, rows * 8, "ssq")) != FC_OK ||
       (st = dev_alloc(&ctx->act, rows * c.max_ffn, "act")) != FC_OK ||
       (st = dev_alloc(&ctx->part, ctx->part_elems, "partials")) != FC_OK ||
       (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||
@@ -212,6 +213,8 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
   if (L->n_heads % L->n_kv_heads)
     return fail(FC_ERR_SHAPE, "%s: n_kv_heads %d does not divide n_heads %d", who, L->n_kv_heads,
                 L->n_heads);
+  if (L->d_model > 8192)
+    return fail(FC_ERR_UNSUPPORTED, "%s: d_model %d > 8192", who, L->d_model);
   if (L->d_model % fc::kGemmBK || L->d_ffn % fc::kGemmBK || (L->n_heads * L->head_dim) % fc::kGemmBK)
     return fail(FC_ERR_SHAPE, "%s: d_model, d_ffn and n_heads*head_dim must be multiples of %d", who,
                 fc::kGemmBK);

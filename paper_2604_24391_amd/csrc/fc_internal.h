@@ -27,8 +27,8 @@ fc_status fail(fc_status st, const char *fmt, ...);
 constexpr int kPatch = 14;          // the transform kernels are specialised for P = 14
 constexpr int kBins = 100;          // unique DFT amplitude bins of a real 14x14 patch
 constexpr int kMaxTokens = 1024;    // token-grid / top-K kernels hold one frame in LDS
-constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 32;
-constexpr int kMaxSplits = 8;
+constexpr int kGemmBK = 64;        // K step of the layer GEMMs (dims must be multiples)
+constexpr int kMaxSplits = 16;
 
 // ----------------------------------------------------------------------------- context
 struct ProfRec {
@@ -51,7 +51,8 @@ struct fc_ctx {
   uint16_t *qbuf = nullptr;    // [rows][qkv-wide] pre-RoPE queries, bf16
   uint16_t *attn = nullptr;    // [rows][n_heads*hd] attention output, bf16
   float *h1 = nullptr;         // [rows][d] post-attention residual stream
-  float *inv2 = nullptr;       // [rows] 1/rms of h1
+  uint16_t *hb = nullptr;      // [rows][d] bf16 copy of h1 (SwiGLU input)
+  float *ssq = nullptr;        // [rows][8] per-1024-column sums of squares of hb
   uint16_t *act = nullptr;     // [rows][ffn] SwiGLU activation, bf16
   float *part = nullptr;       // split-K / split-KV partial sums
   size_t part_elems = 0;

@@ -60,217 +60,361 @@ __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
 }
 
 // ------------------------------------------------------------------------------- GEMM
-constexpr int BM = kGemmBM, BN = kGemmBN, BK = kGemmBK;
-constexpr int LDA = BK + 8;  // LDS row stride in bf16 (16-B pad)
+// Weight-streaming GEMM over the gathered rows, C[rows][cols] = A[rows][K] W[cols][K]^T.
+// With at most a few hundred recomputed rows the layer is bound by streaming the
+// weights from HBM, so each wave owns 32 output columns for every row of its
+// 256-row M tile and loads its weight rows straight into registers, PD K-steps
+// ahead; the (gathered) activation tile is shared by the workgroup's 4 waves
+// through LDS.  Split-K partial sums go to a float32 buffer that the k_red_*
+// kernels reduce; the SwiGLU mode (no split) applies the MLP RMSNorm and
+// SiLU(g) * u in its own epilogue.
+enum { G_QKV = 0, G_O = 1, G_GU = 2, G_DOWN = 3 };
+constexpr int BK = kGemmBK;       // 64
+constexpr int MT = 256;           // rows per M tile: 8 MFMA blocks of 32
+constexpr int LDA = BK + 8;       // LDS row stride in bf16 (16-B pad)
+constexpr int PD = 4;             // weight K-steps in flight per wave
 
-struct GemmArgs {
-  const void *A;             // activations; bf16 or float32
-  int a_f32;                 // 1: A is float32
-  int gather;                // 1: A row of slot (b, j) is b*N + idx[b*N + j]; 0: the slot itself
-  const uint16_t *gain;      // [K] multiplied into A (RMSNorm gain), or null
-  const uint16_t *W0;        // weights [rows][K]
-  const uint16_t *W1;        // SwiGLU: up weights (W0 = gate)
-  int swiglu;
-  int K, Nout;               // reduction length, output columns
-  int kchunk, splits;
-  int N;                     // slots per batch item
+struct WArgs {
+  const uint16_t *A;              // bf16 activations
+  int gather;                     // 1: row of slot (b, j) is b*N + idx[b*N + j]; 0: the slot
+  const uint16_t *gain;           // [K] RMSNorm gain multiplied into A, or null
+  const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
+  int K, Nout, kchunk, splits, N, m_tiles, n_tiles;
   const int32_t *idx, *nrec;
-  int m_tiles, n_tiles;
-  float *C;                  // [split][B*N][Nout] partial sums (non-SwiGLU)
-  uint16_t *act;             // [B*N][Nout] SwiGLU output
-  const float *row_scale;    // [B*N] 1/rms applied to gate and up (SwiGLU)
+  float *part;                    // [split][B*N][Nout]
+  long rows;                      // B*N
+  uint16_t *act;                  // SwiGLU output [B*N][Nout]
+  const float *ssq;               // SwiGLU: [B*N][ss_parts] partial sums of squares of h1
+  int ss_parts;
+  float eps;
 };
 
 // Workgroup id -> tile id so that each XCD (workgroups are dealt round-robin over
-// the 8 XCDs) works on a contiguous range of tiles, M fastest: the M tiles that
-// share a weight tile then run on the same XCD and share its L2.
+// the 8 XCDs) works on a contiguous range of tiles; tiles are ordered N-fastest,
+// so the workgroups of one XCD share the same activation chunk in its L2.
 __device__ __forceinline__ int xcd_tile(int w, int total) {
   const int per = total / 8;
   if (w >= per * 8) return w;
   return (w & 7) * per + (w >> 3);
 }
 
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-  __shared__ __bf16 As[2][BM * LDA];
-  __shared__ __bf16 Bs[2][BN * LDA];
-  const int total = a.m_tiles * a.n_tiles * a.splits;
-  const int tile = xcd_tile(blockIdx.x, total);
-  const int mt = tile % a.m_tiles;
-  const int nt = (tile / a.m_tiles) % a.n_tiles;
-  const int sp = tile / (a.m_tiles * a.n_tiles);
-  const int tpb = (a.N + BM - 1) / BM;
-  const int b = mt / tpb;
-  const int row0 = (mt % tpb) * BM;
-  const int nvalid = min(BM, n_valid(a.nrec, b, a.N) - row0);
-  if (nvalid <= 0) return;
-  const int k0 = sp * a.kchunk;
-  const int k1 = min(a.K, k0 + a.kchunk);
-  if (k0 >= k1) return;
-  const int nk = (k1 - k0) / BK;
+// LDS fragment read issued as inline asm.  The activation stages are filled by LDS
+// DMA; the compiler cannot tell its stages apart and would otherwise drain every
+// in-flight global load before each read.  The caller orders the reads after the
+// stage is complete (manual vmcnt wait + barrier) and waits for them with lds_wait().
+__device__ __forceinline__ bf16x8 lds_read16(uint32_t addr) {
+  bf16x8 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+  return r;
+}
+template <int N>
+__device__ __forceinline__ void lds_wait(bf16x8 (&f)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i]));
+}
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+// Global loads of the pipelined K loop, also as inline asm so that the compiler's
+// wait insertion (which cannot follow this loop's load groups across the back edge)
+// never drains them; the loop waits for each K step's group with one vmcnt.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 gload16(const void *p) {
+  u32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return __builtin_bit_cast(uint4, r);
+}
+// LDS DMA of 16 B per lane to lds + 16 * lane (lds must be wave-uniform).  M0 is
+// reserved to the compiler, so the asm restores it.
+__device__ __forceinline__ void dma16(const void *gp, uint32_t lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gp), "s"(l)
+      : "memory");
+}
+__device__ __forceinline__ void anchor(uint4 &r) {
+  u32x4 v = __builtin_bit_cast(u32x4, r);
+  asm volatile("" : "+v"(v));
+  r = __builtin_bit_cast(uint4, v);
+}
 
+template <int MODE>
+struct WTraits {
+  static constexpr bool gather = MODE == G_QKV;                 // rows through the recompute ids
+  static constexpr bool gain = MODE == G_QKV || MODE == G_GU;   // RMSNorm gain on the weights
+};
+
+constexpr int NST = PD;          // activation stages in LDS (the weight prefetch depth)
+
+// The K loop for a tile whose valid rows fill MBC 32-row blocks.
+//   * activations: gathered rows go straight from global memory into a ring of NST
+//     LDS stages (global_load_lds, 16 B per lane), 16-B chunks XOR-swizzled by row so
+//     that the MFMA fragment reads are free of bank conflicts;
+//   * weights: each wave's 32 rows stream into a ring of PD register stages;
+//   * the RMSNorm gain, when the projection has one, scales the weight fragment
+//     (n W^T = x diag(g) W^T), so the activation tile never passes through registers.
+// Loads of step kt are all issued together, PD steps ahead, so the in-order load
+// counter keeps PD steps in flight.  Straight-line code: out-of-range rows and K
+// steps read clamped in-bounds addresses (padding steps use zero weights).
+template <int MODE, int MBC>
+__device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ S0,
+                                           __bf16 *__restrict__ S1, __bf16 *__restrict__ S2,
+                                           __bf16 *__restrict__ S3, float *rowinv, int b, int row0,
+                                           int nvalid, int k0, int nk, int cb, bool wvalid,
+                                           int sp) {
+  constexpr int ROWS = MBC * 32;
+  // one LDS array per stage: the stage of step kt is kt % PD, a compile-time constant
+  // in the unrolled loop, so alias analysis can tell the in-flight DMA writes apart
+  // from the reads of the current stage
+  __bf16 *const stages[PD] = {S0, S1, S2, S3};
   const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
+  const int nk_pad = (nk + PD - 1) / PD * PD;
+  const uint16_t *Wm = (MODE == G_GU && w >= 2) ? a.W1 : a.W0;
+  const uint16_t *wrow = Wm + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
+  const uint16_t *grow = WTraits<MODE>::gain ? a.gain + k0 + 8 * hi : nullptr;
 
-  // per-thread load assignments: 2 chunks of 8 elements for A and for B
-  const void *a_src[2];
-  const uint16_t *b_src[2];
-  int a_row[2], a_kc[2], b_row[2];
+  // activation loads: instruction i of wave w covers rows (4 i + w) * 8 .. + 7; lane
+  // -> row (4 i + w) * 8 + lane / 8, LDS slot lane % 8 holding chunk slot ^ (row % 8)
+  uint32_t aoff[MBC];
+  {
+    const long first = (long)b * a.N +
+                       (WTraits<MODE>::gather ? tok_of(a.idx, (long)b * a.N + row0, a.N) : row0);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = t + 256 * i;
-    a_row[i] = c >> 2;
-    a_kc[i] = (c & 3) * 8;
-    b_row[i] = c >> 2;
-    const int r = a_row[i];
-    a_src[i] = nullptr;
-    if (r < nvalid) {
-      const int slot_j = row0 + r;
-      const long src_row = a.gather ? (long)b * a.N + tok_of(a.idx, (long)b * a.N + slot_j, a.N)
-                                    : (long)b * a.N + slot_j;
-      if (a.a_f32)
-        a_src[i] = (const float *)a.A + src_row * a.K;
-      else
-        a_src[i] = (const uint16_t *)a.A + src_row * a.K;
+    for (int i = 0; i < MBC; ++i) {
+      const int r = (4 * i + w) * 8 + (lane >> 3);
+      const int chunk = (lane & 7) ^ (r & 7);
+      const bool v = r < nvalid;
+      const long slot = (long)b * a.N + row0 + (v ? r : 0);
+      const long src = WTraits<MODE>::gather ? (long)b * a.N + tok_of(a.idx, slot, a.N) : slot;
+      aoff[i] = (uint32_t)((v ? src : first) * a.K + k0 + chunk * 8);
     }
-    const int br = b_row[i];
-    const uint16_t *wp = nullptr;
-    if (a.swiglu) {
-      const int n = nt * (BN / 2) + (br & 63);
-      if (n < a.Nout) wp = (br < 64 ? a.W0 : a.W1) + (long)n * a.K;
-    } else {
-      const int n = nt * BN + br;
-      if (n < a.Nout) wp = a.W0 + (long)n * a.K;
+  }
+  auto loadA = [&](int kt, int u) {
+    const int kk = min(kt, nk - 1) * BK;
+    const uint32_t dst = lds_addr(stages[u]) + w * 1024;
+#pragma unroll
+    for (int i = 0; i < MBC; ++i) dma16(a.A + aoff[i] + kk, dst + i * 4096);
+  };
+
+  uint4 rb[PD][4];
+  uint4 rgn[PD][4];
+  auto loadB = [&](int kt, int u) {
+    const int kk = min(kt, nk - 1) * BK;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) rb[u][s] = gload16(wrow + kk + 16 * s);
+    if (WTraits<MODE>::gain) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) rgn[u][s] = gload16(grow + kk + 16 * s);
     }
-    b_src[i] = wp;
+  };
+
+  f32x16 acc[MBC];
+#pragma unroll
+  for (int mb = 0; mb < MBC; ++mb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[mb][e] = 0.f;
+
+#pragma unroll
+  for (int u = 0; u < PD; ++u) {
+    loadA(u, u);
+    loadB(u, u);
   }
 
-  U16x8 ra[2], rb[2];
-  auto load_tile = [&](int kk) {
+  for (int kt0 = 0; kt0 < nk_pad; kt0 += PD) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int kbase = kk + a_kc[i];
-      if (a_src[i]) {
-        if (a.a_f32) {
-          const float *p = (const float *)a_src[i] + kbase;
-          const float4 x0 = *reinterpret_cast<const float4 *>(p);
-          const float4 x1 = *reinterpret_cast<const float4 *>(p + 4);
-          float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-          if (a.gain) {
-            const U16x8 gg = *reinterpret_cast<const U16x8 *>(a.gain + kbase);
+    for (int u = 0; u < PD; ++u) {
+      const int kt = kt0 + u;
+      const bool live = kt < nk;
+      // this thread's loads for step kt are the oldest PD-1 steps back; wait for them,
+      // then the barrier makes every thread's share of the stage visible.  (A plain
+      // s_barrier: __syncthreads' release fence would drain every in-flight load.)
+      constexpr int kLater = (PD - 1) * (MBC + (WTraits<MODE>::gain ? 8 : 4));
+      static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
+      __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] *= bf2f(gg.v[e]);
-          }
+      for (int s = 0; s < 4; ++s) {
+        anchor(rb[u][s]);
+        if (WTraits<MODE>::gain) anchor(rgn[u][s]);
+      }
+      __builtin_amdgcn_s_barrier();
+      // fragment (mb, s): row mb*32 + l32, 16-B chunk 2 s + hi, stored at slot chunk ^ (row % 8)
+      const uint32_t abase = lds_addr(stages[u]) + l32 * (BK * 2);
+      const int sw = l32 & 7;
+      bf16x8 af[MBC], an[MBC];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) ra[i].v[e] = f2bf(v[e]);
-        } else {
-          ra[i] = *reinterpret_cast<const U16x8 *>((const uint16_t *)a_src[i] + kbase);
-          if (a.gain) {
-            const U16x8 gg = *reinterpret_cast<const U16x8 *>(a.gain + kbase);
+      for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(abase + mb * 32 * BK * 2 + ((hi ^ sw) << 4));
+      lds_wait(af);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) ra[i].v[e] = f2bf(bf2f(ra[i].v[e]) * bf2f(gg.v[e]));
-          }
+      for (int s = 0; s < 4; ++s) {
+        if (s < 3) {
+          const int slot = (2 * (s + 1) + hi) ^ sw;
+#pragma unroll
+          for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(abase + mb * 32 * BK * 2 + (slot << 4));
         }
-      } else {
+        uint4 bw = live ? rb[u][s] : make_uint4(0, 0, 0, 0);
+        if (WTraits<MODE>::gain) {
+          const uint4 g = rgn[u][s];
+          uint32_t x[4] = {bw.x, bw.y, bw.z, bw.w};
+          const uint32_t gg[4] = {g.x, g.y, g.z, g.w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) ra[i].v[e] = 0;
+          for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(x[e] << 16) * __uint_as_float(gg[e] << 16);
+            const float h2 = __uint_as_float(x[e] & 0xFFFF0000u) * __uint_as_float(gg[e] & 0xFFFF0000u);
+            x[e] = (uint32_t)f2bf(lo) | ((uint32_t)f2bf(h2) << 16);
+          }
+          bw = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+#pragma unroll
+        for (int mb = 0; mb < MBC; ++mb)
+          acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[mb], 0, 0, 0);
+        if (s < 3) {
+          lds_wait(an);
+#pragma unroll
+          for (int mb = 0; mb < MBC; ++mb) af[mb] = an[mb];
+        }
       }
-      if (b_src[i]) {
-        rb[i] = *reinterpret_cast<const U16x8 *>(b_src[i] + kk + a_kc[i]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) rb[i].v[e] = 0;
-      }
+      // every wave is done with this stage before any thread refills it
+      __builtin_amdgcn_s_barrier();
+      loadA(kt + PD, u);
+      loadB(kt + PD, u);
     }
-  };
-  auto store_tile = [&](int buf) {
+  }
+
+  // drain the clamped prefetches of the last steps before their registers or LDS are
+  // reused: the anchors keep every ring register live until the loads have landed
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      *reinterpret_cast<U16x8 *>(&As[buf][a_row[i] * LDA + a_kc[i]]) = ra[i];
-      *reinterpret_cast<U16x8 *>(&Bs[buf][b_row[i] * LDA + a_kc[i]]) = rb[i];
+  for (int u = 0; u < PD; ++u)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      anchor(rb[u][s]);
+      if (WTraits<MODE>::gain) anchor(rgn[u][s]);
     }
-  };
-
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  // rows of this wave's two 32-row blocks that hold valid slots
-  const bool act0 = wm * 64 < nvalid, act1 = wm * 64 + 32 < nvalid;
-  // LDS rows of this wave's two B blocks
-  const int brow0 = a.swiglu ? wn * 32 : wn * 64;
-  const int brow1 = a.swiglu ? 64 + wn * 32 : wn * 64 + 32;
-
-  load_tile(k0);
-  store_tile(0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tile(k0 + (kt + 1) * BK);
-    if (act0) {
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        const int ko = ks * 16 + hi * 8;
-        const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(&Bs[buf][(brow0 + l32) * LDA + ko]);
-        const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(&Bs[buf][(brow1 + l32) * LDA + ko]);
-        const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(&As[buf][(wm * 64 + l32) * LDA + ko]);
-        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
-        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
-        if (act1) {
-          const bf16x8 a1 =
-              *reinterpret_cast<const bf16x8 *>(&As[buf][(wm * 64 + 32 + l32) * LDA + ko]);
-          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
-          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
-        }
-      }
+  // lane holds column l32 and rows (e/4)*8 + hi*4 + e%4 of each 32-row block
+  const long slot0 = (long)b * a.N + row0;
+  if (MODE == G_GU) {
+    // 1/rms of each row from the per-chunk sums of squares of h1
+    for (int r = t; r < ROWS; r += 256) {
+      float v = 0.f;
+      if (r < nvalid)
+        for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
+      rowinv[r] = 1.f / sqrtf(v / (float)a.K + a.eps);
     }
-    if (kt + 1 < nk) store_tile(buf ^ 1);
+    // up-projection waves hand their accumulators to the gate waves through LDS
+    // (stages 0 and 1 hold 64 KB, enough for 2 waves x 8 blocks x 16 x 64 floats)
+    float *xch = reinterpret_cast<float *>(S0);
     __syncthreads();
-  }
-
-  // epilogue: lane holds column l32 and rows (e/4)*8 + hi*4 + e%4 of each 32x32 block
-  const long slot_base = (long)b * a.N + row0;
-  if (a.swiglu) {
-    const int col = nt * (BN / 2) + wn * 32 + l32;
-    if (col >= a.Nout) return;
+    if (w >= 2) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+      for (int mb = 0; mb < MBC; ++mb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = wm * 64 + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-        if (r < nvalid) {
-          const float s = a.row_scale[slot_base + r];
-          const float gv = acc[i][0][e] * s, uv = acc[i][1][e] * s;
-          const float y = gv / (1.f + __expf(-gv)) * uv;
-          a.act[(slot_base + r) * a.Nout + col] = f2bf(y);
-        }
-      }
+        for (int e = 0; e < 16; ++e) xch[(((w - 2) * MBC + mb) * 16 + e) * 64 + lane] = acc[mb][e];
     }
-  } else {
-    const long plane = (long)(a.m_tiles / ((a.N + BM - 1) / BM)) * a.N;  // B*N rows
-    float *Cs = a.C + (long)sp * plane * a.Nout;
+    __syncthreads();
+    if (w < 2 && wvalid) {
+      const int col = cb + l32;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = nt * BN + wn * 64 + j * 32 + l32;
-      if (col >= a.Nout) continue;
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int mb = 0; mb < MBC; ++mb) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int r = wm * 64 + i * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-          if (r < nvalid) Cs[(slot_base + r) * a.Nout + col] = acc[i][j][e];
+          const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+          if (r < nvalid) {
+            const float s = rowinv[r];
+            const float gv = acc[mb][e] * s;
+            const float uv = xch[((w * MBC + mb) * 16 + e) * 64 + lane] * s;
+            a.act[(slot0 + r) * a.Nout + col] = f2bf(gv / (1.f + __expf(-gv)) * uv);
+          }
         }
+      }
+    }
+  } else if (wvalid) {
+    float *Pp = a.part + ((long)sp * a.rows + slot0) * a.Nout + cb + l32;
+#pragma unroll
+    for (int mb = 0; mb < MBC; ++mb) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+        if (r < nvalid) Pp[(long)r * a.Nout] = acc[mb][e];
       }
     }
   }
 }
 
-// ------------------------------------------------------------------------------- epilogues
+template <int MODE>
+__global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
+  // contiguous in practice (S0 then S1): the SwiGLU exchange spans both
+  __shared__ __attribute__((aligned(16))) __bf16 S0[MT * BK], S1[MT * BK], S2[MT * BK], S3[MT * BK];
+  __shared__ float rowinv[MT];
+  const int total = a.m_tiles * a.n_tiles * a.splits;
+  const int tile = xcd_tile(blockIdx.x, total);
+  const int nt = tile % a.n_tiles;
+  const int mt = (tile / a.n_tiles) % a.m_tiles;
+  const int sp = tile / (a.n_tiles * a.m_tiles);
+  const int tpb = (a.N + MT - 1) / MT;
+  const int b = mt / tpb;
+  const int row0 = (mt % tpb) * MT;
+  const int nvalid = min(MT, n_valid(a.nrec, b, a.N) - row0);
+  if (nvalid <= 0) return;
+  const int k0 = sp * a.kchunk;
+  const int k1 = min(a.K, k0 + a.kchunk);
+  if (k0 >= k1) return;
+  const int nk = (k1 - k0) / BK;
+  const int w = threadIdx.x >> 6;
+  const int cb = (MODE == G_GU) ? nt * 64 + (w & 1) * 32 : nt * 128 + w * 32;
+  const bool wvalid = cb < a.Nout;
+  switch ((nvalid + 31) >> 5) {
+    case 1: wgemm_tile<MODE, 1>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 2: wgemm_tile<MODE, 2>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 3: wgemm_tile<MODE, 3>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 4: wgemm_tile<MODE, 4>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 5: wgemm_tile<MODE, 5>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 6: wgemm_tile<MODE, 6>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 7: wgemm_tile<MODE, 7>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    default: wgemm_tile<MODE, 8>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+  }
+}
+
+// ------------------------------------------------------------------------------- reductions
+// One workgroup per (row, 1024-column chunk); each thread sums the split-K partials of
+// 4 columns with float4 loads and applies the epilogue of its projection.
+struct RedArgs {
+  int N, d, splits, ncols, qw, kw, S, cur_row0;
+  long rows;
+  float eps;
+  const int32_t *idx, *nrec;
+  const float *part;              // [split][B*N][ncols]
+  const uint16_t *x;              // [B][N][d] layer input
+  const uint16_t *bias;           // [ncols] (QKV)
+  uint16_t *q, *kc, *vc;          // QKV outputs
+  float *h1;                      // [B*N][d]
+  uint16_t *hb;                   // [B*N][d] bf16 copy of h1 (SwiGLU input)
+  float *ssq;                     // [B*N][chunks] sums of squares of hb per 1024 columns
+  uint16_t *y;                    // [B][N][d]
+};
+
+__device__ __forceinline__ float4 sum_parts(const RedArgs &r, long slot, int c) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float *p = r.part + slot * r.ncols + c;
+  const long stride = r.rows * r.ncols;
+#pragma unroll 4
+  for (int s = 0; s < r.splits; ++s) {
+    const float4 u = *reinterpret_cast<const float4 *>(p + s * stride);
+    v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+  }
+  return v;
+}
+
 __device__ float block_sum256(float v, float *red) {
   const int t = threadIdx.x;
   red[t] = v;
@@ -279,88 +423,86 @@ __device__ float block_sum256(float v, float *red) {
     if (t < s) red[t] += red[t + s];
     __syncthreads();
   }
-  const float r = red[0];
+  const float res = red[0];
   __syncthreads();
-  return r;
+  return res;
 }
 
-struct EpiArgs {
-  int N, d, nh, nkv, hd;
-  int splits, ncols;
-  float eps;
-  const int32_t *idx, *nrec;
-  const float *part;           // [split][B*N][ncols]
-  const uint16_t *x;           // [B][N][d] layer input (bf16)
-  const uint16_t *bias;        // [qkv]
-  uint16_t *q;                 // [B*N][nh*hd]
-  uint16_t *kc, *vc;           // cache [B][S][nkv][hd]
-  int S, cur_row0;             // rows of the current frame start at T + cur_slot * N
-  float *h1;                   // [B*N][d]
-  float *inv2;                 // [B*N]
-  uint16_t *y;                 // [B][N][d]
-};
-
-__device__ __forceinline__ float sum_splits(const EpiArgs &e, long slot, int c, long plane) {
-  float v = 0.f;
-  for (int s = 0; s < e.splits; ++s) v += e.part[(long)s * plane * e.ncols + slot * e.ncols + c];
-  return v;
-}
-
-__global__ __launch_bounds__(256) void k_epi_qkv(EpiArgs e, int B) {
+__global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   __shared__ float red[256];
-  const int slot = blockIdx.x;
-  const int b = slot / e.N, j = slot - b * e.N;
-  if (j >= n_valid(e.nrec, b, e.N)) return;
-  const int tok = tok_of(e.idx, slot, e.N);
-  const uint16_t *xr = e.x + ((long)b * e.N + tok) * e.d;
+  const long slot = blockIdx.x;
+  const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
+  if (j >= n_valid(r.nrec, b, r.N)) return;
+  const int tok = tok_of(r.idx, slot, r.N);
+  const uint16_t *xr = r.x + ((long)b * r.N + tok) * r.d;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < e.d; c += 256) {
-    const float v = bf2f(xr[c]);
-    ss += v * v;
+  for (int c = threadIdx.x * 8; c < r.d; c += 256 * 8) {
+    const U16x8 v = *reinterpret_cast<const U16x8 *>(xr + c);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float f = bf2f(v.v[e]);
+      ss = fmaf(f, f, ss);
+    }
   }
   ss = block_sum256(ss, red);
-  const float inv = 1.f / sqrtf(ss / (float)e.d + e.eps);
-  const long plane = (long)B * e.N;
-  const int qw = e.nh * e.hd, kw = e.nkv * e.hd;
-  const long crow = (long)b * e.S + e.cur_row0 + tok;
-  for (int c = threadIdx.x; c < e.ncols; c += 256) {
-    const float v = sum_splits(e, slot, c, plane) * inv + bf2f(e.bias[c]);
-    if (c < qw)
-      e.q[(long)slot * qw + c] = f2bf(v);
-    else if (c < qw + kw)
-      e.kc[crow * kw + (c - qw)] = f2bf(v);
-    else
-      e.vc[crow * kw + (c - qw - kw)] = f2bf(v);
-  }
+  const float inv = 1.f / sqrtf(ss / (float)r.d + r.eps);
+  const int c = blockIdx.y * 1024 + threadIdx.x * 4;
+  if (c >= r.ncols) return;
+  const float4 v = sum_parts(r, slot, c);
+  const float vv[4] = {v.x, v.y, v.z, v.w};
+  uint16_t o[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e] * inv + bf2f(r.bias[c + e]));
+  uint16_t *dst;
+  if (c < r.qw)
+    dst = r.q + slot * r.qw + c;
+  else if (c < r.qw + r.kw)
+    dst = r.kc + ((long)b * r.S + r.cur_row0 + tok) * r.kw + (c - r.qw);
+  else
+    dst = r.vc + ((long)b * r.S + r.cur_row0 + tok) * r.kw + (c - r.qw - r.kw);
+  *reinterpret_cast<uint2 *>(dst) = make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
 }
 
-__global__ __launch_bounds__(256) void k_epi_o(EpiArgs e, int B) {
+__global__ __launch_bounds__(256) void k_red_o(RedArgs r) {
   __shared__ float red[256];
-  const int slot = blockIdx.x;
-  const int b = slot / e.N, j = slot - b * e.N;
-  if (j >= n_valid(e.nrec, b, e.N)) return;
-  const int tok = tok_of(e.idx, slot, e.N);
-  const uint16_t *xr = e.x + ((long)b * e.N + tok) * e.d;
-  const long plane = (long)B * e.N;
+  const long slot = blockIdx.x;
+  const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
+  if (j >= n_valid(r.nrec, b, r.N)) return;
+  const int c = blockIdx.y * 1024 + threadIdx.x * 4;
+  const int tok = tok_of(r.idx, slot, r.N);
   float ss = 0.f;
-  for (int c = threadIdx.x; c < e.d; c += 256) {
-    const float v = bf2f(xr[c]) + sum_splits(e, slot, c, plane);
-    e.h1[(long)slot * e.d + c] = v;
-    ss += v * v;
+  if (c < r.d) {
+    const float4 v = sum_parts(r, slot, c);
+    const uint2 xb = *reinterpret_cast<const uint2 *>(r.x + ((long)b * r.N + tok) * r.d + c);
+    float4 h;
+    h.x = v.x + __uint_as_float(xb.x << 16);
+    h.y = v.y + __uint_as_float(xb.x & 0xFFFF0000u);
+    h.z = v.z + __uint_as_float(xb.y << 16);
+    h.w = v.w + __uint_as_float(xb.y & 0xFFFF0000u);
+    *reinterpret_cast<float4 *>(r.h1 + slot * r.d + c) = h;
+    const uint16_t b0 = f2bf(h.x), b1 = f2bf(h.y), b2 = f2bf(h.z), b3 = f2bf(h.w);
+    *reinterpret_cast<uint2 *>(r.hb + slot * r.d + c) =
+        make_uint2(b0 | ((uint32_t)b1 << 16), b2 | ((uint32_t)b3 << 16));
+    // the MLP RMSNorm statistics, from the bf16 values the gate/up GEMM reads
+    const float f0 = bf2f(b0), f1 = bf2f(b1), f2 = bf2f(b2), f3 = bf2f(b3);
+    ss = f0 * f0 + f1 * f1 + f2 * f2 + f3 * f3;
   }
   ss = block_sum256(ss, red);
-  if (threadIdx.x == 0) e.inv2[slot] = 1.f / sqrtf(ss / (float)e.d + e.eps);
+  if (threadIdx.x == 0) r.ssq[slot * gridDim.y + blockIdx.y] = ss;
 }
 
-__global__ __launch_bounds__(256) void k_epi_down(EpiArgs e, int B) {
-  const int slot = blockIdx.x;
-  const int b = slot / e.N, j = slot - b * e.N;
-  if (j >= n_valid(e.nrec, b, e.N)) return;
-  const int tok = tok_of(e.idx, slot, e.N);
-  const long plane = (long)B * e.N;
-  uint16_t *yr = e.y + ((long)b * e.N + tok) * e.d;
-  for (int c = threadIdx.x; c < e.d; c += 256)
-    yr[c] = f2bf(e.h1[(long)slot * e.d + c] + sum_splits(e, slot, c, plane));
+__global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
+  const long slot = blockIdx.x;
+  const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
+  if (j >= n_valid(r.nrec, b, r.N)) return;
+  const int c = blockIdx.y * 1024 + threadIdx.x * 4;
+  if (c >= r.d) return;
+  const int tok = tok_of(r.idx, slot, r.N);
+  const float4 v = sum_parts(r, slot, c);
+  const float4 h = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + c);
+  *reinterpret_cast<uint2 *>(r.y + ((long)b * r.N + tok) * r.d + c) =
+      make_uint2(f2bf(h.x + v.x) | ((uint32_t)f2bf(h.y + v.y) << 16),
+                 f2bf(h.z + v.z) | ((uint32_t)f2bf(h.w + v.w) << 16));
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -654,26 +796,30 @@ __global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
   for (int e = lane; e < c.d / 8; e += 64) yd[e] = ys[e];
 }
 
+// Split-K count for a weight-streaming GEMM: enough workgroups to cover the chip
+// about once, at least PD K-steps per split, within the partial-sum buffer.
 int pick_splits(int tiles, int K, int want_wgs, long rows, int ncols, size_t cap_elems) {
-  int s = std::max(1, std::min(kMaxSplits, (want_wgs + tiles - 1) / tiles));
-  s = std::min(s, std::max(1, K / (4 * BK)));
+  // workgroups hold a whole CU each: stay within one round of them
+  int s = std::max(1, std::min(kMaxSplits, want_wgs / std::max(tiles, 1)));
+  s = std::min(s, std::max(1, K / (PD * BK)));
   while (s > 1 && (size_t)s * rows * ncols > cap_elems) --s;
   return s;
 }
 
-fc_status run_gemm(fc_ctx *ctx, hipStream_t st, const char *name, GemmArgs g, int B) {
-  g.m_tiles = B * ((g.N + BM - 1) / BM);
-  if (g.swiglu)
-    g.n_tiles = (g.Nout + BN / 2 - 1) / (BN / 2);
-  else
-    g.n_tiles = (g.Nout + BN - 1) / BN;
-  // split-K chunk, a multiple of BK
-  const int kc = ((g.K + g.splits - 1) / g.splits + BK - 1) / BK * BK;
-  g.kchunk = kc;
-  g.splits = (g.K + kc - 1) / kc;
+template <int MODE>
+fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int B, int want_wgs) {
+  g.m_tiles = B * ((g.N + MT - 1) / MT);
+  g.n_tiles = (MODE == G_GU) ? (g.Nout + 63) / 64 : (g.Nout + 127) / 128;
+  int s = (MODE == G_GU) ? 1
+                         : pick_splits(g.m_tiles * g.n_tiles, g.K, want_wgs, g.rows, g.Nout,
+                                       ctx->part_elems);
+  const int ksteps = g.K / BK;
+  const int per = (ksteps + s - 1) / s;
+  g.kchunk = per * BK;
+  g.splits = (ksteps + per - 1) / per;
   const int total = g.m_tiles * g.n_tiles * g.splits;
   ProfScope ps(ctx, st, name);
-  hipLaunchKernelGGL(k_gemm, dim3(total), dim3(256), 0, st, g);
+  hipLaunchKernelGGL(k_wgemm<MODE>, dim3(total), dim3(256), 0, st, g);
   FC_HIP_TRY(hipGetLastError());
   return FC_OK;
 }
@@ -690,6 +836,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   const long rows = (long)B * N;
   const int cur_slot = (kv.head + kv.window - 1) % kv.window;
   const int cur_row0 = kv.text_tokens + cur_slot * N;
+  const int want = std::max(ctx->num_cus, 1);
 
   // RoPE table for (hd, theta) over the cache length (rebuilt only when they change)
   if (ctx->rope_hd != hd || ctx->rope_theta != L.rope_theta || ctx->rope_seq < S) {
@@ -704,43 +851,25 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     ctx->rope_seq = seq;
   }
 
-  const int mt = B * ((N + BM - 1) / BM);
-  const int want = 2 * std::max(ctx->num_cus, 1);
+  RedArgs r{};
+  r.N = N; r.d = d; r.S = S; r.cur_row0 = cur_row0; r.rows = rows; r.eps = L.rms_eps;
+  r.idx = idx; r.nrec = nrec; r.part = ctx->part; r.x = x_cur;
+  r.qw = nh * hd; r.kw = nkv * hd;
+  fc_status rc;
 
-  // 1. gathered RMSNorm (gain in the tile load, 1/rms in the epilogue) + QKV
-  GemmArgs g{};
-  g.A = x_cur;
-  g.a_f32 = 0;
-  g.gather = 1;
-  g.gain = L.g_attn;
-  g.W0 = L.w_qkv;
-  g.K = d;
-  g.Nout = qkv;
-  g.N = N;
-  g.idx = idx;
-  g.nrec = nrec;
-  g.C = ctx->part;
-  g.splits = pick_splits(mt * ((qkv + BN - 1) / BN), d, want, rows, qkv, ctx->part_elems);
-  const int s_qkv = g.splits;
-  fc_status rc = run_gemm(ctx, st, "fc_gemm_qkv", g, B);
-  if (rc != FC_OK) return rc;
+  // 1. gathered rows (RMSNorm gain on the weight fragments) -> QKV partials; the
+  //    reduction applies 1/rms(x) + bias,
+  //    stores q and scatters raw k, v into the current frame's cache rows
   {
-    // the GEMM may have rounded the split count; recompute what it used
-    const int kc = ((d + s_qkv - 1) / s_qkv + BK - 1) / BK * BK;
-    EpiArgs e{};
-    e.N = N; e.d = d; e.nh = nh; e.nkv = nkv; e.hd = hd;
-    e.splits = (d + kc - 1) / kc;
-    e.ncols = qkv;
-    e.eps = L.rms_eps;
-    e.idx = idx; e.nrec = nrec;
-    e.part = ctx->part;
-    e.x = x_cur;
-    e.bias = L.b_qkv;
-    e.q = ctx->qbuf;
-    e.kc = kv.k; e.vc = kv.v;
-    e.S = S; e.cur_row0 = cur_row0;
-    ProfScope ps(ctx, st, "fc_epi_qkv");
-    hipLaunchKernelGGL(k_epi_qkv, dim3((unsigned)rows), dim3(256), 0, st, e, B);
+    WArgs g{};
+    g.A = x_cur; g.gather = 1; g.gain = L.g_attn; g.W0 = L.w_qkv;
+    g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
+    g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
+    if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B, want)) != FC_OK) return rc;
+    r.splits = g.splits; r.ncols = qkv;
+    r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
+    ProfScope ps(ctx, st, "fc_red_qkv");
+    hipLaunchKernelGGL(k_red_qkv, dim3((unsigned)rows, (qkv + 1023) / 1024), dim3(256), 0, st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
@@ -757,10 +886,9 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.out = ctx->attn;
     const int tiles = B * ((N + 31) / 32);
     const int nkb = (S + 31) / 32;
-    int splits = std::max(1, std::min(kMaxSplits, (2 * std::max(ctx->num_cus, 1)) / (tiles * nkv)));
+    int splits = std::max(1, std::min(8, (2 * want) / (tiles * nkv)));
     splits = std::min(splits, std::max(1, nkb / 4));
-    const size_t need = (size_t)splits * rows * nh * (hd + 2);
-    while (splits > 1 && need > ctx->part_elems) --splits;
+    while (splits > 1 && (size_t)splits * rows * nh * (hd + 2) > ctx->part_elems) --splits;
     a.kb_per_split = (nkb + splits - 1) / splits;
     a.splits = (nkb + a.kb_per_split - 1) / a.kb_per_split;
     a.po = ctx->part;
@@ -791,84 +919,40 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     }
   }
 
-  // 3. O projection + residual -> h1 (float32), 1/rms(h1)
+  // 3. O projection; reduction adds the residual -> h1 (float32) and its bf16 copy
   {
-    GemmArgs go{};
-    go.A = ctx->attn;
-    go.gather = 0;
-    go.W0 = L.w_o;
-    go.K = nh * hd;
-    go.Nout = d;
-    go.N = N;
-    go.idx = idx; go.nrec = nrec;
-    go.C = ctx->part;
-    go.splits = pick_splits(mt * ((d + BN - 1) / BN), nh * hd, want, rows, d, ctx->part_elems);
-    const int s0 = go.splits;
-    rc = run_gemm(ctx, st, "fc_gemm_o", go, B);
-    if (rc != FC_OK) return rc;
-    const int kc = ((nh * hd + s0 - 1) / s0 + BK - 1) / BK * BK;
-    EpiArgs e{};
-    e.N = N; e.d = d;
-    e.splits = (nh * hd + kc - 1) / kc;
-    e.ncols = d;
-    e.eps = L.rms_eps;
-    e.idx = idx; e.nrec = nrec;
-    e.part = ctx->part;
-    e.x = x_cur;
-    e.h1 = ctx->h1;
-    e.inv2 = ctx->inv2;
-    ProfScope ps(ctx, st, "fc_epi_o");
-    hipLaunchKernelGGL(k_epi_o, dim3((unsigned)rows), dim3(256), 0, st, e, B);
+    WArgs g{};
+    g.A = ctx->attn; g.gather = 0; g.W0 = L.w_o;
+    g.K = nh * hd; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
+    g.part = ctx->part; g.rows = rows;
+    if ((rc = run_wgemm<G_O>(ctx, st, "fc_gemm_o", g, B, want)) != FC_OK) return rc;
+    r.splits = g.splits; r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq;
+    ProfScope ps(ctx, st, "fc_red_o");
+    hipLaunchKernelGGL(k_red_o, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
-  // 4. gate/up with the MLP RMSNorm folded in, SiLU(g) * u -> act (bf16)
+  // 4. gate/up with the MLP RMSNorm (gain on the weight fragments, 1/rms from the
+  //    O-reduction's sums of squares), SiLU(g) * u -> act (bf16)
   {
-    GemmArgs gu{};
-    gu.A = ctx->h1;
-    gu.a_f32 = 1;
-    gu.gather = 0;
-    gu.gain = L.g_mlp;
-    gu.W0 = L.w_gate;
-    gu.W1 = L.w_up;
-    gu.swiglu = 1;
-    gu.K = d;
-    gu.Nout = ffn;
-    gu.N = N;
-    gu.idx = idx; gu.nrec = nrec;
-    gu.act = ctx->act;
-    gu.row_scale = ctx->inv2;
-    gu.splits = 1;
-    rc = run_gemm(ctx, st, "fc_gemm_gateup", gu, B);
-    if (rc != FC_OK) return rc;
+    WArgs g{};
+    g.A = ctx->hb; g.gather = 0; g.gain = L.g_mlp; g.W0 = L.w_gate; g.W1 = L.w_up;
+    g.K = d; g.Nout = ffn; g.N = N; g.idx = idx; g.nrec = nrec;
+    g.rows = rows; g.act = ctx->act; g.eps = L.rms_eps;
+    g.ssq = ctx->ssq; g.ss_parts = (d + 1023) / 1024;
+    if ((rc = run_wgemm<G_GU>(ctx, st, "fc_gemm_gateup", g, B, want)) != FC_OK) return rc;
   }
 
-  // 5. down projection + residual, scattered into the output cache
+  // 5. down projection; reduction adds h1 and scatters bf16 rows into the output cache
   {
-    GemmArgs gd{};
-    gd.A = ctx->act;
-    gd.gather = 0;
-    gd.W0 = L.w_down;
-    gd.K = ffn;
-    gd.Nout = d;
-    gd.N = N;
-    gd.idx = idx; gd.nrec = nrec;
-    gd.C = ctx->part;
-    gd.splits = pick_splits(mt * ((d + BN - 1) / BN), ffn, want, rows, d, ctx->part_elems);
-    const int s0 = gd.splits;
-    rc = run_gemm(ctx, st, "fc_gemm_down", gd, B);
-    if (rc != FC_OK) return rc;
-    const int kc = ((ffn + s0 - 1) / s0 + BK - 1) / BK * BK;
-    EpiArgs e{};
-    e.N = N; e.d = d;
-    e.splits = (ffn + kc - 1) / kc;
-    e.ncols = d;
-    e.idx = idx; e.nrec = nrec;
-    e.part = ctx->part;
-    e.h1 = ctx->h1;
-    e.y = y_cur;
-    ProfScope ps(ctx, st, "fc_epi_down");
-    hipLaunchKernelGGL(k_epi_down, dim3((unsigned)rows), dim3(256), 0, st, e, B);
+    WArgs g{};
+    g.A = ctx->act; g.gather = 0; g.W0 = L.w_down;
+    g.K = ffn; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
+    g.part = ctx->part; g.rows = rows;
+    if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B, want)) != FC_OK) return rc;
+    r.splits = g.splits; r.ncols = d; r.y = y_cur;
+    ProfScope ps(ctx, st, "fc_red_down");
+    hipLaunchKernelGGL(k_red_down, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
     FC_HIP_TRY(hipGetLastError());
   }
   return FC_OK;
