@@ -142,7 +142,7 @@ def main():
     log(f"{args.steps} steps in {el:.3f}s: {ms_step:.3f} ms/step, mean recomputed tokens {n_mean:.1f}")
 
     kern = {}
-    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk", "fc_cache_update",
+    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk", "fc_cache_update", "fc_gather_norm",
                  "fc_gemm_qkv", "fc_red_qkv", "fc_attn", "fc_attn_combine", "fc_gemm_o",
                  "fc_red_o", "fc_gemm_gateup", "fc_gemm_down", "fc_red_down"):
         tot, cnt = fc.fc_profile_read(ctx, name)

@@ -4,24 +4,22 @@
 // token of batch item b, j < n_recompute[b] (read on the device, so no host
 // sync); grids are sized for N rows per item and surplus tiles exit.
 //
-//   k_gemm      bf16 MFMA (v_mfma_f32_32x32x16_bf16) GEMM  C = A W^T, W row-major
-//               [out][in] like torch.nn.Linear.  128x128x32 tiles, 4 waves of
-//               64x64, LDS double buffer.  A rows are gathered through the
-//               recompute ids inside the tile load (optionally scaled by an
-//               RMSNorm gain and converted from float32).  Either writes float32
-//               split-K partial sums, or (SwiGLU mode) interleaves gate and up
-//               rows in one tile and applies SiLU(g) * u in the epilogue.
-//   k_epi_qkv   sums the split-K partials, applies 1/rms(x) and the q/k/v bias,
-//               stores q (pre-RoPE) and scatters raw k and v into the current
-//               frame's cache rows.
+//   k_gather_norm  gathers the recomputed tokens' rows of x and writes the RMSNorm
+//               output bf16(x / rms(x) * g) slot by slot: the QKV operand.
+//   k_wgemm     weight-streaming bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16) over the
+//               slots, C = A W^T with W row-major [out][in] like torch.nn.Linear;
+//               split-K float32 partials, or (SwiGLU) SiLU(g) * u in the epilogue.
+//   k_red_qkv   sums the QKV partials, adds the bias, stores q (pre-RoPE) and
+//               scatters raw k and v into the current frame's cache rows.
 //   k_attn      attention of the gathered queries over the whole cache, GQA
 //               (one wave per query head of a KV group), RoPE applied to q and to
 //               each key block as it is staged in LDS, causal by position, float32
 //               online softmax in the transposed form S^T = K Q^T so that a lane
 //               owns one query column.  Optional split over key blocks.
 //   k_attn_combine  merges split-KV partials.
-//   k_epi_o     residual add, h1 in float32, 1/rms(h1) for the MLP norm.
-//   k_epi_down  residual add, bf16 output scattered into the output cache.
+//   k_red_o     residual add -> h1 (float32), the SwiGLU operand bf16(h1 * g_mlp)
+//               and per-chunk sums of squares of h1 for the MLP RMSNorm.
+//   k_red_down  residual add, bf16 output rows scattered into the output cache.
 //   k_cache_update  copies cached K/V/output rows of each reused token from its
 //               aligned source token.
 #include <hip/hip_runtime.h>
@@ -75,9 +73,7 @@ constexpr int LDA = BK + 8;       // LDS row stride in bf16 (16-B pad)
 constexpr int PD = 4;             // weight K-steps in flight per wave
 
 struct WArgs {
-  const uint16_t *A;              // bf16 activations
-  int gather;                     // 1: row of slot (b, j) is b*N + idx[b*N + j]; 0: the slot
-  const uint16_t *gain;           // [K] RMSNorm gain multiplied into A, or null
+  const uint16_t *A;              // bf16 activations, one row per slot
   const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
   int K, Nout, kchunk, splits, N, m_tiles, n_tiles;
   const int32_t *idx, *nrec;
@@ -147,8 +143,11 @@ __device__ __forceinline__ void anchor(uint4 &r) {
 
 template <int MODE>
 struct WTraits {
-  static constexpr bool gather = MODE == G_QKV;                 // rows through the recompute ids
-  static constexpr bool gain = MODE == G_QKV || MODE == G_GU;   // RMSNorm gain on the weights
+  // SwiGLU: each wave computes the gate and the up block of the same 32 columns, so
+  // every activation fragment feeds two MFMAs and SiLU(g) * u needs no exchange
+  static constexpr int NB = MODE == G_GU ? 2 : 1;               // weight blocks per wave
+  static constexpr int PD = MODE == G_GU ? 3 : 4;               // K steps in flight
+  static constexpr int COLS = 128;                              // output columns per workgroup
 };
 
 constexpr int NST = PD;          // activation stages in LDS (the weight prefetch depth)
@@ -157,9 +156,8 @@ constexpr int NST = PD;          // activation stages in LDS (the weight prefetc
 //   * activations: gathered rows go straight from global memory into a ring of NST
 //     LDS stages (global_load_lds, 16 B per lane), 16-B chunks XOR-swizzled by row so
 //     that the MFMA fragment reads are free of bank conflicts;
-//   * weights: each wave's 32 rows stream into a ring of PD register stages;
-//   * the RMSNorm gain, when the projection has one, scales the weight fragment
-//     (n W^T = x diag(g) W^T), so the activation tile never passes through registers.
+//   * weights: each wave's 32 rows (SwiGLU: 32 gate and 32 up rows) stream into a
+//     ring of PD register stages.
 // Loads of step kt are all issued together, PD steps ahead, so the in-order load
 // counter keeps PD steps in flight.  Straight-line code: out-of-range rows and K
 // steps read clamped in-bounds addresses (padding steps use zero weights).
@@ -170,33 +168,28 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
                                            int nvalid, int k0, int nk, int cb, bool wvalid,
                                            int sp) {
   constexpr int ROWS = MBC * 32;
+  constexpr int NB = WTraits<MODE>::NB;
+  constexpr int PD = WTraits<MODE>::PD;
   // one LDS array per stage: the stage of step kt is kt % PD, a compile-time constant
-  // in the unrolled loop, so alias analysis can tell the in-flight DMA writes apart
-  // from the reads of the current stage
-  __bf16 *const stages[PD] = {S0, S1, S2, S3};
+  // in the unrolled loop
+  __bf16 *const stages[4] = {S0, S1, S2, S3};
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int nk_pad = (nk + PD - 1) / PD * PD;
-  const uint16_t *Wm = (MODE == G_GU && w >= 2) ? a.W1 : a.W0;
-  const uint16_t *wrow = Wm + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
-  const uint16_t *grow = WTraits<MODE>::gain ? a.gain + k0 + 8 * hi : nullptr;
+  const uint16_t *wrow[NB];
+  wrow[0] = a.W0 + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
+  if (NB == 2) wrow[NB - 1] = a.W1 + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
 
   // activation loads: instruction i of wave w covers rows (4 i + w) * 8 .. + 7; lane
   // -> row (4 i + w) * 8 + lane / 8, LDS slot lane % 8 holding chunk slot ^ (row % 8)
   uint32_t aoff[MBC];
-  {
-    const long first = (long)b * a.N +
-                       (WTraits<MODE>::gather ? tok_of(a.idx, (long)b * a.N + row0, a.N) : row0);
 #pragma unroll
-    for (int i = 0; i < MBC; ++i) {
-      const int r = (4 * i + w) * 8 + (lane >> 3);
-      const int chunk = (lane & 7) ^ (r & 7);
-      const bool v = r < nvalid;
-      const long slot = (long)b * a.N + row0 + (v ? r : 0);
-      const long src = WTraits<MODE>::gather ? (long)b * a.N + tok_of(a.idx, slot, a.N) : slot;
-      aoff[i] = (uint32_t)((v ? src : first) * a.K + k0 + chunk * 8);
-    }
+  for (int i = 0; i < MBC; ++i) {
+    const int r = (4 * i + w) * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ (r & 7);
+    const long slot = (long)b * a.N + row0 + (r < nvalid ? r : 0);
+    aoff[i] = (uint32_t)(slot * a.K + k0 + chunk * 8);
   }
   auto loadA = [&](int kt, int u) {
     const int kk = min(kt, nk - 1) * BK;
@@ -205,23 +198,22 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
     for (int i = 0; i < MBC; ++i) dma16(a.A + aoff[i] + kk, dst + i * 4096);
   };
 
-  uint4 rb[PD][4];
-  uint4 rgn[PD][4];
+  uint4 rb[PD][NB][4];
   auto loadB = [&](int kt, int u) {
     const int kk = min(kt, nk - 1) * BK;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) rb[u][s] = gload16(wrow + kk + 16 * s);
-    if (WTraits<MODE>::gain) {
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) rgn[u][s] = gload16(grow + kk + 16 * s);
-    }
+      for (int s = 0; s < 4; ++s) rb[u][j][s] = gload16(wrow[j] + kk + 16 * s);
   };
 
-  f32x16 acc[MBC];
+  f32x16 acc[NB][MBC];
 #pragma unroll
-  for (int mb = 0; mb < MBC; ++mb)
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[mb][e] = 0.f;
+    for (int mb = 0; mb < MBC; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[j][mb][e] = 0.f;
 
 #pragma unroll
   for (int u = 0; u < PD; ++u) {
@@ -237,14 +229,13 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
       // this thread's loads for step kt are the oldest PD-1 steps back; wait for them,
       // then the barrier makes every thread's share of the stage visible.  (A plain
       // s_barrier: __syncthreads' release fence would drain every in-flight load.)
-      constexpr int kLater = (PD - 1) * (MBC + (WTraits<MODE>::gain ? 8 : 4));
+      constexpr int kLater = (PD - 1) * (MBC + 4 * NB);
       static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
       __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        anchor(rb[u][s]);
-        if (WTraits<MODE>::gain) anchor(rgn[u][s]);
-      }
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) anchor(rb[u][j][s]);
       __builtin_amdgcn_s_barrier();
       // fragment (mb, s): row mb*32 + l32, 16-B chunk 2 s + hi, stored at slot chunk ^ (row % 8)
       const uint32_t abase = lds_addr(stages[u]) + l32 * (BK * 2);
@@ -260,23 +251,14 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
 #pragma unroll
           for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(abase + mb * 32 * BK * 2 + (slot << 4));
         }
-        uint4 bw = live ? rb[u][s] : make_uint4(0, 0, 0, 0);
-        if (WTraits<MODE>::gain) {
-          const uint4 g = rgn[u][s];
-          uint32_t x[4] = {bw.x, bw.y, bw.z, bw.w};
-          const uint32_t gg[4] = {g.x, g.y, g.z, g.w};
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lo = __uint_as_float(x[e] << 16) * __uint_as_float(gg[e] << 16);
-            const float h2 = __uint_as_float(x[e] & 0xFFFF0000u) * __uint_as_float(gg[e] & 0xFFFF0000u);
-            x[e] = (uint32_t)f2bf(lo) | ((uint32_t)f2bf(h2) << 16);
-          }
-          bw = make_uint4(x[0], x[1], x[2], x[3]);
+        for (int j = 0; j < NB; ++j) {
+          const uint4 bw = live ? rb[u][j][s] : make_uint4(0, 0, 0, 0);
+          const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+#pragma unroll
+          for (int mb = 0; mb < MBC; ++mb)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[j][mb], 0, 0, 0);
         }
-        const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-#pragma unroll
-        for (int mb = 0; mb < MBC; ++mb)
-          acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[mb], 0, 0, 0);
         if (s < 3) {
           lds_wait(an);
 #pragma unroll
@@ -296,10 +278,9 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
 #pragma unroll
   for (int u = 0; u < PD; ++u)
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      anchor(rb[u][s]);
-      if (WTraits<MODE>::gain) anchor(rgn[u][s]);
-    }
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) anchor(rb[u][j][s]);
   __syncthreads();
   // lane holds column l32 and rows (e/4)*8 + hi*4 + e%4 of each 32-row block
   const long slot0 = (long)b * a.N + row0;
@@ -311,18 +292,8 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
         for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
       rowinv[r] = 1.f / sqrtf(v / (float)a.K + a.eps);
     }
-    // up-projection waves hand their accumulators to the gate waves through LDS
-    // (stages 0 and 1 hold 64 KB, enough for 2 waves x 8 blocks x 16 x 64 floats)
-    float *xch = reinterpret_cast<float *>(S0);
     __syncthreads();
-    if (w >= 2) {
-#pragma unroll
-      for (int mb = 0; mb < MBC; ++mb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) xch[(((w - 2) * MBC + mb) * 16 + e) * 64 + lane] = acc[mb][e];
-    }
-    __syncthreads();
-    if (w < 2 && wvalid) {
+    if (wvalid) {
       const int col = cb + l32;
 #pragma unroll
       for (int mb = 0; mb < MBC; ++mb) {
@@ -330,9 +301,9 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
         for (int e = 0; e < 16; ++e) {
           const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
           if (r < nvalid) {
-            const float s = rowinv[r];
-            const float gv = acc[mb][e] * s;
-            const float uv = xch[((w * MBC + mb) * 16 + e) * 64 + lane] * s;
+            const float sc = rowinv[r];
+            const float gv = acc[0][mb][e] * sc;
+            const float uv = acc[NB - 1][mb][e] * sc;
             a.act[(slot0 + r) * a.Nout + col] = f2bf(gv / (1.f + __expf(-gv)) * uv);
           }
         }
@@ -345,7 +316,7 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-        if (r < nvalid) Pp[(long)r * a.Nout] = acc[mb][e];
+        if (r < nvalid) Pp[(long)r * a.Nout] = acc[0][mb][e];
       }
     }
   }
@@ -371,7 +342,7 @@ __global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
   if (k0 >= k1) return;
   const int nk = (k1 - k0) / BK;
   const int w = threadIdx.x >> 6;
-  const int cb = (MODE == G_GU) ? nt * 64 + (w & 1) * 32 : nt * 128 + w * 32;
+  const int cb = nt * WTraits<MODE>::COLS + w * 32;
   const bool wvalid = cb < a.Nout;
   switch ((nvalid + 31) >> 5) {
     case 1: wgemm_tile<MODE, 1>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
@@ -396,10 +367,11 @@ struct RedArgs {
   const float *part;              // [split][B*N][ncols]
   const uint16_t *x;              // [B][N][d] layer input
   const uint16_t *bias;           // [ncols] (QKV)
+  const uint16_t *gain;           // [d] MLP RMSNorm gain (O reduction)
   uint16_t *q, *kc, *vc;          // QKV outputs
   float *h1;                      // [B*N][d]
-  uint16_t *hb;                   // [B*N][d] bf16 copy of h1 (SwiGLU input)
-  float *ssq;                     // [B*N][chunks] sums of squares of hb per 1024 columns
+  uint16_t *hb;                   // [B*N][d] bf16(h1 * g_mlp), the SwiGLU operand
+  float *ssq;                     // [B*N][chunks] sums of squares of h1 per 1024 columns
   uint16_t *y;                    // [B][N][d]
 };
 
@@ -428,15 +400,21 @@ __device__ float block_sum256(float v, float *red) {
   return res;
 }
 
-__global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
+// One workgroup per slot: the gathered token's row of x, normalised and scaled by
+// the attention RMSNorm gain, as the QKV GEMM's bf16 operand.
+__global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict__ x,
+                                                     const uint16_t *__restrict__ gain,
+                                                     const int32_t *__restrict__ idx,
+                                                     const int32_t *__restrict__ nrec, int N,
+                                                     int d, float eps, uint16_t *__restrict__ xs) {
   __shared__ float red[256];
   const long slot = blockIdx.x;
-  const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
-  if (j >= n_valid(r.nrec, b, r.N)) return;
-  const int tok = tok_of(r.idx, slot, r.N);
-  const uint16_t *xr = r.x + ((long)b * r.N + tok) * r.d;
+  const int b = (int)(slot / N), j = (int)(slot - (long)b * N);
+  if (j >= n_valid(nrec, b, N)) return;
+  const int tok = tok_of(idx, slot, N);
+  const uint16_t *xr = x + ((long)b * N + tok) * d;
   float ss = 0.f;
-  for (int c = threadIdx.x * 8; c < r.d; c += 256 * 8) {
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
     const U16x8 v = *reinterpret_cast<const U16x8 *>(xr + c);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -445,14 +423,29 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
     }
   }
   ss = block_sum256(ss, red);
-  const float inv = 1.f / sqrtf(ss / (float)r.d + r.eps);
+  const float inv = 1.f / sqrtf(ss / (float)d + eps);
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const U16x8 v = *reinterpret_cast<const U16x8 *>(xr + c);
+    const U16x8 g = *reinterpret_cast<const U16x8 *>(gain + c);
+    U16x8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o.v[e] = f2bf(bf2f(v.v[e]) * inv * bf2f(g.v[e]));
+    *reinterpret_cast<U16x8 *>(xs + slot * d + c) = o;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
+  const long slot = blockIdx.x;
+  const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
+  if (j >= n_valid(r.nrec, b, r.N)) return;
   const int c = blockIdx.y * 1024 + threadIdx.x * 4;
   if (c >= r.ncols) return;
+  const int tok = tok_of(r.idx, slot, r.N);
   const float4 v = sum_parts(r, slot, c);
   const float vv[4] = {v.x, v.y, v.z, v.w};
   uint16_t o[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e] * inv + bf2f(r.bias[c + e]));
+  for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e] + bf2f(r.bias[c + e]));
   uint16_t *dst;
   if (c < r.qw)
     dst = r.q + slot * r.qw + c;
@@ -480,12 +473,15 @@ __global__ __launch_bounds__(256) void k_red_o(RedArgs r) {
     h.z = v.z + __uint_as_float(xb.y << 16);
     h.w = v.w + __uint_as_float(xb.y & 0xFFFF0000u);
     *reinterpret_cast<float4 *>(r.h1 + slot * r.d + c) = h;
-    const uint16_t b0 = f2bf(h.x), b1 = f2bf(h.y), b2 = f2bf(h.z), b3 = f2bf(h.w);
+    // the SwiGLU operand carries the MLP RMSNorm gain; 1/rms is applied to its sums
+    const uint2 gb = *reinterpret_cast<const uint2 *>(r.gain + c);
+    const uint16_t b0 = f2bf(h.x * __uint_as_float(gb.x << 16));
+    const uint16_t b1 = f2bf(h.y * __uint_as_float(gb.x & 0xFFFF0000u));
+    const uint16_t b2 = f2bf(h.z * __uint_as_float(gb.y << 16));
+    const uint16_t b3 = f2bf(h.w * __uint_as_float(gb.y & 0xFFFF0000u));
     *reinterpret_cast<uint2 *>(r.hb + slot * r.d + c) =
         make_uint2(b0 | ((uint32_t)b1 << 16), b2 | ((uint32_t)b3 << 16));
-    // the MLP RMSNorm statistics, from the bf16 values the gate/up GEMM reads
-    const float f0 = bf2f(b0), f1 = bf2f(b1), f2 = bf2f(b2), f3 = bf2f(b3);
-    ss = f0 * f0 + f1 * f1 + f2 * f2 + f3 * f3;
+    ss = h.x * h.x + h.y * h.y + h.z * h.z + h.w * h.w;
   }
   ss = block_sum256(ss, red);
   if (threadIdx.x == 0) r.ssq[slot * gridDim.y + blockIdx.y] = ss;
@@ -809,7 +805,7 @@ int pick_splits(int tiles, int K, int want_wgs, long rows, int ncols, size_t cap
 template <int MODE>
 fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int B, int want_wgs) {
   g.m_tiles = B * ((g.N + MT - 1) / MT);
-  g.n_tiles = (MODE == G_GU) ? (g.Nout + 63) / 64 : (g.Nout + 127) / 128;
+  g.n_tiles = (g.Nout + WTraits<MODE>::COLS - 1) / WTraits<MODE>::COLS;
   int s = (MODE == G_GU) ? 1
                          : pick_splits(g.m_tiles * g.n_tiles, g.K, want_wgs, g.rows, g.Nout,
                                        ctx->part_elems);
@@ -857,12 +853,17 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   r.qw = nh * hd; r.kw = nkv * hd;
   fc_status rc;
 
-  // 1. gathered rows (RMSNorm gain on the weight fragments) -> QKV partials; the
-  //    reduction applies 1/rms(x) + bias,
-  //    stores q and scatters raw k, v into the current frame's cache rows
+  // 1. gather + RMSNorm of the recomputed rows -> QKV partials; the reduction adds the
+  //    bias, stores q and scatters raw k, v into the current frame's cache rows
   {
+    {
+      ProfScope ps(ctx, st, "fc_gather_norm");
+      hipLaunchKernelGGL(k_gather_norm, dim3((unsigned)rows), dim3(256), 0, st, x_cur, L.g_attn,
+                         idx, nrec, N, d, L.rms_eps, ctx->hb);
+      FC_HIP_TRY(hipGetLastError());
+    }
     WArgs g{};
-    g.A = x_cur; g.gather = 1; g.gain = L.g_attn; g.W0 = L.w_qkv;
+    g.A = ctx->hb; g.W0 = L.w_qkv;
     g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
     if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B, want)) != FC_OK) return rc;
@@ -922,21 +923,22 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   // 3. O projection; reduction adds the residual -> h1 (float32) and its bf16 copy
   {
     WArgs g{};
-    g.A = ctx->attn; g.gather = 0; g.W0 = L.w_o;
+    g.A = ctx->attn; g.W0 = L.w_o;
     g.K = nh * hd; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
     if ((rc = run_wgemm<G_O>(ctx, st, "fc_gemm_o", g, B, want)) != FC_OK) return rc;
     r.splits = g.splits; r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq;
+    r.gain = L.g_mlp;
     ProfScope ps(ctx, st, "fc_red_o");
     hipLaunchKernelGGL(k_red_o, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
-  // 4. gate/up with the MLP RMSNorm (gain on the weight fragments, 1/rms from the
-  //    O-reduction's sums of squares), SiLU(g) * u -> act (bf16)
+  // 4. gate/up on bf16(h1 * g_mlp); 1/rms from the O reduction's sums of squares is
+  //    applied to both sums, then SiLU(g) * u -> act (bf16)
   {
     WArgs g{};
-    g.A = ctx->hb; g.gather = 0; g.gain = L.g_mlp; g.W0 = L.w_gate; g.W1 = L.w_up;
+    g.A = ctx->hb; g.W0 = L.w_gate; g.W1 = L.w_up;
     g.K = d; g.Nout = ffn; g.N = N; g.idx = idx; g.nrec = nrec;
     g.rows = rows; g.act = ctx->act; g.eps = L.rms_eps;
     g.ssq = ctx->ssq; g.ss_parts = (d + 1023) / 1024;
@@ -946,7 +948,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   // 5. down projection; reduction adds h1 and scatters bf16 rows into the output cache
   {
     WArgs g{};
-    g.A = ctx->act; g.gather = 0; g.W0 = L.w_down;
+    g.A = ctx->act; g.W0 = L.w_down;
     g.K = ffn; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
     if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B, want)) != FC_OK) return rc;
