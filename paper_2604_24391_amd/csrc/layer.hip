@@ -145,66 +145,80 @@ template <int MODE>
 struct WTraits {
   // SwiGLU: each wave computes the gate and the up block of the same 32 columns, so
   // every activation fragment feeds two MFMAs and SiLU(g) * u needs no exchange
-  static constexpr int NB = MODE == G_GU ? 2 : 1;               // weight blocks per wave
-  static constexpr int PD = MODE == G_GU ? 3 : 4;               // K steps in flight
-  static constexpr int COLS = 128;                              // output columns per workgroup
+  static constexpr int NB = MODE == G_GU ? 2 : 1;     // weight blocks per wave
+  static constexpr int COLS = 128;                    // output columns per workgroup
+  static constexpr int BROWS = 128 * NB;              // weight rows staged per K step
 };
 
-constexpr int NST = PD;          // activation stages in LDS (the weight prefetch depth)
+constexpr int kLdsBytes = 152 * 1024;                 // activation + weight stages
+
+// Stage geometry for a tile of MBC 32-row blocks: bf16 elements of the activation
+// and weight parts, and how many stages (K steps in flight, at most 4) fit in LDS.
+template <int MODE, int MBC>
+struct WStage {
+  static constexpr int AROWS = MBC * 32;
+  static constexpr int BROWS = WTraits<MODE>::BROWS;
+  static constexpr int ELEMS = (AROWS + BROWS) * BK;
+  static constexpr int PD = (kLdsBytes / (ELEMS * 2)) < 4 ? (kLdsBytes / (ELEMS * 2)) : 4;
+  static_assert(PD >= 2, "at least two stages");
+};
+
+// XOR swizzle of the 16-B chunks of a 128-B LDS row: the 16 lanes served together
+// by a b128 read (16 consecutive rows at one chunk) land on distinct banks.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
 // The K loop for a tile whose valid rows fill MBC 32-row blocks.
-//   * activations: gathered rows go straight from global memory into a ring of NST
-//     LDS stages (global_load_lds, 16 B per lane), 16-B chunks XOR-swizzled by row so
-//     that the MFMA fragment reads are free of bank conflicts;
-//   * weights: each wave's 32 rows (SwiGLU: 32 gate and 32 up rows) stream into a
-//     ring of PD register stages.
-// Loads of step kt are all issued together, PD steps ahead, so the in-order load
-// counter keeps PD steps in flight.  Straight-line code: out-of-range rows and K
-// steps read clamped in-bounds addresses (padding steps use zero weights).
+//   * every K step stages the activation rows and the workgroup's weight rows in LDS
+//     through global_load_lds, 16 B per lane, 8 full 128-B rows per instruction, with
+//     the 16-B chunks of each row XOR-swizzled so the MFMA fragment reads do not
+//     conflict;
+//   * PD stages are in flight; the loads of one K step form one group, so a single
+//     vmcnt wait per step (plus a barrier) hands a complete stage to the MFMAs;
+//   * straight-line code: rows past the valid ones and K steps past the end read
+//     clamped in-bounds addresses; padding steps contribute zero.
+// The loads and LDS reads are inline asm: the compiler cannot follow this loop's
+// load groups across the back edge and would otherwise drain them every step.
 template <int MODE, int MBC>
-__device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ S0,
-                                           __bf16 *__restrict__ S1, __bf16 *__restrict__ S2,
-                                           __bf16 *__restrict__ S3, float *rowinv, int b, int row0,
-                                           int nvalid, int k0, int nk, int cb, bool wvalid,
-                                           int sp) {
-  constexpr int ROWS = MBC * 32;
+__device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *rowinv, int b,
+                                           int row0, int nvalid, int nt, int k0, int nk,
+                                           bool wvalid, int sp) {
+  using G = WStage<MODE, MBC>;
   constexpr int NB = WTraits<MODE>::NB;
-  constexpr int PD = WTraits<MODE>::PD;
-  // one LDS array per stage: the stage of step kt is kt % PD, a compile-time constant
-  // in the unrolled loop
-  __bf16 *const stages[4] = {S0, S1, S2, S3};
+  constexpr int PD = G::PD;
+  constexpr int AI = G::AROWS / 32;    // activation DMA instructions per wave per step
+  constexpr int BI = G::BROWS / 32;    // weight DMA instructions per wave per step
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int nk_pad = (nk + PD - 1) / PD * PD;
-  const uint16_t *wrow[NB];
-  wrow[0] = a.W0 + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
-  if (NB == 2) wrow[NB - 1] = a.W1 + (long)(wvalid ? cb + l32 : 0) * a.K + k0 + 8 * hi;
+  const int cb = nt * WTraits<MODE>::COLS + w * 32;   // this wave's output columns
 
-  // activation loads: instruction i of wave w covers rows (4 i + w) * 8 .. + 7; lane
-  // -> row (4 i + w) * 8 + lane / 8, LDS slot lane % 8 holding chunk slot ^ (row % 8)
-  uint32_t aoff[MBC];
+  // per-lane source offsets (elements) of the rows this lane stages
+  uint32_t aoff[AI];
 #pragma unroll
-  for (int i = 0; i < MBC; ++i) {
+  for (int i = 0; i < AI; ++i) {
     const int r = (4 * i + w) * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ (r & 7);
     const long slot = (long)b * a.N + row0 + (r < nvalid ? r : 0);
-    aoff[i] = (uint32_t)(slot * a.K + k0 + chunk * 8);
+    aoff[i] = (uint32_t)(slot * a.K + k0 + (((lane & 7) ^ swz(r)) * 8));
   }
-  auto loadA = [&](int kt, int u) {
-    const int kk = min(kt, nk - 1) * BK;
-    const uint32_t dst = lds_addr(stages[u]) + w * 1024;
+  const uint16_t *bsrc[BI];
 #pragma unroll
-    for (int i = 0; i < MBC; ++i) dma16(a.A + aoff[i] + kk, dst + i * 4096);
-  };
+  for (int i = 0; i < BI; ++i) {
+    const int r = (4 * i + w) * 8 + (lane >> 3);        // staged weight row
+    const bool up = (MODE == G_GU) && r >= 128;
+    int n = nt * WTraits<MODE>::COLS + (r & 127);        // output column of that row
+    if (n >= a.Nout) n = 0;
+    bsrc[i] = (up ? a.W1 : a.W0) + (long)n * a.K + k0 + (((lane & 7) ^ swz(r)) * 8);
+  }
+  const uint32_t lbase = lds_addr(lds);
 
-  uint4 rb[PD][NB][4];
-  auto loadB = [&](int kt, int u) {
+  auto load_step = [&](int kt, int u) {
     const int kk = min(kt, nk - 1) * BK;
+    const uint32_t st = lbase + u * G::ELEMS * 2;
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int i = 0; i < AI; ++i) dma16(a.A + aoff[i] + kk, st + (4 * i + w) * 1024);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) rb[u][j][s] = gload16(wrow[j] + kk + 16 * s);
+    for (int i = 0; i < BI; ++i) dma16(bsrc[i] + kk, st + G::AROWS * 128 + (4 * i + w) * 1024);
   };
 
   f32x16 acc[NB][MBC];
@@ -216,77 +230,73 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
       for (int e = 0; e < 16; ++e) acc[j][mb][e] = 0.f;
 
 #pragma unroll
-  for (int u = 0; u < PD; ++u) {
-    loadA(u, u);
-    loadB(u, u);
-  }
+  for (int u = 0; u < PD; ++u) load_step(u, u);
 
   for (int kt0 = 0; kt0 < nk_pad; kt0 += PD) {
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
       const int kt = kt0 + u;
       const bool live = kt < nk;
-      // this thread's loads for step kt are the oldest PD-1 steps back; wait for them,
-      // then the barrier makes every thread's share of the stage visible.  (A plain
-      // s_barrier: __syncthreads' release fence would drain every in-flight load.)
-      constexpr int kLater = (PD - 1) * (MBC + 4 * NB);
+      // this thread's share of step kt is the oldest group; then the barrier makes the
+      // whole stage visible (a plain s_barrier: __syncthreads' release fence would
+      // drain every in-flight load)
+      constexpr int kLater = (PD - 1) * (AI + BI);
       static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
       __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int j = 0; j < NB; ++j) anchor(rb[u][j][s]);
       __builtin_amdgcn_s_barrier();
-      // fragment (mb, s): row mb*32 + l32, 16-B chunk 2 s + hi, stored at slot chunk ^ (row % 8)
-      const uint32_t abase = lds_addr(stages[u]) + l32 * (BK * 2);
-      const int sw = l32 & 7;
-      bf16x8 af[MBC], an[MBC];
+      // fragment (row, s): 16-B chunk 2 s + hi of the row, at slot chunk ^ swz(row)
+      const uint32_t st = lbase + u * G::ELEMS * 2;
+      const uint32_t arow = st + l32 * 128;
+      uint32_t brow[NB];
 #pragma unroll
-      for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(abase + mb * 32 * BK * 2 + ((hi ^ sw) << 4));
+      for (int j = 0; j < NB; ++j) brow[j] = st + (G::AROWS + j * 128 + w * 32 + l32) * 128;
+      const int sw = swz(l32);          // row % 16 is l32 % 16 for every block
+      bf16x8 af[MBC], an[MBC], bf[NB], bn[NB];
+#pragma unroll
+      for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(arow + mb * 32 * 128 + ((hi ^ sw) << 4));
+#pragma unroll
+      for (int j = 0; j < NB; ++j) bf[j] = lds_read16(brow[j] + ((hi ^ sw) << 4));
       lds_wait(af);
+      lds_wait(bf);
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         if (s < 3) {
           const int slot = (2 * (s + 1) + hi) ^ sw;
 #pragma unroll
-          for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(abase + mb * 32 * BK * 2 + (slot << 4));
+          for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(arow + mb * 32 * 128 + (slot << 4));
+#pragma unroll
+          for (int j = 0; j < NB; ++j) bn[j] = lds_read16(brow[j] + (slot << 4));
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          const uint4 bw = live ? rb[u][j][s] : make_uint4(0, 0, 0, 0);
-          const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+          const bf16x8 bv = live ? bf[j] : bf16x8{};
 #pragma unroll
           for (int mb = 0; mb < MBC; ++mb)
             acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[j][mb], 0, 0, 0);
         }
         if (s < 3) {
           lds_wait(an);
+          lds_wait(bn);
 #pragma unroll
           for (int mb = 0; mb < MBC; ++mb) af[mb] = an[mb];
+#pragma unroll
+          for (int j = 0; j < NB; ++j) bf[j] = bn[j];
         }
       }
       // every wave is done with this stage before any thread refills it
       __builtin_amdgcn_s_barrier();
-      loadA(kt + PD, u);
-      loadB(kt + PD, u);
+      load_step(kt + PD, u);
     }
   }
-
-  // drain the clamped prefetches of the last steps before their registers or LDS are
-  // reused: the anchors keep every ring register live until the loads have landed
+  // drain the clamped prefetches of the last steps before LDS is reused
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-  for (int u = 0; u < PD; ++u)
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int j = 0; j < NB; ++j) anchor(rb[u][j][s]);
   __syncthreads();
+
   // lane holds column l32 and rows (e/4)*8 + hi*4 + e%4 of each 32-row block
   const long slot0 = (long)b * a.N + row0;
   if (MODE == G_GU) {
     // 1/rms of each row from the per-chunk sums of squares of h1
-    for (int r = t; r < ROWS; r += 256) {
+    for (int r = t; r < G::AROWS; r += 256) {
       float v = 0.f;
       if (r < nvalid)
         for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
@@ -324,8 +334,7 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *__restrict__ 
 
 template <int MODE>
 __global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
-  // contiguous in practice (S0 then S1): the SwiGLU exchange spans both
-  __shared__ __attribute__((aligned(16))) __bf16 S0[MT * BK], S1[MT * BK], S2[MT * BK], S3[MT * BK];
+  __shared__ __attribute__((aligned(16))) __bf16 lds[kLdsBytes / 2];
   __shared__ float rowinv[MT];
   const int total = a.m_tiles * a.n_tiles * a.splits;
   const int tile = xcd_tile(blockIdx.x, total);
@@ -342,17 +351,16 @@ __global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
   if (k0 >= k1) return;
   const int nk = (k1 - k0) / BK;
   const int w = threadIdx.x >> 6;
-  const int cb = nt * WTraits<MODE>::COLS + w * 32;
-  const bool wvalid = cb < a.Nout;
+  const bool wvalid = nt * WTraits<MODE>::COLS + w * 32 < a.Nout;
   switch ((nvalid + 31) >> 5) {
-    case 1: wgemm_tile<MODE, 1>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 2: wgemm_tile<MODE, 2>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 3: wgemm_tile<MODE, 3>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 4: wgemm_tile<MODE, 4>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 5: wgemm_tile<MODE, 5>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 6: wgemm_tile<MODE, 6>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    case 7: wgemm_tile<MODE, 7>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
-    default: wgemm_tile<MODE, 8>(a, S0, S1, S2, S3, rowinv, b, row0, nvalid, k0, nk, cb, wvalid, sp); break;
+    case 1: wgemm_tile<MODE, 1>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 2: wgemm_tile<MODE, 2>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 3: wgemm_tile<MODE, 3>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 4: wgemm_tile<MODE, 4>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 5: wgemm_tile<MODE, 5>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 6: wgemm_tile<MODE, 6>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    case 7: wgemm_tile<MODE, 7>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+    default: wgemm_tile<MODE, 8>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
   }
 }
 
