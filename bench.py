@@ -21,6 +21,7 @@ Also reported, each measured in the same run:
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -47,6 +48,10 @@ def main():
     ap.add_argument("--layers", type=int, default=28)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--calib-mb", type=int, default=0,
+                    help="after the measurement, run an elementwise negation over this many "
+                         "MiB of float32 (reads and writes exactly that many bytes): the "
+                         "reference dispatch that scales the FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the per-step path has no cross-GPU work "
@@ -127,7 +132,9 @@ def main():
         step(s)
     torch.cuda.synchronize()
     n_hist = torch.zeros(args.steps, dtype=torch.int32, device=dev)
+    # timed region: events only around the roofline kernel (fc_gemm_gateup)
     fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_only(ctx, "fc_gemm_gateup")
     fc.fc_profile_enable(ctx, True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -140,23 +147,35 @@ def main():
     ms_step = el * 1e3 / args.steps
     n_mean = float(n_hist.float().mean())
     log(f"{args.steps} steps in {el:.3f}s: {ms_step:.3f} ms/step, mean recomputed tokens {n_mean:.1f}")
+    tot, cnt = fc.fc_profile_read(ctx, "fc_gemm_gateup", reset=True)
+    gu = dict(avg_us=round(tot * 1e3 / cnt, 3), launches=cnt)
 
+    # per-kernel breakdown: a separate untimed pass with events around every launch
     kern = {}
+    nb = max(1, min(args.steps, 8))
+    fc.fc_profile_only(ctx, None)
+    fc.fc_profile_enable(ctx, True)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for k in range(nb):
+        step(args.warmup + args.steps + k)
+    torch.cuda.synchronize()
+    el2 = time.perf_counter() - t2
+    fc.fc_profile_enable(ctx, False)
     for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk", "fc_cache_update", "fc_gather_norm",
                  "fc_gemm_qkv", "fc_red_qkv", "fc_attn", "fc_attn_combine", "fc_gemm_o",
                  "fc_red_o", "fc_gemm_gateup", "fc_gemm_down", "fc_red_down"):
         tot, cnt = fc.fc_profile_read(ctx, name)
         if cnt:
             kern[name] = dict(avg_us=round(tot * 1e3 / cnt, 3), launches=cnt,
-                              share=round(tot / (el * 1e3), 4))
+                              share=round(tot / (el2 * 1e3), 4))
     fc.fc_profile_read(ctx, None, reset=True)
-    gu = kern["fc_gemm_gateup"]
     d, f = shape.d, shape.ffn
     gu_bytes = 2 * f * d * 2 + n_mean * d * 4 + n_mean * f * 2
     achieved = gu_bytes / (gu["avg_us"] * 1e-6) / 1e9
     roofline = dict(bound="hbm", kernel="fc_gemm_gateup", achieved=round(achieved, 1),
                     peak=HBM_PEAK_GBS, unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
-                    traffic=None, bytes_per_launch=round(gu_bytes),
+                    traffic=measured_traffic("fc_gemm_gateup"), bytes_per_launch=round(gu_bytes),
                     avg_us=gu["avg_us"])
 
     result = dict(
@@ -179,8 +198,33 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
                                               T, N, Wn, L, gw)
+    if args.calib_mb > 0:
+        n = args.calib_mb * (1 << 20) // 4
+        src = torch.ones(n, device=dev, dtype=torch.float32)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log(f"calibration: 3 x neg over {args.calib_mb} MiB float32")
+        del src, dst
     ctx.close()
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when
+    there is none or the kernel source changed after the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh).get(kernel)
+    if not rec:
+        return None
+    with open(os.path.join(ROOT, rec["source"]), "rb") as fh:
+        if hashlib.sha256(fh.read()).hexdigest() != rec["source_sha256"]:
+            return None
+    return rec["traffic_bytes"]
 
 
 def bench_select_batch(fc, ctx, torch):

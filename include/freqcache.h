@@ -188,6 +188,10 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
 /* Kernel timing with HIP events recorded on the launch stream around every
  * kernel the context launches (off by default). */
 fc_status fc_profile_enable(fc_ctx *ctx, int32_t on);
+/* Restrict that timing to the launches of kernel `name` (host string, copied);
+ * NULL times every kernel again.  Fewer events keep the timed stream closer to
+ * an untimed one. */
+fc_status fc_profile_only(fc_ctx *ctx, const char *name);
 /* Wait for the recorded events and return the summed duration and launch count
  * of kernel `name` (host string) since the last reset; reset=1 clears all records. */
 fc_status fc_profile_read(fc_ctx *ctx, const char *name, double *total_ms, int64_t *launches,

@@ -32,7 +32,7 @@ fc_status fail(fc_status st, const char *fmt, ...) {
 }
 
 ProfScope::ProfScope(fc_ctx *c, hipStream_t s, const char *name) : ctx(c), st(s) {
-  if (!ctx->prof) return;
+  if (!ctx->prof || (!ctx->prof_only.empty() && ctx->prof_only != name)) return;
   hipEvent_t a, b;
   if (ctx->pool.size() >= 2) {
     a = ctx->pool.back();
@@ -215,6 +215,8 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
                 L->n_heads);
   if (L->d_model > 8192)
     return fail(FC_ERR_UNSUPPORTED, "%s: d_model %d > 8192", who, L->d_model);
+  if (L->n_heads > 128)
+    return fail(FC_ERR_UNSUPPORTED, "%s: n_heads %d > 128", who, L->n_heads);
   if (L->d_model % fc::kGemmBK || L->d_ffn % fc::kGemmBK || (L->n_heads * L->head_dim) % fc::kGemmBK)
     return fail(FC_ERR_SHAPE, "%s: d_model, d_ffn and n_heads*head_dim must be multiples of %d", who,
                 fc::kGemmBK);
@@ -233,6 +235,10 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
       L->d_ffn > c.max_ffn || qkv > c.max_qkv)
     return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%d exceed the context caps",
                 who, B, kv->frame_tokens, S, L->d_model, L->d_ffn, qkv);
+  // the GEMMs address activation rows with 32-bit element offsets
+  const long widest = std::max({(long)L->d_model, (long)L->d_ffn, (long)L->n_heads * L->head_dim});
+  if ((long)B * kv->frame_tokens * widest >= (1L << 32))
+    return fail(FC_ERR_CAPACITY, "%s: B*N*%ld activation elements exceed 2^32", who, widest);
   return FC_OK;
 }
 
@@ -284,6 +290,12 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
 fc_status fc_profile_enable(fc_ctx *ctx, int32_t on) {
   if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_profile_enable: null context");
   ctx->prof = on != 0;
+  return FC_OK;
+}
+
+fc_status fc_profile_only(fc_ctx *ctx, const char *name) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_profile_only: null context");
+  ctx->prof_only = name ? name : "";
   return FC_OK;
 }
 

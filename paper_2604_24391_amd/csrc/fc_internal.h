@@ -63,6 +63,7 @@ struct fc_ctx {
   size_t stage_elems = 0;
   // kernel timing
   bool prof = false;
+  std::string prof_only;       // empty: time every kernel
   std::vector<fc::ProfRec> recs;
   std::vector<hipEvent_t> pool;
 };

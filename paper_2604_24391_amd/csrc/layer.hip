@@ -116,6 +116,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
 // wait insertion (which cannot follow this loop's load groups across the back edge)
 // never drains them; the loop waits for each K step's group with one vmcnt.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint4 gload16(const void *p) {
   u32x4 r;
   asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
@@ -517,6 +518,7 @@ struct AttnArgs {
   const int32_t *idx, *nrec;
   int N, nh, nkv, S, T, W, head;
   int splits, kb_per_split;
+  int tiles;                  // B * ceil(N / 32) query tiles
   float scale_log2;
   uint16_t *out;              // [B*N][nh*HD] (splits == 1)
   float *po;                  // [split][B*N][nh][HD] unnormalised partial output
@@ -532,24 +534,103 @@ __device__ __forceinline__ int key_pos(int row, int T, int N, int W, int head) {
   return T + lg * N + i;
 }
 
+// Workgroup barrier that orders LDS accesses only: global loads in flight stay in
+// flight across it (the full fence of __syncthreads would drain them).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// One staging task of a 32-key block (the same task count for keys and values):
+//   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of one key (pre-RoPE),
+//           the (cos, sin) pairs of those dims at the key's position, and the
+//           position itself (INT_MAX past the end of the cache);
+//   values: dims [4l, 4l + 4) of keys 4kg .. 4kg + 3.
+struct KVRaw {
+  u32x4 k1, k2;
+  u32x4 cs[4];
+  u32x2 v[4];
+  int pos;
+};
+
+// The raw loads are inline asm and their waits explicit: the compiler would otherwise
+// copy the pipelined registers right after issue and wait on every block's loads.
+// These loads read only the cache and the RoPE table, which no kernel of the layer
+// writes while attention runs.
+__device__ __forceinline__ u32x4 kv_load16(const void *p) {
+  u32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p));
+  return r;
+}
+__device__ __forceinline__ u32x2 kv_load8(const void *p) {
+  u32x2 r;
+  asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(r) : "v"(p));
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void kv_anchor(T &r) { asm volatile("" : "+v"(r)); }
+__device__ __forceinline__ float lo_f(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float hi_f(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+__device__ __forceinline__ uint16_t bf16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (__bf16)f);   // round to nearest even
+}
+
+// Rotated keys sit in LDS as unpadded rows of HD bf16; 16-B chunk q of key r is
+// stored at chunk q ^ kswz(r), which spreads both the MFMA reads (16 keys, one
+// chunk) and the staging writes (2 or 4 keys, all chunks) over all banks.
+template <int HD>
+__device__ __forceinline__ int kswz(int key) {
+  return HD == 128 ? (((key & 1) << 3) | ((key >> 1) & 7)) : ((key >> 1) & 7);
+}
+// Values sit as [key / 4][HD / 32][32][4 keys]: the 4 consecutive keys of one dim
+// form one 8-B word (half an MFMA A fragment), and dim h of group h / 32 is at
+// slot (h + h / 32) % 32 of its group, so the staging writes (dims 4 apart across
+// lanes) and the fragment reads (32 consecutive dims) both hit distinct banks.
+template <int HD>
+__device__ __forceinline__ int vq_word(int kg, int hd) {
+  return (kg * (HD / 32) + (hd >> 5)) * 32 + (((hd & 31) + (hd >> 5)) & 31);
+}
+
+// Attention of one 32-query tile of kv head g over key blocks [kb0, kb1) of the cache.
+// Wave w < G handles query head g*G + w.  The 32-key blocks are staged through two
+// LDS buffers (keys rotated, values interleaved) with the raw loads of block kb + 2
+// in flight while block kb is multiplied, so the cache latency is paid once per
+// split rather than once per block.
 template <int HD, int G>
-__global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 16;   // k-steps of the QK^T product
   constexpr int NHB = HD / 32;  // 32-row blocks of the output
-  __shared__ __bf16 Ks[32 * (HD + 8)];
-  __shared__ __bf16 Vt[HD * 40];
-  __shared__ int kpos[32];
+  constexpr int NW = G < 4 ? 4 : G;   // waves: G query heads, at least 4 stagers
+  constexpr int NT = NW * 64;
+  constexpr int CPK = HD / 16;  // key staging tasks per key
+  constexpr int TASKS = 32 * CPK;
+  constexpr int TPT = (TASKS + NT - 1) / NT;
+  constexpr int QLD = HD + 8;   // padded LDS row of the rotated queries
+  static_assert(TASKS % 64 == 0, "staging tasks fill whole waves");
+  static_assert(TASKS == 8 * (HD / 4), "key and value tasks pair up");
+  __shared__ __bf16 Qs[G][32 * QLD];
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][32 * HD];
+  __shared__ __attribute__((aligned(16))) uint2 Vq[2][8 * HD];
+  __shared__ int kpos[2][32];
 
+  // 1-D grid; the query tiles of one (kv head, key split) are consecutive logical
+  // tiles, which xcd_tile places on one XCD, so each XCD's L2 holds only its own
+  // share of the cache
+  const int tiles = a.tiles;
+  const int lt = xcd_tile(blockIdx.x, (int)gridDim.x);
+  const int qt = lt % tiles;
+  const int g = (lt / tiles) % a.nkv;
+  const int sp = lt / (tiles * a.nkv);
   const int tiles_per_b = (a.N + 31) / 32;
-  const int b = blockIdx.x / tiles_per_b;
-  const int j0 = (blockIdx.x % tiles_per_b) * 32;
+  const int b = qt / tiles_per_b;
+  const int j0 = (qt % tiles_per_b) * 32;
   const int n = n_valid(a.nrec, b, a.N);
   if (j0 >= n) return;
-  const int g = blockIdx.y;
-  const int sp = blockIdx.z;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
-  const int h = g * G + w;
+  const bool qwave = w < G;           // waves past G only stage keys and values
+  const int h = g * G + (qwave ? w : 0);
 
   const int j = j0 + l32;
   const bool qvalid = j < n;
@@ -579,11 +660,14 @@ __global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
         qf[s + NS / 2][e] = x2 * cs.x + x1 * cs.y;
       }
   }
-  bf16x8 qb[NS];
+  // each lane keeps its own rotated Q fragments in LDS (read back only by itself)
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
+  for (int s = 0; s < NS; ++s) {
+    bf16x8 v;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qb[s][e] = (__bf16)qf[s][e];
+    for (int e = 0; e < 8; ++e) v[e] = (__bf16)qf[s][e];
+    if (qwave) *reinterpret_cast<bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]) = v;
+  }
 
   f32x16 o[NHB];
 #pragma unroll
@@ -597,83 +681,135 @@ __global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
   const int kb1 = min(nkb, kb0 + a.kb_per_split);
   const long kvbase = (long)b * a.S * a.nkv * HD + (long)g * HD;
   const long kvrow = (long)a.nkv * HD;
+  // only the current frame's keys can lie after a query; other blocks skip the mask
+  const int cur_lo = a.T + ((a.head + a.W - 1) % a.W) * a.N, cur_hi = cur_lo + a.N;
 
-  for (int kb = kb0; kb < kb1; ++kb) {
-    __syncthreads();
-    // stage 32 keys (rotated) and values (transposed) of kv head g
-    for (int task = t; task < 32 * (HD / 16); task += G * 64) {
-      const int key = task / (HD / 16), c = task - key * (HD / 16);
-      const int row = kb * 32 + key;
-      U16x8 k1, k2, v1, v2;
-      if (row < a.S) {
+  // raw loads of block kb (clamped to the split's last block: the extra blocks the
+  // pipeline runs ahead are loaded but never multiplied)
+  auto fetch = [&](int kb, KVRaw (&R)[TPT]) {
+    kb = min(kb, kb1 - 1);
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int task = t + i * NT;
+      if (task < TASKS) {
+        const int key = task / CPK, c = task - key * CPK;
+        const int row0 = kb * 32 + key;
+        const int row = min(row0, a.S - 1);
         const int pos = key_pos(row, a.T, a.N, a.W, a.head);
-        if (c == 0) kpos[key] = pos;
-        const uint16_t *kp = a.kc + kvbase + row * kvrow;
-        const uint16_t *vp = a.vc + kvbase + row * kvrow;
-        k1 = *reinterpret_cast<const U16x8 *>(kp + 8 * c);
-        k2 = *reinterpret_cast<const U16x8 *>(kp + HD / 2 + 8 * c);
-        v1 = *reinterpret_cast<const U16x8 *>(vp + 8 * c);
-        v2 = *reinterpret_cast<const U16x8 *>(vp + HD / 2 + 8 * c);
+        R[i].pos = row0 < a.S ? pos : 0x7fffffff;
+        const uint16_t *kp = a.kc + kvbase + row * kvrow + 8 * c;
+        R[i].k1 = kv_load16(kp);
+        R[i].k2 = kv_load16(kp + HD / 2);
         const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float2 cs = rp[e];
-          const float x1 = bf2f(k1.v[e]), x2 = bf2f(k2.v[e]);
-          k1.v[e] = f2bf(x1 * cs.x - x2 * cs.y);
-          k2.v[e] = f2bf(x2 * cs.x + x1 * cs.y);
+        for (int q = 0; q < 4; ++q) R[i].cs[q] = kv_load16(rp + 2 * q);
+        const int kg = task / (HD / 4), l = task - kg * (HD / 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int vrow = min(kb * 32 + 4 * kg + r, a.S - 1);
+          R[i].v[r] = kv_load8(a.vc + kvbase + vrow * kvrow + 4 * l);
         }
-      } else {
-        if (c == 0) kpos[key] = 0x7fffffff;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) k1.v[e] = k2.v[e] = v1.v[e] = v2.v[e] = 0;
-      }
-      *reinterpret_cast<U16x8 *>(&Ks[key * (HD + 8) + 8 * c]) = k1;
-      *reinterpret_cast<U16x8 *>(&Ks[key * (HD + 8) + HD / 2 + 8 * c]) = k2;
-      uint16_t *vt = reinterpret_cast<uint16_t *>(Vt);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        vt[(8 * c + e) * 40 + key] = v1.v[e];
-        vt[(HD / 2 + 8 * c + e) * 40 + key] = v2.v[e];
       }
     }
-    __syncthreads();
-
-    // S^T block: rows = 32 keys, columns = 32 queries
+  };
+  // the loads of R are complete once only the other set's loads (issued after R's)
+  // may still be in flight
+  auto settle = [&](KVRaw (&R)[TPT]) {
+    constexpr int kLater = 10 * TPT;
+    static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
+    __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      kv_anchor(R[i].k1); kv_anchor(R[i].k2);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) kv_anchor(R[i].cs[q]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) kv_anchor(R[i].v[r]);
+    }
+  };
+  // rotate-half RoPE of the keys into Ks[buf]; values interleaved into Vq[buf]
+  auto stage = [&](const KVRaw (&R)[TPT], int buf) {
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int task = t + i * NT;
+      if (task < TASKS) {
+        const int key = task / CPK, c = task - key * CPK;
+        U16x8 k1, k2;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const u32x4 q = R[i].cs[e >> 1];
+          const float cs = __uint_as_float(q[(e & 1) * 2]), sn = __uint_as_float(q[(e & 1) * 2 + 1]);
+          const uint32_t w1 = R[i].k1[e >> 1], w2 = R[i].k2[e >> 1];
+          const float x1 = (e & 1) ? hi_f(w1) : lo_f(w1), x2 = (e & 1) ? hi_f(w2) : lo_f(w2);
+          k1.v[e] = bf16_bits(x1 * cs - x2 * sn);
+          k2.v[e] = bf16_bits(x2 * cs + x1 * sn);
+        }
+        const int sw = kswz<HD>(key);
+        __bf16 *kr = &Ks[buf][key * HD];
+        *reinterpret_cast<U16x8 *>(kr + 8 * (c ^ sw)) = k1;
+        *reinterpret_cast<U16x8 *>(kr + 8 * ((c + HD / 16) ^ sw)) = k2;
+        if (c == 0) kpos[buf][key] = R[i].pos;
+        const int kg = task / (HD / 4), l = task - kg * (HD / 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int sh = 16 * (j & 1);
+          const uint32_t e0 = (R[i].v[0][j >> 1] >> sh) & 0xFFFFu, e1 = (R[i].v[1][j >> 1] >> sh) & 0xFFFFu;
+          const uint32_t e2 = (R[i].v[2][j >> 1] >> sh) & 0xFFFFu, e3 = (R[i].v[3][j >> 1] >> sh) & 0xFFFFu;
+          Vq[buf][vq_word<HD>(kg, 4 * l + j)] = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+        }
+      }
+    }
+  };
+  // S^T = K Q^T for the 32 keys of buffer buf, online softmax, O^T += V^T P^T
+  auto compute = [&](int buf, bool masked) {
     f32x16 st;
 #pragma unroll
     for (int e = 0; e < 16; ++e) st[e] = 0.f;
+    const int ksw = kswz<HD>(l32);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&Ks[l32 * (HD + 8) + 16 * s + 8 * hi]);
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], st, 0, 0, 0);
+      const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&Ks[buf][l32 * HD + 8 * ((2 * s + hi) ^ ksw)]);
+      const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
+      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv, st, 0, 0, 0);
     }
     float mloc = -INFINITY;
+    if (masked) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = (e >> 2) * 8 + hi * 4 + (e & 3);
-      const float v = (kpos[key] <= qpos) ? st[e] * a.scale_log2 : -INFINITY;
-      st[e] = v;
-      mloc = fmaxf(mloc, v);
+      for (int e = 0; e < 16; ++e) {
+        const int key = (e >> 2) * 8 + hi * 4 + (e & 3);
+        st[e] = (kpos[buf][key] <= qpos) ? st[e] * a.scale_log2 : -INFINITY;
+        mloc = fmaxf(mloc, st[e]);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        st[e] *= a.scale_log2;
+        mloc = fmaxf(mloc, st[e]);
+      }
     }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float m_new = fmaxf(m_run, mloc);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = exp2f(m_run - m_use);
+    if (__ballot(m_new != m_run)) {
+      // some running maximum moved: rescale this wave's sums
+      const float corr = __builtin_amdgcn_exp2f(m_run - m_use);
+      l_run *= corr;
+#pragma unroll
+      for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[hb][e] *= corr;
+    }
+    m_run = m_new;
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      st[e] = exp2f(st[e] - m_use);
+      st[e] = __builtin_amdgcn_exp2f(st[e] - m_use);
       psum += st[e];
     }
-    l_run = l_run * corr + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[hb][e] *= corr;
-    // O^T += V^T P^T; k index (8 hi + i) of step s2 <-> key 16 s2 + 8 (i/4) + 4 hi + i%4,
-    // which is exactly accumulator element 8 s2 + i of S^T in this lane.
-    const uint16_t *vt = reinterpret_cast<const uint16_t *>(Vt);
+    l_run += psum;
+    // k index (8 hi + i) of step s2 <-> key 16 s2 + 8 (i/4) + 4 hi + i%4, which is
+    // accumulator element 8 s2 + i of S^T in this lane; its 4-key halves are words
+    // of key groups 4 s2 + hi and 4 s2 + 2 + hi
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8 pb;
@@ -681,23 +817,44 @@ __global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
       for (int i = 0; i < 8; ++i) pb[i] = (__bf16)st[8 * s2 + i];
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
-        const uint16_t *vr = vt + (hb * 32 + l32) * 40 + 16 * s2 + 4 * hi;
-        const uint2 lo = *reinterpret_cast<const uint2 *>(vr);
-        const uint2 hi8 = *reinterpret_cast<const uint2 *>(vr + 8);
-        bf16x8 va;
-        const uint32_t w4[4] = {lo.x, lo.y, hi8.x, hi8.y};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          va[2 * i] = __builtin_bit_cast(__bf16, (uint16_t)(w4[i] & 0xFFFF));
-          va[2 * i + 1] = __builtin_bit_cast(__bf16, (uint16_t)(w4[i] >> 16));
-        }
+        const int hd = hb * 32 + l32;
+        const uint2 v0 = Vq[buf][vq_word<HD>(4 * s2 + hi, hd)];
+        const uint2 v1 = Vq[buf][vq_word<HD>(4 * s2 + 2 + hi, hd)];
+        const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{v0.x, v0.y, v1.x, v1.y});
         o[hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[hb], 0, 0, 0);
       }
     }
+  };
+  auto needs_mask = [&](int kb) {
+    const int r0 = kb * 32, r1 = r0 + 32;
+    return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
+  };
+
+  KVRaw ra[TPT], rb[TPT];
+  fetch(kb0, ra);
+  fetch(kb0 + 1, rb);
+  settle(ra);
+  stage(ra, 0);
+  lds_barrier();
+  for (int kb = kb0; kb < kb1; kb += 2) {
+    // buffer 0 holds block kb, rb block kb + 1 (in flight)
+    fetch(kb + 2, ra);
+    if (qwave) compute(0, needs_mask(kb));
+    settle(rb);
+    stage(rb, 1);
+    lds_barrier();
+    // buffer 1 holds block kb + 1, ra block kb + 2 (in flight)
+    fetch(kb + 3, rb);
+    if (qwave && kb + 1 < kb1) compute(1, needs_mask(kb + 1));
+    settle(ra);
+    stage(ra, 0);
+    lds_barrier();
   }
+  // nothing may be left in flight into registers the epilogue reuses
+  __builtin_amdgcn_s_waitcnt(0x3F70);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!qvalid) return;
+  if (!qvalid || !qwave) return;
   if (a.splits == 1) {
     uint16_t *orow = a.out + slot * (long)(a.nh * HD) + h * HD;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -707,7 +864,7 @@ __global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
       for (int e = 0; e < 16; ++e)
         orow[hb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3)] = f2bf(o[hb][e] * inv);
   } else {
-    const long plane = (long)gridDim.x / tiles_per_b * a.N;  // B*N
+    const long plane = (long)tiles / tiles_per_b * a.N;  // B*N
     const long pr = ((long)sp * plane + slot) * a.nh + h;
     float *orow = a.po + pr * HD;
 #pragma unroll
@@ -721,29 +878,61 @@ __global__ __launch_bounds__(G * 64) void k_attn(AttnArgs a) {
   }
 }
 
-__global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int HD, int B) {
+// Merges the split-KV partials of one query row: each split's sum is rescaled by
+// 2^(m_s - max m) and the total divided by the rescaled denominators.  blockIdx.y
+// picks 1024 consecutive outputs of the row, one float4 per thread, so all of a
+// thread's split loads are in flight together.
+constexpr int kMaxAttnSplits = 8;
+constexpr int kMaxAttnHeads = 128;
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int HD, int B) {
+  __shared__ float wt[kMaxAttnSplits][kMaxAttnHeads];
   const long slot = blockIdx.x;
   const int b = (int)(slot / a.N), j = (int)(slot - (long)b * a.N);
   if (j >= n_valid(a.nrec, b, a.N)) return;
-  const int h = blockIdx.y;
   const long plane = (long)B * a.N;
-  float mx = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, a.pm[((long)s * plane + slot) * a.nh + h]);
-  const float mu = (mx == -INFINITY) ? 0.f : mx;
-  float l = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const long pr = ((long)s * plane + slot) * a.nh + h;
-    l += a.pl[pr] * exp2f(a.pm[pr] - mu);
-  }
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  for (int d = threadIdx.x; d < HD; d += blockDim.x) {
-    float v = 0.f;
-    for (int s = 0; s < a.splits; ++s) {
-      const long pr = ((long)s * plane + slot) * a.nh + h;
-      v += a.po[pr * HD + d] * exp2f(a.pm[pr] - mu);
+  const int nh = a.nh, splits = a.splits;
+  const int n4 = nh * HD / 4;
+  const int e = blockIdx.y * 256 + threadIdx.x;
+  const int h_lo = (blockIdx.y * 1024) / HD;
+  const int h_hi = min(nh, (blockIdx.y * 1024 + 1023) / HD + 1);
+  for (int h = h_lo + threadIdx.x; h < h_hi; h += blockDim.x) {
+    float m[kMaxAttnSplits], l[kMaxAttnSplits];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kMaxAttnSplits; ++s) {
+      const long pr = ((long)min(s, splits - 1) * plane + slot) * nh + h;
+      m[s] = s < splits ? a.pm[pr] : -INFINITY;
+      l[s] = s < splits ? a.pl[pr] : 0.f;
+      mx = fmaxf(mx, m[s]);
     }
-    a.out[slot * (long)(a.nh * HD) + h * HD + d] = f2bf(v * inv);
+    const float mu = (mx == -INFINITY) ? 0.f : mx;
+    float tot = 0.f;
+#pragma unroll
+    for (int s = 0; s < kMaxAttnSplits; ++s) {
+      m[s] = s < splits ? exp2f(m[s] - mu) : 0.f;
+      tot += l[s] * m[s];
+    }
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+#pragma unroll
+    for (int s = 0; s < kMaxAttnSplits; ++s) wt[s][h] = m[s] * inv;
   }
+  __syncthreads();
+  if (e >= n4) return;
+  const int hh = (4 * e) / HD;
+  const float4 *po = reinterpret_cast<const float4 *>(a.po);
+  float4 p[kMaxAttnSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxAttnSplits; ++s)
+    p[s] = po[((long)min(s, splits - 1) * plane + slot) * n4 + e];
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s = 0; s < kMaxAttnSplits; ++s) {
+    const float ws = wt[s][hh];   // zero for s >= splits
+    v.x += p[s].x * ws; v.y += p[s].y * ws; v.z += p[s].z * ws; v.w += p[s].w * ws;
+  }
+  ushort4 r;
+  r.x = f2bf(v.x); r.y = f2bf(v.y); r.z = f2bf(v.z); r.w = f2bf(v.w);
+  *reinterpret_cast<ushort4 *>(a.out + slot * (long)(nh * HD) + 4 * e) = r;
 }
 
 // ------------------------------------------------------------------------------- rope table
@@ -895,7 +1084,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.out = ctx->attn;
     const int tiles = B * ((N + 31) / 32);
     const int nkb = (S + 31) / 32;
-    int splits = std::max(1, std::min(8, (2 * want) / (tiles * nkv)));
+    int splits = std::max(1, std::min(kMaxAttnSplits, (2 * want) / (tiles * nkv)));
     splits = std::min(splits, std::max(1, nkb / 4));
     while (splits > 1 && (size_t)splits * rows * nh * (hd + 2) > ctx->part_elems) --splits;
     a.kb_per_split = (nkb + splits - 1) / splits;
@@ -904,17 +1093,18 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.pm = ctx->part + (size_t)a.splits * rows * nh * hd;
     a.pl = a.pm + (size_t)a.splits * rows * nh;
     const int G = nh / nkv;
-    dim3 grid(tiles, nkv, a.splits);
+    a.tiles = tiles;
+    dim3 grid(tiles * nkv * a.splits);
     {
       ProfScope ps(ctx, st, "fc_attn");
       if (hd == 128 && G == 7)
         hipLaunchKernelGGL((k_attn<128, 7>), grid, dim3(7 * 64), 0, st, a);
       else if (hd == 128 && G == 1)
-        hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3(256), 0, st, a);
       else if (hd == 64 && G == 1)
-        hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3(256), 0, st, a);
       else if (hd == 64 && G == 2)
-        hipLaunchKernelGGL((k_attn<64, 2>), grid, dim3(128), 0, st, a);
+        hipLaunchKernelGGL((k_attn<64, 2>), grid, dim3(256), 0, st, a);
       else if (hd == 128 && G == 4)
         hipLaunchKernelGGL((k_attn<128, 4>), grid, dim3(256), 0, st, a);
       else
@@ -923,7 +1113,8 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     }
     if (a.splits > 1) {
       ProfScope ps(ctx, st, "fc_attn_combine");
-      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)rows, nh), dim3(128), 0, st, a, hd, B);
+      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)rows, (nh * hd / 4 + 255) / 256), dim3(256),
+                         0, st, a, hd, B);
       FC_HIP_TRY(hipGetLastError());
     }
   }

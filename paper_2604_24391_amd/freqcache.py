@@ -29,7 +29,8 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
-           "fc_cache_update", "fc_layer_forward", "fc_profile_enable", "fc_profile_read")
+           "fc_cache_update", "fc_layer_forward", "fc_profile_enable", "fc_profile_only",
+           "fc_profile_read")
 
 
 class FcError(RuntimeError):
@@ -94,10 +95,11 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_int32, c_void_p]
         L.fc_profile_enable.argtypes = [c_void_p, c_int32]
+        L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_cache_update", "fc_layer_forward",
-                  "fc_profile_enable", "fc_profile_read"):
+                  "fc_profile_enable", "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
         _lib = L
     return _lib
@@ -366,6 +368,11 @@ def fc_cache_update(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev: torch.T
 # ------------------------------------------------------------------------------ timing
 def fc_profile_enable(ctx: Context, on: bool = True):
     _check(lib().fc_profile_enable(ctx.handle, int(on)))
+
+
+def fc_profile_only(ctx: Context, name: str | None = None):
+    """Time only kernel `name` (None: every kernel) while profiling is enabled."""
+    _check(lib().fc_profile_only(ctx.handle, name.encode() if name else None))
 
 
 def fc_profile_read(ctx: Context, name: str | None = None, reset: bool = False):
