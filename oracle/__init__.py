@@ -8,7 +8,8 @@ does and shares no code with it.
 
 Parity pins: every function is pinned by tests/test_oracle_*.py against
 library routines, closed forms, invariants and brute force (see each test's
-docstring).  The paper prints no worked numeric example, so readings the
-paper leaves open (listed in the design doc) are pinned only by those invariants.
+docstring).  The paper prints no worked numeric example, so the readings
+where it is silent (see the select and layer module headers) rest on those
+pins and on the paper's hyper-parameters, not on printed intermediate values.
 """
 from . import select, layer  # noqa: F401

@@ -17,7 +17,7 @@ which the paper computes things:
   Module III (Sec. 4.3, Eqs. 3-6, 4-4): spectral entropy and adaptive budget;
   Fusion     (Sec. 4.4, Algorithm 1): candidates, ascending-energy top-K.
 
-Readings where the paper is silent or garbled (each is listed in the design doc):
+Readings where the paper is silent or garbled:
   * colour -> one channel: BT.601 luma of the [0,1] RGB frame;
   * DFT unnormalised; DCT-II orthonormal;
   * "feature maps" of Modules I/III: the token-grid map of mean luma;
