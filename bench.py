@@ -171,7 +171,8 @@ def main():
                               share=round(tot / (el2 * 1e3), 4))
     fc.fc_profile_read(ctx, None, reset=True)
     d, f = shape.d, shape.ffn
-    gu_bytes = 2 * f * d * 2 + n_mean * d * 4 + n_mean * f * 2
+    # weights (gate + up) + gathered bf16 rows + per-chunk sums of squares + bf16 SwiGLU out
+    gu_bytes = 2 * f * d * 2 + n_mean * (d * 2 + ((d + 1023) // 1024) * 4 + f * 2)
     achieved = gu_bytes / (gu["avg_us"] * 1e-6) / 1e9
     roofline = dict(bound="hbm", kernel="fc_gemm_gateup", achieved=round(achieved, 1),
                     peak=HBM_PEAK_GBS, unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
