@@ -235,7 +235,11 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
       L->d_ffn > c.max_ffn || qkv > c.max_qkv)
     return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%d exceed the context caps",
                 who, B, kv->frame_tokens, S, L->d_model, L->d_ffn, qkv);
-  // the GEMMs address activation rows with 32-bit element offsets
+  // the GEMMs address weights and activation rows with 32-bit element offsets
+  const long wmax = std::max({(long)qkv, (long)L->d_model, (long)L->d_ffn}) *
+                    std::max({(long)L->d_model, (long)L->d_ffn, (long)L->n_heads * L->head_dim});
+  if (wmax >= (1L << 32))
+    return fail(FC_ERR_UNSUPPORTED, "%s: weight matrices of 2^32 or more elements", who);
   const long widest = std::max({(long)L->d_model, (long)L->d_ffn, (long)L->n_heads * L->head_dim});
   if ((long)B * kv->frame_tokens * widest >= (1L << 32))
     return fail(FC_ERR_CAPACITY, "%s: B*N*%ld activation elements exceed 2^32", who, widest);

@@ -69,8 +69,7 @@ __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
 enum { G_QKV = 0, G_O = 1, G_GU = 2, G_DOWN = 3 };
 constexpr int BK = kGemmBK;       // 64
 constexpr int MT = 256;           // rows per M tile: 8 MFMA blocks of 32
-constexpr int LDA = BK + 8;       // LDS row stride in bf16 (16-B pad)
-constexpr int PD = 4;             // weight K-steps in flight per wave
+constexpr int kMinSplitK = 4 * BK;  // shortest K range worth a split of its own
 
 struct WArgs {
   const uint16_t *A;              // bf16 activations, one row per slot
@@ -153,30 +152,42 @@ struct WTraits {
 
 constexpr int kLdsBytes = 152 * 1024;                 // activation + weight stages
 
-// Stage geometry for a tile of MBC 32-row blocks: bf16 elements of the activation
-// and weight parts, and how many stages (K steps in flight, at most 4) fit in LDS.
+// K step of the weight-streaming GEMM: 64, so that every operand row of a stage is
+// one full 128-B line (the vector memory path is bound by requests, not bytes).
+constexpr int KS = 64;
+constexpr int KCH = KS / 8;            // 16-B chunks per LDS row
+constexpr int RPI = 1024 / (KS * 2);   // rows one wave's DMA instruction fills
+
+// Stage geometry for a tile of MBC 32-row blocks: the activation rows are loaded in
+// groups of 64 (one per wave and instruction round), the weight rows of the
+// workgroup follow; PD stages fit in LDS.
 template <int MODE, int MBC>
 struct WStage {
-  static constexpr int AROWS = MBC * 32;
+  static constexpr int AROWS = MBC * 32;                 // rows the MFMAs read
+  static constexpr int ALOAD = (AROWS + 4 * RPI - 1) / (4 * RPI) * (4 * RPI);  // rows staged
   static constexpr int BROWS = WTraits<MODE>::BROWS;
-  static constexpr int ELEMS = (AROWS + BROWS) * BK;
-  static constexpr int PD = (kLdsBytes / (ELEMS * 2)) < 4 ? (kLdsBytes / (ELEMS * 2)) : 4;
+  static constexpr int BYTES = (ALOAD + BROWS) * KS * 2;
+  static constexpr int PD = (kLdsBytes / BYTES) < 8 ? (kLdsBytes / BYTES) : 8;
   static_assert(PD >= 2, "at least two stages");
 };
 
-// XOR swizzle of the 16-B chunks of a 128-B LDS row: the 16 lanes served together
-// by a b128 read (16 consecutive rows at one chunk) land on distinct banks.
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// XOR swizzle of the 16-B chunks of an LDS row: the 16 lanes served together by a
+// b128 read (16 consecutive rows at one chunk) land on distinct banks of the 256-B
+// bank window.
+__device__ __forceinline__ int swz(int row) {
+  return KCH == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+}
 
 // The K loop for a tile whose valid rows fill MBC 32-row blocks.
 //   * every K step stages the activation rows and the workgroup's weight rows in LDS
-//     through global_load_lds, 16 B per lane, 8 full 128-B rows per instruction, with
-//     the 16-B chunks of each row XOR-swizzled so the MFMA fragment reads do not
-//     conflict;
-//   * PD stages are in flight; the loads of one K step form one group, so a single
-//     vmcnt wait per step (plus a barrier) hands a complete stage to the MFMAs;
-//   * straight-line code: rows past the valid ones and K steps past the end read
-//     clamped in-bounds addresses; padding steps contribute zero.
+//     through global_load_lds, 16 B per lane, whole rows per instruction, with the
+//     chunks of each row XOR-swizzled so the MFMA fragment reads do not conflict;
+//   * PD stages rotate: at step k one vmcnt wait and one barrier hand stage k to the
+//     MFMAs and free the stage of step k - 1, which is refilled at once with step
+//     k + PD - 1, so PD - 1 stages are in flight while one is multiplied;
+//   * rows past the valid ones read clamped in-bounds addresses; the last PD - 1
+//     steps issue no loads and drain instead, and the steps that pad the count to a
+//     multiple of PD multiply zeros.
 // The loads and LDS reads are inline asm: the compiler cannot follow this loop's
 // load groups across the back edge and would otherwise drain them every step.
 template <int MODE, int MBC>
@@ -186,40 +197,46 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *r
   using G = WStage<MODE, MBC>;
   constexpr int NB = WTraits<MODE>::NB;
   constexpr int PD = G::PD;
-  constexpr int AI = G::AROWS / 32;    // activation DMA instructions per wave per step
-  constexpr int BI = G::BROWS / 32;    // weight DMA instructions per wave per step
+  constexpr int AI = G::ALOAD / (4 * RPI);   // activation DMA instructions per wave per step
+  constexpr int BI = G::BROWS / (4 * RPI);   // weight DMA instructions per wave per step
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
-  const int nk_pad = (nk + PD - 1) / PD * PD;
   const int cb = nt * WTraits<MODE>::COLS + w * 32;   // this wave's output columns
 
   // per-lane source offsets (elements) of the rows this lane stages
   uint32_t aoff[AI];
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
-    const int r = (4 * i + w) * 8 + (lane >> 3);
+    const int r = (4 * i + w) * RPI + lane / KCH;
     const long slot = (long)b * a.N + row0 + (r < nvalid ? r : 0);
-    aoff[i] = (uint32_t)(slot * a.K + k0 + (((lane & 7) ^ swz(r)) * 8));
+    aoff[i] = (uint32_t)(slot * a.K + k0 + (((lane % KCH) ^ swz(r)) * 8));
   }
-  const uint16_t *bsrc[BI];
+  // weight rows: 32-bit element offsets; in SwiGLU mode the second half of the
+  // instructions stage the up rows (rows 128.. of the stage), so the matrix is
+  // known per unrolled instruction
+  uint32_t boff[BI];
 #pragma unroll
   for (int i = 0; i < BI; ++i) {
-    const int r = (4 * i + w) * 8 + (lane >> 3);        // staged weight row
-    const bool up = (MODE == G_GU) && r >= 128;
+    const int r = (4 * i + w) * RPI + lane / KCH;       // staged weight row
     int n = nt * WTraits<MODE>::COLS + (r & 127);        // output column of that row
     if (n >= a.Nout) n = 0;
-    bsrc[i] = (up ? a.W1 : a.W0) + (long)n * a.K + k0 + (((lane & 7) ^ swz(r)) * 8);
+    boff[i] = (uint32_t)((long)n * a.K + k0 + (((lane % KCH) ^ swz(r)) * 8));
   }
+  static_assert(MODE != G_GU || (BI % 2 == 0 && 4 * (BI / 2) * RPI == 128),
+                "the up rows start at an instruction boundary");
   const uint32_t lbase = lds_addr(lds);
 
   auto load_step = [&](int kt, int u) {
-    const int kk = min(kt, nk - 1) * BK;
-    const uint32_t st = lbase + u * G::ELEMS * 2;
+    const int kk = min(kt, nk - 1) * KS;
+    const uint32_t st = lbase + u * G::BYTES;
 #pragma unroll
     for (int i = 0; i < AI; ++i) dma16(a.A + aoff[i] + kk, st + (4 * i + w) * 1024);
 #pragma unroll
-    for (int i = 0; i < BI; ++i) dma16(bsrc[i] + kk, st + G::AROWS * 128 + (4 * i + w) * 1024);
+    for (int i = 0; i < BI; ++i) {
+      const uint16_t *wm = (MODE == G_GU && i >= BI / 2) ? a.W1 : a.W0;
+      dma16(wm + boff[i] + kk, st + G::ALOAD * KS * 2 + (4 * i + w) * 1024);
+    }
   };
 
   f32x16 acc[NB][MBC];
@@ -230,63 +247,81 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *r
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[j][mb][e] = 0.f;
 
+  // With three or more stages the refill of step k + PD - 1 goes into the stage of
+  // step k - 1 right after the barrier of step k.  With two stages that would leave
+  // nothing in flight at the wait, so the stage just multiplied is refilled (after a
+  // second barrier) with step k + 2 instead.
+  constexpr bool kTwo = PD == 2;
+  constexpr int kAhead = kTwo ? PD : PD - 1;      // steps loaded ahead of the MFMAs
 #pragma unroll
-  for (int u = 0; u < PD; ++u) load_step(u, u);
+  for (int u = 0; u < kAhead; ++u) load_step(u, u);
 
+  const int sw = swz(l32);              // row % 16 is l32 % 16 for every block
+  const int nk_pad = (nk + PD - 1) / PD * PD;
   for (int kt0 = 0; kt0 < nk_pad; kt0 += PD) {
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
       const int kt = kt0 + u;
-      const bool live = kt < nk;
-      // this thread's share of step kt is the oldest group; then the barrier makes the
-      // whole stage visible (a plain s_barrier: __syncthreads' release fence would
-      // drain every in-flight load)
-      constexpr int kLater = (PD - 1) * (AI + BI);
-      static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
-      __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
-      __builtin_amdgcn_s_barrier();
-      // fragment (row, s): 16-B chunk 2 s + hi of the row, at slot chunk ^ swz(row)
-      const uint32_t st = lbase + u * G::ELEMS * 2;
-      const uint32_t arow = st + l32 * 128;
-      uint32_t brow[NB];
+      const bool live = kt < nk;         // padding steps multiply zeros
+      {
+        // this thread's share of step kt is complete once only the later steps'
+        // loads may be outstanding; the barrier then makes the whole stage visible
+        // (a plain s_barrier: __syncthreads' release fence would drain every
+        // in-flight load)
+        const bool refill = kt + kAhead < nk + (kTwo ? 1 : 0);
+        constexpr int kLater = (kAhead - 1) * (AI + BI);
+        static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
+        if (kTwo || refill)
+          __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
+        else
+          __builtin_amdgcn_s_waitcnt(0x3F70);
+        __builtin_amdgcn_s_barrier();
+        if (!kTwo && refill) load_step(kt + PD - 1, (u + PD - 1) % PD);
+        // fragment (row, s): 16-B chunk 2 s + hi of the row, at slot chunk ^ swz(row)
+        const uint32_t st = lbase + u * G::BYTES;
+        const uint32_t arow = st + l32 * (KS * 2);
+        uint32_t brow[NB];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) brow[j] = st + (G::AROWS + j * 128 + w * 32 + l32) * 128;
-      const int sw = swz(l32);          // row % 16 is l32 % 16 for every block
-      bf16x8 af[MBC], an[MBC], bf[NB], bn[NB];
+        for (int j = 0; j < NB; ++j) brow[j] = st + (G::ALOAD + j * 128 + w * 32 + l32) * (KS * 2);
+        bf16x8 af[MBC], an[MBC], bf[NB], bn[NB];
 #pragma unroll
-      for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(arow + mb * 32 * 128 + ((hi ^ sw) << 4));
+        for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(arow + mb * 32 * (KS * 2) + ((hi ^ sw) << 4));
 #pragma unroll
-      for (int j = 0; j < NB; ++j) bf[j] = lds_read16(brow[j] + ((hi ^ sw) << 4));
-      lds_wait(af);
-      lds_wait(bf);
+        for (int j = 0; j < NB; ++j) bf[j] = lds_read16(brow[j] + ((hi ^ sw) << 4));
+        lds_wait(af);
+        lds_wait(bf);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s < 3) {
-          const int slot = (2 * (s + 1) + hi) ^ sw;
+        for (int s = 0; s < KS / 16; ++s) {
+          if (s + 1 < KS / 16) {
+            const int slot = (2 * (s + 1) + hi) ^ sw;
 #pragma unroll
-          for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(arow + mb * 32 * 128 + (slot << 4));
+            for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(arow + mb * 32 * (KS * 2) + (slot << 4));
 #pragma unroll
-          for (int j = 0; j < NB; ++j) bn[j] = lds_read16(brow[j] + (slot << 4));
+            for (int j = 0; j < NB; ++j) bn[j] = lds_read16(brow[j] + (slot << 4));
+          }
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const bf16x8 bv = live ? bf[j] : bf16x8{};
+#pragma unroll
+            for (int mb = 0; mb < MBC; ++mb)
+              acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[j][mb], 0, 0, 0);
+          }
+          if (s + 1 < KS / 16) {
+            lds_wait(an);
+            lds_wait(bn);
+#pragma unroll
+            for (int mb = 0; mb < MBC; ++mb) af[mb] = an[mb];
+#pragma unroll
+            for (int j = 0; j < NB; ++j) bf[j] = bn[j];
+          }
         }
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const bf16x8 bv = live ? bf[j] : bf16x8{};
-#pragma unroll
-          for (int mb = 0; mb < MBC; ++mb)
-            acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[j][mb], 0, 0, 0);
-        }
-        if (s < 3) {
-          lds_wait(an);
-          lds_wait(bn);
-#pragma unroll
-          for (int mb = 0; mb < MBC; ++mb) af[mb] = an[mb];
-#pragma unroll
-          for (int j = 0; j < NB; ++j) bf[j] = bn[j];
+        if (kTwo) {
+          // every wave is done with this stage before any thread refills it; the
+          // clamped loads past the end keep the per-step load count constant
+          __builtin_amdgcn_s_barrier();
+          load_step(kt + PD, u);
         }
       }
-      // every wave is done with this stage before any thread refills it
-      __builtin_amdgcn_s_barrier();
-      load_step(kt + PD, u);
     }
   }
   // drain the clamped prefetches of the last steps before LDS is reused
@@ -350,7 +385,7 @@ __global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
   const int k0 = sp * a.kchunk;
   const int k1 = min(a.K, k0 + a.kchunk);
   if (k0 >= k1) return;
-  const int nk = (k1 - k0) / BK;
+  const int nk = (k1 - k0) / KS;
   const int w = threadIdx.x >> 6;
   const bool wvalid = nt * WTraits<MODE>::COLS + w * 32 < a.Nout;
   switch ((nvalid + 31) >> 5) {
@@ -994,7 +1029,7 @@ __global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
 int pick_splits(int tiles, int K, int want_wgs, long rows, int ncols, size_t cap_elems) {
   // workgroups hold a whole CU each: stay within one round of them
   int s = std::max(1, std::min(kMaxSplits, want_wgs / std::max(tiles, 1)));
-  s = std::min(s, std::max(1, K / (PD * BK)));
+  s = std::min(s, std::max(1, K / kMinSplitK));
   while (s > 1 && (size_t)s * rows * ncols > cap_elems) --s;
   return s;
 }
