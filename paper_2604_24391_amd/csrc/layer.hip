@@ -405,6 +405,8 @@ __global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
 // 4 columns with float4 loads and applies the epilogue of its projection.
 struct RedArgs {
   int N, d, splits, ncols, qw, kw, S, cur_row0;
+  int hd, qpos0;                  // head dim; prompt position of current-frame token 0
+  const float2 *rope;             // [S][hd/2] (cos, sin)
   long rows;
   float eps;
   const int32_t *idx, *nrec;
@@ -478,18 +480,44 @@ __global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict_
   }
 }
 
+// One workgroup per (slot, 1024 columns): split-K sum + bias.  Queries are rotated
+// (rotate-half RoPE at the token's prompt position) in float32 before their single
+// rounding to bf16; a 1024-column block always holds whole heads, so the partner
+// dim of the rotation comes from LDS.  K and V rows go raw into the cache.
 __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
+  __shared__ float qs[1024];
   const long slot = blockIdx.x;
   const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
   if (j >= n_valid(r.nrec, b, r.N)) return;
-  const int c = blockIdx.y * 1024 + threadIdx.x * 4;
-  if (c >= r.ncols) return;
+  const int c0 = blockIdx.y * 1024;
+  const int c = c0 + threadIdx.x * 4;
   const int tok = tok_of(r.idx, slot, r.N);
-  const float4 v = sum_parts(r, slot, c);
-  const float vv[4] = {v.x, v.y, v.z, v.w};
+  float vv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (c < r.ncols) {
+    const float4 v = sum_parts(r, slot, c);
+    vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) vv[e] += bf2f(r.bias[c + e]);
+  }
+  if (c0 < r.qw) {   // uniform: the block's query columns are rotated
+    *reinterpret_cast<float4 *>(&qs[threadIdx.x * 4]) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+    __syncthreads();
+    if (c < r.qw) {
+      const int half = r.hd / 2;
+      const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int d = (c + e) % r.hd;                 // dim within the head
+        const int lc = threadIdx.x * 4 + e;           // column within the block
+        const float2 cs = rp[d % half];
+        vv[e] = d < half ? vv[e] * cs.x - qs[lc + half] * cs.y : vv[e] * cs.x + qs[lc - half] * cs.y;
+      }
+    }
+  }
+  if (c >= r.ncols) return;
   uint16_t o[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e] + bf2f(r.bias[c + e]));
+  for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e]);
   uint16_t *dst;
   if (c < r.qw)
     dst = r.q + slot * r.qw + c;
@@ -547,7 +575,7 @@ __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
 
 // ------------------------------------------------------------------------------- attention
 struct AttnArgs {
-  const uint16_t *q;          // [B*N][nh*HD] pre-RoPE
+  const uint16_t *q;          // [B*N][nh*HD], rotated at the query's position
   const uint16_t *kc, *vc;    // [B][S][nkv][HD]
   const float2 *rope;         // [S][HD/2] (cos, sin)
   const int32_t *idx, *nrec;
@@ -628,7 +656,7 @@ __device__ __forceinline__ int vq_word(int kg, int hd) {
 }
 
 // Attention of one 32-query tile of kv head g over key blocks [kb0, kb1) of the cache.
-// Wave w < G handles query head g*G + w.  The 32-key blocks are staged through two
+// Wave w < G handles query head g*G + w; the queries arrive rotated.  The 32-key blocks are staged through two
 // LDS buffers (keys rotated, values interleaved) with the raw loads of block kb + 2
 // in flight while block kb is multiplied, so the cache latency is paid once per
 // split rather than once per block.
@@ -644,7 +672,7 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   constexpr int QLD = HD + 8;   // padded LDS row of the rotated queries
   static_assert(TASKS % 64 == 0, "staging tasks fill whole waves");
   static_assert(TASKS == 8 * (HD / 4), "key and value tasks pair up");
-  __shared__ __bf16 Qs[G][32 * QLD];
+  __shared__ __attribute__((aligned(16))) __bf16 Qs[G][32 * QLD];
   __shared__ __attribute__((aligned(16))) __bf16 Ks[2][32 * HD];
   __shared__ __attribute__((aligned(16))) uint2 Vq[2][8 * HD];
   __shared__ int kpos[2][32];
@@ -672,37 +700,6 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   const long slot = (long)b * a.N + (qvalid ? j : j0);
   const int tok = tok_of(a.idx, slot, a.N);
   const int qpos = a.T + (a.W - 1) * a.N + tok;
-
-  // Q fragments (B operand of S^T = K Q^T): lane holds q[16 s + 8 hi + e]
-  float qf[NS][8];
-  {
-    const uint16_t *qr = a.q + slot * (long)(a.nh * HD) + h * HD;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const U16x8 v = *reinterpret_cast<const U16x8 *>(qr + 16 * s + 8 * hi);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[s][e] = bf2f(v.v[e]);
-    }
-    // rotate-half RoPE: dims d and d + HD/2 sit in steps s and s + NS/2 of this lane
-    const float2 *rp = a.rope + (long)qpos * (HD / 2);
-#pragma unroll
-    for (int s = 0; s < NS / 2; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float2 cs = rp[16 * s + 8 * hi + e];
-        const float x1 = qf[s][e], x2 = qf[s + NS / 2][e];
-        qf[s][e] = x1 * cs.x - x2 * cs.y;
-        qf[s + NS / 2][e] = x2 * cs.x + x1 * cs.y;
-      }
-  }
-  // each lane keeps its own rotated Q fragments in LDS (read back only by itself)
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    bf16x8 v;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = (__bf16)qf[s][e];
-    if (qwave) *reinterpret_cast<bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]) = v;
-  }
 
   f32x16 o[NHB];
 #pragma unroll
@@ -868,6 +865,29 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   KVRaw ra[TPT], rb[TPT];
   fetch(kb0, ra);
   fetch(kb0 + 1, rb);
+  // Q fragments (B operand of S^T = K Q^T; lane holds q[16 s + 8 hi + e]): the tile's
+  // rotated query rows (the G heads of kv group g are contiguous in a row) are staged
+  // through LDS with whole-line loads while the first key blocks are in flight
+  {
+    constexpr int QCH = G * HD / 8;                  // 16-B chunks of one query row
+    constexpr int QIT = (32 * QCH + NT - 1) / NT;    // chunks per thread
+    uint4 qv[QIT];
+#pragma unroll
+    for (int i = 0; i < QIT; ++i) {
+      const int c = min(t + i * NT, 32 * QCH - 1);
+      const int r = c / QCH, x = c - r * QCH;
+      const long sl = (long)b * a.N + (j0 + r < n ? j0 + r : j0);
+      qv[i] = *reinterpret_cast<const uint4 *>(a.q + sl * (a.nh * HD) + (long)g * G * HD + 8 * x);
+    }
+#pragma unroll
+    for (int i = 0; i < QIT; ++i) {
+      const int c = t + i * NT;
+      if (c < 32 * QCH) {
+        const int r = c / QCH, x = c - r * QCH;
+        *reinterpret_cast<uint4 *>(&Qs[(8 * x) / HD][r * QLD + (8 * x) % HD]) = qv[i];
+      }
+    }
+  }
   settle(ra);
   stage(ra, 0);
   lds_barrier();
@@ -889,8 +909,9 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   __builtin_amdgcn_s_waitcnt(0x3F70);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!qvalid || !qwave) return;
+  if (!qwave) return;
   if (a.splits == 1) {
+    if (!qvalid) return;
     uint16_t *orow = a.out + slot * (long)(a.nh * HD) + h * HD;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
@@ -899,45 +920,56 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
       for (int e = 0; e < 16; ++e)
         orow[hb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3)] = f2bf(o[hb][e] * inv);
   } else {
-    const long plane = (long)tiles / tiles_per_b * a.N;  // B*N
-    const long pr = ((long)sp * plane + slot) * a.nh + h;
-    float *orow = a.po + pr * HD;
+    // partials of this (split, tile, head) in accumulator order: 16-B group i of
+    // lane L at ((i * 64) + L) * 16 B, so each wave store is 1 KB contiguous; the
+    // running max and sum per query follow as [split][tile][head][32]
+    const long blk = ((long)sp * tiles + qt) * a.nh + h;
+    float4 *po = reinterpret_cast<float4 *>(a.po) + blk * (NHB * 4 * 64);
 #pragma unroll
     for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) orow[hb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3)] = o[hb][e];
+      for (int eg = 0; eg < 4; ++eg)
+        po[(hb * 4 + eg) * 64 + lane] =
+            make_float4(o[hb][4 * eg], o[hb][4 * eg + 1], o[hb][4 * eg + 2], o[hb][4 * eg + 3]);
     if (hi == 0) {
-      a.pm[pr] = m_run;
-      a.pl[pr] = l_tot;
+      a.pm[blk * 32 + l32] = m_run;
+      a.pl[blk * 32 + l32] = l_tot;
     }
   }
 }
 
-// Merges the split-KV partials of one query row: each split's sum is rescaled by
-// 2^(m_s - max m) and the total divided by the rescaled denominators.  blockIdx.y
-// picks 1024 consecutive outputs of the row, one float4 per thread, so all of a
-// thread's split loads are in flight together.
+// Merges the split-KV partials of one (32-query tile, head): each split's sum is
+// rescaled by 2^(m_s - max m) and the total divided by the rescaled denominators.
+// The partials are read in the attention kernel's accumulator order and the bf16
+// result is transposed through LDS so that every query row is written contiguously.
 constexpr int kMaxAttnSplits = 8;
-constexpr int kMaxAttnHeads = 128;
-__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int HD, int B) {
-  __shared__ float wt[kMaxAttnSplits][kMaxAttnHeads];
-  const long slot = blockIdx.x;
-  const int b = (int)(slot / a.N), j = (int)(slot - (long)b * a.N);
-  if (j >= n_valid(a.nrec, b, a.N)) return;
-  const long plane = (long)B * a.N;
-  const int nh = a.nh, splits = a.splits;
-  const int n4 = nh * HD / 4;
-  const int e = blockIdx.y * 256 + threadIdx.x;
-  const int h_lo = (blockIdx.y * 1024) / HD;
-  const int h_hi = min(nh, (blockIdx.y * 1024 + 1023) / HD + 1);
-  for (int h = h_lo + threadIdx.x; h < h_hi; h += blockDim.x) {
+template <int HD>
+__global__ __launch_bounds__(HD * 8) void k_attn_combine(AttnArgs a) {
+  constexpr int NG = HD / 8;                       // 16-B groups per lane
+  constexpr int NT = NG * 64;                      // one thread per 16-B group
+  __shared__ float wt[kMaxAttnSplits][32];
+  __shared__ __attribute__((aligned(16))) uint16_t ob[32][HD + 8];
+  const int nh = a.nh, tiles = a.tiles;
+  const int qt = blockIdx.x / nh, h = blockIdx.x - qt * nh;
+  const int tiles_per_b = (a.N + 31) / 32;
+  const int b = qt / tiles_per_b, j0 = (qt % tiles_per_b) * 32;
+  const int n = n_valid(a.nrec, b, a.N);
+  if (j0 >= n) return;
+  const int t = threadIdx.x, splits = a.splits;
+  // every split's group of this thread in flight at once
+  const float4 *po = reinterpret_cast<const float4 *>(a.po);
+  float4 p[kMaxAttnSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxAttnSplits; ++s)
+    p[s] = po[(((long)min(s, splits - 1) * tiles + qt) * nh + h) * NT + t];
+  if (t < 32) {
     float m[kMaxAttnSplits], l[kMaxAttnSplits];
     float mx = -INFINITY;
 #pragma unroll
     for (int s = 0; s < kMaxAttnSplits; ++s) {
-      const long pr = ((long)min(s, splits - 1) * plane + slot) * nh + h;
-      m[s] = s < splits ? a.pm[pr] : -INFINITY;
-      l[s] = s < splits ? a.pl[pr] : 0.f;
+      const long blk = ((long)min(s, splits - 1) * tiles + qt) * nh + h;
+      m[s] = s < splits ? a.pm[blk * 32 + t] : -INFINITY;
+      l[s] = s < splits ? a.pl[blk * 32 + t] : 0.f;
       mx = fmaxf(mx, m[s]);
     }
     const float mu = (mx == -INFINITY) ? 0.f : mx;
@@ -949,25 +981,30 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int HD, int B)
     }
     const float inv = tot > 0.f ? 1.f / tot : 0.f;
 #pragma unroll
-    for (int s = 0; s < kMaxAttnSplits; ++s) wt[s][h] = m[s] * inv;
+    for (int s = 0; s < kMaxAttnSplits; ++s) wt[s][t] = m[s] * inv;
   }
   __syncthreads();
-  if (e >= n4) return;
-  const int hh = (4 * e) / HD;
-  const float4 *po = reinterpret_cast<const float4 *>(a.po);
-  float4 p[kMaxAttnSplits];
+  {
+    const int grp = t >> 6, lane = t & 63, q = lane & 31, hi = lane >> 5;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int s = 0; s < kMaxAttnSplits; ++s)
-    p[s] = po[((long)min(s, splits - 1) * plane + slot) * n4 + e];
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-  for (int s = 0; s < kMaxAttnSplits; ++s) {
-    const float ws = wt[s][hh];   // zero for s >= splits
-    v.x += p[s].x * ws; v.y += p[s].y * ws; v.z += p[s].z * ws; v.w += p[s].w * ws;
+    for (int s = 0; s < kMaxAttnSplits; ++s) {
+      const float ws = wt[s][q];   // zero for s >= splits
+      v.x += p[s].x * ws; v.y += p[s].y * ws; v.z += p[s].z * ws; v.w += p[s].w * ws;
+    }
+    // group grp = hb * 4 + eg holds dims hb * 32 + eg * 8 + hi * 4 + 0..3
+    const int d = (grp >> 2) * 32 + (grp & 3) * 8 + hi * 4;
+    ushort4 r;
+    r.x = f2bf(v.x); r.y = f2bf(v.y); r.z = f2bf(v.z); r.w = f2bf(v.w);
+    *reinterpret_cast<ushort4 *>(&ob[q][d]) = r;
   }
-  ushort4 r;
-  r.x = f2bf(v.x); r.y = f2bf(v.y); r.z = f2bf(v.z); r.w = f2bf(v.w);
-  *reinterpret_cast<ushort4 *>(a.out + slot * (long)(nh * HD) + 4 * e) = r;
+  __syncthreads();
+  if (t < 32 * (HD / 8)) {
+    const int q = t / (HD / 8), x = t - q * (HD / 8);
+    if (j0 + q < n)
+      *reinterpret_cast<uint4 *>(a.out + ((long)b * a.N + j0 + q) * (long)(nh * HD) + h * HD + 8 * x) =
+          *reinterpret_cast<const uint4 *>(&ob[q][8 * x]);
+  }
 }
 
 // ------------------------------------------------------------------------------- rope table
@@ -1083,6 +1120,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   r.N = N; r.d = d; r.S = S; r.cur_row0 = cur_row0; r.rows = rows; r.eps = L.rms_eps;
   r.idx = idx; r.nrec = nrec; r.part = ctx->part; r.x = x_cur;
   r.qw = nh * hd; r.kw = nkv * hd;
+  r.hd = hd; r.qpos0 = kv.text_tokens + (kv.window - 1) * N; r.rope = ctx->rope;
   fc_status rc;
 
   // 1. gather + RMSNorm of the recomputed rows -> QKV partials; the reduction adds the
@@ -1121,12 +1159,13 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     const int nkb = (S + 31) / 32;
     int splits = std::max(1, std::min(kMaxAttnSplits, (2 * want) / (tiles * nkv)));
     splits = std::min(splits, std::max(1, nkb / 4));
-    while (splits > 1 && (size_t)splits * rows * nh * (hd + 2) > ctx->part_elems) --splits;
+    const size_t prow = (size_t)tiles * 32;           // query rows padded to whole tiles
+    while (splits > 1 && (size_t)splits * prow * nh * (hd + 2) > ctx->part_elems) --splits;
     a.kb_per_split = (nkb + splits - 1) / splits;
     a.splits = (nkb + a.kb_per_split - 1) / a.kb_per_split;
     a.po = ctx->part;
-    a.pm = ctx->part + (size_t)a.splits * rows * nh * hd;
-    a.pl = a.pm + (size_t)a.splits * rows * nh;
+    a.pm = ctx->part + (size_t)a.splits * prow * nh * hd;
+    a.pl = a.pm + (size_t)a.splits * prow * nh;
     const int G = nh / nkv;
     a.tiles = tiles;
     dim3 grid(tiles * nkv * a.splits);
@@ -1148,8 +1187,10 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     }
     if (a.splits > 1) {
       ProfScope ps(ctx, st, "fc_attn_combine");
-      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)rows, (nh * hd / 4 + 255) / 256), dim3(256),
-                         0, st, a, hd, B);
+      if (hd == 128)
+        hipLaunchKernelGGL(k_attn_combine<128>, dim3((unsigned)(tiles * nh)), dim3(1024), 0, st, a);
+      else
+        hipLaunchKernelGGL(k_attn_combine<64>, dim3((unsigned)(tiles * nh)), dim3(512), 0, st, a);
       FC_HIP_TRY(hipGetLastError());
     }
   }
