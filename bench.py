@@ -162,7 +162,7 @@ def main():
     torch.cuda.synchronize()
     el2 = time.perf_counter() - t2
     fc.fc_profile_enable(ctx, False)
-    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk", "fc_cache_update", "fc_gather_norm",
+    for name in ("fc_spectra", "fc_grid", "fc_patchsim", "fc_topk", "fc_cache_update", "fc_gather_norm",
                  "fc_gemm_qkv", "fc_red_qkv", "fc_attn", "fc_attn_combine", "fc_gemm_o",
                  "fc_red_o", "fc_gemm_gateup", "fc_gemm_down", "fc_red_down"):
         tot, cnt = fc.fc_profile_read(ctx, name)
@@ -255,7 +255,7 @@ def bench_select_batch(fc, ctx, torch):
     frame_bytes = 2 * B * 3 * H * W * 4
     out_bytes = B * 1024 * (4 + 8 + 1 + 4 + 1)
     kern = {}
-    for name in ("fc_spectra", "fc_grid", "fc_tokensim", "fc_topk"):
+    for name in ("fc_spectra", "fc_grid", "fc_patchsim", "fc_topk"):
         tot, cnt = fc.fc_profile_read(ctx, name)
         kern[name] = round(tot * 1e3 / cnt, 3)
     fc.fc_profile_read(ctx, None, reset=True)

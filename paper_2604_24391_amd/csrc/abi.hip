@@ -75,7 +75,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 }
 
 void free_ws(fc_ctx *c) {
-  void *ptrs[] = {c->amp, c->pmean, c->penergy, c->aligned, c->qbuf, c->attn,
+  void *ptrs[] = {c->amp, c->pmean, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq};
   for (void *p : ptrs)
     if (p) hipFree(p);
@@ -145,7 +145,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np, "amp")) != FC_OK ||
       (st = dev_alloc(&ctx->pmean, B * 2 * np, "pmean")) != FC_OK ||
       (st = dev_alloc(&ctx->penergy, B * np, "penergy")) != FC_OK ||
-      (st = dev_alloc(&ctx->aligned, B * c.max_tokens, "aligned")) != FC_OK ||
+      (st = dev_alloc(&ctx->pdot, B * 3 * np, "pdot")) != FC_OK ||
       (st = dev_alloc(&ctx->qbuf, rows * c.max_qkv, "q")) != FC_OK ||
       (st = dev_alloc(&ctx->attn, rows * c.max_qkv, "attn")) != FC_OK ||
       (st = dev_alloc(&ctx->h1, rows * c.max_d_model, "h1")) != FC_OK ||

@@ -46,7 +46,7 @@ struct fc_ctx {
   float *amp = nullptr;        // [B][2][kBins][Np] per-patch DFT amplitude (prev, cur)
   double *pmean = nullptr;     // [B][2][Np] per-patch mean luma
   double *penergy = nullptr;   // [B][Np] per-patch high-pass DCT energy (current frame)
-  uint8_t *aligned = nullptr;  // [B][N] alignment mask
+  double *pdot = nullptr;      // [B][3][Np] per-patch spectral products (dot, |cur|^2, |src|^2)
   // layer workspace
   uint16_t *qbuf = nullptr;    // [rows][qkv-wide] pre-RoPE queries, bf16
   uint16_t *attn = nullptr;    // [rows][n_heads*hd] attention output, bf16

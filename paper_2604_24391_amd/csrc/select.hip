@@ -12,13 +12,12 @@
 //              migration gate, spectral entropy and the reuse budget (Eqs. 3-6,
 //              4-4), phase correlation and its peak (Eq. 4-1), token energies and
 //              their mean / std / refresh threshold (Eq. 4-3).
-//   k_tokensim one thread per token: the alignment mask (Eq. 4-2) and the cosine
-//              of the token's amplitude spectrum with that of its aligned source
-//              token in the previous frame.
-//   k_topk     one workgroup per frame pair: refresh mask, candidate set,
-//              ascending-energy top-K with ties to the lower id (bitonic sort of
-//              (energy bits, id) pairs in LDS), reuse mask and ballot/prefix-sum
-//              compaction of the recomputed ids.
+//   k_patchsim per patch: the products of its amplitude spectrum with that of the
+//              same patch of its token's aligned source token (Eqs. 3-3, 4-2).
+//   k_topk     one workgroup per frame pair: alignment mask and token similarity,
+//              refresh mask, candidate set, ascending-energy top-K with ties to the
+//              lower id (radix select of the energy bits), reuse mask and
+//              ballot/prefix-sum compaction of the recomputed ids.
 //
 // The transforms are direct (no FFT library): a 14-point DFT folded on its
 // even/odd symmetry costs 84 real FMAs per row and 168 per complex column, and
@@ -85,29 +84,54 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
     return;
   }
 
-  __shared__ double sY[P][PW * P + 1];
-  __shared__ float2 sRow[PW][P][8];
-  __shared__ double sR[PW][3][P];
-  __shared__ double sHp[PW][P];
-  __shared__ double sRs[PW][P];
-  __shared__ double sCol[PW][3];
+  // LDS: the luma tile, then (after every row has been read into registers) the
+  // row-stage results in the same space, so that six workgroups fit on a CU
+  struct RowStage {
+    float2 row[PW][P][8];      // row DFTs, v = 0..7
+    double r3[PW][3][P];       // row DCTs, k < 3
+    double hp[PW][P];          // per-row high-pass energy of columns k >= 3
+    double rs[PW][P];          // per-row luma sums
+    double col[PW][3];         // column-DCT energies of k < 3, u >= 3
+  };
+  constexpr int kTileBytes = P * (PW * P + 1) * (int)sizeof(double);
+  constexpr int kLdsBytes = kTileBytes > (int)sizeof(RowStage) ? kTileBytes : (int)sizeof(RowStage);
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
+  double(*sY)[PW * P + 1] = reinterpret_cast<double(*)[PW * P + 1]>(lds);
+  RowStage &rsg = *reinterpret_cast<RowStage *>(lds);
+  float2(*sRow)[P][8] = rsg.row;
+  double(*sR)[3][P] = rsg.r3;
+  double(*sHp)[P] = rsg.hp;
+  double(*sRs)[P] = rsg.rs;
+  double(*sCol)[3] = rsg.col;
 
-  // ---- load 14 rows x (pw*14) px of R, G, B; luma in float64 (BT.601)
+  // ---- load 14 rows x (pw*14) px of R, G, B (all loads issued before any use); luma
+  //      in float64 (BT.601)
   const int cw = pw * P;
   const size_t plane = (size_t)H * W;
   const float *base = frame + (size_t)b * 3 * plane + (size_t)(pi * P) * W + j0 * P;
   if ((W & 3) == 0 && (cw & 3) == 0) {
     const int q4 = cw >> 2;
-    for (int e = t; e < P * q4; e += blockDim.x) {
-      int y = e / q4, q = e - y * q4;
+    constexpr int kIt = (P * PW * P / 4 + 255) / 256;   // float4 positions per thread
+    float4 r[kIt], g[kIt], bl[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int e = min(t + 256 * i, P * q4 - 1);
+      const int y = e / q4, q = e - y * q4;
       const float *rp = base + (size_t)y * W + 4 * q;
-      float4 r = *reinterpret_cast<const float4 *>(rp);
-      float4 g = *reinterpret_cast<const float4 *>(rp + plane);
-      float4 bl = *reinterpret_cast<const float4 *>(rp + 2 * plane);
-      sY[y][4 * q + 0] = 0.299 * (double)r.x + 0.587 * (double)g.x + 0.114 * (double)bl.x;
-      sY[y][4 * q + 1] = 0.299 * (double)r.y + 0.587 * (double)g.y + 0.114 * (double)bl.y;
-      sY[y][4 * q + 2] = 0.299 * (double)r.z + 0.587 * (double)g.z + 0.114 * (double)bl.z;
-      sY[y][4 * q + 3] = 0.299 * (double)r.w + 0.587 * (double)g.w + 0.114 * (double)bl.w;
+      r[i] = *reinterpret_cast<const float4 *>(rp);
+      g[i] = *reinterpret_cast<const float4 *>(rp + plane);
+      bl[i] = *reinterpret_cast<const float4 *>(rp + 2 * plane);
+    }
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int e = t + 256 * i;
+      if (e < P * q4) {
+        const int y = e / q4, q = e - y * q4;
+        sY[y][4 * q + 0] = 0.299 * (double)r[i].x + 0.587 * (double)g[i].x + 0.114 * (double)bl[i].x;
+        sY[y][4 * q + 1] = 0.299 * (double)r[i].y + 0.587 * (double)g[i].y + 0.114 * (double)bl[i].y;
+        sY[y][4 * q + 2] = 0.299 * (double)r[i].z + 0.587 * (double)g[i].z + 0.114 * (double)bl[i].z;
+        sY[y][4 * q + 3] = 0.299 * (double)r[i].w + 0.587 * (double)g[i].w + 0.114 * (double)bl[i].w;
+      }
     }
   } else {
     for (int e = t; e < P * cw; e += blockDim.x) {
@@ -119,11 +143,13 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   __syncthreads();
 
   // ---- row stage: one thread per (patch, row)
-  if (t < pw * P) {
-    const int p = t / P, y = t - p * P;
-    double v[P];
+  const bool rowt = t < pw * P;
+  const int p = rowt ? t / P : 0, y = rowt ? t - p * P : 0;
+  double v[P];
 #pragma unroll
-    for (int x = 0; x < P; ++x) v[x] = sY[y][p * P + x];
+  for (int x = 0; x < P; ++x) v[x] = rowt ? sY[y][p * P + x] : 0.0;
+  __syncthreads();   // the tile is dead from here on: its space holds the row stage
+  if (rowt) {
     double rs = 0.0;
 #pragma unroll
     for (int x = 0; x < P; ++x) rs += v[x];
@@ -174,12 +200,18 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   __syncthreads();
 
   // ---- column stage
-  if (t < pw * 8) {
+  // the row DFTs are read into registers first: their LDS then holds the amplitudes,
+  // which leave in [bin][patch] rows (one contiguous 16-patch segment per bin)
+  const bool colt = t < pw * 8;
+  float2 z[P];
+#pragma unroll
+  for (int y = 0; y < P; ++y) z[y] = colt ? sRow[t >> 3][y][t & 7] : make_float2(0.f, 0.f);
+  __syncthreads();
+  float(*sAmp)[PW] = reinterpret_cast<float(*)[PW]>(&rsg.row[0][0][0]);
+  static_assert(sizeof(float) * NB * PW <= sizeof(RowStage::row), "amplitudes fit in the row DFTs");
+  if (colt) {
     // DFT along y of column v (complex), all 14 u; y and 14 - y folded.
     const int p = t >> 3, k = t & 7;
-    float2 z[P];
-#pragma unroll
-    for (int y = 0; y < P; ++y) z[y] = sRow[p][y][k];
     float2 s[7], d[7];
 #pragma unroll
     for (int y = 1; y < 7; ++y) {
@@ -188,7 +220,6 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
     }
     const float2 be = make_float2(z[0].x + z[7].x, z[0].y + z[7].y);
     const float2 bo = make_float2(z[0].x - z[7].x, z[0].y - z[7].y);
-    const size_t obase = ((size_t)(b * 2 + f) * NB) * Np + pi * Gpw + j0 + p;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       float2 A = (u & 1) ? bo : be;
@@ -204,11 +235,11 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
       // X(u) = A - i B, X(14 - u) = A + i B
       const float r1 = A.x + Bv.y, i1 = A.y - Bv.x;
       int bin = bin_of(u, k);
-      if (bin >= 0) amp[obase + (size_t)bin * Np] = sqrtf(r1 * r1 + i1 * i1);
+      if (bin >= 0) sAmp[bin][p] = sqrtf(r1 * r1 + i1 * i1);
       if (u >= 1 && u <= 6) {
         const float r2 = A.x - Bv.y, i2 = A.y + Bv.x;
         bin = bin_of(P - u, k);
-        if (bin >= 0) amp[obase + (size_t)bin * Np] = sqrtf(r2 * r2 + i2 * i2);
+        if (bin >= 0) sAmp[bin][p] = sqrtf(r2 * r2 + i2 * i2);
       }
     }
   } else if (f == 1 && t >= 128 && t < 128 + pw * 3) {
@@ -235,6 +266,13 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   }
   __syncthreads();
 
+  {
+    const size_t obase = ((size_t)(b * 2 + f) * NB) * Np + pi * Gpw + j0;
+    for (int e = t; e < NB * pw; e += blockDim.x) {
+      const int bin = e / pw, p = e - bin * pw;
+      amp[obase + (size_t)bin * Np + p] = sAmp[bin][p];
+    }
+  }
   if (t < pw) {
     const int patch = pi * Gpw + j0 + t;
     double sum = 0.0;
@@ -252,57 +290,120 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
 }
 
 // ------------------------------------------------------------------------------- helpers
-template <typename T, typename Op>
-__device__ T block_reduce(T v, T *scratch, Op op) {
-  // Fixed-order tree over the workgroup (deterministic).
-  const int t = threadIdx.x;
-  scratch[t] = v;
+// Deterministic workgroup reductions of K values at once: a fixed shuffle tree inside
+// each wave, then wave 0 combines the per-wave partials with another fixed tree.  Every
+// thread gets the results.  scratch holds NW * K + K doubles.  MAXK: value k < MAXK
+// is a maximum, the others sums.
+template <int NW, int K, int MAXK>
+__device__ void block_reduce(double (&v)[K], double *scratch) {
+  static_assert(NW <= 64 && (NW & (NW - 1)) == 0, "power-of-two wave count");
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const double u = __shfl_xor(v[k], o);
+      v[k] = k < MAXK ? fmax(v[k], u) : v[k] + u;
+    }
   __syncthreads();
-  for (int s = blockDim.x >> 1; s > 0; s >>= 1) {
-    if (t < s) scratch[t] = op(scratch[t], scratch[t + s]);
-    __syncthreads();
+  if (lane == 0)
+#pragma unroll
+    for (int k = 0; k < K; ++k) scratch[w * K + k] = v[k];
+  __syncthreads();
+  if (w == 0) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      double x = lane < NW ? scratch[lane * K + k] : (k < MAXK ? -INFINITY : 0.0);
+#pragma unroll
+      for (int o = NW / 2; o > 0; o >>= 1) {
+        const double u = __shfl_xor(x, o);
+        x = k < MAXK ? fmax(x, u) : x + u;
+      }
+      if (lane == 0) scratch[NW * K + k] = x;
+    }
   }
-  T r = scratch[0];
   __syncthreads();
-  return r;
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = scratch[NW * K + k];
 }
 
-struct Add {
-  __device__ double operator()(double a, double b) const { return a + b; }
-};
-struct Max {
-  __device__ double operator()(double a, double b) const { return a > b ? a : b; }
-};
+// One direct DFT pass over an [Gh][Gw] complex grid in LDS, one output per thread:
+// along x (rows) out[y][v] = sum_x in[y][x] w^(v x), or along y (columns)
+// out[u][x] = sum_y in[y][x] w^(u y); w = tw[1], tw[k] = exp(-2 pi i k / G) (conj for
+// the inverse).  The twiddle index advances by v (or u) modulo G per term.
+template <bool ROWS, bool INV>
+__device__ __forceinline__ double2 dft_pass(const double2 *in, const double2 *tw, int e, int Gh,
+                                            int Gw) {
+  const int y = e / Gw, x0 = e - y * Gw;
+  const int G = ROWS ? Gw : Gh;
+  const int f = ROWS ? x0 : y;             // output frequency
+  double re = 0.0, im = 0.0;
+  int k = 0;
+#pragma unroll 4
+  for (int i = 0; i < G; ++i) {
+    const double2 a = ROWS ? in[y * Gw + i] : in[i * Gw + x0];
+    const double2 w = tw[k];
+    const double wy = INV ? -w.y : w.y;
+    re = fma(a.x, w.x, fma(-a.y, wy, re));
+    im = fma(a.x, wy, fma(a.y, w.x, im));
+    k += f;
+    if (k >= G) k -= G;
+  }
+  return make_double2(re, im);
+}
 
-// 2-D DFT of an [Gh][Gw] complex grid in LDS by two direct passes:
-// out[u][v] = sum_y sum_x in[y][x] w_h^(u y) w_w^(v x), w = exp(sign 2 pi i / G).
-__device__ void dft2_lds(const double2 *in, double2 *tmp, double2 *out, const double2 *twh,
-                         const double2 *tww, int Gh, int Gw) {
-  const int M = Gh * Gw;
-  for (int e = threadIdx.x; e < M; e += blockDim.x) {
-    const int y = e / Gw, v = e - y * Gw;
-    double re = 0.0, im = 0.0;
-    for (int x = 0; x < Gw; ++x) {
-      const double2 a = in[y * Gw + x];
-      const double2 w = tww[(v * x) % Gw];
-      re += a.x * w.x - a.y * w.y;
-      im += a.x * w.y + a.y * w.x;
-    }
-    tmp[e] = make_double2(re, im);
+// Radix-2 FFT of every row (AXIS 0, length Gw) or column (AXIS 1, length Gh) of an
+// [Gh][Gw] complex grid in LDS, in place in Y after a bit-reversed copy from X:
+// out[f] = sum_i in[i] w^(f i), w = exp(-2 pi i / G) (conjugate for INV).  The whole
+// workgroup takes part; tw[k] = exp(-2 pi i k / G) for the transformed axis.
+template <int AXIS, bool INV>
+__device__ void fft_axis(const double2 *X, double2 *Y, const double2 *tw, int Gh, int Gw) {
+  const int G = AXIS == 0 ? Gw : Gh, L = AXIS == 0 ? Gh : Gw;
+  const int lg = __ffs(G) - 1;
+  const int M = Gh * Gw, nt = blockDim.x;
+  auto at = [&](int line, int i) { return AXIS == 0 ? line * Gw + i : i * Gw + line; };
+  for (int e = threadIdx.x; e < M; e += nt) {
+    const int line = AXIS == 0 ? e / Gw : e % Gw, i = AXIS == 0 ? e % Gw : e / Gw;
+    const int r = lg ? (int)(__brev((unsigned)i) >> (32 - lg)) : 0;
+    Y[at(line, r)] = X[e];
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < M; e += blockDim.x) {
-    const int u = e / Gw, v = e - u * Gw;
-    double re = 0.0, im = 0.0;
-    for (int y = 0; y < Gh; ++y) {
-      const double2 a = tmp[y * Gw + v];
-      const double2 w = twh[(u * y) % Gh];
-      re += a.x * w.x - a.y * w.y;
-      im += a.x * w.y + a.y * w.x;
+  for (int sgl = 1; sgl <= lg; ++sgl) {
+    const int half = 1 << (sgl - 1);
+    for (int bt = threadIdx.x; bt < L * (G / 2); bt += nt) {
+      // rows: lanes along a row; columns: lanes across columns (consecutive addresses)
+      const int line = AXIS == 0 ? bt / (G / 2) : bt % L;
+      const int j = AXIS == 0 ? bt - line * (G / 2) : bt / L;
+      const int pos = j & (half - 1), i0 = ((j >> (sgl - 1)) << sgl) + pos, i1 = i0 + half;
+      double2 w = tw[pos << (lg - sgl)];
+      if (INV) w.y = -w.y;
+      const double2 a = Y[at(line, i0)], c = Y[at(line, i1)];
+      const double2 bw = make_double2(c.x * w.x - c.y * w.y, c.x * w.y + c.y * w.x);
+      Y[at(line, i0)] = make_double2(a.x + bw.x, a.y + bw.y);
+      Y[at(line, i1)] = make_double2(a.x - bw.x, a.y - bw.y);
     }
-    out[e] = make_double2(re, im);
+    __syncthreads();
   }
-  __syncthreads();
+}
+
+// 2-D transform of the grid in X (result in X, Z is scratch): FFTs for power-of-two
+// sides, direct passes otherwise.  Ends with a barrier; every thread may read X.
+template <bool INV>
+__device__ void dft2(double2 *X, double2 *Z, const double2 *twh, const double2 *tww, int Gh,
+                     int Gw) {
+  const int M = Gh * Gw, t = threadIdx.x;
+  if ((Gh & (Gh - 1)) == 0 && (Gw & (Gw - 1)) == 0) {
+    fft_axis<0, INV>(X, Z, tww, Gh, Gw);
+    fft_axis<1, INV>(Z, X, twh, Gh, Gw);
+  } else {
+    if (t < M) Z[t] = dft_pass<true, INV>(X, tww, t, Gh, Gw);
+    __syncthreads();
+    double2 r = make_double2(0.0, 0.0);
+    if (t < M) r = dft_pass<false, INV>(Z, twh, t, Gh, Gw);
+    __syncthreads();
+    if (t < M) X[t] = r;
+    __syncthreads();
+  }
 }
 
 struct GridParams {
@@ -312,158 +413,120 @@ struct GridParams {
 };
 
 // ------------------------------------------------------------------------------- k_grid
-// One workgroup (256 threads) per frame pair.  Dynamic LDS: 3 complex grids of
-// M = Gh * Gw <= 1024 doubles2 plus twiddles.
-__global__ __launch_bounds__(256) void k_grid(const double *__restrict__ pmean,
-                                              const double *__restrict__ penergy, GridParams g,
-                                              double *__restrict__ energy,
-                                              int32_t *__restrict__ shift,
-                                              double *__restrict__ scalars,
-                                              int32_t *__restrict__ counts) {
-  extern __shared__ double2 dyn[];
-  __shared__ double red[256];
-  __shared__ int redi[256];
+// One workgroup of 1024 threads per frame pair, one thread per grid point (M <= 1024).
+// LDS: three complex grids and the twiddles of both axes.
+constexpr int kGridThreads = 1024;
+__global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict__ pmean,
+                                                       const double *__restrict__ penergy,
+                                                       GridParams g, double *__restrict__ energy,
+                                                       int32_t *__restrict__ shift,
+                                                       double *__restrict__ scalars,
+                                                       int32_t *__restrict__ counts) {
+  constexpr int NW = kGridThreads / 64;
+  __shared__ double2 A[kMaxTokens], Bg[kMaxTokens], C[kMaxTokens];
+  __shared__ double2 twh[kMaxTokens], tww[kMaxTokens];
+  __shared__ double red[NW * 5 + 5];
+  __shared__ double bestv[NW];
+  __shared__ int besti[NW];
   const int b = blockIdx.x;
   const int t = threadIdx.x;
   const int m = g.m;
   const int Gh = g.Gph / m, Gw = g.Gpw / m, M = Gh * Gw;
   const int Np = g.Gph * g.Gpw;
-  double2 *X1 = dyn, *X2 = dyn + M, *X3 = dyn + 2 * M;
-  double2 *twh = dyn + 3 * M, *tww = twh + Gh;
+  const bool act = t < M;
+  const int I = t / Gw, J = t - I * Gw;
 
-  for (int k = t; k < Gh; k += blockDim.x) {
+  if (t < Gh) {
     double s, c;
-    sincospi(2.0 * k / Gh, &s, &c);
-    twh[k] = make_double2(c, -s);
+    sincospi(2.0 * t / Gh, &s, &c);
+    twh[t] = make_double2(c, -s);
   }
-  for (int k = t; k < Gw; k += blockDim.x) {
+  if (t < Gw) {
     double s, c;
-    sincospi(2.0 * k / Gw, &s, &c);
-    tww[k] = make_double2(c, -s);
+    sincospi(2.0 * t / Gw, &s, &c);
+    tww[t] = make_double2(c, -s);
   }
+  // token-grid mean luma of both frames (A: current, Bg: previous) and token energy
   const double inv_mm = 1.0 / (double)(m * m);
-
-  // token-grid mean luma maps and their spectra: F_t -> X3, F_{t-1} -> X1
-  for (int f = 1; f >= 0; --f) {
-    for (int e = t; e < M; e += blockDim.x) {
-      const int I = e / Gw, J = e - I * Gw;
-      double s = 0.0;
-      for (int a = 0; a < m; ++a)
-        for (int c = 0; c < m; ++c)
-          s += pmean[(size_t)(b * 2 + f) * Np + (m * I + a) * g.Gpw + m * J + c];
-      X1[e] = make_double2(s * inv_mm, 0.0);
-    }
-    __syncthreads();
-    dft2_lds(X1, X2, f ? X3 : X1, twh, tww, Gh, Gw);
-  }
-  double2 *Fc = X3, *Fp = X1;
-
-  // ---- Eq. 3-3 on the global spectra, Eq. 3-6 entropy of the current frame
-  double dot = 0.0, nc = 0.0, np_ = 0.0, mx = 0.0;
-  for (int e = t; e < M; e += blockDim.x) {
-    const double ac = sqrt(Fc[e].x * Fc[e].x + Fc[e].y * Fc[e].y);
-    const double ap = sqrt(Fp[e].x * Fp[e].x + Fp[e].y * Fp[e].y);
-    dot += ac * ap;
-    nc += ac * ac;
-    np_ += ap * ap;
-    // cross power X = F_{t-1} conj(F_t)
-    const double xr = Fp[e].x * Fc[e].x + Fp[e].y * Fc[e].y;
-    const double xi = Fp[e].y * Fc[e].x - Fp[e].x * Fc[e].y;
-    const double mag = sqrt(xr * xr + xi * xi);
-    X2[e] = make_double2(xr, xi);
-    mx = mag > mx ? mag : mx;
-  }
-  dot = block_reduce(dot, red, Add());
-  nc = block_reduce(nc, red, Add());
-  np_ = block_reduce(np_, red, Add());
-  mx = block_reduce(mx, red, Max());
-  double ent = 0.0;
-  for (int e = t; e < M; e += blockDim.x) {
-    const double p2 = Fc[e].x * Fc[e].x + Fc[e].y * Fc[e].y;
-    if (nc > 0.0) {
-      const double pr = p2 / nc;
-      if (pr > 0.0) ent -= pr * log(pr);
-    }
-  }
-  ent = block_reduce(ent, red, Add());
-
-  // ---- Eq. 4-1: normalised cross-power, inverse transform, first maximum
-  for (int e = t; e < M; e += blockDim.x) {
-    const double2 x = X2[e];
-    const double mag = sqrt(x.x * x.x + x.y * x.y);
-    X2[e] = (mx > 0.0 && mag > 1e-9 * mx) ? make_double2(x.x / mag, x.y / mag) : make_double2(0.0, 0.0);
-  }
-  __syncthreads();
-  // inverse: conjugate twiddles.  Row pass X2 -> X3 (F_t is no longer needed),
-  // column pass keeps only the real part.
-  for (int e = t; e < M; e += blockDim.x) {
-    const int y = e / Gw, v = e - y * Gw;
-    double re = 0.0, im = 0.0;
-    for (int x = 0; x < Gw; ++x) {
-      const double2 a = X2[y * Gw + x];
-      const double2 w = tww[(v * x) % Gw];  // conj: (w.x, -w.y)
-      re += a.x * w.x + a.y * w.y;
-      im += a.y * w.x - a.x * w.y;
-    }
-    X3[e] = make_double2(re, im);
-  }
-  __syncthreads();
-  double best = -INFINITY;
-  int besti = 0x7fffffff;
-  for (int e = t; e < M; e += blockDim.x) {
-    const int u = e / Gw, v = e - u * Gw;
-    double re = 0.0;
-    for (int y = 0; y < Gh; ++y) {
-      const double2 a = X3[y * Gw + v];
-      const double2 w = twh[(u * y) % Gh];
-      re += a.x * w.x + a.y * w.y;
-    }
-    re /= (double)M;
-    if (re > best) {  // strided visit in increasing index: keeps the first maximum
-      best = re;
-      besti = e;
-    }
-  }
-  red[t] = best;
-  redi[t] = besti;
-  __syncthreads();
-  for (int s = blockDim.x >> 1; s > 0; s >>= 1) {
-    if (t < s) {
-      const double v2 = red[t + s];
-      const int i2 = redi[t + s];
-      if (v2 > red[t] || (v2 == red[t] && i2 < redi[t])) {
-        red[t] = v2;
-        redi[t] = i2;
+  double gc = 0.0, gp = 0.0, et = 0.0;
+  if (act) {
+    for (int a2 = 0; a2 < m; ++a2)
+      for (int c2 = 0; c2 < m; ++c2) {
+        const int p = (m * I + a2) * g.Gpw + m * J + c2;
+        gc += pmean[(size_t)(b * 2 + 1) * Np + p];
+        gp += pmean[(size_t)(b * 2 + 0) * Np + p];
+        et += penergy[(size_t)b * Np + p];
       }
-    }
-    __syncthreads();
+    A[t] = make_double2(gc * inv_mm, 0.0);
+    Bg[t] = make_double2(gp * inv_mm, 0.0);
+    if (et < 1e-8 * (double)(m * m)) et = 0.0;
+    energy[(size_t)b * M + t] = et;
   }
-  const int kmax = redi[0];
   __syncthreads();
+  // forward 2-D transforms of both maps
+  __syncthreads();
+  dft2<false>(A, C, twh, tww, Gh, Gw);
+  dft2<false>(Bg, C, twh, tww, Gh, Gw);
+  double pc = 0.0, pp = 0.0, cp = 0.0, mag = 0.0;
+  if (act) {
+    const double2 Fc = A[t], Fp = Bg[t];
+    pc = Fc.x * Fc.x + Fc.y * Fc.y;                       // |F_t|^2
+    pp = Fp.x * Fp.x + Fp.y * Fp.y;                       // |F_{t-1}|^2
+    cp = sqrt(pc) * sqrt(pp);                             // |F_t| |F_{t-1}|
+    // cross power X = F_{t-1} conj(F_t), kept in Bg for the inverse transform
+    const double xr = Fp.x * Fc.x + Fp.y * Fc.y;
+    const double xi = Fp.y * Fc.x - Fp.x * Fc.y;
+    mag = sqrt(xr * xr + xi * xi);
+    Bg[t] = make_double2(xr, xi);
+  }
 
-  // ---- token energies (Eq. 3-5 summed over the m*m patches), Eq. 4-3 statistics
-  const double snap = 1e-8 * (double)(m * m);
-  double es = 0.0;
-  for (int e = t; e < M; e += blockDim.x) {
-    const int I = e / Gw, J = e - I * Gw;
-    double s = 0.0;
-    for (int a = 0; a < m; ++a)
-      for (int c = 0; c < m; ++c) s += penergy[(size_t)b * Np + (m * I + a) * g.Gpw + m * J + c];
-    if (s < snap) s = 0.0;
-    energy[(size_t)b * M + e] = s;
-    es += s;
+  // ---- Eq. 3-3 on the global spectra, Eq. 3-6 entropy of the current frame, the
+  //      largest cross-power magnitude, token-energy mean and spread (Eq. 4-3)
+  double r1[5] = {mag, cp, pc, pp, act ? et : 0.0};
+  block_reduce<NW, 5, 1>(r1, red);
+  const double mx = r1[0], dot = r1[1], nc = r1[2], np_ = r1[3];
+  const double mu = r1[4] / (double)M;
+  double r2[2] = {0.0, act ? (et - mu) * (et - mu) : 0.0};
+  if (act && nc > 0.0) {
+    const double pr = pc / nc;
+    if (pr > 0.0) r2[0] = -pr * log(pr);
   }
-  es = block_reduce(es, red, Add());
-  const double mu = es / (double)M;
-  __syncthreads();  // energy[] written by this block; re-read below by the same threads
-  double ev = 0.0;
-  for (int e = t; e < M; e += blockDim.x) {
-    const double d = energy[(size_t)b * M + e] - mu;
-    ev += d * d;
+  block_reduce<NW, 2, 0>(r2, red);
+  const double ent = r2[0], ev = r2[1];
+
+  // ---- Eq. 4-1: normalised cross-power, inverse transform (real part), first maximum
+  if (act) {
+    const double2 x = Bg[t];
+    Bg[t] = (mx > 0.0 && mag > 1e-9 * mx) ? make_double2(x.x / mag, x.y / mag) : make_double2(0.0, 0.0);
   }
-  ev = block_reduce(ev, red, Add());
+  dft2<true>(Bg, C, twh, tww, Gh, Gw);
+  const double re = act ? Bg[t].x / (double)M : -INFINITY;
+  // first maximum in row-major order: (value, index) max with the lower index on ties
+  double bv = re;
+  int bi = act ? t : 0x7fffffff;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double v2 = __shfl_xor(bv, o);
+    const int i2 = __shfl_xor(bi, o);
+    if (v2 > bv || (v2 == bv && i2 < bi)) {
+      bv = v2;
+      bi = i2;
+    }
+  }
+  if ((t & 63) == 0) {
+    bestv[t >> 6] = bv;
+    besti[t >> 6] = bi;
+  }
+  __syncthreads();
 
   if (t == 0) {
+    double v = bestv[0];
+    int kmax = besti[0];
+    for (int i = 1; i < NW; ++i)
+      if (bestv[i] > v || (bestv[i] == v && besti[i] < kmax)) {
+        v = bestv[i];
+        kmax = besti[i];
+      }
     const double sim = (nc > 0.0 && np_ > 0.0) ? dot / (sqrt(nc) * sqrt(np_)) : 0.0;
     double psi = 0.0;
     if (nc > 0.0) psi = ent;
@@ -488,127 +551,195 @@ __global__ __launch_bounds__(256) void k_grid(const double *__restrict__ pmean,
   }
 }
 
-// ------------------------------------------------------------------------------- k_tokensim
-__global__ __launch_bounds__(256) void k_tokensim(const float *__restrict__ amp, int Gph,
-                                                  int Gpw, int m, const int32_t *__restrict__ shift,
-                                                  float *__restrict__ sim,
-                                                  uint8_t *__restrict__ aligned) {
+// ------------------------------------------------------------------------------- k_patchsim
+// Per current-frame patch, the weighted dot product of its amplitude spectrum with that
+// of the patch at the same place in its token's aligned source token (previous frame),
+// and both squared norms; the token cosine (Eq. 3-3 on the concatenated spectra) is
+// their sum over the token's m*m patches.  Grid (ceil(Np / 64), B); the 4 waves of a
+// workgroup split the 100 bins for the same 64 patches, so loads of one bin are 64
+// consecutive patches.  Output pdot[(b * 3 + {dot, n_cur, n_src}) * Np + patch].
+constexpr int kSimBinsPerWave = NB / 4;
+__global__ __launch_bounds__(256) void k_patchsim(const float *__restrict__ amp, int Gph, int Gpw,
+                                                  int m, const int32_t *__restrict__ shift,
+                                                  double *__restrict__ pdot) {
+  __shared__ double part[3][4][64];
   const int b = blockIdx.y;
-  const int Gh = Gph / m, Gw = Gpw / m, M = Gh * Gw;
-  const int tok = blockIdx.x * blockDim.x + threadIdx.x;
-  if (tok >= M) return;
   const int Np = Gph * Gpw;
-  const int I = tok / Gw, J = tok - I * Gw;
-  const int si = I + shift[b * 2 + 0], sj = J + shift[b * 2 + 1];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int p = blockIdx.x * 64 + lane;
+  const int pc = min(p, Np - 1);
+  const int pi = pc / Gpw, pj = pc - pi * Gpw;
+  const int Gh = Gph / m, Gw = Gpw / m;
+  const int di = shift[b * 2 + 0], dj = shift[b * 2 + 1];
+  const int si = pi / m + di, sj = pj / m + dj;
   const bool al = si >= 0 && si < Gh && sj >= 0 && sj < Gw;
-  aligned[(size_t)b * M + tok] = al ? 1 : 0;
-  float out = 0.f;
-  if (al) {
-    const float *ac = amp + (size_t)(b * 2 + 1) * NB * Np;
-    const float *ap = amp + (size_t)(b * 2 + 0) * NB * Np;
-    double dot = 0.0, n1 = 0.0, n2 = 0.0;
-    for (int a = 0; a < m; ++a)
-      for (int c = 0; c < m; ++c) {
-        const int pc = (m * I + a) * Gpw + m * J + c;
-        const int ps = (m * si + a) * Gpw + m * sj + c;
-        for (int bin = 0; bin < NB; ++bin) {
-          const double w = bin_weight(bin);
-          const double x = ac[(size_t)bin * Np + pc];
-          const double y = ap[(size_t)bin * Np + ps];
-          dot = fma(w * x, y, dot);
-          n1 = fma(w * x, x, n1);
-          n2 = fma(w * y, y, n2);
-        }
-      }
-    if (n1 == 0.0 && n2 == 0.0)
-      out = 1.f;
-    else if (n1 == 0.0 || n2 == 0.0)
-      out = 0.f;
-    else
-      out = (float)(dot / (sqrt(n1) * sqrt(n2)));
+  const int ps = al ? (pi + m * di) * Gpw + pj + m * dj : pc;
+  const float *ac = amp + (size_t)(b * 2 + 1) * NB * Np;
+  const float *ap = amp + (size_t)(b * 2 + 0) * NB * Np;
+  float x[kSimBinsPerWave], y[kSimBinsPerWave];
+#pragma unroll
+  for (int i = 0; i < kSimBinsPerWave; ++i) {
+    const int bin = w * kSimBinsPerWave + i;
+    x[i] = ac[(size_t)bin * Np + pc];
+    y[i] = ap[(size_t)bin * Np + ps];
   }
-  sim[(size_t)b * M + tok] = out;
+  double dot = 0.0, n1 = 0.0, n2 = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSimBinsPerWave; ++i) {
+    const double wt = bin_weight(w * kSimBinsPerWave + i);
+    const double xv = x[i], yv = y[i];
+    dot = fma(wt * xv, yv, dot);
+    n1 = fma(wt * xv, xv, n1);
+    n2 = fma(wt * yv, yv, n2);
+  }
+  part[0][w][lane] = dot;
+  part[1][w][lane] = n1;
+  part[2][w][lane] = n2;
+  __syncthreads();
+  if (w == 0 && p < Np) {
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      double s = part[c][0][lane];
+#pragma unroll
+      for (int i = 1; i < 4; ++i) s += part[c][i][lane];
+      pdot[((size_t)b * 3 + c) * Np + p] = s;
+    }
+  }
 }
 
 // ------------------------------------------------------------------------------- k_topk
-__global__ __launch_bounds__(1024) void k_topk(const double *__restrict__ energy,
-                                               const float *__restrict__ sim,
-                                               const uint8_t *__restrict__ aligned,
-                                               const double *__restrict__ scalars,
-                                               int32_t *__restrict__ counts, double tau_sim, int M,
-                                               uint8_t *__restrict__ reuse,
-                                               int32_t *__restrict__ ridx,
-                                               int32_t *__restrict__ nrec,
-                                               uint8_t *__restrict__ flags) {
-  __shared__ unsigned long long key[kMaxTokens];
-  __shared__ int kid[kMaxTokens];
-  __shared__ uint8_t rm[kMaxTokens];
-  __shared__ int wsum[kMaxTokens / 64];
-  __shared__ int ccount[kMaxTokens / 64];
+// One workgroup per frame pair, one thread per token (M <= 1024):
+//   * alignment (Eq. 4-2) and the token's spectral cosine from its patches' products;
+//   * refresh mask (Eq. 4-3) and candidates (Alg. 1);
+//   * the K_final candidates of smallest (energy, id) by an exact radix select of the
+//     64-bit energy keys (non-negative doubles order like their bit patterns), eight
+//     8-bit digits from the top, each from an LDS histogram; ties on the energy go to
+//     the lower ids;
+//   * reuse mask and ballot/prefix compaction of the recomputed ids (ascending).
+__global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ energy,
+                                                     const double *__restrict__ pdot,
+                                                     const int32_t *__restrict__ shift,
+                                                     const double *__restrict__ scalars,
+                                                     int32_t *__restrict__ counts, double tau_sim,
+                                                     int Gph, int Gpw, int m,
+                                                     float *__restrict__ sim,
+                                                     uint8_t *__restrict__ reuse,
+                                                     int32_t *__restrict__ ridx,
+                                                     int32_t *__restrict__ nrec,
+                                                     uint8_t *__restrict__ flags) {
+  constexpr int NW = kMaxTokens / 64;
+  __shared__ int hist[256];
+  __shared__ int wcnt[NW];
+  __shared__ int sel_digit, sel_rem;
   const int b = blockIdx.x;
   const int t = threadIdx.x;
+  const int lane = t & 63, wv = t >> 6;
+  const int Gh = Gph / m, Gw = Gpw / m, M = Gh * Gw, Np = Gph * Gpw;
+  const bool act = t < M;
   const double thr = scalars[(size_t)b * FC_NSCALARS + FC_SCALAR_THR];
   const int k_reuse = counts[(size_t)b * FC_NCOUNTS + FC_COUNT_K_REUSE];
   const int flushed = counts[(size_t)b * FC_NCOUNTS + FC_COUNT_FLUSHED];
-  int npow = 1;
-  while (npow < M) npow <<= 1;
 
   bool cand = false;
-  if (t < M) {
+  unsigned long long key = ~0ull;
+  if (act) {
+    const int I = t / Gw, J = t - I * Gw;
+    const int si = I + shift[b * 2 + 0], sj = J + shift[b * 2 + 1];
+    const bool al = si >= 0 && si < Gh && sj >= 0 && sj < Gw;
+    float s = 0.f;
+    if (al) {
+      double dot = 0.0, n1 = 0.0, n2 = 0.0;
+      for (int a2 = 0; a2 < m; ++a2)
+        for (int c2 = 0; c2 < m; ++c2) {
+          const int p = (m * I + a2) * Gpw + m * J + c2;
+          dot += pdot[((size_t)b * 3 + 0) * Np + p];
+          n1 += pdot[((size_t)b * 3 + 1) * Np + p];
+          n2 += pdot[((size_t)b * 3 + 2) * Np + p];
+        }
+      if (n1 == 0.0 && n2 == 0.0)
+        s = 1.f;
+      else if (n1 == 0.0 || n2 == 0.0)
+        s = 0.f;
+      else
+        s = (float)(dot / (sqrt(n1) * sqrt(n2)));
+    }
+    sim[(size_t)b * M + t] = s;
     const double e = energy[(size_t)b * M + t];
     const bool fr = e > thr;
-    const bool al = aligned[(size_t)b * M + t] != 0;
-    cand = al && !fr && ((double)sim[(size_t)b * M + t] >= tau_sim);
+    cand = al && !fr && ((double)s >= tau_sim);
     if (flags) flags[(size_t)b * M + t] = (al ? FC_FLAG_ALIGNED : 0) | (fr ? FC_FLAG_FRESH : 0) |
                                           (cand ? FC_FLAG_CAND : 0);
-    key[t] = cand ? (unsigned long long)__double_as_longlong(e) : ~0ull;
-    kid[t] = t;
-    rm[t] = 0;
-  } else if (t < npow) {
-    key[t] = ~0ull;
-    kid[t] = 0x7fffffff;
+    if (cand) key = (unsigned long long)__double_as_longlong(e);
   }
   // candidate count
-  const unsigned long long bal = __ballot(cand);
-  const int lane = t & 63, wv = t >> 6;
-  if (lane == 0) ccount[wv] = __popcll(bal);
+  unsigned long long bal = __ballot(cand);
+  if (lane == 0) wcnt[wv] = __popcll(bal);
   __syncthreads();
   int k_cand = 0;
-  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) k_cand += ccount[i];
+#pragma unroll
+  for (int i = 0; i < NW; ++i) k_cand += wcnt[i];
+  const int k_final = flushed ? 0 : min(k_reuse, k_cand);
 
-  // bitonic sort ascending on (key, id)
-  for (int k = 2; k <= npow; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const int ixj = t ^ j;
-      if (t < npow && ixj > t) {
-        const bool up = (t & k) == 0;
-        const unsigned long long ka = key[t], kb = key[ixj];
-        const int ia = kid[t], ib = kid[ixj];
-        const bool gt = ka > kb || (ka == kb && ia > ib);
-        if (gt == up) {
-          key[t] = kb;
-          key[ixj] = ka;
-          kid[t] = ib;
-          kid[ixj] = ia;
+  // radix select of the k_final-th smallest key among the candidates
+  unsigned long long kth = 0, pmask = 0;
+  int rem = k_final;                      // how many to take at or below the prefix
+  if (k_final > 0) {
+    for (int pass = 0; pass < 8; ++pass) {
+      const int sh = 56 - 8 * pass;
+      __syncthreads();
+      if (t < 256) hist[t] = 0;
+      __syncthreads();
+      if (cand && (key & pmask) == kth) atomicAdd(&hist[(key >> sh) & 255], 1);
+      __syncthreads();
+      if (wv == 0) {
+        // lane holds bins 4 lane .. 4 lane + 3; inclusive scan over the wave
+        const int h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
+                  h3 = hist[4 * lane + 3];
+        const int tot = h0 + h1 + h2 + h3;
+        int inc = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int v = __shfl_up(inc, o);
+          if (lane >= o) inc += v;
+        }
+        const int exc = inc - tot;
+        if (exc < rem && inc >= rem) {     // exactly one lane holds the crossing
+          int c = exc, d = 4 * lane;
+          if (c + h0 >= rem) d = 4 * lane;
+          else if ((c += h0) + h1 >= rem) d = 4 * lane + 1;
+          else if ((c += h1) + h2 >= rem) d = 4 * lane + 2;
+          else { c += h2; d = 4 * lane + 3; }
+          sel_digit = d;
+          sel_rem = rem - c;
         }
       }
       __syncthreads();
+      kth |= (unsigned long long)sel_digit << sh;
+      pmask |= 255ull << sh;
+      rem = sel_rem;
     }
   }
-  const int k_final = flushed ? 0 : min(k_reuse, k_cand);
-  if (t < k_final) rm[kid[t]] = 1;
+  // reuse: every candidate below the k-th key, and the lowest-id `rem` at the key
+  const bool eq = cand && k_final > 0 && key == kth;
+  bal = __ballot(eq);
   __syncthreads();
+  if (lane == 0) wcnt[wv] = __popcll(bal);
+  __syncthreads();
+  int eq_before = __popcll(bal & ((1ull << lane) - 1ull));
+  for (int i = 0; i < wv; ++i) eq_before += wcnt[i];
+  const bool use = cand && k_final > 0 && (key < kth || (eq && eq_before < rem));
 
   // compaction of recomputed ids (ascending)
-  const bool keep = (t < M) && rm[t] == 0;
-  const unsigned long long kb = __ballot(keep);
-  const int before = __popcll(kb & ((1ull << lane) - 1ull));
-  if (lane == 0) wsum[wv] = __popcll(kb);
+  const bool keep = act && !use;
+  bal = __ballot(keep);
+  const int before = __popcll(bal & ((1ull << lane) - 1ull));
+  __syncthreads();
+  if (lane == 0) wcnt[wv] = __popcll(bal);
   __syncthreads();
   int off = 0;
-  for (int i = 0; i < wv; ++i) off += wsum[i];
-  if (t < M) {
-    reuse[(size_t)b * M + t] = rm[t];
+  for (int i = 0; i < wv; ++i) off += wcnt[i];
+  if (act) {
+    reuse[(size_t)b * M + t] = use ? 1 : 0;
     ridx[(size_t)b * M + t] = -1;
   }
   __syncthreads();
@@ -656,23 +787,22 @@ fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *p
     ProfScope ps(ctx, st, "fc_grid");
     GridParams g{Gph, Gpw, m, prm.tau_mig, prm.lambda_, prm.alpha_min, prm.alpha_max,
                  prm.alpha_fixed, prm.adaptive, prm.entropy_norm};
-    const size_t lds = (size_t)(3 * M + Gh + Gw) * sizeof(double2);
-    hipLaunchKernelGGL(k_grid, dim3(B), dim3(256), lds, st, ctx->pmean, ctx->penergy, g,
+    hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ctx->pmean, ctx->penergy, g,
                        out.energy, out.shift, out.scalars, out.counts);
     FC_HIP_TRY(hipGetLastError());
   }
   {
-    ProfScope ps(ctx, st, "fc_tokensim");
-    dim3 grid((M + 255) / 256, B);
-    hipLaunchKernelGGL(k_tokensim, grid, dim3(256), 0, st, ctx->amp, Gph, Gpw, m, out.shift,
-                       out.sim, ctx->aligned);
+    ProfScope ps(ctx, st, "fc_patchsim");
+    dim3 grid((Gph * Gpw + 63) / 64, B);
+    hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ctx->amp, Gph, Gpw, m, out.shift,
+                       ctx->pdot);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_topk");
-    hipLaunchKernelGGL(k_topk, dim3(B), dim3(1024), 0, st, out.energy, out.sim, ctx->aligned,
-                       out.scalars, out.counts, prm.tau_sim, M, out.reuse_mask,
-                       out.recompute_idx, out.n_recompute, out.flags);
+    hipLaunchKernelGGL(k_topk, dim3(B), dim3(kMaxTokens), 0, st, out.energy, ctx->pdot, out.shift,
+                       out.scalars, out.counts, prm.tau_sim, Gph, Gpw, m, out.sim,
+                       out.reuse_mask, out.recompute_idx, out.n_recompute, out.flags);
     FC_HIP_TRY(hipGetLastError());
   }
   return FC_OK;
