@@ -223,18 +223,25 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *r
     if (n >= a.Nout) n = 0;
     boff[i] = (uint32_t)((long)n * a.K + k0 + (((lane % KCH) ^ swz(r)) * 8));
   }
-  static_assert(MODE != G_GU || (BI % 2 == 0 && 4 * (BI / 2) * RPI == 128),
+  static_assert(NB == 1 || (BI % 2 == 0 && 4 * (BI / 2) * RPI == 128),
                 "the up rows start at an instruction boundary");
   const uint32_t lbase = lds_addr(lds);
+  // the loop's base pointers as values, so that no asm "memory" clobber can make the
+  // compiler reload them from the argument block
+  const uint16_t *const Abase = a.A, *const W0 = a.W0, *const W1 = a.W1;
 
+  // a wave whose rows of the last activation instruction are all past the valid ones
+  // skips that load (its LDS rows feed only outputs that are never stored)
+  const bool skip_last = (4 * (AI - 1) + w) * RPI >= nvalid;
   auto load_step = [&](int kt, int u) {
     const int kk = min(kt, nk - 1) * KS;
     const uint32_t st = lbase + u * G::BYTES;
 #pragma unroll
-    for (int i = 0; i < AI; ++i) dma16(a.A + aoff[i] + kk, st + (4 * i + w) * 1024);
+    for (int i = 0; i < AI; ++i)
+      if (i < AI - 1 || !skip_last) dma16(Abase + aoff[i] + kk, st + (4 * i + w) * 1024);
 #pragma unroll
     for (int i = 0; i < BI; ++i) {
-      const uint16_t *wm = (MODE == G_GU && i >= BI / 2) ? a.W1 : a.W0;
+      const uint16_t *wm = (NB == 2 && i >= BI / 2) ? W1 : W0;
       dma16(wm + boff[i] + kk, st + G::ALOAD * KS * 2 + (4 * i + w) * 1024);
     }
   };
@@ -255,6 +262,10 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *r
   constexpr int kAhead = kTwo ? PD : PD - 1;      // steps loaded ahead of the MFMAs
 #pragma unroll
   for (int u = 0; u < kAhead; ++u) load_step(u, u);
+  // with fewer steps than stages no refill ever reaches the last stage, yet a padding
+  // step reads it: fill it (with the clamped last step) so that it holds finite data.
+  // Every step of such a tile drains all loads, so the count stays consistent.
+  if (!kTwo && nk < PD) load_step(PD - 1, PD - 1);
 
   const int sw = swz(l32);              // row % 16 is l32 % 16 for every block
   const int nk_pad = (nk + PD - 1) / PD * PD;
@@ -269,12 +280,17 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *r
         // (a plain s_barrier: __syncthreads' release fence would drain every
         // in-flight load)
         const bool refill = kt + kAhead < nk + (kTwo ? 1 : 0);
-        constexpr int kLater = (kAhead - 1) * (AI + BI);
+        constexpr int kLater = (kAhead - 1) * (AI + BI);         // loads per step: AI + BI
+        constexpr int kLaterS = (kAhead - 1) * (AI - 1 + BI);    // ... or one fewer
         static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
-        if (kTwo || refill)
-          __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
-        else
+        if (kTwo || refill) {
+          if (skip_last)
+            __builtin_amdgcn_s_waitcnt(0x3F70 | (kLaterS & 0xF) | ((kLaterS >> 4) << 14));
+          else
+            __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
+        } else {
           __builtin_amdgcn_s_waitcnt(0x3F70);
+        }
         __builtin_amdgcn_s_barrier();
         if (!kTwo && refill) load_step(kt + PD - 1, (u + PD - 1) % PD);
         // fragment (row, s): 16-B chunk 2 s + hi of the row, at slot chunk ^ swz(row)
