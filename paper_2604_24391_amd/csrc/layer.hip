@@ -6,7 +6,7 @@
 //
 //   k_gather_norm  gathers the recomputed tokens' rows of x and writes the RMSNorm
 //               output bf16(x / rms(x) * g) slot by slot: the QKV operand.
-//   k_wgemm     weight-streaming bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16) over the
+//   k_wgemm     weight-streaming bf16 MFMA GEMM (v_mfma_f32_16x16x32_bf16) over the
 //               slots, C = A W^T with W row-major [out][in] like torch.nn.Linear;
 //               split-K float32 partials, or (SwiGLU) SiLU(g) * u in the epilogue.
 //   k_red_qkv   sums the QKV partials, adds the bias, stores q (pre-RoPE) and
@@ -58,23 +58,42 @@ __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
 }
 
 // ------------------------------------------------------------------------------- GEMM
-// Weight-streaming GEMM over the gathered rows, C[rows][cols] = A[rows][K] W[cols][K]^T.
-// With at most a few hundred recomputed rows the layer is bound by streaming the
-// weights from HBM, so each wave owns 32 output columns for every row of its
-// 256-row M tile and loads its weight rows straight into registers, PD K-steps
-// ahead; the (gathered) activation tile is shared by the workgroup's 4 waves
-// through LDS.  Split-K partial sums go to a float32 buffer that the k_red_*
-// kernels reduce; the SwiGLU mode (no split) applies the MLP RMSNorm and
-// SiLU(g) * u in its own epilogue.
+// Weight-streaming GEMM over the gathered rows, C[rows][cols] = A[rows][K] W[cols][K]^T
+// with W row-major [out][in] like torch.nn.Linear.  With a few hundred gathered rows
+// the layer is bound by streaming the weights, and every CU must also re-read the
+// whole activation tile for its columns, so the kernel is shaped by the per-CU load
+// path:
+//   * output columns are dealt in 16-column blocks evenly over all CUs (SwiGLU: the gate
+//     block and the up block of the same columns form a pair); the QKV, O and down
+//     projections add a K split so that the column groups times the splits cover the
+//     chip once, each split's activation K-slice staying in one XCD's L2;
+//   * a K step stages 64 K values of every operand row -- one full 128-B line per row,
+//     8 rows per 1 KB DMA instruction (half lines double the request count) -- into LDS
+//     by global_load_lds.  Rows are unpadded, their 16-B chunks XOR-swizzled by
+//     (row >> 1) & 7, which keeps the fragment reads free of bank conflicts;
+//   * waves 4-7 only issue those DMAs.  A DMA instruction holds its wave at issue, so a
+//     wave that also multiplied would leave its matrix core idle meanwhile;
+//   * waves 0-3 run v_mfma_f32_16x16x32_bf16 on the staged operands, wave w owning the
+//     16-row blocks w, w + 4, ...  Every wave runs the full block grid without a branch
+//     per MFMA: blocks past the valid rows and absent weight blocks multiply stale LDS
+//     into accumulators that are never stored;
+//   * PD stages rotate with one LDS barrier per K step: after barrier k the loaders
+//     refill the stage of step k - 1 with step k + PD - 1.
+// Split-K partial sums go to a float32 buffer [split][rows][cols] that the k_red_*
+// kernels reduce; the SwiGLU mode applies the MLP RMSNorm and SiLU(g) * u in its own
+// epilogue.
 enum { G_QKV = 0, G_O = 1, G_GU = 2, G_DOWN = 3 };
-constexpr int BK = kGemmBK;       // 64
-constexpr int MT = 256;           // rows per M tile: 8 MFMA blocks of 32
-constexpr int kMinSplitK = 4 * BK;  // shortest K range worth a split of its own
+constexpr int KS = kGemmBK;                 // 64 K values per step
+constexpr int RB = KS * 2;                  // bytes per staged operand row
+constexpr int MT = 256;                     // rows per M tile
+constexpr int kLdsBytes = 158 * 1024;       // operand stages
 
 struct WArgs {
   const uint16_t *A;              // bf16 activations, one row per slot
   const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
-  int K, Nout, kchunk, splits, N, m_tiles, n_tiles;
+  int K, Nout, N;                 // N = token slots per batch item
+  int nb, ncg, splits, ksteps;    // 16-col blocks, column groups, K splits, K steps per split
+  int tpb;                        // M tiles per batch item
   const int32_t *idx, *nrec;
   float *part;                    // [split][B*N][Nout]
   long rows;                      // B*N
@@ -85,41 +104,19 @@ struct WArgs {
 };
 
 // Workgroup id -> tile id so that each XCD (workgroups are dealt round-robin over
-// the 8 XCDs) works on a contiguous range of tiles; tiles are ordered N-fastest,
-// so the workgroups of one XCD share the same activation chunk in its L2.
+// the 8 XCDs) works on a contiguous range of tiles.
 __device__ __forceinline__ int xcd_tile(int w, int total) {
   const int per = total / 8;
   if (w >= per * 8) return w;
   return (w & 7) * per + (w >> 3);
 }
 
-// LDS fragment read issued as inline asm.  The activation stages are filled by LDS
-// DMA; the compiler cannot tell its stages apart and would otherwise drain every
-// in-flight global load before each read.  The caller orders the reads after the
-// stage is complete (manual vmcnt wait + barrier) and waits for them with lds_wait().
-__device__ __forceinline__ bf16x8 lds_read16(uint32_t addr) {
-  bf16x8 r;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
-  return r;
-}
-template <int N>
-__device__ __forceinline__ void lds_wait(bf16x8 (&f)[N]) {
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i]));
-}
-__device__ __forceinline__ uint32_t lds_addr(const void *p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-// Global loads of the pipelined K loop, also as inline asm so that the compiler's
-// wait insertion (which cannot follow this loop's load groups across the back edge)
-// never drains them; the loop waits for each K step's group with one vmcnt.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint4 gload16(const void *p) {
-  u32x4 r;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
-  return __builtin_bit_cast(uint4, r);
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
 // LDS DMA of 16 B per lane to lds + 16 * lane (lds must be wave-uniform).  M0 is
 // reserved to the compiler, so the asm restores it.
@@ -135,284 +132,226 @@ __device__ __forceinline__ void dma16(const void *gp, uint32_t lds) {
       : "v"(gp), "s"(l)
       : "memory");
 }
-__device__ __forceinline__ void anchor(uint4 &r) {
-  u32x4 v = __builtin_bit_cast(u32x4, r);
-  asm volatile("" : "+v"(v));
-  r = __builtin_bit_cast(uint4, v);
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds at most 63 outstanding loads");
+  __builtin_amdgcn_s_waitcnt(0x3F70 | (N & 0xF) | ((N >> 4) << 14));
 }
+// wait until at most n (wave-uniform, < 64) of this wave's loads are outstanding
+__device__ __forceinline__ void wait_vm_rt(int n) {
+  switch (n) {
+#define FC_W1(x) case x: wait_vm<x>(); break;
+#define FC_W8(x) FC_W1(x) FC_W1(x + 1) FC_W1(x + 2) FC_W1(x + 3) FC_W1(x + 4) FC_W1(x + 5) FC_W1(x + 6) FC_W1(x + 7)
+    FC_W8(0) FC_W8(8) FC_W8(16) FC_W8(24) FC_W8(32) FC_W8(40) FC_W8(48) FC_W8(56)
+#undef FC_W8
+#undef FC_W1
+    default: wait_vm<0>(); break;
+  }
+}
+// Workgroup barrier that orders LDS accesses only: global loads in flight stay in
+// flight across it (the full fence of __syncthreads would drain them).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+__device__ __forceinline__ int swz8(int row) { return (row >> 1) & 7; }
 
 template <int MODE>
 struct WTraits {
-  // SwiGLU: each wave computes the gate and the up block of the same 32 columns, so
-  // every activation fragment feeds two MFMAs and SiLU(g) * u needs no exchange
-  static constexpr int NB = MODE == G_GU ? 2 : 1;     // weight blocks per wave
-  static constexpr int COLS = 128;                    // output columns per workgroup
-  static constexpr int BROWS = 128 * NB;              // weight rows staged per K step
+  // 16-column blocks a column group may hold: 1184 SwiGLU pairs over 256 groups is
+  // 4.625; the Qwen QKV (288 blocks) and O/down (224 blocks) split into 32 groups of 9
+  // and 7
+  static constexpr int NBLK = MODE == G_GU ? 5 : (MODE == G_QKV ? 9 : 7);
+  static constexpr int NBW = (MODE == G_GU ? 2 : 1) * NBLK;   // staged weight blocks
 };
-
-constexpr int kLdsBytes = 152 * 1024;                 // activation + weight stages
-
-// K step of the weight-streaming GEMM: 64, so that every operand row of a stage is
-// one full 128-B line (the vector memory path is bound by requests, not bytes).
-constexpr int KS = 64;
-constexpr int KCH = KS / 8;            // 16-B chunks per LDS row
-constexpr int RPI = 1024 / (KS * 2);   // rows one wave's DMA instruction fills
-
-// Stage geometry for a tile of MBC 32-row blocks: the activation rows are loaded in
-// groups of 64 (one per wave and instruction round), the weight rows of the
-// workgroup follow; PD stages fit in LDS.
-template <int MODE, int MBC>
+template <int MODE, int MBW>
 struct WStage {
-  static constexpr int AROWS = MBC * 32;                 // rows the MFMAs read
-  static constexpr int ALOAD = (AROWS + 4 * RPI - 1) / (4 * RPI) * (4 * RPI);  // rows staged
-  static constexpr int BROWS = WTraits<MODE>::BROWS;
-  static constexpr int BYTES = (ALOAD + BROWS) * KS * 2;
-  static constexpr int PD = (kLdsBytes / BYTES) < 8 ? (kLdsBytes / BYTES) : 8;
-  static_assert(PD >= 2, "at least two stages");
+  static constexpr int ABLK = 4 * MBW;                        // 16-row activation blocks
+  static constexpr int AROWS = ABLK * 16;
+  static constexpr int BYTES = (AROWS + WTraits<MODE>::NBW * 16) * RB;
+  static constexpr int PD = (kLdsBytes / BYTES) > 6 ? 6 : (kLdsBytes / BYTES);
+  static constexpr int MAXI = (ABLK * 2 + WTraits<MODE>::NBW * 2 + 3) / 4;  // DMAs per loader
+  static_assert(PD >= 3, "at least three stages");
+  static_assert((PD - 2) * MAXI < 64, "vmcnt holds at most 63 outstanding loads");
 };
 
-// XOR swizzle of the 16-B chunks of an LDS row: the 16 lanes served together by a
-// b128 read (16 consecutive rows at one chunk) land on distinct banks of the 256-B
-// bank window.
-__device__ __forceinline__ int swz(int row) {
-  return KCH == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
-}
+// One (M tile, column group, K split) with MBW 16-row blocks per MFMA wave.
+template <int MODE, int MBW>
+__device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, const float *rowinv,
+                                           int b, int row0, int nvalid, int cg, int sp, int nk) {
+  using T = WTraits<MODE>;
+  using S = WStage<MODE, MBW>;
+  constexpr int PD = S::PD, NBLK = T::NBLK, NBW = T::NBW, MAXI = S::MAXI;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int cb0 = (int)((long)cg * a.nb / a.ncg);
+  const int nblk = (int)((long)(cg + 1) * a.nb / a.ncg) - cb0;
+  const int nbm = (nvalid + 15) >> 4;
+  const long k0 = (long)sp * a.ksteps * KS;
+  const long slot0 = (long)b * a.N + row0;
 
-// The K loop for a tile whose valid rows fill MBC 32-row blocks.
-//   * every K step stages the activation rows and the workgroup's weight rows in LDS
-//     through global_load_lds, 16 B per lane, whole rows per instruction, with the
-//     chunks of each row XOR-swizzled so the MFMA fragment reads do not conflict;
-//   * PD stages rotate: at step k one vmcnt wait and one barrier hand stage k to the
-//     MFMAs and free the stage of step k - 1, which is refilled at once with step
-//     k + PD - 1, so PD - 1 stages are in flight while one is multiplied;
-//   * rows past the valid ones read clamped in-bounds addresses; the last PD - 1
-//     steps issue no loads and drain instead, and the steps that pad the count to a
-//     multiple of PD multiply zeros.
-// The loads and LDS reads are inline asm: the compiler cannot follow this loop's
-// load groups across the back edge and would otherwise drain them every step.
-template <int MODE, int MBC>
-__device__ __forceinline__ void wgemm_tile(const WArgs &a, __bf16 *lds, float *rowinv, int b,
-                                           int row0, int nvalid, int nt, int k0, int nk,
-                                           bool wvalid, int sp) {
-  using G = WStage<MODE, MBC>;
-  constexpr int NB = WTraits<MODE>::NB;
-  constexpr int PD = G::PD;
-  constexpr int AI = G::ALOAD / (4 * RPI);   // activation DMA instructions per wave per step
-  constexpr int BI = G::BROWS / (4 * RPI);   // weight DMA instructions per wave per step
-  const int t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6;
-  const int l32 = lane & 31, hi = lane >> 5;
-  const int cb = nt * WTraits<MODE>::COLS + w * 32;   // this wave's output columns
-
-  // per-lane source offsets (elements) of the rows this lane stages
-  uint32_t aoff[AI];
+  if (w >= 4) {
+    // ----------------------------------------------------------------- loader waves
+    // Instruction j of a step stages 8 rows: j < nA the activation rows 8j.., then
+    // two per present weight block.  Loader q issues j = q, q + 4, ...
+    const int q = w - 4;
+    const int nA = nbm * 2;
+    const int npres = MODE == G_GU ? 2 * nblk : nblk;
+    const int ntot = nA + npres * 2;
+    const int rsub = lane >> 3, ch = lane & 7;
+    const uint16_t *gp[MAXI];
+    uint32_t lo[MAXI];
+    int L = 0;
 #pragma unroll
-  for (int i = 0; i < AI; ++i) {
-    const int r = (4 * i + w) * RPI + lane / KCH;
-    const long slot = (long)b * a.N + row0 + (r < nvalid ? r : 0);
-    aoff[i] = (uint32_t)(slot * a.K + k0 + (((lane % KCH) ^ swz(r)) * 8));
-  }
-  // weight rows: 32-bit element offsets; in SwiGLU mode the second half of the
-  // instructions stage the up rows (rows 128.. of the stage), so the matrix is
-  // known per unrolled instruction
-  uint32_t boff[BI];
-#pragma unroll
-  for (int i = 0; i < BI; ++i) {
-    const int r = (4 * i + w) * RPI + lane / KCH;       // staged weight row
-    int n = nt * WTraits<MODE>::COLS + (r & 127);        // output column of that row
-    if (n >= a.Nout) n = 0;
-    boff[i] = (uint32_t)((long)n * a.K + k0 + (((lane % KCH) ^ swz(r)) * 8));
-  }
-  static_assert(NB == 1 || (BI % 2 == 0 && 4 * (BI / 2) * RPI == 128),
-                "the up rows start at an instruction boundary");
-  const uint32_t lbase = lds_addr(lds);
-  // the loop's base pointers as values, so that no asm "memory" clobber can make the
-  // compiler reload them from the argument block
-  const uint16_t *const Abase = a.A, *const W0 = a.W0, *const W1 = a.W1;
-
-  // a wave whose rows of the last activation instruction are all past the valid ones
-  // skips that load (its LDS rows feed only outputs that are never stored)
-  const bool skip_last = (4 * (AI - 1) + w) * RPI >= nvalid;
-  auto load_step = [&](int kt, int u) {
-    const int kk = min(kt, nk - 1) * KS;
-    const uint32_t st = lbase + u * G::BYTES;
-#pragma unroll
-    for (int i = 0; i < AI; ++i)
-      if (i < AI - 1 || !skip_last) dma16(Abase + aoff[i] + kk, st + (4 * i + w) * 1024);
-#pragma unroll
-    for (int i = 0; i < BI; ++i) {
-      const uint16_t *wm = (NB == 2 && i >= BI / 2) ? W1 : W0;
-      dma16(wm + boff[i] + kk, st + G::ALOAD * KS * 2 + (4 * i + w) * 1024);
-    }
-  };
-
-  f32x16 acc[NB][MBC];
-#pragma unroll
-  for (int j = 0; j < NB; ++j)
-#pragma unroll
-    for (int mb = 0; mb < MBC; ++mb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[j][mb][e] = 0.f;
-
-  // With three or more stages the refill of step k + PD - 1 goes into the stage of
-  // step k - 1 right after the barrier of step k.  With two stages that would leave
-  // nothing in flight at the wait, so the stage just multiplied is refilled (after a
-  // second barrier) with step k + 2 instead.
-  constexpr bool kTwo = PD == 2;
-  constexpr int kAhead = kTwo ? PD : PD - 1;      // steps loaded ahead of the MFMAs
-#pragma unroll
-  for (int u = 0; u < kAhead; ++u) load_step(u, u);
-  // with fewer steps than stages no refill ever reaches the last stage, yet a padding
-  // step reads it: fill it (with the clamped last step) so that it holds finite data.
-  // Every step of such a tile drains all loads, so the count stays consistent.
-  if (!kTwo && nk < PD) load_step(PD - 1, PD - 1);
-
-  const int sw = swz(l32);              // row % 16 is l32 % 16 for every block
-  const int nk_pad = (nk + PD - 1) / PD * PD;
-  for (int kt0 = 0; kt0 < nk_pad; kt0 += PD) {
-#pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int kt = kt0 + u;
-      const bool live = kt < nk;         // padding steps multiply zeros
-      {
-        // this thread's share of step kt is complete once only the later steps'
-        // loads may be outstanding; the barrier then makes the whole stage visible
-        // (a plain s_barrier: __syncthreads' release fence would drain every
-        // in-flight load)
-        const bool refill = kt + kAhead < nk + (kTwo ? 1 : 0);
-        constexpr int kLater = (kAhead - 1) * (AI + BI);         // loads per step: AI + BI
-        constexpr int kLaterS = (kAhead - 1) * (AI - 1 + BI);    // ... or one fewer
-        static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
-        if (kTwo || refill) {
-          if (skip_last)
-            __builtin_amdgcn_s_waitcnt(0x3F70 | (kLaterS & 0xF) | ((kLaterS >> 4) << 14));
-          else
-            __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
+    for (int i = 0; i < MAXI; ++i) {
+      const int j = min(q + 4 * i, ntot - 1);
+      L += (q + 4 * i < ntot);
+      if (j < nA) {
+        const int r = j * 8 + rsub;                            // tile row
+        const int rr = r < nvalid ? r : nvalid - 1;            // clamp: never stored
+        gp[i] = a.A + (slot0 + rr) * a.K + k0 + ((ch ^ swz8(r)) * 8);
+        lo[i] = j * 1024;
+      } else {
+        const int jw = j - nA, pb = jw >> 1;                   // present weight block pb
+        int blk, col0;
+        const uint16_t *M = a.W0;
+        if (MODE == G_GU && pb >= nblk) {
+          blk = NBLK + pb - nblk;
+          col0 = (cb0 + pb - nblk) * 16;
+          M = a.W1;
         } else {
-          __builtin_amdgcn_s_waitcnt(0x3F70);
+          blk = pb;
+          col0 = (cb0 + pb) * 16;
         }
-        __builtin_amdgcn_s_barrier();
-        if (!kTwo && refill) load_step(kt + PD - 1, (u + PD - 1) % PD);
-        // fragment (row, s): 16-B chunk 2 s + hi of the row, at slot chunk ^ swz(row)
-        const uint32_t st = lbase + u * G::BYTES;
-        const uint32_t arow = st + l32 * (KS * 2);
-        uint32_t brow[NB];
+        const int r = blk * 16 + (jw & 1) * 8 + rsub;         // row of the weight region
+        gp[i] = M + (long)(col0 + (r & 15)) * a.K + k0 + ((ch ^ swz8(r)) * 8);
+        lo[i] = S::AROWS * RB + (blk * 2 + (jw & 1)) * 1024;
+      }
+    }
+    const uint32_t lbase = lds_addr(lds);
+    auto issue = [&](int kt, int stg) {
+      const int kk = kt * KS;
+      const uint32_t st = lbase + stg * S::BYTES;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) brow[j] = st + (G::ALOAD + j * 128 + w * 32 + l32) * (KS * 2);
-        bf16x8 af[MBC], an[MBC], bf[NB], bn[NB];
+      for (int i = 0; i < MAXI; ++i)
+        if (i < L) dma16(gp[i] + kk, st + lo[i]);
+    };
+    for (int u = 0; u < PD - 1 && u < nk; ++u) issue(u, u);
+    for (int k = 0; k < nk; ++k) {
+      wait_vm_rt(min(nk - 1 - k, PD - 2) * L);                 // this wave's share of step k
+      lds_barrier();                                           // barrier k: step k staged
+      const int nxt = k + PD - 1;
+      if (nxt < nk) issue(nxt, nxt % PD);                      // the stage of step k - 1
+    }
+    return;
+  }
+
+  // -------------------------------------------------------------------- MFMA waves
+  const int l16 = lane & 15, g = lane >> 4;
+  f32x4 acc[MBW][NBW];
 #pragma unroll
-        for (int mb = 0; mb < MBC; ++mb) af[mb] = lds_read16(arow + mb * 32 * (KS * 2) + ((hi ^ sw) << 4));
+  for (int i = 0; i < MBW; ++i)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) bf[j] = lds_read16(brow[j] + ((hi ^ sw) << 4));
-        lds_wait(af);
-        lds_wait(bf);
+    for (int j = 0; j < NBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // fragment (row l16, K sub-step s): 16-B chunk 4 s + g of the row, at its swizzled slot;
+  // A and B use the same K order, so the products are those of the plain K order
+  const uint32_t rowoff = l16 * RB;
+  const int sw = swz8(l16);
+  for (int k = 0; k < nk; ++k) {
+    lds_barrier();                                             // barrier k: step k staged
+    const unsigned char *st = lds + (k % PD) * S::BYTES;
+    bf16x8 fa[2][MBW], fb[2][NBW];
 #pragma unroll
-        for (int s = 0; s < KS / 16; ++s) {
-          if (s + 1 < KS / 16) {
-            const int slot = (2 * (s + 1) + hi) ^ sw;
+    for (int s = 0; s < 2; ++s) {
+      const uint32_t slot = (uint32_t)(((4 * s + g) ^ sw) << 4);
 #pragma unroll
-            for (int mb = 0; mb < MBC; ++mb) an[mb] = lds_read16(arow + mb * 32 * (KS * 2) + (slot << 4));
+      for (int i = 0; i < MBW; ++i)
+        fa[s][i] = *reinterpret_cast<const bf16x8 *>(st + (w + 4 * i) * 16 * RB + rowoff + slot);
 #pragma unroll
-            for (int j = 0; j < NB; ++j) bn[j] = lds_read16(brow[j] + (slot << 4));
-          }
+      for (int j = 0; j < NBW; ++j)
+        fb[s][j] = *reinterpret_cast<const bf16x8 *>(st + (S::AROWS + j * 16) * RB + rowoff + slot);
+    }
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
-            const bf16x8 bv = live ? bf[j] : bf16x8{};
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int mb = 0; mb < MBC; ++mb)
-              acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bv, acc[j][mb], 0, 0, 0);
-          }
-          if (s + 1 < KS / 16) {
-            lds_wait(an);
-            lds_wait(bn);
+      for (int j = 0; j < NBW; ++j)
 #pragma unroll
-            for (int mb = 0; mb < MBC; ++mb) af[mb] = an[mb];
+        for (int i = 0; i < MBW; ++i)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+  }
+
+  // lane holds column l16 and rows 4 g + e of each 16-row block
+  if (MODE == G_GU) {
 #pragma unroll
-            for (int j = 0; j < NB; ++j) bf[j] = bn[j];
+    for (int i = 0; i < MBW; ++i) {
+      if (w + 4 * i >= nbm) continue;
+#pragma unroll
+      for (int j = 0; j < NBLK; ++j) {
+        if (j >= nblk) continue;
+        const int col = (cb0 + j) * 16 + l16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = (w + 4 * i) * 16 + 4 * g + e;
+          if (r < nvalid) {
+            const float sc = rowinv[r];
+            const float gv = acc[i][j][e] * sc;
+            const float uv = acc[i][NBLK + j][e] * sc;
+            a.act[(slot0 + r) * a.Nout + col] = f2bf(gv / (1.f + __expf(-gv)) * uv);
           }
         }
-        if (kTwo) {
-          // every wave is done with this stage before any thread refills it; the
-          // clamped loads past the end keep the per-step load count constant
-          __builtin_amdgcn_s_barrier();
-          load_step(kt + PD, u);
+      }
+    }
+  } else {
+    float *P = a.part + ((long)sp * a.rows + slot0) * a.Nout;
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) {
+      if (w + 4 * i >= nbm) continue;
+#pragma unroll
+      for (int j = 0; j < NBLK; ++j) {
+        if (j >= nblk) continue;
+        const int col = (cb0 + j) * 16 + l16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = (w + 4 * i) * 16 + 4 * g + e;
+          if (r < nvalid) P[(long)r * a.Nout + col] = acc[i][j][e];
         }
       }
     }
   }
-  // drain the clamped prefetches of the last steps before LDS is reused
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
+}
 
-  // lane holds column l32 and rows (e/4)*8 + hi*4 + e%4 of each 32-row block
-  const long slot0 = (long)b * a.N + row0;
+template <int MODE>
+__global__ __launch_bounds__(512) void k_wgemm(WArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
+  __shared__ float rowinv[MT];
+  // split fastest: with 8 splits every split's workgroups share one XCD and its L2
+  const int bid = blockIdx.x;
+  const int sp = bid % a.splits;
+  const int rest = bid / a.splits;
+  const int cg = rest % a.ncg;
+  const int mt = rest / a.ncg;
+  const int b = mt / a.tpb;
+  const int row0 = (mt % a.tpb) * MT;
+  const int nvalid = min(MT, n_valid(a.nrec, b, a.N) - row0);
+  const int nk = min(a.ksteps, a.K / KS - sp * a.ksteps);
+  if (nvalid <= 0 || nk <= 0) return;
   if (MODE == G_GU) {
     // 1/rms of each row from the per-chunk sums of squares of h1
-    for (int r = t; r < G::AROWS; r += 256) {
+    const long slot0 = (long)b * a.N + row0;
+    for (int r = threadIdx.x; r < MT; r += blockDim.x) {
       float v = 0.f;
       if (r < nvalid)
         for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
       rowinv[r] = 1.f / sqrtf(v / (float)a.K + a.eps);
     }
     __syncthreads();
-    if (wvalid) {
-      const int col = cb + l32;
-#pragma unroll
-      for (int mb = 0; mb < MBC; ++mb) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-          if (r < nvalid) {
-            const float sc = rowinv[r];
-            const float gv = acc[0][mb][e] * sc;
-            const float uv = acc[NB - 1][mb][e] * sc;
-            a.act[(slot0 + r) * a.Nout + col] = f2bf(gv / (1.f + __expf(-gv)) * uv);
-          }
-        }
-      }
-    }
-  } else if (wvalid) {
-    float *Pp = a.part + ((long)sp * a.rows + slot0) * a.Nout + cb + l32;
-#pragma unroll
-    for (int mb = 0; mb < MBC; ++mb) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-        if (r < nvalid) Pp[(long)r * a.Nout] = acc[0][mb][e];
-      }
-    }
   }
-}
-
-template <int MODE>
-__global__ __launch_bounds__(256) void k_wgemm(WArgs a) {
-  __shared__ __attribute__((aligned(16))) __bf16 lds[kLdsBytes / 2];
-  __shared__ float rowinv[MT];
-  const int total = a.m_tiles * a.n_tiles * a.splits;
-  const int tile = xcd_tile(blockIdx.x, total);
-  const int nt = tile % a.n_tiles;
-  const int mt = (tile / a.n_tiles) % a.m_tiles;
-  const int sp = tile / (a.n_tiles * a.m_tiles);
-  const int tpb = (a.N + MT - 1) / MT;
-  const int b = mt / tpb;
-  const int row0 = (mt % tpb) * MT;
-  const int nvalid = min(MT, n_valid(a.nrec, b, a.N) - row0);
-  if (nvalid <= 0) return;
-  const int k0 = sp * a.kchunk;
-  const int k1 = min(a.K, k0 + a.kchunk);
-  if (k0 >= k1) return;
-  const int nk = (k1 - k0) / KS;
-  const int w = threadIdx.x >> 6;
-  const bool wvalid = nt * WTraits<MODE>::COLS + w * 32 < a.Nout;
-  switch ((nvalid + 31) >> 5) {
-    case 1: wgemm_tile<MODE, 1>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 2: wgemm_tile<MODE, 2>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 3: wgemm_tile<MODE, 3>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 4: wgemm_tile<MODE, 4>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 5: wgemm_tile<MODE, 5>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 6: wgemm_tile<MODE, 6>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    case 7: wgemm_tile<MODE, 7>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
-    default: wgemm_tile<MODE, 8>(a, lds, rowinv, b, row0, nvalid, nt, k0, nk, wvalid, sp); break;
+  switch ((((nvalid + 15) >> 4) + 3) >> 2) {
+    case 1: wgemm_tile<MODE, 1>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
+    case 2: wgemm_tile<MODE, 2>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
+    case 3: wgemm_tile<MODE, 3>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
+    default: wgemm_tile<MODE, 4>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
   }
 }
 
@@ -613,13 +552,6 @@ __device__ __forceinline__ int key_pos(int row, int T, int N, int W, int head) {
   return T + lg * N + i;
 }
 
-// Workgroup barrier that orders LDS accesses only: global loads in flight stay in
-// flight across it (the full fence of __syncthreads would drain them).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // One staging task of a 32-key block (the same task count for keys and values):
 //   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of one key (pre-RoPE),
@@ -1077,30 +1009,34 @@ __global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
   for (int e = lane; e < c.d / 8; e += 64) yd[e] = ys[e];
 }
 
-// Split-K count for a weight-streaming GEMM: enough workgroups to cover the chip
-// about once, at least PD K-steps per split, within the partial-sum buffer.
-int pick_splits(int tiles, int K, int want_wgs, long rows, int ncols, size_t cap_elems) {
-  // workgroups hold a whole CU each: stay within one round of them
-  int s = std::max(1, std::min(kMaxSplits, want_wgs / std::max(tiles, 1)));
-  s = std::min(s, std::max(1, K / kMinSplitK));
-  while (s > 1 && (size_t)s * rows * ncols > cap_elems) --s;
-  return s;
-}
-
+// Column groups and K splits of a weight-streaming GEMM: columns in 16-wide blocks,
+// at most NBLK blocks per group, and enough (group, split) pairs to cover the CUs
+// about once; every split keeps at least 4 K steps and the partial sums fit.
 template <int MODE>
-fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int B, int want_wgs) {
-  g.m_tiles = B * ((g.N + MT - 1) / MT);
-  g.n_tiles = (g.Nout + WTraits<MODE>::COLS - 1) / WTraits<MODE>::COLS;
-  int s = (MODE == G_GU) ? 1
-                         : pick_splits(g.m_tiles * g.n_tiles, g.K, want_wgs, g.rows, g.Nout,
-                                       ctx->part_elems);
-  const int ksteps = g.K / BK;
-  const int per = (ksteps + s - 1) / s;
-  g.kchunk = per * BK;
-  g.splits = (ksteps + per - 1) / per;
-  const int total = g.m_tiles * g.n_tiles * g.splits;
+fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int B) {
+  if (g.K % KS || g.Nout % 16)
+    return fail(FC_ERR_SHAPE, "%s: K %d must be a multiple of %d and N %d of 16", name, g.K, KS, g.Nout);
+  const int cus = std::max(ctx->num_cus, 1);
+  const int nblk = WTraits<MODE>::NBLK;
+  g.nb = g.Nout / 16;
+  g.tpb = (g.N + MT - 1) / MT;
+  const int ksteps = g.K / KS;
+  int splits = 1;
+  if (MODE == G_GU) {
+    g.ncg = std::max((g.nb + nblk - 1) / nblk, std::min(cus, g.nb));
+  } else {
+    g.ncg = (g.nb + nblk - 1) / nblk;
+    splits = std::max(1, std::min(kMaxSplits, cus / g.ncg));
+    splits = std::min(splits, std::max(1, ksteps / 4));
+    while (splits > 1 && (size_t)splits * g.rows * g.Nout > ctx->part_elems) --splits;
+  }
+  g.ksteps = (ksteps + splits - 1) / splits;
+  g.splits = (ksteps + g.ksteps - 1) / g.ksteps;
+  if (MODE != G_GU && (size_t)g.splits * g.rows * g.Nout > ctx->part_elems)
+    return fail(FC_ERR_CAPACITY, "%s: partial sums exceed the workspace", name);
+  const long total = (long)B * g.tpb * g.ncg * g.splits;
   ProfScope ps(ctx, st, name);
-  hipLaunchKernelGGL(k_wgemm<MODE>, dim3(total), dim3(256), 0, st, g);
+  hipLaunchKernelGGL(k_wgemm<MODE>, dim3((unsigned)total), dim3(512), 0, st, g);
   FC_HIP_TRY(hipGetLastError());
   return FC_OK;
 }
@@ -1152,7 +1088,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     g.A = ctx->hb; g.W0 = L.w_qkv;
     g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
-    if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B, want)) != FC_OK) return rc;
+    if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B)) != FC_OK) return rc;
     r.splits = g.splits; r.ncols = qkv;
     r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
     ProfScope ps(ctx, st, "fc_red_qkv");
@@ -1217,7 +1153,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     g.A = ctx->attn; g.W0 = L.w_o;
     g.K = nh * hd; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
-    if ((rc = run_wgemm<G_O>(ctx, st, "fc_gemm_o", g, B, want)) != FC_OK) return rc;
+    if ((rc = run_wgemm<G_O>(ctx, st, "fc_gemm_o", g, B)) != FC_OK) return rc;
     r.splits = g.splits; r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq;
     r.gain = L.g_mlp;
     ProfScope ps(ctx, st, "fc_red_o");
@@ -1233,7 +1169,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     g.K = d; g.Nout = ffn; g.N = N; g.idx = idx; g.nrec = nrec;
     g.rows = rows; g.act = ctx->act; g.eps = L.rms_eps;
     g.ssq = ctx->ssq; g.ss_parts = (d + 1023) / 1024;
-    if ((rc = run_wgemm<G_GU>(ctx, st, "fc_gemm_gateup", g, B, want)) != FC_OK) return rc;
+    if ((rc = run_wgemm<G_GU>(ctx, st, "fc_gemm_gateup", g, B)) != FC_OK) return rc;
   }
 
   // 5. down projection; reduction adds h1 and scatters bf16 rows into the output cache
@@ -1242,7 +1178,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     g.A = ctx->act; g.W0 = L.w_down;
     g.K = ffn; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
-    if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B, want)) != FC_OK) return rc;
+    if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B)) != FC_OK) return rc;
     r.splits = g.splits; r.ncols = d; r.y = y_cur;
     ProfScope ps(ctx, st, "fc_red_down");
     hipLaunchKernelGGL(k_red_down, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
