@@ -178,7 +178,7 @@ struct WStage {
 
 // One (M tile, column group, K split) with MBW 16-row blocks per MFMA wave.
 template <int MODE, int MBW>
-__device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, const float *rowinv,
+__device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, float *rowinv,
                                            int b, int row0, int nvalid, int cg, int sp, int nk) {
   using T = WTraits<MODE>;
   using S = WStage<MODE, MBW>;
@@ -244,10 +244,21 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, c
       const int nxt = k + PD - 1;
       if (nxt < nk) issue(nxt, nxt % PD);                      // the stage of step k - 1
     }
+    lds_barrier();                                             // barrier nk: LDS is free
     return;
   }
 
   // -------------------------------------------------------------------- MFMA waves
+  if (MODE == G_GU) {
+    // 1/rms of each row from the per-chunk sums of squares of h1, while the first
+    // stages are in flight (these waves have no loads of their own outstanding)
+    for (int r = t; r < MT; r += 256) {
+      float v = 0.f;
+      if (r < nvalid)
+        for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
+      rowinv[r] = 1.f / sqrtf(v / (float)a.K + a.eps);
+    }
+  }
   const int l16 = lane & 15, g = lane >> 4;
   f32x4 acc[MBW][NBW];
 #pragma unroll
@@ -281,43 +292,51 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, c
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
   }
 
+  lds_barrier();                                               // barrier nk: LDS is free
+
+  // Epilogue: each 16-row block goes through a wave-private LDS tile so that the global
+  // stores are whole 16-B chunks of contiguous row segments (a lane's accumulators hold
+  // one column of 4 rows).  The row pitch is 16 B past a multiple of 64 B, which spreads
+  // the 4 row groups of a tile write over distinct banks.
   // lane holds column l16 and rows 4 g + e of each 16-row block
-  if (MODE == G_GU) {
+  constexpr int ESZ = MODE == G_GU ? 2 : 4;                    // bytes per output value
+  constexpr int PITCH = NBLK * 16 * ESZ + (MODE == G_GU ? 48 : 16);
+  static_assert(4 * 16 * PITCH <= kLdsBytes, "epilogue tiles fit in LDS");
+  unsigned char *tile = lds + w * 16 * PITCH;
+  const int nch = nblk * 16 * ESZ / 16;                        // 16-B chunks per row segment
 #pragma unroll
-    for (int i = 0; i < MBW; ++i) {
-      if (w + 4 * i >= nbm) continue;
+  for (int i = 0; i < MBW; ++i) {
+    const int blk = w + 4 * i;
+    if (blk >= nbm) continue;
 #pragma unroll
-      for (int j = 0; j < NBLK; ++j) {
-        if (j >= nblk) continue;
-        const int col = (cb0 + j) * 16 + l16;
+    for (int j = 0; j < NBLK; ++j) {
+      if (j >= nblk) continue;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = (w + 4 * i) * 16 + 4 * g + e;
-          if (r < nvalid) {
-            const float sc = rowinv[r];
-            const float gv = acc[i][j][e] * sc;
-            const float uv = acc[i][NBLK + j][e] * sc;
-            a.act[(slot0 + r) * a.Nout + col] = f2bf(gv / (1.f + __expf(-gv)) * uv);
-          }
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g + e;
+        if (MODE == G_GU) {
+          const float sc = rowinv[min(blk * 16 + r, MT - 1)];
+          const float gv = acc[i][j][e] * sc;
+          const float uv = acc[i][NBLK + j][e] * sc;
+          *reinterpret_cast<uint16_t *>(tile + r * PITCH + (j * 16 + l16) * 2) =
+              f2bf(gv / (1.f + __expf(-gv)) * uv);
+        } else {
+          *reinterpret_cast<float *>(tile + r * PITCH + (j * 16 + l16) * 4) = acc[i][j][e];
         }
       }
     }
-  } else {
-    float *P = a.part + ((long)sp * a.rows + slot0) * a.Nout;
-#pragma unroll
-    for (int i = 0; i < MBW; ++i) {
-      if (w + 4 * i >= nbm) continue;
-#pragma unroll
-      for (int j = 0; j < NBLK; ++j) {
-        if (j >= nblk) continue;
-        const int col = (cb0 + j) * 16 + l16;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = (w + 4 * i) * 16 + 4 * g + e;
-          if (r < nvalid) P[(long)r * a.Nout + col] = acc[i][j][e];
-        }
-      }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+    const int rows_here = min(16, nvalid - blk * 16);
+    for (int c = lane; c < rows_here * nch; c += 64) {
+      const int r = c / nch, x = c - r * nch;
+      const uint4 v = *reinterpret_cast<const uint4 *>(tile + r * PITCH + x * 16);
+      const long grow = slot0 + blk * 16 + r;
+      if (MODE == G_GU)
+        *reinterpret_cast<uint4 *>(a.act + grow * a.Nout + cb0 * 16 + x * 8) = v;
+      else
+        *reinterpret_cast<uint4 *>(a.part + ((long)sp * a.rows + grow) * a.Nout + cb0 * 16 + x * 4) = v;
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
   }
 }
 
@@ -336,17 +355,6 @@ __global__ __launch_bounds__(512) void k_wgemm(WArgs a) {
   const int nvalid = min(MT, n_valid(a.nrec, b, a.N) - row0);
   const int nk = min(a.ksteps, a.K / KS - sp * a.ksteps);
   if (nvalid <= 0 || nk <= 0) return;
-  if (MODE == G_GU) {
-    // 1/rms of each row from the per-chunk sums of squares of h1
-    const long slot0 = (long)b * a.N + row0;
-    for (int r = threadIdx.x; r < MT; r += blockDim.x) {
-      float v = 0.f;
-      if (r < nvalid)
-        for (int c = 0; c < a.ss_parts; ++c) v += a.ssq[(slot0 + r) * a.ss_parts + c];
-      rowinv[r] = 1.f / sqrtf(v / (float)a.K + a.eps);
-    }
-    __syncthreads();
-  }
   switch ((((nvalid + 15) >> 4) + 3) >> 2) {
     case 1: wgemm_tile<MODE, 1>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
     case 2: wgemm_tile<MODE, 2>(a, lds, rowinv, b, row0, nvalid, cg, sp, nk); break;
@@ -984,29 +992,34 @@ struct CacheArgs {
   int N, S, kvw, d, gw, gh, cur_row0;
 };
 
+// One thread per 16-B chunk of a reused token's K row, V row and output row, so that
+// every copy of the remap is in flight at once.
 __global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
   const int b = blockIdx.y;
-  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  const int kc = c.kvw / 8, cpt = 2 * kc + c.d / 8;             // chunks per token
+  const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int tok = (int)(e / cpt);
   if (tok >= c.N) return;
   if (!c.reuse[(long)b * c.N + tok]) return;
+  const int q = (int)(e - (long)tok * cpt);
   const int I = tok / c.gw, J = tok - I * c.gw;
   const int si = I + c.shift[b * 2], sj = J + c.shift[b * 2 + 1];
   if (si < 0 || si >= c.gh || sj < 0 || sj >= c.gw) return;  // never for a valid mask
   const int src = si * c.gw + sj;
-  const long drow = (long)b * c.S + c.cur_row0 + tok;
-  const long srow = (long)b * c.src_bstride / c.kvw + c.src_row0 + src;
-  const uint4 *ks = reinterpret_cast<const uint4 *>(c.ksrc + srow * c.kvw);
-  const uint4 *vs = reinterpret_cast<const uint4 *>(c.vsrc + srow * c.kvw);
-  uint4 *kd = reinterpret_cast<uint4 *>(c.kc + drow * c.kvw);
-  uint4 *vd = reinterpret_cast<uint4 *>(c.vc + drow * c.kvw);
-  for (int e = lane; e < c.kvw / 8; e += 64) {
-    kd[e] = ks[e];
-    vd[e] = vs[e];
+  if (q < 2 * kc) {
+    const long drow = (long)b * c.S + c.cur_row0 + tok;
+    const long srow = (long)b * c.src_bstride / c.kvw + c.src_row0 + src;
+    const bool isk = q < kc;
+    const uint4 *s4 = reinterpret_cast<const uint4 *>((isk ? c.ksrc : c.vsrc) + srow * c.kvw);
+    uint4 *d4 = reinterpret_cast<uint4 *>((isk ? c.kc : c.vc) + drow * c.kvw);
+    const int x = isk ? q : q - kc;
+    d4[x] = s4[x];
+  } else {
+    const int x = q - 2 * kc;
+    const uint4 *ys = reinterpret_cast<const uint4 *>(c.y_prev + ((long)b * c.N + src) * c.d);
+    uint4 *yd = reinterpret_cast<uint4 *>(c.y_cur + ((long)b * c.N + tok) * c.d);
+    yd[x] = ys[x];
   }
-  const uint4 *ys = reinterpret_cast<const uint4 *>(c.y_prev + ((long)b * c.N + src) * c.d);
-  uint4 *yd = reinterpret_cast<uint4 *>(c.y_cur + ((long)b * c.N + tok) * c.d);
-  for (int e = lane; e < c.d / 8; e += 64) yd[e] = ys[e];
 }
 
 // Column groups and K splits of a weight-streaming GEMM: columns in 16-wide blocks,
@@ -1236,7 +1249,8 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
     c.src_row0 = kv.text_tokens + prev_slot * N;
   }
   ProfScope ps(ctx, st, "fc_cache_update");
-  hipLaunchKernelGGL(k_cache_update, dim3((N + 3) / 4, B), dim3(256), 0, st, c);
+  const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
+  hipLaunchKernelGGL(k_cache_update, dim3((unsigned)((chunks + 255) / 256), B), dim3(256), 0, st, c);
   FC_HIP_TRY(hipGetLastError());
   return FC_OK;
 }

@@ -147,3 +147,44 @@ def test_qwen_layer_reuse_ratios(fc, ctx, qwen_case, reuse):
     """Full-size layer at reuse 0/25/50/75/90 % with random masks (0 % = full
     recompute of the current frame), in the launch configuration the benchmark uses."""
     qwen_case.check(fc, ctx, [fcdata.random_reuse_ids(100 + reuse, 256, reuse)])
+
+
+@pytest.mark.parametrize("W,head,B", [(1, 0, 1), (3, 2, 2), (8, 5, 1)])
+def test_cache_update_matches_oracle(fc, ctx, W, head, B):
+    """fc_cache_update against the oracle's remap (Sec. 4.1 alignment, Eq. 4-2): each
+    reused token takes the K/V rows of its aligned source token in the previous frame's
+    slot and its output row; every other byte of K, V and the output cache stays as it
+    was.  W = 1 is the in-place window (the previous frame's rows are the current
+    slot's), W > 1 a ring at a nonzero head; per-item shifts differ in sign."""
+    shape = GQA_SMALL
+    N, gw, T = 64, 8, 16
+    lay = ol.Layout(T=T, N=N, W=W, head=head)
+    rng = np.random.default_rng(100 + 10 * W + B)
+    kvw = shape.n_kv * shape.hd
+    k = rng.integers(0, 1 << 16, size=(B, lay.S, shape.n_kv, shape.hd), dtype=np.uint16)
+    v = rng.integers(0, 1 << 16, size=k.shape, dtype=np.uint16)
+    y_prev = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+    y_cur = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+    shifts = np.array([[1, -2], [-3, 1]][:B], np.int32)
+    mask = np.zeros((B, N), np.uint8)
+    for b in range(B):
+        I, J = np.divmod(np.arange(N), gw)
+        si, sj = I + shifts[b, 0], J + shifts[b, 1]
+        aligned = (si >= 0) & (si < N // gw) & (sj >= 0) & (sj < gw)
+        mask[b] = aligned & (rng.random(N) < 0.6)
+    kc, vc = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v)
+    yp, yc = fcutil.bf16_gpu(y_prev), fcutil.bf16_gpu(y_cur)
+    wg = fcutil.weights_gpu(fcdata.layer_weights(0, shape))
+    desc = fcutil.layer_desc(shape, wg)
+    kv = fc.KVCache(kc, vc, T, N, W, head)
+    fc.fc_cache_update(ctx, desc, kv, yp, yc, torch.from_numpy(shifts).cuda(),
+                       torch.from_numpy(mask).cuda(), gw)
+    torch.cuda.synchronize()
+    kg, vg, yg = fcutil.bf16_np(kc), fcutil.bf16_np(vc), fcutil.bf16_np(yc)
+    for b in range(B):
+        ko, vo, yo = ol.cache_update(k[b].reshape(lay.S, kvw), v[b].reshape(lay.S, kvw),
+                                     y_prev[b], y_cur[b], tuple(shifts[b]), mask[b], gw, lay)
+        np.testing.assert_array_equal(kg[b].reshape(lay.S, kvw), ko)
+        np.testing.assert_array_equal(vg[b].reshape(lay.S, kvw), vo)
+        np.testing.assert_array_equal(yg[b], yo)
+        assert mask[b].sum() > 0
