@@ -384,14 +384,25 @@ struct RedArgs {
   uint16_t *y;                    // [B][N][d]
 };
 
+// Sum of the split-K partials of 4 columns, in split order.  SPL is the split count
+// rounded up to a power of two: every load is issued before the first add (splits past
+// the last re-read it and are not added), so the sum costs one memory round trip.
+template <int SPL>
 __device__ __forceinline__ float4 sum_parts(const RedArgs &r, long slot, int c) {
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   const float *p = r.part + slot * r.ncols + c;
   const long stride = r.rows * r.ncols;
-#pragma unroll 4
-  for (int s = 0; s < r.splits; ++s) {
-    const float4 u = *reinterpret_cast<const float4 *>(p + s * stride);
-    v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+  float4 u[SPL];
+#pragma unroll
+  for (int s = 0; s < SPL; ++s)
+    u[s] = *reinterpret_cast<const float4 *>(p + min(s, r.splits - 1) * stride);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s = 0; s < SPL; ++s) {
+    const bool in = s < r.splits;
+    v.x += in ? u[s].x : 0.f;
+    v.y += in ? u[s].y : 0.f;
+    v.z += in ? u[s].z : 0.f;
+    v.w += in ? u[s].w : 0.f;
   }
   return v;
 }
@@ -447,6 +458,7 @@ __global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict_
 // (rotate-half RoPE at the token's prompt position) in float32 before their single
 // rounding to bf16; a 1024-column block always holds whole heads, so the partner
 // dim of the rotation comes from LDS.  K and V rows go raw into the cache.
+template <int SPL>
 __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   __shared__ float qs[1024];
   const long slot = blockIdx.x;
@@ -457,7 +469,7 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   const int tok = tok_of(r.idx, slot, r.N);
   float vv[4] = {0.f, 0.f, 0.f, 0.f};
   if (c < r.ncols) {
-    const float4 v = sum_parts(r, slot, c);
+    const float4 v = sum_parts<SPL>(r, slot, c);
     vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
 #pragma unroll
     for (int e = 0; e < 4; ++e) vv[e] += bf2f(r.bias[c + e]);
@@ -491,6 +503,7 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   *reinterpret_cast<uint2 *>(dst) = make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
 }
 
+template <int SPL>
 __global__ __launch_bounds__(256) void k_red_o(RedArgs r) {
   __shared__ float red[256];
   const long slot = blockIdx.x;
@@ -500,7 +513,7 @@ __global__ __launch_bounds__(256) void k_red_o(RedArgs r) {
   const int tok = tok_of(r.idx, slot, r.N);
   float ss = 0.f;
   if (c < r.d) {
-    const float4 v = sum_parts(r, slot, c);
+    const float4 v = sum_parts<SPL>(r, slot, c);
     const uint2 xb = *reinterpret_cast<const uint2 *>(r.x + ((long)b * r.N + tok) * r.d + c);
     float4 h;
     h.x = v.x + __uint_as_float(xb.x << 16);
@@ -522,6 +535,7 @@ __global__ __launch_bounds__(256) void k_red_o(RedArgs r) {
   if (threadIdx.x == 0) r.ssq[slot * gridDim.y + blockIdx.y] = ss;
 }
 
+template <int SPL>
 __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
   const long slot = blockIdx.x;
   const int b = (int)(slot / r.N), j = (int)(slot - (long)b * r.N);
@@ -529,7 +543,7 @@ __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
   const int c = blockIdx.y * 1024 + threadIdx.x * 4;
   if (c >= r.d) return;
   const int tok = tok_of(r.idx, slot, r.N);
-  const float4 v = sum_parts(r, slot, c);
+  const float4 v = sum_parts<SPL>(r, slot, c);
   const float4 h = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + c);
   *reinterpret_cast<uint2 *>(r.y + ((long)b * r.N + tok) * r.d + c) =
       make_uint2(f2bf(h.x + v.x) | ((uint32_t)f2bf(h.y + v.y) << 16),
@@ -1056,6 +1070,23 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
 
 }  // namespace
 
+namespace {
+template <int SPL>
+void launch_red(int which, dim3 grid, hipStream_t st, const RedArgs &r) {
+  if (which == 0) hipLaunchKernelGGL(k_red_qkv<SPL>, grid, dim3(256), 0, st, r);
+  else if (which == 1) hipLaunchKernelGGL(k_red_o<SPL>, grid, dim3(256), 0, st, r);
+  else hipLaunchKernelGGL(k_red_down<SPL>, grid, dim3(256), 0, st, r);
+}
+// which: 0 QKV, 1 O, 2 down
+void run_red(int which, dim3 grid, hipStream_t st, const RedArgs &r) {
+  if (r.splits <= 1) launch_red<1>(which, grid, st, r);
+  else if (r.splits <= 2) launch_red<2>(which, grid, st, r);
+  else if (r.splits <= 4) launch_red<4>(which, grid, st, r);
+  else if (r.splits <= 8) launch_red<8>(which, grid, st, r);
+  else launch_red<16>(which, grid, st, r);
+}
+}  // namespace
+
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                        const uint16_t *x_cur, const int32_t *idx, const int32_t *nrec,
                        uint16_t *y_cur, int B, hipStream_t st) {
@@ -1105,7 +1136,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     r.splits = g.splits; r.ncols = qkv;
     r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
     ProfScope ps(ctx, st, "fc_red_qkv");
-    hipLaunchKernelGGL(k_red_qkv, dim3((unsigned)rows, (qkv + 1023) / 1024), dim3(256), 0, st, r);
+    run_red(0, dim3((unsigned)rows, (qkv + 1023) / 1024), st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
@@ -1170,7 +1201,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     r.splits = g.splits; r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq;
     r.gain = L.g_mlp;
     ProfScope ps(ctx, st, "fc_red_o");
-    hipLaunchKernelGGL(k_red_o, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
+    run_red(1, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
@@ -1194,7 +1225,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B)) != FC_OK) return rc;
     r.splits = g.splits; r.ncols = d; r.y = y_cur;
     ProfScope ps(ctx, st, "fc_red_down");
-    hipLaunchKernelGGL(k_red_down, dim3((unsigned)rows, (d + 1023) / 1024), dim3(256), 0, st, r);
+    run_red(2, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
     FC_HIP_TRY(hipGetLastError());
   }
   return FC_OK;
