@@ -626,19 +626,20 @@ __device__ __forceinline__ int vq_word(int kg, int hd) {
 }
 
 // Attention of one 32-query tile of kv head g over key blocks [kb0, kb1) of the cache.
-// Wave w < G handles query head g*G + w; the queries arrive rotated.  The 32-key blocks are staged through two
-// LDS buffers (keys rotated, values interleaved) with the raw loads of block kb + 2
-// in flight while block kb is multiplied, so the cache latency is paid once per
-// split rather than once per block.
+// Wave w < G handles query head g*G + w; the queries arrive rotated.  The waves past
+// them only move data: they fetch the raw K/V rows, rotate the keys and stage both
+// into one of two LDS buffers (keys rotated, values interleaved), with the raw loads
+// of block kb + 2 in flight while block kb is multiplied, so the cache latency is
+// paid once per split and the staging ALU work runs beside the MFMAs.
+constexpr int kAttnStageWaves = 4;
 template <int HD, int G>
-__global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 16;   // k-steps of the QK^T product
   constexpr int NHB = HD / 32;  // 32-row blocks of the output
-  constexpr int NW = G < 4 ? 4 : G;   // waves: G query heads, at least 4 stagers
-  constexpr int NT = NW * 64;
+  constexpr int NL = kAttnStageWaves * 64;   // staging threads
   constexpr int CPK = HD / 16;  // key staging tasks per key
   constexpr int TASKS = 32 * CPK;
-  constexpr int TPT = (TASKS + NT - 1) / NT;
+  constexpr int TPT = (TASKS + NL - 1) / NL;
   constexpr int QLD = HD + 8;   // padded LDS row of the rotated queries
   static_assert(TASKS % 64 == 0, "staging tasks fill whole waves");
   static_assert(TASKS == 8 * (HD / 4), "key and value tasks pair up");
@@ -662,7 +663,10 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   if (j0 >= n) return;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
-  const bool qwave = w < G;           // waves past G only stage keys and values
+  // waves below G multiply (one query head each); the two waves past them fetch, rotate
+  // and stage the next key block meanwhile, so loads and staging overlap the MFMAs
+  const bool qwave = w < G;
+  const int tl = t - G * 64;          // staging thread index (staging waves only)
   const int h = g * G + (qwave ? w : 0);
 
   const int j = j0 + l32;
@@ -670,13 +674,6 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   const long slot = (long)b * a.N + (qvalid ? j : j0);
   const int tok = tok_of(a.idx, slot, a.N);
   const int qpos = a.T + (a.W - 1) * a.N + tok;
-
-  f32x16 o[NHB];
-#pragma unroll
-  for (int hb = 0; hb < NHB; ++hb)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[hb][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
 
   const int nkb = (a.S + 31) / 32;
   const int kb0 = sp * a.kb_per_split;
@@ -692,7 +689,7 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
     kb = min(kb, kb1 - 1);
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
-      const int task = t + i * NT;
+      const int task = tl + i * NL;
       if (task < TASKS) {
         const int key = task / CPK, c = task - key * CPK;
         const int row0 = kb * 32 + key;
@@ -733,7 +730,7 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
   auto stage = [&](const KVRaw (&R)[TPT], int buf) {
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
-      const int task = t + i * NT;
+      const int task = tl + i * NL;
       if (task < TASKS) {
         const int key = task / CPK, c = task - key * CPK;
         U16x8 k1, k2;
@@ -762,6 +759,41 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
       }
     }
   };
+  auto needs_mask = [&](int kb) {
+    const int r0 = kb * 32, r1 = r0 + 32;
+    return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
+  };
+
+  if (!qwave) {
+    // staging waves: fetch, rotate and stage block kb + 1 while block kb is multiplied
+    KVRaw ra[TPT], rb[TPT];
+    fetch(kb0, ra);
+    fetch(kb0 + 1, rb);
+    settle(ra);
+    stage(ra, 0);
+    lds_barrier();
+    for (int kb = kb0; kb < kb1; kb += 2) {
+      fetch(kb + 2, ra);
+      settle(rb);
+      stage(rb, 1);
+      lds_barrier();
+      fetch(kb + 3, rb);
+      settle(ra);
+      stage(ra, 0);
+      lds_barrier();
+    }
+    // nothing may be left in flight when the wave ends
+    __builtin_amdgcn_s_waitcnt(0x3F70);
+    return;
+  }
+
+  // ------------------------------------------------------------ query waves
+  f32x16 o[NHB];
+#pragma unroll
+  for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[hb][e] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
   // S^T = K Q^T for the 32 keys of buffer buf, online softmax, O^T += V^T P^T
   auto compute = [&](int buf, bool masked) {
     f32x16 st;
@@ -827,59 +859,39 @@ __global__ __launch_bounds__((G < 4 ? 4 : G) * 64) void k_attn(AttnArgs a) {
       }
     }
   };
-  auto needs_mask = [&](int kb) {
-    const int r0 = kb * 32, r1 = r0 + 32;
-    return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
-  };
-
-  KVRaw ra[TPT], rb[TPT];
-  fetch(kb0, ra);
-  fetch(kb0 + 1, rb);
-  // Q fragments (B operand of S^T = K Q^T; lane holds q[16 s + 8 hi + e]): the tile's
-  // rotated query rows (the G heads of kv group g are contiguous in a row) are staged
-  // through LDS with whole-line loads while the first key blocks are in flight
   {
-    constexpr int QCH = G * HD / 8;                  // 16-B chunks of one query row
-    constexpr int QIT = (32 * QCH + NT - 1) / NT;    // chunks per thread
+    // Q fragments (B operand of S^T = K Q^T; lane holds q[16 s + 8 hi + e]): the tile's
+    // rotated query rows (the G heads of kv group g are contiguous in a row) are staged
+    // through LDS with whole-line loads while the first key blocks are in flight
+    constexpr int QT = G * 64;                        // query-wave threads
+    constexpr int QCH = G * HD / 8;                   // 16-B chunks of one query row
+    constexpr int QIT = (32 * QCH + QT - 1) / QT;     // chunks per thread
     uint4 qv[QIT];
 #pragma unroll
     for (int i = 0; i < QIT; ++i) {
-      const int c = min(t + i * NT, 32 * QCH - 1);
+      const int c = min(t + i * QT, 32 * QCH - 1);
       const int r = c / QCH, x = c - r * QCH;
       const long sl = (long)b * a.N + (j0 + r < n ? j0 + r : j0);
       qv[i] = *reinterpret_cast<const uint4 *>(a.q + sl * (a.nh * HD) + (long)g * G * HD + 8 * x);
     }
 #pragma unroll
     for (int i = 0; i < QIT; ++i) {
-      const int c = t + i * NT;
+      const int c = t + i * QT;
       if (c < 32 * QCH) {
         const int r = c / QCH, x = c - r * QCH;
         *reinterpret_cast<uint4 *>(&Qs[(8 * x) / HD][r * QLD + (8 * x) % HD]) = qv[i];
       }
     }
   }
-  settle(ra);
-  stage(ra, 0);
   lds_barrier();
   for (int kb = kb0; kb < kb1; kb += 2) {
-    // buffer 0 holds block kb, rb block kb + 1 (in flight)
-    fetch(kb + 2, ra);
-    if (qwave) compute(0, needs_mask(kb));
-    settle(rb);
-    stage(rb, 1);
+    compute(0, needs_mask(kb));                       // buffer 0: block kb
     lds_barrier();
-    // buffer 1 holds block kb + 1, ra block kb + 2 (in flight)
-    fetch(kb + 3, rb);
-    if (qwave && kb + 1 < kb1) compute(1, needs_mask(kb + 1));
-    settle(ra);
-    stage(ra, 0);
+    if (kb + 1 < kb1) compute(1, needs_mask(kb + 1)); // buffer 1: block kb + 1
     lds_barrier();
   }
-  // nothing may be left in flight into registers the epilogue reuses
-  __builtin_amdgcn_s_waitcnt(0x3F70);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!qwave) return;
   if (a.splits == 1) {
     if (!qvalid) return;
     uint16_t *orow = a.out + slot * (long)(a.nh * HD) + h * HD;
@@ -1168,15 +1180,15 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     {
       ProfScope ps(ctx, st, "fc_attn");
       if (hd == 128 && G == 7)
-        hipLaunchKernelGGL((k_attn<128, 7>), grid, dim3(7 * 64), 0, st, a);
+        hipLaunchKernelGGL((k_attn<128, 7>), grid, dim3((7 + kAttnStageWaves) * 64), 0, st, a);
       else if (hd == 128 && G == 1)
-        hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3((1 + kAttnStageWaves) * 64), 0, st, a);
       else if (hd == 64 && G == 1)
-        hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3((1 + kAttnStageWaves) * 64), 0, st, a);
       else if (hd == 64 && G == 2)
-        hipLaunchKernelGGL((k_attn<64, 2>), grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((k_attn<64, 2>), grid, dim3((2 + kAttnStageWaves) * 64), 0, st, a);
       else if (hd == 128 && G == 4)
-        hipLaunchKernelGGL((k_attn<128, 4>), grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((k_attn<128, 4>), grid, dim3((4 + kAttnStageWaves) * 64), 0, st, a);
       else
         return fail(FC_ERR_UNSUPPORTED, "attention: head_dim %d with %d query heads per kv head", hd, G);
       FC_HIP_TRY(hipGetLastError());
