@@ -14,7 +14,11 @@ Also reported, each measured in the same run:
                 peak, its duration from HIP events on its launch stream;
   cpu_baseline  the CPU oracle on a bounded sample of the same step;
   select_batch  fc_select on 64 pairs of 448x448 frames, GB/s of frame input;
-  layer_ratios  one layer at reuse 0/25/50/75/90 %, time, MFMA utilisation.
+  layer_ratios  one layer at reuse 0/25/50/75/90 %, time, MFMA utilisation;
+  batch_episodes  16 concurrent episodes at 896x896 (1024 tokens per frame, a 4-frame
+                window, 4224 cached positions): frames/s of the whole step and the
+                MFMA utilisation of the 28 layers, the regime where the layer is
+                compute bound.
 
     python bench.py [--steps K] [--warmup W]
 """
@@ -48,6 +52,8 @@ def main():
     ap.add_argument("--layers", type=int, default=28)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--batch-steps", type=int, default=3,
+                    help="timed steps of the batched-episode workload (0: skip it)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -62,6 +68,12 @@ def main():
     import torch
     import fcdata
     import paper_2604_24391_amd as fc
+
+    # the batched-episode frames come from a pool of forked workers, which must start
+    # before this process touches the GPU
+    batch_frames = None
+    if not args.no_extras and args.batch_steps > 0:
+        batch_frames = batch_episode_frames(args.batch_steps + 3)
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -199,6 +211,9 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
                                               T, N, Wn, L, gw)
+    if batch_frames is not None:
+        result["batch_episodes"] = bench_batch_episodes(fc, torch, batch_frames, args.batch_steps,
+                                                        L)
     if args.calib_mb > 0:
         n = args.calib_mb * (1 << 20) // 4
         src = torch.ones(n, device=dev, dtype=torch.float32)
@@ -302,6 +317,161 @@ def bench_layer_ratios(fc, ctx, torch, lay, shape):
                                 mfma_util=round(tf / BF16_PEAK_TFLOPS, 4),
                                 weight_gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4))
     return out
+
+
+def _episode_worker(args):
+    import fcdata
+    seed, n_frames = args
+    return fcdata.episode_frames(seed, size=fcdata.BATCH["size"], n_frames=n_frames)
+
+
+def batch_episode_frames(n_frames):
+    """[n_frames, 16, 3, 896, 896] float32: 16 independent seeded trajectories, each
+    over its own texture, generated in parallel by forked workers."""
+    import multiprocessing as mp
+    import fcdata
+    t0 = time.time()
+    E = fcdata.BATCH["episodes"]
+    workers = max(1, min(E, len(os.sched_getaffinity(0))))
+    with mp.get_context("fork").Pool(workers) as pool:
+        eps = pool.map(_episode_worker, [(5000 + e, n_frames) for e in range(E)])
+    out = np.ascontiguousarray(np.stack(eps, axis=1))
+    log(f"batched-episode frames ready in {time.time() - t0:.1f}s ({E} episodes x {n_frames} "
+        f"frames, {workers} workers)")
+    return out
+
+
+def bench_batch_episodes(fc, torch, frames_np, steps, L):
+    """The batched-episode workload: 16 independent episodes, 896x896 frames (4096
+    patches, 2x2 merge -> 1024 tokens), a 4-frame window plus 128 text tokens (4224
+    cached positions), 28 Qwen2.5-VL-7B-shaped layers.  One step = fc_select on the 16
+    (previous, current) pairs, then per layer the window advance, fc_cache_update and
+    fc_layer_forward of the 16 items' recomputed tokens."""
+    import fcdata
+    dev = torch.device("cuda:0")
+    shape = fcdata.QWEN_LAYER
+    B, size, m = fcdata.BATCH["episodes"], fcdata.BATCH["size"], fcdata.BATCH["merge"]
+    T, Wn = fcdata.BATCH["text"], fcdata.BATCH["window"]
+    gw = size // (14 * m)
+    N = gw * gw
+    S = T + Wn * N
+    F = frames_np.shape[0]
+    t0 = time.time()
+    frames = torch.from_numpy(frames_np).to(dev)                       # [F, B, 3, H, W]
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+
+    def randn(*shp, std=0.02):
+        return (torch.randn(*shp, device=dev, generator=g) * std).to(torch.bfloat16)
+
+    # token-embedding stand-in (not timed): a fixed linear map of each token's pixels
+    px = 14 * m
+    proj = randn(3 * px * px, shape.d)
+    emb = torch.empty(F, B, N, shape.d, device=dev, dtype=torch.bfloat16)
+    for f in range(F):
+        tp = frames[f].unfold(2, px, px).unfold(3, px, px).permute(0, 2, 3, 1, 4, 5)
+        emb[f] = (tp.reshape(B, N, 3 * px * px).to(torch.bfloat16) @ proj)
+    layers = []
+    for li in range(L):
+        w = dict(w_qkv=randn(shape.qkv, shape.d), b_qkv=randn(shape.qkv),
+                 w_o=randn(shape.d, shape.n_heads * shape.hd),
+                 w_gate=randn(shape.ffn, shape.d), w_up=randn(shape.ffn, shape.d),
+                 w_down=randn(shape.d, shape.ffn),
+                 g_attn=torch.ones(shape.d, device=dev, dtype=torch.bfloat16),
+                 g_mlp=torch.ones(shape.d, device=dev, dtype=torch.bfloat16))
+        desc = fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w)
+        kv = fc.KVCache(randn(B, S, shape.n_kv, shape.hd, std=1.0),
+                        randn(B, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0)
+        ys = [randn(B, N, shape.d, std=1.0), randn(B, N, shape.d, std=1.0)]
+        layers.append(dict(desc=desc, kv=kv, y=ys))
+    ctx = fc.Context(fc.Caps(max_batch=B, max_height=size, max_width=size, max_tokens=N,
+                             max_seq=S, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    prm = fc.SelectParams(merge=m)
+    sel = fc.SelectOut.alloc(B, N)
+    torch.cuda.synchronize()
+    log(f"batched-episode inputs ready in {time.time() - t0:.1f}s")
+    cur_y = 0
+
+    def step(fi):
+        nonlocal cur_y
+        fc.fc_select(ctx, prm, frames[fi - 1], frames[fi], sel)
+        x = emb[fi]
+        nxt = 1 - cur_y
+        for lay in layers:
+            lay["kv"].advance()
+            fc.fc_cache_update(ctx, lay["desc"], lay["kv"], lay["y"][cur_y], lay["y"][nxt],
+                               sel.shift, sel.reuse_mask, gw)
+            fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, sel.recompute_idx,
+                                sel.n_recompute, lay["y"][nxt])
+            x = lay["y"][nxt]
+        cur_y = nxt
+
+    step(1)                                                            # warmup
+    torch.cuda.synchronize()
+    nrec = []
+    keys = []
+    t1 = time.perf_counter()
+    for k in range(steps):
+        step(2 + k)
+        nrec.append(sel.n_recompute.clone())
+        # keys each recomputed query attends to: text, the older frames, and the current
+        # frame's tokens up to its own
+        ids = sel.recompute_idx.clone()
+        keys.append((ids, sel.n_recompute.clone()))
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t1
+    ms_step = el * 1e3 / steps
+    n_tot = float(torch.stack(nrec).float().sum()) / steps
+    vis = 0.0
+    for ids, nr in keys:
+        valid = torch.arange(N, device=dev)[None, :] < nr[:, None]
+        vis += float(((T + (Wn - 1) * N + ids.clamp(min=0) + 1) * valid).sum())
+    vis /= steps
+    d, f, qkv, o = shape.d, shape.ffn, shape.qkv, shape.n_heads * shape.hd
+    gemm_fl = 2.0 * n_tot * (qkv * d + o * d + 2 * f * d + f * d)
+    attn_fl = 4.0 * shape.n_heads * shape.hd * vis
+    # per-kernel pass (events around every launch), one more step
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    step(2 + steps)
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
+    kern = {}
+    lay_us = 0.0
+    for name in ("fc_spectra", "fc_grid", "fc_patchsim", "fc_topk", "fc_cache_update",
+                 "fc_gather_norm", "fc_mgemm_qkv", "fc_attn", "fc_attn_combine", "fc_mgemm_o",
+                 "fc_mgemm_gateup", "fc_mgemm_down"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        if cnt:
+            kern[name] = dict(avg_us=round(tot * 1e3 / cnt, 2), launches=cnt)
+            if name not in ("fc_spectra", "fc_grid", "fc_patchsim", "fc_topk", "fc_cache_update"):
+                lay_us += tot * 1e3
+    fc.fc_profile_read(ctx, None, reset=True)
+    nr_last = float(sel.n_recompute.float().sum())
+    gu = kern.get("fc_mgemm_gateup")
+    gu_tf = None
+    if gu:
+        gu_tf = 4.0 * nr_last * f * d / (gu["avg_us"] * 1e-6) / 1e12
+    layer_tf = L * (gemm_fl + attn_fl) / (lay_us * 1e-6) / 1e12 if lay_us else None
+    step_tf = L * (gemm_fl + attn_fl) / (ms_step * 1e-3) / 1e12
+    ctx.close()
+    log(f"batched episodes: {ms_step:.1f} ms/step, {B * 1e3 / ms_step:.1f} frames/s, "
+        f"mean recomputed {n_tot / B:.0f}/{N} per item")
+    return dict(
+        workload=f"{B} episodes x 896x896 frames (14-px patches, 2x2 merge, {N} tokens), "
+                 f"adaptive budget, {Wn}-frame window + {T} text = {S} cached positions, "
+                 f"{L} Qwen2.5-VL-7B-shaped bf16 layers",
+        steps=steps, ms_per_step=round(ms_step, 2), frames_per_s=round(B * 1e3 / ms_step, 2),
+        mean_recomputed_per_item=round(n_tot / B, 1),
+        step_tflops=round(step_tf, 1), step_mfma_util=round(step_tf / BF16_PEAK_TFLOPS, 4),
+        layer_tflops=round(layer_tf, 1) if layer_tf else None,
+        layer_mfma_util=round(layer_tf / BF16_PEAK_TFLOPS, 4) if layer_tf else None,
+        gateup_tflops=round(gu_tf, 1) if gu_tf else None,
+        gateup_mfma_util=round(gu_tf / BF16_PEAK_TFLOPS, 4) if gu_tf else None,
+        flops_note="GEMM 2 n (qkv d + d d + 2 ffn d + ffn d) + attention 4 hd heads "
+                   "(keys visible to each recomputed query), per layer",
+        kernels=kern)
 
 
 def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):

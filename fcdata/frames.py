@@ -47,10 +47,13 @@ def canvas(rng: np.random.Generator, h: int, w: int, patch: int = PATCH,
         x0, x1 = max(0, int(cx) - r), min(w, int(cx) + r + 1)
         if y0 >= y1 or x0 >= x1:
             continue
-        yy = (np.arange(y0, y1) - cy)[:, None]
-        xx = (np.arange(x0, x1) - cx)[None, :]
-        g = np.exp(-(yy * yy + xx * xx) / (2 * sig * sig))
-        img[:, y0:y1, x0:x1] += amp[:, None, None] * g[None]
+        yy = np.arange(y0, y1) - cy
+        xx = np.arange(x0, x1) - cx
+        # the isotropic Gaussian is separable: exp(-(y^2 + x^2) / 2s^2) = gy(y) gx(x)
+        gy = np.exp(-(yy * yy) / (2 * sig * sig))
+        gx = np.exp(-(xx * xx) / (2 * sig * sig))
+        for c in range(3):
+            img[c, y0:y1, x0:x1] += np.outer(amp[c] * gy, gx)
     mx = img.max()
     if mx > 0:
         img /= mx

@@ -150,7 +150,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
       (st = dev_alloc(&ctx->attn, rows * c.max_qkv, "attn")) != FC_OK ||
       (st = dev_alloc(&ctx->h1, rows * c.max_d_model, "h1")) != FC_OK ||
       (st = dev_alloc(&ctx->hb, rows * c.max_d_model, "hb")) != FC_OK ||
-      (st = dev_alloc(&ctx->ssq, rows * 8, "ssq")) != FC_OK ||
+      (st = dev_alloc(&ctx->ssq, rows * std::max<size_t>(8, (c.max_d_model + 127) / 128), "ssq")) != FC_OK ||
       (st = dev_alloc(&ctx->act, rows * c.max_ffn, "act")) != FC_OK ||
       (st = dev_alloc(&ctx->part, ctx->part_elems, "partials")) != FC_OK ||
       (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||

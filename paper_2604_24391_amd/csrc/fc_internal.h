@@ -52,7 +52,7 @@ struct fc_ctx {
   uint16_t *attn = nullptr;    // [rows][n_heads*hd] attention output, bf16
   float *h1 = nullptr;         // [rows][d] post-attention residual stream
   uint16_t *hb = nullptr;      // [rows][d] bf16 copy of h1 (SwiGLU input)
-  float *ssq = nullptr;        // [rows][8] per-1024-column sums of squares of hb
+  float *ssq = nullptr;        // [rows][parts] partial sums of squares of h1 per row
   uint16_t *act = nullptr;     // [rows][ffn] SwiGLU activation, bf16
   float *part = nullptr;       // split-K / split-KV partial sums
   size_t part_elems = 0;

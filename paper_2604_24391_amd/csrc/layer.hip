@@ -26,6 +26,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 
 #include "fc_internal.h"
 
@@ -548,6 +549,263 @@ __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
   *reinterpret_cast<uint2 *>(r.y + ((long)b * r.N + tok) * r.d + c) =
       make_uint2(f2bf(h.x + v.x) | ((uint32_t)f2bf(h.y + v.y) << 16),
                  f2bf(h.z + v.z) | ((uint32_t)f2bf(h.w + v.w) << 16));
+}
+
+// ------------------------------------------------------------------------------- large-M GEMM
+// For thousands of gathered rows (many batch items) the projections are compute bound
+// and a square tile pays: each workgroup owns a 256 x 256 output tile and streams
+// K in steps of 64 through two LDS stages (A rows, then the 256 staged weight rows,
+// each one 128-B line with 16-B chunks XOR-swizzled by (row >> 1) & 7).
+//   * eight waves, two per SIMD, each owning 128 x 64 of the tile as 4 x 2 blocks of
+//     v_mfma_f32_32x32x16_bf16; the per-CU load rate grows with the number of waves
+//     issuing, and a wave waiting at a DMA issue leaves its SIMD to the other wave;
+//   * every wave issues an eighth of the next step's DMAs as soon as the step's barrier
+//     frees their stage, and reads the fragments of sub-step s + 1 before the MFMAs of
+//     sub-step s;
+//   * the epilogue is fused and goes through LDS 32 rows at a time, so that every
+//     global access is a 16-B (or 8-B) piece of a row: QKV adds the bias, rotates the
+//     queries and scatters raw k and v into the cache; O adds the residual and writes
+//     h1, the SwiGLU operand and per-256-column sums of squares; SwiGLU stages gate
+//     and up rows of the same 32 columns per wave and writes SiLU(g) * u; down adds h1
+//     and scatters the output rows.
+// Tiles are ordered so that the workgroups resident on one XCD at a time cover 4 M
+// tiles x 8 N tiles, which keeps their operand slabs in that XCD's L2.
+constexpr int MB = 256;                     // tile rows and staged weight rows
+constexpr int kMStage = 2 * MB * RB;        // 64 KB per stage
+constexpr int kMSsqCols = 256;              // columns per sum-of-squares partial
+constexpr long kMGemmMinRows = 2048;        // token slots (B * N) that take this path
+constexpr int kMEpPitch = MB + 4;           // floats per row of the epilogue tile
+
+struct MArgs {
+  const uint16_t *A;              // bf16 activations, one row per slot
+  const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
+  int K, Nout, N;                 // Nout: output columns; N: token slots per item
+  int tpb, mtiles, ntn;           // M tiles per item, all M tiles, N tiles
+  int ss_parts;                   // O writes / SwiGLU reads this many partials per row
+  uint16_t *act;                  // SwiGLU output [B*N][Nout]
+  RedArgs r;                      // epilogue operands (as the reductions use them)
+};
+
+__device__ __forceinline__ void mtile_of(const MArgs &a, int bid, int total, int &mt, int &nt) {
+  const int L = xcd_tile(bid, total);
+  constexpr int GM = 4;
+  const int grp = L / (GM * a.ntn);
+  const int base = grp * GM;
+  const int gsz = min(GM, a.mtiles - base);
+  const int li = L - grp * GM * a.ntn;
+  nt = li / gsz;
+  mt = base + (li - nt * gsz);
+}
+
+__device__ __forceinline__ uint2 pack_bf16x4(float a, float b, float c, float d) {
+  return make_uint2(f2bf(a) | ((uint32_t)f2bf(b) << 16), f2bf(c) | ((uint32_t)f2bf(d) << 16));
+}
+__device__ __forceinline__ float4 unpack_bf16x4(uint2 u) {
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+
+template <int MODE>
+__global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kMStage];
+  __shared__ float rowinv[MB];
+  const int total = a.mtiles * a.ntn;
+  int mt, nt;
+  mtile_of(a, blockIdx.x, total, mt, nt);
+  const int b = mt / a.tpb;
+  const int row0 = (mt % a.tpb) * MB;
+  const int nvalid = min(MB, n_valid(a.r.nrec, b, a.N) - row0);
+  if (nvalid <= 0) return;
+  const long slot0 = (long)b * a.N + row0;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = w & 1, wn = w >> 1;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int nk = a.K / KS;
+  // output columns of this tile: SwiGLU stages 32 gate + 32 up rows per wave column
+  constexpr int TN = MODE == G_GU ? MB / 2 : MB;
+  const int col0 = nt * TN;
+
+  // DMA instruction j of a step (this wave issues j = w + 8 i) stages 8 rows:
+  // j < 32 the activation rows 8 j .., else the staged weight rows 8 (j - 32) ..
+  const int rsub = lane >> 3, ch = lane & 7;
+  const uint16_t *gp[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = w + 8 * i;
+    const int r = (j & 31) * 8 + rsub;                         // row within its operand
+    const int cs = (ch ^ swz8(r)) * 8;
+    if (j < 32) {
+      const int rr = r < nvalid ? r : nvalid - 1;              // clamp: never stored
+      gp[i] = a.A + (slot0 + rr) * a.K + cs;
+    } else {
+      const uint16_t *M = a.W0;
+      int col;
+      if (MODE == G_GU) {
+        col = col0 + (r >> 6) * 32 + (r & 31);
+        if (r & 32) M = a.W1;
+      } else {
+        col = col0 + r;
+      }
+      col = min(col, a.Nout - 1);                              // clamp: never stored
+      gp[i] = M + (long)col * a.K + cs;
+    }
+  }
+  const uint32_t lbase = lds_addr(lds);
+  auto issue = [&](int kt) {
+    const int kk = kt * KS;
+    const uint32_t st = lbase + (kt & 1) * kMStage;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dma16(gp[i] + kk, st + (w + 8 * i) * 1024);
+  };
+
+  if (MODE == G_GU && t < MB) {
+    // 1/rms of each row from the O epilogue's partial sums of squares of h1
+    float v = 0.f;
+    if (t < nvalid)
+      for (int c = 0; c < a.ss_parts; ++c) v += a.r.ssq[(slot0 + t) * a.ss_parts + c];
+    rowinv[t] = 1.f / sqrtf(v / (float)a.K + a.r.eps);
+  }
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // fragment of block i, sub-step s: row l32 of the block, 16-B chunk 2 s + h
+  const int sw = swz8(l32);
+  const uint32_t aoff = (uint32_t)((wm * 128 + l32) * RB);
+  const uint32_t boff = (uint32_t)((MB + wn * 64 + l32) * RB);
+  auto rd = [&](const unsigned char *st, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[2]) {
+    const uint32_t slot = (uint32_t)(((2 * s + h) ^ sw) << 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[i] = *reinterpret_cast<const bf16x8 *>(st + aoff + i * 32 * RB + slot);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) fb[j] = *reinterpret_cast<const bf16x8 *>(st + boff + j * 32 * RB + slot);
+  };
+
+  // The next step's DMAs go into the stage of step k - 1 as soon as the barrier frees
+  // it: waves 0-3 before their first MFMA, waves 4-7 (the other wave of each SIMD) one
+  // sub-step later, so that each SIMD always has a wave issuing MFMAs.
+  const bool early = w < 4;
+  issue(0);
+  for (int k = 0; k < nk; ++k) {
+    wait_vm<0>();                                              // this wave's share of step k
+    lds_barrier();                                             // all of step k; step k - 1 read
+    const unsigned char *st = lds + (k & 1) * kMStage;
+    const bool more = k + 1 < nk;
+    if (more && early) issue(k + 1);
+    bf16x8 fa[2][4], fb[2][2];
+    rd(st, 0, fa[0], fb[0]);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s == 1 && more && !early) issue(k + 1);
+      if (s < 3) rd(st, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s & 1][i], fb[s & 1][j], acc[i][j], 0, 0, 0);
+    }
+  }
+  lds_barrier();                                               // the stages are free
+
+  // ---------------------------------------------------------------- fused epilogue
+  // Per 32-row block i: the waves put their accumulators into an LDS tile ([2][32]
+  // rows of 256 floats; SwiGLU: the 128 products), then each wave handles whole
+  // rows, one 4-column piece per lane.  A lane's accumulator element e of block
+  // (i, j) is column l32 of row 8 (e / 4) + 4 h + e % 4.
+  const RedArgs &r = a.r;
+  float *T = reinterpret_cast<float *>(lds);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int rr = (e >> 2) * 8 + h * 4 + (e & 3);
+      float *trow = T + (wm * 32 + rr) * kMEpPitch;
+      if (MODE == G_GU) {
+        const float sc = rowinv[wm * 128 + i * 32 + rr];
+        const float gv = acc[i][0][e] * sc, uv = acc[i][1][e] * sc;
+        trow[wn * 32 + l32] = gv / (1.f + __expf(-gv)) * uv;
+      } else {
+        trow[wn * 64 + l32] = acc[i][0][e];
+        trow[wn * 64 + 32 + l32] = acc[i][1][e];
+      }
+    }
+    lds_barrier();
+    // 64 rows (two per wave-row half) x 64 four-column pieces; wave w takes rows w, w + 8, ...
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int er = w + 8 * it;                               // epilogue row 0..63
+      const int row = (er >> 5) * 128 + i * 32 + (er & 31);    // tile row
+      const bool rv = row < nvalid;
+      const long slot = slot0 + row;
+      const int tok = rv ? tok_of(r.idx, slot, a.N) : 0;
+      const float *trow = T + er * kMEpPitch;
+      const int c4 = lane * 4;                                 // column within the tile
+      if (MODE == G_GU) {
+        const int col = col0 + c4;
+        if (rv && c4 < TN && col < a.Nout) {
+          const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
+          *reinterpret_cast<uint2 *>(a.act + slot * a.Nout + col) = pack_bf16x4(v.x, v.y, v.z, v.w);
+        }
+        continue;
+      }
+      const int col = col0 + c4;
+      const bool cv = col < a.Nout;
+      const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
+      if (MODE == G_QKV) {
+        if (!rv || !cv) continue;
+        const float4 bs = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col));
+        float o[4] = {v.x + bs.x, v.y + bs.y, v.z + bs.z, v.w + bs.w};
+        uint16_t *dst;
+        if (col < r.qw) {
+          // rotate-half RoPE: the partner dims are half a head away in the same row
+          const int half = r.hd / 2, dim = col % r.hd;
+          const int pc4 = dim < half ? c4 + half : c4 - half;
+          const float4 pv = *reinterpret_cast<const float4 *>(trow + pc4);
+          const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
+          const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
+          const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half + dim % half;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float2 cs = rp[q];
+            o[q] = dim < half ? o[q] * cs.x - p[q] * cs.y : o[q] * cs.x + p[q] * cs.y;
+          }
+          dst = r.q + slot * r.qw + col;
+        } else {
+          const long crow = (long)b * r.S + r.cur_row0 + tok;
+          dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
+                                  : r.vc + crow * r.kw + (col - r.qw - r.kw);
+        }
+        *reinterpret_cast<uint2 *>(dst) = pack_bf16x4(o[0], o[1], o[2], o[3]);
+      } else if (MODE == G_O) {
+        float ss = 0.f;
+        if (rv && cv) {
+          const float4 xv = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.x + ((long)b * a.N + tok) * r.d + col));
+          const float4 hv = make_float4(v.x + xv.x, v.y + xv.y, v.z + xv.z, v.w + xv.w);
+          *reinterpret_cast<float4 *>(r.h1 + slot * r.d + col) = hv;
+          const float4 gn = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.gain + col));
+          *reinterpret_cast<uint2 *>(r.hb + slot * r.d + col) =
+              pack_bf16x4(hv.x * gn.x, hv.y * gn.y, hv.z * gn.z, hv.w * gn.w);
+          ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+        }
+        // the row's 256 columns are this wave's 64 lanes
+#pragma unroll
+        for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m);
+        if (rv && lane == 0 && nt < a.ss_parts) r.ssq[slot * a.ss_parts + nt] = ss;
+      } else {
+        if (!rv || !cv) continue;
+        const float4 hv = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + col);
+        *reinterpret_cast<uint2 *>(r.y + ((long)b * a.N + tok) * r.d + col) =
+            pack_bf16x4(hv.x + v.x, hv.y + v.y, hv.z + v.z, hv.w + v.w);
+      }
+    }
+    lds_barrier();                                             // the tile is free again
+  }
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -1080,6 +1338,24 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
   return FC_OK;
 }
 
+// Tiles of the large-M GEMM: 256 rows per tile and item, 256 output columns (SwiGLU:
+// 128 output columns, staged as gate and up rows).
+template <int MODE>
+fc_status run_mgemm(fc_ctx *ctx, hipStream_t st, const char *name, MArgs &g, int B) {
+  if (g.K % KS || g.Nout % 16)
+    return fail(FC_ERR_SHAPE, "%s: K %d must be a multiple of %d and N %d of 16", name, g.K, KS, g.Nout);
+  g.tpb = (g.N + MB - 1) / MB;
+  g.mtiles = B * g.tpb;
+  const int tn = MODE == G_GU ? MB / 2 : MB;
+  g.ntn = (g.Nout + tn - 1) / tn;
+  const long total = (long)g.mtiles * g.ntn;
+  if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
+  ProfScope ps(ctx, st, name);
+  hipLaunchKernelGGL(k_mgemm<MODE>, dim3((unsigned)total), dim3(512), 0, st, g);
+  FC_HIP_TRY(hipGetLastError());
+  return FC_OK;
+}
+
 }  // namespace
 
 namespace {
@@ -1110,6 +1386,10 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   const int cur_slot = (kv.head + kv.window - 1) % kv.window;
   const int cur_row0 = kv.text_tokens + cur_slot * N;
   const int want = std::max(ctx->num_cus, 1);
+  // thousands of gathered rows (several batch items of large frames) make the
+  // projections compute bound: square MFMA tiles with fused epilogues instead of the
+  // weight-streaming kernels and their split-K reductions
+  const bool big = rows >= kMGemmMinRows && (hd == 64 || hd == 128);
 
   // RoPE table for (hd, theta) over the cache length (rebuilt only when they change)
   if (ctx->rope_hd != hd || ctx->rope_theta != L.rope_theta || ctx->rope_seq < S) {
@@ -1140,16 +1420,24 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
                          idx, nrec, N, d, L.rms_eps, ctx->hb);
       FC_HIP_TRY(hipGetLastError());
     }
-    WArgs g{};
-    g.A = ctx->hb; g.W0 = L.w_qkv;
-    g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
-    g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
-    if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B)) != FC_OK) return rc;
-    r.splits = g.splits; r.ncols = qkv;
+    r.ncols = qkv;
     r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
-    ProfScope ps(ctx, st, "fc_red_qkv");
-    run_red(0, dim3((unsigned)rows, (qkv + 1023) / 1024), st, r);
-    FC_HIP_TRY(hipGetLastError());
+    if (big) {
+      MArgs g{};
+      g.A = ctx->hb; g.W0 = L.w_qkv;
+      g.K = d; g.Nout = qkv; g.N = N; g.r = r;
+      if ((rc = run_mgemm<G_QKV>(ctx, st, "fc_mgemm_qkv", g, B)) != FC_OK) return rc;
+    } else {
+      WArgs g{};
+      g.A = ctx->hb; g.W0 = L.w_qkv;
+      g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
+      g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
+      if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B)) != FC_OK) return rc;
+      r.splits = g.splits;
+      ProfScope ps(ctx, st, "fc_red_qkv");
+      run_red(0, dim3((unsigned)rows, (qkv + 1023) / 1024), st, r);
+      FC_HIP_TRY(hipGetLastError());
+    }
   }
 
   // 2. attention over the whole cache
@@ -1204,38 +1492,56 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   }
 
   // 3. O projection; reduction adds the residual -> h1 (float32) and its bf16 copy
-  {
+  r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq; r.gain = L.g_mlp; r.y = y_cur;
+  // sums of squares of h1 per row: per 1024 columns from the O reduction, per 256
+  // columns from the large-M epilogue
+  const int ss_parts = big ? (d + kMSsqCols - 1) / kMSsqCols : (d + 1023) / 1024;
+  if (big) {
+    MArgs g{};
+    g.A = ctx->attn; g.W0 = L.w_o;
+    g.K = nh * hd; g.Nout = d; g.N = N; g.ss_parts = ss_parts; g.r = r;
+    if ((rc = run_mgemm<G_O>(ctx, st, "fc_mgemm_o", g, B)) != FC_OK) return rc;
+  } else {
     WArgs g{};
     g.A = ctx->attn; g.W0 = L.w_o;
     g.K = nh * hd; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
     if ((rc = run_wgemm<G_O>(ctx, st, "fc_gemm_o", g, B)) != FC_OK) return rc;
-    r.splits = g.splits; r.ncols = d; r.h1 = ctx->h1; r.hb = ctx->hb; r.ssq = ctx->ssq;
-    r.gain = L.g_mlp;
+    r.splits = g.splits;
     ProfScope ps(ctx, st, "fc_red_o");
     run_red(1, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
     FC_HIP_TRY(hipGetLastError());
   }
 
-  // 4. gate/up on bf16(h1 * g_mlp); 1/rms from the O reduction's sums of squares is
-  //    applied to both sums, then SiLU(g) * u -> act (bf16)
-  {
+  // 4. gate/up on bf16(h1 * g_mlp); 1/rms from the sums of squares is applied to both
+  //    sums, then SiLU(g) * u -> act (bf16)
+  if (big) {
+    MArgs g{};
+    g.A = ctx->hb; g.W0 = L.w_gate; g.W1 = L.w_up;
+    g.K = d; g.Nout = ffn; g.N = N; g.ss_parts = ss_parts; g.act = ctx->act; g.r = r;
+    if ((rc = run_mgemm<G_GU>(ctx, st, "fc_mgemm_gateup", g, B)) != FC_OK) return rc;
+  } else {
     WArgs g{};
     g.A = ctx->hb; g.W0 = L.w_gate; g.W1 = L.w_up;
     g.K = d; g.Nout = ffn; g.N = N; g.idx = idx; g.nrec = nrec;
     g.rows = rows; g.act = ctx->act; g.eps = L.rms_eps;
-    g.ssq = ctx->ssq; g.ss_parts = (d + 1023) / 1024;
+    g.ssq = ctx->ssq; g.ss_parts = ss_parts;
     if ((rc = run_wgemm<G_GU>(ctx, st, "fc_gemm_gateup", g, B)) != FC_OK) return rc;
   }
 
-  // 5. down projection; reduction adds h1 and scatters bf16 rows into the output cache
-  {
+  // 5. down projection; adds h1 and scatters bf16 rows into the output cache
+  if (big) {
+    MArgs g{};
+    g.A = ctx->act; g.W0 = L.w_down;
+    g.K = ffn; g.Nout = d; g.N = N; g.r = r;
+    if ((rc = run_mgemm<G_DOWN>(ctx, st, "fc_mgemm_down", g, B)) != FC_OK) return rc;
+  } else {
     WArgs g{};
     g.A = ctx->act; g.W0 = L.w_down;
     g.K = ffn; g.Nout = d; g.N = N; g.idx = idx; g.nrec = nrec;
     g.part = ctx->part; g.rows = rows;
     if ((rc = run_wgemm<G_DOWN>(ctx, st, "fc_gemm_down", g, B)) != FC_OK) return rc;
-    r.splits = g.splits; r.ncols = d; r.y = y_cur;
+    r.splits = g.splits;
     ProfScope ps(ctx, st, "fc_red_down");
     run_red(2, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
     FC_HIP_TRY(hipGetLastError());

@@ -188,3 +188,31 @@ def test_cache_update_matches_oracle(fc, ctx, W, head, B):
         np.testing.assert_array_equal(vg[b].reshape(lay.S, kvw), vo)
         np.testing.assert_array_equal(yg[b], yo)
         assert mask[b].sum() > 0
+
+
+# ----------------------------------------------------------------- many gathered rows
+# With B * N >= 2048 token slots the projections run as square MFMA tiles with fused
+# epilogues (the batched-episode regime); these cases take that path.
+
+@pytest.fixture(scope="module")
+def ctx_big(fc):
+    c = fc.Context(fc.Caps(max_batch=3, max_height=896, max_width=896, max_tokens=1024,
+                           max_seq=4224, max_d_model=3584, max_ffn=18944, max_qkv=4608))
+    yield c
+    c.close()
+
+
+def test_batch_path_gqa_ragged(fc, ctx_big):
+    """GQA 7:1, head_dim 128, 1024 tokens per frame, three items: a ragged third
+    256-row tile (n = 646), a single partial tile (n = 103) and nothing recomputed."""
+    c = Case(GQA_SMALL, T=128, N=1024, W=2, head=1, B=3, seed=60)
+    worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(61, 1024, 37),
+                                  fcdata.random_reuse_ids(62, 1024, 90),
+                                  np.array([], np.int32)])
+    print(f"worst rel-L2 {worst:.2e}")
+
+
+def test_batch_path_mha64_full_recompute(fc, ctx_big):
+    """MHA with head_dim 64 (two heads per 128-column wave span), 0 % and 50 % reuse."""
+    c = Case(fcdata.TINY_LAYER, T=32, N=1024, W=1, head=0, B=2, seed=70)
+    c.check(fc, ctx_big, [fcdata.random_reuse_ids(71, 1024, 0), fcdata.random_reuse_ids(72, 1024, 50)])
