@@ -569,30 +569,35 @@ __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
 //     and up rows of the same 32 columns per wave and writes SiLU(g) * u; down adds h1
 //     and scatters the output rows.
 // Tiles are ordered so that the workgroups resident on one XCD at a time cover 4 M
-// tiles x 8 N tiles, which keeps their operand slabs in that XCD's L2.
+// tiles x 8 N tiles, which keeps their operand slabs in that XCD's L2; only the tiles
+// of the packed rows are mapped, evenly over the XCDs.
 constexpr int MB = 256;                     // tile rows and staged weight rows
 constexpr int kMStage = 2 * MB * RB;        // 64 KB per stage
 constexpr int kMSsqCols = 256;              // columns per sum-of-squares partial
 constexpr long kMGemmMinRows = 2048;        // token slots (B * N) that take this path
 constexpr int kMEpPitch = MB + 4;           // floats per row of the epilogue tile
+constexpr int kMMaxItems = 1024;            // batch items the packed row map holds
 
 struct MArgs {
   const uint16_t *A;              // bf16 activations, one row per slot
   const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
   int K, Nout, N;                 // Nout: output columns; N: token slots per item
-  int tpb, mtiles, ntn;           // M tiles per item, all M tiles, N tiles
+  int B, mtiles, ntn;             // items, M tiles (over the packed rows), N tiles
   int ss_parts;                   // O writes / SwiGLU reads this many partials per row
   uint16_t *act;                  // SwiGLU output [B*N][Nout]
   RedArgs r;                      // epilogue operands (as the reductions use them)
 };
 
-__device__ __forceinline__ void mtile_of(const MArgs &a, int bid, int total, int &mt, int &nt) {
-  const int L = xcd_tile(bid, total);
-  constexpr int GM = 4;
-  const int grp = L / (GM * a.ntn);
-  const int base = grp * GM;
-  const int gsz = min(GM, a.mtiles - base);
-  const int li = L - grp * GM * a.ntn;
+// Tile order over the V valid M tiles (known on the device only): each XCD takes a
+// contiguous range of tiles, walked in groups of 4 M tiles, N tile by N tile, so the
+// workgroups resident on one XCD share 4 activation slabs and about 8 weight slabs.
+constexpr int kMGroupM = 4;
+__device__ __forceinline__ void mtile_of(int V, int ntn, int bid, int &mt, int &nt) {
+  const int L = xcd_tile(bid, V * ntn);
+  const int grp = L / (kMGroupM * ntn);
+  const int base = grp * kMGroupM;
+  const int gsz = min(kMGroupM, V - base);
+  const int li = L - grp * kMGroupM * ntn;
   nt = li / gsz;
   mt = base + (li - nt * gsz);
 }
@@ -605,20 +610,53 @@ __device__ __forceinline__ float4 unpack_bf16x4(uint2 u) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
 }
 
+// The gathered rows of all items, packed: packed row p is slot b * N + (p - pre[b]) of
+// the item b with pre[b] <= p < pre[b + 1] (pre = exclusive prefix sums of the
+// recompute counts), so only the last tile of the whole batch is partly empty.
+__device__ __forceinline__ long packed_slot(const int *pre, int B, int N, int p, int &b) {
+  int lo = 0, hi = B - 1;                       // largest b with pre[b] <= p
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= p) lo = mid; else hi = mid - 1;
+  }
+  b = lo;
+  return (long)lo * N + (p - pre[lo]);
+}
+
 template <int MODE>
 __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kMStage];
   __shared__ float rowinv[MB];
-  const int total = a.mtiles * a.ntn;
-  int mt, nt;
-  mtile_of(a, blockIdx.x, total, mt, nt);
-  const int b = mt / a.tpb;
-  const int row0 = (mt % a.tpb) * MB;
-  const int nvalid = min(MB, n_valid(a.r.nrec, b, a.N) - row0);
-  if (nvalid <= 0) return;
-  const long slot0 = (long)b * a.N + row0;
+  __shared__ int pre[kMMaxItems + 1];
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  if (w == 0) {
+    // exclusive prefix sums of the recompute counts: each lane sums a run of items,
+    // then the runs are scanned across the wave
+    const int per = (a.B + 63) / 64, i0 = lane * per;
+    int run = 0;
+    for (int i = i0; i < min(i0 + per, a.B); ++i) run += n_valid(a.r.nrec, i, a.N);
+    int inc = run;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(inc, o);
+      if (lane >= o) inc += v;
+    }
+    int acc_run = inc - run;
+    for (int i = i0; i < min(i0 + per, a.B); ++i) {
+      pre[i] = acc_run;
+      acc_run += n_valid(a.r.nrec, i, a.N);
+    }
+    if (lane == 63) pre[a.B] = inc;
+  }
+  __syncthreads();
+  // the grid covers every slot; only the tiles of the packed rows run
+  const int V = (pre[a.B] + MB - 1) / MB;
+  if ((int)blockIdx.x >= V * a.ntn) return;
+  int mt, nt;
+  mtile_of(V, a.ntn, blockIdx.x, mt, nt);
+  const int row0 = mt * MB;
+  const int nvalid = min(MB, pre[a.B] - row0);
   const int wm = w & 1, wn = w >> 1;
   const int l32 = lane & 31, h = lane >> 5;
   const int nk = a.K / KS;
@@ -637,7 +675,8 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
     const int cs = (ch ^ swz8(r)) * 8;
     if (j < 32) {
       const int rr = r < nvalid ? r : nvalid - 1;              // clamp: never stored
-      gp[i] = a.A + (slot0 + rr) * a.K + cs;
+      int ib;
+      gp[i] = a.A + packed_slot(pre, a.B, a.N, row0 + rr, ib) * a.K + cs;
     } else {
       const uint16_t *M = a.W0;
       int col;
@@ -662,8 +701,11 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   if (MODE == G_GU && t < MB) {
     // 1/rms of each row from the O epilogue's partial sums of squares of h1
     float v = 0.f;
-    if (t < nvalid)
-      for (int c = 0; c < a.ss_parts; ++c) v += a.r.ssq[(slot0 + t) * a.ss_parts + c];
+    if (t < nvalid) {
+      int ib;
+      const long sl = packed_slot(pre, a.B, a.N, row0 + t, ib);
+      for (int c = 0; c < a.ss_parts; ++c) v += a.r.ssq[sl * a.ss_parts + c];
+    }
     rowinv[t] = 1.f / sqrtf(v / (float)a.K + a.r.eps);
   }
 
@@ -742,7 +784,8 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
       const int er = w + 8 * it;                               // epilogue row 0..63
       const int row = (er >> 5) * 128 + i * 32 + (er & 31);    // tile row
       const bool rv = row < nvalid;
-      const long slot = slot0 + row;
+      int b = 0;
+      const long slot = rv ? packed_slot(pre, a.B, a.N, row0 + row, b) : 0;
       const int tok = rv ? tok_of(r.idx, slot, a.N) : 0;
       const float *trow = T + er * kMEpPitch;
       const int c4 = lane * 4;                                 // column within the tile
@@ -1052,18 +1095,23 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[hb][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  // this wave's Q fragments, loaded from LDS once the tile is staged
+  bf16x8 qf[NS];
   // S^T = K Q^T for the 32 keys of buffer buf, online softmax, O^T += V^T P^T
   auto compute = [&](int buf, bool masked) {
-    f32x16 st;
+    // two independent accumulation chains over the k-steps, summed once
+    f32x16 st, st2;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) st[e] = 0.f;
+    for (int e = 0; e < 16; ++e) st[e] = st2[e] = 0.f;
     const int ksw = kswz<HD>(l32);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&Ks[buf][l32 * HD + 8 * ((2 * s + hi) ^ ksw)]);
-      const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv, st, 0, 0, 0);
+      if (s & 1) st2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], st2, 0, 0, 0);
+      else st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], st, 0, 0, 0);
     }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) st[e] += st2[e];
     float mloc = -INFINITY;
     if (masked) {
 #pragma unroll
@@ -1142,6 +1190,8 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
     }
   }
   lds_barrier();
+#pragma unroll
+  for (int s = 0; s < NS; ++s) qf[s] = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
   for (int kb = kb0; kb < kb1; kb += 2) {
     compute(0, needs_mask(kb));                       // buffer 0: block kb
     lds_barrier();
@@ -1338,14 +1388,15 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
   return FC_OK;
 }
 
-// Tiles of the large-M GEMM: 256 rows per tile and item, 256 output columns (SwiGLU:
-// 128 output columns, staged as gate and up rows).
+// Tiles of the large-M GEMM: 256 packed rows, 256 output columns (SwiGLU: 128 output
+// columns, staged as gate and up rows); tiles past the packed rows exit.
 template <int MODE>
 fc_status run_mgemm(fc_ctx *ctx, hipStream_t st, const char *name, MArgs &g, int B) {
   if (g.K % KS || g.Nout % 16)
     return fail(FC_ERR_SHAPE, "%s: K %d must be a multiple of %d and N %d of 16", name, g.K, KS, g.Nout);
-  g.tpb = (g.N + MB - 1) / MB;
-  g.mtiles = B * g.tpb;
+  if (B > kMMaxItems) return fail(FC_ERR_CAPACITY, "%s: more than %d batch items", name, kMMaxItems);
+  g.B = B;
+  g.mtiles = (int)(((long)B * g.N + MB - 1) / MB);      // packed rows need at most these
   const int tn = MODE == G_GU ? MB / 2 : MB;
   g.ntn = (g.Nout + tn - 1) / tn;
   const long total = (long)g.mtiles * g.ntn;
@@ -1389,7 +1440,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   // thousands of gathered rows (several batch items of large frames) make the
   // projections compute bound: square MFMA tiles with fused epilogues instead of the
   // weight-streaming kernels and their split-K reductions
-  const bool big = rows >= kMGemmMinRows && (hd == 64 || hd == 128);
+  const bool big = rows >= kMGemmMinRows && (hd == 64 || hd == 128) && B <= kMMaxItems;
 
   // RoPE table for (hd, theta) over the cache length (rebuilt only when they change)
   if (ctx->rope_hd != hd || ctx->rope_theta != L.rope_theta || ctx->rope_seq < S) {
