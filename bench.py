@@ -440,7 +440,7 @@ def bench_batch_episodes(fc, torch, frames_np, steps, L):
     kern = {}
     lay_us = 0.0
     for name in ("fc_spectra", "fc_grid", "fc_patchsim", "fc_topk", "fc_cache_update",
-                 "fc_gather_norm", "fc_mgemm_qkv", "fc_attn", "fc_attn_combine", "fc_mgemm_o",
+                 "fc_gather_norm", "fc_mgemm_qkv", "fc_rot_keys", "fc_attn", "fc_attn_combine", "fc_mgemm_o",
                  "fc_mgemm_gateup", "fc_mgemm_down"):
         tot, cnt = fc.fc_profile_read(ctx, name)
         if cnt:

@@ -76,7 +76,8 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->amp, c->pmean, c->penergy, c->pdot, c->qbuf, c->attn,
-                  c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq};
+                  c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
+                  c->krot};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -141,6 +142,8 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   const size_t cap = (size_t)96 << 20;
   ctx->part_elems = base * std::min<size_t>(fc::kMaxSplits, std::max<size_t>(1, cap / base));
   ctx->stage_elems = B * c.max_tokens * (size_t)c.max_qkv;
+  // a kv row is at most a third of a qkv row (n_heads >= n_kv_heads)
+  if ((long)rows >= fc::kBigRows) ctx->krot_elems = B * (size_t)c.max_seq * ((c.max_qkv + 2) / 3);
   fc_status st = FC_OK;
   if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np, "amp")) != FC_OK ||
       (st = dev_alloc(&ctx->pmean, B * 2 * np, "pmean")) != FC_OK ||
@@ -155,6 +158,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
       (st = dev_alloc(&ctx->part, ctx->part_elems, "partials")) != FC_OK ||
       (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||
       (st = dev_alloc(&ctx->stage, ctx->stage_elems, "stage")) != FC_OK ||
+      (ctx->krot_elems && (st = dev_alloc(&ctx->krot, ctx->krot_elems, "rotated keys")) != FC_OK) ||
       (st = fc::upload_select_tables()) != FC_OK) {
     free_ws(ctx);
     delete ctx;

@@ -29,6 +29,9 @@ constexpr int kBins = 100;          // unique DFT amplitude bins of a real 14x14
 constexpr int kMaxTokens = 1024;    // token-grid / top-K kernels hold one frame in LDS
 constexpr int kGemmBK = 64;        // K step of the layer GEMMs (dims must be multiples)
 constexpr int kMaxSplits = 16;
+// Layer calls with at least this many token slots (B * N) run the large-M path:
+// square MFMA tiles with fused epilogues and keys rotated once per call.
+constexpr long kBigRows = 2048;
 
 // ----------------------------------------------------------------------------- context
 struct ProfRec {
@@ -61,6 +64,8 @@ struct fc_ctx {
   double rope_theta = 0.0;
   uint16_t *stage = nullptr;   // [B][N][kv row] staging copy for the W == 1 remap
   size_t stage_elems = 0;
+  uint16_t *krot = nullptr;    // [B][S][kv row] rotated keys (many-row layer calls only)
+  size_t krot_elems = 0;
   // kernel timing
   bool prof = false;
   std::string prof_only;       // empty: time every kernel

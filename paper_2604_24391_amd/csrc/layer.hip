@@ -574,7 +574,6 @@ __global__ __launch_bounds__(256) void k_red_down(RedArgs r) {
 constexpr int MB = 256;                     // tile rows and staged weight rows
 constexpr int kMStage = 2 * MB * RB;        // 64 KB per stage
 constexpr int kMSsqCols = 256;              // columns per sum-of-squares partial
-constexpr long kMGemmMinRows = 2048;        // token slots (B * N) that take this path
 constexpr int kMEpPitch = MB + 4;           // floats per row of the epilogue tile
 constexpr int kMMaxItems = 1024;            // batch items the packed row map holds
 
@@ -876,11 +875,10 @@ __device__ __forceinline__ int key_pos(int row, int T, int N, int W, int head) {
 }
 
 
-// One staging task of a 32-key block (the same task count for keys and values):
-//   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of one key (pre-RoPE),
-//           the (cos, sin) pairs of those dims at the key's position, and the
-//           position itself (INT_MAX past the end of the cache);
-//   values: dims [4l, 4l + 4) of keys 4kg .. 4kg + 3.
+// Raw data of one staging task of a 32-key block (the same task count for keys and
+// values): two 8-dim key chunks, the (cos, sin) pairs of those dims at the key's
+// position when the keys are rotated on load, the position itself (INT_MAX past the
+// end of the cache), and 4 dims of 4 consecutive values.
 struct KVRaw {
   u32x4 k1, k2;
   u32x4 cs[4];
@@ -928,19 +926,20 @@ __device__ __forceinline__ int vq_word(int kg, int hd) {
 
 // Attention of one 32-query tile of kv head g over key blocks [kb0, kb1) of the cache.
 // Wave w < G handles query head g*G + w; the queries arrive rotated.  The waves past
-// them only move data: they fetch the raw K/V rows, rotate the keys and stage both
-// into one of two LDS buffers (keys rotated, values interleaved), with the raw loads
-// of block kb + 2 in flight while block kb is multiplied, so the cache latency is
-// paid once per split and the staging ALU work runs beside the MFMAs.
+// them only move data: they fetch the raw K/V rows, rotate the keys (unless the keys
+// come rotated) and stage both into one of two LDS buffers (keys rotated, values
+// interleaved), with the raw loads of block kb + 2 in flight while block kb is
+// multiplied, so the cache latency is paid once per split and the staging ALU work
+// runs beside the MFMAs.
 constexpr int kAttnStageWaves = 4;
-template <int HD, int G>
+template <int HD, int G, bool ROT>
 __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 16;   // k-steps of the QK^T product
   constexpr int NHB = HD / 32;  // 32-row blocks of the output
   constexpr int NL = kAttnStageWaves * 64;   // staging threads
   constexpr int CPK = HD / 16;  // key staging tasks per key
   constexpr int TASKS = 32 * CPK;
-  constexpr int TPT = (TASKS + NL - 1) / NL;
+  static_assert(TASKS <= NL, "one staging task per thread");
   constexpr int QLD = HD + 8;   // padded LDS row of the rotated queries
   static_assert(TASKS % 64 == 0, "staging tasks fill whole waves");
   static_assert(TASKS == 8 * (HD / 4), "key and value tasks pair up");
@@ -984,90 +983,114 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
   // only the current frame's keys can lie after a query; other blocks skip the mask
   const int cur_lo = a.T + ((a.head + a.W - 1) % a.W) * a.N, cur_hi = cur_lo + a.N;
 
-  // raw loads of block kb (clamped to the split's last block: the extra blocks the
-  // pipeline runs ahead are loaded but never multiplied)
-  auto fetch = [&](int kb, KVRaw (&R)[TPT]) {
-    kb = min(kb, kb1 - 1);
-#pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-      const int task = tl + i * NL;
-      if (task < TASKS) {
-        const int key = task / CPK, c = task - key * CPK;
-        const int row0 = kb * 32 + key;
-        const int row = min(row0, a.S - 1);
-        const int pos = key_pos(row, a.T, a.N, a.W, a.head);
-        R[i].pos = row0 < a.S ? pos : 0x7fffffff;
-        const uint16_t *kp = a.kc + kvbase + row * kvrow + 8 * c;
-        R[i].k1 = kv_load16(kp);
-        R[i].k2 = kv_load16(kp + HD / 2);
-        const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) R[i].cs[q] = kv_load16(rp + 2 * q);
-        const int kg = task / (HD / 4), l = task - kg * (HD / 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int vrow = min(kb * 32 + 4 * kg + r, a.S - 1);
-          R[i].v[r] = kv_load8(a.vc + kvbase + vrow * kvrow + 4 * l);
-        }
-      }
-    }
-  };
-  // the loads of R are complete once only the other set's loads (issued after R's)
-  // may still be in flight
-  auto settle = [&](KVRaw (&R)[TPT]) {
-    constexpr int kLater = 10 * TPT;
-    static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
-    __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
-#pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-      kv_anchor(R[i].k1); kv_anchor(R[i].k2);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) kv_anchor(R[i].cs[q]);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) kv_anchor(R[i].v[r]);
-    }
-  };
-  // rotate-half RoPE of the keys into Ks[buf]; values interleaved into Vq[buf]
-  auto stage = [&](const KVRaw (&R)[TPT], int buf) {
-#pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-      const int task = tl + i * NL;
-      if (task < TASKS) {
-        const int key = task / CPK, c = task - key * CPK;
-        U16x8 k1, k2;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const u32x4 q = R[i].cs[e >> 1];
-          const float cs = __uint_as_float(q[(e & 1) * 2]), sn = __uint_as_float(q[(e & 1) * 2 + 1]);
-          const uint32_t w1 = R[i].k1[e >> 1], w2 = R[i].k2[e >> 1];
-          const float x1 = (e & 1) ? hi_f(w1) : lo_f(w1), x2 = (e & 1) ? hi_f(w2) : lo_f(w2);
-          k1.v[e] = bf16_bits(x1 * cs - x2 * sn);
-          k2.v[e] = bf16_bits(x2 * cs + x1 * sn);
-        }
-        const int sw = kswz<HD>(key);
-        __bf16 *kr = &Ks[buf][key * HD];
-        *reinterpret_cast<U16x8 *>(kr + 8 * (c ^ sw)) = k1;
-        *reinterpret_cast<U16x8 *>(kr + 8 * ((c + HD / 16) ^ sw)) = k2;
-        if (c == 0) kpos[buf][key] = R[i].pos;
-        const int kg = task / (HD / 4), l = task - kg * (HD / 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int sh = 16 * (j & 1);
-          const uint32_t e0 = (R[i].v[0][j >> 1] >> sh) & 0xFFFFu, e1 = (R[i].v[1][j >> 1] >> sh) & 0xFFFFu;
-          const uint32_t e2 = (R[i].v[2][j >> 1] >> sh) & 0xFFFFu, e3 = (R[i].v[3][j >> 1] >> sh) & 0xFFFFu;
-          Vq[buf][vq_word<HD>(kg, 4 * l + j)] = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
-        }
-      }
-    }
-  };
   auto needs_mask = [&](int kb) {
     const int r0 = kb * 32, r1 = r0 + 32;
     return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
   };
 
   if (!qwave) {
-    // staging waves: fetch, rotate and stage block kb + 1 while block kb is multiplied
-    KVRaw ra[TPT], rb[TPT];
+    // ------------------------------------------------------------ staging waves
+    // Fetch, (rotate and) stage block kb + 1 while block kb is multiplied.  Everything
+    // that does not depend on the block is computed once here: a thread's task is
+    //   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of key `key`;
+    //   values: dims [4l, 4l + 4) of keys 4kg .. 4kg + 3,
+    // so per block only the row offset of the block is added.
+    const bool act = tl < TASKS;
+    const int tk = act ? tl : 0;
+    const int key = tk / CPK, c = tk - key * CPK;
+    const int kg = tk / (HD / 4), l = tk - kg * (HD / 4);
+    const int ksw = kswz<HD>(key);
+    const int kofs1 = key * HD + 8 * (c ^ ksw), kofs2 = key * HD + 8 * ((c + HD / 16) ^ ksw);
+    int vofs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) vofs[q] = vq_word<HD>(kg, 4 * l + q);
+    const uint16_t *kbase = a.kc + kvbase + 8 * c;
+    const uint16_t *vbase = a.vc + kvbase + 4 * l;
+    const int S = a.S;
+
+    // raw loads of block kb (clamped to the split's last block: the extra blocks the
+    // pipeline runs ahead are loaded but never multiplied)
+    auto fetch = [&](int kb, KVRaw &R) {
+      kb = min(kb, kb1 - 1);
+      const int rb = kb * 32;                          // first row of the block (uniform)
+      // positions: rows of one region (text, or one frame slot of the ring) share the
+      // shift from row to position
+      int delta = 0;
+      bool uniform_pos = rb + 32 <= a.T;
+      if (!uniform_pos && rb >= a.T) {
+        const int p0 = (rb - a.T) / a.N, p1 = (min(rb + 31, S - 1) - a.T) / a.N;
+        if (p0 == p1) {
+          int lg = p0 - a.head;
+          if (lg < 0) lg += a.W;
+          delta = (lg - p0) * a.N;
+          uniform_pos = true;
+        }
+      }
+      const int row0 = rb + key;
+      const int row = min(row0, S - 1);
+      const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.N, a.W, a.head);
+      R.pos = row0 < S ? pos : 0x7fffffff;
+      const uint16_t *kp = kbase + (long)row * kvrow;
+      R.k1 = kv_load16(kp);
+      R.k2 = kv_load16(kp + HD / 2);
+      if (ROT) {
+        const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) R.cs[q] = kv_load16(rp + 2 * q);
+      }
+      // every asm load is unconditional (no register set chosen at run time)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) R.v[r] = kv_load8(vbase + (long)min(rb + 4 * kg + r, S - 1) * kvrow);
+    };
+    // the loads of R are complete once only the other set's loads (issued after R's)
+    // may still be in flight
+    auto settle = [&](KVRaw &R) {
+      constexpr int kLater = ROT ? 10 : 6;
+      __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
+      kv_anchor(R.k1); kv_anchor(R.k2);
+      if (ROT) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) kv_anchor(R.cs[q]);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) kv_anchor(R.v[r]);
+    };
+    // rotate-half RoPE of the keys (unless they come rotated) into Ks[buf]; values
+    // interleaved into Vq[buf]: word q of the task holds dim 4l + q of its 4 keys
+    auto stage = [&](const KVRaw &R, int buf) {
+      if (!act) return;
+      __bf16 *kr = &Ks[buf][0];
+      if (ROT) {
+        U16x8 k1, k2;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const u32x4 q = R.cs[e >> 1];
+          const float cs = __uint_as_float(q[(e & 1) * 2]), sn = __uint_as_float(q[(e & 1) * 2 + 1]);
+          const uint32_t w1 = R.k1[e >> 1], w2 = R.k2[e >> 1];
+          const float x1 = (e & 1) ? hi_f(w1) : lo_f(w1), x2 = (e & 1) ? hi_f(w2) : lo_f(w2);
+          k1.v[e] = bf16_bits(x1 * cs - x2 * sn);
+          k2.v[e] = bf16_bits(x2 * cs + x1 * sn);
+        }
+        *reinterpret_cast<U16x8 *>(kr + kofs1) = k1;
+        *reinterpret_cast<U16x8 *>(kr + kofs2) = k2;
+      } else {
+        *reinterpret_cast<u32x4 *>(kr + kofs1) = R.k1;
+        *reinterpret_cast<u32x4 *>(kr + kofs2) = R.k2;
+      }
+      if (c == 0) kpos[buf][key] = R.pos;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // low (q even) or high (q odd) bf16 halves of word q / 2 of the 4 rows
+        const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t x = __builtin_amdgcn_perm(R.v[1][q >> 1], R.v[0][q >> 1], sel);
+        const uint32_t y = __builtin_amdgcn_perm(R.v[3][q >> 1], R.v[2][q >> 1], sel);
+        Vq[buf][vofs[q]] = make_uint2(x, y);
+      }
+    };
+
+    // two register sets with fixed roles (an asm load must never write a register set
+    // chosen at run time: the compiler would copy it before it lands)
+    KVRaw ra, rb;
     fetch(kb0, ra);
     fetch(kb0 + 1, rb);
     settle(ra);
@@ -1095,23 +1118,22 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[hb][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  // this wave's Q fragments, loaded from LDS once the tile is staged
-  bf16x8 qf[NS];
-  // S^T = K Q^T for the 32 keys of buffer buf, online softmax, O^T += V^T P^T
-  auto compute = [&](int buf, bool masked) {
-    // two independent accumulation chains over the k-steps, summed once
-    f32x16 st, st2;
+  // S^T = K Q^T for the 32 keys of buffer buf
+  auto qk = [&](int buf) {
+    f32x16 st;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) st[e] = st2[e] = 0.f;
+    for (int e = 0; e < 16; ++e) st[e] = 0.f;
     const int ksw = kswz<HD>(l32);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&Ks[buf][l32 * HD + 8 * ((2 * s + hi) ^ ksw)]);
-      if (s & 1) st2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], st2, 0, 0, 0);
-      else st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], st, 0, 0, 0);
+      const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
+      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv, st, 0, 0, 0);
     }
-#pragma unroll
-    for (int e = 0; e < 16; ++e) st[e] += st2[e];
+    return st;
+  };
+  // online softmax of the scores st of buffer buf, then O^T += V^T P^T
+  auto softmax_pv = [&](f32x16 st, int buf, bool masked) {
     float mloc = -INFINITY;
     if (masked) {
 #pragma unroll
@@ -1190,12 +1212,10 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
     }
   }
   lds_barrier();
-#pragma unroll
-  for (int s = 0; s < NS; ++s) qf[s] = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
   for (int kb = kb0; kb < kb1; kb += 2) {
-    compute(0, needs_mask(kb));                       // buffer 0: block kb
+    softmax_pv(qk(0), 0, needs_mask(kb));                          // buffer 0: block kb
     lds_barrier();
-    if (kb + 1 < kb1) compute(1, needs_mask(kb + 1)); // buffer 1: block kb + 1
+    if (kb + 1 < kb1) softmax_pv(qk(1), 1, needs_mask(kb + 1));    // buffer 1: block kb + 1
     lds_barrier();
   }
 
@@ -1226,6 +1246,38 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
       a.pl[blk * 32 + l32] = l_tot;
     }
   }
+}
+
+// Rotate-half RoPE of every cached key at its position in the current step, raw
+// cache -> rotated copy (same rounding as when the attention kernel rotates on load).
+// For many query tiles per item this replaces one rotation per (key, tile) by one per
+// key.  One thread per 8-dim pair of chunks (dims 8c.. and hd/2 + 8c..) of a key row.
+__global__ __launch_bounds__(256) void k_rot_keys(const uint16_t *__restrict__ kc,
+                                                  const float2 *__restrict__ rope,
+                                                  uint16_t *__restrict__ kr, int S, int nkv,
+                                                  int hd, int T, int N, int W, int head) {
+  const int cpr = hd / 16;                              // chunk pairs per head row
+  const long task = (long)blockIdx.x * 256 + threadIdx.x;
+  const int b = blockIdx.y;
+  if (task >= (long)S * nkv * cpr) return;
+  const int c = (int)(task % cpr);
+  const long rh = task / cpr;                           // row * nkv + kv head
+  const int row = (int)(rh / nkv);
+  const int pos = key_pos(row, T, N, W, head);
+  const long off = ((long)b * S * nkv + rh) * hd + 8 * c;
+  const U16x8 x1 = *reinterpret_cast<const U16x8 *>(kc + off);
+  const U16x8 x2 = *reinterpret_cast<const U16x8 *>(kc + off + hd / 2);
+  const float2 *rp = rope + (long)pos * (hd / 2) + 8 * c;
+  U16x8 y1, y2;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float2 cs = rp[e];
+    const float a1 = bf2f(x1.v[e]), a2 = bf2f(x2.v[e]);
+    y1.v[e] = bf16_bits(a1 * cs.x - a2 * cs.y);
+    y2.v[e] = bf16_bits(a2 * cs.x + a1 * cs.y);
+  }
+  *reinterpret_cast<U16x8 *>(kr + off) = y1;
+  *reinterpret_cast<U16x8 *>(kr + off + hd / 2) = y2;
 }
 
 // Merges the split-KV partials of one (32-query tile, head): each split's sum is
@@ -1388,6 +1440,14 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
   return FC_OK;
 }
 
+template <int HD, int G>
+void launch_attn(dim3 grid, hipStream_t st, const AttnArgs &a, bool rot) {
+  if (rot)
+    hipLaunchKernelGGL((k_attn<HD, G, true>), grid, dim3((G + kAttnStageWaves) * 64), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_attn<HD, G, false>), grid, dim3((G + kAttnStageWaves) * 64), 0, st, a);
+}
+
 // Tiles of the large-M GEMM: 256 packed rows, 256 output columns (SwiGLU: 128 output
 // columns, staged as gate and up rows); tiles past the packed rows exit.
 template <int MODE>
@@ -1440,7 +1500,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   // thousands of gathered rows (several batch items of large frames) make the
   // projections compute bound: square MFMA tiles with fused epilogues instead of the
   // weight-streaming kernels and their split-K reductions
-  const bool big = rows >= kMGemmMinRows && (hd == 64 || hd == 128) && B <= kMMaxItems;
+  const bool big = rows >= kBigRows && (hd == 64 || hd == 128) && B <= kMMaxItems;
 
   // RoPE table for (hd, theta) over the cache length (rebuilt only when they change)
   if (ctx->rope_hd != hd || ctx->rope_theta != L.rope_theta || ctx->rope_seq < S) {
@@ -1516,18 +1576,31 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     const int G = nh / nkv;
     a.tiles = tiles;
     dim3 grid(tiles * nkv * a.splits);
+    // with many query tiles per item, every cached key is rotated once into a copy
+    // instead of once per (key, tile) inside the attention kernel
+    const long kvw = (long)nkv * hd;
+    const bool prerot = big && ctx->krot && (size_t)B * S * kvw <= ctx->krot_elems;
+    if (prerot) {
+      ProfScope ps(ctx, st, "fc_rot_keys");
+      const long tasks = (long)S * nkv * (hd / 16);
+      hipLaunchKernelGGL(k_rot_keys, dim3((unsigned)((tasks + 255) / 256), B), dim3(256), 0, st,
+                         kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, N, kv.window,
+                         kv.head);
+      FC_HIP_TRY(hipGetLastError());
+      a.kc = ctx->krot;
+    }
     {
       ProfScope ps(ctx, st, "fc_attn");
       if (hd == 128 && G == 7)
-        hipLaunchKernelGGL((k_attn<128, 7>), grid, dim3((7 + kAttnStageWaves) * 64), 0, st, a);
+        launch_attn<128, 7>(grid, st, a, !prerot);
       else if (hd == 128 && G == 1)
-        hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3((1 + kAttnStageWaves) * 64), 0, st, a);
+        launch_attn<128, 1>(grid, st, a, !prerot);
       else if (hd == 64 && G == 1)
-        hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3((1 + kAttnStageWaves) * 64), 0, st, a);
+        launch_attn<64, 1>(grid, st, a, !prerot);
       else if (hd == 64 && G == 2)
-        hipLaunchKernelGGL((k_attn<64, 2>), grid, dim3((2 + kAttnStageWaves) * 64), 0, st, a);
+        launch_attn<64, 2>(grid, st, a, !prerot);
       else if (hd == 128 && G == 4)
-        hipLaunchKernelGGL((k_attn<128, 4>), grid, dim3((4 + kAttnStageWaves) * 64), 0, st, a);
+        launch_attn<128, 4>(grid, st, a, !prerot);
       else
         return fail(FC_ERR_UNSUPPORTED, "attention: head_dim %d with %d query heads per kv head", hd, G);
       FC_HIP_TRY(hipGetLastError());
