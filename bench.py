@@ -54,6 +54,12 @@ def main():
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--batch-steps", type=int, default=3,
                     help="timed steps of the batched-episode workload (0: skip it)")
+    ap.add_argument("--serial-frames", action="store_true",
+                    help="generate the batched-episode frames in this process (under a "
+                         "profiler, which initialises the GPU before the program starts)")
+    ap.add_argument("--batch-only", action="store_true",
+                    help="run only the batched-episode workload and print its record (for "
+                         "profiling that workload on its own)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -72,8 +78,13 @@ def main():
     # the batched-episode frames come from a pool of forked workers, which must start
     # before this process touches the GPU
     batch_frames = None
-    if not args.no_extras and args.batch_steps > 0:
-        batch_frames = batch_episode_frames(args.batch_steps + 3)
+    if args.batch_only or (not args.no_extras and args.batch_steps > 0):
+        batch_frames = batch_episode_frames(max(1, args.batch_steps) + 3, args.serial_frames)
+    if args.batch_only:
+        torch.cuda.set_device(0)
+        rec = bench_batch_episodes(fc, torch, batch_frames, max(1, args.batch_steps), args.layers)
+        print(json.dumps(rec), flush=True)
+        return
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -325,16 +336,20 @@ def _episode_worker(args):
     return fcdata.episode_frames(seed, size=fcdata.BATCH["size"], n_frames=n_frames)
 
 
-def batch_episode_frames(n_frames):
+def batch_episode_frames(n_frames, serial=False):
     """[n_frames, 16, 3, 896, 896] float32: 16 independent seeded trajectories, each
-    over its own texture, generated in parallel by forked workers."""
+    over its own texture, generated in parallel by forked workers (or in this process)."""
     import multiprocessing as mp
     import fcdata
     t0 = time.time()
     E = fcdata.BATCH["episodes"]
-    workers = max(1, min(E, len(os.sched_getaffinity(0))))
-    with mp.get_context("fork").Pool(workers) as pool:
-        eps = pool.map(_episode_worker, [(5000 + e, n_frames) for e in range(E)])
+    jobs = [(5000 + e, n_frames) for e in range(E)]
+    workers = 1 if serial else max(1, min(E, len(os.sched_getaffinity(0))))
+    if workers == 1:
+        eps = [_episode_worker(j) for j in jobs]
+    else:
+        with mp.get_context("fork").Pool(workers) as pool:
+            eps = pool.map(_episode_worker, jobs)
     out = np.ascontiguousarray(np.stack(eps, axis=1))
     log(f"batched-episode frames ready in {time.time() - t0:.1f}s ({E} episodes x {n_frames} "
         f"frames, {workers} workers)")
