@@ -164,3 +164,21 @@ def test_boundary_errors(fc, ctx):
     with pytest.raises(fc.FcError) as e:
         fc.fc_select(ctx, fc.SelectParams(patch=16), None, torch.zeros(1, 3, 224, 224, device="cuda"), out)
     assert e.value.status == 6
+
+
+def test_batched_episode_frames_896(fc):
+    """The batched-episode shape: 896x896 frames, 4096 patches, 2x2 merge -> 1024 tokens
+    on a 32x32 grid, two independent trajectories (each over its own texture) in one
+    call, consecutive steps."""
+    c = fc.Context(fc.Caps(max_batch=2, max_height=896, max_width=896, max_tokens=1024,
+                           max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+    try:
+        eps = [fcdata.episode_frames(5000 + e, size=896, n_frames=2) for e in range(2)]
+        prev = np.stack([e[0] for e in eps])
+        cur = np.stack([e[1] for e in eps])
+        o, margins = compare(fc, c, fc.SelectParams(merge=2), prev, cur)
+        assert o["n_recompute"].shape == (2,)
+        print(f"n_recompute {o['n_recompute'].tolist()}, min top-K margin "
+              f"{min(m['topk'] for m in margins):.2e}")
+    finally:
+        c.close()
