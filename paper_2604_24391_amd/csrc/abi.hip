@@ -145,7 +145,9 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   // a kv row is at most a third of a qkv row (n_heads >= n_kv_heads)
   if ((long)rows >= fc::kBigRows) ctx->krot_elems = B * (size_t)c.max_seq * ((c.max_qkv + 2) / 3);
   fc_status st = FC_OK;
-  if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np, "amp")) != FC_OK ||
+  // amplitudes in 16-patch chunks of a patch row (the last chunk of a row padded)
+  const size_t np16 = (size_t)(c.max_height / fc::kPatch) * ((c.max_width / fc::kPatch + 15) / 16) * 16;
+  if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np16, "amp")) != FC_OK ||
       (st = dev_alloc(&ctx->pmean, B * 2 * np, "pmean")) != FC_OK ||
       (st = dev_alloc(&ctx->penergy, B * np, "penergy")) != FC_OK ||
       (st = dev_alloc(&ctx->pdot, B * 3 * np, "pdot")) != FC_OK ||

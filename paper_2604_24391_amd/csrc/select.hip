@@ -6,7 +6,8 @@
 //              staged in LDS, then per patch: the 14x14 DFT amplitude (Eq. 3-2)
 //              with real/even folding in float32, the patch mean, and for the
 //              current frame the orthonormal DCT-II high-pass energy (Eqs. 3-4,
-//              3-5) in float64.
+//              3-5) in float64, as the patch energy minus that of the removed
+//              3 x 3 low block (the transform is orthonormal).
 //   k_grid     one workgroup per frame pair: token-grid mean-luma maps, their
 //              2-D DFTs (float64), global amplitude similarity (Eq. 3-3) and the
 //              migration gate, spectral entropy and the reuse budget (Eqs. 3-6,
@@ -53,10 +54,17 @@ __device__ __forceinline__ double bin_weight(int bin) {
   return (bin == 0 || bin == 7 || bin == 8 || bin == 15) ? 1.0 : 2.0;
 }
 
+// Amplitudes are stored per 16-patch chunk of a patch row, [b*2 + f][chunk][bin][16],
+// chunk = pi * ncx + pj / 16 with ncx = ceil(Gpw / 16): one k_spectra workgroup writes
+// its whole 6.4 KB block with full-line stores (a bin-major layout cost it 64-B pieces).
+__device__ __forceinline__ size_t amp_chunk(int bf, int pi, int cx, int Gph, int ncx) {
+  return ((size_t)bf * Gph * ncx + (size_t)pi * ncx + cx) * NB * 16;
+}
+
 // ------------------------------------------------------------------------------- k_spectra
 // Grid: x = 16-patch chunk of a patch row, y = patch row, z = 2 * b + frame (0 prev,
 // 1 cur).  Outputs (workspace):
-//   amp[((b*2 + f) * NB + bin) * Np + patch]  float32 amplitude, unique bins:
+//   amp[amp_chunk(b*2 + f, pi, chunk) + bin * 16 + slot]  float32 amplitude, unique bins:
 //       bins 0..7   = (u = 0..7,  v = 0),  bins 8..15 = (u = 0..7, v = 7),
 //       bins 16..99 = (u = 0..13, v = 1..6)   (the rest follow from A(u,v) = A(-u,-v));
 //   pmean[(b*2 + f) * Np + patch]  float64 mean luma;
@@ -75,44 +83,50 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   const int t = threadIdx.x;
   const float *frame = f ? cur : prev;
 
+  const int ncx = (Gpw + PW - 1) / PW;
+  float4 *ablk = reinterpret_cast<float4 *>(amp + amp_chunk(b * 2 + f, pi, blockIdx.x, Gph, ncx));
   if (frame == nullptr) {  // no previous frame: an all-zero frame
-    for (int e = t; e < pw * NB; e += blockDim.x) {
-      int p = e % pw, bin = e / pw;
-      amp[((size_t)(b * 2 + f) * NB + bin) * Np + pi * Gpw + j0 + p] = 0.f;
-    }
+    for (int e = t; e < NB * PW / 4; e += blockDim.x) ablk[e] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (t < pw) pmean[(size_t)(b * 2 + f) * Np + pi * Gpw + j0 + t] = 0.0;
     return;
   }
 
   // LDS: the luma tile, then (after every row has been read into registers) the
-  // row-stage results in the same space, so that six workgroups fit on a CU
+  // row-stage results in the same space.  The luma tile is [patch][row][15] doubles:
+  // the row-stage thread of (patch, row) is thread 14 patch + row, so a 15-double
+  // row pitch puts the 32 lanes of a half-wave on 64 distinct banks.  The row DFTs
+  // have a 120-float2 patch pitch for the same reason in the column stage.
+  constexpr int YP = P + 1;                 // luma row pitch (doubles)
+  constexpr int RP = 120;                   // row-DFT patch pitch (float2), 112 used
   struct RowStage {
-    float2 row[PW][P][8];      // row DFTs, v = 0..7
+    float2 row[PW][RP];        // row DFTs [patch][row * 8 + v], v = 0..7
     double r3[PW][3][P];       // row DCTs, k < 3
-    double hp[PW][P];          // per-row high-pass energy of columns k >= 3
+    double ss[PW][P];          // per-row sums of squares of the luma
     double rs[PW][P];          // per-row luma sums
-    double col[PW][3];         // column-DCT energies of k < 3, u >= 3
+    double col[PW][3];         // low-block energies: sum over u < 3 of D(u, k)^2
   };
-  constexpr int kTileBytes = P * (PW * P + 1) * (int)sizeof(double);
+  constexpr int kTileBytes = PW * P * YP * (int)sizeof(double);
   constexpr int kLdsBytes = kTileBytes > (int)sizeof(RowStage) ? kTileBytes : (int)sizeof(RowStage);
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
-  double(*sY)[PW * P + 1] = reinterpret_cast<double(*)[PW * P + 1]>(lds);
+  double *sY = reinterpret_cast<double *>(lds);
   RowStage &rsg = *reinterpret_cast<RowStage *>(lds);
-  float2(*sRow)[P][8] = rsg.row;
+  float2(*sRow)[RP] = rsg.row;
   double(*sR)[3][P] = rsg.r3;
-  double(*sHp)[P] = rsg.hp;
+  double(*sSs)[P] = rsg.ss;
   double(*sRs)[P] = rsg.rs;
   double(*sCol)[3] = rsg.col;
 
-  // ---- load 14 rows x (pw*14) px of R, G, B (all loads issued before any use); luma
-  //      in float64 (BT.601)
+  // ---- 14 rows x (pw*14) px of R, G, B per strip, luma in float64 (BT.601)
   const int cw = pw * P;
   const size_t plane = (size_t)H * W;
-  const float *base = frame + (size_t)b * 3 * plane + (size_t)(pi * P) * W + j0 * P;
-  if ((W & 3) == 0 && (cw & 3) == 0) {
-    const int q4 = cw >> 2;
-    constexpr int kIt = (P * PW * P / 4 + 255) / 256;   // float4 positions per thread
-    float4 r[kIt], g[kIt], bl[kIt];
+  const bool vec = (W & 3) == 0 && (cw & 3) == 0;
+  const int q4 = cw >> 2;
+  constexpr int kIt = (P * PW * P / 4 + 255) / 256;     // float4 positions per thread
+  auto strip_base = [&](int pi) {
+    return frame + (size_t)b * 3 * plane + (size_t)(pi * P) * W + j0 * P;
+  };
+  auto load = [&](int pi, float4 (&r)[kIt], float4 (&g)[kIt], float4 (&bl)[kIt]) {
+    const float *base = strip_base(pi);
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
       const int e = min(t + 256 * i, P * q4 - 1);
@@ -122,24 +136,39 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
       g[i] = *reinterpret_cast<const float4 *>(rp + plane);
       bl[i] = *reinterpret_cast<const float4 *>(rp + 2 * plane);
     }
+  };
+  auto luma = [&](int pi, const float4 (&r)[kIt], const float4 (&g)[kIt], const float4 (&bl)[kIt]) {
+    if (vec) {
 #pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-      const int e = t + 256 * i;
-      if (e < P * q4) {
-        const int y = e / q4, q = e - y * q4;
-        sY[y][4 * q + 0] = 0.299 * (double)r[i].x + 0.587 * (double)g[i].x + 0.114 * (double)bl[i].x;
-        sY[y][4 * q + 1] = 0.299 * (double)r[i].y + 0.587 * (double)g[i].y + 0.114 * (double)bl[i].y;
-        sY[y][4 * q + 2] = 0.299 * (double)r[i].z + 0.587 * (double)g[i].z + 0.114 * (double)bl[i].z;
-        sY[y][4 * q + 3] = 0.299 * (double)r[i].w + 0.587 * (double)g[i].w + 0.114 * (double)bl[i].w;
+      for (int i = 0; i < kIt; ++i) {
+        const int e = t + 256 * i;
+        if (e < P * q4) {
+          const int y = e / q4, q = e - y * q4;
+          const float rr[4] = {r[i].x, r[i].y, r[i].z, r[i].w};
+          const float gg[4] = {g[i].x, g[i].y, g[i].z, g[i].w};
+          const float bb[4] = {bl[i].x, bl[i].y, bl[i].z, bl[i].w};
+          int pp = (4 * q) / P, xx = 4 * q - pp * P;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            sY[(pp * P + y) * YP + xx] = 0.299 * (double)rr[c] + 0.587 * (double)gg[c] + 0.114 * (double)bb[c];
+            if (++xx == P) { xx = 0; ++pp; }
+          }
+        }
+      }
+    } else {
+      const float *base = strip_base(pi);
+      for (int e = t; e < P * cw; e += blockDim.x) {
+        int y = e / cw, x = e - y * cw;
+        const float *rp = base + (size_t)y * W + x;
+        const int pp = x / P;
+        sY[(pp * P + y) * YP + (x - pp * P)] =
+            0.299 * (double)rp[0] + 0.587 * (double)rp[plane] + 0.114 * (double)rp[2 * plane];
       }
     }
-  } else {
-    for (int e = t; e < P * cw; e += blockDim.x) {
-      int y = e / cw, x = e - y * cw;
-      const float *rp = base + (size_t)y * W + x;
-      sY[y][x] = 0.299 * (double)rp[0] + 0.587 * (double)rp[plane] + 0.114 * (double)rp[2 * plane];
-    }
-  }
+  };
+  float4 ra[kIt], ga[kIt], ba[kIt];
+  if (vec) load(pi, ra, ga, ba);
+  luma(pi, ra, ga, ba);
   __syncthreads();
 
   // ---- row stage: one thread per (patch, row)
@@ -147,7 +176,7 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   const int p = rowt ? t / P : 0, y = rowt ? t - p * P : 0;
   double v[P];
 #pragma unroll
-  for (int x = 0; x < P; ++x) v[x] = rowt ? sY[y][p * P + x] : 0.0;
+  for (int x = 0; x < P; ++x) v[x] = rowt ? sY[(p * P + y) * YP + x] : 0.0;
   __syncthreads();   // the tile is dead from here on: its space holds the row stage
   if (rowt) {
     double rs = 0.0;
@@ -173,28 +202,28 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
         re = fmaf(ev[x], c_cos14[(k * x) % P], re);
         im = fmaf(-od[x], c_sin14[(k * x) % P], im);
       }
-      sRow[p][y][k] = make_float2(re, im);
+      sRow[p][y * 8 + k] = make_float2(re, im);
     }
     if (f == 1) {
-      // DCT-II along x (float64): C[k][13 - x] = (-1)^k C[k][x].
-      double s7[7], d7[7];
+      // The orthonormal DCT preserves energy (Parseval), so the high-pass energy is
+      // sum p^2 minus the energy of the removed low block (u < 3 and v < 3): only the
+      // row DCT coefficients k < 3 are needed (float64; C[k][13 - x] = (-1)^k C[k][x]).
+      double s7[7], d7[7], ss = 0.0;
 #pragma unroll
       for (int x = 0; x < 7; ++x) {
         s7[x] = v[x] + v[P - 1 - x];
         d7[x] = v[x] - v[P - 1 - x];
       }
-      double hp = 0.0;
 #pragma unroll
-      for (int k = 0; k < P; ++k) {
+      for (int x = 0; x < P; ++x) ss = fma(v[x], v[x], ss);
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
         double r = 0.0;
 #pragma unroll
         for (int x = 0; x < 7; ++x) r = fma(c_dct14[k * P + x], (k & 1) ? d7[x] : s7[x], r);
-        if (k < 3)
-          sR[p][k][y] = r;
-        else
-          hp = fma(r, r, hp);  // columns v >= 3 keep every u: Parseval along y
+        sR[p][k][y] = r;
       }
-      sHp[p][y] = hp;
+      sSs[p][y] = ss;
     }
   }
   __syncthreads();
@@ -205,7 +234,7 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   const bool colt = t < pw * 8;
   float2 z[P];
 #pragma unroll
-  for (int y = 0; y < P; ++y) z[y] = colt ? sRow[t >> 3][y][t & 7] : make_float2(0.f, 0.f);
+  for (int y = 0; y < P; ++y) z[y] = colt ? sRow[t >> 3][y * 8 + (t & 7)] : make_float2(0.f, 0.f);
   __syncthreads();
   float(*sAmp)[PW] = reinterpret_cast<float(*)[PW]>(&rsg.row[0][0][0]);
   static_assert(sizeof(float) * NB * PW <= sizeof(RowStage::row), "amplitudes fit in the row DFTs");
@@ -243,7 +272,7 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
       }
     }
   } else if (f == 1 && t >= 128 && t < 128 + pw * 3) {
-    // DCT along y of columns v < 3, rows u >= 3 only (the kept part of the block).
+    // DCT along y of the row coefficients k < 3, rows u < 3: the removed low block.
     const int p = (t - 128) / 3, k = (t - 128) % 3;
     double r[P];
 #pragma unroll
@@ -256,7 +285,7 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
     }
     double acc = 0.0;
 #pragma unroll
-    for (int u = 3; u < P; ++u) {
+    for (int u = 0; u < 3; ++u) {
       double dd = 0.0;
 #pragma unroll
       for (int y = 0; y < 7; ++y) dd = fma(c_dct14[u * P + y], (u & 1) ? d7[y] : s7[y], dd);
@@ -267,11 +296,9 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
   __syncthreads();
 
   {
-    const size_t obase = ((size_t)(b * 2 + f) * NB) * Np + pi * Gpw + j0;
-    for (int e = t; e < NB * pw; e += blockDim.x) {
-      const int bin = e / pw, p = e - bin * pw;
-      amp[obase + (size_t)bin * Np + p] = sAmp[bin][p];
-    }
+    // the block in LDS is already [bin][16]; slots past pw are never read
+    const float4 *src = reinterpret_cast<const float4 *>(&sAmp[0][0]);
+    for (int e = t; e < NB * PW / 4; e += blockDim.x) ablk[e] = src[e];
   }
   if (t < pw) {
     const int patch = pi * Gpw + j0 + t;
@@ -282,9 +309,9 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
     if (f == 1) {
       double e = 0.0;
 #pragma unroll
-      for (int y = 0; y < P; ++y) e += sHp[t][y];
-      e += sCol[t][0] + sCol[t][1] + sCol[t][2];
-      penergy[(size_t)b * Np + patch] = e;
+      for (int y = 0; y < P; ++y) e += sSs[t][y];
+      e -= sCol[t][0] + sCol[t][1] + sCol[t][2];
+      penergy[(size_t)b * Np + patch] = fmax(e, 0.0);
     }
   }
 }
@@ -573,15 +600,16 @@ __global__ __launch_bounds__(256) void k_patchsim(const float *__restrict__ amp,
   const int di = shift[b * 2 + 0], dj = shift[b * 2 + 1];
   const int si = pi / m + di, sj = pj / m + dj;
   const bool al = si >= 0 && si < Gh && sj >= 0 && sj < Gw;
-  const int ps = al ? (pi + m * di) * Gpw + pj + m * dj : pc;
-  const float *ac = amp + (size_t)(b * 2 + 1) * NB * Np;
-  const float *ap = amp + (size_t)(b * 2 + 0) * NB * Np;
+  const int spi = al ? pi + m * di : pi, spj = al ? pj + m * dj : pj;
+  const int ncx = (Gpw + PW - 1) / PW;
+  const float *ac = amp + amp_chunk(b * 2 + 1, pi, pj / PW, Gph, ncx) + (pj % PW);
+  const float *ap = amp + amp_chunk(b * 2 + 0, spi, spj / PW, Gph, ncx) + (spj % PW);
   float x[kSimBinsPerWave], y[kSimBinsPerWave];
 #pragma unroll
   for (int i = 0; i < kSimBinsPerWave; ++i) {
     const int bin = w * kSimBinsPerWave + i;
-    x[i] = ac[(size_t)bin * Np + pc];
-    y[i] = ap[(size_t)bin * Np + ps];
+    x[i] = ac[bin * PW];
+    y[i] = ap[bin * PW];
   }
   double dot = 0.0, n1 = 0.0, n2 = 0.0;
 #pragma unroll
