@@ -180,6 +180,31 @@ def layer_partial(x_cur_u16: np.ndarray, recompute_idx: np.ndarray, k_cache_u16:
     return y, kc, vc
 
 
+def layer_partial_sampled(x_cur_u16: np.ndarray, recompute_idx: np.ndarray,
+                          sample_idx: np.ndarray, k_cache_u16: np.ndarray,
+                          v_cache_u16: np.ndarray, lay: Layout, wt: dict, shape):
+    """The partial-recompute layer call for one batch item, with the block's output
+    computed only for `sample_idx` (a subset of recompute_idx): the K/V rows of every
+    recomputed token are still computed and written first, since every sampled query
+    attends to them.  For large shapes, where computing every output row is too slow.
+    Returns float32 (y rows [len(sample_idx), d], k_cache', v_cache')."""
+    idx = np.asarray(recompute_idx, dtype=np.int64)
+    smp = np.asarray(sample_idx, dtype=np.int64)
+    assert np.isin(smp, idx).all(), "samples must be recomputed tokens"
+    nh, nkv, hd = shape.n_heads, shape.n_kv, shape.hd
+    kc, vc = f32(k_cache_u16).copy(), f32(v_cache_u16).copy()
+    x = f32(x_cur_u16)
+    hn = rmsnorm(x[idx], f32(wt["g_attn"]), shape.eps)
+    kv_rows = slice(nh * hd, (nh + 2 * nkv) * hd)
+    kv = _proj(hn, wt["w_qkv"][kv_rows]) + f32(wt["b_qkv"])[kv_rows]
+    rows = lay.cur_rows(idx)
+    kc[rows] = kv[:, :nkv * hd].reshape(-1, nkv, hd)
+    vc[rows] = kv[:, nkv * hd:].reshape(-1, nkv, hd)
+    y, kc, vc = block_rows(x[smp], lay.cur_positions(smp), kc, vc, lay.row_positions(),
+                           lay.cur_rows(smp), wt, shape)
+    return y, kc, vc
+
+
 def cache_update(k_cache: np.ndarray, v_cache: np.ndarray, y_prev: np.ndarray,
                  y_cur: np.ndarray, shift, reuse_mask: np.ndarray, gw: int, lay: Layout):
     """Token-cache preparation for a new step (window already advanced in `lay`).

@@ -216,3 +216,63 @@ def test_batch_path_mha64_full_recompute(fc, ctx_big):
     """MHA with head_dim 64 (two heads per 128-column wave span), 0 % and 50 % reuse."""
     c = Case(fcdata.TINY_LAYER, T=32, N=1024, W=1, head=0, B=2, seed=70)
     c.check(fc, ctx_big, [fcdata.random_reuse_ids(71, 1024, 0), fcdata.random_reuse_ids(72, 1024, 50)])
+
+
+@pytest.fixture(scope="module")
+def ctx_episodes(fc):
+    c = fc.Context(fc.Caps(max_batch=16, max_height=896, max_width=896, max_tokens=1024,
+                           max_seq=4224, max_d_model=3584, max_ffn=18944, max_qkv=4608))
+    yield c
+    c.close()
+
+
+def test_batched_episode_qwen_layer_sampled(fc, ctx_episodes):
+    """The batched-episode launch at full size: the Qwen2.5-VL-7B-shaped layer over 16
+    items x 1024 tokens, 128 text + 4 frames = 4224 cached positions, about 35 % reuse
+    per item, so the packed 256-row tiles straddle items.  For items 0, 7 and 15 the
+    K/V rows of every recomputed token and the outputs of six sampled tokens are
+    checked against the oracle; every row that must not change, byte for byte."""
+    sh = fcdata.QWEN_LAYER
+    B, N = 16, 1024
+    lay = ol.Layout(T=128, N=N, W=4, head=1)
+    S = lay.S
+    wt = fcdata.layer_weights(80, sh)
+    rng = np.random.default_rng(81)
+    x = fcdata.bf16_round(rng.standard_normal((B, N, sh.d), dtype=np.float32))
+    k = fcdata.bf16_round(rng.standard_normal((B, S, sh.n_kv, sh.hd), dtype=np.float32))
+    v = fcdata.bf16_round(rng.standard_normal((B, S, sh.n_kv, sh.hd), dtype=np.float32))
+    y_prev = fcdata.bf16_round(rng.standard_normal((B, N, sh.d), dtype=np.float32))
+    ids = [fcdata.random_reuse_ids(90 + b, N, 35) for b in range(B)]
+    idx = np.full((B, N), -1, np.int32)
+    nrec = np.array([len(i) for i in ids], np.int32)
+    for b in range(B):
+        idx[b, :nrec[b]] = ids[b]
+    kc, vc, y = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v), fcutil.bf16_gpu(y_prev)
+    kv = fc.KVCache(kc, vc, lay.T, N, lay.W, lay.head)
+    fc.fc_layer_forward(ctx_episodes, fcutil.layer_desc(sh, fcutil.weights_gpu(wt)), kv,
+                        fcutil.bf16_gpu(x), torch.from_numpy(idx).cuda(),
+                        torch.from_numpy(nrec).cuda(), y)
+    torch.cuda.synchronize()
+    yg, kg, vg = fcutil.bf16_np(y), fcutil.bf16_np(kc), fcutil.bf16_np(vc)
+    for b in (0, 7, 15):
+        n = len(ids[b])
+        pick = np.unique(np.concatenate([[0, n - 1], rng.choice(n, 4, replace=False)]))
+        smp = ids[b][pick]
+        yo, ko, vo = ol.layer_partial_sampled(x[b], ids[b], smp, k[b], v[b], lay, wt, sh)
+        rows = lay.cur_rows(ids[b])
+        other = np.setdiff1d(np.arange(S), rows)
+        np.testing.assert_array_equal(kg[b][other], k[b][other])
+        np.testing.assert_array_equal(vg[b][other], v[b][other])
+        keep = np.setdiff1d(np.arange(N), ids[b])
+        np.testing.assert_array_equal(yg[b][keep], y_prev[b][keep])
+        ek = fcutil.rel_l2(fcdata.bf16_to_f32(kg[b][rows]), ko[rows])
+        ev = fcutil.rel_l2(fcdata.bf16_to_f32(vg[b][rows]), vo[rows])
+        ys = fcdata.bf16_to_f32(yg[b][smp])
+        xs = fcdata.bf16_to_f32(x[b][smp])
+        ey = fcutil.rel_l2(ys, yo)
+        rnd = np.linalg.norm(fcdata.bf16_to_f32(fcdata.bf16_round(yo)) - yo)
+        print(f"item {b} n={n}: y {ey:.2e}  y-x {fcutil.rel_l2(ys - xs, yo - xs):.2e}  "
+              f"k {ek:.2e}  v {ev:.2e}")
+        for e in (ey, ek, ev):
+            assert e <= fcutil.LAYER_RTOL
+        assert np.linalg.norm(ys - yo) <= fcutil.LAYER_RTOL * np.linalg.norm(yo - xs) + 2 * rnd

@@ -246,3 +246,18 @@ def test_cache_update_copies_source_rows():
         np.testing.assert_array_equal(y2[other], y_cur[other])
         untouched = np.setdiff1d(np.arange(lay.S), lay.cur_rows(np.array(list(src))))
         np.testing.assert_array_equal(k2[untouched], k[untouched])
+
+
+def test_sampled_rows_equal_the_full_partial_call():
+    """The sampled-output form (every recomputed token's K/V, outputs for a subset)
+    gives the same K/V cache and, on the sampled rows, the same outputs as the full
+    partial call; it is what the full-size GPU check uses."""
+    sh = SMALL
+    lay, wt, st, kc, vc, y_prev, _ = _setup(sh=sh)
+    ids = fcdata.random_reuse_ids(17, lay.N, 40)
+    y, k, v = ol.layer_partial(st["x_cur"], ids, kc, vc, y_prev, lay, wt, sh)
+    smp = ids[[0, len(ids) // 2, len(ids) - 1]]
+    ys, ks, vs = ol.layer_partial_sampled(st["x_cur"], ids, smp, kc, vc, lay, wt, sh)
+    np.testing.assert_allclose(ks, k, rtol=1e-5, atol=1e-6)
+    np.testing.assert_allclose(vs, v, rtol=1e-5, atol=1e-6)
+    np.testing.assert_allclose(ys, y[smp], rtol=1e-4, atol=1e-5)
