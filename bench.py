@@ -267,8 +267,6 @@ def bench_select_batch(fc, ctx, torch):
     for _ in range(3):
         fc.fc_select(ctx, prm, prev, cur, out)
     torch.cuda.synchronize()
-    fc.fc_profile_read(ctx, None, reset=True)
-    fc.fc_profile_enable(ctx, True)
     reps = 20
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
@@ -276,8 +274,14 @@ def bench_select_batch(fc, ctx, torch):
         fc.fc_select(ctx, prm, prev, cur, out)
     e1.record()
     torch.cuda.synchronize()
-    fc.fc_profile_enable(ctx, False)
     call_us = e0.elapsed_time(e1) * 1e3 / reps
+    # per-kernel breakdown in a separate pass (events around every launch)
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    for _ in range(reps):
+        fc.fc_select(ctx, prm, prev, cur, out)
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
     frame_bytes = 2 * B * 3 * H * W * 4
     out_bytes = B * 1024 * (4 + 8 + 1 + 4 + 1)
     kern = {}

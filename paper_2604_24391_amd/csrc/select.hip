@@ -433,6 +433,69 @@ __device__ void dft2(double2 *X, double2 *Z, const double2 *twh, const double2 *
   }
 }
 
+// 2-D FFT of a power-of-two [Gh][Gw] complex grid (both sides <= 64) with every line
+// inside one wave: a row (then a column) sits in consecutive lanes and its radix-2
+// decimation-in-frequency butterflies exchange values by lane shuffles, so the whole
+// transform needs two barriers.  X holds the input and receives the result in natural
+// order; T (>= Gw * (Gh + 1) elements) holds the row-transformed grid transposed,
+// with a padded pitch.  out[u][v] = sum_y sum_x in[y][x] w_h^(u y) w_w^(v x),
+// w = exp(-2 pi i / G) (conjugate for INV); tw*[k] = exp(-2 pi i k / G).
+template <int G, bool INV>
+__device__ __forceinline__ double2 fft_lanes(double2 x, int i, const double2 *tw) {
+  constexpr int LG = G == 1 ? 0 : __builtin_ctz(G);
+  // the twiddle of every stage is loaded up front (one LDS round trip)
+  double2 w[LG > 0 ? LG : 1];
+#pragma unroll
+  for (int st = 0; st < LG; ++st) {
+    const int h = G >> (st + 1);
+    w[st] = tw[(i & (h - 1)) * (G / (2 * h))];
+    if (INV) w[st].y = -w[st].y;
+  }
+#pragma unroll
+  for (int st = 0; st < LG; ++st) {
+    const int h = G >> (st + 1);
+    const double px = __shfl_xor(x.x, h), py = __shfl_xor(x.y, h);
+    // upper half of a butterfly: (a - b) w, a = partner; lower half: a + b
+    const bool up = i & h;
+    const double dx = px - x.x, dy = py - x.y;
+    const double ux = dx * w[st].x - dy * w[st].y, uy = dx * w[st].y + dy * w[st].x;
+    x = up ? make_double2(ux, uy) : make_double2(x.x + px, x.y + py);
+  }
+  return x;                                  // lane i holds frequency bitrev(i)
+}
+template <int G, bool INV>
+__device__ __forceinline__ double2 fft_lanes_rt(double2 x, int i, int g, const double2 *tw) {
+  switch (g) {
+    case 64: return fft_lanes<64, INV>(x, i, tw);
+    case 32: return fft_lanes<32, INV>(x, i, tw);
+    case 16: return fft_lanes<16, INV>(x, i, tw);
+    case 8: return fft_lanes<8, INV>(x, i, tw);
+    case 4: return fft_lanes<4, INV>(x, i, tw);
+    case 2: return fft_lanes<2, INV>(x, i, tw);
+    default: return x;
+  }
+}
+template <bool INV>
+__device__ void fft2_wave(double2 *X, double2 *T, const double2 *twh, const double2 *tww, int Gh,
+                          int Gw) {
+  const int t = threadIdx.x, M = Gh * Gw, TP = Gh + 1;
+  const int lw = __ffs(Gw) - 1, lh = __ffs(Gh) - 1;
+  if (t < M) {
+    const int row = t >> lw, col = t & (Gw - 1);
+    const double2 r = fft_lanes_rt<0, INV>(X[t], col, Gw, tww);
+    const int v = lw ? (int)(__brev((unsigned)col) >> (32 - lw)) : 0;
+    T[v * TP + row] = r;
+  }
+  __syncthreads();
+  if (t < M) {
+    const int v = t >> lh, y = t & (Gh - 1);
+    const double2 r = fft_lanes_rt<0, INV>(T[v * TP + y], y, Gh, twh);
+    const int u = lh ? (int)(__brev((unsigned)y) >> (32 - lh)) : 0;
+    X[u * Gw + v] = r;
+  }
+  __syncthreads();
+}
+
 struct GridParams {
   int Gph, Gpw, m;
   double tau_mig, lambda_, alpha_min, alpha_max, alpha_fixed;
@@ -450,9 +513,9 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
                                                        double *__restrict__ scalars,
                                                        int32_t *__restrict__ counts) {
   constexpr int NW = kGridThreads / 64;
-  __shared__ double2 A[kMaxTokens], Bg[kMaxTokens], C[kMaxTokens];
+  __shared__ double2 A[kMaxTokens], Bg[kMaxTokens], C[kMaxTokens + 64];
   __shared__ double2 twh[kMaxTokens], tww[kMaxTokens];
-  __shared__ double red[NW * 5 + 5];
+  __shared__ double red[NW * 7 + 7];
   __shared__ double bestv[NW];
   __shared__ int besti[NW];
   const int b = blockIdx.x;
@@ -462,6 +525,7 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
   const int Np = g.Gph * g.Gpw;
   const bool act = t < M;
   const int I = t / Gw, J = t - I * Gw;
+  const bool wave_fft = (Gh & (Gh - 1)) == 0 && (Gw & (Gw - 1)) == 0 && Gh <= 64 && Gw <= 64;
 
   if (t < Gh) {
     double s, c;
@@ -490,10 +554,15 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
     energy[(size_t)b * M + t] = et;
   }
   __syncthreads();
-  // forward 2-D transforms of both maps
-  __syncthreads();
-  dft2<false>(A, C, twh, tww, Gh, Gw);
-  dft2<false>(Bg, C, twh, tww, Gh, Gw);
+  // forward 2-D transforms of both maps, each on its own (a zero map must give an
+  // exactly zero spectrum: the Sim_freq of Eq. 3-3 is defined as 0 there)
+  if (wave_fft) {
+    fft2_wave<false>(A, C, twh, tww, Gh, Gw);
+    fft2_wave<false>(Bg, C, twh, tww, Gh, Gw);
+  } else {
+    dft2<false>(A, C, twh, tww, Gh, Gw);
+    dft2<false>(Bg, C, twh, tww, Gh, Gw);
+  }
   double pc = 0.0, pp = 0.0, cp = 0.0, mag = 0.0;
   if (act) {
     const double2 Fc = A[t], Fp = Bg[t];
@@ -509,24 +578,26 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
 
   // ---- Eq. 3-3 on the global spectra, Eq. 3-6 entropy of the current frame, the
   //      largest cross-power magnitude, token-energy mean and spread (Eq. 4-3)
-  double r1[5] = {mag, cp, pc, pp, act ? et : 0.0};
-  block_reduce<NW, 5, 1>(r1, red);
+  // one reduction: the entropy of P = pc / nc is ln nc - (sum pc ln pc) / nc, and the
+  // energy spread comes from the sums of e and e^2
+  double r1[7] = {mag, cp, pc, pp, act ? et : 0.0, act ? et * et : 0.0,
+                  (act && pc > 0.0) ? pc * log(pc) : 0.0};
+  block_reduce<NW, 7, 1>(r1, red);
   const double mx = r1[0], dot = r1[1], nc = r1[2], np_ = r1[3];
   const double mu = r1[4] / (double)M;
-  double r2[2] = {0.0, act ? (et - mu) * (et - mu) : 0.0};
-  if (act && nc > 0.0) {
-    const double pr = pc / nc;
-    if (pr > 0.0) r2[0] = -pr * log(pr);
-  }
-  block_reduce<NW, 2, 0>(r2, red);
-  const double ent = r2[0], ev = r2[1];
+  const double ent = nc > 0.0 ? log(nc) - r1[6] / nc : 0.0;
+  const double ev = fmax(r1[5] - r1[4] * mu, 0.0);
 
   // ---- Eq. 4-1: normalised cross-power, inverse transform (real part), first maximum
   if (act) {
     const double2 x = Bg[t];
     Bg[t] = (mx > 0.0 && mag > 1e-9 * mx) ? make_double2(x.x / mag, x.y / mag) : make_double2(0.0, 0.0);
   }
-  dft2<true>(Bg, C, twh, tww, Gh, Gw);
+  __syncthreads();
+  if (wave_fft)
+    fft2_wave<true>(Bg, C, twh, tww, Gh, Gw);
+  else
+    dft2<true>(Bg, C, twh, tww, Gh, Gw);
   const double re = act ? Bg[t].x / (double)M : -INFINITY;
   // first maximum in row-major order: (value, index) max with the lower index on ties
   double bv = re;
