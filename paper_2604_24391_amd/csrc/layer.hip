@@ -932,18 +932,21 @@ __device__ __forceinline__ int vq_word(int kg, int hd) {
 // multiplied, so the cache latency is paid once per split and the staging ALU work
 // runs beside the MFMAs.
 constexpr int kAttnStageWaves = 4;
-template <int HD, int G, bool ROT>
-__global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a) {
+template <int HD, int G, bool ROT, int QB, int SW>
+__global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 16;   // k-steps of the QK^T product
   constexpr int NHB = HD / 32;  // 32-row blocks of the output
-  constexpr int NL = kAttnStageWaves * 64;   // staging threads
+  constexpr int NL = SW * 64;   // staging threads
   constexpr int CPK = HD / 16;  // key staging tasks per key
   constexpr int TASKS = 32 * CPK;
-  static_assert(TASKS <= NL, "one staging task per thread");
+  constexpr int TPT = (TASKS + NL - 1) / NL;   // staging tasks per thread
+  constexpr int QR = 32 * QB;   // query rows of a tile: QB blocks of 32 per query wave
   constexpr int QLD = HD + 8;   // padded LDS row of the rotated queries
   static_assert(TASKS % 64 == 0, "staging tasks fill whole waves");
   static_assert(TASKS == 8 * (HD / 4), "key and value tasks pair up");
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[G][32 * QLD];
+  static_assert(TPT == 1 || TPT * NL == TASKS, "tasks divide over the staging threads");
+  static_assert(QB == 1 || QB == 2, "one or two query blocks per wave");
+  __shared__ __attribute__((aligned(16))) __bf16 Qs[G][QR * QLD];
   __shared__ __attribute__((aligned(16))) __bf16 Ks[2][32 * HD];
   __shared__ __attribute__((aligned(16))) uint2 Vq[2][8 * HD];
   __shared__ int kpos[2][32];
@@ -956,24 +959,18 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
   const int qt = lt % tiles;
   const int g = (lt / tiles) % a.nkv;
   const int sp = lt / (tiles * a.nkv);
-  const int tiles_per_b = (a.N + 31) / 32;
+  const int tiles_per_b = (a.N + QR - 1) / QR;
   const int b = qt / tiles_per_b;
-  const int j0 = (qt % tiles_per_b) * 32;
+  const int j0 = (qt % tiles_per_b) * QR;
   const int n = n_valid(a.nrec, b, a.N);
   if (j0 >= n) return;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
-  // waves below G multiply (one query head each); the two waves past them fetch, rotate
+  // waves below G multiply (one query head each); the waves past them fetch, rotate
   // and stage the next key block meanwhile, so loads and staging overlap the MFMAs
   const bool qwave = w < G;
   const int tl = t - G * 64;          // staging thread index (staging waves only)
   const int h = g * G + (qwave ? w : 0);
-
-  const int j = j0 + l32;
-  const bool qvalid = j < n;
-  const long slot = (long)b * a.N + (qvalid ? j : j0);
-  const int tok = tok_of(a.idx, slot, a.N);
-  const int qpos = a.T + (a.W - 1) * a.N + tok;
 
   const int nkb = (a.S + 31) / 32;
   const int kb0 = sp * a.kb_per_split;
@@ -991,26 +988,34 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
   if (!qwave) {
     // ------------------------------------------------------------ staging waves
     // Fetch, (rotate and) stage block kb + 1 while block kb is multiplied.  Everything
-    // that does not depend on the block is computed once here: a thread's task is
+    // that does not depend on the block is computed once here: task i of a thread is
     //   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of key `key`;
     //   values: dims [4l, 4l + 4) of keys 4kg .. 4kg + 3,
     // so per block only the row offset of the block is added.
-    const bool act = tl < TASKS;
-    const int tk = act ? tl : 0;
-    const int key = tk / CPK, c = tk - key * CPK;
-    const int kg = tk / (HD / 4), l = tk - kg * (HD / 4);
-    const int ksw = kswz<HD>(key);
-    const int kofs1 = key * HD + 8 * (c ^ ksw), kofs2 = key * HD + 8 * ((c + HD / 16) ^ ksw);
-    int vofs[4];
+    bool act[TPT];
+    int key[TPT], c[TPT], kg[TPT], kofs1[TPT], kofs2[TPT], vofs[TPT][4];
+    const uint16_t *kbase[TPT], *vbase[TPT];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) vofs[q] = vq_word<HD>(kg, 4 * l + q);
-    const uint16_t *kbase = a.kc + kvbase + 8 * c;
-    const uint16_t *vbase = a.vc + kvbase + 4 * l;
+    for (int i = 0; i < TPT; ++i) {
+      act[i] = tl + i * NL < TASKS;
+      const int tk = act[i] ? tl + i * NL : 0;
+      key[i] = tk / CPK;
+      c[i] = tk - key[i] * CPK;
+      kg[i] = tk / (HD / 4);
+      const int l = tk - kg[i] * (HD / 4);
+      const int ksw = kswz<HD>(key[i]);
+      kofs1[i] = key[i] * HD + 8 * (c[i] ^ ksw);
+      kofs2[i] = key[i] * HD + 8 * ((c[i] + HD / 16) ^ ksw);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) vofs[i][q] = vq_word<HD>(kg[i], 4 * l + q);
+      kbase[i] = a.kc + kvbase + 8 * c[i];
+      vbase[i] = a.vc + kvbase + 4 * l;
+    }
     const int S = a.S;
 
     // raw loads of block kb (clamped to the split's last block: the extra blocks the
     // pipeline runs ahead are loaded but never multiplied)
-    auto fetch = [&](int kb, KVRaw &R) {
+    auto fetch = [&](int kb, KVRaw (&R)[TPT]) {
       kb = min(kb, kb1 - 1);
       const int rb = kb * 32;                          // first row of the block (uniform)
       // positions: rows of one region (text, or one frame slot of the ring) share the
@@ -1026,71 +1031,82 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
           uniform_pos = true;
         }
       }
-      const int row0 = rb + key;
-      const int row = min(row0, S - 1);
-      const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.N, a.W, a.head);
-      R.pos = row0 < S ? pos : 0x7fffffff;
-      const uint16_t *kp = kbase + (long)row * kvrow;
-      R.k1 = kv_load16(kp);
-      R.k2 = kv_load16(kp + HD / 2);
-      if (ROT) {
-        const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) R.cs[q] = kv_load16(rp + 2 * q);
+      for (int i = 0; i < TPT; ++i) {
+        const int row0 = rb + key[i];
+        const int row = min(row0, S - 1);
+        const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.N, a.W, a.head);
+        R[i].pos = row0 < S ? pos : 0x7fffffff;
+        const uint16_t *kp = kbase[i] + (long)row * kvrow;
+        R[i].k1 = kv_load16(kp);
+        R[i].k2 = kv_load16(kp + HD / 2);
+        if (ROT) {
+          const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c[i];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) R[i].cs[q] = kv_load16(rp + 2 * q);
+        }
+        // every asm load is unconditional (no register set chosen at run time)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          R[i].v[r] = kv_load8(vbase[i] + (long)min(rb + 4 * kg[i] + r, S - 1) * kvrow);
       }
-      // every asm load is unconditional (no register set chosen at run time)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) R.v[r] = kv_load8(vbase + (long)min(rb + 4 * kg + r, S - 1) * kvrow);
     };
     // the loads of R are complete once only the other set's loads (issued after R's)
     // may still be in flight
-    auto settle = [&](KVRaw &R) {
-      constexpr int kLater = ROT ? 10 : 6;
+    auto settle = [&](KVRaw (&R)[TPT]) {
+      constexpr int kLater = (ROT ? 10 : 6) * TPT;
+      static_assert(kLater < 64, "vmcnt holds at most 63 outstanding loads");
       __builtin_amdgcn_s_waitcnt(0x3F70 | (kLater & 0xF) | ((kLater >> 4) << 14));
-      kv_anchor(R.k1); kv_anchor(R.k2);
-      if (ROT) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) kv_anchor(R.cs[q]);
+      for (int i = 0; i < TPT; ++i) {
+        kv_anchor(R[i].k1); kv_anchor(R[i].k2);
+        if (ROT) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) kv_anchor(R[i].cs[q]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) kv_anchor(R[i].v[r]);
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) kv_anchor(R.v[r]);
     };
     // rotate-half RoPE of the keys (unless they come rotated) into Ks[buf]; values
-    // interleaved into Vq[buf]: word q of the task holds dim 4l + q of its 4 keys
-    auto stage = [&](const KVRaw &R, int buf) {
-      if (!act) return;
+    // interleaved into Vq[buf]: word q of a task holds dim 4l + q of its 4 keys
+    auto stage = [&](const KVRaw (&R)[TPT], int buf) {
       __bf16 *kr = &Ks[buf][0];
-      if (ROT) {
-        U16x8 k1, k2;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const u32x4 q = R.cs[e >> 1];
-          const float cs = __uint_as_float(q[(e & 1) * 2]), sn = __uint_as_float(q[(e & 1) * 2 + 1]);
-          const uint32_t w1 = R.k1[e >> 1], w2 = R.k2[e >> 1];
-          const float x1 = (e & 1) ? hi_f(w1) : lo_f(w1), x2 = (e & 1) ? hi_f(w2) : lo_f(w2);
-          k1.v[e] = bf16_bits(x1 * cs - x2 * sn);
-          k2.v[e] = bf16_bits(x2 * cs + x1 * sn);
+      for (int i = 0; i < TPT; ++i) {
+        if (!act[i]) continue;
+        if (ROT) {
+          U16x8 k1, k2;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const u32x4 q = R[i].cs[e >> 1];
+            const float cs = __uint_as_float(q[(e & 1) * 2]), sn = __uint_as_float(q[(e & 1) * 2 + 1]);
+            const uint32_t w1 = R[i].k1[e >> 1], w2 = R[i].k2[e >> 1];
+            const float x1 = (e & 1) ? hi_f(w1) : lo_f(w1), x2 = (e & 1) ? hi_f(w2) : lo_f(w2);
+            k1.v[e] = bf16_bits(x1 * cs - x2 * sn);
+            k2.v[e] = bf16_bits(x2 * cs + x1 * sn);
+          }
+          *reinterpret_cast<U16x8 *>(kr + kofs1[i]) = k1;
+          *reinterpret_cast<U16x8 *>(kr + kofs2[i]) = k2;
+        } else {
+          *reinterpret_cast<u32x4 *>(kr + kofs1[i]) = R[i].k1;
+          *reinterpret_cast<u32x4 *>(kr + kofs2[i]) = R[i].k2;
         }
-        *reinterpret_cast<U16x8 *>(kr + kofs1) = k1;
-        *reinterpret_cast<U16x8 *>(kr + kofs2) = k2;
-      } else {
-        *reinterpret_cast<u32x4 *>(kr + kofs1) = R.k1;
-        *reinterpret_cast<u32x4 *>(kr + kofs2) = R.k2;
-      }
-      if (c == 0) kpos[buf][key] = R.pos;
+        if (c[i] == 0) kpos[buf][key[i]] = R[i].pos;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // low (q even) or high (q odd) bf16 halves of word q / 2 of the 4 rows
-        const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t x = __builtin_amdgcn_perm(R.v[1][q >> 1], R.v[0][q >> 1], sel);
-        const uint32_t y = __builtin_amdgcn_perm(R.v[3][q >> 1], R.v[2][q >> 1], sel);
-        Vq[buf][vofs[q]] = make_uint2(x, y);
+        for (int q = 0; q < 4; ++q) {
+          // low (q even) or high (q odd) bf16 halves of word q / 2 of the 4 rows
+          const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+          const uint32_t x = __builtin_amdgcn_perm(R[i].v[1][q >> 1], R[i].v[0][q >> 1], sel);
+          const uint32_t y = __builtin_amdgcn_perm(R[i].v[3][q >> 1], R[i].v[2][q >> 1], sel);
+          Vq[buf][vofs[i][q]] = make_uint2(x, y);
+        }
       }
     };
 
     // two register sets with fixed roles (an asm load must never write a register set
     // chosen at run time: the compiler would copy it before it lands)
-    KVRaw ra, rb;
+    KVRaw ra[TPT], rb[TPT];
     fetch(kb0, ra);
     fetch(kb0 + 1, rb);
     settle(ra);
@@ -1112,78 +1128,106 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
   }
 
   // ------------------------------------------------------------ query waves
-  f32x16 o[NHB];
+  // query block qb of this wave: queries j0 + 32 qb + l32
+  bool qvalid[QB];
+  long slot[QB];
+  int qpos[QB];
 #pragma unroll
-  for (int hb = 0; hb < NHB; ++hb)
+  for (int qb = 0; qb < QB; ++qb) {
+    const int j = j0 + 32 * qb + l32;
+    qvalid[qb] = j < n;
+    slot[qb] = (long)b * a.N + (qvalid[qb] ? j : j0);
+    qpos[qb] = a.T + (a.W - 1) * a.N + tok_of(a.idx, slot[qb], a.N);
+  }
+  f32x16 o[QB][NHB];
+  float m_run[QB], l_run[QB];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[hb][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-  // S^T = K Q^T for the 32 keys of buffer buf
-  auto qk = [&](int buf) {
-    f32x16 st;
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) st[e] = 0.f;
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[qb][hb][e] = 0.f;
+  }
+  // S^T = K Q^T for the 32 keys of buffer buf, each key fragment serving every query
+  // block (independent accumulation chains)
+  auto qk = [&](int buf, f32x16 (&st)[QB]) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) st[qb][e] = 0.f;
     const int ksw = kswz<HD>(l32);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&Ks[buf][l32 * HD + 8 * ((2 * s + hi) ^ ksw)]);
-      const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[w][l32 * QLD + 16 * s + 8 * hi]);
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv, st, 0, 0, 0);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[w][(32 * qb + l32) * QLD + 16 * s + 8 * hi]);
+        st[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv, st[qb], 0, 0, 0);
+      }
     }
-    return st;
   };
-  // online softmax of the scores st of buffer buf, then O^T += V^T P^T
-  auto softmax_pv = [&](f32x16 st, int buf, bool masked) {
-    float mloc = -INFINITY;
-    if (masked) {
+  // online softmax of the scores of buffer buf, then O^T += V^T P^T, each value
+  // fragment serving every query block
+  auto softmax_pv = [&](f32x16 (&st)[QB], int buf, bool masked) {
+    bf16x8 pb[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mloc = -INFINITY;
+      if (masked) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = (e >> 2) * 8 + hi * 4 + (e & 3);
+          st[qb][e] = (kpos[buf][key] <= qpos[qb]) ? st[qb][e] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, st[qb][e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          st[qb][e] *= a.scale_log2;
+          mloc = fmaxf(mloc, st[qb][e]);
+        }
+      }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      const float m_new = fmaxf(m_run[qb], mloc);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      if (__ballot(m_new != m_run[qb])) {
+        // some running maximum moved: rescale this block's sums
+        const float corr = __builtin_amdgcn_exp2f(m_run[qb] - m_use);
+        l_run[qb] *= corr;
+#pragma unroll
+        for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[qb][hb][e] *= corr;
+      }
+      m_run[qb] = m_new;
+      float psum = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int key = (e >> 2) * 8 + hi * 4 + (e & 3);
-        st[e] = (kpos[buf][key] <= qpos) ? st[e] * a.scale_log2 : -INFINITY;
-        mloc = fmaxf(mloc, st[e]);
+        st[qb][e] = __builtin_amdgcn_exp2f(st[qb][e] - m_use);
+        psum += st[qb][e];
       }
-    } else {
+      l_run[qb] += psum;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        st[e] *= a.scale_log2;
-        mloc = fmaxf(mloc, st[e]);
-      }
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pb[qb][s2][i] = (__bf16)st[qb][8 * s2 + i];
     }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    if (__ballot(m_new != m_run)) {
-      // some running maximum moved: rescale this wave's sums
-      const float corr = __builtin_amdgcn_exp2f(m_run - m_use);
-      l_run *= corr;
-#pragma unroll
-      for (int hb = 0; hb < NHB; ++hb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[hb][e] *= corr;
-    }
-    m_run = m_new;
-    float psum = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      st[e] = __builtin_amdgcn_exp2f(st[e] - m_use);
-      psum += st[e];
-    }
-    l_run += psum;
     // k index (8 hi + i) of step s2 <-> key 16 s2 + 8 (i/4) + 4 hi + i%4, which is
     // accumulator element 8 s2 + i of S^T in this lane; its 4-key halves are words
     // of key groups 4 s2 + hi and 4 s2 + 2 + hi
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      bf16x8 pb;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) pb[i] = (__bf16)st[8 * s2 + i];
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
         const int hd = hb * 32 + l32;
         const uint2 v0 = Vq[buf][vq_word<HD>(4 * s2 + hi, hd)];
         const uint2 v1 = Vq[buf][vq_word<HD>(4 * s2 + 2 + hi, hd)];
         const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{v0.x, v0.y, v1.x, v1.y});
-        o[hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[hb], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][s2], o[qb][hb], 0, 0, 0);
       }
     }
   };
@@ -1193,11 +1237,11 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
     // through LDS with whole-line loads while the first key blocks are in flight
     constexpr int QT = G * 64;                        // query-wave threads
     constexpr int QCH = G * HD / 8;                   // 16-B chunks of one query row
-    constexpr int QIT = (32 * QCH + QT - 1) / QT;     // chunks per thread
+    constexpr int QIT = (QR * QCH + QT - 1) / QT;     // chunks per thread
     uint4 qv[QIT];
 #pragma unroll
     for (int i = 0; i < QIT; ++i) {
-      const int c = min(t + i * QT, 32 * QCH - 1);
+      const int c = min(t + i * QT, QR * QCH - 1);
       const int r = c / QCH, x = c - r * QCH;
       const long sl = (long)b * a.N + (j0 + r < n ? j0 + r : j0);
       qv[i] = *reinterpret_cast<const uint4 *>(a.q + sl * (a.nh * HD) + (long)g * G * HD + 8 * x);
@@ -1205,7 +1249,7 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
 #pragma unroll
     for (int i = 0; i < QIT; ++i) {
       const int c = t + i * QT;
-      if (c < 32 * QCH) {
+      if (c < QR * QCH) {
         const int r = c / QCH, x = c - r * QCH;
         *reinterpret_cast<uint4 *>(&Qs[(8 * x) / HD][r * QLD + (8 * x) % HD]) = qv[i];
       }
@@ -1213,37 +1257,46 @@ __global__ __launch_bounds__((G + kAttnStageWaves) * 64) void k_attn(AttnArgs a)
   }
   lds_barrier();
   for (int kb = kb0; kb < kb1; kb += 2) {
-    softmax_pv(qk(0), 0, needs_mask(kb));                          // buffer 0: block kb
+    f32x16 st[QB];
+    qk(0, st);
+    softmax_pv(st, 0, needs_mask(kb));                             // buffer 0: block kb
     lds_barrier();
-    if (kb + 1 < kb1) softmax_pv(qk(1), 1, needs_mask(kb + 1));    // buffer 1: block kb + 1
+    if (kb + 1 < kb1) {                                            // buffer 1: block kb + 1
+      qk(1, st);
+      softmax_pv(st, 1, needs_mask(kb + 1));
+    }
     lds_barrier();
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (a.splits == 1) {
-    if (!qvalid) return;
-    uint16_t *orow = a.out + slot * (long)(a.nh * HD) + h * HD;
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
+  for (int qb = 0; qb < QB; ++qb) {
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    if (a.splits == 1) {
+      if (!qvalid[qb]) continue;
+      uint16_t *orow = a.out + slot[qb] * (long)(a.nh * HD) + h * HD;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        orow[hb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3)] = f2bf(o[hb][e] * inv);
-  } else {
-    // partials of this (split, tile, head) in accumulator order: 16-B group i of
-    // lane L at ((i * 64) + L) * 16 B, so each wave store is 1 KB contiguous; the
-    // running max and sum per query follow as [split][tile][head][32]
-    const long blk = ((long)sp * tiles + qt) * a.nh + h;
-    float4 *po = reinterpret_cast<float4 *>(a.po) + blk * (NHB * 4 * 64);
+      for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
+        for (int e = 0; e < 16; ++e)
+          orow[hb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3)] = f2bf(o[qb][hb][e] * inv);
+    } else if (QB == 1) {
+      // partials of this (split, tile, head) in accumulator order: 16-B group i of
+      // lane L at ((i * 64) + L) * 16 B, so each wave store is 1 KB contiguous; the
+      // running max and sum per query follow as [split][tile][head][32].  (Two-block
+      // tiles are launched with one split only.)
+      const long blk = ((long)sp * tiles + qt) * a.nh + h;
+      float4 *po = reinterpret_cast<float4 *>(a.po) + blk * (NHB * 4 * 64);
 #pragma unroll
-      for (int eg = 0; eg < 4; ++eg)
-        po[(hb * 4 + eg) * 64 + lane] =
-            make_float4(o[hb][4 * eg], o[hb][4 * eg + 1], o[hb][4 * eg + 2], o[hb][4 * eg + 3]);
-    if (hi == 0) {
-      a.pm[blk * 32 + l32] = m_run;
-      a.pl[blk * 32 + l32] = l_tot;
+      for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+        for (int eg = 0; eg < 4; ++eg)
+          po[(hb * 4 + eg) * 64 + lane] = make_float4(o[qb][hb][4 * eg], o[qb][hb][4 * eg + 1],
+                                                      o[qb][hb][4 * eg + 2], o[qb][hb][4 * eg + 3]);
+      if (hi == 0) {
+        a.pm[blk * 32 + l32] = m_run[qb];
+        a.pl[blk * 32 + l32] = l_tot;
+      }
     }
   }
 }
@@ -1440,12 +1493,23 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
   return FC_OK;
 }
 
+// rot: keys rotated on load (32-query tiles, four staging waves); otherwise keys come
+// rotated and, with one key split, each query wave takes two 32-query blocks (one
+// staging wave), so a staged key block feeds twice the MFMAs
 template <int HD, int G>
-void launch_attn(dim3 grid, hipStream_t st, const AttnArgs &a, bool rot) {
-  if (rot)
-    hipLaunchKernelGGL((k_attn<HD, G, true>), grid, dim3((G + kAttnStageWaves) * 64), 0, st, a);
-  else
-    hipLaunchKernelGGL((k_attn<HD, G, false>), grid, dim3((G + kAttnStageWaves) * 64), 0, st, a);
+void launch_attn(hipStream_t st, AttnArgs a, bool rot, int nkv) {
+  if (rot) {
+    hipLaunchKernelGGL((k_attn<HD, G, true, 1, kAttnStageWaves>), dim3(a.tiles * nkv * a.splits),
+                       dim3((G + kAttnStageWaves) * 64), 0, st, a);
+  } else if (a.splits > 1) {
+    hipLaunchKernelGGL((k_attn<HD, G, false, 1, kAttnStageWaves>), dim3(a.tiles * nkv * a.splits),
+                       dim3((G + kAttnStageWaves) * 64), 0, st, a);
+  } else {
+    const int tiles_per_b = (a.N + 63) / 64;
+    a.tiles = (a.tiles / ((a.N + 31) / 32)) * tiles_per_b;      // B * tiles of 64 queries
+    hipLaunchKernelGGL((k_attn<HD, G, false, 2, 1>), dim3(a.tiles * nkv), dim3((G + 1) * 64), 0,
+                       st, a);
+  }
 }
 
 // Tiles of the large-M GEMM: 256 packed rows, 256 output columns (SwiGLU: 128 output
@@ -1575,7 +1639,6 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.pl = a.pm + (size_t)a.splits * prow * nh;
     const int G = nh / nkv;
     a.tiles = tiles;
-    dim3 grid(tiles * nkv * a.splits);
     // with many query tiles per item, every cached key is rotated once into a copy
     // instead of once per (key, tile) inside the attention kernel
     const long kvw = (long)nkv * hd;
@@ -1592,15 +1655,15 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     {
       ProfScope ps(ctx, st, "fc_attn");
       if (hd == 128 && G == 7)
-        launch_attn<128, 7>(grid, st, a, !prerot);
+        launch_attn<128, 7>(st, a, !prerot, nkv);
       else if (hd == 128 && G == 1)
-        launch_attn<128, 1>(grid, st, a, !prerot);
+        launch_attn<128, 1>(st, a, !prerot, nkv);
       else if (hd == 64 && G == 1)
-        launch_attn<64, 1>(grid, st, a, !prerot);
+        launch_attn<64, 1>(st, a, !prerot, nkv);
       else if (hd == 64 && G == 2)
-        launch_attn<64, 2>(grid, st, a, !prerot);
+        launch_attn<64, 2>(st, a, !prerot, nkv);
       else if (hd == 128 && G == 4)
-        launch_attn<128, 4>(grid, st, a, !prerot);
+        launch_attn<128, 4>(st, a, !prerot, nkv);
       else
         return fail(FC_ERR_UNSUPPORTED, "attention: head_dim %d with %d query heads per kv head", hd, G);
       FC_HIP_TRY(hipGetLastError());
