@@ -317,19 +317,92 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
 }
 
 // ------------------------------------------------------------------------------- helpers
-// Deterministic workgroup reductions of K values at once: a fixed shuffle tree inside
-// each wave, then wave 0 combines the per-wave partials with another fixed tree.  Every
-// thread gets the results.  scratch holds NW * K + K doubles.  MAXK: value k < MAXK
-// is a maximum, the others sums.
+// The value that lane (lane ^ O) of the wave holds, moved without the LDS: DPP lane
+// permutes inside rows of 16 lanes (quad permutes for 1 and 2, row rotations for 4
+// and 8) and the gfx950 row-swap instructions for 16 and 32 (with both operands the
+// same register, each swap returns the even rows' and the odd rows' values).
+template <int O>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+  if constexpr (O == 1) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  } else if constexpr (O == 2) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  } else if constexpr (O == 4) {
+    const uint32_t r4 = __builtin_amdgcn_update_dpp(0u, x, 0x124, 0xF, 0xF, false);   // row_ror:4
+    const uint32_t r12 = __builtin_amdgcn_update_dpp(0u, x, 0x12C, 0xF, 0xF, false);  // row_ror:12
+    return (lane & 4) ? r4 : r12;
+  } else if constexpr (O == 8) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (O == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return (lane & 16) ? r[0] : r[1];
+  } else {
+    static_assert(O == 32, "lane distance 1 .. 32");
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return (lane & 32) ? r[0] : r[1];
+  }
+}
+template <int O>
+__device__ __forceinline__ double xor_lane_d(double x) {
+  const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+  const uint32_t lo = xor_lane<O>((uint32_t)u), hi = xor_lane<O>((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+__device__ __forceinline__ double xor_lane_d(double x, int o) {
+  switch (o) {
+    case 1: return xor_lane_d<1>(x);
+    case 2: return xor_lane_d<2>(x);
+    case 4: return xor_lane_d<4>(x);
+    case 8: return xor_lane_d<8>(x);
+    case 16: return xor_lane_d<16>(x);
+    default: return xor_lane_d<32>(x);
+  }
+}
+__device__ __forceinline__ int xor_lane_i(int x, int o) {
+  switch (o) {
+    case 1: return (int)xor_lane<1>((uint32_t)x);
+    case 2: return (int)xor_lane<2>((uint32_t)x);
+    case 4: return (int)xor_lane<4>((uint32_t)x);
+    case 8: return (int)xor_lane<8>((uint32_t)x);
+    case 16: return (int)xor_lane<16>((uint32_t)x);
+    default: return (int)xor_lane<32>((uint32_t)x);
+  }
+}
+__device__ __forceinline__ double first_lane_d(double x) {
+  const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: DPP shifts inside each row of 16
+// lanes, then each row adds the totals of the rows before it.
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int lane = threadIdx.x & 63;
+  x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31),
+            r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = lane >> 4;
+  return x + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
+}
+
+// Deterministic workgroup reductions of K values at once: a fixed butterfly inside each
+// wave, the per-wave partials through LDS, then the same fixed butterfly over them in
+// every wave, so every thread gets the results after one barrier pair.  scratch holds
+// NW * K doubles.  MAXK: value k < MAXK is a maximum, the others sums.
 template <int NW, int K, int MAXK>
 __device__ void block_reduce(double (&v)[K], double *scratch) {
   static_assert(NW <= 64 && (NW & (NW - 1)) == 0, "power-of-two wave count");
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
-  for (int k = 0; k < K; ++k)
+  for (int o = 32; o > 0; o >>= 1)
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const double u = __shfl_xor(v[k], o);
+    for (int k = 0; k < K; ++k) {
+      const double u = xor_lane_d(v[k], o);
       v[k] = k < MAXK ? fmax(v[k], u) : v[k] + u;
     }
   __syncthreads();
@@ -337,21 +410,19 @@ __device__ void block_reduce(double (&v)[K], double *scratch) {
 #pragma unroll
     for (int k = 0; k < K; ++k) scratch[w * K + k] = v[k];
   __syncthreads();
-  if (w == 0) {
+  double x[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    x[k] = lane < NW ? scratch[lane * K + k] : (k < MAXK ? -INFINITY : 0.0);
+#pragma unroll
+  for (int o = NW / 2; o > 0; o >>= 1)
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      double x = lane < NW ? scratch[lane * K + k] : (k < MAXK ? -INFINITY : 0.0);
-#pragma unroll
-      for (int o = NW / 2; o > 0; o >>= 1) {
-        const double u = __shfl_xor(x, o);
-        x = k < MAXK ? fmax(x, u) : x + u;
-      }
-      if (lane == 0) scratch[NW * K + k] = x;
+      const double u = xor_lane_d(x[k], o);
+      x[k] = k < MAXK ? fmax(x[k], u) : x[k] + u;
     }
-  }
-  __syncthreads();
 #pragma unroll
-  for (int k = 0; k < K; ++k) v[k] = scratch[NW * K + k];
+  for (int k = 0; k < K; ++k) v[k] = first_lane_d(x[k]);
 }
 
 // One direct DFT pass over an [Gh][Gw] complex grid in LDS, one output per thread:
@@ -454,7 +525,7 @@ __device__ __forceinline__ double2 fft_lanes(double2 x, int i, const double2 *tw
 #pragma unroll
   for (int st = 0; st < LG; ++st) {
     const int h = G >> (st + 1);
-    const double px = __shfl_xor(x.x, h), py = __shfl_xor(x.y, h);
+    const double px = xor_lane_d(x.x, h), py = xor_lane_d(x.y, h);
     // upper half of a butterfly: (a - b) w, a = partner; lower half: a + b
     const bool up = i & h;
     const double dx = px - x.x, dy = py - x.y;
@@ -604,8 +675,8 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
   int bi = act ? t : 0x7fffffff;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    const double v2 = __shfl_xor(bv, o);
-    const int i2 = __shfl_xor(bi, o);
+    const double v2 = xor_lane_d(bv, o);
+    const int i2 = xor_lane_i(bi, o);
     if (v2 > bv || (v2 == bv && i2 < bi)) {
       bv = v2;
       bi = i2;
@@ -729,7 +800,7 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
   constexpr int NW = kMaxTokens / 64;
   __shared__ int hist[256];
   __shared__ int wcnt[NW];
-  __shared__ int sel_digit, sel_rem;
+  __shared__ int sel_digit, sel_rem, sel_cnt;
   const int b = blockIdx.x;
   const int t = threadIdx.x;
   const int lane = t & 63, wv = t >> 6;
@@ -795,38 +866,37 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
         const int h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
                   h3 = hist[4 * lane + 3];
         const int tot = h0 + h1 + h2 + h3;
-        int inc = tot;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int v = __shfl_up(inc, o);
-          if (lane >= o) inc += v;
-        }
+        const int inc = wave_inclusive_scan(tot);
         const int exc = inc - tot;
         if (exc < rem && inc >= rem) {     // exactly one lane holds the crossing
-          int c = exc, d = 4 * lane;
-          if (c + h0 >= rem) d = 4 * lane;
-          else if ((c += h0) + h1 >= rem) d = 4 * lane + 1;
-          else if ((c += h1) + h2 >= rem) d = 4 * lane + 2;
+          int c = exc, d = 4 * lane, n = h3;
+          if (c + h0 >= rem) { d = 4 * lane; n = h0; }
+          else if ((c += h0) + h1 >= rem) { d = 4 * lane + 1; n = h1; }
+          else if ((c += h1) + h2 >= rem) { d = 4 * lane + 2; n = h2; }
           else { c += h2; d = 4 * lane + 3; }
           sel_digit = d;
           sel_rem = rem - c;
+          sel_cnt = n;
         }
       }
       __syncthreads();
       kth |= (unsigned long long)sel_digit << sh;
       pmask |= 255ull << sh;
       rem = sel_rem;
+      // every candidate in the chosen bin is taken: the keys need no more digits
+      if (sel_cnt == rem) break;
     }
   }
-  // reuse: every candidate below the k-th key, and the lowest-id `rem` at the key
-  const bool eq = cand && k_final > 0 && key == kth;
+  // reuse: every candidate below the selected key prefix, and the lowest-id `rem` of
+  // those at the prefix (all of them when the select stopped early)
+  const bool eq = cand && k_final > 0 && (key & pmask) == kth;
   bal = __ballot(eq);
   __syncthreads();
   if (lane == 0) wcnt[wv] = __popcll(bal);
   __syncthreads();
   int eq_before = __popcll(bal & ((1ull << lane) - 1ull));
   for (int i = 0; i < wv; ++i) eq_before += wcnt[i];
-  const bool use = cand && k_final > 0 && (key < kth || (eq && eq_before < rem));
+  const bool use = cand && k_final > 0 && ((key & pmask) < kth || (eq && eq_before < rem));
 
   // compaction of recomputed ids (ascending)
   const bool keep = act && !use;
