@@ -133,6 +133,20 @@ __device__ __forceinline__ void dma16(const void *gp, uint32_t lds) {
       : "v"(gp), "s"(l)
       : "memory");
 }
+// The same for data read once (streamed weights): the non-temporal hint keeps such
+// lines from displacing the re-read activation rows in L2.
+__device__ __forceinline__ void dma16_nt(const void *gp, uint32_t lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off nt\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gp), "s"(l)
+      : "memory");
+}
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt holds at most 63 outstanding loads");
@@ -203,11 +217,13 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
     const int rsub = lane >> 3, ch = lane & 7;
     const uint16_t *gp[MAXI];
     uint32_t lo[MAXI];
+    bool wt[MAXI];
     int L = 0;
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int j = min(q + 4 * i, ntot - 1);
       L += (q + 4 * i < ntot);
+      wt[i] = j >= nA;
       if (j < nA) {
         const int r = j * 8 + rsub;                            // tile row
         const int rr = r < nvalid ? r : nvalid - 1;            // clamp: never stored
@@ -235,8 +251,12 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
       const int kk = kt * KS;
       const uint32_t st = lbase + stg * S::BYTES;
 #pragma unroll
-      for (int i = 0; i < MAXI; ++i)
-        if (i < L) dma16(gp[i] + kk, st + lo[i]);
+      for (int i = 0; i < MAXI; ++i) {
+        if (i < L) {
+          if (wt[i]) dma16_nt(gp[i] + kk, st + lo[i]);
+          else dma16(gp[i] + kk, st + lo[i]);
+        }
+      }
     };
     for (int u = 0; u < PD - 1 && u < nk; ++u) issue(u, u);
     for (int k = 0; k < nk; ++k) {
