@@ -604,8 +604,34 @@ struct MArgs {
   int B, mtiles, ntn;             // items, M tiles (over the packed rows), N tiles
   int ss_parts;                   // O writes / SwiGLU reads this many partials per row
   uint16_t *act;                  // SwiGLU output [B*N][Nout]
+  int cus;                        // workgroup slots: one resident workgroup per CU
+  int part_units;                 // 256 x 256 fp32 tiles the partial buffer holds
+  float *part;                    // K-range partial tiles of the split tail
   RedArgs r;                      // epilogue operands (as the reductions use them)
 };
+
+// With one workgroup per CU, tiles run in rounds of `cus`.  When there are few rounds
+// and the last is at most half full, its `tail` tiles run as `ks` parts over K ranges
+// each (written as fp32 partial tiles, summed in part order by k_mtail), so the round
+// takes about 1/ks of a tile's time; tiles [0, F) run whole.  (Over many rounds the
+// tiles' uneven durations already blur the last round, and the partial round trip
+// would cost more than it saves.)  Host and device take the same decision.
+__host__ __device__ inline void mtail_split(int total, int cus, int part_units, int nk, int &F,
+                                            int &tail, int &ks) {
+  tail = cus > 0 ? total % cus : 0;
+  ks = 1;
+  if (tail > 0 && 2 * tail <= cus && total < 8 * cus) {
+    ks = cus / tail;
+    ks = ks < 4 ? ks : 4;
+    ks = ks < nk / 4 ? ks : nk / 4;              // at least 4 K steps per part
+    while (ks > 1 && tail * ks > part_units) --ks;
+  }
+  if (ks < 2) {
+    tail = 0;
+    ks = 1;
+  }
+  F = total - tail;
+}
 
 // Tile order over the V valid M tiles (known on the device only): each XCD takes a
 // contiguous range of tiles, walked in groups of 4 M tiles, N tile by N tile, so the
@@ -642,6 +668,111 @@ __device__ __forceinline__ long packed_slot(const int *pre, int B, int N, int p,
   return (long)lo * N + (p - pre[lo]);
 }
 
+// Exclusive prefix sums of the recompute counts into pre[0..B] (wave 0; the caller
+// synchronises): each lane sums a run of items, then the runs are scanned.
+__device__ __forceinline__ void mg_prefix(const MArgs &a, int *pre) {
+  const int lane = threadIdx.x & 63;
+  const int per = (a.B + 63) / 64, i0 = lane * per;
+  int run = 0;
+  for (int i = i0; i < min(i0 + per, a.B); ++i) run += n_valid(a.r.nrec, i, a.N);
+  int inc = run;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(inc, o);
+    if (lane >= o) inc += v;
+  }
+  int acc_run = inc - run;
+  for (int i = i0; i < min(i0 + per, a.B); ++i) {
+    pre[i] = acc_run;
+    acc_run += n_valid(a.r.nrec, i, a.N);
+  }
+  if (lane == 63) pre[a.B] = inc;
+}
+
+// Row `row` of a tile's epilogue: trow holds its 256 accumulated columns (SwiGLU: the
+// 128 products), lane l handles columns 4 l .. 4 l + 3.  Called by whole waves.
+template <int MODE>
+__device__ __forceinline__ void mg_epi_row(const MArgs &a, const int *pre, const float *trow,
+                                           int row0, int row, int nvalid, int col0, int nt) {
+  const RedArgs &r = a.r;
+  const int lane = threadIdx.x & 63;
+  constexpr int TN = MODE == G_GU ? MB / 2 : MB;
+  const bool rv = row < nvalid;
+  int b = 0;
+  const long slot = rv ? packed_slot(pre, a.B, a.N, row0 + row, b) : 0;
+  const int tok = rv ? tok_of(r.idx, slot, a.N) : 0;
+  const int c4 = lane * 4;                                   // column within the tile
+  if (MODE == G_GU) {
+    const int col = col0 + c4;
+    if (rv && c4 < TN && col < a.Nout) {
+      const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
+      *reinterpret_cast<uint2 *>(a.act + slot * a.Nout + col) = pack_bf16x4(v.x, v.y, v.z, v.w);
+    }
+    return;
+  }
+  const int col = col0 + c4;
+  const bool cv = col < a.Nout;
+  const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
+  if (MODE == G_QKV) {
+    if (!rv || !cv) return;
+    const float4 bs = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col));
+    float o[4] = {v.x + bs.x, v.y + bs.y, v.z + bs.z, v.w + bs.w};
+    uint16_t *dst;
+    if (col < r.qw) {
+      // rotate-half RoPE: the partner dims are half a head away in the same row
+      const int half = r.hd / 2, dim = col % r.hd;
+      const int pc4 = dim < half ? c4 + half : c4 - half;
+      const float4 pv = *reinterpret_cast<const float4 *>(trow + pc4);
+      const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
+      const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
+      const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half + dim % half;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float2 cs = rp[q];
+        o[q] = dim < half ? o[q] * cs.x - p[q] * cs.y : o[q] * cs.x + p[q] * cs.y;
+      }
+      dst = r.q + slot * r.qw + col;
+    } else {
+      const long crow = (long)b * r.S + r.cur_row0 + tok;
+      dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
+                              : r.vc + crow * r.kw + (col - r.qw - r.kw);
+    }
+    *reinterpret_cast<uint2 *>(dst) = pack_bf16x4(o[0], o[1], o[2], o[3]);
+  } else if (MODE == G_O) {
+    float ss = 0.f;
+    if (rv && cv) {
+      const float4 xv = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.x + ((long)b * a.N + tok) * r.d + col));
+      const float4 hv = make_float4(v.x + xv.x, v.y + xv.y, v.z + xv.z, v.w + xv.w);
+      *reinterpret_cast<float4 *>(r.h1 + slot * r.d + col) = hv;
+      const float4 gn = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.gain + col));
+      *reinterpret_cast<uint2 *>(r.hb + slot * r.d + col) =
+          pack_bf16x4(hv.x * gn.x, hv.y * gn.y, hv.z * gn.z, hv.w * gn.w);
+      ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+    }
+    // the row's 256 columns are this wave's 64 lanes
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m);
+    if (rv && lane == 0 && nt < a.ss_parts) r.ssq[slot * a.ss_parts + nt] = ss;
+  } else {
+    if (!rv || !cv) return;
+    const float4 hv = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + col);
+    *reinterpret_cast<uint2 *>(r.y + ((long)b * a.N + tok) * r.d + col) =
+        pack_bf16x4(hv.x + v.x, hv.y + v.y, hv.z + v.z, hv.w + v.w);
+  }
+}
+
+// 1/rms of tile row `row` from the O epilogue's partial sums of squares of h1
+__device__ __forceinline__ float mg_rowinv(const MArgs &a, const int *pre, int row0, int row,
+                                           int nvalid) {
+  float v = 0.f;
+  if (row < nvalid) {
+    int ib;
+    const long sl = packed_slot(pre, a.B, a.N, row0 + row, ib);
+    for (int c = 0; c < a.ss_parts; ++c) v += a.r.ssq[sl * a.ss_parts + c];
+  }
+  return 1.f / sqrtf(v / (float)a.K + a.r.eps);
+}
+
 template <int MODE>
 __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kMStage];
@@ -649,36 +780,30 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   __shared__ int pre[kMMaxItems + 1];
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
-  if (w == 0) {
-    // exclusive prefix sums of the recompute counts: each lane sums a run of items,
-    // then the runs are scanned across the wave
-    const int per = (a.B + 63) / 64, i0 = lane * per;
-    int run = 0;
-    for (int i = i0; i < min(i0 + per, a.B); ++i) run += n_valid(a.r.nrec, i, a.N);
-    int inc = run;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(inc, o);
-      if (lane >= o) inc += v;
-    }
-    int acc_run = inc - run;
-    for (int i = i0; i < min(i0 + per, a.B); ++i) {
-      pre[i] = acc_run;
-      acc_run += n_valid(a.r.nrec, i, a.N);
-    }
-    if (lane == 63) pre[a.B] = inc;
-  }
+  if (w == 0) mg_prefix(a, pre);
   __syncthreads();
-  // the grid covers every slot; only the tiles of the packed rows run
+  // the grid covers every slot; only the tiles of the packed rows run, the tail
+  // tiles as K-range parts
   const int V = (pre[a.B] + MB - 1) / MB;
-  if ((int)blockIdx.x >= V * a.ntn) return;
-  int mt, nt;
-  mtile_of(V, a.ntn, blockIdx.x, mt, nt);
+  const int nk = a.K / KS;
+  int F, tail, ks;
+  mtail_split(V * a.ntn, a.cus, a.part_units, nk, F, tail, ks);
+  const int bid = blockIdx.x;
+  if (bid >= F + tail * ks) return;
+  int mt, nt, kb = 0, ke = nk, unit = -1;
+  if (bid < F) {
+    mtile_of(V, a.ntn, bid, mt, nt);
+  } else {
+    const int u = bid - F, ti = u % tail, kp = u / tail;
+    mtile_of(V, a.ntn, F + ti, mt, nt);
+    kb = kp * nk / ks;
+    ke = (kp + 1) * nk / ks;
+    unit = ti * ks + kp;
+  }
   const int row0 = mt * MB;
   const int nvalid = min(MB, pre[a.B] - row0);
   const int wm = w & 1, wn = w >> 1;
   const int l32 = lane & 31, h = lane >> 5;
-  const int nk = a.K / KS;
   // output columns of this tile: SwiGLU stages 32 gate + 32 up rows per wave column
   constexpr int TN = MODE == G_GU ? MB / 2 : MB;
   const int col0 = nt * TN;
@@ -717,16 +842,7 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
     for (int i = 0; i < 8; ++i) dma16(gp[i] + kk, st + (w + 8 * i) * 1024);
   };
 
-  if (MODE == G_GU && t < MB) {
-    // 1/rms of each row from the O epilogue's partial sums of squares of h1
-    float v = 0.f;
-    if (t < nvalid) {
-      int ib;
-      const long sl = packed_slot(pre, a.B, a.N, row0 + t, ib);
-      for (int c = 0; c < a.ss_parts; ++c) v += a.r.ssq[sl * a.ss_parts + c];
-    }
-    rowinv[t] = 1.f / sqrtf(v / (float)a.K + a.r.eps);
-  }
+  if (MODE == G_GU && t < MB && unit < 0) rowinv[t] = mg_rowinv(a, pre, row0, t, nvalid);
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -752,12 +868,12 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   // it: waves 0-3 before their first MFMA, waves 4-7 (the other wave of each SIMD) one
   // sub-step later, so that each SIMD always has a wave issuing MFMAs.
   const bool early = w < 4;
-  issue(0);
-  for (int k = 0; k < nk; ++k) {
+  issue(kb);
+  for (int k = kb; k < ke; ++k) {
     wait_vm<0>();                                              // this wave's share of step k
     lds_barrier();                                             // all of step k; step k - 1 read
     const unsigned char *st = lds + (k & 1) * kMStage;
-    const bool more = k + 1 < nk;
+    const bool more = k + 1 < ke;
     if (more && early) issue(k + 1);
     bf16x8 fa[2][4], fb[2][2];
     rd(st, 0, fa[0], fb[0]);
@@ -774,12 +890,26 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   }
   lds_barrier();                                               // the stages are free
 
+  if (unit >= 0) {
+    // a part of a tail tile: the raw fp32 accumulators, [256 rows][256 staged columns]
+    float *pt = a.part + (long)unit * (MB * MB);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int rr = wm * 128 + i * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
+          pt[rr * MB + wn * 64 + j * 32 + l32] = acc[i][j][e];
+        }
+    return;
+  }
+
   // ---------------------------------------------------------------- fused epilogue
   // Per 32-row block i: the waves put their accumulators into an LDS tile ([2][32]
   // rows of 256 floats; SwiGLU: the 128 products), then each wave handles whole
   // rows, one 4-column piece per lane.  A lane's accumulator element e of block
   // (i, j) is column l32 of row 8 (e / 4) + 4 h + e % 4.
-  const RedArgs &r = a.r;
   float *T = reinterpret_cast<float *>(lds);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -802,71 +932,79 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
     for (int it = 0; it < 8; ++it) {
       const int er = w + 8 * it;                               // epilogue row 0..63
       const int row = (er >> 5) * 128 + i * 32 + (er & 31);    // tile row
-      const bool rv = row < nvalid;
-      int b = 0;
-      const long slot = rv ? packed_slot(pre, a.B, a.N, row0 + row, b) : 0;
-      const int tok = rv ? tok_of(r.idx, slot, a.N) : 0;
-      const float *trow = T + er * kMEpPitch;
-      const int c4 = lane * 4;                                 // column within the tile
-      if (MODE == G_GU) {
-        const int col = col0 + c4;
-        if (rv && c4 < TN && col < a.Nout) {
-          const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
-          *reinterpret_cast<uint2 *>(a.act + slot * a.Nout + col) = pack_bf16x4(v.x, v.y, v.z, v.w);
-        }
-        continue;
-      }
-      const int col = col0 + c4;
-      const bool cv = col < a.Nout;
-      const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
-      if (MODE == G_QKV) {
-        if (!rv || !cv) continue;
-        const float4 bs = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col));
-        float o[4] = {v.x + bs.x, v.y + bs.y, v.z + bs.z, v.w + bs.w};
-        uint16_t *dst;
-        if (col < r.qw) {
-          // rotate-half RoPE: the partner dims are half a head away in the same row
-          const int half = r.hd / 2, dim = col % r.hd;
-          const int pc4 = dim < half ? c4 + half : c4 - half;
-          const float4 pv = *reinterpret_cast<const float4 *>(trow + pc4);
-          const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
-          const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
-          const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half + dim % half;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float2 cs = rp[q];
-            o[q] = dim < half ? o[q] * cs.x - p[q] * cs.y : o[q] * cs.x + p[q] * cs.y;
-          }
-          dst = r.q + slot * r.qw + col;
-        } else {
-          const long crow = (long)b * r.S + r.cur_row0 + tok;
-          dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
-                                  : r.vc + crow * r.kw + (col - r.qw - r.kw);
-        }
-        *reinterpret_cast<uint2 *>(dst) = pack_bf16x4(o[0], o[1], o[2], o[3]);
-      } else if (MODE == G_O) {
-        float ss = 0.f;
-        if (rv && cv) {
-          const float4 xv = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.x + ((long)b * a.N + tok) * r.d + col));
-          const float4 hv = make_float4(v.x + xv.x, v.y + xv.y, v.z + xv.z, v.w + xv.w);
-          *reinterpret_cast<float4 *>(r.h1 + slot * r.d + col) = hv;
-          const float4 gn = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.gain + col));
-          *reinterpret_cast<uint2 *>(r.hb + slot * r.d + col) =
-              pack_bf16x4(hv.x * gn.x, hv.y * gn.y, hv.z * gn.z, hv.w * gn.w);
-          ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
-        }
-        // the row's 256 columns are this wave's 64 lanes
-#pragma unroll
-        for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m);
-        if (rv && lane == 0 && nt < a.ss_parts) r.ssq[slot * a.ss_parts + nt] = ss;
-      } else {
-        if (!rv || !cv) continue;
-        const float4 hv = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + col);
-        *reinterpret_cast<uint2 *>(r.y + ((long)b * a.N + tok) * r.d + col) =
-            pack_bf16x4(hv.x + v.x, hv.y + v.y, hv.z + v.z, hv.w + v.w);
-      }
+      mg_epi_row<MODE>(a, pre, T + er * kMEpPitch, row0, row, nvalid, col0, nt);
     }
     lds_barrier();                                             // the tile is free again
+  }
+}
+
+// The tail tiles of a large-M GEMM: the ks K-range partial tiles are summed in part
+// order and go through the same epilogue as a whole tile.  Workgroup 4 q + i handles
+// tail tile q, rows i * 32 .. and 128 + i * 32 .. (the rows of epilogue block i).
+template <int MODE>
+__global__ __launch_bounds__(512) void k_mtail(MArgs a) {
+  __shared__ __attribute__((aligned(16))) float S[64 * kMEpPitch];
+  __shared__ __attribute__((aligned(16))) float P[MODE == G_GU ? 64 * kMEpPitch : 4];
+  __shared__ float rowinv[64];
+  __shared__ int pre[kMMaxItems + 1];
+  const int t = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  if (w == 0) mg_prefix(a, pre);
+  __syncthreads();
+  const int V = (pre[a.B] + MB - 1) / MB;
+  const int nk = a.K / KS;
+  int F, tail, ks;
+  mtail_split(V * a.ntn, a.cus, a.part_units, nk, F, tail, ks);
+  const int q = blockIdx.x >> 2, i = blockIdx.x & 3;
+  if (q >= tail) return;
+  int mt, nt;
+  mtile_of(V, a.ntn, F + q, mt, nt);
+  const int row0 = mt * MB;
+  const int nvalid = min(MB, pre[a.B] - row0);
+  constexpr int TN = MODE == G_GU ? MB / 2 : MB;
+  const int col0 = nt * TN;
+  // thread t sums row er = t / 8, columns 32 (t % 8) .. + 32, over the parts in order
+  {
+    const int er = t >> 3, row = (er >> 5) * 128 + i * 32 + (er & 31);
+    const float *p0 = a.part + (long)q * ks * (MB * MB) + (long)row * MB + (t & 7) * 32;
+    float4 sum[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) sum[c] = *reinterpret_cast<const float4 *>(p0 + 4 * c);
+    for (int kp = 1; kp < ks; ++kp) {
+      const float *pk = p0 + (long)kp * (MB * MB);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const float4 v = *reinterpret_cast<const float4 *>(pk + 4 * c);
+        sum[c] = make_float4(sum[c].x + v.x, sum[c].y + v.y, sum[c].z + v.z, sum[c].w + v.w);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      *reinterpret_cast<float4 *>(&S[er * kMEpPitch + (t & 7) * 32 + 4 * c]) = sum[c];
+    if (MODE == G_GU && t < 64) {
+      const int r2 = (t >> 5) * 128 + i * 32 + (t & 31);
+      rowinv[t] = mg_rowinv(a, pre, row0, r2, nvalid);
+    }
+  }
+  __syncthreads();
+  const float *T = S;
+  if (MODE == G_GU) {
+    // product c of a row: gate at staged column 64 (c / 32) + c % 32, up 32 further
+    for (int e = t; e < 64 * (MB / 2); e += 512) {
+      const int er = e >> 7, c = e & 127;
+      const float sc = rowinv[er];
+      const float gv = S[er * kMEpPitch + (c >> 5) * 64 + (c & 31)] * sc;
+      const float uv = S[er * kMEpPitch + (c >> 5) * 64 + 32 + (c & 31)] * sc;
+      P[er * kMEpPitch + c] = gv / (1.f + __expf(-gv)) * uv;
+    }
+    __syncthreads();
+    T = P;
+  }
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int er = w + 8 * it;
+    const int row = (er >> 5) * 128 + i * 32 + (er & 31);
+    mg_epi_row<MODE>(a, pre, T + er * kMEpPitch, row0, row, nvalid, col0, nt);
   }
 }
 
@@ -1543,10 +1681,17 @@ fc_status run_mgemm(fc_ctx *ctx, hipStream_t st, const char *name, MArgs &g, int
   g.mtiles = (int)(((long)B * g.N + MB - 1) / MB);      // packed rows need at most these
   const int tn = MODE == G_GU ? MB / 2 : MB;
   g.ntn = (g.Nout + tn - 1) / tn;
-  const long total = (long)g.mtiles * g.ntn;
+  g.cus = std::max(ctx->num_cus, 1);
+  g.part = ctx->part;
+  g.part_units = (int)std::min<size_t>(ctx->part_elems / ((size_t)MB * MB), 1 << 20);
+  // whole tiles plus the extra parts of a split tail (fewer than one round)
+  const long total = (long)g.mtiles * g.ntn + g.cus;
   if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
   ProfScope ps(ctx, st, name);
   hipLaunchKernelGGL(k_mgemm<MODE>, dim3((unsigned)total), dim3(512), 0, st, g);
+  FC_HIP_TRY(hipGetLastError());
+  // a split tail has at most cus / 2 tiles, 4 workgroups each
+  hipLaunchKernelGGL(k_mtail<MODE>, dim3((unsigned)(2 * g.cus)), dim3(512), 0, st, g);
   FC_HIP_TRY(hipGetLastError());
   return FC_OK;
 }
