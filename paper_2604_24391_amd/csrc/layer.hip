@@ -1142,6 +1142,28 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     const int r0 = kb * 32, r1 = r0 + 32;
     return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
   };
+  // Key blocks of the current frame's slot past the tile's last query: every key in
+  // them comes after every query of the tile, so they add exactly nothing to the
+  // softmax and are skipped.  Loop index i runs over the other blocks of the split.
+  __shared__ int tile_tok_max;
+  if (w == 0) {
+    int v = -1;
+    if (lane < QR && j0 + lane < n) v = tok_of(a.idx, (long)b * a.N + j0 + lane, a.N);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+    if (lane == 0) tile_tok_max = v;
+  }
+  __syncthreads();
+  int s0 = (cur_lo + tile_tok_max + 1 + 31) / 32, s1 = min(cur_hi, a.S) / 32;
+  s0 = max(s0, kb0);
+  s1 = min(s1, kb1);
+  if (s1 < s0) s1 = s0;
+  const int nb = (kb1 - kb0) - (s1 - s0);
+  auto blk = [&](int i) {                 // block of loop index i (clamped to the last)
+    i = max(min(i, nb - 1), 0);
+    const int k = kb0 + i;
+    return min(k >= s0 ? k + (s1 - s0) : k, nkb - 1);
+  };
 
   if (!qwave) {
     // ------------------------------------------------------------ staging waves
@@ -1171,10 +1193,9 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     }
     const int S = a.S;
 
-    // raw loads of block kb (clamped to the split's last block: the extra blocks the
-    // pipeline runs ahead are loaded but never multiplied)
+    // raw loads of block kb (the pipeline runs ahead onto the last block again: those
+    // loads are never multiplied)
     auto fetch = [&](int kb, KVRaw (&R)[TPT]) {
-      kb = min(kb, kb1 - 1);
       const int rb = kb * 32;                          // first row of the block (uniform)
       // positions: rows of one region (text, or one frame slot of the ring) share the
       // shift from row to position
@@ -1265,17 +1286,17 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     // two register sets with fixed roles (an asm load must never write a register set
     // chosen at run time: the compiler would copy it before it lands)
     KVRaw ra[TPT], rb[TPT];
-    fetch(kb0, ra);
-    fetch(kb0 + 1, rb);
+    fetch(blk(0), ra);
+    fetch(blk(1), rb);
     settle(ra);
     stage(ra, 0);
     lds_barrier();
-    for (int kb = kb0; kb < kb1; kb += 2) {
-      fetch(kb + 2, ra);
+    for (int i = 0; i < nb; i += 2) {
+      fetch(blk(i + 2), ra);
       settle(rb);
       stage(rb, 1);
       lds_barrier();
-      fetch(kb + 3, rb);
+      fetch(blk(i + 3), rb);
       settle(ra);
       stage(ra, 0);
       lds_barrier();
@@ -1414,14 +1435,14 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     }
   }
   lds_barrier();
-  for (int kb = kb0; kb < kb1; kb += 2) {
+  for (int i = 0; i < nb; i += 2) {
     f32x16 st[QB];
     qk(0, st);
-    softmax_pv(st, 0, needs_mask(kb));                             // buffer 0: block kb
+    softmax_pv(st, 0, needs_mask(blk(i)));                         // buffer 0: index i
     lds_barrier();
-    if (kb + 1 < kb1) {                                            // buffer 1: block kb + 1
+    if (i + 1 < nb) {                                              // buffer 1: index i + 1
       qk(1, st);
-      softmax_pv(st, 1, needs_mask(kb + 1));
+      softmax_pv(st, 1, needs_mask(blk(i + 1)));
     }
     lds_barrier();
   }
