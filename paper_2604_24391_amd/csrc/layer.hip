@@ -1369,18 +1369,21 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
         }
       }
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run[qb], mloc);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      if (__ballot(m_new != m_run[qb])) {
-        // some running maximum moved: rescale this block's sums
-        const float corr = __builtin_amdgcn_exp2f(m_run[qb] - m_use);
+      // The reference maximum moves only when a score exceeds it by more than 2^8 (in
+      // log2 units): below that the probabilities stay under 256, which fp32 sums and
+      // bf16 products hold with the same relative precision, and the rescale of the
+      // output sums is skipped.  The final division uses the same reference.
+      const bool grow = mloc > m_run[qb] + 8.f;
+      if (__ballot(grow)) {
+        const float corr = grow ? __builtin_amdgcn_exp2f(m_run[qb] - mloc) : 1.f;
         l_run[qb] *= corr;
 #pragma unroll
         for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[qb][hb][e] *= corr;
+        if (grow) m_run[qb] = mloc;
       }
-      m_run[qb] = m_new;
+      const float m_use = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
       float psum = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
