@@ -1058,6 +1058,24 @@ __device__ __forceinline__ u32x2 kv_load8(const void *p) {
   asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(r) : "v"(p));
   return r;
 }
+// The same from a wave-uniform base (scalar registers) plus a 32-bit byte offset per
+// lane, which spares the 64-bit address arithmetic per load.
+__device__ __forceinline__ const unsigned char *uniform_ptr(const void *p) {
+  const uint64_t u = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return reinterpret_cast<const unsigned char *>((uintptr_t)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ u32x4 kv_load16s(const unsigned char *base, uint32_t off) {
+  u32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, %2" : "=v"(r) : "v"(off), "s"(base));
+  return r;
+}
+__device__ __forceinline__ u32x2 kv_load8s(const unsigned char *base, uint32_t off) {
+  u32x2 r;
+  asm volatile("global_load_dwordx2 %0, %1, %2" : "=v"(r) : "v"(off), "s"(base));
+  return r;
+}
 template <typename T>
 __device__ __forceinline__ void kv_anchor(T &r) { asm volatile("" : "+v"(r)); }
 __device__ __forceinline__ float lo_f(uint32_t u) { return __uint_as_float(u << 16); }
@@ -1172,9 +1190,11 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     //   keys:   dims [8c, 8c + 8) and [HD/2 + 8c, HD/2 + 8c + 8) of key `key`;
     //   values: dims [4l, 4l + 4) of keys 4kg .. 4kg + 3,
     // so per block only the row offset of the block is added.
+    // Byte offsets of a task's loads from the first row of a full block: key row
+    // `key`, dims 8c..; value rows 4kg + r, dims 4l..
     bool act[TPT];
-    int key[TPT], c[TPT], kg[TPT], kofs1[TPT], kofs2[TPT], vofs[TPT][4];
-    const uint16_t *kbase[TPT], *vbase[TPT];
+    int key[TPT], c[TPT], kg[TPT], lq[TPT], kofs1[TPT], kofs2[TPT], vofs[TPT][4];
+    uint32_t koff[TPT], voff[TPT][4];
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       act[i] = tl + i * NL < TASKS;
@@ -1182,14 +1202,15 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
       key[i] = tk / CPK;
       c[i] = tk - key[i] * CPK;
       kg[i] = tk / (HD / 4);
-      const int l = tk - kg[i] * (HD / 4);
+      lq[i] = tk - kg[i] * (HD / 4);
       const int ksw = kswz<HD>(key[i]);
       kofs1[i] = key[i] * HD + 8 * (c[i] ^ ksw);
       kofs2[i] = key[i] * HD + 8 * ((c[i] + HD / 16) ^ ksw);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) vofs[i][q] = vq_word<HD>(kg[i], 4 * l + q);
-      kbase[i] = a.kc + kvbase + 8 * c[i];
-      vbase[i] = a.vc + kvbase + 4 * l;
+      for (int q = 0; q < 4; ++q) vofs[i][q] = vq_word<HD>(kg[i], 4 * lq[i] + q);
+      koff[i] = (uint32_t)(key[i] * kvrow * 2 + 16 * c[i]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) voff[i][r] = (uint32_t)((4 * kg[i] + r) * kvrow * 2 + 8 * lq[i]);
     }
     const int S = a.S;
 
@@ -1210,15 +1231,21 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
           uniform_pos = true;
         }
       }
+      // the block's first K and V rows as scalar bases; rows past the end of the cache
+      // read its last row (lim, relative to the block) again and are never multiplied
+      const int lim = S - 1 - rb;
+      const uint32_t lim_off = (uint32_t)(lim * kvrow * 2);
+      const unsigned char *kblk = uniform_ptr(a.kc + kvbase + (long)rb * kvrow);
+      const unsigned char *vblk = uniform_ptr(a.vc + kvbase + (long)rb * kvrow);
 #pragma unroll
       for (int i = 0; i < TPT; ++i) {
         const int row0 = rb + key[i];
         const int row = min(row0, S - 1);
         const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.N, a.W, a.head);
         R[i].pos = row0 < S ? pos : 0x7fffffff;
-        const uint16_t *kp = kbase[i] + (long)row * kvrow;
-        R[i].k1 = kv_load16(kp);
-        R[i].k2 = kv_load16(kp + HD / 2);
+        const uint32_t ko = key[i] <= lim ? koff[i] : lim_off + 16 * c[i];
+        R[i].k1 = kv_load16s(kblk, ko);
+        R[i].k2 = kv_load16s(kblk, ko + HD);
         if (ROT) {
           const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c[i];
 #pragma unroll
@@ -1226,8 +1253,10 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
         }
         // every asm load is unconditional (no register set chosen at run time)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          R[i].v[r] = kv_load8(vbase[i] + (long)min(rb + 4 * kg[i] + r, S - 1) * kvrow);
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t vo = 4 * kg[i] + r <= lim ? voff[i][r] : lim_off + 8 * lq[i];
+          R[i].v[r] = kv_load8s(vblk, vo);
+        }
       }
     };
     // the loads of R are complete once only the other set's loads (issued after R's)
@@ -1353,22 +1382,21 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     bf16x8 pb[QB][2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
+      // raw scores here; the scale (> 0, in log2 units) enters the maximum once and each
+      // exponent through one fused multiply-add
       float mloc = -INFINITY;
       if (masked) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = (e >> 2) * 8 + hi * 4 + (e & 3);
-          st[qb][e] = (kpos[buf][key] <= qpos[qb]) ? st[qb][e] * a.scale_log2 : -INFINITY;
+          st[qb][e] = (kpos[buf][key] <= qpos[qb]) ? st[qb][e] : -INFINITY;
           mloc = fmaxf(mloc, st[qb][e]);
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          st[qb][e] *= a.scale_log2;
-          mloc = fmaxf(mloc, st[qb][e]);
-        }
+        for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, st[qb][e]);
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32)) * a.scale_log2;
       // The reference maximum moves only when a score exceeds it by more than 2^8 (in
       // log2 units): below that the probabilities stay under 256, which fp32 sums and
       // bf16 products hold with the same relative precision, and the rescale of the
@@ -1387,7 +1415,7 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
       float psum = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        st[qb][e] = __builtin_amdgcn_exp2f(st[qb][e] - m_use);
+        st[qb][e] = __builtin_amdgcn_exp2f(fmaf(st[qb][e], a.scale_log2, -m_use));
         psum += st[qb][e];
       }
       l_run[qb] += psum;
