@@ -15,6 +15,8 @@ Also reported, each measured in the same run:
   cpu_baseline  the CPU oracle on a bounded sample of the same step;
   select_batch  fc_select on 64 pairs of 448x448 frames, GB/s of frame input;
   layer_ratios  one layer at reuse 0/25/50/75/90 %, time, MFMA utilisation;
+  ablations     the module ablations of Table 3 (w/o alignment, w/o refresh, fixed
+                30 % budget) on the episode's frame pairs: mean token reuse;
   batch_episodes  16 concurrent episodes at 896x896 (1024 tokens per frame, a 4-frame
                 window, 4224 cached positions): frames/s of the whole step and the
                 MFMA utilisation of the 28 layers, the regime where the layer is
@@ -219,6 +221,7 @@ def main():
     if not args.no_extras:
         result["select_batch"] = bench_select_batch(fc, ctx, torch)
         result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
+        result["ablations"] = bench_ablations(fc, ctx, torch, frames, m, N)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
                                               T, N, Wn, L, gw)
@@ -295,6 +298,36 @@ def bench_select_batch(fc, ctx, torch):
                 call_us=round(call_us, 2), algorithmic_bytes=frame_bytes + out_bytes,
                 gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
                 spectra_gbs=round(spectra_gbs, 1), kernel_avg_us=kern)
+
+
+def bench_ablations(fc, ctx, torch, frames, m, N):
+    """Token reuse of the full selection and of its module ablations (Table 3, Sec. 6.3)
+    over all consecutive frame pairs of the episode, in one batched fc_select call per
+    variant.  The paper's own reuse figures (InternVLA-N1 on R2R-CE) are context only."""
+    prev, cur = frames[:-1].contiguous(), frames[1:].contiguous()
+    B = cur.shape[0]
+    out = fc.SelectOut.alloc(B, N)
+    variants = {
+        "full": dict(),
+        "wo_module1": dict(align=False),
+        "wo_module2": dict(refresh=False),
+        "wo_module3_fixed30": dict(adaptive=False, alpha_fixed=0.3),
+        "full_tau_sim_0.9": dict(tau_sim=0.9),
+        "wo_module1_tau_sim_0.9": dict(align=False, tau_sim=0.9),
+    }
+    res = {}
+    for name, kw in variants.items():
+        prm = fc.SelectParams(merge=m, **kw)
+        fc.fc_select(ctx, prm, prev, cur, out)
+        torch.cuda.synchronize()
+        counts = out.counts.cpu().numpy()
+        res[name] = dict(mean_reuse=round(float(counts[:, 2].mean()) / N, 4),
+                         mean_candidates=round(float(counts[:, 1].mean()) / N, 4),
+                         flushed=int(counts[:, 3].sum()))
+    res["pairs"] = B
+    res["paper_context"] = ("Table 3 token reuse on R2R-CE: full 53.5 %, w/o I 19.8 %, "
+                            "w/o II 57.0 %, w/o III (fixed 30 %) 38.6 %")
+    return res
 
 
 def bench_layer_ratios(fc, ctx, torch, lay, shape):

@@ -84,6 +84,11 @@ typedef struct {
   double alpha_fixed;       /* fixed reuse ratio (the "w/o Module III" ablation, Table 3)  */
   int32_t entropy_norm;     /* 1: entropy divided by ln(grid bins), so Psi is in [0, 1]    */
   double tau_sim;           /* extra per-token similarity floor; 0 = exact Algorithm 1     */
+  /* Module ablations of Table 3 (Sec. 6.3); 0 (zero-initialised) = the full method.       */
+  int32_t no_align;         /* 1: "w/o Module I", position-wise matching: shift = (0, 0)
+                               and every token aligned (phase correlation not used)       */
+  int32_t no_refresh;       /* 1: "w/o Module II", no token is refreshed by its edge energy
+                               (mu_E, sigma_E and the threshold are still reported)       */
 } fc_select_params;
 
 enum { FC_SCALAR_SIM_FREQ = 0, FC_SCALAR_PSI, FC_SCALAR_ALPHA, FC_SCALAR_MU,

@@ -49,6 +49,9 @@ class SelectParams:
     alpha_fixed: float = 0.5
     entropy_norm: bool = True
     tau_sim: float = 0.0           # per-token similarity floor; 0 is exact Algorithm 1
+    # Module ablations of Table 3 (Sec. 6.3):
+    align: bool = True             # False: "w/o Module I", position-wise matching (Delta = 0)
+    refresh: bool = True           # False: "w/o Module II", no high-frequency refresh
 
 
 # ---------------------------------------------------------------- O1, O2: luma and tiling
@@ -292,12 +295,18 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
     sim_freq = global_similarity(f_cur, f_prev)
     flushed = sim_freq < prm.tau_mig
     (di, dj), resp = phase_correlation(f_prev, f_cur)
+    if not prm.align:
+        # "w/o Module I": tokens are matched at their own positions
+        di, dj = 0, 0
     aligned = align_mask(gh, gw, di, dj)
     sim = token_similarity(a_cur, a_prev, di, dj, aligned)
     # Module II
     e_tok = token_view(patch_energy(pc), m).sum(axis=-1)
     e_tok = np.where(e_tok < 1e-8 * m * m, 0.0, e_tok)
     fresh, mu, sd, thr = refresh_mask(e_tok, prm.lam)
+    if not prm.refresh:
+        # "w/o Module II": no token is forced to recompute by its edge energy
+        fresh = np.zeros_like(fresh)
     # Module III
     psi = spectral_entropy(f_cur, prm.entropy_norm)
     alpha, k_reuse = reuse_budget(psi, n, prm)

@@ -193,7 +193,8 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
   if (p.merge < 1 || p.merge > 4) return fail(FC_ERR_INVALID_ARG, "fc_select: merge %d", p.merge);
   if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
       !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
-      !std::isfinite(p.tau_sim))
+      !std::isfinite(p.tau_sim) || (p.no_align != 0 && p.no_align != 1) ||
+      (p.no_refresh != 0 && p.no_refresh != 1))
     return fail(FC_ERR_INVALID_ARG, "fc_select: hyper-parameter out of range");
   if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "fc_select: B=%d H=%d W=%d", B, H, W);
   const int tp = p.patch * p.merge;

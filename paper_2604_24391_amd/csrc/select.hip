@@ -571,6 +571,7 @@ struct GridParams {
   int Gph, Gpw, m;
   double tau_mig, lambda_, alpha_min, alpha_max, alpha_fixed;
   int adaptive, entropy_norm;
+  int no_align;                 // ablation "w/o Module I": shift (0, 0)
 };
 
 // ------------------------------------------------------------------------------- k_grid
@@ -705,8 +706,8 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
     const int k_reuse = (int)floor(alpha * (double)M);
     const double sd = sqrt(ev / (double)M);
     const int ki = kmax / Gw, kj = kmax - ki * Gw;
-    shift[b * 2 + 0] = ki <= Gh / 2 ? ki : ki - Gh;
-    shift[b * 2 + 1] = kj <= Gw / 2 ? kj : kj - Gw;
+    shift[b * 2 + 0] = g.no_align ? 0 : (ki <= Gh / 2 ? ki : ki - Gh);
+    shift[b * 2 + 1] = g.no_align ? 0 : (kj <= Gw / 2 ? kj : kj - Gw);
     double *sc = scalars + (size_t)b * FC_NSCALARS;
     sc[FC_SCALAR_SIM_FREQ] = sim;
     sc[FC_SCALAR_PSI] = psi;
@@ -791,7 +792,7 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
                                                      const int32_t *__restrict__ shift,
                                                      const double *__restrict__ scalars,
                                                      int32_t *__restrict__ counts, double tau_sim,
-                                                     int Gph, int Gpw, int m,
+                                                     int no_refresh, int Gph, int Gpw, int m,
                                                      float *__restrict__ sim,
                                                      uint8_t *__restrict__ reuse,
                                                      int32_t *__restrict__ ridx,
@@ -835,7 +836,7 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
     }
     sim[(size_t)b * M + t] = s;
     const double e = energy[(size_t)b * M + t];
-    const bool fr = e > thr;
+    const bool fr = !no_refresh && e > thr;
     cand = al && !fr && ((double)s >= tau_sim);
     if (flags) flags[(size_t)b * M + t] = (al ? FC_FLAG_ALIGNED : 0) | (fr ? FC_FLAG_FRESH : 0) |
                                           (cand ? FC_FLAG_CAND : 0);
@@ -955,7 +956,7 @@ fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *p
   {
     ProfScope ps(ctx, st, "fc_grid");
     GridParams g{Gph, Gpw, m, prm.tau_mig, prm.lambda_, prm.alpha_min, prm.alpha_max,
-                 prm.alpha_fixed, prm.adaptive, prm.entropy_norm};
+                 prm.alpha_fixed, prm.adaptive, prm.entropy_norm, prm.no_align};
     hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ctx->pmean, ctx->penergy, g,
                        out.energy, out.shift, out.scalars, out.counts);
     FC_HIP_TRY(hipGetLastError());
@@ -970,7 +971,7 @@ fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *p
   {
     ProfScope ps(ctx, st, "fc_topk");
     hipLaunchKernelGGL(k_topk, dim3(B), dim3(kMaxTokens), 0, st, out.energy, ctx->pdot, out.shift,
-                       out.scalars, out.counts, prm.tau_sim, Gph, Gpw, m, out.sim,
+                       out.scalars, out.counts, prm.tau_sim, prm.no_refresh, Gph, Gpw, m, out.sim,
                        out.reuse_mask, out.recompute_idx, out.n_recompute, out.flags);
     FC_HIP_TRY(hipGetLastError());
   }

@@ -49,7 +49,7 @@ class fc_select_params(ctypes.Structure):
     _fields_ = [("patch", c_int32), ("merge", c_int32), ("tau_mig", c_double),
                 ("lambda_", c_double), ("alpha_min", c_double), ("alpha_max", c_double),
                 ("adaptive", c_int32), ("alpha_fixed", c_double), ("entropy_norm", c_int32),
-                ("tau_sim", c_double)]
+                ("tau_sim", c_double), ("no_align", c_int32), ("no_refresh", c_int32)]
 
 
 class fc_select_out(ctypes.Structure):
@@ -209,11 +209,14 @@ class SelectParams:
     alpha_fixed: float = 0.5
     entropy_norm: bool = True
     tau_sim: float = 0.0
+    align: bool = True          # False: ablation "w/o Module I" (position-wise matching)
+    refresh: bool = True        # False: ablation "w/o Module II" (no edge refresh)
 
     def c(self) -> fc_select_params:
         return fc_select_params(self.patch, self.merge, self.tau_mig, self.lam, self.alpha_min,
                                 self.alpha_max, int(self.adaptive), self.alpha_fixed,
-                                int(self.entropy_norm), self.tau_sim)
+                                int(self.entropy_norm), self.tau_sim, int(not self.align),
+                                int(not self.refresh))
 
 
 @dataclass

@@ -128,4 +128,5 @@ def oracle_select_params(prm) -> osel.SelectParams:
     return osel.SelectParams(patch=prm.patch, merge=prm.merge, tau_mig=prm.tau_mig, lam=prm.lam,
                              alpha_min=prm.alpha_min, alpha_max=prm.alpha_max,
                              adaptive=prm.adaptive, alpha_fixed=prm.alpha_fixed,
-                             entropy_norm=prm.entropy_norm, tau_sim=prm.tau_sim)
+                             entropy_norm=prm.entropy_norm, tau_sim=prm.tau_sim,
+                             align=prm.align, refresh=prm.refresh)

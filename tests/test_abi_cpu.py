@@ -77,10 +77,31 @@ def test_bad_caps_rejected(fc):
     assert e.value.status == 6
 
 
-def test_struct_layouts_match_the_header(fc):
-    """ctypes mirrors of the C structs have the sizes the C compiler gives them."""
-    assert ctypes.sizeof(fc.freqcache.fc_caps) == 8 * 4
-    assert ctypes.sizeof(fc.freqcache.fc_select_params) == 72
-    assert ctypes.sizeof(fc.freqcache.fc_select_out) == 9 * 8
-    assert ctypes.sizeof(fc.freqcache.fc_kv_cache) == 32
-    assert ctypes.sizeof(fc.freqcache.fc_layer_desc) == 5 * 4 + 4 + 8 + 8 * 8
+def test_struct_layouts_match_the_header(fc, tmp_path):
+    """ctypes mirrors of the C structs have the size and field offsets that the C
+    compiler gives the header's structs (a small C program prints them)."""
+    import shutil
+    import subprocess
+    structs = [fc.freqcache.fc_caps, fc.freqcache.fc_select_params, fc.freqcache.fc_select_out,
+               fc.freqcache.fc_kv_cache, fc.freqcache.fc_layer_desc]
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "freqcache.h"', 'int main(void) {']
+    for st in structs:
+        lines.append(f'  printf("%zu\\n", sizeof({st.__name__}));')
+        for name, _ in st._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({st.__name__}, {name}));')
+    lines += ['  return 0;', '}']
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run([cc, "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    want = []
+    for st in structs:
+        want.append(ctypes.sizeof(st))
+        want += [getattr(st, name).offset for name, _ in st._fields_]
+    assert got == want

@@ -116,6 +116,25 @@ def test_merge2_episode_frames(fc, ctx):
     compare(fc, ctx, prm, fr[:3], fr[1:4])
 
 
+@pytest.mark.parametrize("ablation", [dict(align=False), dict(refresh=False),
+                                      dict(align=False, refresh=False, tau_sim=0.9),
+                                      dict(adaptive=False, alpha_fixed=0.3)])
+def test_module_ablations(fc, ctx, ablation):
+    """The module ablations of Table 3 (Sec. 6.3) on camera frames (2x2 merge) and on
+    a rolled pair: without alignment the shift is (0, 0) and every token aligned;
+    without refresh no token is fresh; the fixed 30 % budget."""
+    fr = fcdata.episode_frames(12, n_frames=3)
+    prm = fc.SelectParams(merge=2, **ablation)
+    o, _ = compare(fc, ctx, prm, fr[:2], fr[1:3])
+    rng = np.random.default_rng(13)
+    base = rng.uniform(size=(1, 3, 224, 224)).astype(np.float32)
+    o2, _ = compare(fc, ctx, fc.SelectParams(**ablation), base, np.roll(base, (14, 28), (2, 3)))
+    if not ablation.get("align", True):
+        assert (o["shift"] == 0).all() and (o2["shift"] == 0).all()
+    else:
+        assert tuple(o2["shift"][0]) == (-1, -2)
+
+
 @pytest.mark.parametrize("hw", [(154, 154), (168, 252), (196, 112), (42, 70)])
 def test_ragged_frame_sizes(fc, ctx, hw):
     """Patch rows that do not fill a 16-patch workgroup and widths that are not a

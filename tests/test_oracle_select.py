@@ -360,6 +360,46 @@ def test_fixed_budget_mode():
     assert r.alpha == 0.3 and r.k_reuse == 19
 
 
+def test_ablation_without_alignment_matches_positions():
+    """Ablation 'w/o Module I' (Table 3, Sec. 6.3): position-wise matching.  On a frame
+    rolled by one token the full method finds Delta = (-1, -1) and gives the aligned
+    tokens similarity 1; without alignment Delta = (0, 0), every token counts as
+    aligned, and each token is compared with the previous frame's token at its own
+    position, which for a roll of random content is not the same patch (similarity
+    below 1).  Identical frames give the same result either way."""
+    fr = RNG.uniform(size=(3, 112, 112))
+    cur = np.roll(fr, (14, 14), (1, 2))
+    full = osel.select_item(fr, cur, osel.SelectParams())
+    pos = osel.select_item(fr, cur, osel.SelectParams(align=False))
+    assert full.shift == (-1, -1) and pos.shift == (0, 0)
+    assert pos.aligned.all()
+    assert np.all(pos.sim < 1.0 - 1e-3)
+    # the source of token (I, J) without alignment is token (I, J): rolling the previous
+    # frame by the same whole tokens makes every position-wise pair identical
+    same = osel.select_item(cur, cur, osel.SelectParams(align=False))
+    np.testing.assert_allclose(same.sim, 1.0, atol=1e-12)
+    ref = osel.select_item(cur, cur, osel.SelectParams())
+    np.testing.assert_array_equal(same.reuse_mask, ref.reuse_mask)
+    # the global gate, energies and budget do not depend on the alignment
+    assert pos.sim_freq == full.sim_freq and pos.k_reuse == full.k_reuse
+    np.testing.assert_array_equal(pos.energy, full.energy)
+
+
+def test_ablation_without_refresh_keeps_edge_tokens_as_candidates():
+    """Ablation 'w/o Module II' (Table 3, Sec. 6.3): the edge tokens that the full
+    method refreshes become candidates again; mu, sigma and the threshold are still
+    reported.  With a budget above the candidate count every token is reused."""
+    fr = np.full((3, 112, 112), 0.2)
+    fr[:, :, 61:] = 0.8
+    prm = dict(adaptive=False, alpha_fixed=1.0)
+    full = osel.select_item(fr, fr, osel.SelectParams(**prm))
+    nof = osel.select_item(fr, fr, osel.SelectParams(refresh=False, **prm))
+    assert full.fresh.sum() == 8 and not nof.fresh.any()
+    assert nof.k_cand == full.k_cand + 8 == 64
+    assert (nof.mu, nof.sigma, nof.thr) == (full.mu, full.sigma, full.thr)
+    assert full.k_final == 56 and nof.k_final == 64 and nof.n_recompute == 0
+
+
 def test_luma_weights():
     """O1 reading: BT.601 luma; a pure grey frame maps to its grey level."""
     g = np.full((3, 14, 14), 0.25)
