@@ -110,6 +110,16 @@ def test_tiny_layer_half_reuse(fc, ctx):
     c.check(fc, ctx, [fcdata.random_reuse_ids(3, 256, 50)])
 
 
+@pytest.mark.parametrize("ids", [np.arange(11), np.arange(245, 256), np.array([3, 40, 130])])
+def test_key_blocks_after_the_last_query(fc, ctx, ids):
+    """Only a few early tokens recomputed: the current frame's key blocks after the
+    tile's last query are skipped, which here leaves two of the four key splits with
+    no block at all (their partials must drop out of the merge); late tokens skip
+    nothing."""
+    c = Case(GQA_SMALL, T=32, N=256, W=2, head=0, B=1, seed=25)
+    c.check(fc, ctx, [ids])
+
+
 @pytest.mark.parametrize("head", [0, 2])
 def test_gqa_ring_layout_two_items(fc, ctx, head):
     """GQA 7:1 with head_dim 128, a 3-frame ring at two head positions, two batch
