@@ -689,75 +689,99 @@ __device__ __forceinline__ void mg_prefix(const MArgs &a, int *pre) {
   if (lane == 63) pre[a.B] = inc;
 }
 
-// Row `row` of a tile's epilogue: trow holds its 256 accumulated columns (SwiGLU: the
-// 128 products), lane l handles columns 4 l .. 4 l + 3.  Called by whole waves.
-template <int MODE>
-__device__ __forceinline__ void mg_epi_row(const MArgs &a, const int *pre, const float *trow,
-                                           int row0, int row, int nvalid, int col0, int nt) {
+// Epilogue of 8 tile rows, rows(it) for it = 0..7, by one wave: trow(it) holds the row's
+// 256 accumulated columns (SwiGLU: the 128 products), lane l handles columns
+// 4 l .. 4 l + 3.  The rows' slots, token ids and residual inputs are loaded for all 8
+// rows first, so their memory latencies overlap instead of adding up row by row.
+template <int MODE, typename RowOf, typename TrowOf>
+__device__ __forceinline__ void mg_epi_rows8(const MArgs &a, const int *pre, RowOf rows,
+                                             TrowOf trow, int row0, int nvalid, int col0, int nt) {
   const RedArgs &r = a.r;
   const int lane = threadIdx.x & 63;
   constexpr int TN = MODE == G_GU ? MB / 2 : MB;
-  const bool rv = row < nvalid;
-  int b = 0;
-  const long slot = rv ? packed_slot(pre, a.B, a.N, row0 + row, b) : 0;
-  const int tok = rv ? tok_of(r.idx, slot, a.N) : 0;
   const int c4 = lane * 4;                                   // column within the tile
-  if (MODE == G_GU) {
-    const int col = col0 + c4;
-    if (rv && c4 < TN && col < a.Nout) {
-      const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
-      *reinterpret_cast<uint2 *>(a.act + slot * a.Nout + col) = pack_bf16x4(v.x, v.y, v.z, v.w);
-    }
-    return;
-  }
   const int col = col0 + c4;
-  const bool cv = col < a.Nout;
-  const float4 v = *reinterpret_cast<const float4 *>(trow + c4);
-  if (MODE == G_QKV) {
-    if (!rv || !cv) return;
-    const float4 bs = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col));
-    float o[4] = {v.x + bs.x, v.y + bs.y, v.z + bs.z, v.w + bs.w};
-    uint16_t *dst;
-    if (col < r.qw) {
-      // rotate-half RoPE: the partner dims are half a head away in the same row
-      const int half = r.hd / 2, dim = col % r.hd;
-      const int pc4 = dim < half ? c4 + half : c4 - half;
-      const float4 pv = *reinterpret_cast<const float4 *>(trow + pc4);
-      const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
-      const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
-      const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half + dim % half;
+  const bool cv = col < a.Nout && c4 < TN;
+  bool rv[8];
+  int bi[8], tok[8];
+  long slot[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float2 cs = rp[q];
-        o[q] = dim < half ? o[q] * cs.x - p[q] * cs.y : o[q] * cs.x + p[q] * cs.y;
+  for (int it = 0; it < 8; ++it) {
+    rv[it] = rows(it) < nvalid;
+    bi[it] = 0;
+    slot[it] = rv[it] ? packed_slot(pre, a.B, a.N, row0 + rows(it), bi[it]) : 0;
+    tok[it] = (MODE != G_GU && rv[it]) ? tok_of(r.idx, slot[it], a.N) : 0;
+  }
+  // residual inputs: x rows for O, h1 rows for down
+  uint2 xin[MODE == G_O ? 8 : 1];
+  float4 hin[MODE == G_DOWN ? 8 : 1];
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    if (MODE == G_O)
+      xin[it] = (rv[it] && cv) ? *reinterpret_cast<const uint2 *>(
+                                     r.x + ((long)bi[it] * a.N + tok[it]) * r.d + col)
+                               : make_uint2(0, 0);
+    if (MODE == G_DOWN)
+      hin[it] = (rv[it] && cv) ? *reinterpret_cast<const float4 *>(r.h1 + slot[it] * r.d + col)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const float *tr = trow(it);
+    if (MODE == G_GU) {
+      if (rv[it] && cv) {
+        const float4 v = *reinterpret_cast<const float4 *>(tr + c4);
+        *reinterpret_cast<uint2 *>(a.act + slot[it] * a.Nout + col) = pack_bf16x4(v.x, v.y, v.z, v.w);
       }
-      dst = r.q + slot * r.qw + col;
-    } else {
-      const long crow = (long)b * r.S + r.cur_row0 + tok;
-      dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
-                              : r.vc + crow * r.kw + (col - r.qw - r.kw);
+      continue;
     }
-    *reinterpret_cast<uint2 *>(dst) = pack_bf16x4(o[0], o[1], o[2], o[3]);
-  } else if (MODE == G_O) {
-    float ss = 0.f;
-    if (rv && cv) {
-      const float4 xv = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.x + ((long)b * a.N + tok) * r.d + col));
-      const float4 hv = make_float4(v.x + xv.x, v.y + xv.y, v.z + xv.z, v.w + xv.w);
-      *reinterpret_cast<float4 *>(r.h1 + slot * r.d + col) = hv;
-      const float4 gn = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.gain + col));
-      *reinterpret_cast<uint2 *>(r.hb + slot * r.d + col) =
-          pack_bf16x4(hv.x * gn.x, hv.y * gn.y, hv.z * gn.z, hv.w * gn.w);
-      ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
-    }
-    // the row's 256 columns are this wave's 64 lanes
+    const float4 v = *reinterpret_cast<const float4 *>(tr + c4);
+    if (MODE == G_QKV) {
+      if (!rv[it] || !cv) continue;
+      const float4 bs = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col));
+      float o[4] = {v.x + bs.x, v.y + bs.y, v.z + bs.z, v.w + bs.w};
+      uint16_t *dst;
+      if (col < r.qw) {
+        // rotate-half RoPE: the partner dims are half a head away in the same row
+        const int half = r.hd / 2, dim = col % r.hd;
+        const int pc4 = dim < half ? c4 + half : c4 - half;
+        const float4 pv = *reinterpret_cast<const float4 *>(tr + pc4);
+        const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
+        const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
+        const float2 *rp = r.rope + (long)(r.qpos0 + tok[it]) * half + dim % half;
 #pragma unroll
-    for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m);
-    if (rv && lane == 0 && nt < a.ss_parts) r.ssq[slot * a.ss_parts + nt] = ss;
-  } else {
-    if (!rv || !cv) return;
-    const float4 hv = *reinterpret_cast<const float4 *>(r.h1 + slot * r.d + col);
-    *reinterpret_cast<uint2 *>(r.y + ((long)b * a.N + tok) * r.d + col) =
-        pack_bf16x4(hv.x + v.x, hv.y + v.y, hv.z + v.z, hv.w + v.w);
+        for (int q = 0; q < 4; ++q) {
+          const float2 cs = rp[q];
+          o[q] = dim < half ? o[q] * cs.x - p[q] * cs.y : o[q] * cs.x + p[q] * cs.y;
+        }
+        dst = r.q + slot[it] * r.qw + col;
+      } else {
+        const long crow = (long)bi[it] * r.S + r.cur_row0 + tok[it];
+        dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
+                                : r.vc + crow * r.kw + (col - r.qw - r.kw);
+      }
+      *reinterpret_cast<uint2 *>(dst) = pack_bf16x4(o[0], o[1], o[2], o[3]);
+    } else if (MODE == G_O) {
+      float ss = 0.f;
+      if (rv[it] && cv) {
+        const float4 xv = unpack_bf16x4(xin[it]);
+        const float4 hv = make_float4(v.x + xv.x, v.y + xv.y, v.z + xv.z, v.w + xv.w);
+        *reinterpret_cast<float4 *>(r.h1 + slot[it] * r.d + col) = hv;
+        const float4 gn = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.gain + col));
+        *reinterpret_cast<uint2 *>(r.hb + slot[it] * r.d + col) =
+            pack_bf16x4(hv.x * gn.x, hv.y * gn.y, hv.z * gn.z, hv.w * gn.w);
+        ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+      }
+      // the row's 256 columns are this wave's 64 lanes
+#pragma unroll
+      for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m);
+      if (rv[it] && lane == 0 && nt < a.ss_parts) r.ssq[slot[it] * a.ss_parts + nt] = ss;
+    } else {
+      if (!rv[it] || !cv) continue;
+      const float4 hv = hin[it];
+      *reinterpret_cast<uint2 *>(r.y + ((long)bi[it] * a.N + tok[it]) * r.d + col) =
+          pack_bf16x4(hv.x + v.x, hv.y + v.y, hv.z + v.z, hv.w + v.w);
+    }
   }
 }
 
@@ -927,13 +951,11 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
       }
     }
     lds_barrier();
-    // 64 rows (two per wave-row half) x 64 four-column pieces; wave w takes rows w, w + 8, ...
-#pragma unroll
-    for (int it = 0; it < 8; ++it) {
-      const int er = w + 8 * it;                               // epilogue row 0..63
-      const int row = (er >> 5) * 128 + i * 32 + (er & 31);    // tile row
-      mg_epi_row<MODE>(a, pre, T + er * kMEpPitch, row0, row, nvalid, col0, nt);
-    }
+    // 64 rows (two per wave-row half) x 64 four-column pieces: wave w takes epilogue rows
+    // er = w + 8 it (0..63), tile rows 128 (er / 32) + 32 i + er % 32
+    mg_epi_rows8<MODE>(
+        a, pre, [&](int it) { const int er = w + 8 * it; return (er >> 5) * 128 + i * 32 + (er & 31); },
+        [&](int it) { return T + (w + 8 * it) * kMEpPitch; }, row0, nvalid, col0, nt);
     lds_barrier();                                             // the tile is free again
   }
 }
@@ -1000,12 +1022,9 @@ __global__ __launch_bounds__(512) void k_mtail(MArgs a) {
     __syncthreads();
     T = P;
   }
-#pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int er = w + 8 * it;
-    const int row = (er >> 5) * 128 + i * 32 + (er & 31);
-    mg_epi_row<MODE>(a, pre, T + er * kMEpPitch, row0, row, nvalid, col0, nt);
-  }
+  mg_epi_rows8<MODE>(
+      a, pre, [&](int it) { const int er = w + 8 * it; return (er >> 5) * 128 + i * 32 + (er & 31); },
+      [&](int it) { return T + (w + 8 * it) * kMEpPitch; }, row0, nvalid, col0, nt);
 }
 
 // ------------------------------------------------------------------------------- attention
