@@ -158,6 +158,33 @@ def test_batch_items_are_independent(fc, ctx):
             np.testing.assert_array_equal(ob[k][b], o1[k][0], err_msg=k)
 
 
+def test_two_contexts_on_two_streams(fc, ctx):
+    """Independent batches on two streams, each with its own context, overlapping in
+    time: both give exactly the single-stream outputs."""
+    prev, cur, _ = fcdata.sel_pairs(1)
+    p, c = torch.from_numpy(prev).cuda(), torch.from_numpy(cur).cuda()
+    prm = fc.SelectParams()
+    ref = fc.SelectOut.alloc(64, 1024)
+    fc.fc_select(ctx, prm, p, c, ref)
+    torch.cuda.synchronize()
+    ref_np = fcutil.select_out_np(ref)
+    ctx2 = fc.Context(fc.Caps(max_batch=64, max_height=448, max_width=448, max_tokens=1024,
+                              max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+    outs = [fc.SelectOut.alloc(64, 1024), fc.SelectOut.alloc(64, 1024)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s_ in streams:
+        s_.wait_stream(torch.cuda.current_stream())
+    for i in range(6):
+        fc.fc_select((ctx, ctx2)[i % 2], prm, p, c, outs[i % 2], stream=streams[i % 2])
+    torch.cuda.synchronize()
+    ctx2.close()
+    for o in outs:
+        on = fcutil.select_out_np(o)
+        for k, v in ref_np.items():
+            if v is not None:
+                np.testing.assert_array_equal(on[k], v, err_msg=k)
+
+
 def test_deterministic(fc, ctx):
     """Two runs on the same inputs are byte-identical."""
     prev, cur, _ = fcdata.sel_pairs(4, batch=8)
