@@ -294,41 +294,45 @@ def bench_select_batch(fc, ctx, torch):
     fc.fc_profile_read(ctx, None, reset=True)
     gbs = (frame_bytes + out_bytes) / (call_us * 1e-6) / 1e9
     spectra_gbs = frame_bytes / (kern["fc_spectra"] * 1e-6) / 1e9
-    # Independent batches on two streams (each with its own context and outputs): the
-    # next batch's frame reads overlap the previous batch's per-item chain (grid
-    # transforms, similarity, top-K), which occupies few CUs.  Same work per call.
-    ctx2 = fc.Context(fc.Caps(max_batch=B, max_height=H, max_width=W, max_tokens=1024,
-                              max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
-    outs = [out, fc.SelectOut.alloc(B, 1024)]
-    ctxs = [ctx, ctx2]
-    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    # Independent batches on two and three streams (each with its own context and
+    # outputs): the next batch's frame reads overlap the previous batch's per-item chain
+    # (grid transforms, similarity, top-K), which occupies few CUs.  Same work per call.
     main = torch.cuda.current_stream()
+    extra_ctx = [fc.Context(fc.Caps(max_batch=B, max_height=H, max_width=W, max_tokens=1024,
+                                    max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+                 for _ in range(2)]
+    ctxs = [ctx] + extra_ctx
+    outs = [out] + [fc.SelectOut.alloc(B, 1024) for _ in range(2)]
+    streams = [torch.cuda.Stream() for _ in range(3)]
 
-    def two_stream_run(n):
-        for s_ in streams:
+    def multi_stream_run(k, n):
+        for s_ in streams[:k]:
             s_.wait_stream(main)
         for i in range(n):
-            fc.fc_select(ctxs[i % 2], prm, prev, cur, outs[i % 2], stream=streams[i % 2])
-        for s_ in streams:
+            fc.fc_select(ctxs[i % k], prm, prev, cur, outs[i % k], stream=streams[i % k])
+        for s_ in streams[:k]:
             main.wait_stream(s_)
 
-    two_stream_run(4)
-    torch.cuda.synchronize()
-    e0.record()
-    two_stream_run(2 * reps)
-    e1.record()
-    torch.cuda.synchronize()
-    pipe_us = e0.elapsed_time(e1) * 1e3 / (2 * reps)
-    ctx2.close()
-    pipe_gbs = (frame_bytes + out_bytes) / (pipe_us * 1e-6) / 1e9
+    multi = {}
+    for k in (2, 3):
+        multi_stream_run(k, 2 * k)
+        torch.cuda.synchronize()
+        e0.record()
+        multi_stream_run(k, k * reps)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (k * reps)
+        g_ = (frame_bytes + out_bytes) / (us * 1e-6) / 1e9
+        multi[f"{k}_streams"] = dict(us_per_call=round(us, 2), gbs=round(g_, 1),
+                                    frac_hbm=round(g_ / HBM_PEAK_GBS, 4))
+    for c_ in extra_ctx:
+        c_.close()
+    multi["note"] = "independent 64-pair batches over 2 or 3 streams, each with its own context"
     return dict(workload="64 pairs 448x448, 14-px patches, 1024 patches/frame, adaptive",
                 call_us=round(call_us, 2), algorithmic_bytes=frame_bytes + out_bytes,
                 gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
                 spectra_gbs=round(spectra_gbs, 1), kernel_avg_us=kern,
-                two_streams=dict(us_per_call=round(pipe_us, 2), gbs=round(pipe_gbs, 1),
-                                 frac_hbm=round(pipe_gbs / HBM_PEAK_GBS, 4),
-                                 note="independent 64-pair batches alternating over two "
-                                      "streams, each with its own context"))
+                multi_stream=multi)
 
 
 def bench_ablations(fc, ctx, torch, frames, m, N):
