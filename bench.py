@@ -15,6 +15,8 @@ Also reported, each measured in the same run:
   cpu_baseline  the CPU oracle on a bounded sample of the same step;
   select_batch  fc_select on 64 pairs of 448x448 frames, GB/s of frame input;
   layer_ratios  one layer at reuse 0/25/50/75/90 %, time, MFMA utilisation;
+  tiny          the tiny configuration (one 224x224 pair, fixed 50 % budget, a toy block
+                of d 256 over 32 text + 256 visual tokens): microseconds per call;
   ablations     the module ablations of Table 3 (w/o alignment, w/o refresh, fixed
                 30 % budget) on the episode's frame pairs: mean token reuse;
   batch_episodes  16 concurrent episodes at 896x896 (1024 tokens per frame, a 4-frame
@@ -221,6 +223,7 @@ def main():
     if not args.no_extras:
         result["select_batch"] = bench_select_batch(fc, ctx, torch)
         result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
+        result["tiny"] = bench_tiny(fc, torch)
         result["ablations"] = bench_ablations(fc, ctx, torch, frames, m, N)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
@@ -363,6 +366,59 @@ def bench_ablations(fc, ctx, torch, frames, m, N):
     res["paper_context"] = ("Table 3 token reuse on R2R-CE: full 53.5 %, w/o I 19.8 %, "
                             "w/o II 57.0 %, w/o III (fixed 30 %) 38.6 %")
     return res
+
+
+def bench_tiny(fc, torch):
+    """The tiny configuration: fc_select on one 224x224 pair (256 patches, fixed 50 %
+    budget), then fc_cache_update and fc_layer_forward of a toy block (d 256, 4 heads x
+    64, SwiGLU 1024) over 32 text + 256 visual tokens; launch-latency bound."""
+    import fcdata
+    dev = torch.device("cuda:0")
+    shape = fcdata.TINY_LAYER
+    ctx = fc.Context(fc.Caps(max_batch=1, max_height=224, max_width=224, max_tokens=256,
+                             max_seq=288, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    prev_np, cur_np, _ = fcdata.tiny_pair(0)
+    prev, cur = torch.from_numpy(prev_np).to(dev), torch.from_numpy(cur_np).to(dev)
+    wt = fcdata.layer_weights(10, shape)
+    w = {k: torch.from_numpy(v.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+         for k, v in wt.items()}
+    desc = fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w)
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+
+    def rn(*shp):
+        return torch.randn(*shp, device=dev, generator=g).to(torch.bfloat16)
+    kv = fc.KVCache(rn(1, 288, shape.n_kv, shape.hd), rn(1, 288, shape.n_kv, shape.hd), 32, 256,
+                    1, head=0)
+    x, y0, y1 = rn(1, 256, shape.d), rn(1, 256, shape.d), rn(1, 256, shape.d)
+    prm = fc.SelectParams(adaptive=False, alpha_fixed=0.5)
+    out = fc.SelectOut.alloc(1, 256)
+
+    def sel():
+        fc.fc_select(ctx, prm, prev, cur, out)
+
+    def lay():
+        fc.fc_cache_update(ctx, desc, kv, y0, y1, out.shift, out.reuse_mask, 16)
+        fc.fc_layer_forward(ctx, desc, kv, x, out.recompute_idx, out.n_recompute, y1)
+
+    res = {}
+    for name, fn in (("select_us", sel), ("layer_us", lay)):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        reps = 200
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+    res["n_recompute"] = int(out.n_recompute[0])
+    ctx.close()
+    return dict(workload="224x224 pair, 256 patches, fixed 50 % budget; toy block d 256, "
+                         "4 heads x 64, SwiGLU 1024, 32 text + 256 visual tokens", **res)
 
 
 def bench_layer_ratios(fc, ctx, torch, lay, shape):
@@ -590,10 +646,35 @@ def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
         ol.layer_partial(x, res.recompute_idx, kc, vc, y_prev, lay_o, wt, shape)
     t_layer = (time.perf_counter() - t0) / reps
     t_step = t_sel + L * t_layer
+    # the oracle on the other configurations, small samples
+    import fcdata
+    other = {}
+    sp, sc, _ = fcdata.sel_pairs(1)
+    t0 = time.perf_counter()
+    for b in range(2):
+        osel.select_item(sp[b], sc[b], osel.SelectParams())
+    other["selection_64x448_pairs_per_s"] = round(2 / (time.perf_counter() - t0), 2)
+    tp, tc, _ = fcdata.tiny_pair(0)
+    tshape = fcdata.TINY_LAYER
+    twt = fcdata.layer_weights(10, tshape)
+    rng = np.random.default_rng(3)
+    tk = fcdata.bf16_round(rng.standard_normal((288, tshape.n_kv, tshape.hd), dtype=np.float32))
+    tx = fcdata.bf16_round(rng.standard_normal((256, tshape.d), dtype=np.float32))
+    t0 = time.perf_counter()
+    tres = osel.select_item(tp[0], tc[0], osel.SelectParams(adaptive=False, alpha_fixed=0.5))
+    ol.layer_partial(tx, tres.recompute_idx, tk, tk, tx, ol.Layout(T=32, N=256, W=1, head=0),
+                     twt, tshape)
+    other["tiny_select_plus_layer_ms"] = round((time.perf_counter() - t0) * 1e3, 2)
+    for r in (0, 50):
+        ids = fcdata.random_reuse_ids(100 + r, N, r)
+        t0 = time.perf_counter()
+        ol.layer_partial(x, ids, kc, vc, y_prev, lay_o, wt, shape)
+        other[f"qwen_layer_reuse{r}_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
     return dict(value=round(1.0 / t_step, 5), unit="frames/s", cores=int(cores), kind="oracle",
                 sample=f"oracle selection of one 448x448 pair ({t_sel:.2f}s) + {reps} oracle "
                        f"layer calls at n={res.n_recompute} ({t_layer:.2f}s each), extrapolated "
-                       f"to select + {L} layers = {t_step:.1f}s/step")
+                       f"to select + {L} layers = {t_step:.1f}s/step",
+                other_configs=other)
 
 
 if __name__ == "__main__":
