@@ -55,7 +55,7 @@ typedef enum {
   FC_ERR_CAPACITY = 3,      /* sizes above what the context was created for */
   FC_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed   */
   FC_ERR_NO_DEVICE = 5,     /* no usable GPU                                */
-  FC_ERR_UNSUPPORTED = 6    /* a valid request this build does not handle   */
+  FC_ERR_UNSUPPORTED = 6    /* a valid request the library does not handle  */
 } fc_status;
 
 /* Upper bounds fixed at context creation; they size the workspace.  (host) */

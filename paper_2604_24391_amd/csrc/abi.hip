@@ -125,7 +125,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   e = hipGetDeviceProperties(&prop, device);
   if (e != hipSuccess) return fail(FC_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-    return fail(FC_ERR_UNSUPPORTED, "fc_create: device is %s, this build targets gfx950",
+    return fail(FC_ERR_UNSUPPORTED, "fc_create: device is %s, the library targets gfx950",
                 prop.gcnArchName);
 
   fc_ctx *ctx = new (std::nothrow) fc_ctx();
@@ -189,7 +189,7 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
     return fail(FC_ERR_INVALID_ARG, "fc_select: an output buffer is null");
   const fc_select_params &p = *prm;
   if (p.patch != fc::kPatch)
-    return fail(FC_ERR_UNSUPPORTED, "fc_select: patch %d (this build implements P = 14)", p.patch);
+    return fail(FC_ERR_UNSUPPORTED, "fc_select: patch %d (the library implements P = 14)", p.patch);
   if (p.merge < 1 || p.merge > 4) return fail(FC_ERR_INVALID_ARG, "fc_select: merge %d", p.merge);
   if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
       !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
