@@ -1151,11 +1151,14 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
   // share of the cache
   const int tiles = a.tiles;
   const int lt = xcd_tile(blockIdx.x, (int)gridDim.x);
-  const int qt = lt % tiles;
   const int g = (lt / tiles) % a.nkv;
   const int sp = lt / (tiles * a.nkv);
   const int tiles_per_b = (a.N + QR - 1) / QR;
-  const int b = qt / tiles_per_b;
+  // an item's tiles are dispatched last first: later tiles see more of the current
+  // frame's keys (fewer skipped blocks), so the longest workgroups start first and the
+  // short ones fill the last round
+  const int b = (lt % tiles) / tiles_per_b;
+  const int qt = b * tiles_per_b + (tiles_per_b - 1 - (lt % tiles) % tiles_per_b);
   const int j0 = (qt % tiles_per_b) * QR;
   const int n = n_valid(a.nrec, b, a.N);
   if (j0 >= n) return;
