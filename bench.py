@@ -64,6 +64,9 @@ def main():
     ap.add_argument("--batch-only", action="store_true",
                     help="run only the batched-episode workload and print its record (for "
                          "profiling that workload on its own)")
+    ap.add_argument("--select-only", action="store_true",
+                    help="run only the 64-pair selection workload and print its record (for "
+                         "profiling that workload on its own)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -78,6 +81,22 @@ def main():
     import torch
     import fcdata
     import paper_2604_24391_amd as fc
+
+    if args.select_only:
+        torch.cuda.set_device(0)
+        ctx = fc.Context(fc.Caps(max_batch=64, max_height=448, max_width=448, max_tokens=1024,
+                                 max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+        rec = bench_select_batch(fc, ctx, torch)
+        ctx.close()
+        if args.calib_mb > 0:
+            n = args.calib_mb * (1 << 20) // 4
+            src = torch.ones(n, device="cuda", dtype=torch.float32)
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+        print(json.dumps(rec), flush=True)
+        return
 
     # the batched-episode frames come from a pool of forked workers, which must start
     # before this process touches the GPU
