@@ -2,10 +2,10 @@
 
 A step is one navigation step of a 32-step camera episode at batch 1:
   fc_select on the (previous, current) 448x448 frame pair (14-px patches, 2x2
-  merge -> 256 visual tokens, adaptive budget), then for each of 28
-  Qwen2.5-VL-7B-shaped bf16 decoder layers (128 text + 8 frames x 256 tokens =
-  2176 cached positions) the window advance, fc_cache_update and
-  fc_layer_forward on the tokens the selection left for recompute.
+  merge -> 256 visual tokens, adaptive budget), then the window advance and cache
+  remap of 28 Qwen2.5-VL-7B-shaped bf16 decoder layers (128 text + 8 frames x 256
+  tokens = 2176 cached positions) in one fc_cache_update_layers call, and
+  fc_layer_forward of each layer on the tokens the selection left for recompute.
 Inputs (frames, token embeddings, weights, caches) are resident in HBM before
 the timed region.  value = steps/s = frames/s at batch 1.
 
@@ -165,10 +165,15 @@ def main():
         fc.fc_select(ctx, prm, prev, frames[fi:fi + 1], sel)
         x = emb[fi:fi + 1]
         nxt = 1 - cur_y
+        # every layer's window advance and cache remap in one launch: a layer reads
+        # only the recomputed rows of its input, so the reused rows the remap writes
+        # into the next layer's input may land before the earlier layers run
         for lay in layers:
             lay["kv"].advance()
-            fc.fc_cache_update(ctx, lay["desc"], lay["kv"], lay["y"][cur_y], lay["y"][nxt],
-                               sel.shift, sel.reuse_mask, gw)
+        fc.fc_cache_update_layers(ctx, layers[0]["desc"], [lay["kv"] for lay in layers],
+                                  [lay["y"][cur_y] for lay in layers],
+                                  [lay["y"][nxt] for lay in layers], sel.shift, sel.reuse_mask, gw)
+        for lay in layers:
             fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, sel.recompute_idx,
                                 sel.n_recompute, lay["y"][nxt])
             x = lay["y"][nxt]
@@ -507,8 +512,8 @@ def bench_batch_episodes(fc, torch, frames_np, steps, L):
     """The batched-episode workload: 16 independent episodes, 896x896 frames (4096
     patches, 2x2 merge -> 1024 tokens), a 4-frame window plus 128 text tokens (4224
     cached positions), 28 Qwen2.5-VL-7B-shaped layers.  One step = fc_select on the 16
-    (previous, current) pairs, then per layer the window advance, fc_cache_update and
-    fc_layer_forward of the 16 items' recomputed tokens."""
+    (previous, current) pairs, the window advance and one fc_cache_update_layers call
+    for all layers, then per layer fc_layer_forward of the 16 items' recomputed tokens."""
     import fcdata
     dev = torch.device("cuda:0")
     shape = fcdata.QWEN_LAYER
@@ -560,10 +565,15 @@ def bench_batch_episodes(fc, torch, frames_np, steps, L):
         fc.fc_select(ctx, prm, frames[fi - 1], frames[fi], sel)
         x = emb[fi]
         nxt = 1 - cur_y
+        # every layer's window advance and cache remap in one launch: a layer reads
+        # only the recomputed rows of its input, so the reused rows the remap writes
+        # into the next layer's input may land before the earlier layers run
         for lay in layers:
             lay["kv"].advance()
-            fc.fc_cache_update(ctx, lay["desc"], lay["kv"], lay["y"][cur_y], lay["y"][nxt],
-                               sel.shift, sel.reuse_mask, gw)
+        fc.fc_cache_update_layers(ctx, layers[0]["desc"], [lay["kv"] for lay in layers],
+                                  [lay["y"][cur_y] for lay in layers],
+                                  [lay["y"][nxt] for lay in layers], sel.shift, sel.reuse_mask, gw)
+        for lay in layers:
             fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, sel.recompute_idx,
                                 sel.n_recompute, lay["y"][nxt])
             x = lay["y"][nxt]

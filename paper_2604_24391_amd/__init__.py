@@ -6,7 +6,8 @@ is the Python binding (argument marshalling only) plus the in-tree build step.
 """
 from .freqcache import (  # noqa: F401
     Caps, Context, FcError, KVCache, LayerDesc, SelectOut, SelectParams, EXPORTS, COUNTS,
-    SCALARS, FLAG_ALIGNED, FLAG_CAND, FLAG_FRESH, fc_cache_update, fc_create, fc_destroy,
+    SCALARS, FLAG_ALIGNED, FLAG_CAND, FLAG_FRESH, fc_cache_update, fc_cache_update_layers,
+    fc_create, fc_destroy,
     fc_last_error, fc_layer_forward, fc_profile_enable, fc_profile_only, fc_profile_read, fc_select,
     fc_version,
     lib, token_grid)

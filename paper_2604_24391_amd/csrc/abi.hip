@@ -298,6 +298,36 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
                                  reinterpret_cast<hipStream_t>(stream));
 }
 
+fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_t n_layers,
+                                 const fc_kv_cache *kvs, const uint16_t *const *y_prev,
+                                 uint16_t *const *y_cur, const int32_t *shift,
+                                 const uint8_t *reuse_mask, int32_t grid_w, int32_t B,
+                                 void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: null context");
+  if (n_layers < 1 || !kvs || !y_prev || !y_cur)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: n_layers %d or null arrays", n_layers);
+  if (!shift || !reuse_mask)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: null buffer");
+  for (int l = 0; l < n_layers; ++l) {
+    fc_status st = check_layer(ctx, layer, &kvs[l], B, "fc_cache_update_layers");
+    if (st != FC_OK) return st;
+    if (!y_prev[l] || !y_cur[l] || y_prev[l] == y_cur[l])
+      return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d: null or aliased outputs", l);
+    if (kvs[l].text_tokens != kvs[0].text_tokens || kvs[l].frame_tokens != kvs[0].frame_tokens ||
+        kvs[l].window != kvs[0].window || kvs[l].head != kvs[0].head)
+      return fail(FC_ERR_SHAPE, "fc_cache_update_layers: layer %d's cache layout or head differs", l);
+  }
+  if (grid_w < 1 || kvs[0].frame_tokens % grid_w)
+    return fail(FC_ERR_SHAPE, "fc_cache_update_layers: grid_w %d does not divide N=%d", grid_w,
+                kvs[0].frame_tokens);
+  if ((layer->n_kv_heads * layer->head_dim) % 8 || layer->d_model % 8)
+    return fail(FC_ERR_SHAPE, "fc_cache_update_layers: row sizes must be multiples of 8 elements");
+  fc_status st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_cache_update_layers(ctx, *layer, n_layers, kvs, y_prev, y_cur, shift, reuse_mask,
+                                        grid_w, B, reinterpret_cast<hipStream_t>(stream));
+}
+
 fc_status fc_profile_enable(fc_ctx *ctx, int32_t on) {
   if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_profile_enable: null context");
   ctx->prof = on != 0;

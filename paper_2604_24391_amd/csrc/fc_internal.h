@@ -96,6 +96,10 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
 fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                               const uint8_t *reuse, int grid_w, int B, hipStream_t st);
+fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_layers,
+                                     const fc_kv_cache *kvs, const uint16_t *const *y_prev,
+                                     uint16_t *const *y_cur, const int32_t *shift,
+                                     const uint8_t *reuse, int grid_w, int B, hipStream_t st);
 
 fc_status upload_select_tables();
 

@@ -1665,7 +1665,7 @@ struct CacheArgs {
 
 // One thread per 16-B chunk of a reused token's K row, V row and output row, so that
 // every copy of the remap is in flight at once.
-__global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
+__device__ __forceinline__ void cache_copy(const CacheArgs &c) {
   const int b = blockIdx.y;
   const int kc = c.kvw / 8, cpt = 2 * kc + c.d / 8;             // chunks per token
   const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1691,6 +1691,29 @@ __global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) {
     uint4 *yd = reinterpret_cast<uint4 *>(c.y_cur + ((long)b * c.N + tok) * c.d);
     yd[x] = ys[x];
   }
+}
+
+__global__ __launch_bounds__(256) void k_cache_update(CacheArgs c) { cache_copy(c); }
+
+// The remap of up to kCacheLayers layers' caches in one launch (blockIdx.z = layer);
+// each layer's rows move exactly as in k_cache_update.
+constexpr int kCacheLayers = 32;
+struct CacheLayers {
+  CacheArgs c;                                   // shared sizes; pointers of layer 0
+  uint16_t *kc[kCacheLayers], *vc[kCacheLayers];
+  const uint16_t *yp[kCacheLayers];
+  uint16_t *yc[kCacheLayers];
+};
+__global__ __launch_bounds__(256) void k_cache_update_layers(CacheLayers m) {
+  CacheArgs c = m.c;
+  const int l = blockIdx.z;
+  c.kc = m.kc[l];
+  c.vc = m.vc[l];
+  c.ksrc = m.kc[l];
+  c.vsrc = m.vc[l];
+  c.y_prev = m.yp[l];
+  c.y_cur = m.yc[l];
+  cache_copy(c);
 }
 
 // Column groups and K splits of a weight-streaming GEMM: columns in 16-wide blocks,
@@ -2027,6 +2050,55 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
   const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
   hipLaunchKernelGGL(k_cache_update, dim3((unsigned)((chunks + 255) / 256), B), dim3(256), 0, st, c);
   FC_HIP_TRY(hipGetLastError());
+  return FC_OK;
+}
+
+fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_layers,
+                                     const fc_kv_cache *kvs, const uint16_t *const *y_prev,
+                                     uint16_t *const *y_cur, const int32_t *shift,
+                                     const uint8_t *reuse, int grid_w, int B, hipStream_t st) {
+  const fc_kv_cache &kv = kvs[0];
+  if (kv.window == 1) {
+    // in-place overwrite of the only frame slot: the per-layer path stages the old rows
+    for (int l = 0; l < n_layers; ++l) {
+      fc_status s = launch_cache_update(ctx, L, kvs[l], y_prev[l], y_cur[l], shift, reuse, grid_w,
+                                        B, st);
+      if (s != FC_OK) return s;
+    }
+    return FC_OK;
+  }
+  const int N = kv.frame_tokens;
+  const int S = kv.text_tokens + kv.window * N;
+  const int kvw = L.n_kv_heads * L.head_dim;
+  const int cur_slot = (kv.head + kv.window - 1) % kv.window;
+  const int prev_slot = (kv.head + kv.window - 2) % kv.window;
+  CacheLayers m{};
+  CacheArgs &c = m.c;
+  c.shift = shift;
+  c.reuse = reuse;
+  c.N = N;
+  c.S = S;
+  c.kvw = kvw;
+  c.d = L.d_model;
+  c.gw = grid_w;
+  c.gh = N / grid_w;
+  c.cur_row0 = kv.text_tokens + cur_slot * N;
+  c.src_bstride = (long)S * kvw;
+  c.src_row0 = kv.text_tokens + prev_slot * N;
+  ProfScope ps(ctx, st, "fc_cache_update");
+  const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
+  for (int l0 = 0; l0 < n_layers; l0 += kCacheLayers) {
+    const int nl = std::min(kCacheLayers, n_layers - l0);
+    for (int i = 0; i < nl; ++i) {
+      m.kc[i] = kvs[l0 + i].k;
+      m.vc[i] = kvs[l0 + i].v;
+      m.yp[i] = y_prev[l0 + i];
+      m.yc[i] = y_cur[l0 + i];
+    }
+    hipLaunchKernelGGL(k_cache_update_layers, dim3((unsigned)((chunks + 255) / 256), B, nl),
+                       dim3(256), 0, st, m);
+    FC_HIP_TRY(hipGetLastError());
+  }
   return FC_OK;
 }
 

@@ -29,8 +29,8 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
-           "fc_cache_update", "fc_layer_forward", "fc_profile_enable", "fc_profile_only",
-           "fc_profile_read")
+           "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
+           "fc_profile_only", "fc_profile_read")
 
 
 class FcError(RuntimeError):
@@ -91,6 +91,10 @@ def lib() -> ctypes.CDLL:
         L.fc_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                       ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                       c_void_p, c_int32, c_int32, c_void_p]
+        L.fc_cache_update_layers.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc), c_int32,
+                                             ctypes.POINTER(fc_kv_cache), ctypes.POINTER(c_void_p),
+                                             ctypes.POINTER(c_void_p), c_void_p, c_void_p, c_int32,
+                                             c_int32, c_void_p]
         L.fc_layer_forward.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                        ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_int32, c_void_p]
@@ -98,8 +102,9 @@ def lib() -> ctypes.CDLL:
         L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
-        for n in ("fc_create", "fc_destroy", "fc_select", "fc_cache_update", "fc_layer_forward",
-                  "fc_profile_enable", "fc_profile_only", "fc_profile_read"):
+        for n in ("fc_create", "fc_destroy", "fc_select", "fc_cache_update",
+                  "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
+                  "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
         _lib = L
     return _lib
@@ -364,6 +369,29 @@ def fc_cache_update(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev: torch.T
         ctx.handle, ctypes.byref(cl), ctypes.byref(ck),
         _ptr(y_prev, torch.bfloat16, B * N * d, "y_prev"),
         _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur"),
+        _ptr(shift, torch.int32, 2 * B, "shift"),
+        _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
+
+
+def fc_cache_update_layers(ctx: Context, layer: LayerDesc, kvs, y_prevs, y_curs,
+                           shift: torch.Tensor, reuse_mask: torch.Tensor, grid_w: int,
+                           stream=None):
+    """fc_cache_update over several layers' caches in one launch.
+
+    kvs, y_prevs, y_curs: equal-length sequences (one entry per layer); the caches
+    share their layout and have all been advanced to the same step."""
+    n = len(kvs)
+    if n < 1 or len(y_prevs) != n or len(y_curs) != n:
+        raise ValueError("fc_cache_update_layers: kvs, y_prevs and y_curs need one entry per layer")
+    B = y_curs[0].shape[0]
+    N, d = kvs[0].frame_tokens, layer.d_model
+    kvw = layer.n_kv_heads * layer.head_dim
+    cl = layer.c()
+    cks = (fc_kv_cache * n)(*[kv.c(B, kvw) for kv in kvs])
+    yp = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_prev") for y in y_prevs])
+    yc = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_cur") for y in y_curs])
+    _check(lib().fc_cache_update_layers(
+        ctx.handle, ctypes.byref(cl), n, cks, yp, yc,
         _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
 

@@ -50,6 +50,8 @@ def test_null_arguments_are_rejected_without_a_device(fc):
     assert "null" in fc.fc_last_error()
     assert lib.fc_layer_forward(None, None, None, None, None, None, None, 1, None) == 1
     assert lib.fc_cache_update(None, None, None, None, None, None, None, 16, 1, None) == 1
+    assert lib.fc_cache_update_layers(None, None, 2, None, None, None, None, None, 16, 1,
+                                      None) == 1
     assert lib.fc_profile_enable(None, 1) == 1
     assert lib.fc_destroy(None) == 1
 

@@ -200,6 +200,65 @@ def test_cache_update_matches_oracle(fc, ctx, W, head, B):
         assert mask[b].sum() > 0
 
 
+@pytest.mark.parametrize("W,head,n_layers", [(1, 0, 3), (3, 2, 4), (2, 1, 35)])
+def test_cache_update_layers_matches_oracle(fc, ctx, W, head, n_layers):
+    """fc_cache_update_layers (one launch for many layers' caches) against the oracle's
+    remap of each layer (Sec. 4.1 alignment, Eq. 4-2): every layer's cache and output
+    buffer holds different bytes, so a layer reading another's rows fails.  35 layers
+    take two launches of at most 32; W = 1 takes the in-place per-layer path."""
+    shape = GQA_SMALL
+    N, gw, T, B = 64, 8, 16, 2
+    lay = ol.Layout(T=T, N=N, W=W, head=head)
+    rng = np.random.default_rng(7000 + 10 * W + n_layers)
+    kvw = shape.n_kv * shape.hd
+    shifts = np.array([[1, -2], [-3, 1]], np.int32)
+    mask = np.zeros((B, N), np.uint8)
+    for b in range(B):
+        I, J = np.divmod(np.arange(N), gw)
+        si, sj = I + shifts[b, 0], J + shifts[b, 1]
+        aligned = (si >= 0) & (si < N // gw) & (sj >= 0) & (sj < gw)
+        mask[b] = aligned & (rng.random(N) < 0.6)
+    host, kvs, yps, ycs = [], [], [], []
+    for _ in range(n_layers):
+        k = rng.integers(0, 1 << 16, size=(B, lay.S, shape.n_kv, shape.hd), dtype=np.uint16)
+        v = rng.integers(0, 1 << 16, size=k.shape, dtype=np.uint16)
+        y_prev = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+        y_cur = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+        host.append((k, v, y_prev, y_cur))
+        kvs.append(fc.KVCache(fcutil.bf16_gpu(k), fcutil.bf16_gpu(v), T, N, W, head))
+        yps.append(fcutil.bf16_gpu(y_prev))
+        ycs.append(fcutil.bf16_gpu(y_cur))
+    wg = fcutil.weights_gpu(fcdata.layer_weights(0, shape))
+    desc = fcutil.layer_desc(shape, wg)
+    fc.fc_cache_update_layers(ctx, desc, kvs, yps, ycs, torch.from_numpy(shifts).cuda(),
+                              torch.from_numpy(mask).cuda(), gw)
+    torch.cuda.synchronize()
+    for (k, v, y_prev, y_cur), kv, yc in zip(host, kvs, ycs):
+        kg, vg, yg = fcutil.bf16_np(kv.k), fcutil.bf16_np(kv.v), fcutil.bf16_np(yc)
+        for b in range(B):
+            ko, vo, yo = ol.cache_update(k[b].reshape(lay.S, kvw), v[b].reshape(lay.S, kvw),
+                                         y_prev[b], y_cur[b], tuple(shifts[b]), mask[b], gw, lay)
+            np.testing.assert_array_equal(kg[b].reshape(lay.S, kvw), ko)
+            np.testing.assert_array_equal(vg[b].reshape(lay.S, kvw), vo)
+            np.testing.assert_array_equal(yg[b], yo)
+    assert mask.sum() > 0
+
+
+def test_cache_update_layers_rejects_mixed_heads(fc, ctx):
+    """Caches advanced to different steps cannot share one remap."""
+    shape = GQA_SMALL
+    N, T, W, B = 64, 16, 3, 1
+    S = T + W * N
+    mk = lambda: torch.zeros(B, S, shape.n_kv, shape.hd, dtype=torch.bfloat16, device="cuda")
+    kvs = [fc.KVCache(mk(), mk(), T, N, W, 0), fc.KVCache(mk(), mk(), T, N, W, 1)]
+    ys = [torch.zeros(B, N, shape.d, dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    desc = fcutil.layer_desc(shape, fcutil.weights_gpu(fcdata.layer_weights(0, shape)))
+    with pytest.raises(fc.FcError, match="head differs"):
+        fc.fc_cache_update_layers(ctx, desc, kvs, ys[:2], ys[2:],
+                                  torch.zeros(B, 2, dtype=torch.int32, device="cuda"),
+                                  torch.zeros(B, N, dtype=torch.uint8, device="cuda"), 8)
+
+
 # ----------------------------------------------------------------- many gathered rows
 # With B * N >= 2048 token slots the projections run as square MFMA tiles with fused
 # epilogues (the batched-episode regime); these cases take that path.
