@@ -176,12 +176,14 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
                           const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                           const uint8_t *reuse_mask, int32_t grid_w, int32_t B, void *stream);
 
-/* The same remap for the caches of n_layers layers at once (one launch): kvs[l],
+/* The remap of Sec. 4.1 / Eq. 4-2 for the caches of n_layers layers at once (one launch): kvs[l],
  * y_prev[l] and y_cur[l] (host arrays of n_layers entries, device pointers inside)
  * are layer l's cache and output buffers.  The layers share `layer`'s dimensions and
  * the caches' text_tokens, frame_tokens, window and head (all advanced to the same
  * step); otherwise FC_ERR_SHAPE.  Equivalent to fc_cache_update on each layer in
- * turn; a window of one frame (in-place overwrite) runs those per-layer calls. */
+ * turn; a window of one frame (in-place overwrite) runs those per-layer calls.
+ * The layers are copied concurrently, so no two layers' K, V or output buffers
+ * may overlap (not checked). */
 fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_t n_layers,
                                  const fc_kv_cache *kvs, const uint16_t *const *y_prev,
                                  uint16_t *const *y_cur, const int32_t *shift,
