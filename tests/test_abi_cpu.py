@@ -107,3 +107,12 @@ def test_struct_layouts_match_the_header(fc, tmp_path):
         want.append(ctypes.sizeof(st))
         want += [getattr(st, name).offset for name, _ in st._fields_]
     assert got == want
+
+
+def test_cache_update_layers_binding_checks_lengths(fc):
+    """The binding refuses per-layer lists of different lengths before any call."""
+    with pytest.raises(ValueError, match="one entry per layer"):
+        fc.fc_cache_update_layers(None, None, [], [], [], None, None, 16)
+    with pytest.raises(ValueError, match="one entry per layer"):
+        fc.fc_cache_update_layers(None, None, [object()], [object(), object()], [object()], None,
+                                  None, 16)
