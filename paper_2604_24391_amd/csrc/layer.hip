@@ -428,15 +428,15 @@ __device__ __forceinline__ float4 sum_parts(const RedArgs &r, long slot, int c) 
   return v;
 }
 
+// Sum over a 256-thread workgroup: a butterfly within each wave, then the four wave
+// sums in a fixed order (every thread gets the same bits).
 __device__ float block_sum256(float v, float *red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   const int t = threadIdx.x;
-  red[t] = v;
+  if ((t & 63) == 0) red[t >> 6] = v;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (t < s) red[t] += red[t + s];
-    __syncthreads();
-  }
-  const float res = red[0];
+  const float res = (red[0] + red[1]) + (red[2] + red[3]);
   __syncthreads();
   return res;
 }
@@ -454,24 +454,34 @@ __global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict_
   if (j >= n_valid(nrec, b, N)) return;
   const int tok = tok_of(idx, slot, N);
   const uint16_t *xr = x + ((long)b * N + tok) * d;
+  // the row is read once and held in registers (d <= 8192: at most 4 chunks a thread)
+  constexpr int kIt = 4;
+  U16x8 v[kIt];
   float ss = 0.f;
-  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
-    const U16x8 v = *reinterpret_cast<const U16x8 *>(xr + c);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float f = bf2f(v.v[e]);
-      ss = fmaf(f, f, ss);
+  for (int it = 0; it < kIt; ++it) {
+    const int c = (it * 256 + threadIdx.x) * 8;
+    if (c < d) {
+      v[it] = *reinterpret_cast<const U16x8 *>(xr + c);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = bf2f(v[it].v[e]);
+        ss = fmaf(f, f, ss);
+      }
     }
   }
   ss = block_sum256(ss, red);
   const float inv = 1.f / sqrtf(ss / (float)d + eps);
-  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
-    const U16x8 v = *reinterpret_cast<const U16x8 *>(xr + c);
-    const U16x8 g = *reinterpret_cast<const U16x8 *>(gain + c);
-    U16x8 o;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o.v[e] = f2bf(bf2f(v.v[e]) * inv * bf2f(g.v[e]));
-    *reinterpret_cast<U16x8 *>(xs + slot * d + c) = o;
+  for (int it = 0; it < kIt; ++it) {
+    const int c = (it * 256 + threadIdx.x) * 8;
+    if (c < d) {
+      const U16x8 g = *reinterpret_cast<const U16x8 *>(gain + c);
+      U16x8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o.v[e] = f2bf(bf2f(v[it].v[e]) * inv * bf2f(g.v[e]));
+      *reinterpret_cast<U16x8 *>(xs + slot * d + c) = o;
+    }
   }
 }
 
