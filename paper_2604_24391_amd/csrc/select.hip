@@ -567,6 +567,71 @@ __device__ void fft2_wave(double2 *X, double2 *T, const double2 *twh, const doub
   __syncthreads();
 }
 
+// Two independent grids through the same transform in one pass: every stage issues the
+// lane exchanges of both before either butterfly, so the two shuffle chains overlap.
+// Each grid gets exactly the operations of fft_lanes (same results bit for bit).
+template <int G, bool INV>
+__device__ __forceinline__ void fft_lanes2(double2 &x, double2 &y, int i, const double2 *tw) {
+  constexpr int LG = G == 1 ? 0 : __builtin_ctz(G);
+  double2 w[LG > 0 ? LG : 1];
+#pragma unroll
+  for (int st = 0; st < LG; ++st) {
+    const int h = G >> (st + 1);
+    w[st] = tw[(i & (h - 1)) * (G / (2 * h))];
+    if (INV) w[st].y = -w[st].y;
+  }
+#pragma unroll
+  for (int st = 0; st < LG; ++st) {
+    const int h = G >> (st + 1);
+    const double px = xor_lane_d(x.x, h), py = xor_lane_d(x.y, h);
+    const double qx = xor_lane_d(y.x, h), qy = xor_lane_d(y.y, h);
+    const bool up = i & h;
+    const double dx = px - x.x, dy = py - x.y;
+    const double ux = dx * w[st].x - dy * w[st].y, uy = dx * w[st].y + dy * w[st].x;
+    x = up ? make_double2(ux, uy) : make_double2(x.x + px, x.y + py);
+    const double ex = qx - y.x, ey = qy - y.y;
+    const double vx = ex * w[st].x - ey * w[st].y, vy = ex * w[st].y + ey * w[st].x;
+    y = up ? make_double2(vx, vy) : make_double2(y.x + qx, y.y + qy);
+  }
+}
+template <bool INV>
+__device__ __forceinline__ void fft_lanes2_rt(double2 &x, double2 &y, int i, int g, const double2 *tw) {
+  switch (g) {
+    case 64: fft_lanes2<64, INV>(x, y, i, tw); break;
+    case 32: fft_lanes2<32, INV>(x, y, i, tw); break;
+    case 16: fft_lanes2<16, INV>(x, y, i, tw); break;
+    case 8: fft_lanes2<8, INV>(x, y, i, tw); break;
+    case 4: fft_lanes2<4, INV>(x, y, i, tw); break;
+    case 2: fft_lanes2<2, INV>(x, y, i, tw); break;
+    default: break;
+  }
+}
+// fft2_wave on two grids X and Y at once; T and U are their transposed scratch grids.
+template <bool INV>
+__device__ void fft2_wave2(double2 *X, double2 *Y, double2 *T, double2 *U, const double2 *twh,
+                           const double2 *tww, int Gh, int Gw) {
+  const int t = threadIdx.x, M = Gh * Gw, TP = Gh + 1;
+  const int lw = __ffs(Gw) - 1, lh = __ffs(Gh) - 1;
+  if (t < M) {
+    const int row = t >> lw, col = t & (Gw - 1);
+    double2 a = X[t], c = Y[t];
+    fft_lanes2_rt<INV>(a, c, col, Gw, tww);
+    const int v = lw ? (int)(__brev((unsigned)col) >> (32 - lw)) : 0;
+    T[v * TP + row] = a;
+    U[v * TP + row] = c;
+  }
+  __syncthreads();
+  if (t < M) {
+    const int v = t >> lh, y = t & (Gh - 1);
+    double2 a = T[v * TP + y], c = U[v * TP + y];
+    fft_lanes2_rt<INV>(a, c, y, Gh, twh);
+    const int u = lh ? (int)(__brev((unsigned)y) >> (32 - lh)) : 0;
+    X[u * Gw + v] = a;
+    Y[u * Gw + v] = c;
+  }
+  __syncthreads();
+}
+
 struct GridParams {
   int Gph, Gpw, m;
   double tau_mig, lambda_, alpha_min, alpha_max, alpha_fixed;
@@ -576,7 +641,8 @@ struct GridParams {
 
 // ------------------------------------------------------------------------------- k_grid
 // One workgroup of 1024 threads per frame pair, one thread per grid point (M <= 1024).
-// LDS: three complex grids and the twiddles of both axes.
+// LDS: four complex grids (two maps, two transposed scratch grids) and the twiddles
+// of both axes.
 constexpr int kGridThreads = 1024;
 __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict__ pmean,
                                                        const double *__restrict__ penergy,
@@ -585,7 +651,7 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
                                                        double *__restrict__ scalars,
                                                        int32_t *__restrict__ counts) {
   constexpr int NW = kGridThreads / 64;
-  __shared__ double2 A[kMaxTokens], Bg[kMaxTokens], C[kMaxTokens + 64];
+  __shared__ double2 A[kMaxTokens], Bg[kMaxTokens], C[kMaxTokens + 64], C2[kMaxTokens + 64];
   __shared__ double2 twh[kMaxTokens], tww[kMaxTokens];
   __shared__ double red[NW * 7 + 7];
   __shared__ double bestv[NW];
@@ -629,8 +695,7 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
   // forward 2-D transforms of both maps, each on its own (a zero map must give an
   // exactly zero spectrum: the Sim_freq of Eq. 3-3 is defined as 0 there)
   if (wave_fft) {
-    fft2_wave<false>(A, C, twh, tww, Gh, Gw);
-    fft2_wave<false>(Bg, C, twh, tww, Gh, Gw);
+    fft2_wave2<false>(A, Bg, C, C2, twh, tww, Gh, Gw);
   } else {
     dft2<false>(A, C, twh, tww, Gh, Gw);
     dft2<false>(Bg, C, twh, tww, Gh, Gw);
