@@ -336,7 +336,19 @@ def select_batch(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) ->
 def decision_margins(res: SelectResult, prm: SelectParams) -> dict:
     """How close each of the oracle's decisions came to flipping (relative), for
     auditing any mismatch against the GPU: a mismatch is tolerated only where the
-    oracle's own margin is below 1e-5."""
+    oracle's own margin is below 1e-5.
+
+      threshold  per token, |E - thr| / |thr|            (refresh rule, Eq. 4-3)
+      topk       (key_(K+1) - key_K) / key_(K+1) over the sorted candidate keys
+                 (the ascending top-K boundary of Algorithm 1); inf without one
+      budget     |alpha N - round(alpha N)| / (alpha N)  (floor of Eq. 4-4);
+                 inf for a fixed ratio
+      gate       |Sim_freq - tau_mig| / tau_mig          (migration gate)
+      shift      (r_1 - r_2) / |r_1| of the two largest phase-correlation values
+                 (argmax of Eq. 4-1)
+      tau_sim    per token, |sim - tau_sim| / tau_sim where the similarity floor
+                 is active (tau_sim > 0 and the token aligned); inf elsewhere
+    """
     n = res.energy.size
     thr = res.thr
     thr_m = np.abs(res.energy - thr) / max(abs(thr), 1e-300)
@@ -352,5 +364,9 @@ def decision_margins(res: SelectResult, prm: SelectParams) -> dict:
     gate_m = abs(res.sim_freq - prm.tau_mig) / prm.tau_mig
     r = np.sort(res.response.ravel())
     shift_m = (r[-1] - r[-2]) / max(abs(r[-1]), 1e-300) if r.size > 1 else np.inf
+    if prm.tau_sim > 0:
+        sim_m = np.where(res.aligned, np.abs(res.sim - prm.tau_sim) / prm.tau_sim, np.inf)
+    else:
+        sim_m = np.full(n, np.inf)
     return dict(threshold=thr_m, topk=float(topk_m), budget=float(budget_m),
-                gate=float(gate_m), shift=float(shift_m))
+                gate=float(gate_m), shift=float(shift_m), tau_sim=sim_m)

@@ -882,7 +882,9 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
     const int I = t / Gw, J = t - I * Gw;
     const int si = I + shift[b * 2 + 0], sj = J + shift[b * 2 + 1];
     const bool al = si >= 0 && si < Gh && sj >= 0 && sj < Gw;
-    float s = 0.f;
+    // the cosine in float64; the similarity floor is applied to it before the
+    // exported value is rounded to float32
+    double cs = 0.0;
     if (al) {
       double dot = 0.0, n1 = 0.0, n2 = 0.0;
       for (int a2 = 0; a2 < m; ++a2)
@@ -893,16 +895,16 @@ __global__ __launch_bounds__(kMaxTokens) void k_topk(const double *__restrict__ 
           n2 += pdot[((size_t)b * 3 + 2) * Np + p];
         }
       if (n1 == 0.0 && n2 == 0.0)
-        s = 1.f;
+        cs = 1.0;
       else if (n1 == 0.0 || n2 == 0.0)
-        s = 0.f;
+        cs = 0.0;
       else
-        s = (float)(dot / (sqrt(n1) * sqrt(n2)));
+        cs = dot / (sqrt(n1) * sqrt(n2));
     }
-    sim[(size_t)b * M + t] = s;
+    sim[(size_t)b * M + t] = (float)cs;
     const double e = energy[(size_t)b * M + t];
     const bool fr = !no_refresh && e > thr;
-    cand = al && !fr && ((double)s >= tau_sim);
+    cand = al && !fr && cs >= tau_sim;
     if (flags) flags[(size_t)b * M + t] = (al ? FC_FLAG_ALIGNED : 0) | (fr ? FC_FLAG_FRESH : 0) |
                                           (cand ? FC_FLAG_CAND : 0);
     if (cand) key = (unsigned long long)__double_as_longlong(e);

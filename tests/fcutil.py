@@ -78,13 +78,23 @@ def check_valid_selection(o: dict, b: int, N: int):
     np.testing.assert_array_equal(ids, np.flatnonzero(~reuse))
 
 
-def check_select(o: dict, res: osel.SelectResult, prm: osel.SelectParams, b: int) -> dict:
-    """Compare item b of the GPU outputs with the oracle; returns the oracle margins.
+class Escapes(list):
+    """Names of the decisions where the GPU and the oracle differ but the oracle's own
+    margin is below MARGIN (the only mismatches the comparison can tolerate)."""
 
-    Scores must be within tolerance.  Every decision must agree, except where
-    the oracle's own margin for it is below MARGIN; then the GPU outcome need
-    only be valid for its own masks and keys."""
+
+def check_select(o: dict, res: osel.SelectResult, prm: osel.SelectParams, b: int,
+                 allow_escapes: bool = False):
+    """Compare item b of the GPU outputs with the oracle; returns (margins, escapes).
+
+    Scores must be within tolerance.  Every decision must agree bit for bit.  A
+    mismatch is an "escape" only where the oracle's own margin for that decision is
+    below MARGIN; any other mismatch fails at once.  Escapes also fail unless
+    `allow_escapes` (no committed seed needs that: a seed that did would be marked
+    xfail with the margin as its reason).  Decisions downstream of an escaped one are
+    still compared wherever they do not depend on it."""
     N = res.energy.size
+    esc = Escapes()
     check_valid_selection(o, b, N)
     _close(o["energy"][b], res.energy, "energy")
     _close(o["sim"][b], res.sim, "sim")
@@ -94,34 +104,57 @@ def check_select(o: dict, res: osel.SelectResult, prm: osel.SelectParams, b: int
         assert abs(g - w) <= SCORE_RTOL * abs(w) + 1e-12, f"{name}: gpu {g!r} oracle {w!r}"
     mg = osel.decision_margins(res, prm)
     k_reuse, k_cand, k_final, flushed = (int(x) for x in o["counts"][b])
+    flags = o["flags"][b]
+
+    def finish():
+        assert allow_escapes or not esc, f"item {b}: tolerated mismatches {list(esc)}"
+        return mg, esc
+
+    # shift (argmax of Eq. 4-1): every alignment-dependent decision follows from it
     if tuple(o["shift"][b]) != res.shift:
         assert mg["shift"] < MARGIN, f"shift {tuple(o['shift'][b])} vs {res.shift}, margin {mg['shift']}"
-        return mg
+        esc.append(f"shift (margin {mg['shift']:.2e})")
+        return finish()
+    np.testing.assert_array_equal((flags & 1) != 0, res.aligned, err_msg="Mask_align")
+    # refresh (Eq. 4-3): token by token
+    fresh = (flags & 2) != 0
+    bad_f = np.flatnonzero(fresh != res.fresh)
+    assert all(mg["threshold"][t] < MARGIN for t in bad_f), \
+        f"refresh decisions differ at {bad_f[:8]} with margins {mg['threshold'][bad_f[:8]]}"
+    if bad_f.size:
+        esc.append(f"threshold at {bad_f[:8].tolist()}")
+    # candidates: may differ only where the refresh or the similarity floor escaped
+    cand = (flags & 4) != 0
+    bad_c = np.flatnonzero(cand != res.cand)
+    bad_s = np.setdiff1d(bad_c, bad_f)
+    assert all(mg["tau_sim"][t] < MARGIN for t in bad_s), \
+        f"candidates differ at {bad_s[:8]} with similarity-floor margins {mg['tau_sim'][bad_s[:8]]}"
+    if bad_s.size:
+        esc.append(f"tau_sim at {bad_s[:8].tolist()}")
+    if bad_c.size == 0:
+        assert k_cand == res.k_cand
+    # gate and budget (scalars decided from fp64 sums)
     if bool(flushed) != res.flushed:
         assert mg["gate"] < MARGIN, f"flush decision differs, margin {mg['gate']}"
-        return mg
+        esc.append(f"gate (margin {mg['gate']:.2e})")
+        return finish()
     if k_reuse != res.k_reuse:
         assert mg["budget"] < MARGIN, f"K_reuse {k_reuse} vs {res.k_reuse}, margin {mg['budget']}"
-    flags = o["flags"][b]
-    np.testing.assert_array_equal((flags & 1) != 0, res.aligned)
-    fresh = (flags & 2) != 0
-    bad = np.flatnonzero(fresh != res.fresh)
-    assert all(mg["threshold"][t] < MARGIN for t in bad), \
-        f"refresh decisions differ at {bad[:8]} with margins {mg['threshold'][bad[:8]]}"
-    cand = (flags & 4) != 0
-    if bad.size == 0:
-        np.testing.assert_array_equal(cand, res.cand)
-        assert k_cand == res.k_cand
-        if k_reuse == res.k_reuse:
-            assert k_final == res.k_final
-            diff = np.flatnonzero(o["reuse_mask"][b] != res.reuse_mask)
-            assert diff.size == 0 or mg["topk"] < MARGIN, \
-                f"reuse masks differ at {diff[:8]} (top-K margin {mg['topk']})"
-            if diff.size == 0:
-                n = res.n_recompute
-                assert int(o["n_recompute"][b]) == n
-                np.testing.assert_array_equal(o["recompute_idx"][b][:n], res.recompute_idx)
-    return mg
+        esc.append(f"budget (margin {mg['budget']:.2e})")
+        return finish()
+    if bad_c.size:
+        return finish()
+    # the ascending top-K and the compaction
+    assert k_final == res.k_final
+    diff = np.flatnonzero(o["reuse_mask"][b] != res.reuse_mask)
+    if diff.size:
+        assert mg["topk"] < MARGIN, f"reuse masks differ at {diff[:8]} (top-K margin {mg['topk']})"
+        esc.append(f"topk (margin {mg['topk']:.2e})")
+        return finish()
+    n = res.n_recompute
+    assert int(o["n_recompute"][b]) == n
+    np.testing.assert_array_equal(o["recompute_idx"][b][:n], res.recompute_idx)
+    return finish()
 
 
 def oracle_select_params(prm) -> osel.SelectParams:

@@ -48,7 +48,9 @@ def compare(fc, ctx, prm, prev, cur, items=None):
     margins = []
     for b in items:
         res = osel.select_item(None if prev is None else prev[b], cur[b], op)
-        margins.append(fcutil.check_select(o, res, op, b))
+        mg, esc = fcutil.check_select(o, res, op, b)
+        assert not esc
+        margins.append(mg)
     return o, margins
 
 
@@ -65,12 +67,29 @@ def test_tiny_pair_adaptive(fc, ctx):
     compare(fc, ctx, fc.SelectParams(), prev, cur)
 
 
-def test_selection_at_scale_sampled(fc, ctx):
+def test_selection_at_scale_all_pairs(fc, ctx):
     """64 pairs at 448x448 (1024 patches each), adaptive budget: the launch the
-    benchmark times; the oracle checks a spread sample of 8 pairs."""
+    benchmark times; every pair is checked against the oracle, with no tolerated
+    mismatch."""
     prev, cur, _ = fcdata.sel_pairs(1)
-    o, margins = compare(fc, ctx, fc.SelectParams(), prev, cur, items=range(0, 64, 8))
-    print("min top-K margin", min(m["topk"] for m in margins))
+    o, margins = compare(fc, ctx, fc.SelectParams(), prev, cur)
+    print("min top-K margin", min(m["topk"] for m in margins),
+          "min shift margin", min(m["shift"] for m in margins))
+
+
+def test_budget_clamped_to_candidates(fc, ctx):
+    """Algorithm 1 takes K_final = min(K_reuse, |C|): with a 100 % budget on a pair
+    rolled by one token (one row and one column unaligned, edge tokens refreshed)
+    the budget exceeds the candidates, so every candidate is reused and nothing
+    else."""
+    rng = np.random.default_rng(21)
+    base = fcdata.canvas(rng, 224, 224)[None].astype(np.float32)
+    rolled = np.roll(base, (14, 0), (2, 3))
+    o, _ = compare(fc, ctx, fc.SelectParams(adaptive=False, alpha_fixed=1.0), base, rolled)
+    k_reuse, k_cand, k_final, flushed = (int(x) for x in o["counts"][0])
+    assert k_reuse == 256 and k_cand < 256 and k_final == k_cand and not flushed
+    flags = o["flags"][0]
+    np.testing.assert_array_equal(o["reuse_mask"][0].astype(bool), (flags & 4) != 0)
 
 
 def test_flush_without_previous_frame(fc, ctx):

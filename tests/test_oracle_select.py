@@ -401,9 +401,145 @@ def test_ablation_without_refresh_keeps_edge_tokens_as_candidates():
 
 
 def test_luma_weights():
-    """O1 reading: BT.601 luma; a pure grey frame maps to its grey level."""
+    """O1 reading: BT.601 luma, Y = 0.299 R + 0.587 G + 0.114 B (ITU-R BT.601).  Each
+    primary alone gives its own weight, so a swap of any two weights fails; white
+    and any grey map to their level (the weights sum to 1)."""
     g = np.full((3, 14, 14), 0.25)
     np.testing.assert_allclose(osel.luma(g), 0.25, rtol=1e-15)
-    red = np.zeros((3, 14, 14))
-    red[0] = 1.0
-    np.testing.assert_allclose(osel.luma(red), 0.299)
+    for ch, w in enumerate((0.299, 0.587, 0.114)):
+        prim = np.zeros((3, 14, 14))
+        prim[ch] = 1.0
+        np.testing.assert_allclose(osel.luma(prim), w, rtol=1e-15)
+    np.testing.assert_allclose(osel.luma(np.ones((3, 4, 4))), 1.0, rtol=1e-15)
+    # a frame that is pure green in one half and pure blue in the other: the half
+    # means of the token-grid map carry the two weights
+    fr = np.zeros((3, 28, 56))
+    fr[1, :, :28] = 1.0
+    fr[2, :, 28:] = 1.0
+    y = osel.luma(fr)
+    assert y[:, :28].mean() == pytest.approx(0.587, abs=1e-15)
+    assert y[:, 28:].mean() == pytest.approx(0.114, abs=1e-15)
+
+
+# ------------------------------------------------------------------ zero-norm similarity
+def test_token_similarity_zero_norm_rules():
+    """O13 reading R13: two all-zero amplitude vectors are the same content (sim = 1);
+    exactly one all-zero vector has nothing in common with the other (sim = 0); an
+    unaligned token is 0 whatever its content."""
+    a_cur = np.zeros((1, 3, 5))
+    a_prev = np.zeros((1, 3, 5))
+    a_cur[0, 1] = [1.0, 2.0, 0.0, 0.0, 1.0]       # token 1: current has content, previous none
+    a_prev[0, 2] = [0.5, 0.0, 0.0, 3.0, 0.0]      # token 2: previous has content, current none
+    sim = osel.token_similarity(a_cur, a_prev, 0, 0, np.ones((1, 3), bool))
+    assert sim[0, 0] == 1.0 and sim[0, 1] == 0.0 and sim[0, 2] == 0.0
+    sim = osel.token_similarity(a_cur, a_prev, 0, 0, np.array([[False, True, True]]))
+    assert sim[0, 0] == 0.0
+
+
+def test_black_tokens_end_to_end():
+    """R13 through select_item: a token that is black in both frames has similarity 1;
+    one that turns black has similarity 0 (the other tokens are identical, so the
+    shift stays 0 and their similarity is 1)."""
+    fr = RNG.uniform(0.2, 1.0, size=(3, 112, 112))
+    fr[:, :14, :14] = 0.0                      # token 0 black in both frames
+    cur = fr.copy()
+    cur[:, 14:28, 28:42] = 0.0                 # token 10 = (1, 2) turns black
+    r = osel.select_item(fr, cur, osel.SelectParams())
+    assert r.shift == (0, 0)
+    assert r.sim[0] == 1.0 and r.sim[10] == 0.0
+    others = np.setdiff1d(np.arange(64), [0, 10])
+    np.testing.assert_allclose(r.sim[others], 1.0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ energy snap (R15)
+@pytest.mark.parametrize("m", [1, 2])
+def test_energy_snap_constant(m):
+    """R15: token energies below 1e-8 m^2 snap to exactly 0, larger ones are kept.  A
+    patch 0.5 + c B_55 (B_55 the orthonormal DCT basis image (5, 5), outside the
+    removed 3x3 block) has E = c^2 exactly: c = 1e-3 (E = 1e-6, a faint texture) must
+    survive, c = 3e-5 (E = 9e-10, rounding-noise level) must snap."""
+    coef = np.zeros((14, 14))
+    coef[5, 5] = 1.0
+    basis = scipy.fft.idctn(coef, type=2, norm="ortho")
+    side = 14 * m * 2
+    for c, keep in [(1e-3, True), (3e-5, False)]:
+        y = np.full((side, side), 0.5)
+        for i in range(0, side, 14):
+            for j in range(0, side, 14):
+                y[i:i + 14, j:j + 14] += c * basis
+        fr = np.stack([y, y, y])
+        r = osel.select_item(fr, fr, osel.SelectParams(merge=m))
+        want = m * m * c * c
+        if keep:
+            np.testing.assert_allclose(r.energy, want, rtol=1e-6)
+        else:
+            assert np.all(r.energy == 0.0)
+
+
+# ------------------------------------------------------------------ decision margins
+def _hand_result(**kw):
+    base = dict(reuse_mask=np.zeros(4, np.uint8), recompute_idx=np.arange(4, dtype=np.int32),
+                shift=(0, 0), sim=np.array([0.95, 0.90, 0.80, 0.0]),
+                energy=np.array([1.0, 2.0, 3.0, 4.0]),
+                aligned=np.array([True, True, True, False]),
+                fresh=np.array([False, False, False, True]),
+                cand=np.array([True, True, True, False]), sim_freq=0.13, psi=0.5, alpha=0.30,
+                mu=2.5, sigma=1.118, thr=2.5, k_reuse=1, k_cand=3, k_final=2, flushed=False,
+                response=np.array([[1.0, 0.25], [-0.1, 0.0]]))
+    base.update(kw)
+    return osel.SelectResult(**base)
+
+
+def test_decision_margins_hand_built():
+    """Each margin of the mismatch audit on a result with known gaps:
+    threshold |E - 2.5| / 2.5, top-K gap between the 2nd and 3rd candidate keys
+    (3 - 2) / 3, budget |0.3 * 4 - 1| / 1.2, gate |0.13 - 0.12| / 0.12, shift peak
+    minus runner-up (1 - 0.25) / 1, and the similarity floor |sim - 0.85| / 0.85 on
+    aligned tokens only."""
+    prm = osel.SelectParams(tau_sim=0.85)
+    mg = osel.decision_margins(_hand_result(), prm)
+    np.testing.assert_allclose(mg["threshold"], [0.6, 0.2, 0.2, 0.6], rtol=1e-14)
+    assert mg["topk"] == pytest.approx(1.0 / 3.0, rel=1e-14)
+    assert mg["budget"] == pytest.approx(0.2 / 1.2, rel=1e-12)
+    assert mg["gate"] == pytest.approx(0.01 / 0.12, rel=1e-12)
+    assert mg["shift"] == pytest.approx(0.75, rel=1e-14)
+    np.testing.assert_allclose(mg["tau_sim"][:3], np.abs([0.95, 0.90, 0.80] - np.float64(0.85)) / 0.85,
+                               rtol=1e-12)
+    assert mg["tau_sim"][3] == np.inf
+
+
+def test_decision_margins_degenerate_cases():
+    """No top-K boundary when every candidate (or none) is taken; a fixed budget has no
+    rounding decision; without a similarity floor no token has a floor margin; a tie
+    of the two largest phase-correlation values has margin 0."""
+    prm = osel.SelectParams(adaptive=False)
+    mg = osel.decision_margins(_hand_result(k_final=3), prm)
+    assert mg["topk"] == np.inf and mg["budget"] == np.inf and np.all(mg["tau_sim"] == np.inf)
+    mg = osel.decision_margins(_hand_result(k_final=0), prm)
+    assert mg["topk"] == np.inf
+    mg = osel.decision_margins(_hand_result(response=np.array([[0.5, 0.5], [0.1, 0.0]])), prm)
+    assert mg["shift"] == 0.0
+    # a budget exactly on an integer has margin 0 (alpha N = 2)
+    mg = osel.decision_margins(_hand_result(alpha=0.5), osel.SelectParams())
+    assert mg["budget"] == 0.0
+
+
+def test_decision_margins_on_a_real_result_bound_the_decisions():
+    """On a computed selection every margin is consistent with the decision it audits:
+    no token sits exactly on the threshold, the K-th reused key is below the first
+    unused candidate's by the top-K margin, and the argmax of the response is unique."""
+    prev, cur, _ = _tiny()
+    r = osel.select_item(prev, cur, osel.SelectParams())
+    mg = osel.decision_margins(r, osel.SelectParams())
+    assert np.all(mg["threshold"] > 0)
+    assert (r.energy > r.thr).tolist() == r.fresh.tolist()
+    keys = np.sort(r.energy[r.cand])
+    if 0 < r.k_final < keys.size:
+        assert keys[r.k_final] - keys[r.k_final - 1] == pytest.approx(mg["topk"] * keys[r.k_final])
+    assert mg["shift"] > 0
+
+
+def _tiny():
+    import fcdata
+    prev, cur, _ = fcdata.tiny_pair(0)
+    return prev[0], cur[0], None
