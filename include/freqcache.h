@@ -163,6 +163,24 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
                     const float *frames_cur, int32_t B, int32_t H, int32_t W,
                     const fc_select_out *out, void *stream);
 
+/* fc_select without a context and without any device allocation, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, kernels and outputs as fc_select,
+ * on the calling thread's current device; the workspace (per-patch amplitudes, means,
+ * energies and spectral products: about 0.85 MB per 448x448 pair) lives in a static
+ * device array of 16 MiB that each GPU holds until the process ends.
+ *   - Sizes whose workspace exceeds 16 MiB return FC_ERR_CAPACITY before any device
+ *     work (e.g. at most 19 pairs of 448x448 frames, 4 of 896x896).
+ *   - The first call on a device does a one-time set-up that synchronises with it
+ *     (architecture check, the array's device address, the transform tables); make
+ *     that first call outside graph capture.  Later calls only launch kernels.
+ *   - Every call on one GPU shares that GPU's array: calls that overlap in time on
+ *     one GPU (other streams, other host threads) race and must be serialised by the
+ *     caller.  Nothing in the array needs clearing between calls. */
+fc_status fc_select_noalloc(const fc_select_params *prm, const float *frames_prev,
+                            const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                            const fc_select_out *out, void *stream);
+
 /* Token-cache preparation for one layer at a new step.  The caller has already
  * advanced kv->head, so the current frame lives in slot (head + W - 1) mod W and
  * the previous frame in slot (head + W - 2) mod W (the same slot when W = 1).  For

@@ -32,7 +32,7 @@ fc_status fail(fc_status st, const char *fmt, ...) {
 }
 
 ProfScope::ProfScope(fc_ctx *c, hipStream_t s, const char *name) : ctx(c), st(s) {
-  if (!ctx->prof || (!ctx->prof_only.empty() && ctx->prof_only != name)) return;
+  if (!ctx || !ctx->prof || (!ctx->prof_only.empty() && ctx->prof_only != name)) return;
   hipEvent_t a, b;
   if (ctx->pool.size() >= 2) {
     a = ctx->pool.back();
@@ -53,6 +53,46 @@ ProfScope::ProfScope(fc_ctx *c, hipStream_t s, const char *name) : ctx(c), st(s)
 
 ProfScope::~ProfScope() {
   if (stop) hipEventRecord(stop, st);
+}
+
+SelectWsBytes select_ws_bytes(long B, long H, long W) {
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t np = (size_t)(H / kPatch) * (W / kPatch);
+  // amplitudes in 16-patch chunks of a patch row (the last chunk of a row padded)
+  const size_t np16 = (size_t)(H / kPatch) * ((W / kPatch + 15) / 16) * 16;
+  SelectWsBytes b;
+  b.amp = al((size_t)B * 2 * kBins * np16 * sizeof(float));
+  b.pmean = al((size_t)B * 2 * np * sizeof(double));
+  b.penergy = al((size_t)B * np * sizeof(double));
+  b.pdot = al((size_t)B * 3 * np * sizeof(double));
+  b.total = b.amp + b.pmean + b.penergy + b.pdot;
+  return b;
+}
+
+fc_status check_select_args(const fc_select_params *prm, const float *cur,
+                            const fc_select_out *out, int B, int H, int W, const char *who) {
+  if (!prm || !cur || !out)
+    return fail(FC_ERR_INVALID_ARG, "%s: null params, current frames or outputs", who);
+  if (!out->sim || !out->energy || !out->reuse_mask || !out->recompute_idx || !out->n_recompute ||
+      !out->shift || !out->scalars || !out->counts)
+    return fail(FC_ERR_INVALID_ARG, "%s: an output buffer is null", who);
+  const fc_select_params &p = *prm;
+  if (p.patch != kPatch)
+    return fail(FC_ERR_UNSUPPORTED, "%s: patch %d (the library implements P = 14)", who, p.patch);
+  if (p.merge < 1 || p.merge > 4) return fail(FC_ERR_INVALID_ARG, "%s: merge %d", who, p.merge);
+  if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
+      !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
+      !std::isfinite(p.tau_sim) || (p.no_align != 0 && p.no_align != 1) ||
+      (p.no_refresh != 0 && p.no_refresh != 1))
+    return fail(FC_ERR_INVALID_ARG, "%s: hyper-parameter out of range", who);
+  if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "%s: B=%d H=%d W=%d", who, B, H, W);
+  const int tp = p.patch * p.merge;
+  if (H % tp || W % tp)
+    return fail(FC_ERR_SHAPE, "%s: H=%d, W=%d not multiples of patch*merge=%d", who, H, W, tp);
+  const long M = (long)(H / tp) * (W / tp);
+  if (M > kMaxTokens)
+    return fail(FC_ERR_UNSUPPORTED, "%s: %ld tokens per frame > %d", who, M, kMaxTokens);
+  return FC_OK;
 }
 
 }  // namespace fc
@@ -133,9 +173,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   ctx->device = device;
   ctx->caps = c;
   ctx->num_cus = prop.multiProcessorCount;
-
   const size_t B = c.max_batch;
-  const size_t np = (size_t)(c.max_height / fc::kPatch) * (c.max_width / fc::kPatch);
   const size_t rows = B * c.max_tokens;
   const size_t wide = std::max(c.max_qkv, c.max_d_model) + 64;
   const size_t base = rows * wide;
@@ -145,12 +183,11 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   // a kv row is at most a third of a qkv row (n_heads >= n_kv_heads)
   if ((long)rows >= fc::kBigRows) ctx->krot_elems = B * (size_t)c.max_seq * ((c.max_qkv + 2) / 3);
   fc_status st = FC_OK;
-  // amplitudes in 16-patch chunks of a patch row (the last chunk of a row padded)
-  const size_t np16 = (size_t)(c.max_height / fc::kPatch) * ((c.max_width / fc::kPatch + 15) / 16) * 16;
-  if ((st = dev_alloc(&ctx->amp, B * 2 * fc::kBins * np16, "amp")) != FC_OK ||
-      (st = dev_alloc(&ctx->pmean, B * 2 * np, "pmean")) != FC_OK ||
-      (st = dev_alloc(&ctx->penergy, B * np, "penergy")) != FC_OK ||
-      (st = dev_alloc(&ctx->pdot, B * 3 * np, "pdot")) != FC_OK ||
+  const fc::SelectWsBytes sb = fc::select_ws_bytes(B, c.max_height, c.max_width);
+  if ((st = dev_alloc(&ctx->amp, sb.amp / sizeof(float), "amp")) != FC_OK ||
+      (st = dev_alloc(&ctx->pmean, sb.pmean / sizeof(double), "pmean")) != FC_OK ||
+      (st = dev_alloc(&ctx->penergy, sb.penergy / sizeof(double), "penergy")) != FC_OK ||
+      (st = dev_alloc(&ctx->pdot, sb.pdot / sizeof(double), "pdot")) != FC_OK ||
       (st = dev_alloc(&ctx->qbuf, rows * c.max_qkv, "q")) != FC_OK ||
       (st = dev_alloc(&ctx->attn, rows * c.max_qkv, "attn")) != FC_OK ||
       (st = dev_alloc(&ctx->h1, rows * c.max_d_model, "h1")) != FC_OK ||
@@ -182,34 +219,34 @@ fc_status fc_destroy(fc_ctx *ctx) {
 fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frames_prev,
                     const float *frames_cur, int32_t B, int32_t H, int32_t W,
                     const fc_select_out *out, void *stream) {
-  if (!ctx || !prm || !frames_cur || !out)
-    return fail(FC_ERR_INVALID_ARG, "fc_select: null context, params, current frames or outputs");
-  if (!out->sim || !out->energy || !out->reuse_mask || !out->recompute_idx || !out->n_recompute ||
-      !out->shift || !out->scalars || !out->counts)
-    return fail(FC_ERR_INVALID_ARG, "fc_select: an output buffer is null");
-  const fc_select_params &p = *prm;
-  if (p.patch != fc::kPatch)
-    return fail(FC_ERR_UNSUPPORTED, "fc_select: patch %d (the library implements P = 14)", p.patch);
-  if (p.merge < 1 || p.merge > 4) return fail(FC_ERR_INVALID_ARG, "fc_select: merge %d", p.merge);
-  if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
-      !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
-      !std::isfinite(p.tau_sim) || (p.no_align != 0 && p.no_align != 1) ||
-      (p.no_refresh != 0 && p.no_refresh != 1))
-    return fail(FC_ERR_INVALID_ARG, "fc_select: hyper-parameter out of range");
-  if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "fc_select: B=%d H=%d W=%d", B, H, W);
-  const int tp = p.patch * p.merge;
-  if (H % tp || W % tp)
-    return fail(FC_ERR_SHAPE, "fc_select: H=%d, W=%d not multiples of patch*merge=%d", H, W, tp);
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_select: null context");
+  fc_status st = fc::check_select_args(prm, frames_cur, out, B, H, W, "fc_select");
+  if (st != FC_OK) return st;
+  const int tp = prm->patch * prm->merge;
   const int M = (H / tp) * (W / tp);
   if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width ||
       M > ctx->caps.max_tokens)
     return fail(FC_ERR_CAPACITY, "fc_select: B=%d H=%d W=%d N=%d exceed the context caps", B, H, W, M);
-  if (M > fc::kMaxTokens)
-    return fail(FC_ERR_UNSUPPORTED, "fc_select: %d tokens per frame > %d", M, fc::kMaxTokens);
-  fc_status st = use_device(ctx);
+  st = use_device(ctx);
   if (st != FC_OK) return st;
-  return fc::launch_select(ctx, p, frames_prev, frames_cur, B, H, W, *out,
+  const fc::SelectWs ws{ctx->amp, ctx->pmean, ctx->penergy, ctx->pdot};
+  return fc::launch_select(ctx, ws, *prm, frames_prev, frames_cur, B, H, W, *out,
                            reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_select_noalloc(const fc_select_params *prm, const float *frames_prev,
+                            const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                            const fc_select_out *out, void *stream) {
+  fc_status st = fc::check_select_args(prm, frames_cur, out, B, H, W, "fc_select_noalloc");
+  if (st != FC_OK) return st;
+  const size_t need = fc::select_ws_bytes(B, H, W).total;
+  if (need > fc::noalloc_scratch_bytes())
+    return fail(FC_ERR_CAPACITY,
+                "fc_select_noalloc: B=%d pairs of %dx%d frames need %zu bytes of scratch, "
+                "the static scratch holds %zu",
+                B, H, W, need, fc::noalloc_scratch_bytes());
+  return fc::launch_select_noalloc(*prm, frames_prev, frames_cur, B, H, W, *out,
+                                   reinterpret_cast<hipStream_t>(stream));
 }
 
 static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_cache *kv, int B,

@@ -85,9 +85,33 @@ struct ProfScope {
 };
 
 // ----------------------------------------------------------------------------- launchers
-fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *prev,
-                        const float *cur, int B, int H, int W, const fc_select_out &out,
-                        hipStream_t st);
+// Selection workspace: per-patch amplitudes, means, energies and spectral products.
+struct SelectWs {
+  float *amp;        // [B][2][chunk rows][kBins][16]
+  double *pmean;     // [B][2][Np]
+  double *penergy;   // [B][Np]
+  double *pdot;      // [B][3][Np]
+};
+// Bytes of each workspace part for B pairs of H x W frames (256-B aligned parts).
+struct SelectWsBytes {
+  size_t amp, pmean, penergy, pdot, total;
+};
+SelectWsBytes select_ws_bytes(long B, long H, long W);
+
+// Argument checks shared by the selection entry points (synchronous, no device work).
+fc_status check_select_args(const fc_select_params *prm, const float *cur,
+                            const fc_select_out *out, int B, int H, int W, const char *who);
+
+// ctx may be null (no kernel timing)
+fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params &prm,
+                        const float *prev, const float *cur, int B, int H, int W,
+                        const fc_select_out &out, hipStream_t st);
+// The same on the calling thread's current device, with the workspace in the library's
+// static device scratch array (no allocation).
+fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
+                                const float *cur, int B, int H, int W,
+                                const fc_select_out &out, hipStream_t st);
+size_t noalloc_scratch_bytes();
 
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                        const uint16_t *x_cur, const int32_t *idx, const int32_t *nrec,

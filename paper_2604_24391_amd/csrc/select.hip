@@ -27,6 +27,8 @@
 
 #include <cmath>
 #include <cstdio>
+#include <cstring>
+#include <mutex>
 
 #include "fc_internal.h"
 
@@ -1007,42 +1009,107 @@ fc_status upload_select_tables() {
   return FC_OK;
 }
 
-fc_status launch_select(fc_ctx *ctx, const fc_select_params &prm, const float *prev,
-                        const float *cur, int B, int H, int W, const fc_select_out &out,
-                        hipStream_t st) {
+fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params &prm,
+                        const float *prev, const float *cur, int B, int H, int W,
+                        const fc_select_out &out, hipStream_t st) {
   const int m = prm.merge;
   const int Gph = H / P, Gpw = W / P;
-  const int Gh = Gph / m, Gw = Gpw / m, M = Gh * Gw;
   {
     ProfScope ps(ctx, st, "fc_spectra");
     dim3 grid((Gpw + PW - 1) / PW, Gph, 2 * B);
-    hipLaunchKernelGGL(k_spectra, grid, dim3(256), 0, st, prev, cur, H, W, Gph, Gpw, ctx->amp,
-                       ctx->pmean, ctx->penergy);
+    hipLaunchKernelGGL(k_spectra, grid, dim3(256), 0, st, prev, cur, H, W, Gph, Gpw, ws.amp,
+                       ws.pmean, ws.penergy);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_grid");
     GridParams g{Gph, Gpw, m, prm.tau_mig, prm.lambda_, prm.alpha_min, prm.alpha_max,
                  prm.alpha_fixed, prm.adaptive, prm.entropy_norm, prm.no_align};
-    hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ctx->pmean, ctx->penergy, g,
+    hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ws.pmean, ws.penergy, g,
                        out.energy, out.shift, out.scalars, out.counts);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_patchsim");
     dim3 grid((Gph * Gpw + 63) / 64, B);
-    hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ctx->amp, Gph, Gpw, m, out.shift,
-                       ctx->pdot);
+    hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ws.amp, Gph, Gpw, m, out.shift,
+                       ws.pdot);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_topk");
-    hipLaunchKernelGGL(k_topk, dim3(B), dim3(kMaxTokens), 0, st, out.energy, ctx->pdot, out.shift,
+    hipLaunchKernelGGL(k_topk, dim3(B), dim3(kMaxTokens), 0, st, out.energy, ws.pdot, out.shift,
                        out.scalars, out.counts, prm.tau_sim, prm.no_refresh, Gph, Gpw, m, out.sim,
                        out.reuse_mask, out.recompute_idx, out.n_recompute, out.flags);
     FC_HIP_TRY(hipGetLastError());
   }
   return FC_OK;
+}
+
+// ------------------------------------------------------------------------------ no-alloc path
+// Workspace of fc_select_noalloc: a static device array, so that the call needs no
+// allocation.  Every GPU the library runs on holds its own copy until the process ends.
+// In host code the array's name is only a host-side handle; the device address of
+// each GPU's copy comes from hipGetSymbolAddress (once per device, with that device
+// current) and only that address is passed to kernels.  No part needs clearing: every
+// element a kernel reads was written earlier in the same call.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_noalloc_mu;
+unsigned char *g_noalloc_ptr[kMaxDevices];   // per-device address of `scratch`
+bool g_noalloc_ready[kMaxDevices];
+
+// One-time set-up on the current device: architecture check, the scratch array's device
+// address, and the transform tables (constant memory of this device).
+fc_status noalloc_setup(int dev, unsigned char **ptr) {
+  std::lock_guard<std::mutex> lk(g_noalloc_mu);
+  if (!g_noalloc_ready[dev]) {
+    hipDeviceProp_t prop;
+    FC_HIP_TRY(hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+      return fail(FC_ERR_UNSUPPORTED, "fc_select_noalloc: device %d is %s, the library targets gfx950",
+                  dev, prop.gcnArchName);
+    void *p = nullptr;
+    FC_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return fail(FC_ERR_HIP, "fc_select_noalloc: no device address for the scratch");
+    fc_status s = upload_select_tables();
+    if (s != FC_OK) return s;
+    g_noalloc_ptr[dev] = static_cast<unsigned char *>(p);
+    g_noalloc_ready[dev] = true;
+  }
+  *ptr = g_noalloc_ptr[dev];
+  return FC_OK;
+}
+}  // namespace
+
+size_t noalloc_scratch_bytes() { return kNoAllocScratchBytes; }
+
+fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
+                                const float *cur, int B, int H, int W,
+                                const fc_select_out &out, hipStream_t st) {
+  const SelectWsBytes sb = select_ws_bytes(B, H, W);
+  if (sb.total > kNoAllocScratchBytes)
+    return fail(FC_ERR_CAPACITY, "fc_select_noalloc: %zu bytes of scratch needed, %zu available",
+                sb.total, kNoAllocScratchBytes);
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0)
+    return fail(FC_ERR_NO_DEVICE, "fc_select_noalloc: no current HIP device (%s)",
+                e != hipSuccess ? hipGetErrorString(e) : "none");
+  if (dev >= kMaxDevices)
+    return fail(FC_ERR_UNSUPPORTED, "fc_select_noalloc: device %d >= %d", dev, kMaxDevices);
+  unsigned char *base = nullptr;
+  fc_status s = noalloc_setup(dev, &base);
+  if (s != FC_OK) return s;
+  SelectWs ws;
+  ws.amp = reinterpret_cast<float *>(base);
+  ws.pmean = reinterpret_cast<double *>(base + sb.amp);
+  ws.penergy = reinterpret_cast<double *>(base + sb.amp + sb.pmean);
+  ws.pdot = reinterpret_cast<double *>(base + sb.amp + sb.pmean + sb.penergy);
+  return launch_select(nullptr, ws, prm, prev, cur, B, H, W, out, st);
 }
 
 }  // namespace fc

@@ -29,7 +29,7 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
-           "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
+           "fc_select_noalloc", "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
            "fc_profile_only", "fc_profile_read")
 
 
@@ -88,6 +88,9 @@ def lib() -> ctypes.CDLL:
         L.fc_select.argtypes = [c_void_p, ctypes.POINTER(fc_select_params), c_void_p, c_void_p,
                                 c_int32, c_int32, c_int32, ctypes.POINTER(fc_select_out),
                                 c_void_p]
+        L.fc_select_noalloc.argtypes = [ctypes.POINTER(fc_select_params), c_void_p, c_void_p,
+                                        c_int32, c_int32, c_int32, ctypes.POINTER(fc_select_out),
+                                        c_void_p]
         L.fc_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                       ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                       c_void_p, c_int32, c_int32, c_void_p]
@@ -102,7 +105,7 @@ def lib() -> ctypes.CDLL:
         L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
-        for n in ("fc_create", "fc_destroy", "fc_select", "fc_cache_update",
+        for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_cache_update",
                   "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
@@ -269,9 +272,8 @@ def token_grid(H: int, W: int, prm: SelectParams):
     return H // tp, W // tp
 
 
-def fc_select(ctx: Context, prm: SelectParams, prev: torch.Tensor | None, cur: torch.Tensor,
-              out: SelectOut, stream=None):
-    """Algorithm 1 for a [B, 3, H, W] float32 batch of frame pairs (prev may be None)."""
+def _select_args(prm: SelectParams, prev: torch.Tensor | None, cur: torch.Tensor,
+                 out: SelectOut):
     if cur.dim() != 4 or cur.shape[1] != 3:
         raise ValueError("cur must be [B, 3, H, W]")
     B, _, H, W = cur.shape
@@ -284,10 +286,24 @@ def fc_select(ctx: Context, prm: SelectParams, prev: torch.Tensor | None, cur: t
         pp = _ptr(prev, torch.float32, B * 3 * H * W, "prev")
     else:
         pp = c_void_p(0)
-    co = out.c(B, N)
-    cp = prm.c()
+    return prm.c(), pp, pc, B, H, W, out.c(B, N)
+
+
+def fc_select(ctx: Context, prm: SelectParams, prev: torch.Tensor | None, cur: torch.Tensor,
+              out: SelectOut, stream=None):
+    """Algorithm 1 for a [B, 3, H, W] float32 batch of frame pairs (prev may be None)."""
+    cp, pp, pc, B, H, W, co = _select_args(prm, prev, cur, out)
     _check(lib().fc_select(ctx.handle, ctypes.byref(cp), pp, pc, B, H, W, ctypes.byref(co),
                            _stream(stream)))
+
+
+def fc_select_noalloc(prm: SelectParams, prev: torch.Tensor | None, cur: torch.Tensor,
+                      out: SelectOut, stream=None):
+    """fc_select with the library's static scratch instead of a context (no device
+    allocation; on the current device; at most 16 MiB of workspace)."""
+    cp, pp, pc, B, H, W, co = _select_args(prm, prev, cur, out)
+    _check(lib().fc_select_noalloc(ctypes.byref(cp), pp, pc, B, H, W, ctypes.byref(co),
+                                   _stream(stream)))
 
 
 # ------------------------------------------------------------------------------ layer

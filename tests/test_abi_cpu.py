@@ -116,3 +116,19 @@ def test_cache_update_layers_binding_checks_lengths(fc):
     with pytest.raises(ValueError, match="one entry per layer"):
         fc.fc_cache_update_layers(None, None, [object()], [object(), object()], [object()], None,
                                   None, 16)
+
+
+def test_select_noalloc_rejects_before_device_work(fc):
+    """fc_select_noalloc checks its arguments and its scratch limit synchronously: null
+    arguments are FC_ERR_INVALID_ARG and a batch whose workspace exceeds the static
+    16 MiB scratch is FC_ERR_CAPACITY, both without a GPU (no pointer is touched)."""
+    lib = fc.lib()
+    assert lib.fc_select_noalloc(None, None, None, 1, 224, 224, None, None) == 1
+    fake = fc.freqcache.fc_select_out(*([1] * 9))
+    prm = fc.SelectParams().c()
+    st = lib.fc_select_noalloc(ctypes.byref(prm), None, ctypes.c_void_p(1), 64, 448, 448,
+                               ctypes.byref(fake), None)
+    assert st == 3 and "scratch" in fc.fc_last_error()
+    st = lib.fc_select_noalloc(ctypes.byref(prm), None, ctypes.c_void_p(1), 1, 100, 224,
+                               ctypes.byref(fake), None)
+    assert st == 2
