@@ -99,3 +99,17 @@ def random_reuse_ids(seed: int, n_tokens: int, reuse_percent: int) -> np.ndarray
     reused = np.zeros(n_tokens, bool)
     reused[perm[:k]] = True
     return np.flatnonzero(~reused).astype(np.int32)
+
+
+def token_embeddings(frames: np.ndarray, d: int, token_px: int, seed: int,
+                     std: float = 0.02) -> np.ndarray:
+    """Stand-in for the vision tower (out of scope): a fixed seeded linear map of each
+    token's token_px x token_px x 3 pixels to d.  frames [F, 3, H, W] float32 ->
+    bf16 bit patterns [F, N, d], tokens row-major on the token grid."""
+    rng = np.random.default_rng(seed)
+    nf, _, h, w = frames.shape
+    gh, gw = h // token_px, w // token_px
+    proj = rng.standard_normal((3 * token_px * token_px, d), dtype=np.float32) * np.float32(std)
+    px = np.asarray(frames, np.float32).reshape(nf, 3, gh, token_px, gw, token_px)
+    px = px.transpose(0, 2, 4, 1, 3, 5).reshape(nf, gh * gw, 3 * token_px * token_px)
+    return bf16_round(px @ proj)

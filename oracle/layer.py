@@ -29,7 +29,11 @@ import numpy as np
 
 
 def f32(u16: np.ndarray) -> np.ndarray:
-    """bf16 bit patterns -> float32 (exact)."""
+    """bf16 bit patterns -> float32 (exact).  float32 arrays pass through unchanged, so
+    a caller may carry float32 state (an episode's caches between steps) or hand in
+    weights upcast once."""
+    if isinstance(u16, np.ndarray) and u16.dtype == np.float32:
+        return u16
     return (np.asarray(u16, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
