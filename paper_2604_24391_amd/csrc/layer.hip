@@ -4,13 +4,14 @@
 // token of batch item b, j < n_recompute[b] (read on the device, so no host
 // sync); grids are sized for N rows per item and surplus tiles exit.
 //
-//   k_gather_norm  gathers the recomputed tokens' rows of x and writes the RMSNorm
-//               output bf16(x / rms(x) * g) slot by slot: the QKV operand.
 //   k_wgemm     weight-streaming bf16 MFMA GEMM (v_mfma_f32_16x16x32_bf16) over the
 //               slots, C = A W^T with W row-major [out][in] like torch.nn.Linear;
 //               split-K float32 partials, or (SwiGLU) SiLU(g) * u in the epilogue.
-//   k_red_qkv   sums the QKV partials, adds the bias, stores q (pre-RoPE) and
-//               scatters raw k and v into the current frame's cache rows.
+//               The QKV projection gathers the recomputed tokens' rows of x by id and
+//               multiplies x g (the attention RMSNorm gain) on its A fragments.
+//   k_red_qkv   sums the QKV partials, scales by the token's 1/rms, adds the bias,
+//               stores rotated q and scatters raw k and v into the current frame's
+//               cache rows.
 //   k_attn      attention of the gathered queries over the whole cache, GQA
 //               (one wave per query head of a KV group), RoPE applied to q and to
 //               each key block as it is staged in LDS, causal by position, float32
@@ -88,9 +89,12 @@ constexpr int KS = kGemmBK;                 // 64 K values per step
 constexpr int RB = KS * 2;                  // bytes per staged operand row
 constexpr int MT = 256;                     // rows per M tile
 constexpr int kLdsBytes = 158 * 1024;       // operand stages
+constexpr int kGainSteps = 2 * MT * 4 / (KS * 2);   // K steps of gain the QKV LDS slice holds
 
 struct WArgs {
-  const uint16_t *A;              // bf16 activations, one row per slot
+  const uint16_t *A;              // bf16 activations: one row per slot, or (gather) x [B][N][K]
+  int gather;                     // QKV: A rows are the layer input's rows at the token ids
+  const uint16_t *gain;           // QKV: attention RMSNorm gain, applied along K to A
   const uint16_t *W0, *W1;        // weights [cols][K]; SwiGLU: gate, up
   int K, Nout, N;                 // N = token slots per batch item
   int nb, ncg, splits, ksteps;    // 16-col blocks, column groups, K splits, K steps per split
@@ -227,7 +231,8 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
       if (j < nA) {
         const int r = j * 8 + rsub;                            // tile row
         const int rr = r < nvalid ? r : nvalid - 1;            // clamp: never stored
-        gp[i] = a.A + (slot0 + rr) * a.K + k0 + ((ch ^ swz8(r)) * 8);
+        const long arow = a.gather ? (long)b * a.N + tok_of(a.idx, slot0 + rr, a.N) : slot0 + rr;
+        gp[i] = a.A + arow * a.K + k0 + ((ch ^ swz8(r)) * 8);
         lo[i] = j * 1024;
       } else {
         const int jw = j - nA, pb = jw >> 1;                   // present weight block pb
@@ -286,6 +291,14 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
   for (int i = 0; i < MBW; ++i)
 #pragma unroll
     for (int j = 0; j < NBW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // QKV multiplies x g: the attention RMSNorm gain of this split's K range is staged in
+  // LDS before barrier 0 (at most kGainSteps K steps, checked at launch); 1/rms scales
+  // the summed rows in k_red_qkv
+  const __bf16 *gsl = reinterpret_cast<const __bf16 *>(rowinv);
+  if (MODE == G_QKV) {
+    for (int e = t; e < nk * KS / 8; e += 256)
+      reinterpret_cast<uint4 *>(rowinv)[e] = *reinterpret_cast<const uint4 *>(a.gain + k0 + 8 * e);
+  }
   // fragment (row l16, K sub-step s): 16-B chunk 4 s + g of the row, at its swizzled slot;
   // A and B use the same K order, so the products are those of the plain K order
   const uint32_t rowoff = l16 * RB;
@@ -303,6 +316,16 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
 #pragma unroll
       for (int j = 0; j < NBW; ++j)
         fb[s][j] = *reinterpret_cast<const bf16x8 *>(st + (S::AROWS + j * 16) * RB + rowoff + slot);
+    }
+    if (MODE == G_QKV) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bf16x8 gc = *reinterpret_cast<const bf16x8 *>(gsl + k * KS + (4 * s + g) * 8);
+#pragma unroll
+        for (int i = 0; i < MBW; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) fa[s][i][e] = (__bf16)((float)fa[s][i][e] * (float)gc[e]);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -364,7 +387,8 @@ __device__ __forceinline__ void wgemm_tile(const WArgs &a, unsigned char *lds, f
 template <int MODE>
 __global__ __launch_bounds__(512) void k_wgemm(WArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
-  __shared__ float rowinv[MT];
+  // SwiGLU: 1/rms per row; QKV: the attention RMSNorm gain of the split's K range
+  __shared__ __attribute__((aligned(16))) float rowinv[2 * MT];
   // split fastest: with 8 splits every split's workgroups share one XCD and its L2
   const int bid = blockIdx.x;
   const int sp = bid % a.splits;
@@ -441,8 +465,8 @@ __device__ float block_sum256(float v, float *red) {
   return res;
 }
 
-// One workgroup per slot: the gathered token's row of x, normalised and scaled by
-// the attention RMSNorm gain, as the QKV GEMM's bf16 operand.
+// Large-M path: one workgroup per slot, the gathered token's row of x, normalised and
+// scaled by the attention RMSNorm gain, as the QKV GEMM's bf16 operand.
 __global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict__ x,
                                                      const uint16_t *__restrict__ gain,
                                                      const int32_t *__restrict__ idx,
@@ -485,10 +509,11 @@ __global__ __launch_bounds__(256) void k_gather_norm(const uint16_t *__restrict_
   }
 }
 
-// One workgroup per (slot, 1024 columns): split-K sum + bias.  Queries are rotated
-// (rotate-half RoPE at the token's prompt position) in float32 before their single
-// rounding to bf16; a 1024-column block always holds whole heads, so the partner
-// dim of the rotation comes from LDS.  K and V rows go raw into the cache.
+// One workgroup per (slot, 1024 columns): split-K sum of (x g) W^T, scaled by the
+// token's 1/rms (from its row of x, read once per workgroup), plus the bias.  Queries
+// are rotated (rotate-half RoPE at the token's prompt position) in float32 before
+// their single rounding to bf16; a 1024-column block always holds whole heads, so
+// the partner dim of the rotation comes from LDS.  K and V rows go raw into the cache.
 template <int SPL>
 __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   __shared__ float qs[1024];
@@ -498,12 +523,26 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   const int c0 = blockIdx.y * 1024;
   const int c = c0 + threadIdx.x * 4;
   const int tok = tok_of(r.idx, slot, r.N);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (c < r.ncols) v = sum_parts<SPL>(r, slot, c);
+  // 1/rms of the token's input row (d <= 8192: at most 4 chunks of 8 a thread)
+  const uint16_t *xr = r.x + ((long)b * r.N + tok) * r.d;
+  float ss = 0.f;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int cx = (it * 256 + threadIdx.x) * 8;
+    if (cx < r.d) {
+      const U16x8 xv = *reinterpret_cast<const U16x8 *>(xr + cx);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(bf2f(xv.v[e]), bf2f(xv.v[e]), ss);
+    }
+  }
+  const float inv = 1.f / sqrtf(block_sum256(ss, qs) / (float)r.d + r.eps);
   float vv[4] = {0.f, 0.f, 0.f, 0.f};
   if (c < r.ncols) {
-    const float4 v = sum_parts<SPL>(r, slot, c);
     vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) vv[e] += bf2f(r.bias[c + e]);
+    for (int e = 0; e < 4; ++e) vv[e] = fmaf(vv[e], inv, bf2f(r.bias[c + e]));
   }
   if (c0 < r.qw) {   // uniform: the block's query columns are rotated
     *reinterpret_cast<float4 *>(&qs[threadIdx.x * 4]) = make_float4(vv[0], vv[1], vv[2], vv[3]);
@@ -1747,6 +1786,12 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
     splits = std::min(splits, std::max(1, ksteps / 4));
     while (splits > 1 && (size_t)splits * g.rows * g.Nout > ctx->part_elems) --splits;
   }
+  if (MODE == G_QKV && (ksteps + splits - 1) / splits > kGainSteps) {
+    // the gain slice of a split's K range must fit in LDS
+    splits = (ksteps + kGainSteps - 1) / kGainSteps;
+    if (splits > kMaxSplits || (size_t)splits * g.rows * g.Nout > ctx->part_elems)
+      return fail(FC_ERR_UNSUPPORTED, "%s: K %d needs more than %d splits", name, g.K, kMaxSplits);
+  }
   g.ksteps = (ksteps + splits - 1) / splits;
   g.splits = (ksteps + g.ksteps - 1) / g.ksteps;
   if (MODE != G_GU && (size_t)g.splits * g.rows * g.Nout > ctx->part_elems)
@@ -1858,25 +1903,28 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   r.hd = hd; r.qpos0 = kv.text_tokens + (kv.window - 1) * N; r.rope = ctx->rope;
   fc_status rc;
 
-  // 1. gather + RMSNorm of the recomputed rows -> QKV partials; the reduction adds the
-  //    bias, stores q and scatters raw k, v into the current frame's cache rows
+  // 1. QKV of the recomputed rows.  Large-M path: gather + RMSNorm of the rows, then a
+  //    GEMM whose epilogue adds the bias, rotates q and scatters raw k, v into the
+  //    current frame's cache rows.  Few-row path: the GEMM gathers the rows of x by
+  //    token id itself and multiplies x g; the reduction scales by 1/rms, adds the bias,
+  //    stores rotated q and scatters raw k, v
   {
-    {
-      ProfScope ps(ctx, st, "fc_gather_norm");
-      hipLaunchKernelGGL(k_gather_norm, dim3((unsigned)rows), dim3(256), 0, st, x_cur, L.g_attn,
-                         idx, nrec, N, d, L.rms_eps, ctx->hb);
-      FC_HIP_TRY(hipGetLastError());
-    }
     r.ncols = qkv;
     r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
     if (big) {
+      {
+        ProfScope ps(ctx, st, "fc_gather_norm");
+        hipLaunchKernelGGL(k_gather_norm, dim3((unsigned)rows), dim3(256), 0, st, x_cur, L.g_attn,
+                           idx, nrec, N, d, L.rms_eps, ctx->hb);
+        FC_HIP_TRY(hipGetLastError());
+      }
       MArgs g{};
       g.A = ctx->hb; g.W0 = L.w_qkv;
       g.K = d; g.Nout = qkv; g.N = N; g.r = r;
       if ((rc = run_mgemm<G_QKV>(ctx, st, "fc_mgemm_qkv", g, B)) != FC_OK) return rc;
     } else {
       WArgs g{};
-      g.A = ctx->hb; g.W0 = L.w_qkv;
+      g.A = x_cur; g.gather = 1; g.gain = L.g_attn; g.W0 = L.w_qkv;
       g.K = d; g.Nout = qkv; g.N = N; g.idx = idx; g.nrec = nrec;
       g.part = ctx->part; g.rows = rows; g.eps = L.rms_eps;
       if ((rc = run_wgemm<G_QKV>(ctx, st, "fc_gemm_qkv", g, B)) != FC_OK) return rc;
