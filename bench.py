@@ -230,6 +230,21 @@ def main():
                     traffic=measured_traffic("fc_gemm_gateup"), bytes_per_launch=round(gu_bytes),
                     avg_us=gu["avg_us"])
 
+    # the whole step against HBM: every layer streams its weights and reads the cached
+    # K/V; recomputed tokens read x and write y, K and V rows; reused tokens are copied by
+    # the cache remap (K, V and output rows read and written); the selection reads both
+    # frames
+    kvw = shape.n_kv * shape.hd
+    wbytes = 2 * (shape.qkv * d + d * shape.n_heads * shape.hd + 2 * f * d + d * f)
+    layer_bytes = (wbytes + 4 * S * kvw + n_mean * (4 * d + 4 * kvw)
+                   + (N - n_mean) * (8 * kvw + 4 * d))
+    step_bytes = L * layer_bytes + 2 * 3 * size * size * 4
+    step_gbs = step_bytes / (ms_step * 1e-3) / 1e9
+    roofline_step = dict(bound="hbm", achieved=round(step_gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                         frac=round(step_gbs / HBM_PEAK_GBS, 4), bytes_per_step=round(step_bytes),
+                         ideal_ms_per_step=round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4))
+    sclk = observed_sclk_mhz()
+
     result = dict(
         metric="frames/s per-step (select+cached layer); select HBM GB/s; layer MFMA util",
         value=round(args.steps / el, 3), unit="frames/s", n_gpus=1, steps=args.steps,
@@ -240,7 +255,7 @@ def main():
                     f"{L} Qwen2.5-VL-7B-shaped bf16 decoder layers over 2176 cached "
                     "positions, batch 1", frame=size, tokens=N, layers=L, seq=S, batch=1,
                     mean_recomputed_tokens=round(n_mean, 1)),
-        roofline=roofline, kernels=kern,
+        roofline=roofline, roofline_step=roofline_step, sclk_mhz=sclk, kernels=kern,
         context="paper (Table 2): 637 -> 401 ms/step, 1.59x, InternVLA-N1 on R2R-CE, one "
                 "NVIDIA A100 40GB, precision not stated; a different (whole-model) workload")
 
@@ -249,6 +264,20 @@ def main():
         result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
         result["tiny"] = bench_tiny(fc, torch)
         result["ablations"] = bench_ablations(fc, ctx, torch, frames, m, N)
+        # the two targets of the hot path side by side: selection (64 pairs of 448x448)
+        # against HBM peak, and the one-layer call against bf16 MFMA peak with its
+        # roofline ceiling (compute time over the larger of compute and HBM time)
+        ceil = {}
+        for k, v in result["layer_ratios"].items():
+            nn = v["n"]
+            lb = wbytes + 4 * S * kvw + nn * (4 * d + 4 * kvw)
+            t_c = v["flops"] / (BF16_PEAK_TFLOPS * 1e12)
+            t_m = lb / (HBM_PEAK_GBS * 1e9)
+            ceil[k] = round(t_c / max(t_c, t_m), 4)
+        result["north_star"] = dict(
+            selection_frac_hbm=result["select_batch"]["frac_hbm"], selection_target=0.60,
+            layer_mfma_util={k: v["mfma_util"] for k, v in result["layer_ratios"].items()},
+            layer_mfma_ceiling=ceil, layer_target=0.50)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(fc, torch, frames_np, layers[0], shape, sel, prm,
                                               T, N, Wn, L, gw)
@@ -266,6 +295,37 @@ def main():
         del src, dst
     ctx.close()
     print(json.dumps(result), flush=True)
+
+
+def timed_calls(torch, fn, reps=60, warm=5):
+    """Median, p10 and p90 (us) of `reps` calls of fn, each bracketed by its own pair of
+    HIP events on the current stream."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    return dict(p50=round(float(np.median(us)), 2), p10=round(float(np.percentile(us, 10)), 2),
+                p90=round(float(np.percentile(us, 90)), 2), runs=reps)
+
+
+def observed_sclk_mhz():
+    """Current shader clock of GPU 0 as rocm-smi reports it (None if unavailable)."""
+    import re
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "-d", "0", "--showclocks"], capture_output=True,
+                             text=True, timeout=20).stdout
+    except Exception:
+        return None
+    m = re.search(r"sclk.*?\((\d+)\s*Mhz\)", out, re.I)
+    return int(m.group(1)) if m else None
 
 
 def measured_traffic(kernel):
@@ -305,6 +365,7 @@ def bench_select_batch(fc, ctx, torch):
     e1.record()
     torch.cuda.synchronize()
     call_us = e0.elapsed_time(e1) * 1e3 / reps
+    dist = timed_calls(torch, lambda: fc.fc_select(ctx, prm, prev, cur, out))
     # per-kernel breakdown in a separate pass (events around every launch)
     fc.fc_profile_read(ctx, None, reset=True)
     fc.fc_profile_enable(ctx, True)
@@ -355,9 +416,11 @@ def bench_select_batch(fc, ctx, torch):
     for c_ in extra_ctx:
         c_.close()
     multi["note"] = "independent 64-pair batches over 2 or 3 streams, each with its own context"
+    g50 = (frame_bytes + out_bytes) / (dist["p50"] * 1e-6) / 1e9
     return dict(workload="64 pairs 448x448, 14-px patches, 1024 patches/frame, adaptive",
                 call_us=round(call_us, 2), algorithmic_bytes=frame_bytes + out_bytes,
                 gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
+                call_us_dist=dist, frac_hbm_p50=round(g50 / HBM_PEAK_GBS, 4),
                 spectra_gbs=round(spectra_gbs, 1), kernel_avg_us=kern,
                 multi_stream=multi)
 
@@ -472,13 +535,18 @@ def bench_layer_ratios(fc, ctx, torch, lay, shape):
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / reps
+        dist = timed_calls(torch, lambda: fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, idx,
+                                                              nrec, y))
         S = lay["kv"].S
         flops = 2.0 * n * (qkv * d + o * d + 2 * f * d + f * d) + 4.0 * n * shape.n_heads * shape.hd * (S - N / 2)
         tf = flops / (us * 1e-6) / 1e12
         gbs = wbytes / (us * 1e-6) / 1e9
+        tf50 = flops / (dist["p50"] * 1e-6) / 1e12
         out[f"reuse{r}"] = dict(n=n, us=round(us, 2), tflops=round(tf, 1),
                                 mfma_util=round(tf / BF16_PEAK_TFLOPS, 4),
-                                weight_gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4))
+                                weight_gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
+                                us_dist=dist, mfma_util_p50=round(tf50 / BF16_PEAK_TFLOPS, 4),
+                                flops=round(flops))
     return out
 
 
@@ -647,16 +715,18 @@ def bench_batch_episodes(fc, torch, frames_np, steps, L):
 
 
 def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
-    """The oracle as it stands on a bounded sample of the same step: selection of one
-    frame pair and two of the 28 layer calls at this step's mask, extrapolated to a
-    whole step (select + 28 layers)."""
+    """The oracle as it stands, timed on this host on bounded samples of the workloads:
+      * the episode step: selection of one frame pair and two of the 28 layer calls at
+        that step's mask, extrapolated to a whole step (select + 28 layers);
+      * the one-layer workload at every reuse ratio (one call each);
+      * selection of 448x448 pairs and the tiny configuration;
+      * a single-core leg: this thread pinned to one core with one BLAS thread, for the
+        selection of one pair and one layer call at 0 % reuse.
+    cores = the CPUs this process may run on (all-core figures)."""
     from oracle import layer as ol
     from oracle import select as osel
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
+    import fcdata
+    cores = len(os.sched_getaffinity(0))
     op = osel.SelectParams(merge=prm.merge)
     t0 = time.perf_counter()
     res = osel.select_item(frames_np[10], frames_np[11], op)
@@ -675,9 +745,12 @@ def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
         ol.layer_partial(x, res.recompute_idx, kc, vc, y_prev, lay_o, wt, shape)
     t_layer = (time.perf_counter() - t0) / reps
     t_step = t_sel + L * t_layer
-    # the oracle on the other configurations, small samples
-    import fcdata
     other = {}
+    for r in (0, 25, 50, 75, 90):
+        ids = fcdata.random_reuse_ids(100 + r, N, r)
+        t0 = time.perf_counter()
+        ol.layer_partial(x, ids, kc, vc, y_prev, lay_o, wt, shape)
+        other[f"qwen_layer_reuse{r}_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
     sp, sc, _ = fcdata.sel_pairs(1)
     t0 = time.perf_counter()
     for b in range(2):
@@ -694,16 +767,32 @@ def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
     ol.layer_partial(tx, tres.recompute_idx, tk, tk, tx, ol.Layout(T=32, N=256, W=1, head=0),
                      twt, tshape)
     other["tiny_select_plus_layer_ms"] = round((time.perf_counter() - t0) * 1e3, 2)
-    for r in (0, 50):
-        ids = fcdata.random_reuse_ids(100 + r, N, r)
-        t0 = time.perf_counter()
-        ol.layer_partial(x, ids, kc, vc, y_prev, lay_o, wt, shape)
-        other[f"qwen_layer_reuse{r}_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+    # single core: this thread on one CPU, one BLAS thread
+    single = None
+    try:
+        from threadpoolctl import threadpool_limits
+        aff = os.sched_getaffinity(0)
+        os.sched_setaffinity(0, {min(aff)})
+        try:
+            with threadpool_limits(limits=1):
+                t0 = time.perf_counter()
+                osel.select_item(frames_np[10], frames_np[11], op)
+                t1 = time.perf_counter()
+                ol.layer_partial(x, fcdata.random_reuse_ids(100, N, 0), kc, vc, y_prev, lay_o, wt,
+                                 shape)
+                t2 = time.perf_counter()
+        finally:
+            os.sched_setaffinity(0, aff)
+        single = dict(cores=1, select_448_pair_m2_ms=round((t1 - t0) * 1e3, 1),
+                      qwen_layer_reuse0_ms=round((t2 - t1) * 1e3, 1),
+                      step_frames_per_s=round(1.0 / ((t1 - t0) + L * (t2 - t1)), 5))
+    except Exception as e:  # a host without threadpoolctl or affinity control
+        single = dict(error=str(e))
     return dict(value=round(1.0 / t_step, 5), unit="frames/s", cores=int(cores), kind="oracle",
                 sample=f"oracle selection of one 448x448 pair ({t_sel:.2f}s) + {reps} oracle "
                        f"layer calls at n={res.n_recompute} ({t_layer:.2f}s each), extrapolated "
                        f"to select + {L} layers = {t_step:.1f}s/step",
-                other_configs=other)
+                other_configs=other, single_core=single)
 
 
 if __name__ == "__main__":
