@@ -1,8 +1,9 @@
 """Benchmark of the FreqCache per-step hot path on one MI355X.
 
 A step is one navigation step of a 32-step camera episode at batch 1:
-  fc_select on the (previous, current) 448x448 frame pair (14-px patches, 2x2
-  merge -> 256 visual tokens, adaptive budget), then the window advance and cache
+  fc_select_carry on the current 448x448 frame, the previous frame's spectra carried
+  from the previous step (14-px patches, 2x2 merge -> 256 visual tokens, adaptive
+  budget), then the window advance and cache
   remap of 28 Qwen2.5-VL-7B-shaped bf16 decoder layers (128 text + 8 frames x 256
   tokens = 2176 cached positions) in one fc_cache_update_layers call, and
   fc_layer_forward of each layer on the tokens the selection left for recompute.
@@ -156,13 +157,15 @@ def main():
                              max_qkv=shape.qkv))
     prm = fc.SelectParams(merge=m)
     sel = fc.SelectOut.alloc(1, N)
+    # the previous frame's spectra are carried from step to step (two state buffers)
+    states = [fc.select_state_alloc(1, size, size), fc.select_state_alloc(1, size, size)]
     cur_y = 0
 
     def step(s):
         nonlocal cur_y
         fi = s % n_frames
-        prev = None if fi == 0 else frames[fi - 1:fi]
-        fc.fc_select(ctx, prm, prev, frames[fi:fi + 1], sel)
+        fc.fc_select_carry(ctx, prm, None if fi == 0 else states[(s - 1) % 2],
+                           frames[fi:fi + 1], states[s % 2], sel)
         x = emb[fi:fi + 1]
         nxt = 1 - cur_y
         # every layer's window advance and cache remap in one launch: a layer reads
@@ -238,7 +241,7 @@ def main():
     wbytes = 2 * (shape.qkv * d + d * shape.n_heads * shape.hd + 2 * f * d + d * f)
     layer_bytes = (wbytes + 4 * S * kvw + n_mean * (4 * d + 4 * kvw)
                    + (N - n_mean) * (8 * kvw + 4 * d))
-    step_bytes = L * layer_bytes + 2 * 3 * size * size * 4
+    step_bytes = L * layer_bytes + 3 * size * size * 4 + 2 * fc.select_state_bytes(1, size, size)
     step_gbs = step_bytes / (ms_step * 1e-3) / 1e9
     roofline_step = dict(bound="hbm", achieved=round(step_gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                          frac=round(step_gbs / HBM_PEAK_GBS, 4), bytes_per_step=round(step_bytes),
@@ -439,10 +442,15 @@ def bench_ablations(fc, ctx, torch, frames, m, N):
         "wo_module3_fixed30": dict(adaptive=False, alpha_fixed=0.3),
         "full_tau_sim_0.9": dict(tau_sim=0.9),
         "wo_module1_tau_sim_0.9": dict(align=False, tau_sim=0.9),
+        "naive_tau_0.99": "naive",
+        "naive_tau_0.999": "naive",
     }
     res = {}
     for name, kw in variants.items():
-        prm = fc.SelectParams(merge=m, **kw)
+        if kw == "naive":
+            prm = fc.SelectParams.naive(float(name.rsplit("_", 1)[1]), merge=m)
+        else:
+            prm = fc.SelectParams(merge=m, **kw)
         fc.fc_select(ctx, prm, prev, cur, out)
         torch.cuda.synchronize()
         counts = out.counts.cpu().numpy()
@@ -451,7 +459,8 @@ def bench_ablations(fc, ctx, torch, frames, m, N):
                          flushed=int(counts[:, 3].sum()))
     res["pairs"] = B
     res["paper_context"] = ("Table 3 token reuse on R2R-CE: full 53.5 %, w/o I 19.8 %, "
-                            "w/o II 57.0 %, w/o III (fixed 30 %) 38.6 %")
+                            "w/o II 57.0 %, w/o III (fixed 30 %) 38.6 %; Table 2: naive "
+                            "frequency method 15.2 %")
     return res
 
 

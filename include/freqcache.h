@@ -40,6 +40,7 @@
 #ifndef FREQCACHE_H
 #define FREQCACHE_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -89,6 +90,9 @@ typedef struct {
                                and every token aligned (phase correlation not used)       */
   int32_t no_refresh;       /* 1: "w/o Module II", no token is refreshed by its edge energy
                                (mu_E, sigma_E and the threshold are still reported)       */
+  /* The paper's naive frequency baseline (Sec. 6.1: position-wise amplitude similarity,
+     static reuse above a fixed threshold tau) is no_align = 1, no_refresh = 1,
+     adaptive = 0 with alpha_fixed = 1, tau_mig = 0 and tau_sim = tau.                     */
 } fc_select_params;
 
 enum { FC_SCALAR_SIM_FREQ = 0, FC_SCALAR_PSI, FC_SCALAR_ALPHA, FC_SCALAR_MU,
@@ -162,6 +166,26 @@ fc_status fc_destroy(fc_ctx *ctx);
 fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frames_prev,
                     const float *frames_cur, int32_t B, int32_t H, int32_t W,
                     const fc_select_out *out, void *stream);
+
+/* Bytes of the carried selection state of a batch of B frames of H x W pixels (the
+ * spectra of one frame per item: per-patch DFT amplitudes and mean luma; an opaque
+ * device buffer the caller allocates, at least 16-byte aligned).  0 for sizes that
+ * hold no patch.  (host function, no device work) */
+size_t fc_select_state_bytes(int32_t B, int32_t H, int32_t W);
+
+/* fc_select along an episode, with the previous frame's spectra carried from the
+ * previous step instead of recomputed from its pixels (Algorithm 1 needs the
+ * previous frame only through its per-patch amplitude spectra and patch means).
+ *   state_prev: the state_cur of the previous call on the same frame size and batch,
+ *               or NULL at the first step (no previous frame: flushed, as fc_select
+ *               with frames_prev = NULL);
+ *   state_cur:  receives this frame's spectra; fc_select_state_bytes(B, H, W) bytes,
+ *               not aliasing state_prev (callers alternate two buffers).
+ * Outputs are byte-identical to fc_select on the pixels of both frames.  The states
+ * hold no meaning for other sizes or parameters of P (not checked). */
+fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *state_prev,
+                          const float *frames_cur, void *state_cur, int32_t B, int32_t H,
+                          int32_t W, const fc_select_out *out, void *stream);
 
 /* fc_select without a context and without any device allocation, for callers that
  * cannot allocate device memory (code under HIP graph capture, tight serving loops,

@@ -327,6 +327,46 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
         flushed=bool(flushed), response=resp)
 
 
+@dataclass
+class NaiveResult:
+    reuse_mask: np.ndarray        # [N] uint8
+    recompute_idx: np.ndarray     # ascending int32
+    sim: np.ndarray               # [N] position-wise amplitude-spectrum cosine
+
+    @property
+    def n_recompute(self) -> int:
+        return int(self.recompute_idx.size)
+
+
+def naive_select(prev: np.ndarray | None, cur: np.ndarray, patch: int, merge: int,
+                 tau: float) -> NaiveResult:
+    """The naive frequency baseline the paper compares against (Sec. 6.1): the frame is
+    cut into patches, each token's 2-D FFT amplitude spectrum is compared with the
+    previous frame's at the same position (cosine, Eq. 3-3 per token), and every token
+    whose similarity reaches the fixed threshold tau is reused -- no alignment, no
+    refresh, no adaptive budget and no migration gate.  A missing previous frame is an
+    all-zero frame (similarity 0: nothing is reused)."""
+    y_cur = luma(cur)
+    y_prev = luma(prev) if prev is not None else np.zeros_like(y_cur)
+    a_cur = token_view(patch_amplitude(patches(y_cur, patch)), merge)
+    a_prev = token_view(patch_amplitude(patches(y_prev, patch)), merge)
+    gh, gw = a_cur.shape[:2]
+    sim = np.zeros((gh, gw))
+    for i in range(gh):
+        for j in range(gw):
+            u = a_cur[i, j].ravel()
+            v = a_prev[i, j].ravel()
+            nu, nv = np.sqrt(np.sum(u * u)), np.sqrt(np.sum(v * v))
+            if nu == 0.0 and nv == 0.0:
+                sim[i, j] = 1.0
+            elif nu > 0.0 and nv > 0.0:
+                sim[i, j] = np.sum(u * v) / (nu * nv)
+    reuse = (sim.ravel() >= tau).astype(np.uint8)
+    return NaiveResult(reuse_mask=reuse,
+                       recompute_idx=np.flatnonzero(reuse == 0).astype(np.int32),
+                       sim=sim.ravel())
+
+
 def select_batch(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> list:
     """select_item over a [B, 3, H, W] batch."""
     return [select_item(None if prev is None else prev[b], cur[b], prm)

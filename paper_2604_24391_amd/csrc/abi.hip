@@ -55,17 +55,32 @@ ProfScope::~ProfScope() {
   if (stop) hipEventRecord(stop, st);
 }
 
-SelectWsBytes select_ws_bytes(long B, long H, long W) {
+SpectraBytes spectra_bytes(long B, long H, long W) {
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t np = (size_t)(H / kPatch) * (W / kPatch);
   // amplitudes in 16-patch chunks of a patch row (the last chunk of a row padded)
   const size_t np16 = (size_t)(H / kPatch) * ((W / kPatch + 15) / 16) * 16;
+  SpectraBytes b;
+  b.amp = al((size_t)B * kBins * np16 * sizeof(float));
+  b.pmean = al((size_t)B * np * sizeof(double));
+  b.total = b.amp + b.pmean;
+  return b;
+}
+
+FrameSpectra spectra_at(void *base, long B, long H, long W) {
+  const SpectraBytes b = spectra_bytes(B, H, W);
+  unsigned char *p = static_cast<unsigned char *>(base);
+  return FrameSpectra{reinterpret_cast<float *>(p), reinterpret_cast<double *>(p + b.amp)};
+}
+
+SelectWsBytes select_ws_bytes(long B, long H, long W) {
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t np = (size_t)(H / kPatch) * (W / kPatch);
   SelectWsBytes b;
-  b.amp = al((size_t)B * 2 * kBins * np16 * sizeof(float));
-  b.pmean = al((size_t)B * 2 * np * sizeof(double));
+  b.spectra = spectra_bytes(B, H, W).total;
   b.penergy = al((size_t)B * np * sizeof(double));
   b.pdot = al((size_t)B * 3 * np * sizeof(double));
-  b.total = b.amp + b.pmean + b.penergy + b.pdot;
+  b.total = 2 * b.spectra + b.penergy + b.pdot;
   return b;
 }
 
@@ -115,7 +130,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 }
 
 void free_ws(fc_ctx *c) {
-  void *ptrs[] = {c->amp, c->pmean, c->penergy, c->pdot, c->qbuf, c->attn,
+  void *ptrs[] = {c->spec, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
                   c->krot};
   for (void *p : ptrs)
@@ -184,8 +199,8 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
   if ((long)rows >= fc::kBigRows) ctx->krot_elems = B * (size_t)c.max_seq * ((c.max_qkv + 2) / 3);
   fc_status st = FC_OK;
   const fc::SelectWsBytes sb = fc::select_ws_bytes(B, c.max_height, c.max_width);
-  if ((st = dev_alloc(&ctx->amp, sb.amp / sizeof(float), "amp")) != FC_OK ||
-      (st = dev_alloc(&ctx->pmean, sb.pmean / sizeof(double), "pmean")) != FC_OK ||
+  ctx->spec_half = sb.spectra;
+  if ((st = dev_alloc(&ctx->spec, 2 * sb.spectra, "spectra")) != FC_OK ||
       (st = dev_alloc(&ctx->penergy, sb.penergy / sizeof(double), "penergy")) != FC_OK ||
       (st = dev_alloc(&ctx->pdot, sb.pdot / sizeof(double), "pdot")) != FC_OK ||
       (st = dev_alloc(&ctx->qbuf, rows * c.max_qkv, "q")) != FC_OK ||
@@ -229,9 +244,43 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
     return fail(FC_ERR_CAPACITY, "fc_select: B=%d H=%d W=%d N=%d exceed the context caps", B, H, W, M);
   st = use_device(ctx);
   if (st != FC_OK) return st;
-  const fc::SelectWs ws{ctx->amp, ctx->pmean, ctx->penergy, ctx->pdot};
+  const fc::SelectWs ws{fc::spectra_at(ctx->spec, B, H, W),
+                        fc::spectra_at(ctx->spec + ctx->spec_half, B, H, W), ctx->penergy,
+                        ctx->pdot};
   return fc::launch_select(ctx, ws, *prm, frames_prev, frames_cur, B, H, W, *out,
                            reinterpret_cast<hipStream_t>(stream));
+}
+
+size_t fc_select_state_bytes(int32_t B, int32_t H, int32_t W) {
+  if (B < 1 || H < fc::kPatch || W < fc::kPatch) return 0;
+  return fc::spectra_bytes(B, H, W).total;
+}
+
+fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *state_prev,
+                          const float *frames_cur, void *state_cur, int32_t B, int32_t H,
+                          int32_t W, const fc_select_out *out, void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_select_carry: null context");
+  fc_status st = fc::check_select_args(prm, frames_cur, out, B, H, W, "fc_select_carry");
+  if (st != FC_OK) return st;
+  if (!state_cur) return fail(FC_ERR_INVALID_ARG, "fc_select_carry: null state_cur");
+  if (state_cur == state_prev)
+    return fail(FC_ERR_INVALID_ARG, "fc_select_carry: state_prev and state_cur alias");
+  const int tp = prm->patch * prm->merge;
+  const int M = (H / tp) * (W / tp);
+  if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width ||
+      M > ctx->caps.max_tokens)
+    return fail(FC_ERR_CAPACITY, "fc_select_carry: B=%d H=%d W=%d N=%d exceed the context caps",
+                B, H, W, M);
+  st = use_device(ctx);
+  if (st != FC_OK) return st;
+  // without a previous state the previous frame is an all-zero frame, transformed into
+  // the context's own previous half
+  const bool carried = state_prev != nullptr;
+  const fc::SelectWs ws{carried ? fc::spectra_at(const_cast<void *>(state_prev), B, H, W)
+                                : fc::spectra_at(ctx->spec, B, H, W),
+                        fc::spectra_at(state_cur, B, H, W), ctx->penergy, ctx->pdot};
+  return fc::launch_select(ctx, ws, *prm, nullptr, frames_cur, B, H, W, *out,
+                           reinterpret_cast<hipStream_t>(stream), carried);
 }
 
 fc_status fc_select_noalloc(const fc_select_params *prm, const float *frames_prev,

@@ -46,8 +46,8 @@ struct fc_ctx {
   fc_caps caps{};
   int num_cus = 0;
   // selection workspace
-  float *amp = nullptr;        // [B][2][kBins][Np] per-patch DFT amplitude (prev, cur)
-  double *pmean = nullptr;     // [B][2][Np] per-patch mean luma
+  unsigned char *spec = nullptr;   // spectra of two frame batches (prev, cur), FrameSpectra layout
+  size_t spec_half = 0;            // bytes of one
   double *penergy = nullptr;   // [B][Np] per-patch high-pass DCT energy (current frame)
   double *pdot = nullptr;      // [B][3][Np] per-patch spectral products (dot, |cur|^2, |src|^2)
   // layer workspace
@@ -85,16 +85,28 @@ struct ProfScope {
 };
 
 // ----------------------------------------------------------------------------- launchers
-// Selection workspace: per-patch amplitudes, means, energies and spectral products.
+// Spectra of one batch of frames: per-patch DFT amplitudes in 16-patch chunks
+// [B][patch row][chunk][kBins][16] and per-patch mean luma [B][Np].  The layout of the
+// carried selection state of fc_select_carry.
+struct FrameSpectra {
+  float *amp;
+  double *pmean;
+};
+// Selection workspace: spectra of the previous and the current frames, per-patch
+// high-pass energies (current frame) and spectral products.
 struct SelectWs {
-  float *amp;        // [B][2][chunk rows][kBins][16]
-  double *pmean;     // [B][2][Np]
+  FrameSpectra prev, cur;
   double *penergy;   // [B][Np]
   double *pdot;      // [B][3][Np]
 };
-// Bytes of each workspace part for B pairs of H x W frames (256-B aligned parts).
+// Bytes of one frame batch's spectra (256-B aligned parts) and of the whole workspace.
+struct SpectraBytes {
+  size_t amp, pmean, total;
+};
+SpectraBytes spectra_bytes(long B, long H, long W);
+FrameSpectra spectra_at(void *base, long B, long H, long W);
 struct SelectWsBytes {
-  size_t amp, pmean, penergy, pdot, total;
+  size_t spectra, penergy, pdot, total;   // spectra: one frame batch (two are used)
 };
 SelectWsBytes select_ws_bytes(long B, long H, long W);
 
@@ -102,10 +114,11 @@ SelectWsBytes select_ws_bytes(long B, long H, long W);
 fc_status check_select_args(const fc_select_params *prm, const float *cur,
                             const fc_select_out *out, int B, int H, int W, const char *who);
 
-// ctx may be null (no kernel timing)
+// ctx may be null (no kernel timing).  carried: the previous frame's spectra are
+// already in ws.prev (prev pixels unused); otherwise both frames are transformed.
 fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params &prm,
                         const float *prev, const float *cur, int B, int H, int W,
-                        const fc_select_out &out, hipStream_t st);
+                        const fc_select_out &out, hipStream_t st, bool carried = false);
 // The same on the calling thread's current device, with the workspace in the library's
 // static device scratch array (no allocation).
 fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,

@@ -56,40 +56,45 @@ __device__ __forceinline__ double bin_weight(int bin) {
   return (bin == 0 || bin == 7 || bin == 8 || bin == 15) ? 1.0 : 2.0;
 }
 
-// Amplitudes are stored per 16-patch chunk of a patch row, [b*2 + f][chunk][bin][16],
-// chunk = pi * ncx + pj / 16 with ncx = ceil(Gpw / 16): one k_spectra workgroup writes
-// its whole 6.4 KB block with full-line stores (a bin-major layout cost it 64-B pieces).
-__device__ __forceinline__ size_t amp_chunk(int bf, int pi, int cx, int Gph, int ncx) {
-  return ((size_t)bf * Gph * ncx + (size_t)pi * ncx + cx) * NB * 16;
+// Amplitudes of a frame batch are stored per 16-patch chunk of a patch row,
+// [b][chunk][bin][16], chunk = pi * ncx + pj / 16 with ncx = ceil(Gpw / 16): one
+// k_spectra workgroup writes its whole 6.4 KB block with full-line stores (a bin-major
+// layout cost it 64-B pieces).  The previous and the current frames have separate
+// buffers, so the current frame's spectra can be carried to the next step.
+__device__ __forceinline__ size_t amp_chunk(int b, int pi, int cx, int Gph, int ncx) {
+  return ((size_t)b * Gph * ncx + (size_t)pi * ncx + cx) * NB * 16;
 }
 
 // ------------------------------------------------------------------------------- k_spectra
-// Grid: x = 16-patch chunk of a patch row, y = patch row, z = 2 * b + frame (0 prev,
-// 1 cur).  Outputs (workspace):
-//   amp[amp_chunk(b*2 + f, pi, chunk) + bin * 16 + slot]  float32 amplitude, unique bins:
+// Grid: x = 16-patch chunk of a patch row, y = patch row, z = item and frame: z = 2 b + f
+// (f = 0 prev, 1 cur), or z = b for the current frame only (nf = 1, the previous
+// frame's spectra carried).  Outputs per frame f:
+//   amp_f[amp_chunk(b, pi, chunk) + bin * 16 + slot]  float32 amplitude, unique bins:
 //       bins 0..7   = (u = 0..7,  v = 0),  bins 8..15 = (u = 0..7, v = 7),
 //       bins 16..99 = (u = 0..13, v = 1..6)   (the rest follow from A(u,v) = A(-u,-v));
-//   pmean[(b*2 + f) * Np + patch]  float64 mean luma;
-//   penergy[b * Np + patch]        float64 high-pass DCT energy (current frame only).
+//   pmean_f[b * Np + patch]       float64 mean luma;
+//   penergy[b * Np + patch]       float64 high-pass DCT energy (current frame only).
 __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
                                                  const float *__restrict__ cur, int H, int W,
-                                                 int Gph, int Gpw, float *__restrict__ amp,
-                                                 double *__restrict__ pmean,
+                                                 int Gph, int Gpw, int nf, FrameSpectra sp_prev,
+                                                 FrameSpectra sp_cur,
                                                  double *__restrict__ penergy) {
-  const int f = blockIdx.z & 1;
-  const int b = blockIdx.z >> 1;
+  const int f = nf == 1 ? 1 : (int)(blockIdx.z & 1);
+  const int b = nf == 1 ? (int)blockIdx.z : (int)(blockIdx.z >> 1);
   const int pi = blockIdx.y;
   const int j0 = blockIdx.x * PW;
   const int pw = min(PW, Gpw - j0);
   const int Np = Gph * Gpw;
   const int t = threadIdx.x;
   const float *frame = f ? cur : prev;
+  float *__restrict__ amp = f ? sp_cur.amp : sp_prev.amp;
+  double *__restrict__ pmean = f ? sp_cur.pmean : sp_prev.pmean;
 
   const int ncx = (Gpw + PW - 1) / PW;
-  float4 *ablk = reinterpret_cast<float4 *>(amp + amp_chunk(b * 2 + f, pi, blockIdx.x, Gph, ncx));
+  float4 *ablk = reinterpret_cast<float4 *>(amp + amp_chunk(b, pi, blockIdx.x, Gph, ncx));
   if (frame == nullptr) {  // no previous frame: an all-zero frame
     for (int e = t; e < NB * PW / 4; e += blockDim.x) ablk[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (t < pw) pmean[(size_t)(b * 2 + f) * Np + pi * Gpw + j0 + t] = 0.0;
+    if (t < pw) pmean[(size_t)b * Np + pi * Gpw + j0 + t] = 0.0;
     return;
   }
 
@@ -307,7 +312,7 @@ __global__ __launch_bounds__(256) void k_spectra(const float *__restrict__ prev,
     double sum = 0.0;
 #pragma unroll
     for (int y = 0; y < P; ++y) sum += sRs[t][y];
-    pmean[(size_t)(b * 2 + f) * Np + patch] = sum / (double)(P * P);
+    pmean[(size_t)b * Np + patch] = sum / (double)(P * P);
     if (f == 1) {
       double e = 0.0;
 #pragma unroll
@@ -646,7 +651,8 @@ struct GridParams {
 // LDS: four complex grids (two maps, two transposed scratch grids) and the twiddles
 // of both axes.
 constexpr int kGridThreads = 1024;
-__global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict__ pmean,
+__global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict__ pmean_prev,
+                                                       const double *__restrict__ pmean_cur,
                                                        const double *__restrict__ penergy,
                                                        GridParams g, double *__restrict__ energy,
                                                        int32_t *__restrict__ shift,
@@ -684,8 +690,8 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
     for (int a2 = 0; a2 < m; ++a2)
       for (int c2 = 0; c2 < m; ++c2) {
         const int p = (m * I + a2) * g.Gpw + m * J + c2;
-        gc += pmean[(size_t)(b * 2 + 1) * Np + p];
-        gp += pmean[(size_t)(b * 2 + 0) * Np + p];
+        gc += pmean_cur[(size_t)b * Np + p];
+        gp += pmean_prev[(size_t)b * Np + p];
         et += penergy[(size_t)b * Np + p];
       }
     A[t] = make_double2(gc * inv_mm, 0.0);
@@ -796,7 +802,8 @@ __global__ __launch_bounds__(kGridThreads) void k_grid(const double *__restrict_
 // workgroup split the 100 bins for the same 64 patches, so loads of one bin are 64
 // consecutive patches.  Output pdot[(b * 3 + {dot, n_cur, n_src}) * Np + patch].
 constexpr int kSimBinsPerWave = NB / 4;
-__global__ __launch_bounds__(256) void k_patchsim(const float *__restrict__ amp, int Gph, int Gpw,
+__global__ __launch_bounds__(256) void k_patchsim(const float *__restrict__ amp_prev,
+                                                  const float *__restrict__ amp_cur, int Gph, int Gpw,
                                                   int m, const int32_t *__restrict__ shift,
                                                   double *__restrict__ pdot) {
   __shared__ double part[3][4][64];
@@ -812,8 +819,8 @@ __global__ __launch_bounds__(256) void k_patchsim(const float *__restrict__ amp,
   const bool al = si >= 0 && si < Gh && sj >= 0 && sj < Gw;
   const int spi = al ? pi + m * di : pi, spj = al ? pj + m * dj : pj;
   const int ncx = (Gpw + PW - 1) / PW;
-  const float *ac = amp + amp_chunk(b * 2 + 1, pi, pj / PW, Gph, ncx) + (pj % PW);
-  const float *ap = amp + amp_chunk(b * 2 + 0, spi, spj / PW, Gph, ncx) + (spj % PW);
+  const float *ac = amp_cur + amp_chunk(b, pi, pj / PW, Gph, ncx) + (pj % PW);
+  const float *ap = amp_prev + amp_chunk(b, spi, spj / PW, Gph, ncx) + (spj % PW);
   float x[kSimBinsPerWave], y[kSimBinsPerWave];
 #pragma unroll
   for (int i = 0; i < kSimBinsPerWave; ++i) {
@@ -1011,29 +1018,31 @@ fc_status upload_select_tables() {
 
 fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params &prm,
                         const float *prev, const float *cur, int B, int H, int W,
-                        const fc_select_out &out, hipStream_t st) {
+                        const fc_select_out &out, hipStream_t st, bool carried) {
   const int m = prm.merge;
   const int Gph = H / P, Gpw = W / P;
   {
     ProfScope ps(ctx, st, "fc_spectra");
-    dim3 grid((Gpw + PW - 1) / PW, Gph, 2 * B);
-    hipLaunchKernelGGL(k_spectra, grid, dim3(256), 0, st, prev, cur, H, W, Gph, Gpw, ws.amp,
-                       ws.pmean, ws.penergy);
+    const int nf = carried ? 1 : 2;
+    dim3 grid((Gpw + PW - 1) / PW, Gph, nf * B);
+    hipLaunchKernelGGL(k_spectra, grid, dim3(256), 0, st, prev, cur, H, W, Gph, Gpw, nf, ws.prev,
+                       ws.cur, ws.penergy);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_grid");
     GridParams g{Gph, Gpw, m, prm.tau_mig, prm.lambda_, prm.alpha_min, prm.alpha_max,
                  prm.alpha_fixed, prm.adaptive, prm.entropy_norm, prm.no_align};
-    hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ws.pmean, ws.penergy, g,
+    hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ws.prev.pmean, ws.cur.pmean,
+                       ws.penergy, g,
                        out.energy, out.shift, out.scalars, out.counts);
     FC_HIP_TRY(hipGetLastError());
   }
   {
     ProfScope ps(ctx, st, "fc_patchsim");
     dim3 grid((Gph * Gpw + 63) / 64, B);
-    hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ws.amp, Gph, Gpw, m, out.shift,
-                       ws.pdot);
+    hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ws.prev.amp, ws.cur.amp, Gph, Gpw, m,
+                       out.shift, ws.pdot);
     FC_HIP_TRY(hipGetLastError());
   }
   {
@@ -1105,10 +1114,10 @@ fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
   fc_status s = noalloc_setup(dev, &base);
   if (s != FC_OK) return s;
   SelectWs ws;
-  ws.amp = reinterpret_cast<float *>(base);
-  ws.pmean = reinterpret_cast<double *>(base + sb.amp);
-  ws.penergy = reinterpret_cast<double *>(base + sb.amp + sb.pmean);
-  ws.pdot = reinterpret_cast<double *>(base + sb.amp + sb.pmean + sb.penergy);
+  ws.prev = spectra_at(base, B, H, W);
+  ws.cur = spectra_at(base + sb.spectra, B, H, W);
+  ws.penergy = reinterpret_cast<double *>(base + 2 * sb.spectra);
+  ws.pdot = reinterpret_cast<double *>(base + 2 * sb.spectra + sb.penergy);
   return launch_select(nullptr, ws, prm, prev, cur, B, H, W, out, st);
 }
 

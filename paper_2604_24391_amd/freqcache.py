@@ -29,7 +29,7 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
-           "fc_select_noalloc", "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
+           "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
            "fc_profile_only", "fc_profile_read")
 
 
@@ -91,6 +91,11 @@ def lib() -> ctypes.CDLL:
         L.fc_select_noalloc.argtypes = [ctypes.POINTER(fc_select_params), c_void_p, c_void_p,
                                         c_int32, c_int32, c_int32, ctypes.POINTER(fc_select_out),
                                         c_void_p]
+        L.fc_select_state_bytes.argtypes = [c_int32, c_int32, c_int32]
+        L.fc_select_state_bytes.restype = ctypes.c_size_t
+        L.fc_select_carry.argtypes = [c_void_p, ctypes.POINTER(fc_select_params), c_void_p,
+                                      c_void_p, c_void_p, c_int32, c_int32, c_int32,
+                                      ctypes.POINTER(fc_select_out), c_void_p]
         L.fc_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                       ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                       c_void_p, c_int32, c_int32, c_void_p]
@@ -105,7 +110,8 @@ def lib() -> ctypes.CDLL:
         L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
-        for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_cache_update",
+        for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
+                  "fc_cache_update",
                   "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
@@ -220,6 +226,16 @@ class SelectParams:
     align: bool = True          # False: ablation "w/o Module I" (position-wise matching)
     refresh: bool = True        # False: ablation "w/o Module II" (no edge refresh)
 
+    @classmethod
+    def naive(cls, tau: float, merge: int = 1) -> "SelectParams":
+        """The paper's naive frequency baseline (Sec. 6.1): position-wise amplitude-spectrum
+        similarity and static reuse of every token that reaches the fixed threshold tau.
+        It is Algorithm 1 with alignment, refresh, the adaptive budget and the migration
+        gate switched off (shift 0, no fresh token, a 100 % budget, tau_mig = 0) and the
+        similarity floor at tau."""
+        return cls(merge=merge, tau_mig=0.0, adaptive=False, alpha_fixed=1.0, tau_sim=tau,
+                   align=False, refresh=False)
+
     def c(self) -> fc_select_params:
         return fc_select_params(self.patch, self.merge, self.tau_mig, self.lam, self.alpha_min,
                                 self.alpha_max, int(self.adaptive), self.alpha_fixed,
@@ -304,6 +320,30 @@ def fc_select_noalloc(prm: SelectParams, prev: torch.Tensor | None, cur: torch.T
     cp, pp, pc, B, H, W, co = _select_args(prm, prev, cur, out)
     _check(lib().fc_select_noalloc(ctypes.byref(cp), pp, pc, B, H, W, ctypes.byref(co),
                                    _stream(stream)))
+
+
+def select_state_bytes(B: int, H: int, W: int) -> int:
+    return int(lib().fc_select_state_bytes(B, H, W))
+
+
+def select_state_alloc(B: int, H: int, W: int, device="cuda") -> torch.Tensor:
+    """A device buffer for the carried selection state of B frames of H x W."""
+    n = select_state_bytes(B, H, W)
+    if n == 0:
+        raise ValueError(f"no selection state for B={B} H={H} W={W}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def fc_select_carry(ctx: Context, prm: SelectParams, state_prev: torch.Tensor | None,
+                    cur: torch.Tensor, state_cur: torch.Tensor, out: SelectOut, stream=None):
+    """fc_select with the previous frame's spectra carried in state_prev (None at the
+    first step); this frame's spectra go to state_cur."""
+    cp, _, pc, B, H, W, co = _select_args(prm, None, cur, out)
+    n = select_state_bytes(B, H, W)
+    ps = c_void_p(0) if state_prev is None else _ptr(state_prev, torch.uint8, n, "state_prev")
+    pcur = _ptr(state_cur, torch.uint8, n, "state_cur")
+    _check(lib().fc_select_carry(ctx.handle, ctypes.byref(cp), ps, pc, pcur, B, H, W,
+                                 ctypes.byref(co), _stream(stream)))
 
 
 # ------------------------------------------------------------------------------ layer

@@ -132,3 +132,15 @@ def test_select_noalloc_rejects_before_device_work(fc):
     st = lib.fc_select_noalloc(ctypes.byref(prm), None, ctypes.c_void_p(1), 1, 100, 224,
                                ctypes.byref(fake), None)
     assert st == 2
+
+
+def test_select_state_bytes_and_carry_errors(fc):
+    """The carried selection state of one 448x448 frame: 1024 patches x 100 amplitude bins
+    (float32, 16-patch chunks) and 1024 patch means (float64), each part 256-B aligned;
+    sizes without a patch give 0.  fc_select_carry rejects null or aliased arguments
+    before any device work."""
+    assert fc.select_state_bytes(1, 448, 448) == 409600 + 8192
+    assert fc.select_state_bytes(2, 224, 448) == 2 * 16 * 32 * 100 * 4 + 2 * 512 * 8
+    assert fc.select_state_bytes(0, 448, 448) == 0 and fc.select_state_bytes(1, 10, 448) == 0
+    lib = fc.lib()
+    assert lib.fc_select_carry(None, None, None, None, None, 1, 224, 224, None, None) == 1

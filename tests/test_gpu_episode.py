@@ -1,6 +1,7 @@
 """The per-step chain of an episode against an oracle chain (through the C ABI).
 
-A step is: fc_select on the (previous, current) frame pair, the window advance of
+A step is: fc_select_carry on the current frame (the previous frame's spectra carried
+from the previous step), the window advance of
 every layer's cache, one fc_cache_update_layers call for all layers (each reused
 token takes its aligned source token's cached rows, Sec. 4.1 / Eq. 4-2), then
 fc_layer_forward layer by layer on the tokens the selection left for recompute
@@ -46,6 +47,7 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
     emb_gpu = fcutil.bf16_gpu(emb)
     frames_gpu = torch.from_numpy(np.ascontiguousarray(frames)).cuda()
     sel = fc.SelectOut.alloc(1, N)
+    states = [fc.select_state_alloc(1, H, Wpx), fc.select_state_alloc(1, H, Wpx)]
 
     # seeded start: random caches and output buffers per layer, identical on both sides
     gpu, ora = [], []
@@ -68,7 +70,8 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         prev = None if fi == 0 else frames[fi - 1]
         nxt = 1 - cur
         # ---- GPU: the benchmark's step
-        fc.fc_select(ctx, prm, None if fi == 0 else frames_gpu[fi - 1:fi], frames_gpu[fi:fi + 1], sel)
+        fc.fc_select_carry(ctx, prm, None if fi == 0 else states[(s - 1) % 2],
+                           frames_gpu[fi:fi + 1], states[s % 2], sel)
         for g in gpu:
             g["kv"].advance()
         fc.fc_cache_update_layers(ctx, gpu[0]["desc"], [g["kv"] for g in gpu],

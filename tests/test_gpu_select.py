@@ -247,3 +247,63 @@ def test_batched_episode_frames_896(fc):
               f"{min(m['topk'] for m in margins):.2e}")
     finally:
         c.close()
+
+
+@pytest.mark.parametrize("case", ["episode_merge2", "pairs_448"])
+def test_naive_selector(fc, ctx, case):
+    """The naive frequency baseline of Sec. 6.1 (position-wise amplitude similarity,
+    static reuse at a fixed threshold), run as fc_select with alignment, refresh, the
+    adaptive budget and the gate switched off, against the oracle's direct
+    formulation of it: reuse masks and recompute ids bit-exact, similarities within
+    1e-5, no token within 1e-5 of the threshold on these seeds."""
+    if case == "episode_merge2":
+        fr = fcdata.episode_frames(2024, size=448, n_frames=5)
+        prev, cur, m = fr[:4], fr[1:5], 2
+    else:
+        prev, cur, _ = fcdata.sel_pairs(1, batch=4)
+        m = 1
+    # thresholds chosen so that no similarity of these seeds lies within 1e-4 of them
+    # (position-wise similarities crowd just below 1 on these frames)
+    for tau in (0.94, 0.9675):
+        prm = fc.SelectParams.naive(tau, merge=m)
+        o = run_select(fc, ctx, prm, prev, cur)
+        for b in range(cur.shape[0]):
+            res = osel.naive_select(prev[b], cur[b], 14, m, tau)
+            near = np.abs(res.sim - tau) < fcutil.MARGIN * tau
+            assert not near.any(), f"tokens within 1e-5 of tau: {np.flatnonzero(near)}"
+            fcutil._close(o["sim"][b], res.sim, "sim")
+            np.testing.assert_array_equal(o["reuse_mask"][b], res.reuse_mask)
+            n = res.n_recompute
+            assert int(o["n_recompute"][b]) == n
+            np.testing.assert_array_equal(o["recompute_idx"][b][:n], res.recompute_idx)
+            assert tuple(o["shift"][b]) == (0, 0) and int(o["counts"][b][3]) == 0
+            assert int(o["counts"][b][2]) == int(res.reuse_mask.sum())
+
+
+def test_carried_spectra_match_pixels(fc, ctx):
+    """fc_select_carry along two trajectories at once (448x448, 2x2 merge): the first
+    step without a previous state is flushed, and every step's outputs are byte for
+    byte those of fc_select on both frames' pixels; two steps are also checked against
+    the oracle."""
+    eps = [fcdata.episode_frames(40 + e, size=448, n_frames=5) for e in range(2)]
+    fr = torch.from_numpy(np.ascontiguousarray(np.stack(eps, axis=1))).cuda()   # [5, 2, 3, H, W]
+    prm = fc.SelectParams(merge=2)
+    op = fcutil.oracle_select_params(prm)
+    states = [fc.select_state_alloc(2, 448, 448), fc.select_state_alloc(2, 448, 448)]
+    for s in range(5):
+        got = fc.SelectOut.alloc(2, 256)
+        ref = fc.SelectOut.alloc(2, 256)
+        fc.fc_select_carry(ctx, prm, None if s == 0 else states[(s - 1) % 2], fr[s], states[s % 2],
+                           got)
+        fc.fc_select(ctx, prm, None if s == 0 else fr[s - 1], fr[s], ref)
+        torch.cuda.synchronize()
+        g, r = fcutil.select_out_np(got), fcutil.select_out_np(ref)
+        for k, v in r.items():
+            np.testing.assert_array_equal(g[k], v, err_msg=f"step {s}: {k}")
+        if s == 0:
+            assert (g["counts"][:, 3] == 1).all()
+        if s in (1, 4):
+            for b in range(2):
+                res = osel.select_item(eps[b][s - 1], eps[b][s], op)
+                mg, esc = fcutil.check_select(g, res, op, b)
+                assert not esc

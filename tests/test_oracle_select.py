@@ -543,3 +543,66 @@ def _tiny():
     import fcdata
     prev, cur, _ = fcdata.tiny_pair(0)
     return prev[0], cur[0], None
+
+
+# ------------------------------------------------------------------ naive baseline (Sec. 6.1)
+def test_naive_selector_position_wise():
+    """The naive baseline compares each token with the previous frame's token at the same
+    position: identical frames reuse everything; a whole-token roll of random content
+    (which the full method aligns) leaves almost nothing above a strict threshold; a
+    missing previous frame reuses nothing."""
+    fr = RNG.uniform(size=(3, 112, 112))
+    r = osel.naive_select(fr, fr, 14, 1, 0.999)
+    assert r.reuse_mask.all() and r.n_recompute == 0
+    np.testing.assert_allclose(r.sim, 1.0, atol=1e-12)
+    cur = np.roll(fr, (14, 14), (1, 2))
+    r = osel.naive_select(fr, cur, 14, 1, 0.999)
+    assert r.reuse_mask.sum() == 0 and np.all(r.sim < 0.999)
+    full = osel.select_item(fr, cur, osel.SelectParams())
+    assert full.shift == (-1, -1) and full.k_final > 0
+    r = osel.naive_select(None, fr, 14, 1, 0.0)
+    # a zero previous spectrum: cosine 0, which still reaches tau = 0
+    assert r.reuse_mask.all() and np.all(r.sim == 0)
+    r = osel.naive_select(None, fr, 14, 1, 1e-9)
+    assert not r.reuse_mask.any()
+
+
+def test_naive_selector_amplitude_invariances_and_threshold():
+    """Amplitude spectra ignore a circular shift inside a patch (Fourier shift theorem):
+    such a change keeps similarity 1 and the token is reused, while a token whose
+    content is replaced falls below the threshold.  The threshold is inclusive (>=)
+    and the recompute list is ascending."""
+    prev = RNG.uniform(size=(3, 28, 56))                     # 2 x 4 tokens of 14 px
+    cur = prev.copy()
+    cur[:, 0:14, 14:28] = np.roll(prev[:, 0:14, 14:28], (3, 5), (1, 2))   # token 1: rolled
+    cur[:, 14:28, 28:42] = RNG.uniform(size=(3, 14, 14))                   # token 6: replaced
+    r = osel.naive_select(prev, cur, 14, 1, 0.999)
+    assert r.sim[1] == pytest.approx(1.0, abs=1e-12) and r.reuse_mask[1] == 1
+    assert r.sim[6] < 0.999 and r.reuse_mask[6] == 0
+    assert r.recompute_idx.tolist() == [6]
+    r2 = osel.naive_select(prev, cur, 14, 1, float(r.sim[6]))
+    assert r2.reuse_mask[6] == 1                              # sim == tau is reused
+    # brute force: the cosine of the flattened amplitude spectra, token 6
+    a = np.abs(np.fft.fft2(osel.luma(cur)[14:28, 28:42]))
+    b = np.abs(np.fft.fft2(osel.luma(prev)[14:28, 28:42]))
+    assert r.sim[6] == pytest.approx(np.sum(a * b) / np.linalg.norm(a) / np.linalg.norm(b), rel=1e-12)
+
+
+def test_naive_selector_equals_the_module_ablation_combination():
+    """With alignment, refresh, the adaptive budget and the gate all switched off
+    (shift 0, no fresh token, a 100 % budget, tau_mig = 0) Algorithm 1 reduces to the
+    naive baseline: the candidates are the tokens whose position-wise similarity
+    reaches tau_sim, and all of them are reused."""
+    fr = fcdata_frames()
+    for b in range(1, 3):
+        naive = osel.naive_select(fr[b - 1], fr[b], 14, 2, 0.99)
+        alg1 = osel.select_item(fr[b - 1], fr[b], osel.SelectParams(
+            merge=2, align=False, refresh=False, adaptive=False, alpha_fixed=1.0, tau_sim=0.99,
+            tau_mig=0.0))
+        np.testing.assert_array_equal(naive.reuse_mask, alg1.reuse_mask)
+        np.testing.assert_allclose(naive.sim, alg1.sim, rtol=1e-14)
+
+
+def fcdata_frames():
+    import fcdata
+    return fcdata.episode_frames(2024, size=448, n_frames=3)
