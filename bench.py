@@ -42,6 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+QWEN_MROPE = (16, 24, 24)      # Qwen2.5-VL multimodal RoPE: rotary pairs per (t, h, w)
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
@@ -146,7 +147,8 @@ def main():
                  g_mlp=torch.ones(shape.d, device=dev, dtype=torch.bfloat16))
         desc = fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w)
         kv = fc.KVCache(randn(1, S, shape.n_kv, shape.hd, std=1.0),
-                        randn(1, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0)
+                        randn(1, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0,
+                        grid_w=gw, mrope=QWEN_MROPE)
         ys = [randn(1, N, shape.d, std=1.0), randn(1, N, shape.d, std=1.0)]
         layers.append(dict(desc=desc, kv=kv, y=ys))
     torch.cuda.synchronize()
@@ -255,8 +257,8 @@ def main():
         scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
         config=dict(workload="episode step: 448x448 frame-pair selection (14-px patches, 2x2 "
                     "merge, 256 tokens, adaptive budget) + window advance + cache remap + "
-                    f"{L} Qwen2.5-VL-7B-shaped bf16 decoder layers over 2176 cached "
-                    "positions, batch 1", frame=size, tokens=N, layers=L, seq=S, batch=1,
+                    f"{L} Qwen2.5-VL-7B-shaped bf16 decoder layers (multimodal RoPE) over "
+                    "2176 cached positions, batch 1", frame=size, tokens=N, layers=L, seq=S, batch=1,
                     mean_recomputed_tokens=round(n_mean, 1)),
         roofline=roofline, roofline_step=roofline_step, sclk_mhz=sclk, kernels=kern,
         context="paper (Table 2): 637 -> 401 ms/step, 1.59x, InternVLA-N1 on R2R-CE, one "
@@ -625,7 +627,8 @@ def bench_batch_episodes(fc, torch, frames_np, steps, L):
                  g_mlp=torch.ones(shape.d, device=dev, dtype=torch.bfloat16))
         desc = fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w)
         kv = fc.KVCache(randn(B, S, shape.n_kv, shape.hd, std=1.0),
-                        randn(B, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0)
+                        randn(B, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=0,
+                        grid_w=gw, mrope=QWEN_MROPE)
         ys = [randn(B, N, shape.d, std=1.0), randn(B, N, shape.d, std=1.0)]
         layers.append(dict(desc=desc, kv=kv, y=ys))
     ctx = fc.Context(fc.Caps(max_batch=B, max_height=size, max_width=size, max_tokens=N,

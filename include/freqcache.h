@@ -144,6 +144,14 @@ typedef struct {
   int32_t frame_tokens;     /* N */
   int32_t window;           /* W >= 1 (frames kept, including the current one) */
   int32_t head;             /* 0 <= head < W */
+  /* Multimodal RoPE of Qwen2.5-VL (all zero: 1-D RoPE by prompt index).  The rotary
+     frequency pairs are split into sections of mrope_section[0..2] pairs (sum
+     head_dim / 2, each a multiple of 8) rotated by a token's temporal, row and column
+     position: text token p has (p, p, p); token (I, J) of the frame with logical index l
+     (0 = oldest) has (st, st + I, st + J), st = T + l max(N / grid_w, grid_w).  Causality
+     stays by prompt index. */
+  int32_t grid_w;           /* token-grid width of a frame (M-RoPE only)      */
+  int32_t mrope_section[3];
 } fc_kv_cache;
 
 /* Library version string. */

@@ -19,7 +19,10 @@ tokens].  The frame slots form a ring: physical slot p holds the frame whose
 logical index is (p - head) mod W (0 = oldest, W-1 = current).  A key or query
 sits at position T + logical * N + token for frames and at its index for text,
 so positions are those of the current step's prompt and the K cache holds raw
-(pre-RoPE) keys, rotated when used.
+(pre-RoPE) keys, rotated when used.  With the multimodal RoPE of Qwen2.5-VL (a
+reading: the paper deploys that model but does not describe its RoPE) the
+rotation angles come from each token's (t, h, w) position instead, while
+causality stays by prompt index.
 """
 from __future__ import annotations
 
@@ -43,6 +46,8 @@ class Layout:
     N: int      # tokens per frame
     W: int      # frames in the window (including the current one)
     head: int   # physical slot of the oldest frame
+    gw: int = 0                 # token-grid width of a frame (multimodal RoPE)
+    mrope: tuple = (0, 0, 0)    # rotary pairs per (t, h, w) section; zeros = 1-D RoPE
 
     @property
     def S(self) -> int:
@@ -71,6 +76,23 @@ class Layout:
     def cur_positions(self, tok: np.ndarray) -> np.ndarray:
         return self.T + (self.W - 1) * self.N + np.asarray(tok)
 
+    def rope_positions(self, seqpos: np.ndarray) -> np.ndarray:
+        """Multimodal RoPE positions [n, 3] = (t, h, w) of the tokens at prompt indices
+        `seqpos` (Qwen2.5-VL): a text token p has (p, p, p); token (I, J) of the frame
+        with logical index l has (st, st + I, st + J), st = T + l max(N / gw, gw) -- each
+        frame takes as many positions as its longer grid side, after the previous one."""
+        pos = np.asarray(seqpos, dtype=np.int64)
+        out = np.repeat(pos[:, None], 3, axis=1)
+        vis = pos >= self.T
+        r = pos[vis] - self.T
+        l, tok = r // self.N, r % self.N
+        span = max(self.N // self.gw, self.gw)
+        st = self.T + l * span
+        out[vis, 0] = st
+        out[vis, 1] = st + tok // self.gw
+        out[vis, 2] = st + tok % self.gw
+        return out
+
 
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
     """x / sqrt(mean(x^2) + eps) * g, per row."""
@@ -84,6 +106,25 @@ def rope_cos_sin(pos: np.ndarray, hd: int, theta: float):
     inv = theta ** (-(2.0 * np.arange(hd // 2)) / hd)
     ang = np.asarray(pos, dtype=np.float64)[:, None] * inv[None, :]
     return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
+
+
+def mrope_cos_sin(pos3: np.ndarray, sections, hd: int, theta: float):
+    """Multimodal RoPE angles: rotary pair i of the first sections[0] pairs turns by the
+    temporal position, of the next sections[1] by the row position and of the last
+    sections[2] by the column position, phi_i = pos_c(i) theta^(-2i/hd)
+    (float64 -> float32)."""
+    inv = theta ** (-(2.0 * np.arange(hd // 2)) / hd)
+    comp = np.repeat(np.arange(3), sections)                      # component of each pair
+    assert comp.size == hd // 2
+    ang = np.asarray(pos3, dtype=np.float64)[:, comp] * inv[None, :]
+    return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
+
+
+def layout_rope(lay, seqpos: np.ndarray, hd: int, theta: float):
+    """(cos, sin) of the tokens at prompt indices seqpos under the layout's RoPE."""
+    if sum(lay.mrope) == 0:
+        return rope_cos_sin(seqpos, hd, theta)
+    return mrope_cos_sin(lay.rope_positions(seqpos), lay.mrope, hd, theta)
 
 
 def rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
@@ -125,9 +166,11 @@ def _proj(x, w):
 
 
 def block_rows(x: np.ndarray, qpos: np.ndarray, kc: np.ndarray, vc: np.ndarray,
-               kpos: np.ndarray, rows: np.ndarray, wt: dict, shape):
+               kpos: np.ndarray, rows: np.ndarray, wt: dict, shape, lay=None):
     """One decoder block for the rows `x` [n, d] whose K/V go to physical cache rows
-    `rows`.  kc/vc [S, Hkv, hd] float32 (raw keys).  Returns (y [n, d], kc', vc').
+    `rows`.  kc/vc [S, Hkv, hd] float32 (raw keys).  qpos/kpos are prompt indices
+    (causality); the RoPE angles follow the layout `lay` (1-D by prompt index when
+    None).  Returns (y [n, d], kc', vc').
 
     QKV for every listed row is computed and written first; attention then runs
     over the whole cache, so the rows see each other's new keys and values."""
@@ -142,8 +185,12 @@ def block_rows(x: np.ndarray, qpos: np.ndarray, kc: np.ndarray, vc: np.ndarray,
     vc = vc.copy()
     kc[rows] = k_raw
     vc[rows] = v_new
-    cq, sq = rope_cos_sin(qpos, hd, shape.theta)
-    ck, sk = rope_cos_sin(kpos, hd, shape.theta)
+    if lay is None:
+        cq, sq = rope_cos_sin(qpos, hd, shape.theta)
+        ck, sk = rope_cos_sin(kpos, hd, shape.theta)
+    else:
+        cq, sq = layout_rope(lay, qpos, hd, shape.theta)
+        ck, sk = layout_rope(lay, kpos, hd, shape.theta)
     o = attention(rope(q, cq, sq), qpos, rope(kc, ck, sk), vc, kpos)
     h1 = x + _proj(o.reshape(n, nh * hd), wt["w_o"])
     h2 = rmsnorm(h1, f32(wt["g_mlp"]), shape.eps)
@@ -179,7 +226,7 @@ def layer_partial(x_cur_u16: np.ndarray, recompute_idx: np.ndarray, k_cache_u16:
         return y, kc, vc
     x = f32(x_cur_u16)[idx]
     yr, kc, vc = block_rows(x, lay.cur_positions(idx), kc, vc, lay.row_positions(),
-                            lay.cur_rows(idx), wt, shape)
+                            lay.cur_rows(idx), wt, shape, lay)
     y[idx] = yr
     return y, kc, vc
 
@@ -205,7 +252,7 @@ def layer_partial_sampled(x_cur_u16: np.ndarray, recompute_idx: np.ndarray,
     kc[rows] = kv[:, :nkv * hd].reshape(-1, nkv, hd)
     vc[rows] = kv[:, nkv * hd:].reshape(-1, nkv, hd)
     y, kc, vc = block_rows(x[smp], lay.cur_positions(smp), kc, vc, lay.row_positions(),
-                           lay.cur_rows(smp), wt, shape)
+                           lay.cur_rows(smp), wt, shape, lay)
     return y, kc, vc
 
 

@@ -322,6 +322,16 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
                 kv->text_tokens, kv->frame_tokens, kv->window, kv->head);
   const long S = (long)kv->text_tokens + (long)kv->window * kv->frame_tokens;
   const int qkv = (L->n_heads + 2 * L->n_kv_heads) * L->head_dim;
+  const int *ms = kv->mrope_section;
+  if (ms[0] || ms[1] || ms[2]) {
+    if (ms[0] < 0 || ms[1] < 0 || ms[2] < 0 || ms[0] % 8 || ms[1] % 8 || ms[2] % 8 ||
+        ms[0] + ms[1] + ms[2] != L->head_dim / 2)
+      return fail(FC_ERR_INVALID_ARG, "%s: M-RoPE sections %d/%d/%d must be multiples of 8 "
+                  "summing to head_dim/2 = %d", who, ms[0], ms[1], ms[2], L->head_dim / 2);
+    if (kv->grid_w < 1 || kv->frame_tokens % kv->grid_w)
+      return fail(FC_ERR_SHAPE, "%s: grid_w %d does not divide N=%d", who, kv->grid_w,
+                  kv->frame_tokens);
+  }
   const fc_caps &c = ctx->caps;
   if (B < 1) return fail(FC_ERR_SHAPE, "%s: B=%d", who, B);
   if (B > c.max_batch || kv->frame_tokens > c.max_tokens || S > c.max_seq || L->d_model > c.max_d_model ||

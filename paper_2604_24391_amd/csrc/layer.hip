@@ -59,6 +59,25 @@ __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
   return min(max(idx[slot], 0), N - 1);
 }
 
+// RoPE position of rotary frequency pair k for the token at sequence position seqpos
+// (its index in the current step's prompt, which also decides causality).  1-D RoPE:
+// seqpos itself.  Multimodal RoPE (Qwen2.5-VL): pairs [0, s1) rotate by the temporal,
+// [s1, s2) by the row and [s2, hd/2) by the column position; a text token has all three
+// equal to its index, the token (I, J) of the frame with logical index l has
+// (st, st + I, st + J) with st = T + l span, span = max(grid rows, grid columns), each
+// frame taking span positions after the one before it.
+struct MRope {
+  int on, T, N, gw, span, s1, s2;
+};
+__device__ __forceinline__ int rope_pos(const MRope &m, int seqpos, int k) {
+  if (!m.on || seqpos < m.T) return seqpos;
+  const int r = seqpos - m.T, l = r / m.N, tok = r - l * m.N;
+  const int st = m.T + l * m.span;
+  if (k < m.s1) return st;
+  const int I = tok / m.gw;
+  return k < m.s2 ? st + I : st + (tok - I * m.gw);
+}
+
 // ------------------------------------------------------------------------------- GEMM
 // Weight-streaming GEMM over the gathered rows, C[rows][cols] = A[rows][K] W[cols][K]^T
 // with W row-major [out][in] like torch.nn.Linear.  With a few hundred gathered rows
@@ -415,6 +434,7 @@ struct RedArgs {
   int N, d, splits, ncols, qw, kw, S, cur_row0;
   int hd, qpos0;                  // head dim; prompt position of current-frame token 0
   const float2 *rope;             // [S][hd/2] (cos, sin)
+  MRope mr;                       // RoPE positions (1-D or multimodal)
   long rows;
   float eps;
   const int32_t *idx, *nrec;
@@ -549,12 +569,12 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
     __syncthreads();
     if (c < r.qw) {
       const int half = r.hd / 2;
-      const float2 *rp = r.rope + (long)(r.qpos0 + tok) * half;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int d = (c + e) % r.hd;                 // dim within the head
         const int lc = threadIdx.x * 4 + e;           // column within the block
-        const float2 cs = rp[d % half];
+        const int k = d % half;                       // rotary frequency pair
+        const float2 cs = r.rope[(long)rope_pos(r.mr, r.qpos0 + tok, k) * half + k];
         vv[e] = d < half ? vv[e] * cs.x - qs[lc + half] * cs.y : vv[e] * cs.x + qs[lc - half] * cs.y;
       }
     }
@@ -797,7 +817,8 @@ __device__ __forceinline__ void mg_epi_rows8(const MArgs &a, const int *pre, Row
         const float4 pv = *reinterpret_cast<const float4 *>(tr + pc4);
         const float4 pb = unpack_bf16x4(*reinterpret_cast<const uint2 *>(r.bias + col0 + pc4));
         const float p[4] = {pv.x + pb.x, pv.y + pb.y, pv.z + pb.z, pv.w + pb.w};
-        const float2 *rp = r.rope + (long)(r.qpos0 + tok[it]) * half + dim % half;
+        // four consecutive pairs share one M-RoPE section (sections are multiples of 8)
+        const float2 *rp = r.rope + (long)rope_pos(r.mr, r.qpos0 + tok[it], dim % half) * half + dim % half;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const float2 cs = rp[q];
@@ -1083,6 +1104,7 @@ struct AttnArgs {
   const float2 *rope;         // [S][HD/2] (cos, sin)
   const int32_t *idx, *nrec;
   int N, nh, nkv, S, T, W, head;
+  MRope mr;                   // RoPE positions of the keys (1-D or multimodal)
   int splits, kb_per_split;
   int tiles;                  // B * ceil(N / 32) query tiles
   float scale_log2;
@@ -1318,7 +1340,7 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
         R[i].k1 = kv_load16s(kblk, ko);
         R[i].k2 = kv_load16s(kblk, ko + HD);
         if (ROT) {
-          const float2 *rp = a.rope + (long)pos * (HD / 2) + 8 * c[i];
+          const float2 *rp = a.rope + (long)rope_pos(a.mr, pos, 8 * c[i]) * (HD / 2) + 8 * c[i];
 #pragma unroll
           for (int q = 0; q < 4; ++q) R[i].cs[q] = kv_load16(rp + 2 * q);
         }
@@ -1589,7 +1611,8 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
 __global__ __launch_bounds__(256) void k_rot_keys(const uint16_t *__restrict__ kc,
                                                   const float2 *__restrict__ rope,
                                                   uint16_t *__restrict__ kr, int S, int nkv,
-                                                  int hd, int T, int N, int W, int head) {
+                                                  int hd, int T, int N, int W, int head,
+                                                  MRope mr) {
   const int cpr = hd / 16;                              // chunk pairs per head row
   const long task = (long)blockIdx.x * 256 + threadIdx.x;
   const int b = blockIdx.y;
@@ -1601,7 +1624,7 @@ __global__ __launch_bounds__(256) void k_rot_keys(const uint16_t *__restrict__ k
   const long off = ((long)b * S * nkv + rh) * hd + 8 * c;
   const U16x8 x1 = *reinterpret_cast<const U16x8 *>(kc + off);
   const U16x8 x2 = *reinterpret_cast<const U16x8 *>(kc + off + hd / 2);
-  const float2 *rp = rope + (long)pos * (hd / 2) + 8 * c;
+  const float2 *rp = rope + (long)rope_pos(mr, pos, 8 * c) * (hd / 2) + 8 * c;
   U16x8 y1, y2;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -1901,6 +1924,13 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   r.idx = idx; r.nrec = nrec; r.part = ctx->part; r.x = x_cur;
   r.qw = nh * hd; r.kw = nkv * hd;
   r.hd = hd; r.qpos0 = kv.text_tokens + (kv.window - 1) * N; r.rope = ctx->rope;
+  MRope mr{};
+  if (kv.mrope_section[0] + kv.mrope_section[1] + kv.mrope_section[2] > 0) {
+    const int gh = N / kv.grid_w;
+    mr = MRope{1, kv.text_tokens, N, kv.grid_w, std::max(gh, kv.grid_w), kv.mrope_section[0],
+               kv.mrope_section[0] + kv.mrope_section[1]};
+  }
+  r.mr = mr;
   fc_status rc;
 
   // 1. QKV of the recomputed rows.  Large-M path: gather + RMSNorm of the rows, then a
@@ -1941,6 +1971,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.q = ctx->qbuf;
     a.kc = kv.k; a.vc = kv.v;
     a.rope = ctx->rope;
+    a.mr = mr;
     a.idx = idx; a.nrec = nrec;
     a.N = N; a.nh = nh; a.nkv = nkv; a.S = S;
     a.T = kv.text_tokens; a.W = kv.window; a.head = kv.head;
@@ -1968,7 +1999,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
       const long tasks = (long)S * nkv * (hd / 16);
       hipLaunchKernelGGL(k_rot_keys, dim3((unsigned)((tasks + 255) / 256), B), dim3(256), 0, st,
                          kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, N, kv.window,
-                         kv.head);
+                         kv.head, mr);
       FC_HIP_TRY(hipGetLastError());
       a.kc = ctx->krot;
     }

@@ -67,7 +67,8 @@ class fc_layer_desc(ctypes.Structure):
 
 class fc_kv_cache(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("text_tokens", c_int32),
-                ("frame_tokens", c_int32), ("window", c_int32), ("head", c_int32)]
+                ("frame_tokens", c_int32), ("window", c_int32), ("head", c_int32),
+                ("grid_w", c_int32), ("mrope_section", c_int32 * 3)]
 
 
 _lib = None
@@ -382,6 +383,10 @@ class KVCache:
     frame_tokens: int
     window: int
     head: int = 0
+    # Multimodal RoPE (Qwen2.5-VL): frame token-grid width and rotary pairs per
+    # (t, h, w) section; (0, 0, 0) = 1-D RoPE by prompt index
+    grid_w: int = 0
+    mrope: tuple = (0, 0, 0)
 
     @property
     def S(self) -> int:
@@ -394,7 +399,8 @@ class KVCache:
     def c(self, B: int, kvw: int) -> fc_kv_cache:
         n = B * self.S * kvw
         return fc_kv_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
-                           self.text_tokens, self.frame_tokens, self.window, self.head)
+                           self.text_tokens, self.frame_tokens, self.window, self.head,
+                           self.grid_w, (c_int32 * 3)(*self.mrope))
 
 
 def fc_layer_forward(ctx: Context, layer: LayerDesc, kv: KVCache, x_cur: torch.Tensor,

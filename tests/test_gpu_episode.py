@@ -34,7 +34,8 @@ def fc():
     return fc
 
 
-def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, log=print):
+def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, log=print,
+              mrope=(0, 0, 0)):
     """Run `steps` episode steps on both sides and compare after every checked step.
     Returns the per-step recompute counts."""
     F, _, H, Wpx = frames.shape
@@ -57,7 +58,8 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         wt = fcdata.layer_weights(seed + 100 + li, shape)
         k0, v0 = fcdata.text_kv(seed + 200 + li, shape, S)
         y0 = fcdata.bf16_round(rng.standard_normal((2, N, shape.d), dtype=np.float32))
-        kv = fc.KVCache(fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(v0[None]), T, N, W, head=0)
+        kv = fc.KVCache(fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(v0[None]), T, N, W, head=0,
+                        grid_w=gw, mrope=tuple(mrope))
         gpu.append(dict(desc=fcutil.layer_desc(shape, fcutil.weights_gpu(wt)), kv=kv,
                         y=[fcutil.bf16_gpu(y0[0][None]), fcutil.bf16_gpu(y0[1][None])]))
         ora.append(dict(wt={k: ol.f32(v).copy() for k, v in wt.items()}, k=ol.f32(k0).copy(),
@@ -85,7 +87,7 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         # ---- oracle: its own chain
         res = osel.select_item(prev, frames[fi], op)
         head = (head + 1) % W
-        lay = ol.Layout(T=T, N=N, W=W, head=head)
+        lay = ol.Layout(T=T, N=N, W=W, head=head, gw=gw, mrope=tuple(mrope))
         xo = ol.f32(emb[fi])
         xs = []
         for o in ora:
@@ -154,9 +156,9 @@ def test_two_toy_layers_ring_of_two(fc):
 def test_qwen_episode_two_layers(fc):
     """The benchmark's episode workload (seed-2024 trajectory of 448x448 frames, 2x2
     merge, 256 tokens, 128 text tokens, 8-frame window: 2176 cached positions) on
-    two Qwen2.5-VL-7B-shaped layers, in the benchmark's launch configuration (the
-    same context capacities), over its 7 warm-up and first 9 measured steps, every
-    step compared."""
+    two Qwen2.5-VL-7B-shaped layers with its multimodal RoPE (t, h, w sections
+    16/24/24), in the benchmark's launch configuration (the same context capacities),
+    over its 7 warm-up and first 9 measured steps, every step compared."""
     shape = fcdata.QWEN_LAYER
     frames = fcdata.episode_frames(2024, size=448, n_frames=16)
     T, W, N = 128, 8, 256
@@ -165,7 +167,7 @@ def test_qwen_episode_two_layers(fc):
                              max_qkv=shape.qkv))
     try:
         counts = run_chain(fc, ctx, shape, frames, fc.SelectParams(merge=2), L=2, T=T, W=W,
-                           steps=16, seed=900)
+                           steps=16, seed=900, mrope=(16, 24, 24))
     finally:
         ctx.close()
     assert counts[0] == N and min(counts[1:]) < N

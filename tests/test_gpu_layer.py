@@ -35,9 +35,9 @@ class Case:
     """Seeded inputs for one layer call, the oracle's cache from a full forward of
     [prefix; x_prev], and the GPU tensors."""
 
-    def __init__(self, shape, T, N, W, head, B, seed, wt=None):
+    def __init__(self, shape, T, N, W, head, B, seed, wt=None, gw=0, mrope=(0, 0, 0)):
         self.shape, self.B = shape, B
-        self.lay = ol.Layout(T=T, N=N, W=W, head=head)
+        self.lay = ol.Layout(T=T, N=N, W=W, head=head, gw=gw, mrope=tuple(mrope))
         self.wt = wt if wt is not None else fcdata.layer_weights(seed, shape)
         pos = self.lay.row_positions()
         S = self.lay.S
@@ -63,7 +63,8 @@ class Case:
             nrec[b] = len(ids)
         kc, vc = fcutil.bf16_gpu(self.k), fcutil.bf16_gpu(self.v)
         y = fcutil.bf16_gpu(self.y_prev)
-        kv = fc.KVCache(kc, vc, self.lay.T, N, self.lay.W, self.lay.head)
+        kv = fc.KVCache(kc, vc, self.lay.T, N, self.lay.W, self.lay.head, grid_w=self.lay.gw,
+                        mrope=self.lay.mrope)
         fc.fc_layer_forward(ctx, fcutil.layer_desc(self.shape, self.wgpu), kv,
                             fcutil.bf16_gpu(self.x_cur), torch.from_numpy(idx).cuda(),
                             torch.from_numpy(nrec).cuda(), y)
@@ -259,6 +260,36 @@ def test_cache_update_layers_rejects_mixed_heads(fc, ctx):
                                   torch.zeros(B, N, dtype=torch.uint8, device="cuda"), 8)
 
 
+# ----------------------------------------------------------------- multimodal RoPE
+QWEN_MROPE = (16, 24, 24)      # Qwen2.5-VL's rotary pairs per (t, h, w), head_dim 128
+
+
+def test_mrope_qwen_layer(fc, ctx, qwen_case):
+    """The Qwen2.5-VL-7B-shaped layer with multimodal RoPE (t, h, w sections 16/24/24 of
+    the 64 rotary pairs, 16 x 16 token grid) at 25 % reuse, against the oracle."""
+    c = Case(fcdata.QWEN_LAYER, T=128, N=256, W=8, head=3, B=1, seed=40, wt=qwen_case.wt,
+             gw=16, mrope=QWEN_MROPE)
+    c.check(fc, ctx, [fcdata.random_reuse_ids(125, 256, 25)])
+
+
+@pytest.mark.parametrize("head", [0, 2])
+def test_mrope_gqa_ring_two_items(fc, ctx, head):
+    """Multimodal RoPE on a 3-frame ring (8 x 8 token grid: each frame spans 8 positions)
+    at two head positions, two items; and with head_dim 64 (sections 8/8/16) on the toy
+    block."""
+    c = Case(GQA_SMALL, T=16, N=64, W=3, head=head, B=2, seed=50 + head, gw=8, mrope=QWEN_MROPE)
+    c.check(fc, ctx, [fcdata.random_reuse_ids(7, 64, 25), fcdata.random_reuse_ids(8, 64, 60)])
+    c = Case(fcdata.TINY_LAYER, T=32, N=256, W=2, head=head % 2, B=1, seed=55, gw=16,
+             mrope=(8, 8, 16))
+    c.check(fc, ctx, [fcdata.random_reuse_ids(9, 256, 50)])
+
+
+def test_mrope_rejects_bad_sections(fc, ctx):
+    c = Case(fcdata.TINY_LAYER, T=32, N=256, W=1, head=0, B=1, seed=56, gw=16, mrope=(8, 8, 8))
+    with pytest.raises(fc.FcError, match="M-RoPE"):
+        c.run(fc, ctx, [np.arange(4)])
+
+
 # ----------------------------------------------------------------- many gathered rows
 # With B * N >= 2048 token slots the projections run as square MFMA tiles with fused
 # epilogues (the batched-episode regime); these cases take that path.
@@ -285,6 +316,15 @@ def test_batch_path_mha64_full_recompute(fc, ctx_big):
     """MHA with head_dim 64 (two heads per 128-column wave span), 0 % and 50 % reuse."""
     c = Case(fcdata.TINY_LAYER, T=32, N=1024, W=1, head=0, B=2, seed=70)
     c.check(fc, ctx_big, [fcdata.random_reuse_ids(71, 1024, 0), fcdata.random_reuse_ids(72, 1024, 50)])
+
+
+def test_batch_path_mrope(fc, ctx_big):
+    """The large-M path (keys rotated once per call, fused QKV epilogue) with
+    multimodal RoPE on a 32 x 32 token grid, two items."""
+    c = Case(GQA_SMALL, T=64, N=1024, W=2, head=1, B=2, seed=75, gw=32, mrope=QWEN_MROPE)
+    worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(76, 1024, 40),
+                                  fcdata.random_reuse_ids(77, 1024, 70)])
+    print(f"worst rel-L2 {worst:.2e}")
 
 
 @pytest.fixture(scope="module")

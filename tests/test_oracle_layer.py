@@ -261,3 +261,70 @@ def test_sampled_rows_equal_the_full_partial_call():
     np.testing.assert_allclose(ks, k, rtol=1e-5, atol=1e-6)
     np.testing.assert_allclose(vs, v, rtol=1e-5, atol=1e-6)
     np.testing.assert_allclose(ys, y[smp], rtol=1e-4, atol=1e-5)
+
+
+# ------------------------------------------------------------------ multimodal RoPE
+def test_mrope_positions_hand_layout():
+    """Multimodal RoPE positions of a small prompt (2 text tokens, two frames of a 2 x 2
+    token grid, ring head 1): text p -> (p, p, p); frame l, token (I, J) ->
+    (st, st + I, st + J) with st = T + l max(grid rows, grid cols) = 2 + 2 l."""
+    lay = ol.Layout(T=2, N=4, W=2, head=1, gw=2, mrope=(16, 24, 24))
+    want = [[0, 0, 0], [1, 1, 1], [2, 2, 2], [2, 2, 3], [2, 3, 2], [2, 3, 3],
+            [4, 4, 4], [4, 4, 5], [4, 5, 4], [4, 5, 5]]
+    np.testing.assert_array_equal(lay.rope_positions(np.arange(lay.S)), want)
+    # a 3-wide, 2-high grid: each frame takes max(2, 3) = 3 positions
+    lay = ol.Layout(T=1, N=6, W=2, head=0, gw=3, mrope=(16, 24, 24))
+    np.testing.assert_array_equal(lay.rope_positions(np.array([1, 6, 7, 12])),
+                                  [[1, 1, 1], [1, 2, 3], [4, 4, 4], [4, 5, 6]])
+
+
+def test_mrope_matches_transformers_qwen2_vl():
+    """The rotation equals transformers' apply_multimodal_rotary_pos_emb of Qwen2-VL (an
+    independent implementation: per-component cos/sin over the full head dim, spliced
+    by section) for random queries at random (t, h, w) positions."""
+    import torch
+    from transformers.models.qwen2_vl.modeling_qwen2_vl import apply_multimodal_rotary_pos_emb
+    rng = np.random.default_rng(5)
+    hd, theta, sec = 128, 1e6, (16, 24, 24)
+    n = 40
+    pos3 = rng.integers(0, 3000, size=(n, 3))
+    x = rng.standard_normal((n, 2, hd)).astype(np.float32)
+    c, s = ol.mrope_cos_sin(pos3, sec, hd, theta)
+    got = ol.rope(x, c, s)
+    inv = theta ** (-(torch.arange(0, hd, 2, dtype=torch.float64) / hd))
+    ang = torch.from_numpy(pos3.T.astype(np.float64))[:, None, :, None] * inv       # [3,1,n,64]
+    emb = torch.cat([ang, ang], dim=-1)
+    xt = torch.from_numpy(x.astype(np.float64)).permute(1, 0, 2)[None]             # [1,2,n,hd]
+    q, _ = apply_multimodal_rotary_pos_emb(xt, xt, emb.cos(), emb.sin(), list(sec))
+    want = q[0].permute(1, 0, 2).numpy()
+    np.testing.assert_allclose(got, want, rtol=2e-5, atol=2e-5)
+
+
+def test_mrope_reduces_to_rope_and_keeps_relative_positions():
+    """Equal components (a text token) rotate exactly as 1-D RoPE; each section turns
+    only with its own component; and a common shift of all three components leaves
+    every query-key product unchanged (relative positions per component)."""
+    rng = np.random.default_rng(6)
+    hd, theta, sec = 128, 1e6, (16, 24, 24)
+    p = rng.integers(0, 2000, size=9)
+    c1, s1 = ol.rope_cos_sin(p, hd, theta)
+    c3, s3 = ol.mrope_cos_sin(np.stack([p, p, p], 1), sec, hd, theta)
+    np.testing.assert_array_equal(c1, c3)
+    np.testing.assert_array_equal(s1, s3)
+    base = np.array([[100, 200, 300]])
+    for comp, (lo, hi) in enumerate([(0, 16), (16, 40), (40, 64)]):
+        moved = base.copy()
+        moved[0, comp] += 37
+        ca, _ = ol.mrope_cos_sin(base, sec, hd, theta)
+        cb, _ = ol.mrope_cos_sin(moved, sec, hd, theta)
+        changed = np.flatnonzero(ca[0] != cb[0])
+        assert changed.min() >= lo and changed.max() < hi
+    q = rng.standard_normal((1, 1, hd)).astype(np.float32)
+    k = rng.standard_normal((1, 1, hd)).astype(np.float32)
+    pq, pk = np.array([[50, 60, 70]]), np.array([[10, 90, 30]])
+    dots = []
+    for d in (0, 123):
+        cq, sq = ol.mrope_cos_sin(pq + d, sec, hd, theta)
+        ck, sk = ol.mrope_cos_sin(pk + d, sec, hd, theta)
+        dots.append(float((ol.rope(q, cq, sq) * ol.rope(k, ck, sk)).sum()))
+    assert dots[0] == pytest.approx(dots[1], rel=1e-4)
