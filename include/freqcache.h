@@ -132,7 +132,7 @@ typedef struct {
 } fc_layer_desc;
 
 /* One layer's token cache.  Sequence layout: [T text tokens][W frame slots of N
- * tokens].  The frame slots are a ring: physical slot p holds the frame with
+ * tokens][U text tokens].  The frame slots are a ring: physical slot p holds the frame with
  * logical index (p - head) mod W (0 = oldest, W - 1 = current).  A key sits at
  * position T + logical * N + token (text: its index), i.e. at its place in the
  * current step's prompt.  K holds raw (pre-RoPE) keys; rotation happens on use,
@@ -152,6 +152,11 @@ typedef struct {
      stays by prompt index. */
   int32_t grid_w;           /* token-grid width of a frame (M-RoPE only)      */
   int32_t mrope_section[3];
+  /* Text after the frames: U tokens at rows (and prompt indices) T + W N + u, e.g. the
+     instruction that follows the current image.  They come after the current frame,
+     so fc_layer_forward_trail recomputes all of them at every step; frame tokens never
+     attend to them.  With M-RoPE their three positions are T + W span + u.  0: none. */
+  int32_t trail_tokens;
 } fc_kv_cache;
 
 /* Library version string. */
@@ -212,6 +217,15 @@ fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *
 fc_status fc_select_noalloc(const fc_select_params *prm, const float *frames_prev,
                             const float *frames_cur, int32_t B, int32_t H, int32_t W,
                             const fc_select_out *out, void *stream);
+
+/* The text rows after the frames (kv->trail_tokens = U > 0) through the same decoder
+ * block, all U of them, after fc_layer_forward of this layer at this step (their
+ * queries attend to the whole cache, the current frame's new rows included):
+ *   x_trail: [B][U][d_model] bf16 layer input of the trailing text;
+ *   y_trail: [B][U][d_model] bf16 output; the K/V rows T + W N + u are written. */
+fc_status fc_layer_forward_trail(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                                 const uint16_t *x_trail, uint16_t *y_trail, int32_t B,
+                                 void *stream);
 
 /* Token-cache preparation for one layer at a new step.  The caller has already
  * advanced kv->head, so the current frame lives in slot (head + W - 1) mod W and

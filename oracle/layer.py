@@ -48,10 +48,15 @@ class Layout:
     head: int   # physical slot of the oldest frame
     gw: int = 0                 # token-grid width of a frame (multimodal RoPE)
     mrope: tuple = (0, 0, 0)    # rotary pairs per (t, h, w) section; zeros = 1-D RoPE
+    U: int = 0                  # text tokens after the frames
 
     @property
     def S(self) -> int:
-        return self.T + self.W * self.N
+        return self.T + self.W * self.N + self.U
+
+    def trail_rows(self) -> np.ndarray:
+        """Rows (= prompt indices) of the text after the frames."""
+        return self.T + self.W * self.N + np.arange(self.U)
 
     def cur_slot(self) -> int:
         return (self.head + self.W - 1) % self.W
@@ -64,6 +69,7 @@ class Layout:
         """Position of every physical cache row."""
         pos = np.empty(self.S, np.int64)
         pos[:self.T] = np.arange(self.T)
+        pos[self.T + self.W * self.N:] = self.trail_rows()
         for p in range(self.W):
             logical = (p - self.head) % self.W
             pos[self.T + p * self.N:self.T + (p + 1) * self.N] = \
@@ -80,13 +86,17 @@ class Layout:
         """Multimodal RoPE positions [n, 3] = (t, h, w) of the tokens at prompt indices
         `seqpos` (Qwen2.5-VL): a text token p has (p, p, p); token (I, J) of the frame
         with logical index l has (st, st + I, st + J), st = T + l max(N / gw, gw) -- each
-        frame takes as many positions as its longer grid side, after the previous one."""
+        frame takes as many positions as its longer grid side, after the previous one;
+        text after the frames continues at T + W max(N / gw, gw)."""
         pos = np.asarray(seqpos, dtype=np.int64)
         out = np.repeat(pos[:, None], 3, axis=1)
-        vis = pos >= self.T
+        span = max(self.N // self.gw, self.gw)
+        end = self.T + self.W * self.N
+        after = pos >= end                 # text after the frames continues after the spans
+        out[after] = (pos[after] - end + self.T + self.W * span)[:, None]
+        vis = (pos >= self.T) & ~after
         r = pos[vis] - self.T
         l, tok = r // self.N, r % self.N
-        span = max(self.N // self.gw, self.gw)
         st = self.T + l * span
         out[vis, 0] = st
         out[vis, 1] = st + tok // self.gw
@@ -254,6 +264,16 @@ def layer_partial_sampled(x_cur_u16: np.ndarray, recompute_idx: np.ndarray,
     y, kc, vc = block_rows(x[smp], lay.cur_positions(smp), kc, vc, lay.row_positions(),
                            lay.cur_rows(smp), wt, shape, lay)
     return y, kc, vc
+
+
+def layer_trail(x_trail_u16: np.ndarray, k_cache_u16: np.ndarray, v_cache_u16: np.ndarray,
+                lay: Layout, wt: dict, shape):
+    """The text after the frames through the block for one batch item: all U rows are
+    recomputed (they follow the current frame), their K/V go to rows T + W N + u, and
+    they attend causally to the whole cache.  Returns float32 (y [U, d], k', v')."""
+    kc, vc = f32(k_cache_u16), f32(v_cache_u16)
+    rows = lay.trail_rows()
+    return block_rows(f32(x_trail_u16), rows, kc, vc, lay.row_positions(), rows, wt, shape, lay)
 
 
 def cache_update(k_cache: np.ndarray, v_cache: np.ndarray, y_prev: np.ndarray,

@@ -320,7 +320,9 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
       kv->head >= kv->window)
     return fail(FC_ERR_INVALID_ARG, "%s: bad cache layout T=%d N=%d W=%d head=%d", who,
                 kv->text_tokens, kv->frame_tokens, kv->window, kv->head);
-  const long S = (long)kv->text_tokens + (long)kv->window * kv->frame_tokens;
+  if (kv->trail_tokens < 0)
+    return fail(FC_ERR_INVALID_ARG, "%s: trail_tokens %d", who, kv->trail_tokens);
+  const long S = (long)kv->text_tokens + (long)kv->window * kv->frame_tokens + kv->trail_tokens;
   const int qkv = (L->n_heads + 2 * L->n_kv_heads) * L->head_dim;
   const int *ms = kv->mrope_section;
   if (ms[0] || ms[1] || ms[2]) {
@@ -334,7 +336,8 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
   }
   const fc_caps &c = ctx->caps;
   if (B < 1) return fail(FC_ERR_SHAPE, "%s: B=%d", who, B);
-  if (B > c.max_batch || kv->frame_tokens > c.max_tokens || S > c.max_seq || L->d_model > c.max_d_model ||
+  if (B > c.max_batch || kv->frame_tokens > c.max_tokens || kv->trail_tokens > c.max_tokens ||
+      S > c.max_seq || L->d_model > c.max_d_model ||
       L->d_ffn > c.max_ffn || qkv > c.max_qkv)
     return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%d exceed the context caps",
                 who, B, kv->frame_tokens, S, L->d_model, L->d_ffn, qkv);
@@ -366,12 +369,37 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
         (L.head_dim == 64 && (L.n_heads / L.n_kv_heads == 1 || L.n_heads / L.n_kv_heads == 2))))
     return fail(FC_ERR_UNSUPPORTED, "fc_layer_forward: head_dim %d with %d query heads per kv head",
                 L.head_dim, L.n_heads / L.n_kv_heads);
-  if ((long)kv->text_tokens + (long)kv->window * kv->frame_tokens > (long)ctx->caps.max_seq)
+  if ((long)kv->text_tokens + (long)kv->window * kv->frame_tokens + kv->trail_tokens >
+      (long)ctx->caps.max_seq)
     return fail(FC_ERR_CAPACITY, "fc_layer_forward: sequence exceeds max_seq");
   st = use_device(ctx);
   if (st != FC_OK) return st;
   return fc::launch_layer(ctx, L, *kv, x_cur, recompute_idx, n_recompute, y_cur, B,
                           reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_layer_forward_trail(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                                 const uint16_t *x_trail, uint16_t *y_trail, int32_t B,
+                                 void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_layer_forward_trail: null context");
+  fc_status st = check_layer(ctx, layer, kv, B, "fc_layer_forward_trail");
+  if (st != FC_OK) return st;
+  const fc_layer_desc &L = *layer;
+  if (kv->trail_tokens < 1)
+    return fail(FC_ERR_INVALID_ARG, "fc_layer_forward_trail: the cache has no trailing text");
+  if (!x_trail || !y_trail)
+    return fail(FC_ERR_INVALID_ARG, "fc_layer_forward_trail: null activation buffer");
+  if (!L.w_qkv || !L.b_qkv || !L.w_o || !L.w_gate || !L.w_up || !L.w_down || !L.g_attn || !L.g_mlp)
+    return fail(FC_ERR_INVALID_ARG, "fc_layer_forward_trail: null weight pointer");
+  if (!((L.head_dim == 128 && (L.n_heads / L.n_kv_heads == 7 || L.n_heads / L.n_kv_heads == 1 ||
+                               L.n_heads / L.n_kv_heads == 4)) ||
+        (L.head_dim == 64 && (L.n_heads / L.n_kv_heads == 1 || L.n_heads / L.n_kv_heads == 2))))
+    return fail(FC_ERR_UNSUPPORTED, "fc_layer_forward_trail: head_dim %d with %d query heads per kv head",
+                L.head_dim, L.n_heads / L.n_kv_heads);
+  st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_layer(ctx, L, *kv, x_trail, nullptr, nullptr, y_trail, B,
+                          reinterpret_cast<hipStream_t>(stream), true);
 }
 
 fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,

@@ -126,9 +126,10 @@ fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
                                 const fc_select_out &out, hipStream_t st);
 size_t noalloc_scratch_bytes();
 
+// trail: recompute the text rows after the frames instead of the selected frame tokens
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                        const uint16_t *x_cur, const int32_t *idx, const int32_t *nrec,
-                       uint16_t *y_cur, int B, hipStream_t st);
+                       uint16_t *y_cur, int B, hipStream_t st, bool trail = false);
 
 fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,

@@ -52,11 +52,12 @@ struct alignas(16) U16x8 {
 
 // Device-side counts and ids come from fc_select; clamp them so that a caller
 // passing anything else can never make a kernel leave its buffers.
+// Null counts and ids (the trailing-text rows) mean every token of the region, in order.
 __device__ __forceinline__ int n_valid(const int32_t *nrec, int b, int N) {
-  return min(max(nrec[b], 0), N);
+  return nrec ? min(max(nrec[b], 0), N) : N;
 }
 __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
-  return min(max(idx[slot], 0), N - 1);
+  return idx ? min(max(idx[slot], 0), N - 1) : (int)(slot % N);
 }
 
 // RoPE position of rotary frequency pair k for the token at sequence position seqpos
@@ -66,11 +67,14 @@ __device__ __forceinline__ int tok_of(const int32_t *idx, long slot, int N) {
 // equal to its index, the token (I, J) of the frame with logical index l has
 // (st, st + I, st + J) with st = T + l span, span = max(grid rows, grid columns), each
 // frame taking span positions after the one before it.
+// Text after the frames continues from the last frame's span: its three positions are
+// T + W span + (its index past the frames).
 struct MRope {
-  int on, T, N, gw, span, s1, s2;
+  int on, T, N, W, gw, span, s1, s2;
 };
 __device__ __forceinline__ int rope_pos(const MRope &m, int seqpos, int k) {
   if (!m.on || seqpos < m.T) return seqpos;
+  if (seqpos >= m.T + m.W * m.N) return seqpos - m.W * m.N + m.W * m.span;
   const int r = seqpos - m.T, l = r / m.N, tok = r - l * m.N;
   const int st = m.T + l * m.span;
   if (k < m.s1) return st;
@@ -1104,6 +1108,9 @@ struct AttnArgs {
   const float2 *rope;         // [S][HD/2] (cos, sin)
   const int32_t *idx, *nrec;
   int N, nh, nkv, S, T, W, head;
+  int fN;                     // tokens per frame (N: query tokens of the region)
+  int cur_lo, qpos0;          // first cache row and prompt index of the query region
+  int frames_end;             // T + W fN: text after the frames starts here
   MRope mr;                   // RoPE positions of the keys (1-D or multimodal)
   int splits, kb_per_split;
   int tiles;                  // B * ceil(N / 32) query tiles
@@ -1114,7 +1121,7 @@ struct AttnArgs {
 };
 
 __device__ __forceinline__ int key_pos(int row, int T, int N, int W, int head) {
-  if (row < T) return row;
+  if (row < T || row >= T + W * N) return row;     // text before and after the frames
   const int r = row - T;
   const int p = r / N, i = r - p * N;
   int lg = p - head;
@@ -1247,11 +1254,12 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
   const long kvbase = (long)b * a.S * a.nkv * HD + (long)g * HD;
   const long kvrow = (long)a.nkv * HD;
   // only the current frame's keys can lie after a query; other blocks skip the mask
-  const int cur_lo = a.T + ((a.head + a.W - 1) % a.W) * a.N, cur_hi = cur_lo + a.N;
+  // (the query region: the current frame's slot, or the text after the frames)
+  const int cur_lo = a.cur_lo, cur_hi = cur_lo + a.N;
 
   auto needs_mask = [&](int kb) {
     const int r0 = kb * 32, r1 = r0 + 32;
-    return r1 > a.S || (r1 > cur_lo && r0 < cur_hi);
+    return r1 > a.S || (r1 > cur_lo && r0 < cur_hi) || r1 > a.frames_end;
   };
   // Key blocks of the current frame's slot past the tile's last query: every key in
   // them comes after every query of the tile, so they add exactly nothing to the
@@ -1314,13 +1322,13 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
       // positions: rows of one region (text, or one frame slot of the ring) share the
       // shift from row to position
       int delta = 0;
-      bool uniform_pos = rb + 32 <= a.T;
+      bool uniform_pos = rb + 32 <= a.T || rb >= a.frames_end;
       if (!uniform_pos && rb >= a.T) {
-        const int p0 = (rb - a.T) / a.N, p1 = (min(rb + 31, S - 1) - a.T) / a.N;
+        const int p0 = (rb - a.T) / a.fN, p1 = (min(rb + 31, S - 1) - a.T) / a.fN;
         if (p0 == p1) {
           int lg = p0 - a.head;
           if (lg < 0) lg += a.W;
-          delta = (lg - p0) * a.N;
+          delta = (lg - p0) * a.fN;
           uniform_pos = true;
         }
       }
@@ -1334,7 +1342,7 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
       for (int i = 0; i < TPT; ++i) {
         const int row0 = rb + key[i];
         const int row = min(row0, S - 1);
-        const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.N, a.W, a.head);
+        const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.fN, a.W, a.head);
         R[i].pos = row0 < S ? pos : 0x7fffffff;
         const uint32_t ko = key[i] <= lim ? koff[i] : lim_off + 16 * c[i];
         R[i].k1 = kv_load16s(kblk, ko);
@@ -1438,7 +1446,7 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     const int j = j0 + 32 * qb + l32;
     qvalid[qb] = j < n;
     slot[qb] = (long)b * a.N + (qvalid[qb] ? j : j0);
-    qpos[qb] = a.T + (a.W - 1) * a.N + tok_of(a.idx, slot[qb], a.N);
+    qpos[qb] = a.qpos0 + tok_of(a.idx, slot[qb], a.N);
   }
   f32x16 o[QB][NHB];
   float m_run[QB], l_run[QB];
@@ -1892,19 +1900,27 @@ void run_red(int which, dim3 grid, hipStream_t st, const RedArgs &r) {
 
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                        const uint16_t *x_cur, const int32_t *idx, const int32_t *nrec,
-                       uint16_t *y_cur, int B, hipStream_t st) {
-  const int N = kv.frame_tokens, d = L.d_model, nh = L.n_heads, nkv = L.n_kv_heads,
+                       uint16_t *y_cur, int B, hipStream_t st, bool trail) {
+  // The rows a call recomputes form its region: the current frame's recomputed tokens
+  // (ids and counts from the selection), or every text token after the frames (trail:
+  // null ids and counts, the region's tokens in order).  N below is the region's token
+  // count; FN the frame's.
+  const int FN = kv.frame_tokens, d = L.d_model, nh = L.n_heads, nkv = L.n_kv_heads,
             hd = L.head_dim, ffn = L.d_ffn;
-  const int S = kv.text_tokens + kv.window * N;
+  const int frames_end = kv.text_tokens + kv.window * FN;
+  const int S = frames_end + kv.trail_tokens;
+  const int N = trail ? kv.trail_tokens : FN;
   const int qkv = (nh + 2 * nkv) * hd;
   const long rows = (long)B * N;
   const int cur_slot = (kv.head + kv.window - 1) % kv.window;
-  const int cur_row0 = kv.text_tokens + cur_slot * N;
+  const int cur_row0 = trail ? frames_end : kv.text_tokens + cur_slot * FN;
+  const int qpos0 = trail ? frames_end : kv.text_tokens + (kv.window - 1) * FN;
+  if (trail) idx = nrec = nullptr;
   const int want = std::max(ctx->num_cus, 1);
   // thousands of gathered rows (several batch items of large frames) make the
   // projections compute bound: square MFMA tiles with fused epilogues instead of the
   // weight-streaming kernels and their split-K reductions
-  const bool big = rows >= kBigRows && (hd == 64 || hd == 128) && B <= kMMaxItems;
+  const bool big = !trail && rows >= kBigRows && (hd == 64 || hd == 128) && B <= kMMaxItems;
 
   // RoPE table for (hd, theta) over the cache length (rebuilt only when they change)
   if (ctx->rope_hd != hd || ctx->rope_theta != L.rope_theta || ctx->rope_seq < S) {
@@ -1923,12 +1939,12 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   r.N = N; r.d = d; r.S = S; r.cur_row0 = cur_row0; r.rows = rows; r.eps = L.rms_eps;
   r.idx = idx; r.nrec = nrec; r.part = ctx->part; r.x = x_cur;
   r.qw = nh * hd; r.kw = nkv * hd;
-  r.hd = hd; r.qpos0 = kv.text_tokens + (kv.window - 1) * N; r.rope = ctx->rope;
+  r.hd = hd; r.qpos0 = qpos0; r.rope = ctx->rope;
   MRope mr{};
   if (kv.mrope_section[0] + kv.mrope_section[1] + kv.mrope_section[2] > 0) {
-    const int gh = N / kv.grid_w;
-    mr = MRope{1, kv.text_tokens, N, kv.grid_w, std::max(gh, kv.grid_w), kv.mrope_section[0],
-               kv.mrope_section[0] + kv.mrope_section[1]};
+    const int gh = FN / kv.grid_w;
+    mr = MRope{1, kv.text_tokens, FN, kv.window, kv.grid_w, std::max(gh, kv.grid_w),
+               kv.mrope_section[0], kv.mrope_section[0] + kv.mrope_section[1]};
   }
   r.mr = mr;
   fc_status rc;
@@ -1975,6 +1991,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.idx = idx; a.nrec = nrec;
     a.N = N; a.nh = nh; a.nkv = nkv; a.S = S;
     a.T = kv.text_tokens; a.W = kv.window; a.head = kv.head;
+    a.fN = FN; a.cur_lo = cur_row0; a.qpos0 = qpos0; a.frames_end = frames_end;
     a.scale_log2 = (float)(1.0 / std::sqrt((double)hd) * 1.4426950408889634);
     a.out = ctx->attn;
     const int tiles = B * ((N + 31) / 32);
@@ -1998,7 +2015,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
       ProfScope ps(ctx, st, "fc_rot_keys");
       const long tasks = (long)S * nkv * (hd / 16);
       hipLaunchKernelGGL(k_rot_keys, dim3((unsigned)((tasks + 255) / 256), B), dim3(256), 0, st,
-                         kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, N, kv.window,
+                         kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, FN, kv.window,
                          kv.head, mr);
       FC_HIP_TRY(hipGetLastError());
       a.kc = ctx->krot;
@@ -2091,7 +2108,7 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                               const uint8_t *reuse, int grid_w, int B, hipStream_t st) {
   const int N = kv.frame_tokens;
-  const int S = kv.text_tokens + kv.window * N;
+  const int S = kv.text_tokens + kv.window * N + kv.trail_tokens;
   const int kvw = L.n_kv_heads * L.head_dim;
   const int cur_slot = (kv.head + kv.window - 1) % kv.window;
   const int prev_slot = kv.window > 1 ? (kv.head + kv.window - 2) % kv.window : cur_slot;
@@ -2157,7 +2174,7 @@ fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_
     return FC_OK;
   }
   const int N = kv.frame_tokens;
-  const int S = kv.text_tokens + kv.window * N;
+  const int S = kv.text_tokens + kv.window * N + kv.trail_tokens;
   const int kvw = L.n_kv_heads * L.head_dim;
   const int cur_slot = (kv.head + kv.window - 1) % kv.window;
   const int prev_slot = (kv.head + kv.window - 2) % kv.window;

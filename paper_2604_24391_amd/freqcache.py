@@ -29,6 +29,7 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
+           "fc_layer_forward_trail",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
            "fc_profile_only", "fc_profile_read")
 
@@ -68,7 +69,7 @@ class fc_layer_desc(ctypes.Structure):
 class fc_kv_cache(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("text_tokens", c_int32),
                 ("frame_tokens", c_int32), ("window", c_int32), ("head", c_int32),
-                ("grid_w", c_int32), ("mrope_section", c_int32 * 3)]
+                ("grid_w", c_int32), ("mrope_section", c_int32 * 3), ("trail_tokens", c_int32)]
 
 
 _lib = None
@@ -107,11 +108,15 @@ def lib() -> ctypes.CDLL:
         L.fc_layer_forward.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                        ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_int32, c_void_p]
+        L.fc_layer_forward_trail.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
+                                             ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p,
+                                             c_int32, c_void_p]
         L.fc_profile_enable.argtypes = [c_void_p, c_int32]
         L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
+                  "fc_layer_forward_trail",
                   "fc_cache_update",
                   "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
@@ -387,10 +392,11 @@ class KVCache:
     # (t, h, w) section; (0, 0, 0) = 1-D RoPE by prompt index
     grid_w: int = 0
     mrope: tuple = (0, 0, 0)
+    trail_tokens: int = 0      # text tokens after the frames (recomputed every step)
 
     @property
     def S(self) -> int:
-        return self.text_tokens + self.window * self.frame_tokens
+        return self.text_tokens + self.window * self.frame_tokens + self.trail_tokens
 
     def advance(self):
         """Move to the next step: the oldest frame's slot becomes the current one."""
@@ -400,7 +406,7 @@ class KVCache:
         n = B * self.S * kvw
         return fc_kv_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
                            self.text_tokens, self.frame_tokens, self.window, self.head,
-                           self.grid_w, (c_int32 * 3)(*self.mrope))
+                           self.grid_w, (c_int32 * 3)(*self.mrope), self.trail_tokens)
 
 
 def fc_layer_forward(ctx: Context, layer: LayerDesc, kv: KVCache, x_cur: torch.Tensor,
@@ -417,6 +423,20 @@ def fc_layer_forward(ctx: Context, layer: LayerDesc, kv: KVCache, x_cur: torch.T
         _ptr(recompute_idx, torch.int32, B * N, "recompute_idx"),
         _ptr(n_recompute, torch.int32, B, "n_recompute"),
         _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur"), B, _stream(stream)))
+
+
+def fc_layer_forward_trail(ctx: Context, layer: LayerDesc, kv: KVCache, x_trail: torch.Tensor,
+                           y_trail: torch.Tensor, stream=None):
+    """The text rows after the frames (x_trail, y_trail: [B, U, d] bf16), all recomputed;
+    call after fc_layer_forward of the same layer."""
+    B = x_trail.shape[0]
+    U, d = kv.trail_tokens, layer.d_model
+    cl = layer.c()
+    ck = kv.c(B, layer.n_kv_heads * layer.head_dim)
+    _check(lib().fc_layer_forward_trail(ctx.handle, ctypes.byref(cl), ctypes.byref(ck),
+                                        _ptr(x_trail, torch.bfloat16, B * U * d, "x_trail"),
+                                        _ptr(y_trail, torch.bfloat16, B * U * d, "y_trail"), B,
+                                        _stream(stream)))
 
 
 def fc_cache_update(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev: torch.Tensor,

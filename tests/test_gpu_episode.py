@@ -35,15 +35,19 @@ def fc():
 
 
 def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, log=print,
-              mrope=(0, 0, 0)):
+              mrope=(0, 0, 0), U=0):
     """Run `steps` episode steps on both sides and compare after every checked step.
     Returns the per-step recompute counts."""
     F, _, H, Wpx = frames.shape
     m = prm.merge
     gh, gw = H // (14 * m), Wpx // (14 * m)
     N = gh * gw
-    S = T + W * N
+    S = T + W * N + U
     op = fcutil.oracle_select_params(prm)
+    # text after the frames: seeded embeddings (the layer-0 input at every step)
+    x_text = fcdata.bf16_round(np.random.default_rng(seed + 2).standard_normal((U, shape.d),
+                                                                               dtype=np.float32))
+    x_text_gpu = fcutil.bf16_gpu(x_text[None]) if U else None
     emb = fcdata.token_embeddings(frames, shape.d, 14 * m, seed + 1)        # [F, N, d] bf16
     emb_gpu = fcutil.bf16_gpu(emb)
     frames_gpu = torch.from_numpy(np.ascontiguousarray(frames)).cuda()
@@ -59,9 +63,11 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         k0, v0 = fcdata.text_kv(seed + 200 + li, shape, S)
         y0 = fcdata.bf16_round(rng.standard_normal((2, N, shape.d), dtype=np.float32))
         kv = fc.KVCache(fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(v0[None]), T, N, W, head=0,
-                        grid_w=gw, mrope=tuple(mrope))
+                        grid_w=gw, mrope=tuple(mrope), trail_tokens=U)
         gpu.append(dict(desc=fcutil.layer_desc(shape, fcutil.weights_gpu(wt)), kv=kv,
-                        y=[fcutil.bf16_gpu(y0[0][None]), fcutil.bf16_gpu(y0[1][None])]))
+                        y=[fcutil.bf16_gpu(y0[0][None]), fcutil.bf16_gpu(y0[1][None])],
+                        yt=torch.empty((1, U, shape.d), dtype=torch.bfloat16, device="cuda")
+                        if U else None))
         ora.append(dict(wt={k: ol.f32(v).copy() for k, v in wt.items()}, k=ol.f32(k0).copy(),
                         v=ol.f32(v0).copy(), y=[ol.f32(y0[0]).copy(), ol.f32(y0[1]).copy()],
                         k0=k0, v0=v0, written=np.zeros(S, bool)))
@@ -80,15 +86,20 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
                                   [g["y"][cur] for g in gpu], [g["y"][nxt] for g in gpu],
                                   sel.shift, sel.reuse_mask, gw)
         x = emb_gpu[fi:fi + 1]
+        xt = x_text_gpu
         for g in gpu:
             fc.fc_layer_forward(ctx, g["desc"], g["kv"], x, sel.recompute_idx, sel.n_recompute,
                                 g["y"][nxt])
             x = g["y"][nxt]
+            if U:
+                fc.fc_layer_forward_trail(ctx, g["desc"], g["kv"], xt, g["yt"])
+                xt = g["yt"]
         # ---- oracle: its own chain
         res = osel.select_item(prev, frames[fi], op)
         head = (head + 1) % W
-        lay = ol.Layout(T=T, N=N, W=W, head=head, gw=gw, mrope=tuple(mrope))
+        lay = ol.Layout(T=T, N=N, W=W, head=head, gw=gw, mrope=tuple(mrope), U=U)
         xo = ol.f32(emb[fi])
+        xto = ol.f32(x_text) if U else None
         xs = []
         for o in ora:
             kc, vc, yc = ol.cache_update(o["k"], o["v"], o["y"][cur], o["y"][nxt], res.shift,
@@ -99,6 +110,11 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
             o["written"][lay.cur_rows(res.recompute_idx)] = True
             xs.append(xo)
             xo = y
+            if U:
+                yt, o["k"], o["v"] = ol.layer_trail(xto, o["k"], o["v"], lay, o["wt"], shape)
+                o["written"][lay.trail_rows()] = True
+                o["yt"] = yt
+                xto = yt
         cur = nxt
         counts.append(res.n_recompute)
         if s % check_every and s != steps - 1:
@@ -121,7 +137,9 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
             w = o["written"]
             e_k = fcutil.rel_l2(kg[w], o["k"][w]) if w.any() else 0.0
             e_v = fcutil.rel_l2(vg[w], o["v"][w]) if w.any() else 0.0
-            for name, e in (("y", e_y), ("y rec", e_rec), ("y-x rec", e_res), ("K", e_k), ("V", e_v)):
+            e_t = fcutil.rel_l2(ol.f32(fcutil.bf16_np(g["yt"])[0]), o["yt"]) if U else 0.0
+            for name, e in (("y", e_y), ("y rec", e_rec), ("y-x rec", e_res), ("K", e_k), ("V", e_v),
+                            ("y trail", e_t)):
                 assert e <= fcutil.LAYER_RTOL, f"step {s} layer {li}: {name} rel-L2 {e:.3e}"
                 worst = max(worst, e)
             # rows nobody has written still hold their initial bytes
@@ -135,19 +153,20 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
 
 
 def test_two_toy_layers_ring_of_two(fc):
-    """Two toy layers (d 256, 4 heads x 64, SwiGLU 1024), 32 text tokens and a ring of
-    two frame slots, over six steps of a 448x448 camera trajectory with the 2x2
-    merge (256 tokens): the first step is flushed (no previous frame), the rest
+    """Two toy layers (d 256, 4 heads x 64, SwiGLU 1024), 32 text tokens, a ring of two
+    frame slots and 24 text tokens after the frames (recomputed every step, after
+    each layer's frame tokens), over six steps of a 448x448 camera trajectory with the
+    2x2 merge (256 tokens): the first step is flushed (no previous frame), the rest
     reuse part of the cache."""
     shape = fcdata.TINY_LAYER
     frames = fcdata.episode_frames(31, n_frames=6)
     T, W, N = 32, 2, 256
     ctx = fc.Context(fc.Caps(max_batch=1, max_height=448, max_width=448, max_tokens=N,
-                             max_seq=T + W * N, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_seq=T + W * N + 24, max_d_model=shape.d, max_ffn=shape.ffn,
                              max_qkv=shape.qkv))
     try:
         counts = run_chain(fc, ctx, shape, frames, fc.SelectParams(merge=2), L=2, T=T, W=W,
-                           steps=6, seed=500)
+                           steps=6, seed=500, U=24)
     finally:
         ctx.close()
     assert counts[0] == N and min(counts[1:]) < N

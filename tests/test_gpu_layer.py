@@ -290,6 +290,58 @@ def test_mrope_rejects_bad_sections(fc, ctx):
         c.run(fc, ctx, [np.arange(4)])
 
 
+# ----------------------------------------------------------------- text after the frames
+@pytest.mark.parametrize("mrope", [(0, 0, 0), QWEN_MROPE])
+def test_trailing_text_rows(fc, ctx, mrope):
+    """A prompt with 40 text tokens after a 3-frame ring: fc_layer_forward on the current
+    frame's recomputed tokens (which must not see the trailing text), then
+    fc_layer_forward_trail on all 40 trailing rows (which see everything before them,
+    the new frame rows included); both against the oracle's two calls in the same
+    order, with 1-D and multimodal RoPE."""
+    shape = GQA_SMALL
+    T, N, W, U, head = 16, 64, 3, 40, 2
+    lay = ol.Layout(T=T, N=N, W=W, head=head, gw=8 if sum(mrope) else 0, mrope=tuple(mrope), U=U)
+    wt = fcdata.layer_weights(57, shape)
+    rng = np.random.default_rng(58)
+
+    def rnd(*shp):
+        return fcdata.bf16_round(rng.standard_normal(shp, dtype=np.float32))
+    k, v = rnd(1, lay.S, shape.n_kv, shape.hd), rnd(1, lay.S, shape.n_kv, shape.hd)
+    x, y_prev, xt = rnd(1, N, shape.d), rnd(1, N, shape.d), rnd(1, U, shape.d)
+    ids = fcdata.random_reuse_ids(59, N, 50)
+    idx = np.full((1, N), -1, np.int32)
+    idx[0, :len(ids)] = ids
+    kc, vc, y, yt = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v), fcutil.bf16_gpu(y_prev), fcutil.bf16_gpu(rnd(1, U, shape.d))
+    kv = fc.KVCache(kc, vc, T, N, W, head, grid_w=lay.gw, mrope=lay.mrope, trail_tokens=U)
+    desc = fcutil.layer_desc(shape, fcutil.weights_gpu(wt))
+    fc.fc_layer_forward(ctx, desc, kv, fcutil.bf16_gpu(x), torch.from_numpy(idx).cuda(),
+                        torch.tensor([len(ids)], dtype=torch.int32, device="cuda"), y)
+    fc.fc_layer_forward_trail(ctx, desc, kv, fcutil.bf16_gpu(xt), yt)
+    torch.cuda.synchronize()
+    yo, ko, vo = ol.layer_partial(x[0], ids, k[0], v[0], y_prev[0], lay, wt, shape)
+    yto, kto, vto = ol.layer_trail(xt[0], ko, vo, lay, wt, shape)
+    yg, ytg = fcutil.bf16_np(y)[0], fcutil.bf16_np(yt)[0]
+    kg, vg = fcutil.bf16_np(kc)[0], fcutil.bf16_np(vc)[0]
+    written = np.concatenate([lay.cur_rows(ids), lay.trail_rows()])
+    other = np.setdiff1d(np.arange(lay.S), written)
+    np.testing.assert_array_equal(kg[other], k[0][other])
+    np.testing.assert_array_equal(vg[other], v[0][other])
+    np.testing.assert_array_equal(yg[np.setdiff1d(np.arange(N), ids)],
+                                  y_prev[0][np.setdiff1d(np.arange(N), ids)])
+    errs = dict(y=fcutil.rel_l2(fcdata.bf16_to_f32(yg[ids]), yo[ids]),
+                y_trail=fcutil.rel_l2(fcdata.bf16_to_f32(ytg), yto),
+                k=fcutil.rel_l2(fcdata.bf16_to_f32(kg[written]), kto[written]),
+                v=fcutil.rel_l2(fcdata.bf16_to_f32(vg[written]), vto[written]))
+    print(errs)
+    for name, e in errs.items():
+        assert e <= fcutil.LAYER_RTOL, name
+    # y - x without the exact residual: 2e-2 of the layer's own update, plus the bf16
+    # rounding of the stored output (as for the frame rows)
+    yt32, xt32 = fcdata.bf16_to_f32(ytg), fcdata.bf16_to_f32(xt[0])
+    rnd = np.linalg.norm(fcdata.bf16_to_f32(fcdata.bf16_round(yto)) - yto)
+    assert np.linalg.norm(yt32 - yto) <= fcutil.LAYER_RTOL * np.linalg.norm(yto - xt32) + 2 * rnd
+
+
 # ----------------------------------------------------------------- many gathered rows
 # With B * N >= 2048 token slots the projections run as square MFMA tiles with fused
 # epilogues (the batched-episode regime); these cases take that path.

@@ -328,3 +328,53 @@ def test_mrope_reduces_to_rope_and_keeps_relative_positions():
         ck, sk = ol.mrope_cos_sin(pk + d, sec, hd, theta)
         dots.append(float((ol.rope(q, cq, sq) * ol.rope(k, ck, sk)).sum()))
     assert dots[0] == pytest.approx(dots[1], rel=1e-4)
+
+
+# ------------------------------------------------------------------ text after the frames
+def test_trailing_text_positions():
+    """Text after the frames sits at its prompt index (1-D) and, with multimodal RoPE,
+    continues after the last frame's span: T + W max(grid rows, cols) + u."""
+    lay = ol.Layout(T=2, N=4, W=2, head=1, gw=2, mrope=(16, 24, 24), U=3)
+    np.testing.assert_array_equal(lay.trail_rows(), [10, 11, 12])
+    np.testing.assert_array_equal(lay.row_positions()[10:], [10, 11, 12])
+    np.testing.assert_array_equal(lay.rope_positions(np.array([10, 12])), [[6, 6, 6], [8, 8, 8]])
+
+
+def test_trailing_text_equals_full_causal_forward():
+    """With the ring head at 0 (physical = prompt order), recomputing the text after the
+    frames over the cache of everything before it gives exactly the rows a full causal
+    forward of the whole prompt gives (1-D positions = indices)."""
+    shape = fcdata.TINY_LAYER
+    wt = fcdata.layer_weights(12, shape)
+    lay = ol.Layout(T=8, N=16, W=2, head=0, U=5)
+    rng = np.random.default_rng(4)
+    x = fcdata.bf16_round(rng.standard_normal((lay.S, shape.d), dtype=np.float32))
+    y_full, k_full, v_full = ol.layer_full(x, wt, shape)
+    pre = lay.T + lay.W * lay.N
+    kc = k_full.copy()
+    vc = v_full.copy()
+    kc[pre:] = rng.standard_normal(kc[pre:].shape)        # stale trailing rows are rewritten
+    vc[pre:] = rng.standard_normal(vc[pre:].shape)
+    y, k2, v2 = ol.layer_trail(x[pre:], kc, vc, lay, wt, shape)
+    np.testing.assert_allclose(y, y_full[pre:], rtol=2e-5, atol=2e-5)
+    np.testing.assert_allclose(k2, k_full, rtol=2e-5, atol=2e-5)
+    np.testing.assert_allclose(v2, v_full, rtol=2e-5, atol=2e-5)
+
+
+def test_frame_tokens_do_not_see_trailing_text():
+    """Causality: the current frame's recomputed rows are the same whether or not text
+    rows follow the frames (whatever those rows hold)."""
+    shape = fcdata.TINY_LAYER
+    wt = fcdata.layer_weights(13, shape)
+    rng = np.random.default_rng(5)
+    base = ol.Layout(T=8, N=16, W=2, head=1)
+    with_text = ol.Layout(T=8, N=16, W=2, head=1, U=6)
+    k = fcdata.bf16_round(rng.standard_normal((with_text.S, shape.n_kv, shape.hd), dtype=np.float32))
+    v = fcdata.bf16_round(rng.standard_normal((with_text.S, shape.n_kv, shape.hd), dtype=np.float32))
+    x = fcdata.bf16_round(rng.standard_normal((16, shape.d), dtype=np.float32))
+    y0 = fcdata.bf16_round(rng.standard_normal((16, shape.d), dtype=np.float32))
+    ids = np.array([1, 4, 9, 15])
+    ya, ka, va = ol.layer_partial(x, ids, k[:base.S], v[:base.S], y0, base, wt, shape)
+    yb, kb, vb = ol.layer_partial(x, ids, k, v, y0, with_text, wt, shape)
+    np.testing.assert_array_equal(ya, yb)
+    np.testing.assert_array_equal(ka, kb[:base.S])
