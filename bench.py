@@ -69,6 +69,9 @@ def main():
     ap.add_argument("--select-only", action="store_true",
                     help="run only the 64-pair selection workload and print its record (for "
                          "profiling that workload on its own)")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="run only the one-layer workload (reuse 0/25/50/75/90 %%) and print its "
+                         "record (for profiling that workload on its own)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -97,6 +100,14 @@ def main():
             for _ in range(3):
                 torch.neg(src, out=dst)
             torch.cuda.synchronize()
+        print(json.dumps(rec), flush=True)
+        return
+
+    if args.layer_only:
+        torch.cuda.set_device(0)
+        rec = bench_layer_only(fc, torch)
+        if args.calib_mb > 0:
+            calib_copy(torch, args.calib_mb)
         print(json.dumps(rec), flush=True)
         return
 
@@ -300,6 +311,49 @@ def main():
         del src, dst
     ctx.close()
     print(json.dumps(result), flush=True)
+
+
+def calib_copy(torch, mib):
+    """An elementwise negation over `mib` MiB of float32, three times: it reads and writes
+    exactly that many bytes, the reference that scales the FETCH_SIZE / WRITE_SIZE
+    counters."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda", dtype=torch.float32)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+
+
+def bench_layer_only(fc, torch):
+    """The one-layer workload alone: one Qwen2.5-VL-7B-shaped layer (random bf16 weights,
+    multimodal RoPE) over 128 text + 8 frames x 256 tokens, random caches."""
+    import fcdata
+    dev = torch.device("cuda:0")
+    shape = fcdata.QWEN_LAYER
+    T, N, Wn = 128, 256, 8
+    S = T + Wn * N
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+
+    def randn(*shp, std=0.02):
+        return (torch.randn(*shp, device=dev, generator=g) * std).to(torch.bfloat16)
+    w = dict(w_qkv=randn(shape.qkv, shape.d), b_qkv=randn(shape.qkv),
+             w_o=randn(shape.d, shape.n_heads * shape.hd), w_gate=randn(shape.ffn, shape.d),
+             w_up=randn(shape.ffn, shape.d), w_down=randn(shape.d, shape.ffn),
+             g_attn=torch.ones(shape.d, device=dev, dtype=torch.bfloat16),
+             g_mlp=torch.ones(shape.d, device=dev, dtype=torch.bfloat16))
+    lay = dict(desc=fc.LayerDesc(shape.d, shape.n_heads, shape.n_kv, shape.hd, shape.ffn, w),
+               kv=fc.KVCache(randn(1, S, shape.n_kv, shape.hd, std=1.0),
+                             randn(1, S, shape.n_kv, shape.hd, std=1.0), T, N, Wn, head=3,
+                             grid_w=16, mrope=QWEN_MROPE),
+               y=[randn(1, N, shape.d, std=1.0), randn(1, N, shape.d, std=1.0)])
+    ctx = fc.Context(fc.Caps(max_batch=64, max_height=448, max_width=448, max_tokens=1024,
+                             max_seq=S, max_d_model=shape.d, max_ffn=shape.ffn, max_qkv=shape.qkv))
+    rec = bench_layer_ratios(fc, ctx, torch, lay, shape)
+    ctx.close()
+    return dict(workload="one Qwen2.5-VL-7B-shaped layer, 128 text + 8 x 256 tokens, random "
+                         "masks", layer_ratios=rec, sclk_mhz=observed_sclk_mhz())
 
 
 def timed_calls(torch, fn, reps=60, warm=5):
