@@ -375,15 +375,21 @@ def timed_calls(torch, fn, reps=60, warm=5):
 
 
 def observed_sclk_mhz():
-    """Current shader clock of GPU 0 as rocm-smi reports it (None if unavailable)."""
+    """Current shader clock of GPU 0: the level the driver marks current in its pp_dpm_sclk
+    table (what rocm-smi --showclocks prints), found through the device's PCI bus id; None
+    if unavailable.  A file read, so it works under a profiler too."""
+    import ctypes
     import re
-    import subprocess
     try:
-        out = subprocess.run(["rocm-smi", "-d", "0", "--showclocks"], capture_output=True,
-                             text=True, timeout=20).stdout
-    except Exception:
+        hip = ctypes.CDLL("libamdhip64.so")
+        buf = ctypes.create_string_buffer(64)
+        if hip.hipDeviceGetPCIBusId(buf, ctypes.c_int(64), ctypes.c_int(0)) != 0:
+            return None
+        with open(f"/sys/bus/pci/devices/{buf.value.decode().lower()}/pp_dpm_sclk") as fh:
+            txt = fh.read()
+    except (OSError, AttributeError, UnicodeDecodeError):
         return None
-    m = re.search(r"sclk.*?\((\d+)\s*Mhz\)", out, re.I)
+    m = re.search(r"(\d+)\s*Mhz\s*\*", txt, re.I)
     return int(m.group(1)) if m else None
 
 

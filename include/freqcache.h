@@ -268,6 +268,14 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
                            const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
                            void *stream);
 
+/* Debug mode (process-wide): after every kernel launch the library waits for the
+ * launch stream and reports an error raised while the kernel ran as FC_ERR_HIP from
+ * the call that launched it, with the kernel's name in fc_last_error().  Streams under
+ * graph capture are not waited for.  The mode starts on when the environment variable
+ * FC_DEBUG holds anything but "" or "0" as the library loads.  on = 1 / 0 sets it, a
+ * negative value leaves it; returns the previous mode.  Outputs are the same either way. */
+int32_t fc_debug(int32_t on);
+
 /* Kernel timing with HIP events recorded on the launch stream around every
  * kernel the context launches (off by default). */
 fc_status fc_profile_enable(fc_ctx *ctx, int32_t on);

@@ -4,9 +4,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 
@@ -29,6 +31,24 @@ fc_status fail(fc_status st, const char *fmt, ...) {
   vsnprintf(g_err, sizeof(g_err), fmt, ap);
   va_end(ap);
   return st;
+}
+
+// Debug mode: FC_DEBUG set to anything but "" or "0" when the library loads, or fc_debug.
+static std::atomic<int> g_debug{[] {
+  const char *e = std::getenv("FC_DEBUG");
+  return (e && *e && std::strcmp(e, "0") != 0) ? 1 : 0;
+}()};
+
+bool debug_mode() { return g_debug.load(std::memory_order_relaxed) != 0; }
+
+hipError_t after_launch(hipStream_t st) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !debug_mode()) return e;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+    return hipSuccess;
+  e = hipStreamSynchronize(st);
+  return e != hipSuccess ? e : hipGetLastError();
 }
 
 ProfScope::ProfScope(fc_ctx *c, hipStream_t s, const char *name) : ctx(c), st(s) {
@@ -310,7 +330,9 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
     return fail(FC_ERR_UNSUPPORTED, "%s: d_model %d > 8192", who, L->d_model);
   if (L->n_heads > 128)
     return fail(FC_ERR_UNSUPPORTED, "%s: n_heads %d > 128", who, L->n_heads);
-  if (L->d_model % fc::kGemmBK || L->d_ffn % fc::kGemmBK || (L->n_heads * L->head_dim) % fc::kGemmBK)
+  if (L->head_dim > 256)
+    return fail(FC_ERR_UNSUPPORTED, "%s: head_dim %d > 256", who, L->head_dim);
+  if (L->d_model % fc::kGemmBK || L->d_ffn % fc::kGemmBK || ((long)L->n_heads * L->head_dim) % fc::kGemmBK)
     return fail(FC_ERR_SHAPE, "%s: d_model, d_ffn and n_heads*head_dim must be multiples of %d", who,
                 fc::kGemmBK);
   if (!(L->rms_eps > 0) || !(L->rope_theta > 1))
@@ -323,11 +345,11 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
   if (kv->trail_tokens < 0)
     return fail(FC_ERR_INVALID_ARG, "%s: trail_tokens %d", who, kv->trail_tokens);
   const long S = (long)kv->text_tokens + (long)kv->window * kv->frame_tokens + kv->trail_tokens;
-  const int qkv = (L->n_heads + 2 * L->n_kv_heads) * L->head_dim;
+  const long qkv = ((long)L->n_heads + 2L * L->n_kv_heads) * L->head_dim;
   const int *ms = kv->mrope_section;
   if (ms[0] || ms[1] || ms[2]) {
     if (ms[0] < 0 || ms[1] < 0 || ms[2] < 0 || ms[0] % 8 || ms[1] % 8 || ms[2] % 8 ||
-        ms[0] + ms[1] + ms[2] != L->head_dim / 2)
+        (long)ms[0] + ms[1] + ms[2] != L->head_dim / 2)
       return fail(FC_ERR_INVALID_ARG, "%s: M-RoPE sections %d/%d/%d must be multiples of 8 "
                   "summing to head_dim/2 = %d", who, ms[0], ms[1], ms[2], L->head_dim / 2);
     if (kv->grid_w < 1 || kv->frame_tokens % kv->grid_w)
@@ -339,7 +361,7 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
   if (B > c.max_batch || kv->frame_tokens > c.max_tokens || kv->trail_tokens > c.max_tokens ||
       S > c.max_seq || L->d_model > c.max_d_model ||
       L->d_ffn > c.max_ffn || qkv > c.max_qkv)
-    return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%d exceed the context caps",
+    return fail(FC_ERR_CAPACITY, "%s: B=%d N=%d S=%ld d=%d ffn=%d qkv=%ld exceed the context caps",
                 who, B, kv->frame_tokens, S, L->d_model, L->d_ffn, qkv);
   // the GEMMs address weights and activation rows with 32-bit element offsets
   const long wmax = std::max({(long)qkv, (long)L->d_model, (long)L->d_ffn}) *
@@ -450,6 +472,12 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
   if (st != FC_OK) return st;
   return fc::launch_cache_update_layers(ctx, *layer, n_layers, kvs, y_prev, y_cur, shift, reuse_mask,
                                         grid_w, B, reinterpret_cast<hipStream_t>(stream));
+}
+
+int32_t fc_debug(int32_t on) {
+  const int prev = fc::g_debug.load();
+  if (on >= 0) fc::g_debug.store(on != 0 ? 1 : 0);
+  return prev;
 }
 
 fc_status fc_profile_enable(fc_ctx *ctx, int32_t on) {

@@ -23,6 +23,21 @@ fc_status fail(fc_status st, const char *fmt, ...);
                         __FILE__, __LINE__);                                              \
   } while (0)
 
+// Check after a kernel launch: the launch error and, in debug mode, the stream's
+// completion, so that a fault inside the kernel surfaces as FC_ERR_HIP from the call
+// that launched it.  Streams under graph capture are not waited for.
+hipError_t after_launch(hipStream_t st);
+bool debug_mode();
+
+#define FC_LAUNCH_OK(st, what)                                                            \
+  do {                                                                                    \
+    hipError_t _e = ::fc::after_launch(st);                                               \
+    if (_e != hipSuccess)                                                                 \
+      return ::fc::fail(FC_ERR_HIP, "%s: %s%s", what, hipGetErrorString(_e),              \
+                        ::fc::debug_mode() ? " (debug mode: found when the stream drained)" \
+                                           : "");                                         \
+  } while (0)
+
 // ----------------------------------------------------------------------------- sizes
 constexpr int kPatch = 14;          // the transform kernels are specialised for P = 14
 constexpr int kBins = 100;          // unique DFT amplitude bins of a real 14x14 patch

@@ -1830,7 +1830,7 @@ fc_status run_wgemm(fc_ctx *ctx, hipStream_t st, const char *name, WArgs &g, int
   const long total = (long)B * g.tpb * g.ncg * g.splits;
   ProfScope ps(ctx, st, name);
   hipLaunchKernelGGL(k_wgemm<MODE>, dim3((unsigned)total), dim3(512), 0, st, g);
-  FC_HIP_TRY(hipGetLastError());
+  FC_LAUNCH_OK(st, "k_wgemm");
   return FC_OK;
 }
 
@@ -1872,10 +1872,10 @@ fc_status run_mgemm(fc_ctx *ctx, hipStream_t st, const char *name, MArgs &g, int
   if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
   ProfScope ps(ctx, st, name);
   hipLaunchKernelGGL(k_mgemm<MODE>, dim3((unsigned)total), dim3(512), 0, st, g);
-  FC_HIP_TRY(hipGetLastError());
+  FC_LAUNCH_OK(st, "k_mgemm");
   // a split tail has at most cus / 2 tiles, 4 workgroups each
   hipLaunchKernelGGL(k_mtail<MODE>, dim3((unsigned)(2 * g.cus)), dim3(512), 0, st, g);
-  FC_HIP_TRY(hipGetLastError());
+  FC_LAUNCH_OK(st, "k_mtail");
   return FC_OK;
 }
 
@@ -1929,7 +1929,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     ProfScope ps(ctx, st, "fc_rope_table");
     hipLaunchKernelGGL(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                        ctx->rope, seq, hd / 2, hd, L.rope_theta);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_rope_table");
     ctx->rope_hd = hd;
     ctx->rope_theta = L.rope_theta;
     ctx->rope_seq = seq;
@@ -1962,7 +1962,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
         ProfScope ps(ctx, st, "fc_gather_norm");
         hipLaunchKernelGGL(k_gather_norm, dim3((unsigned)rows), dim3(256), 0, st, x_cur, L.g_attn,
                            idx, nrec, N, d, L.rms_eps, ctx->hb);
-        FC_HIP_TRY(hipGetLastError());
+        FC_LAUNCH_OK(st, "k_gather_norm");
       }
       MArgs g{};
       g.A = ctx->hb; g.W0 = L.w_qkv;
@@ -1977,7 +1977,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
       r.splits = g.splits;
       ProfScope ps(ctx, st, "fc_red_qkv");
       run_red(0, dim3((unsigned)rows, (qkv + 1023) / 1024), st, r);
-      FC_HIP_TRY(hipGetLastError());
+      FC_LAUNCH_OK(st, "k_red_qkv");
     }
   }
 
@@ -2017,7 +2017,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
       hipLaunchKernelGGL(k_rot_keys, dim3((unsigned)((tasks + 255) / 256), B), dim3(256), 0, st,
                          kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, FN, kv.window,
                          kv.head, mr);
-      FC_HIP_TRY(hipGetLastError());
+      FC_LAUNCH_OK(st, "k_rot_keys");
       a.kc = ctx->krot;
     }
     {
@@ -2034,7 +2034,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
         launch_attn<128, 4>(st, a, !prerot, nkv);
       else
         return fail(FC_ERR_UNSUPPORTED, "attention: head_dim %d with %d query heads per kv head", hd, G);
-      FC_HIP_TRY(hipGetLastError());
+      FC_LAUNCH_OK(st, "k_attn");
     }
     if (a.splits > 1) {
       ProfScope ps(ctx, st, "fc_attn_combine");
@@ -2042,7 +2042,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
         hipLaunchKernelGGL(k_attn_combine<128>, dim3((unsigned)(tiles * nh)), dim3(1024), 0, st, a);
       else
         hipLaunchKernelGGL(k_attn_combine<64>, dim3((unsigned)(tiles * nh)), dim3(512), 0, st, a);
-      FC_HIP_TRY(hipGetLastError());
+      FC_LAUNCH_OK(st, "k_attn_combine");
     }
   }
 
@@ -2065,7 +2065,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     r.splits = g.splits;
     ProfScope ps(ctx, st, "fc_red_o");
     run_red(1, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_red_o");
   }
 
   // 4. gate/up on bf16(h1 * g_mlp); 1/rms from the sums of squares is applied to both
@@ -2099,7 +2099,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     r.splits = g.splits;
     ProfScope ps(ctx, st, "fc_red_down");
     run_red(2, dim3((unsigned)rows, (d + 1023) / 1024), st, r);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_red_down");
   }
   return FC_OK;
 }
@@ -2140,7 +2140,7 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
       hipLaunchKernelGGL(k_copy16, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, st,
                          reinterpret_cast<const uint4 *>(vs),
                          reinterpret_cast<uint4 *>(ctx->stage + (long)b * 2 * per + per), n16);
-      FC_HIP_TRY(hipGetLastError());
+      FC_LAUNCH_OK(st, "k_copy16");
     }
     c.ksrc = ctx->stage;
     c.vsrc = ctx->stage + per;
@@ -2155,7 +2155,7 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
   ProfScope ps(ctx, st, "fc_cache_update");
   const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
   hipLaunchKernelGGL(k_cache_update, dim3((unsigned)((chunks + 255) / 256), B), dim3(256), 0, st, c);
-  FC_HIP_TRY(hipGetLastError());
+  FC_LAUNCH_OK(st, "k_cache_update");
   return FC_OK;
 }
 
@@ -2203,7 +2203,7 @@ fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_
     }
     hipLaunchKernelGGL(k_cache_update_layers, dim3((unsigned)((chunks + 255) / 256), B, nl),
                        dim3(256), 0, st, m);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_cache_update_layers");
   }
   return FC_OK;
 }

@@ -1027,7 +1027,7 @@ fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params 
     dim3 grid((Gpw + PW - 1) / PW, Gph, nf * B);
     hipLaunchKernelGGL(k_spectra, grid, dim3(256), 0, st, prev, cur, H, W, Gph, Gpw, nf, ws.prev,
                        ws.cur, ws.penergy);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_spectra");
   }
   {
     ProfScope ps(ctx, st, "fc_grid");
@@ -1036,21 +1036,21 @@ fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params 
     hipLaunchKernelGGL(k_grid, dim3(B), dim3(kGridThreads), 0, st, ws.prev.pmean, ws.cur.pmean,
                        ws.penergy, g,
                        out.energy, out.shift, out.scalars, out.counts);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_grid");
   }
   {
     ProfScope ps(ctx, st, "fc_patchsim");
     dim3 grid((Gph * Gpw + 63) / 64, B);
     hipLaunchKernelGGL(k_patchsim, grid, dim3(256), 0, st, ws.prev.amp, ws.cur.amp, Gph, Gpw, m,
                        out.shift, ws.pdot);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_patchsim");
   }
   {
     ProfScope ps(ctx, st, "fc_topk");
     hipLaunchKernelGGL(k_topk, dim3(B), dim3(kMaxTokens), 0, st, out.energy, ws.pdot, out.shift,
                        out.scalars, out.counts, prm.tau_sim, prm.no_refresh, Gph, Gpw, m, out.sim,
                        out.reuse_mask, out.recompute_idx, out.n_recompute, out.flags);
-    FC_HIP_TRY(hipGetLastError());
+    FC_LAUNCH_OK(st, "k_topk");
   }
   return FC_OK;
 }

@@ -29,9 +29,9 @@ COUNTS = ("k_reuse", "k_cand", "k_final", "flushed")
 FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
-           "fc_layer_forward_trail",
-           "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
-           "fc_profile_only", "fc_profile_read")
+           "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
+           "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
+           "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
 
 class FcError(RuntimeError):
@@ -111,15 +111,16 @@ def lib() -> ctypes.CDLL:
         L.fc_layer_forward_trail.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                              ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p,
                                              c_int32, c_void_p]
+        L.fc_debug.argtypes = [c_int32]
+        L.fc_debug.restype = c_int32
         L.fc_profile_enable.argtypes = [c_void_p, c_int32]
         L.fc_profile_only.argtypes = [c_void_p, c_char_p]
         L.fc_profile_read.argtypes = [c_void_p, c_char_p, ctypes.POINTER(c_double),
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
-                  "fc_layer_forward_trail",
-                  "fc_cache_update",
-                  "fc_cache_update_layers", "fc_layer_forward", "fc_profile_enable",
-                  "fc_profile_only", "fc_profile_read"):
+                  "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward",
+                  "fc_layer_forward_trail", "fc_profile_enable", "fc_profile_only",
+                  "fc_profile_read"):
             getattr(L, n).restype = c_int32
         _lib = L
     return _lib
@@ -479,6 +480,13 @@ def fc_cache_update_layers(ctx: Context, layer: LayerDesc, kvs, y_prevs, y_curs,
 
 
 # ------------------------------------------------------------------------------ timing
+def fc_debug(on: bool | None = None) -> bool:
+    """Debug mode (process-wide): every kernel launch waits for its stream, so a fault
+    inside a kernel is reported by the call that launched it.  None leaves the mode as it
+    is; returns the previous mode."""
+    return bool(lib().fc_debug(-1 if on is None else int(bool(on))))
+
+
 def fc_profile_enable(ctx: Context, on: bool = True):
     _check(lib().fc_profile_enable(ctx.handle, int(on)))
 

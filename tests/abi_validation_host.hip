@@ -1,0 +1,285 @@
+// Host-side driver over the argument validation of the C ABI, built together with the
+// library sources with the host code under AddressSanitizer and UndefinedBehaviorSanitizer
+// (tests/test_abi_sanitize.py) and run on a machine without a GPU.  A context is built by
+// hand (caps set, no device buffers), so every check of fc_select, fc_select_carry,
+// fc_select_noalloc, fc_layer_forward, fc_layer_forward_trail, fc_cache_update and
+// fc_cache_update_layers runs, down to the first device call, which then fails cleanly.
+// Extreme sizes probe the overflow of the size arithmetic.  Exit status 0: every
+// expectation held (the sanitizers abort on a finding).
+#include <climits>
+#include <cstdio>
+#include <cstring>
+
+#include "../paper_2604_24391_amd/csrc/fc_internal.h"
+
+static int g_fail = 0;
+
+#define EXPECT(call, want)                                                              \
+  do {                                                                                  \
+    const fc_status _s = (call);                                                        \
+    const char *_m = fc_last_error();                                                   \
+    if (_s != (want) || (_s != FC_OK && (!_m || !*_m || std::strlen(_m) >= 1024))) {    \
+      std::printf("FAIL line %d: %s -> %d (want %d): %s\n", __LINE__, #call, (int)_s,  \
+                  (int)(want), _m ? _m : "(null)");                                     \
+      ++g_fail;                                                                         \
+    }                                                                                   \
+  } while (0)
+
+// any status but OK: calls that pass validation stop at the first device call
+#define EXPECT_DEVICE_FAIL(call)                                                        \
+  do {                                                                                  \
+    const fc_status _s = (call);                                                        \
+    if (_s != FC_ERR_HIP && _s != FC_ERR_NO_DEVICE) {                                   \
+      std::printf("FAIL line %d: %s -> %d (want a device error): %s\n", __LINE__, #call, \
+                  (int)_s, fc_last_error());                                            \
+      ++g_fail;                                                                         \
+    }                                                                                   \
+  } while (0)
+
+static fc_select_params default_params() {
+  fc_select_params p{};
+  p.patch = 14;
+  p.merge = 2;
+  p.tau_mig = 0.12;
+  p.lambda_ = 0.25;
+  p.alpha_min = 0.08;
+  p.alpha_max = 0.5;
+  p.adaptive = 1;
+  p.alpha_fixed = 0.5;
+  p.entropy_norm = 1;
+  return p;
+}
+
+static fc_layer_desc qwen_layer(uint16_t *w) {
+  fc_layer_desc L{};
+  L.d_model = 3584;
+  L.n_heads = 28;
+  L.n_kv_heads = 4;
+  L.head_dim = 128;
+  L.d_ffn = 18944;
+  L.rms_eps = 1e-6f;
+  L.rope_theta = 1e6;
+  L.w_qkv = L.b_qkv = L.w_o = L.w_gate = L.w_up = L.w_down = L.g_attn = L.g_mlp = w;
+  return L;
+}
+
+static fc_kv_cache qwen_cache(uint16_t *k, uint16_t *v) {
+  fc_kv_cache c{};
+  c.k = k;
+  c.v = v;
+  c.text_tokens = 128;
+  c.frame_tokens = 256;
+  c.window = 8;
+  c.head = 0;
+  return c;
+}
+
+int main() {
+  // buffers are never dereferenced on the host: any non-null address will do
+  alignas(16) static unsigned char host[4096];
+  float *f = reinterpret_cast<float *>(host);
+  uint16_t *h16 = reinterpret_cast<uint16_t *>(host);
+  int32_t *i32 = reinterpret_cast<int32_t *>(host);
+  uint8_t *u8 = host;
+
+  fc_select_out out{};
+  out.sim = f;
+  out.energy = reinterpret_cast<double *>(host);
+  out.reuse_mask = u8;
+  out.recompute_idx = i32;
+  out.n_recompute = i32;
+  out.shift = i32;
+  out.scalars = reinterpret_cast<double *>(host);
+  out.counts = i32;
+
+  // ---------------------------------------------------------------- context-free calls
+  EXPECT(fc_create(nullptr, 0, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_destroy(nullptr), FC_ERR_INVALID_ARG);
+  if (!fc_version() || !*fc_version()) { std::printf("FAIL: empty version\n"); ++g_fail; }
+  if (fc_select_state_bytes(-1, 448, 448) != 0 || fc_select_state_bytes(1, 0, 448) != 0 ||
+      fc_select_state_bytes(1, 448, INT_MIN) != 0) {
+    std::printf("FAIL: state bytes of invalid sizes must be 0\n");
+    ++g_fail;
+  }
+  (void)fc_select_state_bytes(INT_MAX, INT_MAX, INT_MAX);    // no overflow UB
+  (void)fc_select_state_bytes(INT_MAX, 14, 14);
+  const fc_select_params p = default_params();
+  EXPECT(fc_select_noalloc(nullptr, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_select_noalloc(&p, f, f, INT_MAX, 448, 448, &out, nullptr), FC_ERR_CAPACITY);
+  EXPECT(fc_select_noalloc(&p, f, f, 1, INT_MAX - INT_MAX % 28, 28, &out, nullptr),
+         FC_ERR_UNSUPPORTED);
+  EXPECT(fc_select_noalloc(&p, f, f, 64, 448, 448, &out, nullptr), FC_ERR_CAPACITY);
+  EXPECT_DEVICE_FAIL(fc_select_noalloc(&p, f, f, 1, 224, 224, &out, nullptr));
+  {
+    fc_select_params q = p;
+    q.patch = 16;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_UNSUPPORTED);
+    q = p;
+    q.merge = INT_MAX;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    q = p;
+    q.tau_sim = __builtin_nan("");
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    q = p;
+    q.alpha_min = 0.95;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    q = p;
+    q.no_align = 2;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    fc_select_out o2 = out;
+    o2.counts = nullptr;
+    EXPECT(fc_select_noalloc(&p, f, f, 1, 448, 448, &o2, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_select_noalloc(&p, f, f, 1, 450, 448, &out, nullptr), FC_ERR_SHAPE);
+    EXPECT(fc_select_noalloc(&p, f, f, 0, 448, 448, &out, nullptr), FC_ERR_SHAPE);
+    EXPECT(fc_select_noalloc(&p, f, f, 1, 28 * 64, 28 * 64, &out, nullptr), FC_ERR_UNSUPPORTED);
+  }
+  if (fc_debug(-1) != 0 && fc_debug(-1) != 1) { std::printf("FAIL: debug mode\n"); ++g_fail; }
+
+  // --------------------------------------------- a context by hand: caps, no device memory
+  fc_ctx *ctx = new fc_ctx;
+  ctx->device = 0;
+  ctx->caps.max_batch = 4;
+  ctx->caps.max_height = 448;
+  ctx->caps.max_width = 448;
+  ctx->caps.max_tokens = 256;
+  ctx->caps.max_seq = 128 + 8 * 256 + 64;
+  ctx->caps.max_d_model = 3584;
+  ctx->caps.max_ffn = 18944;
+  ctx->caps.max_qkv = 4608;
+
+  EXPECT(fc_select(nullptr, &p, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_select(ctx, &p, f, f, 5, 448, 448, &out, nullptr), FC_ERR_CAPACITY);
+  EXPECT(fc_select(ctx, &p, f, f, 1, 896, 448, &out, nullptr), FC_ERR_CAPACITY);
+  EXPECT_DEVICE_FAIL(fc_select(ctx, &p, f, f, 4, 448, 448, &out, nullptr));
+  EXPECT(fc_select_carry(ctx, &p, host, f, host, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_select_carry(ctx, &p, nullptr, f, nullptr, 1, 448, 448, &out, nullptr),
+         FC_ERR_INVALID_ARG);
+  EXPECT(fc_select_carry(ctx, &p, nullptr, f, host, INT_MAX, 448, 448, &out, nullptr),
+         FC_ERR_CAPACITY);
+  EXPECT_DEVICE_FAIL(fc_select_carry(ctx, &p, nullptr, f, host, 1, 448, 448, &out, nullptr));
+
+  fc_layer_desc L = qwen_layer(h16);
+  fc_kv_cache kv = qwen_cache(h16, h16);
+  auto fwd = [&](const fc_layer_desc &l, const fc_kv_cache &c, int B) {
+    return fc_layer_forward(ctx, &l, &c, h16, i32, i32, h16, B, nullptr);
+  };
+  EXPECT(fc_layer_forward(nullptr, &L, &kv, h16, i32, i32, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_layer_forward(ctx, nullptr, &kv, h16, i32, i32, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_layer_forward(ctx, &L, &kv, nullptr, i32, i32, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT_DEVICE_FAIL(fwd(L, kv, 1));
+  EXPECT(fwd(L, kv, 0), FC_ERR_SHAPE);
+  EXPECT(fwd(L, kv, 5), FC_ERR_CAPACITY);
+  EXPECT(fwd(L, kv, INT_MAX), FC_ERR_CAPACITY);
+  {
+    fc_layer_desc l = L;
+    l.head_dim = INT_MAX;                      // products of dimensions must not overflow
+    EXPECT(fwd(l, kv, 1), FC_ERR_UNSUPPORTED);
+    l = L;
+    l.d_ffn = INT_MAX - 1;
+    EXPECT(fwd(l, kv, 1), FC_ERR_SHAPE);
+    l.d_ffn = INT_MAX - INT_MAX % 64;
+    EXPECT(fwd(l, kv, 1), FC_ERR_CAPACITY);
+    l = L;
+    l.n_kv_heads = 3;
+    EXPECT(fwd(l, kv, 1), FC_ERR_SHAPE);
+    l = L;
+    l.n_heads = 0;
+    EXPECT(fwd(l, kv, 1), FC_ERR_INVALID_ARG);
+    l = L;
+    l.d_model = 8256;
+    EXPECT(fwd(l, kv, 1), FC_ERR_UNSUPPORTED);
+    l = L;
+    l.rms_eps = 0.f;
+    EXPECT(fwd(l, kv, 1), FC_ERR_INVALID_ARG);
+    l = L;
+    l.rope_theta = __builtin_nan("");
+    EXPECT(fwd(l, kv, 1), FC_ERR_INVALID_ARG);
+    l = L;
+    l.w_down = nullptr;
+    EXPECT(fwd(l, kv, 1), FC_ERR_INVALID_ARG);
+    l = L;
+    l.n_heads = 32;                            // 8 query heads per KV head: not built
+    l.d_model = 3584;
+    ctx->caps.max_qkv = 8192;
+    EXPECT(fwd(l, kv, 1), FC_ERR_UNSUPPORTED);
+    ctx->caps.max_qkv = 4608;
+  }
+  {
+    fc_kv_cache c = kv;
+    c.head = 8;
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c = kv;
+    c.window = INT_MAX;                        // T + W N must not overflow
+    c.frame_tokens = INT_MAX;
+    EXPECT(fwd(L, c, 1), FC_ERR_CAPACITY);
+    c = kv;
+    c.trail_tokens = -1;
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c = kv;
+    c.trail_tokens = INT_MAX;
+    EXPECT(fwd(L, c, 1), FC_ERR_CAPACITY);
+    c = kv;
+    c.k = nullptr;
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c = kv;
+    c.mrope_section[0] = 16;
+    c.mrope_section[1] = 24;
+    c.mrope_section[2] = 24;
+    c.grid_w = 16;
+    EXPECT_DEVICE_FAIL(fwd(L, c, 1));
+    c.grid_w = 15;
+    EXPECT(fwd(L, c, 1), FC_ERR_SHAPE);
+    c.grid_w = 0;
+    EXPECT(fwd(L, c, 1), FC_ERR_SHAPE);
+    c.grid_w = 16;
+    c.mrope_section[2] = INT_MAX;              // the sum must not overflow
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c.mrope_section[2] = 20;
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c.mrope_section[0] = -8;
+    c.mrope_section[2] = 40;
+    EXPECT(fwd(L, c, 1), FC_ERR_INVALID_ARG);
+    c = kv;
+    c.trail_tokens = 64;
+    EXPECT_DEVICE_FAIL(fc_layer_forward_trail(ctx, &L, &c, h16, h16, 1, nullptr));
+    EXPECT(fc_layer_forward_trail(ctx, &L, &kv, h16, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_layer_forward_trail(ctx, &L, &c, nullptr, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+    c.trail_tokens = 65;
+    EXPECT(fc_layer_forward_trail(ctx, &L, &c, h16, h16, 1, nullptr), FC_ERR_CAPACITY);
+  }
+  {
+    uint16_t *y2 = h16 + 8;
+    EXPECT(fc_cache_update(ctx, &L, &kv, h16, h16, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 15, 1, nullptr), FC_ERR_SHAPE);
+    EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, nullptr, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT_DEVICE_FAIL(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 16, 1, nullptr));
+    fc_kv_cache kvs[3] = {kv, kv, kv};
+    const uint16_t *yp[3] = {h16, h16, h16};
+    uint16_t *yc[3] = {y2, y2, y2};
+    EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr));
+    EXPECT(fc_cache_update_layers(ctx, &L, 0, kvs, yp, yc, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+    EXPECT(fc_cache_update_layers(ctx, &L, INT_MIN, kvs, yp, yc, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+    kvs[2].head = 1;
+    EXPECT(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr), FC_ERR_SHAPE);
+    kvs[2] = kv;
+    yc[1] = h16;
+    EXPECT(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+  }
+  EXPECT(fc_profile_enable(nullptr, 1), FC_ERR_INVALID_ARG);
+  EXPECT(fc_profile_only(nullptr, "k"), FC_ERR_INVALID_ARG);
+  {
+    double ms = 0;
+    int64_t n = 0;
+    EXPECT(fc_profile_read(nullptr, "k", &ms, &n, 0), FC_ERR_INVALID_ARG);
+    EXPECT(fc_profile_only(ctx, "k_wgemm"), FC_OK);
+    EXPECT(fc_profile_read(ctx, "k_wgemm", &ms, &n, 1), FC_OK);
+    if (ms != 0 || n != 0) { std::printf("FAIL: records of an unused context\n"); ++g_fail; }
+  }
+  delete ctx;                                  // no device buffers to free
+
+  std::printf("%s (%d failed expectations)\n", g_fail ? "FAILED" : "OK", g_fail);
+  return g_fail ? 1 : 0;
+}

@@ -144,3 +144,34 @@ def test_select_state_bytes_and_carry_errors(fc):
     assert fc.select_state_bytes(0, 448, 448) == 0 and fc.select_state_bytes(1, 10, 448) == 0
     lib = fc.lib()
     assert lib.fc_select_carry(None, None, None, None, None, 1, 224, 224, None, None) == 1
+
+
+def test_debug_mode_switch(fc):
+    """fc_debug sets and reports the process-wide debug mode; a negative argument only
+    reads it."""
+    start = fc.fc_debug()
+    try:
+        assert fc.fc_debug(True) == start
+        assert fc.fc_debug() is True
+        assert fc.lib().fc_debug(-5) == 1
+        assert fc.fc_debug(False) is True
+        assert fc.fc_debug() is False
+    finally:
+        fc.fc_debug(start)
+
+
+@pytest.mark.parametrize("value,expect", [("1", 1), ("yes", 1), ("0", 0), ("", 0), (None, 0)])
+def test_debug_mode_from_environment(fc, value, expect):
+    """The mode starts from FC_DEBUG as the library loads (a fresh process loads it)."""
+    import subprocess
+    import sys
+    env = dict(os.environ)
+    env.pop("FC_DEBUG", None)
+    if value is not None:
+        env["FC_DEBUG"] = value
+    code = ("import ctypes; L = ctypes.CDLL(%r); L.fc_debug.restype = ctypes.c_int32; "
+            "print(L.fc_debug(-1))" % fc.freqcache.LIB)
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                         timeout=60)
+    assert out.returncode == 0, out.stderr
+    assert int(out.stdout.strip()) == expect

@@ -212,3 +212,23 @@ def test_episode_selection_every_step(fc):
             assert not esc
     finally:
         ctx.close()
+
+
+def test_toy_chain_in_debug_mode(fc):
+    """The toy chain (three steps) with the debug mode on: every launch waits for its
+    stream and checks for errors; the results still match the oracle chain."""
+    shape = fcdata.TINY_LAYER
+    frames = fcdata.episode_frames(31, n_frames=3)
+    T, W, N = 32, 2, 256
+    before = fc.fc_debug(True)
+    ctx = fc.Context(fc.Caps(max_batch=1, max_height=448, max_width=448, max_tokens=N,
+                             max_seq=T + W * N + 24, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    try:
+        assert fc.fc_debug() is True
+        counts = run_chain(fc, ctx, shape, frames, fc.SelectParams(merge=2), L=2, T=T, W=W,
+                           steps=3, seed=501, U=24)
+    finally:
+        ctx.close()
+        fc.fc_debug(before)
+    assert counts[0] == N
