@@ -26,7 +26,10 @@ Readings where the paper is silent or garbled:
   * std is the population std; E below 1e-8 * m^2 is snapped to exactly 0;
   * phase-correlation guard |X| <= 1e-9 max|X| -> 0, real part, first
     (lowest row-major) index on ties, signed wrap keeping +G/2 positive;
-  * a missing previous frame is treated as an all-zero previous frame.
+  * a missing previous frame is treated as an all-zero previous frame;
+  * align_pixel (a Module I variant): F of Eq. 4-1 is the full-resolution luma,
+    the integer peak is refined per axis by a three-point parabola, and the
+    displacement is rounded to whole tokens (halves away from zero).
 """
 from __future__ import annotations
 
@@ -51,6 +54,8 @@ class SelectParams:
     tau_sim: float = 0.0           # per-token similarity floor; 0 is exact Algorithm 1
     # Module ablations of Table 3 (Sec. 6.3):
     align: bool = True             # False: "w/o Module I", position-wise matching (Delta = 0)
+    align_pixel: bool = False      # True: Eq. 4-1 on full-resolution luma, sub-pixel peak,
+                                   # displacement rounded to whole tokens
     refresh: bool = True           # False: "w/o Module II", no high-frequency refresh
 
 
@@ -195,6 +200,38 @@ def phase_correlation(f_prev: np.ndarray, f_cur: np.ndarray):
     return (di, dj), r
 
 
+def parabolic_offset(a: float, b: float, c: float) -> float:
+    """Vertex of the parabola through (-1, a), (0, b), (+1, c), relative to 0:
+    (a - c) / (2 (a - 2b + c)); 0 when the three points are not a strict peak
+    (a - 2b + c >= 0).  With b the maximum of the three, |offset| <= 1/2."""
+    den = a - 2.0 * b + c
+    if den >= 0.0:
+        return 0.0
+    return float((a - c) / (2.0 * den))
+
+
+def pixel_phase_correlation(y_prev: np.ndarray, y_cur: np.ndarray):
+    """Eq. 4-1 with the feature maps F taken as the frames' full-resolution luma: the
+    integer displacement (pixels) is the argmax of the phase-correlation surface (same
+    guard, tie and wrap rules as on the token grid), refined per axis by the vertex of
+    the parabola through the peak and its two circular neighbours along that axis.
+
+    Returns ((di, dj) sub-pixel floats, (pi, pj) integer peak, response)."""
+    (pi, pj), r = phase_correlation(dft2(y_prev), dft2(y_cur))
+    h, w = r.shape
+    ki, kj = pi % h, pj % w
+    di = pi + parabolic_offset(r[(ki - 1) % h, kj], r[ki, kj], r[(ki + 1) % h, kj])
+    dj = pj + parabolic_offset(r[ki, (kj - 1) % w], r[ki, kj], r[ki, (kj + 1) % w])
+    return (float(di), float(dj)), (int(pi), int(pj)), r
+
+
+def token_shift(d_px: float, tp: int) -> int:
+    """A pixel displacement in whole tokens of tp pixels: d / tp rounded to the
+    nearest integer, halves away from zero."""
+    q = abs(d_px) / tp
+    return int(np.floor(q + 0.5)) * (1 if d_px >= 0 else -1)
+
+
 def align_mask(gh: int, gw: int, di: int, dj: int) -> np.ndarray:
     """O12, Eq. 4-2: token (I, J) is aligned iff its source (I + di, J + dj) lies in
     the previous token grid."""
@@ -265,6 +302,7 @@ class SelectResult:
     k_final: int
     flushed: bool
     response: np.ndarray = field(repr=False, default=None)   # phase-correlation surface
+    shift_px: tuple = None        # sub-pixel displacement (align_pixel only)
 
     @property
     def n_recompute(self) -> int:
@@ -294,7 +332,12 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
     # Module I
     sim_freq = global_similarity(f_cur, f_prev)
     flushed = sim_freq < prm.tau_mig
-    (di, dj), resp = phase_correlation(f_prev, f_cur)
+    shift_px = None
+    if prm.align_pixel:
+        shift_px, _, resp = pixel_phase_correlation(y_prev, y_cur)
+        di, dj = token_shift(shift_px[0], p * m), token_shift(shift_px[1], p * m)
+    else:
+        (di, dj), resp = phase_correlation(f_prev, f_cur)
     if not prm.align:
         # "w/o Module I": tokens are matched at their own positions
         di, dj = 0, 0
@@ -324,7 +367,7 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
         shift=(int(di), int(dj)), sim=sim.ravel(), energy=e_flat, aligned=aligned.ravel(),
         fresh=fresh.ravel(), cand=cand, sim_freq=sim_freq, psi=psi, alpha=alpha, mu=mu,
         sigma=sd, thr=thr, k_reuse=k_reuse, k_cand=k_cand, k_final=k_final,
-        flushed=bool(flushed), response=resp)
+        flushed=bool(flushed), response=resp, shift_px=shift_px)
 
 
 @dataclass
@@ -385,7 +428,11 @@ def decision_margins(res: SelectResult, prm: SelectParams) -> dict:
                  inf for a fixed ratio
       gate       |Sim_freq - tau_mig| / tau_mig          (migration gate)
       shift      (r_1 - r_2) / |r_1| of the two largest phase-correlation values
-                 (argmax of Eq. 4-1)
+                 (argmax of Eq. 4-1); with align_pixel the smaller of the distance of
+                 each axis' d / (P m) to the nearest rounding boundary (a half-integer)
+                 and (r_1 - r_far) / |r_1|, r_far the largest value outside the 3 x 3
+                 neighbourhood of the peak (a flip between neighbours moves the
+                 sub-pixel estimate only slightly)
       tau_sim    per token, |sim - tau_sim| / tau_sim where the similarity floor
                  is active (tau_sim > 0 and the token aligned); inf elsewhere
     """
@@ -402,8 +449,22 @@ def decision_margins(res: SelectResult, prm: SelectParams) -> dict:
     an = res.alpha * n
     budget_m = abs(an - np.round(an)) / max(an, 1e-300) if prm.adaptive else np.inf
     gate_m = abs(res.sim_freq - prm.tau_mig) / prm.tau_mig
-    r = np.sort(res.response.ravel())
-    shift_m = (r[-1] - r[-2]) / max(abs(r[-1]), 1e-300) if r.size > 1 else np.inf
+    if res.shift_px is None:
+        r = np.sort(res.response.ravel())
+        shift_m = (r[-1] - r[-2]) / max(abs(r[-1]), 1e-300) if r.size > 1 else np.inf
+    else:
+        tp = prm.patch * prm.merge
+        rnd = min(abs(abs(d) / tp - np.floor(abs(d) / tp) - 0.5) for d in res.shift_px)
+        resp = res.response
+        h, w = resp.shape
+        ki, kj = divmod(int(np.argmax(resp)), w)
+        far = resp.copy()
+        for a in (-1, 0, 1):
+            for b in (-1, 0, 1):
+                far[(ki + a) % h, (kj + b) % w] = -np.inf
+        r1 = resp[ki, kj]
+        far_m = (r1 - far.max()) / max(abs(r1), 1e-300) if np.isfinite(far.max()) else np.inf
+        shift_m = min(rnd, far_m)
     if prm.tau_sim > 0:
         sim_m = np.where(res.aligned, np.abs(res.sim - prm.tau_sim) / prm.tau_sim, np.inf)
     else:
