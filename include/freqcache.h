@@ -93,6 +93,12 @@ typedef struct {
   /* The paper's naive frequency baseline (Sec. 6.1: position-wise amplitude similarity,
      static reuse above a fixed threshold tau) is no_align = 1, no_refresh = 1,
      adaptive = 0 with alpha_fixed = 1, tau_mig = 0 and tau_sim = tau.                     */
+  int32_t align_pixel;      /* 1: Module I's displacement from Eq. 4-1 on the full-resolution
+                               luma (fc_phase_correlate), rounded to whole tokens of P m
+                               pixels (halves away from zero), instead of the token-grid map.
+                               Needs H and W of the form 7 * 2^k (14 ... 896); the first such
+                               call on a context allocates its workspace.  fc_select and
+                               fc_select_noalloc only (not fc_select_carry).               */
 } fc_select_params;
 
 enum { FC_SCALAR_SIM_FREQ = 0, FC_SCALAR_PSI, FC_SCALAR_ALPHA, FC_SCALAR_MU,
@@ -267,6 +273,26 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
                            const uint16_t *x_cur, const int32_t *recompute_idx,
                            const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
                            void *stream);
+
+/* Pixel-resolution phase correlation: Eq. 4-1 (Sec. 4.1) with the feature maps taken
+ * as the frames' full-resolution BT.601 luma (float64).  The displacement is the first
+ * maximum (row-major) of Re F^-1(C), C = X / |X|, X = F(Y_prev) conj(F(Y_cur)), with bins
+ * |X| <= 1e-9 max|X| set to 0, wrapped to (-N/2, N/2]; each axis is then refined by the
+ * vertex of the parabola through the peak and its two circular neighbours on that axis.
+ * Token (I, J) of the current frame shows the content of previous-frame pixel
+ * position + (di, dj).
+ *   frames_prev, frames_cur: [B][3][H][W] float32 (device); frames_prev may be NULL
+ *                (an all-zero previous frame: shift (0, 0)).
+ *   H, W:        each 7 * 2^k with 14 <= H, W <= 896 (e.g. 224, 448, 896), within caps;
+ *                otherwise FC_ERR_UNSUPPORTED / FC_ERR_CAPACITY.
+ *   shift_px:    [B][2] float64 (di, dj) sub-pixel displacement (device, caller-owned).
+ *   peak:        [B][2] int32 integer peak (di, dj), or NULL.
+ *   response:    [B][H][W] float64 phase-correlation surface, or NULL.
+ * The first call on a context allocates its workspace (B H (W/2 + 1) 32 bytes plus row
+ * and strip maxima at the caps' sizes); later calls allocate nothing.  Stream-ordered. */
+fc_status fc_phase_correlate(fc_ctx *ctx, const float *frames_prev, const float *frames_cur,
+                             int32_t B, int32_t H, int32_t W, double *shift_px, int32_t *peak,
+                             double *response, void *stream);
 
 /* Debug mode (process-wide): after every kernel launch the library waits for the
  * launch stream and reports an error raised while the kernel ran as FC_ERR_HIP from

@@ -118,7 +118,7 @@ fc_status check_select_args(const fc_select_params *prm, const float *cur,
   if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
       !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
       !std::isfinite(p.tau_sim) || (p.no_align != 0 && p.no_align != 1) ||
-      (p.no_refresh != 0 && p.no_refresh != 1))
+      (p.no_refresh != 0 && p.no_refresh != 1) || (p.align_pixel != 0 && p.align_pixel != 1))
     return fail(FC_ERR_INVALID_ARG, "%s: hyper-parameter out of range", who);
   if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "%s: B=%d H=%d W=%d", who, B, H, W);
   const int tp = p.patch * p.merge;
@@ -127,6 +127,9 @@ fc_status check_select_args(const fc_select_params *prm, const float *cur,
   const long M = (long)(H / tp) * (W / tp);
   if (M > kMaxTokens)
     return fail(FC_ERR_UNSUPPORTED, "%s: %ld tokens per frame > %d", who, M, kMaxTokens);
+  if (p.align_pixel && (!pix_size_ok(H) || !pix_size_ok(W)))
+    return fail(FC_ERR_UNSUPPORTED, "%s: align_pixel needs H and W of the form 7 * 2^k up to 896 "
+                "(got %dx%d)", who, H, W);
   return FC_OK;
 }
 
@@ -152,7 +155,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->spec, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
-                  c->krot};
+                  c->krot, c->pix};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -167,6 +170,21 @@ void free_ws(fc_ctx *c) {
 fc_status use_device(fc_ctx *ctx) {
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return fail(FC_ERR_HIP, "hipSetDevice(%d): %s", ctx->device, hipGetErrorString(e));
+  return FC_OK;
+}
+
+// The pixel phase-correlation workspace, sized for the context's caps at its first use.
+fc_status ensure_pix(fc_ctx *ctx) {
+  if (ctx->pix) return FC_OK;
+  const size_t bytes = fc::pix_ws_bytes(ctx->caps.max_batch, ctx->caps.max_height,
+                                        ctx->caps.max_width);
+  hipError_t e = hipMalloc(reinterpret_cast<void **>(&ctx->pix), bytes);
+  if (e != hipSuccess) {
+    ctx->pix = nullptr;
+    return fail(FC_ERR_HIP, "hipMalloc(pixel phase correlation, %zu bytes): %s", bytes,
+                hipGetErrorString(e));
+  }
+  ctx->pix_bytes = bytes;
   return FC_OK;
 }
 
@@ -264,9 +282,13 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
     return fail(FC_ERR_CAPACITY, "fc_select: B=%d H=%d W=%d N=%d exceed the context caps", B, H, W, M);
   st = use_device(ctx);
   if (st != FC_OK) return st;
-  const fc::SelectWs ws{fc::spectra_at(ctx->spec, B, H, W),
-                        fc::spectra_at(ctx->spec + ctx->spec_half, B, H, W), ctx->penergy,
-                        ctx->pdot};
+  fc::SelectWs ws{fc::spectra_at(ctx->spec, B, H, W),
+                  fc::spectra_at(ctx->spec + ctx->spec_half, B, H, W), ctx->penergy, ctx->pdot,
+                  {}};
+  if (prm->align_pixel) {
+    if ((st = ensure_pix(ctx)) != FC_OK) return st;
+    ws.pix = fc::pix_ws_at(ctx->pix, B, H, W);
+  }
   return fc::launch_select(ctx, ws, *prm, frames_prev, frames_cur, B, H, W, *out,
                            reinterpret_cast<hipStream_t>(stream));
 }
@@ -283,6 +305,9 @@ fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *
   fc_status st = fc::check_select_args(prm, frames_cur, out, B, H, W, "fc_select_carry");
   if (st != FC_OK) return st;
   if (!state_cur) return fail(FC_ERR_INVALID_ARG, "fc_select_carry: null state_cur");
+  if (prm->align_pixel)
+    return fail(FC_ERR_UNSUPPORTED, "fc_select_carry: align_pixel needs the previous frame's "
+                "pixels; use fc_select");
   if (state_cur == state_prev)
     return fail(FC_ERR_INVALID_ARG, "fc_select_carry: state_prev and state_cur alias");
   const int tp = prm->patch * prm->merge;
@@ -298,7 +323,7 @@ fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *
   const bool carried = state_prev != nullptr;
   const fc::SelectWs ws{carried ? fc::spectra_at(const_cast<void *>(state_prev), B, H, W)
                                 : fc::spectra_at(ctx->spec, B, H, W),
-                        fc::spectra_at(state_cur, B, H, W), ctx->penergy, ctx->pdot};
+                        fc::spectra_at(state_cur, B, H, W), ctx->penergy, ctx->pdot, {}};
   return fc::launch_select(ctx, ws, *prm, nullptr, frames_cur, B, H, W, *out,
                            reinterpret_cast<hipStream_t>(stream), carried);
 }
@@ -316,6 +341,26 @@ fc_status fc_select_noalloc(const fc_select_params *prm, const float *frames_pre
                 B, H, W, need, fc::noalloc_scratch_bytes());
   return fc::launch_select_noalloc(*prm, frames_prev, frames_cur, B, H, W, *out,
                                    reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_phase_correlate(fc_ctx *ctx, const float *frames_prev, const float *frames_cur,
+                             int32_t B, int32_t H, int32_t W, double *shift_px, int32_t *peak,
+                             double *response, void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_phase_correlate: null context");
+  if (!frames_cur || !shift_px)
+    return fail(FC_ERR_INVALID_ARG, "fc_phase_correlate: null current frames or shift output");
+  if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "fc_phase_correlate: B=%d H=%d W=%d", B, H, W);
+  if (!fc::pix_size_ok(H) || !fc::pix_size_ok(W))
+    return fail(FC_ERR_UNSUPPORTED, "fc_phase_correlate: H and W must be 7 * 2^k up to 896 "
+                "(got %dx%d)", H, W);
+  if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width)
+    return fail(FC_ERR_CAPACITY, "fc_phase_correlate: B=%d H=%d W=%d exceed the context caps", B, H, W);
+  fc_status st = use_device(ctx);
+  if (st != FC_OK) return st;
+  if ((st = ensure_pix(ctx)) != FC_OK) return st;
+  return fc::launch_pixel_pc(ctx, fc::pix_ws_at(ctx->pix, B, H, W), frames_prev, frames_cur, B, H,
+                             W, shift_px, peak, response, nullptr, 1, false,
+                             reinterpret_cast<hipStream_t>(stream));
 }
 
 static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_cache *kv, int B,

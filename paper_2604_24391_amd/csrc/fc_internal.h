@@ -81,6 +81,8 @@ struct fc_ctx {
   size_t stage_elems = 0;
   uint16_t *krot = nullptr;    // [B][S][kv row] rotated keys (many-row layer calls only)
   size_t krot_elems = 0;
+  unsigned char *pix = nullptr;  // pixel phase-correlation workspace, allocated at first use
+  size_t pix_bytes = 0;
   // kernel timing
   bool prof = false;
   std::string prof_only;       // empty: time every kernel
@@ -107,12 +109,35 @@ struct FrameSpectra {
   float *amp;
   double *pmean;
 };
+// Workspace of the pixel-resolution phase correlation (pixpc.hip): the half-plane
+// spectra of both frames [B][H][W/2 + 1] (sa later holds the cross power and its inverse
+// column transforms; sb the response surface when the caller gives no buffer), per-row
+// maxima and their columns, per-strip largest |X|, and the sub-pixel shifts [B][2].
+struct PixWs {
+  double2 *sa = nullptr, *sb = nullptr;
+  double *rowmax = nullptr;
+  int *rowarg = nullptr;
+  double *bmax = nullptr;
+  double *shift_px = nullptr;
+};
+bool pix_size_ok(int n);                       // n = 7 2^k, 14 <= n <= 896
+size_t pix_ws_bytes(long B, long H, long W);
+PixWs pix_ws_at(void *base, long B, long H, long W);
+// Eq. 4-1 on full-resolution luma for B pairs (prev may be null: an all-zero frame).
+// shift_px [B][2] (null: the workspace's), peak [B][2] integer peak (may be null),
+// resp [B][H][W] response surface (may be null), tok_shift [B][2] the displacement in
+// whole tokens of tp pixels, (0, 0) with zero_shift (may be null).
+fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
+                          int B, int H, int W, double *shift_px, int32_t *peak, double *resp,
+                          int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st);
+
 // Selection workspace: spectra of the previous and the current frames, per-patch
-// high-pass energies (current frame) and spectral products.
+// high-pass energies (current frame) and spectral products; pix only with align_pixel.
 struct SelectWs {
   FrameSpectra prev, cur;
   double *penergy;   // [B][Np]
   double *pdot;      // [B][3][Np]
+  PixWs pix;
 };
 // Bytes of one frame batch's spectra (256-B aligned parts) and of the whole workspace.
 struct SpectraBytes {

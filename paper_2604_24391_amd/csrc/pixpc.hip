@@ -1,0 +1,468 @@
+// Pixel-resolution phase correlation on gfx950: Eq. 4-1 with the feature maps taken as
+// the frames' full-resolution BT.601 luma, the integer peak refined per axis by a
+// three-point parabola, and (for the selection) the displacement rounded to whole tokens.
+// A variant of Module I (Sec. 4.1) for frames whose motion is not a whole number of
+// tokens; the token-grid reading stays the default.
+//
+// The frames are real, so only columns 0..W/2 of each row spectrum are kept (the rest
+// is their conjugate mirror).  Five kernels per call, all float64 like the oracle's
+// decision:
+//
+//   k_pc_rows      one workgroup per (image row, pair): luma of both frames, their
+//                  length-W FFTs in LDS, the two half-row spectra.
+//   k_pc_cols<1>   one workgroup per (strip of CW columns, pair): column FFTs of both
+//                  half-spectra, cross power X = F_{t-1} conj(F_t) in place, the
+//                  strip's largest |X|.
+//   k_pc_cols<0>   same strips: X / |X| under the guard |X| > 1e-9 max|X| (else 0),
+//                  inverse column FFTs.
+//   k_pc_rows_inv  one workgroup per (row, pair): the Hermitian row completed from its
+//                  half, inverse FFT, real part / (H W) = the response surface, and the
+//                  row's first maximum.
+//   k_pc_peak      one workgroup per pair: first maximum over the rows (row-major ties
+//                  to the lower index), signed wrap, parabolic refinement with circular
+//                  neighbours, the token shift.
+//
+// The FFTs are self-sorting (Stockham) mixed-radix transforms of length n = 7 2^k:
+// one radix-7 stage, then radix-4 stages and at most one radix-2 stage, each stage a
+// pass over LDS between two buffers.  Twiddles come from sincospi of the exact
+// rational angle.  Sizes: H and W of the form 7 2^k with 2 <= 2^k <= 128 (14 ... 896).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "fc_internal.h"
+
+namespace fc {
+namespace {
+
+constexpr int kPcThreads = 256;
+constexpr int kPcMaxN = 896;
+
+__device__ __forceinline__ double2 cmul(double2 a, double2 b) {
+  return make_double2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+__device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
+
+// e^{sgn 2 pi i num / den}
+__device__ __forceinline__ double2 root(long num, long den, double sgn) {
+  double s, c;
+  sincospi(2.0 * (double)num / (double)den, &s, &c);
+  return make_double2(c, sgn * s);
+}
+
+// In-register DFT of R points: V[q] = sum_r v[r] e^{sgn 2 pi i r q / R}.
+template <int R>
+__device__ __forceinline__ void dft_reg(double2 (&v)[R], double sgn);
+
+template <>
+__device__ __forceinline__ void dft_reg<2>(double2 (&v)[2], double) {
+  const double2 a = v[0], b = v[1];
+  v[0] = cadd(a, b);
+  v[1] = csub(a, b);
+}
+
+template <>
+__device__ __forceinline__ void dft_reg<4>(double2 (&v)[4], double sgn) {
+  const double2 s02 = cadd(v[0], v[2]), d02 = csub(v[0], v[2]);
+  const double2 s13 = cadd(v[1], v[3]), d13 = csub(v[1], v[3]);
+  // sgn i (v1 - v3)
+  const double2 jd13 = make_double2(-sgn * d13.y, sgn * d13.x);
+  v[0] = cadd(s02, s13);
+  v[1] = cadd(d02, jd13);
+  v[2] = csub(s02, s13);
+  v[3] = csub(d02, jd13);
+}
+
+template <>
+__device__ __forceinline__ void dft_reg<7>(double2 (&v)[7], double sgn) {
+  double2 w[7];
+#pragma unroll
+  for (int k = 0; k < 7; ++k) w[k] = root(k, 7, sgn);
+  double2 out[7];
+#pragma unroll
+  for (int q = 0; q < 7; ++q) {
+    double2 acc = v[0];
+#pragma unroll
+    for (int r = 1; r < 7; ++r) acc = cadd(acc, cmul(v[r], w[(r * q) % 7]));
+    out[q] = acc;
+  }
+#pragma unroll
+  for (int q = 0; q < 7; ++q) v[q] = out[q];
+}
+
+// One Stockham stage of radix R over nseq sequences of length n (pitch n) in LDS:
+// it combines R sub-transforms of length ns into ones of length ns R.
+template <int R>
+__device__ __forceinline__ void stage(const double2 *__restrict__ d0, double2 *__restrict__ d1,
+                                      int n, int nseq, int ns, double sgn) {
+  const int per = n / R;
+  for (int it = threadIdx.x; it < nseq * per; it += blockDim.x) {
+    const int s = it / per, j = it - s * per;
+    const double2 *src = d0 + (long)s * n;
+    double2 *dst = d1 + (long)s * n;
+    const int k = j % ns;
+    double2 v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      v[r] = src[j + r * per];
+      if (r > 0 && k > 0) v[r] = cmul(v[r], root((long)r * k, (long)ns * R, sgn));
+    }
+    dft_reg<R>(v, sgn);
+    const int o = (j / ns) * ns * R + k;
+#pragma unroll
+    for (int q = 0; q < R; ++q) dst[o + q * ns] = v[q];
+  }
+}
+
+// Batched FFT of nseq length-n sequences (n = 7 2^k) held in a; b is scratch of the same
+// size.  Returns the buffer that holds the result.  sgn -1: forward, +1: inverse
+// (unnormalised).
+__device__ double2 *fft_lds(double2 *a, double2 *b, int n, int nseq, double sgn) {
+  int ns = 1;
+  stage<7>(a, b, n, nseq, ns, sgn);
+  __syncthreads();
+  ns = 7;
+  double2 *x = b, *y = a;
+  int rest = n / 7;
+  while (rest >= 4) {
+    stage<4>(x, y, n, nseq, ns, sgn);
+    __syncthreads();
+    ns *= 4;
+    rest /= 4;
+    double2 *t = x;
+    x = y;
+    y = t;
+  }
+  if (rest == 2) {
+    stage<2>(x, y, n, nseq, ns, sgn);
+    __syncthreads();
+    double2 *t = x;
+    x = y;
+    y = t;
+  }
+  return x;
+}
+
+__device__ __forceinline__ double luma_at(const float *frame, size_t plane, size_t off) {
+  return 0.299 * (double)frame[off] + 0.587 * (double)frame[plane + off] +
+         0.114 * (double)frame[2 * plane + off];
+}
+
+// ------------------------------------------------------------------------- k_pc_rows
+// The two frames' rows are transformed as two separate sequences (not packed into one
+// complex sequence): packing leaks rounding noise of one frame's spectrum into the
+// other's, which dominates when a frame is (nearly) zero.
+__global__ __launch_bounds__(kPcThreads) void k_pc_rows(const float *__restrict__ prev,
+                                                        const float *__restrict__ cur, int H,
+                                                        int W, PixWs ws) {
+  __shared__ double2 buf[2][2 * kPcMaxN];
+  const int y = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  const int hw = W / 2 + 1;
+  const size_t plane = (size_t)H * W;
+  const float *fp = prev ? prev + (size_t)b * 3 * plane : nullptr;
+  const float *fc = cur + (size_t)b * 3 * plane;
+  for (int x = t; x < W; x += blockDim.x) {
+    const size_t off = (size_t)y * W + x;
+    buf[0][x] = make_double2(fp ? luma_at(fp, plane, off) : 0.0, 0.0);
+    buf[0][W + x] = make_double2(luma_at(fc, plane, off), 0.0);
+  }
+  __syncthreads();
+  const double2 *Z = fft_lds(buf[0], buf[1], W, 2, -1.0);
+  double2 *sa = ws.sa + ((size_t)b * H + y) * hw;
+  double2 *sb = ws.sb + ((size_t)b * H + y) * hw;
+  for (int k = t; k < hw; k += blockDim.x) {
+    sa[k] = Z[k];
+    sb[k] = Z[W + k];
+  }
+}
+
+// ------------------------------------------------------------------------- k_pc_cols
+// Column strips: CW adjacent half-spectrum columns per workgroup, for H <= MAXH.
+template <int MAXH, int CW, bool FWD>
+__global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) {
+  constexpr int NS = FWD ? 2 * CW : CW;
+  __shared__ double2 buf[2][NS * MAXH];
+  __shared__ double red[kPcThreads / 64];
+  const int b = blockIdx.y, t = threadIdx.x;
+  const int hw = W / 2 + 1;
+  const int c0 = blockIdx.x * CW;
+  const int cw = min(CW, hw - c0);
+  double2 *sa = ws.sa + (size_t)b * H * hw;
+  const double2 *sb = ws.sb + (size_t)b * H * hw;
+  if (FWD) {
+    for (int e = t; e < NS * H; e += blockDim.x) {
+      const int s = e / H, y = e - s * H;
+      const int c = s < CW ? s : s - CW;
+      double2 v = make_double2(0.0, 0.0);
+      if (c < cw) v = (s < CW ? sa : sb)[(size_t)y * hw + c0 + c];
+      buf[0][s * H + y] = v;
+    }
+    __syncthreads();
+    double2 *F = fft_lds(buf[0], buf[1], H, NS, -1.0);
+    double mx = 0.0;
+    for (int e = t; e < cw * H; e += blockDim.x) {
+      const int c = e / H, ky = e - c * H;
+      const double2 f1 = F[c * H + ky], f2 = F[(CW + c) * H + ky];
+      const double xr = f1.x * f2.x + f1.y * f2.y;
+      const double xi = f1.y * f2.x - f1.x * f2.y;
+      sa[(size_t)ky * hw + c0 + c] = make_double2(xr, xi);
+      mx = fmax(mx, sqrt(xr * xr + xi * xi));
+    }
+    for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o));
+    if ((t & 63) == 0) red[t >> 6] = mx;
+    __syncthreads();
+    if (t == 0) {
+      double m = red[0];
+      for (int i = 1; i < kPcThreads / 64; ++i) m = fmax(m, red[i]);
+      ws.bmax[(size_t)b * gridDim.x + blockIdx.x] = m;
+    }
+  } else {
+    if (t < 64) {
+      double m = 0.0;
+      for (int i = t; i < (int)gridDim.x; i += 64) m = fmax(m, ws.bmax[(size_t)b * gridDim.x + i]);
+      for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+      if (t == 0) red[0] = m;
+    }
+    __syncthreads();
+    const double gmax = red[0];
+    for (int e = t; e < NS * H; e += blockDim.x) {
+      const int c = e / H, y = e - c * H;
+      double2 v = make_double2(0.0, 0.0);
+      if (c < cw) {
+        const double2 x = sa[(size_t)y * hw + c0 + c];
+        const double mag = sqrt(x.x * x.x + x.y * x.y);
+        if (gmax > 0.0 && mag > 1e-9 * gmax) v = make_double2(x.x / mag, x.y / mag);
+      }
+      buf[0][c * H + y] = v;
+    }
+    __syncthreads();
+    const double2 *G = fft_lds(buf[0], buf[1], H, NS, 1.0);
+    for (int e = t; e < cw * H; e += blockDim.x) {
+      const int c = e / H, y = e - c * H;
+      sa[(size_t)y * hw + c0 + c] = G[c * H + y];
+    }
+  }
+}
+
+// --------------------------------------------------------------------- k_pc_rows_inv
+__global__ __launch_bounds__(kPcThreads) void k_pc_rows_inv(int H, int W, PixWs ws,
+                                                            double *__restrict__ resp) {
+  __shared__ double2 buf[2][kPcMaxN];
+  __shared__ double bv[kPcThreads / 64];
+  __shared__ int bi[kPcThreads / 64];
+  const int y = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  const int hw = W / 2 + 1;
+  const double2 *g = ws.sa + ((size_t)b * H + y) * hw;
+  for (int k = t; k < W; k += blockDim.x) {
+    double2 v;
+    if (k < hw) {
+      v = g[k];
+    } else {
+      const double2 m = g[W - k];
+      v = make_double2(m.x, -m.y);
+    }
+    buf[0][k] = v;
+  }
+  __syncthreads();
+  const double2 *R = fft_lds(buf[0], buf[1], W, 1, 1.0);
+  const double hwn = (double)H * (double)W;
+  double best = -INFINITY;
+  int arg = 0x7fffffff;
+  double *row = resp + ((size_t)b * H + y) * W;
+  for (int x = t; x < W; x += blockDim.x) {
+    const double r = R[x].x / hwn;
+    row[x] = r;
+    if (r > best) {  // ascending x per thread: the first maximum
+      best = r;
+      arg = x;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const double v2 = __shfl_xor(best, o);
+    const int i2 = __shfl_xor(arg, o);
+    if (v2 > best || (v2 == best && i2 < arg)) {
+      best = v2;
+      arg = i2;
+    }
+  }
+  if ((t & 63) == 0) {
+    bv[t >> 6] = best;
+    bi[t >> 6] = arg;
+  }
+  __syncthreads();
+  if (t == 0) {
+    double v = bv[0];
+    int a = bi[0];
+    for (int i = 1; i < kPcThreads / 64; ++i)
+      if (bv[i] > v || (bv[i] == v && bi[i] < a)) {
+        v = bv[i];
+        a = bi[i];
+      }
+    ws.rowmax[(size_t)b * H + y] = v;
+    ws.rowarg[(size_t)b * H + y] = a;
+  }
+}
+
+// ------------------------------------------------------------------------- k_pc_peak
+__device__ __forceinline__ double parabolic(double a, double c0, double c) {
+  const double den = a - 2.0 * c0 + c;
+  return den >= 0.0 ? 0.0 : (a - c) / (2.0 * den);
+}
+
+__device__ __forceinline__ int token_round(double d, int tp) {
+  const double q = fabs(d) / (double)tp;
+  const int k = (int)floor(q + 0.5);
+  return d >= 0.0 ? k : -k;
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_pc_peak(int H, int W, PixWs ws,
+                                                        const double *__restrict__ resp,
+                                                        double *__restrict__ shift_px,
+                                                        int32_t *__restrict__ peak,
+                                                        int32_t *__restrict__ tok_shift, int tp,
+                                                        int zero_shift) {
+  __shared__ double bv[kPcThreads / 64];
+  __shared__ long bi[kPcThreads / 64];
+  const int b = blockIdx.x, t = threadIdx.x;
+  double best = -INFINITY;
+  long arg = 0x7fffffffffffffffL;
+  for (int y = t; y < H; y += blockDim.x) {
+    const double v = ws.rowmax[(size_t)b * H + y];
+    const long i = (long)y * W + ws.rowarg[(size_t)b * H + y];
+    if (v > best || (v == best && i < arg)) {
+      best = v;
+      arg = i;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const double v2 = __shfl_xor(best, o);
+    const long i2 = __shfl_xor(arg, o);
+    if (v2 > best || (v2 == best && i2 < arg)) {
+      best = v2;
+      arg = i2;
+    }
+  }
+  if ((t & 63) == 0) {
+    bv[t >> 6] = best;
+    bi[t >> 6] = arg;
+  }
+  __syncthreads();
+  if (t != 0) return;
+  double v = bv[0];
+  long a = bi[0];
+  for (int i = 1; i < kPcThreads / 64; ++i)
+    if (bv[i] > v || (bv[i] == v && bi[i] < a)) {
+      v = bv[i];
+      a = bi[i];
+    }
+  const int ki = (int)(a / W), kj = (int)(a - (long)ki * W);
+  const int pi = ki <= H / 2 ? ki : ki - H;
+  const int pj = kj <= W / 2 ? kj : kj - W;
+  const double *r = resp + (size_t)b * H * W;
+  const double c0 = r[(size_t)ki * W + kj];
+  const double di = pi + parabolic(r[(size_t)((ki - 1 + H) % H) * W + kj], c0,
+                                   r[(size_t)((ki + 1) % H) * W + kj]);
+  const double dj = pj + parabolic(r[(size_t)ki * W + (kj - 1 + W) % W], c0,
+                                   r[(size_t)ki * W + (kj + 1) % W]);
+  if (shift_px) {
+    shift_px[2 * b] = di;
+    shift_px[2 * b + 1] = dj;
+  }
+  if (peak) {
+    peak[2 * b] = pi;
+    peak[2 * b + 1] = pj;
+  }
+  if (tok_shift) {
+    tok_shift[2 * b] = zero_shift ? 0 : token_round(di, tp);
+    tok_shift[2 * b + 1] = zero_shift ? 0 : token_round(dj, tp);
+  }
+}
+
+template <int MAXH, int CW>
+void launch_cols(int H, int W, int B, const PixWs &ws, hipStream_t st) {
+  const int hw = W / 2 + 1;
+  const dim3 grid((unsigned)((hw + CW - 1) / CW), (unsigned)B);
+  hipLaunchKernelGGL((k_pc_cols<MAXH, CW, true>), grid, dim3(kPcThreads), 0, st, H, W, ws);
+  hipLaunchKernelGGL((k_pc_cols<MAXH, CW, false>), grid, dim3(kPcThreads), 0, st, H, W, ws);
+}
+
+}  // namespace
+
+bool pix_size_ok(int n) {
+  if (n < 14 || n > kPcMaxN || n % 7) return false;
+  const int p = n / 7;
+  return (p & (p - 1)) == 0;
+}
+
+size_t pix_ws_bytes(long B, long H, long W) {
+  const long hw = W / 2 + 1;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const long ncb = (hw + 1) / 2;             // strips of the narrowest kind (CW = 2)
+  return 2 * al((size_t)B * H * hw * sizeof(double2)) + al((size_t)B * H * sizeof(double)) +
+         al((size_t)B * H * sizeof(int)) + al((size_t)B * ncb * sizeof(double)) +
+         al((size_t)B * 2 * sizeof(double));
+}
+
+PixWs pix_ws_at(void *base, long B, long H, long W) {
+  const long hw = W / 2 + 1;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const long ncb = (hw + 1) / 2;
+  unsigned char *p = static_cast<unsigned char *>(base);
+  PixWs ws;
+  ws.sa = reinterpret_cast<double2 *>(p);
+  p += al((size_t)B * H * hw * sizeof(double2));
+  ws.sb = reinterpret_cast<double2 *>(p);
+  p += al((size_t)B * H * hw * sizeof(double2));
+  ws.rowmax = reinterpret_cast<double *>(p);
+  p += al((size_t)B * H * sizeof(double));
+  ws.rowarg = reinterpret_cast<int *>(p);
+  p += al((size_t)B * H * sizeof(int));
+  ws.bmax = reinterpret_cast<double *>(p);
+  p += al((size_t)B * ncb * sizeof(double));
+  ws.shift_px = reinterpret_cast<double *>(p);
+  return ws;
+}
+
+fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
+                          int B, int H, int W, double *shift_px, int32_t *peak, double *resp,
+                          int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st) {
+  if (!pix_size_ok(H) || !pix_size_ok(W))
+    return fail(FC_ERR_UNSUPPORTED, "pixel phase correlation: H=%d, W=%d must be 7 * 2^k, 14..%d",
+                H, W, kPcMaxN);
+  // the response surface goes to the caller's buffer or over the current-frame
+  // half-spectra, which the forward column pass has consumed by then
+  double *r = resp ? resp : reinterpret_cast<double *>(ws.sb);
+  {
+    ProfScope ps(ctx, st, "fc_pc_rows");
+    hipLaunchKernelGGL(k_pc_rows, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, prev,
+                       cur, H, W, ws);
+    FC_LAUNCH_OK(st, "k_pc_rows");
+  }
+  {
+    ProfScope ps(ctx, st, "fc_pc_cols");
+    if (H <= 224)
+      launch_cols<224, 8>(H, W, B, ws, st);
+    else if (H <= 448)
+      launch_cols<448, 4>(H, W, B, ws, st);
+    else
+      launch_cols<896, 2>(H, W, B, ws, st);
+    FC_LAUNCH_OK(st, "k_pc_cols");
+  }
+  {
+    ProfScope ps(ctx, st, "fc_pc_rows_inv");
+    hipLaunchKernelGGL(k_pc_rows_inv, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, H,
+                       W, ws, r);
+    FC_LAUNCH_OK(st, "k_pc_rows_inv");
+  }
+  {
+    ProfScope ps(ctx, st, "fc_pc_peak");
+    hipLaunchKernelGGL(k_pc_peak, dim3((unsigned)B), dim3(kPcThreads), 0, st, H, W, ws,
+                       (const double *)r, shift_px ? shift_px : ws.shift_px, peak, tok_shift, tp,
+                       zero_shift ? 1 : 0);
+    FC_LAUNCH_OK(st, "k_pc_peak");
+  }
+  return FC_OK;
+}
+
+}  // namespace fc

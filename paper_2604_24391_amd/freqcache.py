@@ -31,6 +31,7 @@ FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
            "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
+           "fc_phase_correlate",
            "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
 
@@ -50,7 +51,8 @@ class fc_select_params(ctypes.Structure):
     _fields_ = [("patch", c_int32), ("merge", c_int32), ("tau_mig", c_double),
                 ("lambda_", c_double), ("alpha_min", c_double), ("alpha_max", c_double),
                 ("adaptive", c_int32), ("alpha_fixed", c_double), ("entropy_norm", c_int32),
-                ("tau_sim", c_double), ("no_align", c_int32), ("no_refresh", c_int32)]
+                ("tau_sim", c_double), ("no_align", c_int32), ("no_refresh", c_int32),
+                ("align_pixel", c_int32)]
 
 
 class fc_select_out(ctypes.Structure):
@@ -111,6 +113,8 @@ def lib() -> ctypes.CDLL:
         L.fc_layer_forward_trail.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                              ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p,
                                              c_int32, c_void_p]
+        L.fc_phase_correlate.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
+                                         c_void_p, c_void_p, c_void_p, c_void_p]
         L.fc_debug.argtypes = [c_int32]
         L.fc_debug.restype = c_int32
         L.fc_profile_enable.argtypes = [c_void_p, c_int32]
@@ -119,8 +123,8 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
                   "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward",
-                  "fc_layer_forward_trail", "fc_profile_enable", "fc_profile_only",
-                  "fc_profile_read"):
+                  "fc_layer_forward_trail", "fc_phase_correlate", "fc_profile_enable",
+                  "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
         _lib = L
     return _lib
@@ -232,6 +236,7 @@ class SelectParams:
     tau_sim: float = 0.0
     align: bool = True          # False: ablation "w/o Module I" (position-wise matching)
     refresh: bool = True        # False: ablation "w/o Module II" (no edge refresh)
+    align_pixel: bool = False   # True: Module I's displacement from full-resolution luma
 
     @classmethod
     def naive(cls, tau: float, merge: int = 1) -> "SelectParams":
@@ -247,7 +252,7 @@ class SelectParams:
         return fc_select_params(self.patch, self.merge, self.tau_mig, self.lam, self.alpha_min,
                                 self.alpha_max, int(self.adaptive), self.alpha_fixed,
                                 int(self.entropy_norm), self.tau_sim, int(not self.align),
-                                int(not self.refresh))
+                                int(not self.refresh), int(self.align_pixel))
 
 
 @dataclass
@@ -327,6 +332,28 @@ def fc_select_noalloc(prm: SelectParams, prev: torch.Tensor | None, cur: torch.T
     cp, pp, pc, B, H, W, co = _select_args(prm, prev, cur, out)
     _check(lib().fc_select_noalloc(ctypes.byref(cp), pp, pc, B, H, W, ctypes.byref(co),
                                    _stream(stream)))
+
+
+def fc_phase_correlate(ctx: Context, prev: torch.Tensor | None, cur: torch.Tensor,
+                       shift_px: torch.Tensor, peak: torch.Tensor | None = None,
+                       response: torch.Tensor | None = None, stream=None):
+    """Pixel-resolution phase correlation of a [B, 3, H, W] float32 batch of frame pairs
+    (prev may be None): shift_px [B, 2] float64 sub-pixel displacement, optionally peak
+    [B, 2] int32 integer peak and response [B, H, W] float64 surface."""
+    if cur.dim() != 4 or cur.shape[1] != 3:
+        raise ValueError("cur must be [B, 3, H, W]")
+    B, _, H, W = cur.shape
+    pc = _ptr(cur, torch.float32, B * 3 * H * W, "cur")
+    if prev is not None:
+        if tuple(prev.shape) != tuple(cur.shape):
+            raise ValueError("prev and cur shapes differ")
+        pp = _ptr(prev, torch.float32, B * 3 * H * W, "prev")
+    else:
+        pp = c_void_p(0)
+    sp = _ptr(shift_px, torch.float64, 2 * B, "shift_px")
+    pk = _ptr(peak, torch.int32, 2 * B, "peak") if peak is not None else c_void_p(0)
+    rs = _ptr(response, torch.float64, B * H * W, "response") if response is not None else c_void_p(0)
+    _check(lib().fc_phase_correlate(ctx.handle, pp, pc, B, H, W, sp, pk, rs, _stream(stream)))
 
 
 def select_state_bytes(B: int, H: int, W: int) -> int:

@@ -2,7 +2,7 @@
 // library sources with the host code under AddressSanitizer and UndefinedBehaviorSanitizer
 // (tests/test_abi_sanitize.py) and run on a machine without a GPU.  A context is built by
 // hand (caps set, no device buffers), so every check of fc_select, fc_select_carry,
-// fc_select_noalloc, fc_layer_forward, fc_layer_forward_trail, fc_cache_update and
+// fc_select_noalloc, fc_phase_correlate, fc_layer_forward, fc_layer_forward_trail, fc_cache_update and
 // fc_cache_update_layers runs, down to the first device call, which then fails cleanly.
 // Extreme sizes probe the overflow of the size arithmetic.  Exit status 0: every
 // expectation held (the sanitizers abort on a finding).
@@ -132,6 +132,13 @@ int main() {
     EXPECT(fc_select_noalloc(&p, f, f, 1, 450, 448, &out, nullptr), FC_ERR_SHAPE);
     EXPECT(fc_select_noalloc(&p, f, f, 0, 448, 448, &out, nullptr), FC_ERR_SHAPE);
     EXPECT(fc_select_noalloc(&p, f, f, 1, 28 * 64, 28 * 64, &out, nullptr), FC_ERR_UNSUPPORTED);
+    q = p;
+    q.align_pixel = 2;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    q.align_pixel = 1;
+    EXPECT(fc_select_noalloc(&q, f, f, 1, 420, 448, &out, nullptr), FC_ERR_UNSUPPORTED);
+    EXPECT(fc_select_noalloc(&q, f, f, 8, 448, 448, &out, nullptr), FC_ERR_CAPACITY);
+    EXPECT_DEVICE_FAIL(fc_select_noalloc(&q, f, f, 1, 448, 448, &out, nullptr));
   }
   if (fc_debug(-1) != 0 && fc_debug(-1) != 1) { std::printf("FAIL: debug mode\n"); ++g_fail; }
 
@@ -157,6 +164,31 @@ int main() {
   EXPECT(fc_select_carry(ctx, &p, nullptr, f, host, INT_MAX, 448, 448, &out, nullptr),
          FC_ERR_CAPACITY);
   EXPECT_DEVICE_FAIL(fc_select_carry(ctx, &p, nullptr, f, host, 1, 448, 448, &out, nullptr));
+  {
+    fc_select_params q = p;
+    q.align_pixel = 1;
+    EXPECT(fc_select_carry(ctx, &q, nullptr, f, host, 1, 448, 448, &out, nullptr),
+           FC_ERR_UNSUPPORTED);
+    EXPECT_DEVICE_FAIL(fc_select(ctx, &q, f, f, 1, 448, 448, &out, nullptr));
+    double *sp = reinterpret_cast<double *>(host);
+    EXPECT(fc_phase_correlate(nullptr, f, f, 1, 448, 448, sp, nullptr, nullptr, nullptr),
+           FC_ERR_INVALID_ARG);
+    EXPECT(fc_phase_correlate(ctx, f, f, 1, 448, 448, nullptr, nullptr, nullptr, nullptr),
+           FC_ERR_INVALID_ARG);
+    EXPECT(fc_phase_correlate(ctx, f, f, 1, 448, 420, sp, nullptr, nullptr, nullptr),
+           FC_ERR_UNSUPPORTED);
+    EXPECT(fc_phase_correlate(ctx, f, f, 1, 7 * 256, 448, sp, nullptr, nullptr, nullptr),
+           FC_ERR_UNSUPPORTED);
+    EXPECT(fc_phase_correlate(ctx, f, f, 1, INT_MAX, 448, sp, nullptr, nullptr, nullptr),
+           FC_ERR_UNSUPPORTED);
+    EXPECT(fc_phase_correlate(ctx, f, f, 0, 448, 448, sp, nullptr, nullptr, nullptr), FC_ERR_SHAPE);
+    EXPECT(fc_phase_correlate(ctx, f, f, 5, 448, 448, sp, nullptr, nullptr, nullptr),
+           FC_ERR_CAPACITY);
+    EXPECT(fc_phase_correlate(ctx, f, f, 1, 896, 448, sp, nullptr, nullptr, nullptr),
+           FC_ERR_CAPACITY);
+    EXPECT_DEVICE_FAIL(fc_phase_correlate(ctx, nullptr, f, 4, 448, 448, sp, nullptr, nullptr,
+                                          nullptr));
+  }
 
   fc_layer_desc L = qwen_layer(h16);
   fc_kv_cache kv = qwen_cache(h16, h16);

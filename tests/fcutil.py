@@ -162,4 +162,5 @@ def oracle_select_params(prm) -> osel.SelectParams:
                              alpha_min=prm.alpha_min, alpha_max=prm.alpha_max,
                              adaptive=prm.adaptive, alpha_fixed=prm.alpha_fixed,
                              entropy_norm=prm.entropy_norm, tau_sim=prm.tau_sim,
-                             align=prm.align, refresh=prm.refresh)
+                             align=prm.align, refresh=prm.refresh,
+                             align_pixel=prm.align_pixel)

@@ -20,7 +20,8 @@ HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
 def test_abi_validation_under_host_sanitizers(tmp_path):
     exe = str(tmp_path / "abi_validation")
-    srcs = [os.path.join(CSRC, s) for s in ("abi.hip", "select.hip", "layer.hip")]
+    from paper_2604_24391_amd import build as fcbuild
+    srcs = [os.path.join(CSRC, s) for s in fcbuild.SOURCES]
     srcs.append(os.path.join(ROOT, "tests", "abi_validation_host.hip"))
     cmd = [HIPCC, "--offload-arch=gfx950", "-O1", "-std=c++17", "-Xarch_host", "-g",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

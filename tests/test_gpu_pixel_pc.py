@@ -1,0 +1,159 @@
+"""Pixel-resolution phase correlation (Eq. 4-1 on full-resolution luma) through the C ABI
+against the oracle: the response surface element by element, the integer peak exactly,
+the sub-pixel displacement to 1e-9 px, and the selection with align_pixel bit-exact
+(strict harness, no tolerated decision mismatch)."""
+import numpy as np
+import pytest
+import torch
+
+import fcdata
+from oracle import select as osel
+from tests import fcutil
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fc():
+    import paper_2604_24391_amd as fc
+    fc.lib()
+    return fc
+
+
+def ctx_for(fc, B, H, W):
+    return fc.Context(fc.Caps(max_batch=B, max_height=H, max_width=W, max_tokens=1024,
+                              max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+
+
+def run_pc(fc, ctx, prev, cur):
+    B, _, H, W = cur.shape
+    sp = torch.empty(B, 2, dtype=torch.float64, device="cuda")
+    pk = torch.empty(B, 2, dtype=torch.int32, device="cuda")
+    rs = torch.empty(B, H, W, dtype=torch.float64, device="cuda")
+    fc.fc_phase_correlate(ctx, None if prev is None else torch.from_numpy(prev).cuda(),
+                          torch.from_numpy(cur).cuda(), sp, pk, rs)
+    torch.cuda.synchronize()
+    return sp.cpu().numpy(), pk.cpu().numpy(), rs.cpu().numpy()
+
+
+def compare_pc(prev, cur, sp, pk, rs):
+    for b in range(cur.shape[0]):
+        yp = osel.luma(prev[b]) if prev is not None else np.zeros(cur.shape[2:])
+        (di, dj), (pi, pj), r = osel.pixel_phase_correlation(yp, osel.luma(cur[b]))
+        np.testing.assert_allclose(rs[b], r, rtol=0, atol=1e-9 * max(1.0, np.abs(r).max()),
+                                   err_msg=f"pair {b}: response")
+        assert tuple(pk[b]) == (pi, pj), f"pair {b}: peak {tuple(pk[b])} vs {(pi, pj)}"
+        np.testing.assert_allclose(sp[b], (di, dj), rtol=0, atol=1e-9, err_msg=f"pair {b}")
+
+
+@pytest.mark.parametrize("H,W", [(28, 56), (112, 224), (224, 224), (448, 448), (896, 448),
+                                 (14, 896)])
+def test_surface_peak_and_shift_random_rolls(fc, H, W):
+    """Random frames rolled by random (also fractional, band-limited) amounts, at every
+    transform length the kernels are built for."""
+    rng = np.random.default_rng(H * 1000 + W)
+    B = 3
+    prev = rng.random((B, 3, H, W)).astype(np.float32)
+    cur = np.empty_like(prev)
+    for b in range(B):
+        cur[b] = np.roll(prev[b], (int(rng.integers(-H // 3, H // 3 + 1)),
+                                   int(rng.integers(-W // 3, W // 3 + 1))), axis=(1, 2))
+    # the last pair: a fractional shift through the Fourier shift theorem
+    u = np.fft.fftfreq(H)[:, None]
+    v = np.fft.fftfreq(W)[None, :]
+    ramp = np.exp(-2j * np.pi * (u * 2.3 + v * -1.6))
+    cur[-1] = np.clip(np.real(np.fft.ifft2(np.fft.fft2(prev[-1]) * ramp)), 0, 1).astype(np.float32)
+    ctx = ctx_for(fc, B, H, W)
+    try:
+        sp, pk, rs = run_pc(fc, ctx, prev, cur)
+    finally:
+        ctx.close()
+    compare_pc(prev, cur, sp, pk, rs)
+
+
+def test_trajectory_pairs_and_missing_previous(fc):
+    """Consecutive 448 x 448 frames of the benchmark trajectory, and batches without a
+    previous frame or with an all-black one (shift 0, zero surface, as in the oracle)."""
+    frames = fcdata.episode_frames(2024, size=448, n_frames=9)
+    prev, cur = frames[:-1], frames[1:]
+    ctx = ctx_for(fc, 8, 448, 448)
+    try:
+        sp, pk, rs = run_pc(fc, ctx, prev, cur)
+        compare_pc(prev, cur, sp, pk, rs)
+        sp0, pk0, rs0 = run_pc(fc, ctx, None, cur[:2])
+        sp1, pk1, rs1 = run_pc(fc, ctx, np.zeros_like(cur[:2]), cur[:2])
+    finally:
+        ctx.close()
+    # a missing and an all-black previous frame: zero spectrum, zero surface, shift 0
+    for sp_, pk_, rs_ in ((sp0, pk0, rs0), (sp1, pk1, rs1)):
+        assert not rs_.any() and not pk_.any() and not sp_.any()
+
+
+def test_rejects_unsupported_sizes(fc):
+    ctx = ctx_for(fc, 1, 448, 448)
+    try:
+        cur = torch.zeros(1, 3, 420, 448, device="cuda")
+        sp = torch.empty(1, 2, dtype=torch.float64, device="cuda")
+        with pytest.raises(fc.FcError, match="UNSUPPORTED"):
+            fc.fc_phase_correlate(ctx, None, cur, sp)
+        big = torch.zeros(2, 3, 448, 448, device="cuda")
+        with pytest.raises(fc.FcError, match="CAPACITY"):
+            fc.fc_phase_correlate(ctx, None, big, torch.empty(2, 2, dtype=torch.float64,
+                                                              device="cuda"))
+        prm = fc.SelectParams(merge=2, align_pixel=True)
+        out = fc.SelectOut.alloc(1, 1024)
+        st = fc.select_state_alloc(1, 448, 448)
+        with pytest.raises(fc.FcError, match="UNSUPPORTED"):
+            fc.fc_select_carry(ctx, prm, None, torch.zeros(1, 3, 448, 448, device="cuda"), st, out)
+    finally:
+        ctx.close()
+
+
+@pytest.mark.parametrize("case", ["trajectory_merge2", "shear_free_merge1"])
+def test_selection_with_pixel_alignment(fc, case):
+    """fc_select with align_pixel on consecutive trajectory frames, every output against
+    the oracle's selection with the same variant (strict: no tolerated mismatch)."""
+    if case == "trajectory_merge2":
+        frames = fcdata.episode_frames(2024, size=448, n_frames=9)
+        prm = fc.SelectParams(merge=2, align_pixel=True)
+    else:
+        frames = fcdata.episode_frames(99, size=224, n_frames=9, shear=0.0)
+        prm = fc.SelectParams(merge=1, align_pixel=True)
+    op = fcutil.oracle_select_params(prm)
+    B, _, H, W = frames[1:].shape
+    ctx = ctx_for(fc, B, H, W)
+    try:
+        fr = torch.from_numpy(frames).cuda()
+        gh, gw = fc.token_grid(H, W, prm)
+        out = fc.SelectOut.alloc(B, gh * gw)
+        fc.fc_select(ctx, prm, fr[:-1], fr[1:], out)
+        torch.cuda.synchronize()
+        o = fcutil.select_out_np(out)
+    finally:
+        ctx.close()
+    shifts = set()
+    for b in range(B):
+        res = osel.select_item(frames[b], frames[b + 1], op)
+        mg, esc = fcutil.check_select(o, res, op, b)
+        assert not esc, f"pair {b}: {esc}"
+        shifts.add(res.shift)
+    assert len(shifts) > 1          # the trajectory exercises several displacements
+
+
+def test_noalloc_with_pixel_alignment(fc):
+    """fc_select_noalloc with align_pixel gives the bytes fc_select gives."""
+    frames = fcdata.episode_frames(5, size=224, n_frames=3)
+    prm = fc.SelectParams(merge=2, align_pixel=True)
+    fr = torch.from_numpy(frames).cuda()
+    ctx = ctx_for(fc, 2, 224, 224)
+    try:
+        a = fc.SelectOut.alloc(2, 64)
+        b = fc.SelectOut.alloc(2, 64)
+        fc.fc_select(ctx, prm, fr[:-1], fr[1:], a)
+        fc.fc_select_noalloc(prm, fr[:-1], fr[1:], b)
+        torch.cuda.synchronize()
+    finally:
+        ctx.close()
+    oa, ob = fcutil.select_out_np(a), fcutil.select_out_np(b)
+    for k in oa:
+        np.testing.assert_array_equal(oa[k], ob[k], err_msg=k)
