@@ -482,12 +482,56 @@ def bench_select_batch(fc, ctx, torch):
         c_.close()
     multi["note"] = "independent 64-pair batches over 2 or 3 streams, each with its own context"
     g50 = (frame_bytes + out_bytes) / (dist["p50"] * 1e-6) / 1e9
+    pixel = bench_pixel_pc(fc, ctx, torch, prev, cur, out, dist["p50"])
     return dict(workload="64 pairs 448x448, 14-px patches, 1024 patches/frame, adaptive",
                 call_us=round(call_us, 2), algorithmic_bytes=frame_bytes + out_bytes,
                 gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
                 call_us_dist=dist, frac_hbm_p50=round(g50 / HBM_PEAK_GBS, 4),
                 spectra_gbs=round(spectra_gbs, 1), kernel_avg_us=kern,
-                multi_stream=multi)
+                multi_stream=multi, pixel_alignment=pixel)
+
+
+def bench_pixel_pc(fc, ctx, torch, prev, cur, out, base_p50):
+    """The pixel-resolution Module I on the same 64 pairs: fc_phase_correlate alone and
+    fc_select with align_pixel (event-timed medians), with the per-kernel split."""
+    B, _, H, W = cur.shape
+    shift_px = torch.empty(B, 2, dtype=torch.float64, device="cuda")
+    prm = fc.SelectParams(align_pixel=True)
+    for _ in range(3):
+        fc.fc_phase_correlate(ctx, prev, cur, shift_px)
+        fc.fc_select(ctx, prm, prev, cur, out)
+    torch.cuda.synchronize()
+    pc = timed_calls(torch, lambda: fc.fc_phase_correlate(ctx, prev, cur, shift_px))
+    sel = timed_calls(torch, lambda: fc.fc_select(ctx, prm, prev, cur, out))
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    for _ in range(20):
+        fc.fc_phase_correlate(ctx, prev, cur, shift_px)
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
+    kern = {}
+    for name in ("fc_pc_rows", "fc_pc_cols", "fc_pc_rows_inv", "fc_pc_peak"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        kern[name] = round(tot * 1e3 / cnt, 3)
+    fc.fc_profile_read(ctx, None, reset=True)
+    hw = W // 2 + 1
+    frames = 2 * B * 3 * H * W * 4
+    # workspace round trips per pair: half-spectra of both frames written by the row pass
+    # and read by the forward column pass, the cross power written and read back, its
+    # inverse column transforms written and read by the inverse row pass, the surface
+    # written and its peak neighbourhood read
+    ws = B * (2 * H * hw * 16 * 2 + H * hw * 16 * 2 + H * hw * 16 * 2 + H * W * 8)
+    flops = B * 5 * (2 * H * W * np.log2(W) + 2 * hw * H * np.log2(H) + hw * H * np.log2(H)
+                     + H * W * np.log2(W))
+    p50 = pc["p50"]
+    return dict(workload="Eq. 4-1 on 448x448 luma (float64), 64 pairs",
+                phase_correlate_us=pc, select_align_pixel_us=sel,
+                select_token_grid_p50_us=round(base_p50, 2), kernel_avg_us=kern,
+                frame_bytes=frames, workspace_bytes=int(ws),
+                frame_gbs_p50=round(frames / (p50 * 1e-6) / 1e9, 1),
+                frac_hbm_frames_p50=round(frames / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                frac_hbm_with_workspace_p50=round((frames + ws) / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                fp64_tflops_p50=round(flops / (p50 * 1e-6) / 1e12, 2))
 
 
 def bench_ablations(fc, ctx, torch, frames, m, N):

@@ -24,8 +24,8 @@
 //
 // The FFTs are self-sorting (Stockham) mixed-radix transforms of length n = 7 2^k:
 // one radix-7 stage, then radix-4 stages and at most one radix-2 stage, each stage a
-// pass over LDS between two buffers.  Twiddles come from sincospi of the exact
-// rational angle.  Sizes: H and W of the form 7 2^k with 2 <= 2^k <= 128 (14 ... 896).
+// pass over LDS between two buffers.  Twiddles come from one table per workgroup
+// (sincospi of the exact rational angle m / n).  Sizes: H and W of the form 7 2^k with 2 <= 2^k <= 128 (14 ... 896).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -44,59 +44,89 @@ __device__ __forceinline__ double2 cmul(double2 a, double2 b) {
 __device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
 
-// e^{sgn 2 pi i num / den}
-__device__ __forceinline__ double2 root(long num, long den, double sgn) {
-  double s, c;
-  sincospi(2.0 * (double)num / (double)den, &s, &c);
-  return make_double2(c, sgn * s);
+// Twiddle table of a length-n transform in LDS: tw[m] = e^{-2 pi i m / n}, m < n, from
+// sincospi of the exact rational angle.  Every stage's twiddle and the radix-7 roots are
+// entries of it (the inverse transform takes their conjugates).
+__device__ void make_twiddles(double2 *tw, int n) {
+  for (int m = threadIdx.x; m < n; m += blockDim.x) {
+    double s, c;
+    sincospi(2.0 * (double)m / (double)n, &s, &c);
+    tw[m] = make_double2(c, -s);
+  }
 }
 
-// In-register DFT of R points: V[q] = sum_r v[r] e^{sgn 2 pi i r q / R}.
-template <int R>
-__device__ __forceinline__ void dft_reg(double2 (&v)[R], double sgn);
+template <bool INV>
+__device__ __forceinline__ double2 tw_at(const double2 *tw, int m) {
+  const double2 w = tw[m];
+  return INV ? make_double2(w.x, -w.y) : w;
+}
+
+// In-register DFT of R points: V[q] = sum_r v[r] e^{-+2 pi i r q / R} (- forward).
+// w7: the seventh roots of unity of the transform's direction (radix 7 only).
+template <int R, bool INV>
+__device__ __forceinline__ void dft_reg(double2 (&v)[R], const double2 *w7);
 
 template <>
-__device__ __forceinline__ void dft_reg<2>(double2 (&v)[2], double) {
+__device__ __forceinline__ void dft_reg<2, false>(double2 (&v)[2], const double2 *) {
+  const double2 a = v[0], b = v[1];
+  v[0] = cadd(a, b);
+  v[1] = csub(a, b);
+}
+template <>
+__device__ __forceinline__ void dft_reg<2, true>(double2 (&v)[2], const double2 *) {
   const double2 a = v[0], b = v[1];
   v[0] = cadd(a, b);
   v[1] = csub(a, b);
 }
 
-template <>
-__device__ __forceinline__ void dft_reg<4>(double2 (&v)[4], double sgn) {
+template <bool INV>
+__device__ __forceinline__ void dft4(double2 (&v)[4]) {
   const double2 s02 = cadd(v[0], v[2]), d02 = csub(v[0], v[2]);
   const double2 s13 = cadd(v[1], v[3]), d13 = csub(v[1], v[3]);
-  // sgn i (v1 - v3)
-  const double2 jd13 = make_double2(-sgn * d13.y, sgn * d13.x);
+  // -i (v1 - v3) forward, +i (v1 - v3) inverse
+  const double2 jd13 = INV ? make_double2(-d13.y, d13.x) : make_double2(d13.y, -d13.x);
   v[0] = cadd(s02, s13);
   v[1] = cadd(d02, jd13);
   v[2] = csub(s02, s13);
   v[3] = csub(d02, jd13);
 }
-
 template <>
-__device__ __forceinline__ void dft_reg<7>(double2 (&v)[7], double sgn) {
-  double2 w[7];
-#pragma unroll
-  for (int k = 0; k < 7; ++k) w[k] = root(k, 7, sgn);
+__device__ __forceinline__ void dft_reg<4, false>(double2 (&v)[4], const double2 *) { dft4<false>(v); }
+template <>
+__device__ __forceinline__ void dft_reg<4, true>(double2 (&v)[4], const double2 *) { dft4<true>(v); }
+
+template <bool INV>
+__device__ __forceinline__ void dft7(double2 (&v)[7], const double2 *w7) {
   double2 out[7];
 #pragma unroll
   for (int q = 0; q < 7; ++q) {
     double2 acc = v[0];
 #pragma unroll
-    for (int r = 1; r < 7; ++r) acc = cadd(acc, cmul(v[r], w[(r * q) % 7]));
+    for (int r = 1; r < 7; ++r) acc = cadd(acc, cmul(v[r], w7[(r * q) % 7]));
     out[q] = acc;
   }
 #pragma unroll
   for (int q = 0; q < 7; ++q) v[q] = out[q];
 }
+template <>
+__device__ __forceinline__ void dft_reg<7, false>(double2 (&v)[7], const double2 *w7) { dft7<false>(v, w7); }
+template <>
+__device__ __forceinline__ void dft_reg<7, true>(double2 (&v)[7], const double2 *w7) { dft7<true>(v, w7); }
 
 // One Stockham stage of radix R over nseq sequences of length n (pitch n) in LDS:
-// it combines R sub-transforms of length ns into ones of length ns R.
-template <int R>
+// it combines R sub-transforms of length ns into ones of length ns R.  The twiddle of
+// element r of butterfly j is e^{-+2 pi i r k / (ns R)}, k = j mod ns, which is
+// tw[r k n / (ns R)].
+template <int R, bool INV>
 __device__ __forceinline__ void stage(const double2 *__restrict__ d0, double2 *__restrict__ d1,
-                                      int n, int nseq, int ns, double sgn) {
+                                      const double2 *__restrict__ tw, int n, int nseq, int ns) {
   const int per = n / R;
+  const int step = n / (ns * R);
+  double2 w7[7];
+  if (R == 7) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) w7[k] = tw_at<INV>(tw, k * (n / 7));
+  }
   for (int it = threadIdx.x; it < nseq * per; it += blockDim.x) {
     const int s = it / per, j = it - s * per;
     const double2 *src = d0 + (long)s * n;
@@ -106,9 +136,9 @@ __device__ __forceinline__ void stage(const double2 *__restrict__ d0, double2 *_
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       v[r] = src[j + r * per];
-      if (r > 0 && k > 0) v[r] = cmul(v[r], root((long)r * k, (long)ns * R, sgn));
+      if (r > 0 && k > 0) v[r] = cmul(v[r], tw_at<INV>(tw, r * k * step));
     }
-    dft_reg<R>(v, sgn);
+    dft_reg<R, INV>(v, w7);
     const int o = (j / ns) * ns * R + k;
 #pragma unroll
     for (int q = 0; q < R; ++q) dst[o + q * ns] = v[q];
@@ -116,17 +146,18 @@ __device__ __forceinline__ void stage(const double2 *__restrict__ d0, double2 *_
 }
 
 // Batched FFT of nseq length-n sequences (n = 7 2^k) held in a; b is scratch of the same
-// size.  Returns the buffer that holds the result.  sgn -1: forward, +1: inverse
-// (unnormalised).
-__device__ double2 *fft_lds(double2 *a, double2 *b, int n, int nseq, double sgn) {
+// size, tw the table of make_twiddles(n).  Returns the buffer that holds the result.
+// INV: the inverse transform, unnormalised.
+template <bool INV>
+__device__ double2 *fft_lds(double2 *a, double2 *b, const double2 *tw, int n, int nseq) {
   int ns = 1;
-  stage<7>(a, b, n, nseq, ns, sgn);
+  stage<7, INV>(a, b, tw, n, nseq, ns);
   __syncthreads();
   ns = 7;
   double2 *x = b, *y = a;
   int rest = n / 7;
   while (rest >= 4) {
-    stage<4>(x, y, n, nseq, ns, sgn);
+    stage<4, INV>(x, y, tw, n, nseq, ns);
     __syncthreads();
     ns *= 4;
     rest /= 4;
@@ -135,7 +166,7 @@ __device__ double2 *fft_lds(double2 *a, double2 *b, int n, int nseq, double sgn)
     y = t;
   }
   if (rest == 2) {
-    stage<2>(x, y, n, nseq, ns, sgn);
+    stage<2, INV>(x, y, tw, n, nseq, ns);
     __syncthreads();
     double2 *t = x;
     x = y;
@@ -157,9 +188,11 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_rows(const float *__restrict_
                                                         const float *__restrict__ cur, int H,
                                                         int W, PixWs ws) {
   __shared__ double2 buf[2][2 * kPcMaxN];
+  __shared__ double2 tw[kPcMaxN];
   const int y = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   const int hw = W / 2 + 1;
   const size_t plane = (size_t)H * W;
+  make_twiddles(tw, W);
   const float *fp = prev ? prev + (size_t)b * 3 * plane : nullptr;
   const float *fc = cur + (size_t)b * 3 * plane;
   for (int x = t; x < W; x += blockDim.x) {
@@ -168,7 +201,7 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_rows(const float *__restrict_
     buf[0][W + x] = make_double2(luma_at(fc, plane, off), 0.0);
   }
   __syncthreads();
-  const double2 *Z = fft_lds(buf[0], buf[1], W, 2, -1.0);
+  const double2 *Z = fft_lds<false>(buf[0], buf[1], tw, W, 2);
   double2 *sa = ws.sa + ((size_t)b * H + y) * hw;
   double2 *sb = ws.sb + ((size_t)b * H + y) * hw;
   for (int k = t; k < hw; k += blockDim.x) {
@@ -183,8 +216,10 @@ template <int MAXH, int CW, bool FWD>
 __global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) {
   constexpr int NS = FWD ? 2 * CW : CW;
   __shared__ double2 buf[2][NS * MAXH];
+  __shared__ double2 tw[MAXH];
   __shared__ double red[kPcThreads / 64];
   const int b = blockIdx.y, t = threadIdx.x;
+  make_twiddles(tw, H);
   const int hw = W / 2 + 1;
   const int c0 = blockIdx.x * CW;
   const int cw = min(CW, hw - c0);
@@ -199,7 +234,7 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) 
       buf[0][s * H + y] = v;
     }
     __syncthreads();
-    double2 *F = fft_lds(buf[0], buf[1], H, NS, -1.0);
+    double2 *F = fft_lds<false>(buf[0], buf[1], tw, H, NS);
     double mx = 0.0;
     for (int e = t; e < cw * H; e += blockDim.x) {
       const int c = e / H, ky = e - c * H;
@@ -237,7 +272,7 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) 
       buf[0][c * H + y] = v;
     }
     __syncthreads();
-    const double2 *G = fft_lds(buf[0], buf[1], H, NS, 1.0);
+    const double2 *G = fft_lds<true>(buf[0], buf[1], tw, H, NS);
     for (int e = t; e < cw * H; e += blockDim.x) {
       const int c = e / H, y = e - c * H;
       sa[(size_t)y * hw + c0 + c] = G[c * H + y];
@@ -249,10 +284,12 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) 
 __global__ __launch_bounds__(kPcThreads) void k_pc_rows_inv(int H, int W, PixWs ws,
                                                             double *__restrict__ resp) {
   __shared__ double2 buf[2][kPcMaxN];
+  __shared__ double2 tw[kPcMaxN];
   __shared__ double bv[kPcThreads / 64];
   __shared__ int bi[kPcThreads / 64];
   const int y = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   const int hw = W / 2 + 1;
+  make_twiddles(tw, W);
   const double2 *g = ws.sa + ((size_t)b * H + y) * hw;
   for (int k = t; k < W; k += blockDim.x) {
     double2 v;
@@ -265,7 +302,7 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_rows_inv(int H, int W, PixWs 
     buf[0][k] = v;
   }
   __syncthreads();
-  const double2 *R = fft_lds(buf[0], buf[1], W, 1, 1.0);
+  const double2 *R = fft_lds<true>(buf[0], buf[1], tw, W, 1);
   const double hwn = (double)H * (double)W;
   double best = -INFINITY;
   int arg = 0x7fffffff;
