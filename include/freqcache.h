@@ -163,6 +163,14 @@ typedef struct {
      so fc_layer_forward_trail recomputes all of them at every step; frame tokens never
      attend to them.  With M-RoPE their three positions are T + W span + u.  0: none. */
   int32_t trail_tokens;
+  /* Slot map (NULL: every row is stored at its own index).  Otherwise the first part of
+     a slot state of fc_slot_state_bytes(B, S) bytes (device, int32), set up by
+     fc_slot_map_init: row r of item b lives at pool row slot_map[b S + r] of the same
+     K and V arrays.  One state serves every layer of the item (all layers share the
+     reuse decisions), so all layers' caches point at the same state.  A reused token
+     then shares its source's pool row: fc_cache_update_layers moves no K/V bytes, it
+     updates the map (reference-counted pool rows, freed when no row maps to them). */
+  int32_t *slot_map;
 } fc_kv_cache;
 
 /* Library version string. */
@@ -246,19 +254,39 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
                           const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                           const uint8_t *reuse_mask, int32_t grid_w, int32_t B, void *stream);
 
-/* The remap of Sec. 4.1 / Eq. 4-2 for the caches of n_layers layers at once (one launch): kvs[l],
- * y_prev[l] and y_cur[l] (host arrays of n_layers entries, device pointers inside)
- * are layer l's cache and output buffers.  The layers share `layer`'s dimensions and
- * the caches' text_tokens, frame_tokens, window and head (all advanced to the same
- * step); otherwise FC_ERR_SHAPE.  Equivalent to fc_cache_update on each layer in
- * turn; a window of one frame (in-place overwrite) runs those per-layer calls.
- * The layers are copied concurrently, so no two layers' K, V or output buffers
- * may overlap (not checked). */
+/* The same remap as fc_cache_update for the caches of n_layers layers at once (Sec. 4.1 /
+ * Eq. 4-2): kvs[l], y_prev[l] and y_cur[l] (host arrays of n_layers entries, device
+ * pointers inside) are layer l's cache and output buffers.  The layers share `layer`'s
+ * dimensions and the caches' text_tokens, frame_tokens, window, head and trail_tokens
+ * (all advanced to the same step); otherwise FC_ERR_SHAPE.  No two layers' K, V or
+ * output buffers may overlap (not checked): the layers are copied concurrently.
+ *   y_prev, y_cur: both NULL moves no output rows (the layer calls read only the
+ *     recomputed rows of their inputs; skip them when the reused tokens' outputs are
+ *     not consumed), else as in fc_cache_update.
+ *   Slot-mapped caches (every kvs[l].slot_map the same state, else FC_ERR_INVALID_ARG):
+ *     no K/V row moves; the map of each item is updated once for all layers: the rows
+ *     of the frame that left the window release their pool rows, each reused token
+ *     maps to its source's pool row, each recomputed token takes a free pool row.
+ *   Otherwise equivalent to fc_cache_update on each layer in turn (a window of one frame,
+ *     an in-place overwrite, runs those per-layer calls). */
 fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_t n_layers,
                                  const fc_kv_cache *kvs, const uint16_t *const *y_prev,
                                  uint16_t *const *y_cur, const int32_t *shift,
                                  const uint8_t *reuse_mask, int32_t grid_w, int32_t B,
                                  void *stream);
+
+/* Bytes of the slot state of B items with S cache rows (S = T + W N + U): the map
+ * [B][S] (the slot_map pointer of fc_kv_cache points at its start), reference counts
+ * [B][S], a free list [B][S] and its tops [B], int32.  0 for B < 1, S < 1 or B S above
+ * 2^40. */
+size_t fc_slot_state_bytes(int32_t B, int32_t S);
+
+/* Sets up the slot state at kv->slot_map for kv's layout (every row at its own pool row,
+ * each frame pool row referenced once, no free row), e.g. with a fresh cache or after
+ * fc_cache_update_layers of another layout.  Stream-ordered; `layer` gives the row
+ * sizes the validation checks. */
+fc_status fc_slot_map_init(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                           int32_t B, void *stream);
 
 /* The partial-recompute decoder layer for B batch items.
  *   x_cur:         [B][N][d_model] bf16 layer input of the current frame's tokens;

@@ -155,7 +155,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->spec, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
-                  c->krot, c->pix};
+                  c->krot, c->pix, c->vlog};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -413,6 +413,8 @@ static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_ca
                     std::max({(long)L->d_model, (long)L->d_ffn, (long)L->n_heads * L->head_dim});
   if (wmax >= (1L << 32))
     return fail(FC_ERR_UNSUPPORTED, "%s: weight matrices of 2^32 or more elements", who);
+  if (kv->slot_map && S * (long)L->n_kv_heads * L->head_dim * 2 >= (1L << 32))
+    return fail(FC_ERR_UNSUPPORTED, "%s: a slot-mapped item's K or V rows must span less than 4 GiB", who);
   const long widest = std::max({(long)L->d_model, (long)L->d_ffn, (long)L->n_heads * L->head_dim});
   if ((long)B * kv->frame_tokens * widest >= (1L << 32))
     return fail(FC_ERR_CAPACITY, "%s: B*N*%ld activation elements exceed 2^32", who, widest);
@@ -477,6 +479,9 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
   if (st != FC_OK) return st;
   if (!y_prev || !y_cur || !shift || !reuse_mask)
     return fail(FC_ERR_INVALID_ARG, "fc_cache_update: null buffer");
+  if (kv->slot_map)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update: a slot-mapped cache is remapped once for all "
+                "layers by fc_cache_update_layers");
   if (y_prev == y_cur) return fail(FC_ERR_INVALID_ARG, "fc_cache_update: y_prev and y_cur alias");
   if (grid_w < 1 || kv->frame_tokens % grid_w)
     return fail(FC_ERR_SHAPE, "fc_cache_update: grid_w %d does not divide N=%d", grid_w,
@@ -495,18 +500,25 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
                                  const uint8_t *reuse_mask, int32_t grid_w, int32_t B,
                                  void *stream) {
   if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: null context");
-  if (n_layers < 1 || !kvs || !y_prev || !y_cur)
-    return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: n_layers %d or null arrays", n_layers);
+  if (n_layers < 1 || !kvs)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: n_layers %d or null cache array", n_layers);
+  if ((y_prev == nullptr) != (y_cur == nullptr))
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: y_prev and y_cur must both be given "
+                "or both be NULL");
   if (!shift || !reuse_mask)
     return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: null buffer");
   for (int l = 0; l < n_layers; ++l) {
     fc_status st = check_layer(ctx, layer, &kvs[l], B, "fc_cache_update_layers");
     if (st != FC_OK) return st;
-    if (!y_prev[l] || !y_cur[l] || y_prev[l] == y_cur[l])
+    if (y_prev && (!y_prev[l] || !y_cur[l] || y_prev[l] == y_cur[l]))
       return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d: null or aliased outputs", l);
     if (kvs[l].text_tokens != kvs[0].text_tokens || kvs[l].frame_tokens != kvs[0].frame_tokens ||
-        kvs[l].window != kvs[0].window || kvs[l].head != kvs[0].head)
+        kvs[l].window != kvs[0].window || kvs[l].head != kvs[0].head ||
+        kvs[l].trail_tokens != kvs[0].trail_tokens)
       return fail(FC_ERR_SHAPE, "fc_cache_update_layers: layer %d's cache layout or head differs", l);
+    if (kvs[l].slot_map != kvs[0].slot_map)
+      return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d's slot map differs from "
+                  "layer 0's (one map serves all layers)", l);
   }
   if (grid_w < 1 || kvs[0].frame_tokens % grid_w)
     return fail(FC_ERR_SHAPE, "fc_cache_update_layers: grid_w %d does not divide N=%d", grid_w,
@@ -517,6 +529,20 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
   if (st != FC_OK) return st;
   return fc::launch_cache_update_layers(ctx, *layer, n_layers, kvs, y_prev, y_cur, shift, reuse_mask,
                                         grid_w, B, reinterpret_cast<hipStream_t>(stream));
+}
+
+size_t fc_slot_state_bytes(int32_t B, int32_t S) { return fc::slot_state_bytes(B, S); }
+
+fc_status fc_slot_map_init(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
+                           int32_t B, void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_slot_map_init: null context");
+  fc_status st = check_layer(ctx, layer, kv, B, "fc_slot_map_init");
+  if (st != FC_OK) return st;
+  if (!kv->slot_map) return fail(FC_ERR_INVALID_ARG, "fc_slot_map_init: the cache has no slot map");
+  if (kv->frame_tokens > fc::kMaxTokens)
+    return fail(FC_ERR_UNSUPPORTED, "fc_slot_map_init: N=%d > %d", kv->frame_tokens, fc::kMaxTokens);
+  if ((st = use_device(ctx)) != FC_OK) return st;
+  return fc::launch_slot_init(ctx, *kv, B, reinterpret_cast<hipStream_t>(stream));
 }
 
 int32_t fc_debug(int32_t on) {

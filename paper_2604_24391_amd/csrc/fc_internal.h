@@ -83,6 +83,8 @@ struct fc_ctx {
   size_t krot_elems = 0;
   unsigned char *pix = nullptr;  // pixel phase-correlation workspace, allocated at first use
   size_t pix_bytes = 0;
+  uint16_t *vlog = nullptr;     // [B][S][kv row] values in row order (slot-mapped caches,
+  size_t vlog_elems = 0;        // many-row layer calls only), allocated at first use
   // kernel timing
   bool prof = false;
   std::string prof_only;       // empty: time every kernel
@@ -165,6 +167,27 @@ fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
                                 const float *cur, int B, int H, int W,
                                 const fc_select_out &out, hipStream_t st);
 size_t noalloc_scratch_bytes();
+
+// Slot-map state of B items with S cache rows (slotmap.hip): map [B][S], ref [B][S],
+// free [B][S], top [B], int32, in that order.
+struct SlotState {
+  int32_t *map, *ref, *free, *top;
+};
+__host__ __device__ inline SlotState slot_state_at(int32_t *base, long B, long S) {
+  return SlotState{base, base + B * S, base + 2 * B * S, base + 3 * B * S};
+}
+size_t slot_state_bytes(long B, long S);
+fc_status launch_slot_init(fc_ctx *ctx, const fc_kv_cache &kv, int B, hipStream_t st);
+// The step's map update for all layers sharing kv.slot_map (window already advanced).
+fc_status launch_slot_remap(fc_ctx *ctx, const fc_kv_cache &kv, const int32_t *shift,
+                            const uint8_t *reuse, int grid_w, int B, hipStream_t st);
+// Pool row of cache row r of item b: the map's entry (clamped into the item's rows), or
+// r itself without a map.
+__device__ __forceinline__ int pool_row(const int32_t *map, int b, int S, int r) {
+  if (!map) return r;
+  const int p = map[(long)b * S + r];
+  return p < 0 ? 0 : (p >= S ? S - 1 : p);
+}
 
 // trail: recompute the text rows after the frames instead of the selected frame tokens
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,

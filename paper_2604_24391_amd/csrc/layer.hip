@@ -447,6 +447,7 @@ struct RedArgs {
   const uint16_t *bias;           // [ncols] (QKV)
   const uint16_t *gain;           // [d] MLP RMSNorm gain (O reduction)
   uint16_t *q, *kc, *vc;          // QKV outputs
+  const int32_t *smap;            // slot map of the K/V rows (null: rows in place)
   float *h1;                      // [B*N][d]
   uint16_t *hb;                   // [B*N][d] bf16(h1 * g_mlp), the SwiGLU operand
   float *ssq;                     // [B*N][chunks] sums of squares of h1 per 1024 columns
@@ -591,9 +592,10 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   if (c < r.qw)
     dst = r.q + slot * r.qw + c;
   else if (c < r.qw + r.kw)
-    dst = r.kc + ((long)b * r.S + r.cur_row0 + tok) * r.kw + (c - r.qw);
+    dst = r.kc + ((long)b * r.S + pool_row(r.smap, b, r.S, r.cur_row0 + tok)) * r.kw + (c - r.qw);
   else
-    dst = r.vc + ((long)b * r.S + r.cur_row0 + tok) * r.kw + (c - r.qw - r.kw);
+    dst = r.vc + ((long)b * r.S + pool_row(r.smap, b, r.S, r.cur_row0 + tok)) * r.kw +
+          (c - r.qw - r.kw);
   *reinterpret_cast<uint2 *>(dst) = make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
 }
 
@@ -830,7 +832,7 @@ __device__ __forceinline__ void mg_epi_rows8(const MArgs &a, const int *pre, Row
         }
         dst = r.q + slot[it] * r.qw + col;
       } else {
-        const long crow = (long)bi[it] * r.S + r.cur_row0 + tok[it];
+        const long crow = (long)bi[it] * r.S + pool_row(r.smap, bi[it], r.S, r.cur_row0 + tok[it]);
         dst = col < r.qw + r.kw ? r.kc + crow * r.kw + (col - r.qw)
                                 : r.vc + crow * r.kw + (col - r.qw - r.kw);
       }
@@ -1105,6 +1107,7 @@ __global__ __launch_bounds__(512) void k_mtail(MArgs a) {
 struct AttnArgs {
   const uint16_t *q;          // [B*N][nh*HD], rotated at the query's position
   const uint16_t *kc, *vc;    // [B][S][nkv][HD]
+  const int32_t *smap;        // slot map of the K/V rows (null: rows in place)
   const float2 *rope;         // [S][HD/2] (cos, sin)
   const int32_t *idx, *nrec;
   int N, nh, nkv, S, T, W, head;
@@ -1205,6 +1208,9 @@ __device__ __forceinline__ int vq_word(int kg, int hd) {
 // multiplied, so the cache latency is paid once per split and the staging ALU work
 // runs beside the MFMAs.
 constexpr int kAttnStageWaves = 4;
+// Slot-mapped caches: the pool rows of a workgroup's key range are staged in LDS (at
+// most this many rows per key split); only the four-staging-wave variants take a map.
+constexpr int kAttnMapRows = 4096;
 template <int HD, int G, bool ROT, int QB, int SW>
 __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 16;   // k-steps of the QK^T product
@@ -1223,6 +1229,7 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) __bf16 Ks[2][32 * HD];
   __shared__ __attribute__((aligned(16))) uint2 Vq[2][8 * HD];
   __shared__ int kpos[2][32];
+  __shared__ int rmap[SW > 1 ? kAttnMapRows : 1];
 
   // 1-D grid; the query tiles of one (kv head, key split) are consecutive logical
   // tiles, which xcd_tile places on one XCD, so each XCD's L2 holds only its own
@@ -1272,16 +1279,25 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
     for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
     if (lane == 0) tile_tok_max = v;
   }
+  // slot-mapped caches: the pool row of every row of the split's key range
+  const bool mapped = SW > 1 && a.smap != nullptr;
+  const int m0 = kb0 * 32;
+  const int m1 = min(kb1 * 32, a.S);          // rows [m0, m1) are staged
+  if (mapped) {
+    for (int r = t; r < m1 - m0; r += blockDim.x) rmap[r] = pool_row(a.smap, b, a.S, m0 + r);
+  }
   __syncthreads();
   int s0 = (cur_lo + tile_tok_max + 1 + 31) / 32, s1 = min(cur_hi, a.S) / 32;
   s0 = max(s0, kb0);
   s1 = min(s1, kb1);
   if (s1 < s0) s1 = s0;
   const int nb = (kb1 - kb0) - (s1 - s0);
-  auto blk = [&](int i) {                 // block of loop index i (clamped to the last)
+  // block of loop index i (clamped to the last); a split with no block left (nb = 0)
+  // still prefetches one block of its own range, never multiplied
+  auto blk = [&](int i) {
     i = max(min(i, nb - 1), 0);
     const int k = kb0 + i;
-    return min(k >= s0 ? k + (s1 - s0) : k, nkb - 1);
+    return min(min(k >= s0 ? k + (s1 - s0) : k, kb1 - 1), nkb - 1);
   };
 
   if (!qwave) {
@@ -1336,15 +1352,17 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
       // read its last row (lim, relative to the block) again and are never multiplied
       const int lim = S - 1 - rb;
       const uint32_t lim_off = (uint32_t)(lim * kvrow * 2);
-      const unsigned char *kblk = uniform_ptr(a.kc + kvbase + (long)rb * kvrow);
-      const unsigned char *vblk = uniform_ptr(a.vc + kvbase + (long)rb * kvrow);
+      // (slot-mapped: the item's first row as base, each row's pool row as offset)
+      const unsigned char *kblk = uniform_ptr(a.kc + kvbase + (mapped ? 0L : (long)rb * kvrow));
+      const unsigned char *vblk = uniform_ptr(a.vc + kvbase + (mapped ? 0L : (long)rb * kvrow));
 #pragma unroll
       for (int i = 0; i < TPT; ++i) {
         const int row0 = rb + key[i];
         const int row = min(row0, S - 1);
         const int pos = uniform_pos ? row + delta : key_pos(row, a.T, a.fN, a.W, a.head);
         R[i].pos = row0 < S ? pos : 0x7fffffff;
-        const uint32_t ko = key[i] <= lim ? koff[i] : lim_off + 16 * c[i];
+        const uint32_t ko = mapped ? (uint32_t)(rmap[min(row, m1 - 1) - m0] * kvrow * 2 + 16 * c[i])
+                                   : (key[i] <= lim ? koff[i] : lim_off + 16 * c[i]);
         R[i].k1 = kv_load16s(kblk, ko);
         R[i].k2 = kv_load16s(kblk, ko + HD);
         if (ROT) {
@@ -1355,7 +1373,9 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
         // every asm load is unconditional (no register set chosen at run time)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const uint32_t vo = 4 * kg[i] + r <= lim ? voff[i][r] : lim_off + 8 * lq[i];
+          const uint32_t vo =
+              mapped ? (uint32_t)(rmap[min(rb + 4 * kg[i] + r, m1 - 1) - m0] * kvrow * 2 + 8 * lq[i])
+                     : (4 * kg[i] + r <= lim ? voff[i][r] : lim_off + 8 * lq[i]);
           R[i].v[r] = kv_load8s(vblk, vo);
         }
       }
@@ -1616,11 +1636,16 @@ __global__ __launch_bounds__((G + SW) * 64) void k_attn(AttnArgs a) {
 // cache -> rotated copy (same rounding as when the attention kernel rotates on load).
 // For many query tiles per item this replaces one rotation per (key, tile) by one per
 // key.  One thread per 8-dim pair of chunks (dims 8c.. and hd/2 + 8c..) of a key row.
+// Slot-mapped caches (smap): keys are read from their pool rows and written in row
+// order, and the values are gathered into vr in row order too, so that the attention
+// kernel reads both without the map.
 __global__ __launch_bounds__(256) void k_rot_keys(const uint16_t *__restrict__ kc,
                                                   const float2 *__restrict__ rope,
                                                   uint16_t *__restrict__ kr, int S, int nkv,
                                                   int hd, int T, int N, int W, int head,
-                                                  MRope mr) {
+                                                  MRope mr, const int32_t *__restrict__ smap,
+                                                  const uint16_t *__restrict__ vc,
+                                                  uint16_t *__restrict__ vr) {
   const int cpr = hd / 16;                              // chunk pairs per head row
   const long task = (long)blockIdx.x * 256 + threadIdx.x;
   const int b = blockIdx.y;
@@ -1630,8 +1655,15 @@ __global__ __launch_bounds__(256) void k_rot_keys(const uint16_t *__restrict__ k
   const int row = (int)(rh / nkv);
   const int pos = key_pos(row, T, N, W, head);
   const long off = ((long)b * S * nkv + rh) * hd + 8 * c;
-  const U16x8 x1 = *reinterpret_cast<const U16x8 *>(kc + off);
-  const U16x8 x2 = *reinterpret_cast<const U16x8 *>(kc + off + hd / 2);
+  const long src = smap ? ((long)b * S + pool_row(smap, b, S, row)) * nkv * hd +
+                              (rh - (long)row * nkv) * hd + 8 * c
+                        : off;
+  const U16x8 x1 = *reinterpret_cast<const U16x8 *>(kc + src);
+  const U16x8 x2 = *reinterpret_cast<const U16x8 *>(kc + src + hd / 2);
+  if (vr) {
+    *reinterpret_cast<U16x8 *>(vr + off) = *reinterpret_cast<const U16x8 *>(vc + src);
+    *reinterpret_cast<U16x8 *>(vr + off + hd / 2) = *reinterpret_cast<const U16x8 *>(vc + src + hd / 2);
+  }
   const float2 *rp = rope + (long)rope_pos(mr, pos, 8 * c) * (hd / 2) + 8 * c;
   U16x8 y1, y2;
 #pragma unroll
@@ -1741,13 +1773,20 @@ struct CacheArgs {
   const int32_t *shift;
   const uint8_t *reuse;
   int N, S, kvw, d, gw, gh, cur_row0;
+  int kv_copy;                   // 0: K/V rows are not moved (slot-mapped caches)
+  int y_copy;                    // 0: output rows are not moved
 };
+
+// Chunks of 16 B the remap moves per reused token.
+__host__ __device__ inline int cache_chunks(const CacheArgs &c) {
+  return (c.kv_copy ? 2 * (c.kvw / 8) : 0) + (c.y_copy ? c.d / 8 : 0);
+}
 
 // One thread per 16-B chunk of a reused token's K row, V row and output row, so that
 // every copy of the remap is in flight at once.
 __device__ __forceinline__ void cache_copy(const CacheArgs &c) {
   const int b = blockIdx.y;
-  const int kc = c.kvw / 8, cpt = 2 * kc + c.d / 8;             // chunks per token
+  const int kc = c.kv_copy ? c.kvw / 8 : 0, cpt = cache_chunks(c);   // chunks per token
   const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
   const int tok = (int)(e / cpt);
   if (tok >= c.N) return;
@@ -1956,7 +1995,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   //    stores rotated q and scatters raw k, v
   {
     r.ncols = qkv;
-    r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v;
+    r.bias = L.b_qkv; r.q = ctx->qbuf; r.kc = kv.k; r.vc = kv.v; r.smap = kv.slot_map;
     if (big) {
       {
         ProfScope ps(ctx, st, "fc_gather_norm");
@@ -1985,7 +2024,7 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   {
     AttnArgs a{};
     a.q = ctx->qbuf;
-    a.kc = kv.k; a.vc = kv.v;
+    a.kc = kv.k; a.vc = kv.v; a.smap = kv.slot_map;
     a.rope = ctx->rope;
     a.mr = mr;
     a.idx = idx; a.nrec = nrec;
@@ -1999,7 +2038,18 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     int splits = std::max(1, std::min(kMaxAttnSplits, (2 * want) / (tiles * nkv)));
     splits = std::min(splits, std::max(1, nkb / 4));
     const size_t prow = (size_t)tiles * 32;           // query rows padded to whole tiles
-    while (splits > 1 && (size_t)splits * prow * nh * (hd + 2) > ctx->part_elems) --splits;
+    // with many query tiles per item, every cached key is rotated once into a copy
+    // instead of once per (key, tile) inside the attention kernel
+    const long kvw = (long)nkv * hd;
+    const bool prerot = big && ctx->krot && (size_t)B * S * kvw <= ctx->krot_elems;
+    // a slot map read by the attention kernel itself: at most kAttnMapRows rows per split
+    const bool map_in_attn = kv.slot_map && !prerot;
+    const int min_splits = map_in_attn ? (nkb * 32 + kAttnMapRows - 1) / kAttnMapRows : 1;
+    splits = std::max(splits, min_splits);
+    while (splits > min_splits && (size_t)splits * prow * nh * (hd + 2) > ctx->part_elems) --splits;
+    if (splits > kMaxAttnSplits || (splits > 1 && (size_t)splits * prow * nh * (hd + 2) > ctx->part_elems))
+      return fail(FC_ERR_UNSUPPORTED, "attention: a slot-mapped cache of %d rows needs %d key "
+                  "splits, more than the workspace holds", S, splits);
     a.kb_per_split = (nkb + splits - 1) / splits;
     a.splits = (nkb + a.kb_per_split - 1) / a.kb_per_split;
     a.po = ctx->part;
@@ -2007,18 +2057,33 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
     a.pl = a.pm + (size_t)a.splits * prow * nh;
     const int G = nh / nkv;
     a.tiles = tiles;
-    // with many query tiles per item, every cached key is rotated once into a copy
-    // instead of once per (key, tile) inside the attention kernel
-    const long kvw = (long)nkv * hd;
-    const bool prerot = big && ctx->krot && (size_t)B * S * kvw <= ctx->krot_elems;
     if (prerot) {
+      // slot-mapped: the values are gathered into row order beside the rotated keys
+      uint16_t *vr = nullptr;
+      if (kv.slot_map) {
+        if (!ctx->vlog) {
+          hipError_t e = hipMalloc(reinterpret_cast<void **>(&ctx->vlog),
+                                   ctx->krot_elems * sizeof(uint16_t));
+          if (e != hipSuccess) {
+            ctx->vlog = nullptr;
+            return fail(FC_ERR_HIP, "hipMalloc(slot-mapped values, %zu bytes): %s",
+                        ctx->krot_elems * sizeof(uint16_t), hipGetErrorString(e));
+          }
+          ctx->vlog_elems = ctx->krot_elems;
+        }
+        vr = ctx->vlog;
+      }
       ProfScope ps(ctx, st, "fc_rot_keys");
       const long tasks = (long)S * nkv * (hd / 16);
       hipLaunchKernelGGL(k_rot_keys, dim3((unsigned)((tasks + 255) / 256), B), dim3(256), 0, st,
                          kv.k, ctx->rope, ctx->krot, S, nkv, hd, kv.text_tokens, FN, kv.window,
-                         kv.head, mr);
+                         kv.head, mr, kv.slot_map, kv.v, vr);
       FC_LAUNCH_OK(st, "k_rot_keys");
       a.kc = ctx->krot;
+      if (vr) {
+        a.vc = vr;
+        a.smap = nullptr;
+      }
     }
     {
       ProfScope ps(ctx, st, "fc_attn");
@@ -2126,6 +2191,8 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
   c.gw = grid_w;
   c.gh = N / grid_w;
   c.cur_row0 = kv.text_tokens + cur_slot * N;
+  c.kv_copy = 1;
+  c.y_copy = y_prev != nullptr;
   if (kv.window == 1) {
     // the current frame overwrites the previous one in place: stage the old rows
     const long per = (long)N * kvw;
@@ -2153,7 +2220,7 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
     c.src_row0 = kv.text_tokens + prev_slot * N;
   }
   ProfScope ps(ctx, st, "fc_cache_update");
-  const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
+  const long chunks = (long)N * cache_chunks(c);
   hipLaunchKernelGGL(k_cache_update, dim3((unsigned)((chunks + 255) / 256), B), dim3(256), 0, st, c);
   FC_LAUNCH_OK(st, "k_cache_update");
   return FC_OK;
@@ -2164,11 +2231,16 @@ fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_
                                      uint16_t *const *y_cur, const int32_t *shift,
                                      const uint8_t *reuse, int grid_w, int B, hipStream_t st) {
   const fc_kv_cache &kv = kvs[0];
-  if (kv.window == 1) {
+  const bool ycopy = y_prev != nullptr;
+  if (kv.slot_map) {
+    // one map for all layers: the reused rows are shared, no K/V byte moves
+    fc_status s = launch_slot_remap(ctx, kv, shift, reuse, grid_w, B, st);
+    if (s != FC_OK || !ycopy) return s;
+  } else if (kv.window == 1) {
     // in-place overwrite of the only frame slot: the per-layer path stages the old rows
     for (int l = 0; l < n_layers; ++l) {
-      fc_status s = launch_cache_update(ctx, L, kvs[l], y_prev[l], y_cur[l], shift, reuse, grid_w,
-                                        B, st);
+      fc_status s = launch_cache_update(ctx, L, kvs[l], ycopy ? y_prev[l] : nullptr,
+                                        ycopy ? y_cur[l] : nullptr, shift, reuse, grid_w, B, st);
       if (s != FC_OK) return s;
     }
     return FC_OK;
@@ -2191,15 +2263,17 @@ fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_
   c.cur_row0 = kv.text_tokens + cur_slot * N;
   c.src_bstride = (long)S * kvw;
   c.src_row0 = kv.text_tokens + prev_slot * N;
+  c.kv_copy = kv.slot_map == nullptr;
+  c.y_copy = ycopy;
   ProfScope ps(ctx, st, "fc_cache_update");
-  const long chunks = (long)N * (2 * (kvw / 8) + L.d_model / 8);
+  const long chunks = (long)N * cache_chunks(c);
   for (int l0 = 0; l0 < n_layers; l0 += kCacheLayers) {
     const int nl = std::min(kCacheLayers, n_layers - l0);
     for (int i = 0; i < nl; ++i) {
       m.kc[i] = kvs[l0 + i].k;
       m.vc[i] = kvs[l0 + i].v;
-      m.yp[i] = y_prev[l0 + i];
-      m.yc[i] = y_cur[l0 + i];
+      m.yp[i] = ycopy ? y_prev[l0 + i] : nullptr;
+      m.yc[i] = ycopy ? y_cur[l0 + i] : nullptr;
     }
     hipLaunchKernelGGL(k_cache_update_layers, dim3((unsigned)((chunks + 255) / 256), B, nl),
                        dim3(256), 0, st, m);

@@ -31,7 +31,7 @@ FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
            "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
-           "fc_phase_correlate",
+           "fc_phase_correlate", "fc_slot_state_bytes", "fc_slot_map_init",
            "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
 
@@ -71,7 +71,8 @@ class fc_layer_desc(ctypes.Structure):
 class fc_kv_cache(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("text_tokens", c_int32),
                 ("frame_tokens", c_int32), ("window", c_int32), ("head", c_int32),
-                ("grid_w", c_int32), ("mrope_section", c_int32 * 3), ("trail_tokens", c_int32)]
+                ("grid_w", c_int32), ("mrope_section", c_int32 * 3), ("trail_tokens", c_int32),
+                ("slot_map", c_void_p)]
 
 
 _lib = None
@@ -115,6 +116,10 @@ def lib() -> ctypes.CDLL:
                                              c_int32, c_void_p]
         L.fc_phase_correlate.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fc_slot_state_bytes.argtypes = [c_int32, c_int32]
+        L.fc_slot_state_bytes.restype = ctypes.c_size_t
+        L.fc_slot_map_init.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
+                                       ctypes.POINTER(fc_kv_cache), c_int32, c_void_p]
         L.fc_debug.argtypes = [c_int32]
         L.fc_debug.restype = c_int32
         L.fc_profile_enable.argtypes = [c_void_p, c_int32]
@@ -123,7 +128,8 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
                   "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward",
-                  "fc_layer_forward_trail", "fc_phase_correlate", "fc_profile_enable",
+                  "fc_layer_forward_trail", "fc_phase_correlate", "fc_slot_map_init",
+                  "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
         _lib = L
@@ -421,6 +427,9 @@ class KVCache:
     grid_w: int = 0
     mrope: tuple = (0, 0, 0)
     trail_tokens: int = 0      # text tokens after the frames (recomputed every step)
+    # slot state (slot_state_alloc) shared by every layer of the items, or None: rows
+    # stored at their own index
+    slot_map: torch.Tensor | None = None
 
     @property
     def S(self) -> int:
@@ -434,7 +443,16 @@ class KVCache:
         n = B * self.S * kvw
         return fc_kv_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
                            self.text_tokens, self.frame_tokens, self.window, self.head,
-                           self.grid_w, (c_int32 * 3)(*self.mrope), self.trail_tokens)
+                           self.grid_w, (c_int32 * 3)(*self.mrope), self.trail_tokens,
+                           _ptr(self.slot_map, torch.int32, B * self.S, "slot_map")
+                           if self.slot_map is not None else c_void_p(0))
+
+    def logical(self, t: torch.Tensor, B: int) -> torch.Tensor:
+        """k or v in row order: rows gathered through the slot map (t itself without one)."""
+        if self.slot_map is None:
+            return t
+        m = self.slot_map[:B * self.S].view(B, self.S).long()
+        return torch.stack([t[b].index_select(0, m[b]) for b in range(B)])
 
 
 def fc_layer_forward(ctx: Context, layer: LayerDesc, kv: KVCache, x_cur: torch.Tensor,
@@ -491,19 +509,46 @@ def fc_cache_update_layers(ctx: Context, layer: LayerDesc, kvs, y_prevs, y_curs,
     kvs, y_prevs, y_curs: equal-length sequences (one entry per layer); the caches
     share their layout and have all been advanced to the same step."""
     n = len(kvs)
-    if n < 1 or len(y_prevs) != n or len(y_curs) != n:
+    if (y_prevs is None) != (y_curs is None):
+        raise ValueError("fc_cache_update_layers: give both y_prevs and y_curs or neither")
+    if n < 1 or (y_prevs is not None and (len(y_prevs) != n or len(y_curs) != n)):
         raise ValueError("fc_cache_update_layers: kvs, y_prevs and y_curs need one entry per layer")
-    B = y_curs[0].shape[0]
+    B = reuse_mask.shape[0]
     N, d = kvs[0].frame_tokens, layer.d_model
     kvw = layer.n_kv_heads * layer.head_dim
     cl = layer.c()
     cks = (fc_kv_cache * n)(*[kv.c(B, kvw) for kv in kvs])
-    yp = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_prev") for y in y_prevs])
-    yc = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_cur") for y in y_curs])
+    if y_prevs is None:
+        yp = yc = None
+    else:
+        yp = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_prev") for y in y_prevs])
+        yc = (c_void_p * n)(*[_ptr(y, torch.bfloat16, B * N * d, "y_cur") for y in y_curs])
     _check(lib().fc_cache_update_layers(
         ctx.handle, ctypes.byref(cl), n, cks, yp, yc,
         _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
+
+
+def slot_state_bytes(B: int, S: int) -> int:
+    return int(lib().fc_slot_state_bytes(B, S))
+
+
+def slot_state_alloc(B: int, S: int, device="cuda") -> torch.Tensor:
+    """A slot state for B items of S cache rows (int32; set it up with fc_slot_map_init)."""
+    n = slot_state_bytes(B, S)
+    if n == 0:
+        raise ValueError("slot_state_alloc: B and S must be positive")
+    return torch.empty(n // 4, dtype=torch.int32, device=device)
+
+
+def fc_slot_map_init(ctx: Context, layer: LayerDesc, kv: KVCache, B: int, stream=None):
+    """Every row at its own pool row (the state that kv.slot_map points at)."""
+    if kv.slot_map is None:
+        raise ValueError("fc_slot_map_init: the cache has no slot map")
+    cl = layer.c()
+    ck = kv.c(B, layer.n_kv_heads * layer.head_dim)
+    _check(lib().fc_slot_map_init(ctx.handle, ctypes.byref(cl), ctypes.byref(ck), B,
+                                  _stream(stream)))
 
 
 # ------------------------------------------------------------------------------ timing

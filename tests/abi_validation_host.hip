@@ -300,6 +300,39 @@ int main() {
     EXPECT(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr),
            FC_ERR_INVALID_ARG);
   }
+  {
+    // slot-mapped caches
+    int32_t *smap = i32;
+    fc_kv_cache mk = kv;
+    mk.slot_map = smap;
+    uint16_t *y2 = h16 + 8;
+    EXPECT(fc_cache_update(ctx, &L, &mk, h16, y2, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
+    fc_kv_cache kvs[2] = {mk, mk};
+    const uint16_t *yp[2] = {h16, h16};
+    uint16_t *yc[2] = {y2, y2};
+    EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 2, kvs, yp, yc, i32, u8, 16, 1, nullptr));
+    EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 2, kvs, nullptr, nullptr, i32, u8, 16, 1,
+                                              nullptr));
+    EXPECT(fc_cache_update_layers(ctx, &L, 2, kvs, yp, nullptr, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+    kvs[1].slot_map = nullptr;
+    EXPECT(fc_cache_update_layers(ctx, &L, 2, kvs, yp, yc, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+    kvs[1] = mk;
+    kvs[1].trail_tokens = 8;
+    EXPECT(fc_cache_update_layers(ctx, &L, 2, kvs, yp, yc, i32, u8, 16, 1, nullptr), FC_ERR_SHAPE);
+    EXPECT(fc_slot_map_init(ctx, &L, &kv, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_slot_map_init(nullptr, &L, &mk, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_slot_map_init(ctx, &L, &mk, 0, nullptr), FC_ERR_SHAPE);
+    EXPECT_DEVICE_FAIL(fc_slot_map_init(ctx, &L, &mk, 1, nullptr));
+    EXPECT_DEVICE_FAIL(fwd(L, mk, 1));
+    if (fc_slot_state_bytes(0, 10) != 0 || fc_slot_state_bytes(1, -1) != 0 ||
+        fc_slot_state_bytes(2, 100) != (3 * 2 * 100 + 2) * 4) {
+      std::printf("FAIL: slot state bytes\n");
+      ++g_fail;
+    }
+    (void)fc_slot_state_bytes(INT_MAX, INT_MAX);
+  }
   EXPECT(fc_profile_enable(nullptr, 1), FC_ERR_INVALID_ARG);
   EXPECT(fc_profile_only(nullptr, "k"), FC_ERR_INVALID_ARG);
   {

@@ -34,9 +34,27 @@ def fc():
     return fc
 
 
+def check_slot_state(state, S, T, WN):
+    """Invariants of a slot state after a step: text and trailing rows in place, frame
+    rows on frame pool rows, every reference counted, the free list exactly the frame
+    pool rows nobody maps to."""
+    st = state.cpu().numpy()
+    mp, ref, fre, top = st[:S], st[S:2 * S], st[2 * S:3 * S], int(st[3 * S])
+    rows = np.arange(S)
+    frame = (rows >= T) & (rows < T + WN)
+    np.testing.assert_array_equal(mp[~frame], rows[~frame])
+    assert ((mp[frame] >= T) & (mp[frame] < T + WN)).all()
+    cnt = np.bincount(mp[frame], minlength=S)
+    np.testing.assert_array_equal(ref[T:T + WN], cnt[T:T + WN])
+    free = np.sort(fre[:top])
+    np.testing.assert_array_equal(free, np.flatnonzero(cnt[T:T + WN] == 0) + T)
+
+
 def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, log=print,
-              mrope=(0, 0, 0), U=0):
+              mrope=(0, 0, 0), U=0, slot=False, no_y=False):
     """Run `steps` episode steps on both sides and compare after every checked step.
+    slot: the GPU caches are slot-mapped (one state for all layers); no_y: the GPU
+    remap moves no output rows (only the recomputed rows of y are compared).
     Returns the per-step recompute counts."""
     F, _, H, Wpx = frames.shape
     m = prm.merge
@@ -53,6 +71,7 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
     frames_gpu = torch.from_numpy(np.ascontiguousarray(frames)).cuda()
     sel = fc.SelectOut.alloc(1, N)
     states = [fc.select_state_alloc(1, H, Wpx), fc.select_state_alloc(1, H, Wpx)]
+    slot_state = fc.slot_state_alloc(1, S) if slot else None
 
     # seeded start: random caches and output buffers per layer, identical on both sides
     gpu, ora = [], []
@@ -63,7 +82,7 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         k0, v0 = fcdata.text_kv(seed + 200 + li, shape, S)
         y0 = fcdata.bf16_round(rng.standard_normal((2, N, shape.d), dtype=np.float32))
         kv = fc.KVCache(fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(v0[None]), T, N, W, head=0,
-                        grid_w=gw, mrope=tuple(mrope), trail_tokens=U)
+                        grid_w=gw, mrope=tuple(mrope), trail_tokens=U, slot_map=slot_state)
         gpu.append(dict(desc=fcutil.layer_desc(shape, fcutil.weights_gpu(wt)), kv=kv,
                         y=[fcutil.bf16_gpu(y0[0][None]), fcutil.bf16_gpu(y0[1][None])],
                         yt=torch.empty((1, U, shape.d), dtype=torch.bfloat16, device="cuda")
@@ -71,6 +90,8 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         ora.append(dict(wt={k: ol.f32(v).copy() for k, v in wt.items()}, k=ol.f32(k0).copy(),
                         v=ol.f32(v0).copy(), y=[ol.f32(y0[0]).copy(), ol.f32(y0[1]).copy()],
                         k0=k0, v0=v0, written=np.zeros(S, bool)))
+    if slot:
+        fc.fc_slot_map_init(ctx, gpu[0]["desc"], gpu[0]["kv"], 1)
     head, cur = 0, 0
     counts = []
     for s in range(steps):
@@ -83,7 +104,8 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         for g in gpu:
             g["kv"].advance()
         fc.fc_cache_update_layers(ctx, gpu[0]["desc"], [g["kv"] for g in gpu],
-                                  [g["y"][cur] for g in gpu], [g["y"][nxt] for g in gpu],
+                                  None if no_y else [g["y"][cur] for g in gpu],
+                                  None if no_y else [g["y"][nxt] for g in gpu],
                                   sel.shift, sel.reuse_mask, gw)
         x = emb_gpu[fi:fi + 1]
         xt = x_text_gpu
@@ -126,12 +148,16 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
         assert not esc, f"step {s}: {esc}"
         idx = res.recompute_idx
         worst = 0.0
+        if slot:
+            check_slot_state(slot_state, S, T, W * N)
         for li, (g, o) in enumerate(zip(gpu, ora)):
             yg = ol.f32(fcutil.bf16_np(g["y"][cur])[0])
-            kg = ol.f32(fcutil.bf16_np(g["kv"].k)[0])
-            vg = ol.f32(fcutil.bf16_np(g["kv"].v)[0])
+            kl = g["kv"].logical(g["kv"].k, 1)
+            vl = g["kv"].logical(g["kv"].v, 1)
+            kg = ol.f32(fcutil.bf16_np(kl)[0])
+            vg = ol.f32(fcutil.bf16_np(vl)[0])
             xg = ol.f32(fcutil.bf16_np(emb_gpu[fi:fi + 1] if li == 0 else gpu[li - 1]["y"][cur])[0])
-            e_y = fcutil.rel_l2(yg, o["y"][cur])
+            e_y = fcutil.rel_l2(yg, o["y"][cur]) if not no_y else 0.0
             e_rec = fcutil.rel_l2(yg[idx], o["y"][cur][idx]) if idx.size else 0.0
             e_res = fcutil.rel_l2((yg - xg)[idx], (o["y"][cur] - xs[li])[idx]) if idx.size else 0.0
             w = o["written"]
@@ -143,9 +169,9 @@ def run_chain(fc, ctx, shape, frames, prm, L, T, W, steps, seed, check_every=1, 
                 assert e <= fcutil.LAYER_RTOL, f"step {s} layer {li}: {name} rel-L2 {e:.3e}"
                 worst = max(worst, e)
             # rows nobody has written still hold their initial bytes
-            np.testing.assert_array_equal(fcutil.bf16_np(g["kv"].k)[0][~w], o["k0"][~w],
+            np.testing.assert_array_equal(fcutil.bf16_np(kl)[0][~w], o["k0"][~w],
                                           err_msg=f"step {s} layer {li}: unwritten K rows")
-            np.testing.assert_array_equal(fcutil.bf16_np(g["kv"].v)[0][~w], o["v0"][~w],
+            np.testing.assert_array_equal(fcutil.bf16_np(vl)[0][~w], o["v0"][~w],
                                           err_msg=f"step {s} layer {li}: unwritten V rows")
         log(f"[episode] step {s}: n_recompute {res.n_recompute}, shift {res.shift}, "
             f"worst rel-L2 {worst:.2e}")
@@ -232,3 +258,41 @@ def test_toy_chain_in_debug_mode(fc):
         ctx.close()
         fc.fc_debug(before)
     assert counts[0] == N
+
+
+@pytest.mark.parametrize("W,no_y", [(2, False), (1, False), (3, True)])
+def test_slot_mapped_toy_chain(fc, W, no_y):
+    """The toy chain on slot-mapped caches (one state for both layers): the remap moves
+    no K/V row, reused tokens share their source's pool row, and every step's caches in
+    row order match the oracle chain; the slot state stays consistent (references
+    counted, free list exact).  W = 1 reuses rows of the frame being replaced; no_y
+    leaves the output rows of reused tokens unmoved."""
+    shape = fcdata.TINY_LAYER
+    frames = fcdata.episode_frames(33, n_frames=7)
+    T, N = 32, 256
+    ctx = fc.Context(fc.Caps(max_batch=1, max_height=448, max_width=448, max_tokens=N,
+                             max_seq=T + W * N + 24, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    try:
+        counts = run_chain(fc, ctx, shape, frames, fc.SelectParams(merge=2), L=2, T=T, W=W,
+                           steps=7, seed=510 + W, U=24, slot=True, no_y=no_y)
+    finally:
+        ctx.close()
+    assert counts[0] == N and min(counts[1:]) < N
+
+
+def test_slot_mapped_qwen_episode(fc):
+    """The benchmark's episode workload (two Qwen2.5-VL-7B-shaped layers, multimodal RoPE,
+    8-frame window) on slot-mapped caches, 12 steps, every step compared."""
+    shape = fcdata.QWEN_LAYER
+    frames = fcdata.episode_frames(2024, size=448, n_frames=12)
+    T, W, N = 128, 8, 256
+    ctx = fc.Context(fc.Caps(max_batch=64, max_height=448, max_width=448, max_tokens=1024,
+                             max_seq=T + W * N, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    try:
+        counts = run_chain(fc, ctx, shape, frames, fc.SelectParams(merge=2), L=2, T=T, W=W,
+                           steps=12, seed=910, mrope=(16, 24, 24), slot=True)
+    finally:
+        ctx.close()
+    assert counts[0] == N and min(counts[1:]) < N

@@ -35,7 +35,8 @@ class Case:
     """Seeded inputs for one layer call, the oracle's cache from a full forward of
     [prefix; x_prev], and the GPU tensors."""
 
-    def __init__(self, shape, T, N, W, head, B, seed, wt=None, gw=0, mrope=(0, 0, 0)):
+    def __init__(self, shape, T, N, W, head, B, seed, wt=None, gw=0, mrope=(0, 0, 0),
+                 slot_seed=None):
         self.shape, self.B = shape, B
         self.lay = ol.Layout(T=T, N=N, W=W, head=head, gw=gw, mrope=tuple(mrope))
         self.wt = wt if wt is not None else fcdata.layer_weights(seed, shape)
@@ -53,6 +54,14 @@ class Case:
             self.y_prev[b] = fcdata.bf16_round(y[-N:])
             self.x_cur[b] = st["x_cur"]
         self.wgpu = fcutil.weights_gpu(self.wt)
+        # slot-mapped cache: each item's frame rows at a seeded permutation of the frame
+        # pool rows (text rows in place); the physical arrays hold row r at map[r]
+        self.smap = None
+        if slot_seed is not None:
+            rng = np.random.default_rng(slot_seed)
+            self.smap = np.tile(np.arange(S, dtype=np.int32), (B, 1))
+            for b in range(B):
+                self.smap[b, T:T + W * N] = T + rng.permutation(W * N).astype(np.int32)
 
     def run(self, fc, ctx, ids_per_item):
         B, N = self.B, self.lay.N
@@ -61,15 +70,28 @@ class Case:
         for b, ids in enumerate(ids_per_item):
             idx[b, :len(ids)] = ids
             nrec[b] = len(ids)
-        kc, vc = fcutil.bf16_gpu(self.k), fcutil.bf16_gpu(self.v)
+        S = self.lay.S
+        kp, vp, state = self.k, self.v, None
+        if self.smap is not None:
+            kp, vp = np.empty_like(self.k), np.empty_like(self.v)
+            for b in range(B):
+                kp[b][self.smap[b]] = self.k[b]
+                vp[b][self.smap[b]] = self.v[b]
+            state = fc.slot_state_alloc(B, S)
+            state[:B * S] = torch.from_numpy(self.smap.ravel()).cuda()
+        kc, vc = fcutil.bf16_gpu(kp), fcutil.bf16_gpu(vp)
         y = fcutil.bf16_gpu(self.y_prev)
         kv = fc.KVCache(kc, vc, self.lay.T, N, self.lay.W, self.lay.head, grid_w=self.lay.gw,
-                        mrope=self.lay.mrope)
+                        mrope=self.lay.mrope, slot_map=state)
         fc.fc_layer_forward(ctx, fcutil.layer_desc(self.shape, self.wgpu), kv,
                             fcutil.bf16_gpu(self.x_cur), torch.from_numpy(idx).cuda(),
                             torch.from_numpy(nrec).cuda(), y)
         torch.cuda.synchronize()
-        return fcutil.bf16_np(y), fcutil.bf16_np(kc), fcutil.bf16_np(vc)
+        k, v = fcutil.bf16_np(kc), fcutil.bf16_np(vc)
+        if self.smap is not None:
+            k = np.stack([k[b][self.smap[b]] for b in range(B)])
+            v = np.stack([v[b][self.smap[b]] for b in range(B)])
+        return fcutil.bf16_np(y), k, v
 
     def check(self, fc, ctx, ids_per_item):
         y, k, v = self.run(fc, ctx, ids_per_item)
@@ -127,6 +149,23 @@ def test_gqa_ring_layout_two_items(fc, ctx, head):
     items with different recompute counts (one ragged 32-row tile)."""
     c = Case(GQA_SMALL, T=16, N=64, W=3, head=head, B=2, seed=20 + head)
     c.check(fc, ctx, [fcdata.random_reuse_ids(5, 64, 25), fcdata.random_reuse_ids(6, 64, 75)])
+
+
+@pytest.mark.parametrize("head", [0, 2])
+def test_slot_mapped_gqa_ring_two_items(fc, ctx, head):
+    """The same on slot-mapped caches: every frame row at a seeded permutation of the
+    pool rows, so attention, the K/V scatter and the untouched rows all go through the
+    map (compared in row order)."""
+    c = Case(GQA_SMALL, T=16, N=64, W=3, head=head, B=2, seed=20 + head, slot_seed=90 + head)
+    c.check(fc, ctx, [fcdata.random_reuse_ids(5, 64, 25), fcdata.random_reuse_ids(6, 64, 75)])
+
+
+def test_slot_mapped_qwen_layer(fc, ctx):
+    """The Qwen2.5-VL-7B-shaped layer (2176 cached rows, multimodal RoPE) on a
+    slot-mapped cache at 50 % reuse."""
+    c = Case(fcdata.QWEN_LAYER, T=128, N=256, W=8, head=3, B=1, seed=41, gw=16,
+             mrope=QWEN_MROPE, slot_seed=95)
+    c.check(fc, ctx, [fcdata.random_reuse_ids(150, 256, 50)])
 
 
 def test_full_reuse_leaves_cache_untouched(fc, ctx):
@@ -376,6 +415,17 @@ def test_batch_path_mrope(fc, ctx_big):
     c = Case(GQA_SMALL, T=64, N=1024, W=2, head=1, B=2, seed=75, gw=32, mrope=QWEN_MROPE)
     worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(76, 1024, 40),
                                   fcdata.random_reuse_ids(77, 1024, 70)])
+    print(f"worst rel-L2 {worst:.2e}")
+
+
+def test_batch_path_slot_map(fc, ctx_big):
+    """The large-M path on slot-mapped caches (frame rows at seeded permutations of the
+    pool rows): keys rotated and values gathered through the map, the fused QKV
+    epilogue scattering into the mapped rows; two ragged items, multimodal RoPE."""
+    c = Case(GQA_SMALL, T=64, N=1024, W=2, head=1, B=2, seed=78, gw=32, mrope=QWEN_MROPE,
+             slot_seed=79)
+    worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(80, 1024, 40),
+                                  fcdata.random_reuse_ids(81, 1024, 85)])
     print(f"worst rel-L2 {worst:.2e}")
 
 
