@@ -173,6 +173,7 @@ def main():
     # the previous frame's spectra are carried from step to step (two state buffers)
     states = [fc.select_state_alloc(1, size, size), fc.select_state_alloc(1, size, size)]
     cur_y = 0
+    remap_y = [True]           # False: the remap moves no output rows (slot-map extra)
 
     def step(s):
         nonlocal cur_y
@@ -187,8 +188,9 @@ def main():
         for lay in layers:
             lay["kv"].advance()
         fc.fc_cache_update_layers(ctx, layers[0]["desc"], [lay["kv"] for lay in layers],
-                                  [lay["y"][cur_y] for lay in layers],
-                                  [lay["y"][nxt] for lay in layers], sel.shift, sel.reuse_mask, gw)
+                                  [lay["y"][cur_y] for lay in layers] if remap_y[0] else None,
+                                  [lay["y"][nxt] for lay in layers] if remap_y[0] else None,
+                                  sel.shift, sel.reuse_mask, gw)
         for lay in layers:
             fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], x, sel.recompute_idx,
                                 sel.n_recompute, lay["y"][nxt])
@@ -276,6 +278,8 @@ def main():
                 "NVIDIA A100 40GB, precision not stated; a different (whole-model) workload")
 
     if not args.no_extras:
+        result["slot_map"] = bench_slot_map(fc, ctx, torch, layers, step, remap_y,
+                                            args.warmup + args.steps + nb, args.steps, ms_step)
         result["select_batch"] = bench_select_batch(fc, ctx, torch)
         result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
         result["tiny"] = bench_tiny(fc, torch)
@@ -311,6 +315,53 @@ def main():
         del src, dst
     ctx.close()
     print(json.dumps(result), flush=True)
+
+
+def bench_slot_map(fc, ctx, torch, layers, step, remap_y, s0, steps, base_ms):
+    """The same episode step with the caches slot-mapped (one state for all layers: the
+    remap moves no K/V row), with and without the output-row remap, and the plain caches
+    without it; the per-step remap kernels from a separate pass with events."""
+    kv0 = layers[0]["kv"]
+    state = fc.slot_state_alloc(1, kv0.S)
+    for lay in layers:
+        lay["kv"].slot_map = state
+    fc.fc_slot_map_init(ctx, layers[0]["desc"], kv0, 1)
+    out = dict(workload="episode step, slot-mapped caches", base_ms_per_step=round(base_ms, 4))
+    s = s0
+
+    def timed(tag):
+        nonlocal s
+        for _ in range(4):
+            step(s)
+            s += 1
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(steps):
+            step(s)
+            s += 1
+        torch.cuda.synchronize()
+        out[tag] = round((time.perf_counter() - t) * 1e3 / steps, 4)
+        fc.fc_profile_read(ctx, None, reset=True)
+        fc.fc_profile_enable(ctx, True)
+        for _ in range(8):
+            step(s)
+            s += 1
+        torch.cuda.synchronize()
+        fc.fc_profile_enable(ctx, False)
+        for name in ("fc_cache_update", "fc_slot_remap", "fc_attn"):
+            tot, cnt = fc.fc_profile_read(ctx, name)
+            if cnt:
+                out[f"{tag}_{name}_us_per_step"] = round(tot * 1e3 / 8, 3)
+        fc.fc_profile_read(ctx, None, reset=True)
+
+    timed("slot_map_ms_per_step")
+    remap_y[0] = False
+    timed("slot_map_no_y_remap_ms_per_step")
+    for lay in layers:
+        lay["kv"].slot_map = None
+    timed("plain_no_y_remap_ms_per_step")
+    remap_y[0] = True
+    return out
 
 
 def calib_copy(torch, mib):
