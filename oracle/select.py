@@ -29,7 +29,10 @@ Readings where the paper is silent or garbled:
   * a missing previous frame is treated as an all-zero previous frame;
   * align_pixel (a Module I variant): F of Eq. 4-1 is the full-resolution luma,
     the integer peak is refined per axis by a three-point parabola, and the
-    displacement is rounded to whole tokens (halves away from zero).
+    displacement is rounded to whole tokens (halves away from zero);
+  * align_rotation (with align_pixel): the rotation comes first from Eq. 4-1 on
+    log-polar resampled, high-pass weighted magnitude spectra (Fourier-Mellin) and is
+    undone by bilinear resampling about the frame centre before the displacement.
 """
 from __future__ import annotations
 
@@ -56,6 +59,8 @@ class SelectParams:
     align: bool = True             # False: "w/o Module I", position-wise matching (Delta = 0)
     align_pixel: bool = False      # True: Eq. 4-1 on full-resolution luma, sub-pixel peak,
                                    # displacement rounded to whole tokens
+    align_rotation: bool = False   # with align_pixel: the current frame's rotation found
+                                   # and undone first (log-polar spectra)
     refresh: bool = True           # False: "w/o Module II", no high-frequency refresh
 
 
@@ -232,6 +237,78 @@ def token_shift(d_px: float, tp: int) -> int:
     return int(np.floor(q + 0.5)) * (1 if d_px >= 0 else -1)
 
 
+def highpass_weight(h: int, w: int) -> np.ndarray:
+    """High-pass emphasis of a magnitude spectrum before log-polar resampling:
+    (1 - X)(2 - X) with X = cos(pi f_u) cos(pi f_v), f the signed frequency in cycles per
+    sample (0 at DC, 2 at the Nyquist corners)."""
+    fu = np.fft.fftfreq(h)[:, None]
+    fv = np.fft.fftfreq(w)[None, :]
+    x = np.cos(np.pi * fu) * np.cos(np.pi * fv)
+    return (1.0 - x) * (2.0 - x)
+
+
+def bilinear(img: np.ndarray, y: np.ndarray, x: np.ndarray, wrap: bool) -> np.ndarray:
+    """Bilinear interpolation of img at (y, x); wrap: circular indices, otherwise 0
+    outside the image."""
+    h, w = img.shape
+    y0, x0 = np.floor(y).astype(np.int64), np.floor(x).astype(np.int64)
+    fy, fx = y - y0, x - x0
+    out = np.zeros(np.broadcast(y, x).shape)
+    for a, wa in ((0, 1.0 - fy), (1, fy)):
+        for b, wb in ((0, 1.0 - fx), (1, fx)):
+            yy, xx = y0 + a, x0 + b
+            if wrap:
+                v = img[yy % h, xx % w]
+            else:
+                ok = (yy >= 0) & (yy < h) & (xx >= 0) & (xx < w)
+                v = np.where(ok, img[np.clip(yy, 0, h - 1), np.clip(xx, 0, w - 1)], 0.0)
+            out = out + wa * wb * v
+    return out
+
+
+def log_polar(mag: np.ndarray, n_theta: int, n_rho: int) -> np.ndarray:
+    """Samples a (centrally symmetric) magnitude spectrum at angles theta_i = pi i / n_theta
+    and radii r_j = R^(j / n_rho), R = min(H, W) / 2 - 1, i.e. at frequency
+    (r sin theta, r cos theta) with circular indexing; bilinear."""
+    h, w = mag.shape
+    big_r = min(h, w) / 2.0 - 1.0
+    th = np.pi * np.arange(n_theta)[:, None] / n_theta
+    r = big_r ** (np.arange(n_rho)[None, :] / n_rho)
+    return bilinear(mag, r * np.sin(th), r * np.cos(th), wrap=True)
+
+
+def rotate_image(y: np.ndarray, angle: float) -> np.ndarray:
+    """y sampled at the points q rotated by `angle` about the image centre,
+    out(q) = y(R(angle) (q - c) + c) with (x', y') = (x cos a - y sin a, x sin a + y cos a)
+    in (column, row) coordinates; bilinear, 0 outside."""
+    h, w = y.shape
+    cy, cx = (h - 1) / 2.0, (w - 1) / 2.0
+    qy, qx = np.meshgrid(np.arange(h) - cy, np.arange(w) - cx, indexing="ij")
+    ca, sa = np.cos(angle), np.sin(angle)
+    return bilinear(y, qx * sa + qy * ca + cy, qx * ca - qy * sa + cx, wrap=False)
+
+
+def rotation_phase_correlation(y_prev: np.ndarray, y_cur: np.ndarray):
+    """Fourier-Mellin step of the pixel-resolution Module I: Eq. 4-1 on the log-polar
+    resampled, high-pass weighted magnitude spectra (n_theta = H angles over [0, pi),
+    n_rho = min(H, W) / 2 radii) gives the rotation of the current frame relative to the
+    previous one from the angular coordinate of the peak (sub-sample peak as in
+    pixel_phase_correlation; its radial coordinate, the scale, is not used); the current
+    frame is rotated back and Eq. 4-1 on the pair gives the displacement of the image
+    centre.
+
+    Returns (angle, (di, dj) sub-pixel floats, response of the final correlation)."""
+    h, w = y_prev.shape
+    n_theta, n_rho = h, min(h, w) // 2
+    hp = highpass_weight(h, w)
+    lp_prev = log_polar(np.abs(dft2(y_prev)) * hp, n_theta, n_rho)
+    lp_cur = log_polar(np.abs(dft2(y_cur)) * hp, n_theta, n_rho)
+    (d_th, _), _, _ = pixel_phase_correlation(lp_prev, lp_cur)
+    angle = -d_th * np.pi / n_theta
+    (di, dj), _, resp = pixel_phase_correlation(y_prev, rotate_image(y_cur, angle))
+    return float(angle), (float(di), float(dj)), resp
+
+
 def align_mask(gh: int, gw: int, di: int, dj: int) -> np.ndarray:
     """O12, Eq. 4-2: token (I, J) is aligned iff its source (I + di, J + dj) lies in
     the previous token grid."""
@@ -303,6 +380,7 @@ class SelectResult:
     flushed: bool
     response: np.ndarray = field(repr=False, default=None)   # phase-correlation surface
     shift_px: tuple = None        # sub-pixel displacement (align_pixel only)
+    angle: float = 0.0            # rotation of the current frame (align_rotation only)
 
     @property
     def n_recompute(self) -> int:
@@ -333,8 +411,12 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
     sim_freq = global_similarity(f_cur, f_prev)
     flushed = sim_freq < prm.tau_mig
     shift_px = None
+    angle = 0.0
     if prm.align_pixel:
-        shift_px, _, resp = pixel_phase_correlation(y_prev, y_cur)
+        if prm.align_rotation:
+            angle, shift_px, resp = rotation_phase_correlation(y_prev, y_cur)
+        else:
+            shift_px, _, resp = pixel_phase_correlation(y_prev, y_cur)
         di, dj = token_shift(shift_px[0], p * m), token_shift(shift_px[1], p * m)
     else:
         (di, dj), resp = phase_correlation(f_prev, f_cur)
@@ -367,7 +449,7 @@ def select_item(prev: np.ndarray | None, cur: np.ndarray, prm: SelectParams) -> 
         shift=(int(di), int(dj)), sim=sim.ravel(), energy=e_flat, aligned=aligned.ravel(),
         fresh=fresh.ravel(), cand=cand, sim_freq=sim_freq, psi=psi, alpha=alpha, mu=mu,
         sigma=sd, thr=thr, k_reuse=k_reuse, k_cand=k_cand, k_final=k_final,
-        flushed=bool(flushed), response=resp, shift_px=shift_px)
+        flushed=bool(flushed), response=resp, shift_px=shift_px, angle=angle)
 
 
 @dataclass

@@ -163,3 +163,97 @@ def test_pixel_mode_margins():
     assert res.shift == (0, -1)
     mg = osel.decision_margins(res, prm)
     assert mg["shift"] == pytest.approx(0.25, abs=1e-9)
+
+
+# ------------------------------------------------- rotation (log-polar, Fourier-Mellin)
+def test_highpass_weight_closed_forms():
+    hp = osel.highpass_weight(8, 12)
+    assert hp[0, 0] == 0.0                                   # DC
+    assert hp[4, 6] == pytest.approx(2.0, abs=1e-15)         # both Nyquist: X = 0
+    x = np.cos(np.pi * 1 / 8) * np.cos(np.pi * 2 / 12)
+    assert hp[1, 2] == pytest.approx((1 - x) * (2 - x), rel=1e-14)
+    np.testing.assert_allclose(hp[1:, 1:], hp[1:, 1:][::-1, ::-1], rtol=1e-14)   # central symmetry
+
+
+def test_bilinear_exact_on_affine_and_zero_outside():
+    yy, xx = np.meshgrid(np.arange(6.0), np.arange(7.0), indexing="ij")
+    img = 0.5 * yy - 0.25 * xx + 2.0
+    ys, xs = np.array([0.3, 2.75, 4.5]), np.array([1.2, 5.9, 0.0])
+    np.testing.assert_allclose(osel.bilinear(img, ys, xs, wrap=False), 0.5 * ys - 0.25 * xs + 2.0,
+                               rtol=1e-14)
+    assert osel.bilinear(img, np.array([-1.5]), np.array([2.0]), wrap=False)[0] == 0.0
+    assert osel.bilinear(img, np.array([-1.0]), np.array([0.0]), wrap=True)[0] == img[5, 0]
+
+
+def test_rotate_image_quarter_turn_is_rot90():
+    y = np.random.default_rng(7).random((9, 9))
+    np.testing.assert_allclose(osel.rotate_image(y, np.pi / 2), np.rot90(y), atol=1e-12)
+    np.testing.assert_allclose(osel.rotate_image(y, 0.0), y, atol=0)
+
+
+def test_log_polar_of_radial_spectrum_is_constant_in_angle():
+    """A spectrum that depends on the radius only resamples to rows equal across angles
+    (up to the bilinear error of a smooth function)."""
+    h = w = 64
+    fu = np.fft.fftfreq(h)[:, None] * h
+    fv = np.fft.fftfreq(w)[None, :] * w
+    mag = np.exp(-(fu ** 2 + fv ** 2) / 200.0)
+    lp = osel.log_polar(mag, 32, 16)
+    assert np.abs(lp - lp.mean(axis=0, keepdims=True)).max() < 0.02
+    # column j samples radius R^(j / n_rho): compare with the function itself
+    r = (31.0) ** (np.arange(16) / 16)
+    np.testing.assert_allclose(lp.mean(axis=0), np.exp(-r ** 2 / 200.0), atol=0.02)
+
+
+def trajectory_luma(size=224):
+    return osel.luma(fcdata.episode_frames(11, size=size, n_frames=1, shear=0.0)[0])
+
+
+@pytest.mark.parametrize("a", [0.05, -0.1, 0.2])
+def test_rotation_recovered_with_its_sign(a):
+    """The current frame is the previous one rotated by a (about the centre): the
+    estimated angle is within 0.01 rad of a (the angular bins are pi / 224 = 0.014 rad),
+    and the centre's displacement after rotating back under 0.5 px."""
+    y0 = trajectory_luma()
+    y1 = osel.rotate_image(y0, -a)
+    ang, (di, dj), _ = osel.rotation_phase_correlation(y0, y1)
+    assert abs(ang - a) < 0.01
+    assert abs(di) < 0.5 and abs(dj) < 0.5
+
+
+def test_rotation_then_translation():
+    """Rotated by 0.1 rad and then moved by (6, -9) px: the angle is found and the
+    centre's displacement is the move back, (-6, 9), within a pixel."""
+    y0 = trajectory_luma()
+    y1 = np.roll(osel.rotate_image(y0, -0.1), (6, -9), axis=(0, 1))
+    ang, (di, dj), _ = osel.rotation_phase_correlation(y0, y1)
+    assert abs(ang - 0.1) < 0.01
+    assert abs(di + 6) < 1.0 and abs(dj - 9) < 1.0
+
+
+def test_pure_roll_has_no_rotation():
+    """A circular roll leaves the magnitude spectra equal (up to rounding): angle 0, and
+    the displacement is the plain pixel-resolution one."""
+    y0 = trajectory_luma()
+    y1 = np.roll(y0, (-5, 12), axis=(0, 1))
+    ang, d, _ = osel.rotation_phase_correlation(y0, y1)
+    assert abs(ang) < 1e-12
+    assert d == pytest.approx(osel.pixel_phase_correlation(y0, y1)[0], abs=1e-12)
+
+
+def test_rotation_mode_in_the_selection():
+    """select_item with align_rotation on a rotated-then-moved pair: the rotation is
+    reported and the token displacement is that of the image centre after undoing it;
+    on a pure whole-token roll it equals the plain pixel mode."""
+    frames = fcdata.episode_frames(11, size=224, n_frames=1, shear=0.0)
+    prev = frames[0]
+    cur = np.stack([np.roll(osel.rotate_image(prev[c].astype(np.float64), -0.08), (28, 0),
+                            axis=(0, 1)) for c in range(3)]).astype(np.float32)
+    prm = osel.SelectParams(merge=2, align_pixel=True, align_rotation=True)
+    res = osel.select_item(prev, cur, prm)
+    assert abs(res.angle - 0.08) < 0.01 and res.shift == (-1, 0)
+    rolled = np.roll(prev, (0, -56), axis=(1, 2))
+    a = osel.select_item(prev, rolled, prm)
+    b = osel.select_item(prev, rolled, osel.SelectParams(merge=2, align_pixel=True))
+    assert a.shift == b.shift == (0, 2) and abs(a.angle) < 1e-12
+    np.testing.assert_array_equal(a.reuse_mask, b.reuse_mask)
