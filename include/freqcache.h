@@ -99,6 +99,10 @@ typedef struct {
                                Needs H and W of the form 7 * 2^k (14 ... 896); the first such
                                call on a context allocates its workspace.  fc_select and
                                fc_select_noalloc only (not fc_select_carry).               */
+  int32_t align_rotation;   /* with align_pixel = 1: the rotation of the current frame is found
+                               first and undone (fc_phase_correlate_rotation), and the token
+                               displacement is that of the frame centre.  Needs
+                               min(H, W) >= 28.                                             */
 } fc_select_params;
 
 enum { FC_SCALAR_SIM_FREQ = 0, FC_SCALAR_PSI, FC_SCALAR_ALPHA, FC_SCALAR_MU,
@@ -321,6 +325,24 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
 fc_status fc_phase_correlate(fc_ctx *ctx, const float *frames_prev, const float *frames_cur,
                              int32_t B, int32_t H, int32_t W, double *shift_px, int32_t *peak,
                              double *response, void *stream);
+
+/* Pixel-resolution phase correlation after a rotation estimate (Fourier-Mellin): the
+ * magnitude spectra of both frames' luma, weighted by (1 - X)(2 - X) with
+ * X = cos(pi f_y) cos(pi f_x) (f: signed frequency in cycles per pixel), are sampled
+ * bilinearly at H angles i pi / H and min(H, W) / 2 radii R^(j / (min(H, W) / 2)),
+ * R = min(H, W) / 2 - 1; Eq. 4-1 on those maps (as fc_phase_correlate, sub-sample peak)
+ * gives the angular offset d, and the rotation of the current frame relative to the
+ * previous one is a = -d pi / H (radians, in (-pi/2, pi/2]; counter-clockwise in
+ * (column, row) coordinates).  The current frame's luma is rotated back about the
+ * centre ((H-1)/2, (W-1)/2), bilinear, 0 outside, and Eq. 4-1 on the pair gives
+ * shift_px, the displacement of the frame centre.
+ *   frames_prev, frames_cur: [B][3][H][W] float32 (device); frames_prev may be NULL.
+ *   H, W: 7 * 2^k up to 896 with min(H, W) >= 28, within caps.
+ *   angle: [B] float64 or NULL; shift_px: [B][2] float64 (device, caller-owned).
+ * Shares the workspace of fc_phase_correlate (allocated at the first call of either). */
+fc_status fc_phase_correlate_rotation(fc_ctx *ctx, const float *frames_prev,
+                                      const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                                      double *angle, double *shift_px, void *stream);
 
 /* Debug mode (process-wide): after every kernel launch the library waits for the
  * launch stream and reports an error raised while the kernel ran as FC_ERR_HIP from

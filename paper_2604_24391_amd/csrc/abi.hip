@@ -118,7 +118,8 @@ fc_status check_select_args(const fc_select_params *prm, const float *cur,
   if (!(p.alpha_min >= 0 && p.alpha_max <= 1 && p.alpha_min <= p.alpha_max) ||
       !(p.alpha_fixed >= 0 && p.alpha_fixed <= 1) || !(p.lambda_ >= 0) || !std::isfinite(p.tau_mig) ||
       !std::isfinite(p.tau_sim) || (p.no_align != 0 && p.no_align != 1) ||
-      (p.no_refresh != 0 && p.no_refresh != 1) || (p.align_pixel != 0 && p.align_pixel != 1))
+      (p.no_refresh != 0 && p.no_refresh != 1) || (p.align_pixel != 0 && p.align_pixel != 1) ||
+      (p.align_rotation != 0 && p.align_rotation != 1) || (p.align_rotation && !p.align_pixel))
     return fail(FC_ERR_INVALID_ARG, "%s: hyper-parameter out of range", who);
   if (B < 1 || H < 1 || W < 1) return fail(FC_ERR_SHAPE, "%s: B=%d H=%d W=%d", who, B, H, W);
   const int tp = p.patch * p.merge;
@@ -127,6 +128,9 @@ fc_status check_select_args(const fc_select_params *prm, const float *cur,
   const long M = (long)(H / tp) * (W / tp);
   if (M > kMaxTokens)
     return fail(FC_ERR_UNSUPPORTED, "%s: %ld tokens per frame > %d", who, M, kMaxTokens);
+  if (p.align_rotation && !pix_rot_size_ok(H, W))
+    return fail(FC_ERR_UNSUPPORTED, "%s: align_rotation needs H and W of the form 7 * 2^k up to "
+                "896 with min(H, W) >= 28 (got %dx%d)", who, H, W);
   if (p.align_pixel && (!pix_size_ok(H) || !pix_size_ok(W)))
     return fail(FC_ERR_UNSUPPORTED, "%s: align_pixel needs H and W of the form 7 * 2^k up to 896 "
                 "(got %dx%d)", who, H, W);
@@ -176,8 +180,9 @@ fc_status use_device(fc_ctx *ctx) {
 // The pixel phase-correlation workspace, sized for the context's caps at its first use.
 fc_status ensure_pix(fc_ctx *ctx) {
   if (ctx->pix) return FC_OK;
+  // sized for the rotation mode, whose parts come after the plain mode's
   const size_t bytes = fc::pix_ws_bytes(ctx->caps.max_batch, ctx->caps.max_height,
-                                        ctx->caps.max_width);
+                                        ctx->caps.max_width, true);
   hipError_t e = hipMalloc(reinterpret_cast<void **>(&ctx->pix), bytes);
   if (e != hipSuccess) {
     ctx->pix = nullptr;
@@ -287,7 +292,7 @@ fc_status fc_select(fc_ctx *ctx, const fc_select_params *prm, const float *frame
                   {}};
   if (prm->align_pixel) {
     if ((st = ensure_pix(ctx)) != FC_OK) return st;
-    ws.pix = fc::pix_ws_at(ctx->pix, B, H, W);
+    ws.pix = fc::pix_ws_at(ctx->pix, B, H, W, prm->align_rotation != 0);
   }
   return fc::launch_select(ctx, ws, *prm, frames_prev, frames_cur, B, H, W, *out,
                            reinterpret_cast<hipStream_t>(stream));
@@ -358,9 +363,31 @@ fc_status fc_phase_correlate(fc_ctx *ctx, const float *frames_prev, const float 
   fc_status st = use_device(ctx);
   if (st != FC_OK) return st;
   if ((st = ensure_pix(ctx)) != FC_OK) return st;
-  return fc::launch_pixel_pc(ctx, fc::pix_ws_at(ctx->pix, B, H, W), frames_prev, frames_cur, B, H,
+  return fc::launch_pixel_pc(ctx, fc::pix_ws_at(ctx->pix, B, H, W, false), frames_prev, frames_cur, B, H,
                              W, shift_px, peak, response, nullptr, 1, false,
                              reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_phase_correlate_rotation(fc_ctx *ctx, const float *frames_prev,
+                                      const float *frames_cur, int32_t B, int32_t H, int32_t W,
+                                      double *angle, double *shift_px, void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_phase_correlate_rotation: null context");
+  if (!frames_cur || !shift_px)
+    return fail(FC_ERR_INVALID_ARG, "fc_phase_correlate_rotation: null current frames or shift output");
+  if (B < 1 || H < 1 || W < 1)
+    return fail(FC_ERR_SHAPE, "fc_phase_correlate_rotation: B=%d H=%d W=%d", B, H, W);
+  if (!fc::pix_rot_size_ok(H, W))
+    return fail(FC_ERR_UNSUPPORTED, "fc_phase_correlate_rotation: H and W must be 7 * 2^k up to 896 "
+                "with min(H, W) >= 28 (got %dx%d)", H, W);
+  if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width)
+    return fail(FC_ERR_CAPACITY, "fc_phase_correlate_rotation: B=%d H=%d W=%d exceed the context caps",
+                B, H, W);
+  fc_status st = use_device(ctx);
+  if (st != FC_OK) return st;
+  if ((st = ensure_pix(ctx)) != FC_OK) return st;
+  return fc::launch_pixel_pc_rot(ctx, fc::pix_ws_at(ctx->pix, B, H, W, true), frames_prev,
+                                 frames_cur, B, H, W, angle, shift_px, nullptr, 1, false,
+                                 reinterpret_cast<hipStream_t>(stream));
 }
 
 static fc_status check_layer(fc_ctx *ctx, const fc_layer_desc *L, const fc_kv_cache *kv, int B,

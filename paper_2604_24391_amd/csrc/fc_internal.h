@@ -121,10 +121,13 @@ struct PixWs {
   int *rowarg = nullptr;
   double *bmax = nullptr;
   double *shift_px = nullptr;
+  // rotation only: weighted magnitude spectra, log-polar maps, rotated-back luma
+  double *mag = nullptr, *lp = nullptr, *yrot = nullptr;
 };
 bool pix_size_ok(int n);                       // n = 7 2^k, 14 <= n <= 896
-size_t pix_ws_bytes(long B, long H, long W);
-PixWs pix_ws_at(void *base, long B, long H, long W);
+bool pix_rot_size_ok(int H, int W);            // and min(H, W) / 2 too
+size_t pix_ws_bytes(long B, long H, long W, bool rot);
+PixWs pix_ws_at(void *base, long B, long H, long W, bool rot);
 // Eq. 4-1 on full-resolution luma for B pairs (prev may be null: an all-zero frame).
 // shift_px [B][2] (null: the workspace's), peak [B][2] integer peak (may be null),
 // resp [B][H][W] response surface (may be null), tok_shift [B][2] the displacement in
@@ -132,6 +135,11 @@ PixWs pix_ws_at(void *base, long B, long H, long W);
 fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
                           int B, int H, int W, double *shift_px, int32_t *peak, double *resp,
                           int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st);
+// The same after finding the current frame's rotation (angle [B], may be null) and undoing
+// it; shift_px is then the displacement of the image centre.  ws from pix_ws_at(rot=true).
+fc_status launch_pixel_pc_rot(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
+                              int B, int H, int W, double *angle, double *shift_px,
+                              int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st);
 
 // Selection workspace: spectra of the previous and the current frames, per-patch
 // high-pass energies (current frame) and spectral products; pix only with align_pixel.

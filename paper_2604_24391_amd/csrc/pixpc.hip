@@ -25,7 +25,15 @@
 // The FFTs are self-sorting (Stockham) mixed-radix transforms of length n = 7 2^k:
 // one radix-7 stage, then radix-4 stages and at most one radix-2 stage, each stage a
 // pass over LDS between two buffers.  Twiddles come from one table per workgroup
-// (sincospi of the exact rational angle m / n).  Sizes: H and W of the form 7 2^k with 2 <= 2^k <= 128 (14 ... 896).
+// (sincospi of the exact rational angle m / n).  Sizes: H and W of the form 7 2^k with
+// 2 <= 2^k <= 128 (14 ... 896).
+//
+// Rotation (Fourier-Mellin, launch_pixel_pc_rot): the forward column pass also writes
+// the high-pass weighted magnitude spectra of both frames; k_lp_sample resamples them
+// on a log-polar grid (H angles over [0, pi), min(H, W) / 2 radii); the same correlation
+// kernels on those maps give the rotation from the peak's angular coordinate;
+// k_derotate rotates the current frame's luma back about the centre; a last
+// correlation gives the displacement of the image centre.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -184,21 +192,30 @@ __device__ __forceinline__ double luma_at(const float *frame, size_t plane, size
 // The two frames' rows are transformed as two separate sequences (not packed into one
 // complex sequence): packing leaks rounding noise of one frame's spectrum into the
 // other's, which dominates when a frame is (nearly) zero.
-__global__ __launch_bounds__(kPcThreads) void k_pc_rows(const float *__restrict__ prev,
-                                                        const float *__restrict__ cur, int H,
-                                                        int W, PixWs ws) {
+// Each side of a pair is a real map ([B][H][W] float64) or a frame's luma ([B][3][H][W]
+// float32 RGB), or all zero when both are null.
+struct PcIn {
+  const float *rgb_prev, *rgb_cur;
+  const double *map_prev, *map_cur;
+};
+
+__device__ __forceinline__ double pc_input(const float *rgb, const double *map, int b, int H, int W,
+                                           int y, int x) {
+  const size_t plane = (size_t)H * W, off = (size_t)y * W + x;
+  if (map) return map[(size_t)b * plane + off];
+  if (rgb) return luma_at(rgb + (size_t)b * 3 * plane, plane, off);
+  return 0.0;
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_pc_rows(PcIn in, int H, int W, PixWs ws) {
   __shared__ double2 buf[2][2 * kPcMaxN];
   __shared__ double2 tw[kPcMaxN];
   const int y = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   const int hw = W / 2 + 1;
-  const size_t plane = (size_t)H * W;
   make_twiddles(tw, W);
-  const float *fp = prev ? prev + (size_t)b * 3 * plane : nullptr;
-  const float *fc = cur + (size_t)b * 3 * plane;
   for (int x = t; x < W; x += blockDim.x) {
-    const size_t off = (size_t)y * W + x;
-    buf[0][x] = make_double2(fp ? luma_at(fp, plane, off) : 0.0, 0.0);
-    buf[0][W + x] = make_double2(luma_at(fc, plane, off), 0.0);
+    buf[0][x] = make_double2(pc_input(in.rgb_prev, in.map_prev, b, H, W, y, x), 0.0);
+    buf[0][W + x] = make_double2(pc_input(in.rgb_cur, in.map_cur, b, H, W, y, x), 0.0);
   }
   __syncthreads();
   const double2 *Z = fft_lds<false>(buf[0], buf[1], tw, W, 2);
@@ -212,8 +229,11 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_rows(const float *__restrict_
 
 // ------------------------------------------------------------------------- k_pc_cols
 // Column strips: CW adjacent half-spectrum columns per workgroup, for H <= MAXH.
+// FWD with mag: also the high-pass weighted magnitudes of both spectra,
+// mag[b][side][ky][kx] = (1 - X)(2 - X) |F|, X = cos(pi f_y) cos(pi f_x) (f the signed
+// frequency in cycles per sample).
 template <int MAXH, int CW, bool FWD>
-__global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) {
+__global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws, double *mag) {
   constexpr int NS = FWD ? 2 * CW : CW;
   __shared__ double2 buf[2][NS * MAXH];
   __shared__ double2 tw[MAXH];
@@ -239,6 +259,16 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_cols(int H, int W, PixWs ws) 
     for (int e = t; e < cw * H; e += blockDim.x) {
       const int c = e / H, ky = e - c * H;
       const double2 f1 = F[c * H + ky], f2 = F[(CW + c) * H + ky];
+      if (mag) {
+        const int kx = c0 + c;
+        const double fy = (double)(2 * ky < H ? ky : ky - H) / (double)H;
+        const double fx = (double)(2 * kx < W ? kx : kx - W) / (double)W;
+        const double X = cospi(fy) * cospi(fx);
+        const double hp = (1.0 - X) * (2.0 - X);
+        const size_t o = ((size_t)b * 2 * H + ky) * hw + kx;
+        mag[o] = hp * sqrt(f1.x * f1.x + f1.y * f1.y);
+        mag[o + (size_t)H * hw] = hp * sqrt(f2.x * f2.x + f2.y * f2.y);
+      }
       const double xr = f1.x * f2.x + f1.y * f2.y;
       const double xi = f1.y * f2.x - f1.x * f2.y;
       sa[(size_t)ky * hw + c0 + c] = make_double2(xr, xi);
@@ -417,11 +447,89 @@ __global__ __launch_bounds__(kPcThreads) void k_pc_peak(int H, int W, PixWs ws,
 }
 
 template <int MAXH, int CW>
-void launch_cols(int H, int W, int B, const PixWs &ws, hipStream_t st) {
+void launch_cols(int H, int W, int B, const PixWs &ws, double *mag, bool fwd_only, hipStream_t st) {
   const int hw = W / 2 + 1;
   const dim3 grid((unsigned)((hw + CW - 1) / CW), (unsigned)B);
-  hipLaunchKernelGGL((k_pc_cols<MAXH, CW, true>), grid, dim3(kPcThreads), 0, st, H, W, ws);
-  hipLaunchKernelGGL((k_pc_cols<MAXH, CW, false>), grid, dim3(kPcThreads), 0, st, H, W, ws);
+  hipLaunchKernelGGL((k_pc_cols<MAXH, CW, true>), grid, dim3(kPcThreads), 0, st, H, W, ws, mag);
+  if (!fwd_only)
+    hipLaunchKernelGGL((k_pc_cols<MAXH, CW, false>), grid, dim3(kPcThreads), 0, st, H, W, ws,
+                       (double *)nullptr);
+}
+
+// ----------------------------------------------------------------- rotation (log-polar)
+// Log-polar samples of both frames' weighted magnitude spectra: angle i pi / NT, radius
+// R^(j / NR), R = min(H, W) / 2 - 1, bilinear over the half-plane kx in [0, W/2] (a point
+// with kx outside it is read at its mirror -k: the magnitudes of real frames are centrally
+// symmetric).  lp[side][b][i][j] (side 0: previous frame), so each side is a batch of
+// NT x NR maps.
+__device__ __forceinline__ double mag_at(const double *m, int H, int W, int ky, int kx) {
+  const int hw = W / 2 + 1;
+  kx %= W;
+  if (kx < 0) kx += W;
+  ky %= H;
+  if (ky < 0) ky += H;
+  if (kx >= hw) {            // the mirror -k
+    kx = W - kx;
+    ky = ky == 0 ? 0 : H - ky;
+  }
+  return m[(size_t)ky * hw + kx];
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_lp_sample(const double *__restrict__ mag, int H,
+                                                          int W, int NT, int NR,
+                                                          double *__restrict__ lp) {
+  const int i = blockIdx.x, b = blockIdx.y;
+  const int hw = W / 2 + 1;
+  const double R = (double)min(H, W) / 2.0 - 1.0;
+  double sn, cs;
+  sincospi((double)i / (double)NT, &sn, &cs);
+  for (int e = threadIdx.x; e < 2 * NR; e += blockDim.x) {
+    const int side = e / NR, j = e - side * NR;
+    const double r = pow(R, (double)j / (double)NR);
+    const double fy = r * sn, fx = r * cs;
+    const double y0 = floor(fy), x0 = floor(fx);
+    const double wy = fy - y0, wx = fx - x0;
+    const int iy = (int)y0, ix = (int)x0;
+    const double *m = mag + ((size_t)b * 2 + side) * H * hw;
+    const double v = (1.0 - wy) * (1.0 - wx) * mag_at(m, H, W, iy, ix) +
+                     (1.0 - wy) * wx * mag_at(m, H, W, iy, ix + 1) +
+                     wy * (1.0 - wx) * mag_at(m, H, W, iy + 1, ix) +
+                     wy * wx * mag_at(m, H, W, iy + 1, ix + 1);
+    lp[(((size_t)side * gridDim.y + b) * NT + i) * NR + j] = v;
+  }
+}
+
+// The current frame's luma rotated back by the estimated angle, a = -dtheta pi / NT
+// (dtheta: the angular coordinate of the log-polar correlation peak):
+// yrot(q) = Y(R(a)(q - c) + c), bilinear, 0 outside the frame.
+__global__ __launch_bounds__(kPcThreads) void k_derotate(const float *__restrict__ cur, int H,
+                                                         int W, const double *__restrict__ dth,
+                                                         int NT, double *__restrict__ yrot,
+                                                         double *__restrict__ angle) {
+  const int y = blockIdx.x, b = blockIdx.y;
+  const double a = -dth[2 * b] * M_PI / (double)NT;
+  if (angle && y == 0 && threadIdx.x == 0) angle[b] = a;
+  double sa, ca;
+  sincos(a, &sa, &ca);
+  const double cy = (H - 1) / 2.0, cx = (W - 1) / 2.0;
+  const size_t plane = (size_t)H * W;
+  const float *fr = cur + (size_t)b * 3 * plane;
+  for (int x = threadIdx.x; x < W; x += blockDim.x) {
+    const double qy = y - cy, qx = x - cx;
+    const double sy = qx * sa + qy * ca + cy, sx = qx * ca - qy * sa + cx;
+    const double y0 = floor(sy), x0 = floor(sx);
+    const double wy = sy - y0, wx = sx - x0;
+    const int iy = (int)y0, ix = (int)x0;
+    double v = 0.0;
+    for (int u = 0; u < 2; ++u)
+      for (int w2 = 0; w2 < 2; ++w2) {
+        const int yy = iy + u, xx = ix + w2;
+        if (yy < 0 || yy >= H || xx < 0 || xx >= W) continue;
+        const double wgt = (u ? wy : 1.0 - wy) * (w2 ? wx : 1.0 - wx);
+        v += wgt * luma_at(fr, plane, (size_t)yy * W + xx);
+      }
+    yrot[(size_t)b * plane + (size_t)y * W + x] = v;
+  }
 }
 
 }  // namespace
@@ -432,60 +540,85 @@ bool pix_size_ok(int n) {
   return (p & (p - 1)) == 0;
 }
 
-size_t pix_ws_bytes(long B, long H, long W) {
-  const long hw = W / 2 + 1;
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const long ncb = (hw + 1) / 2;             // strips of the narrowest kind (CW = 2)
-  return 2 * al((size_t)B * H * hw * sizeof(double2)) + al((size_t)B * H * sizeof(double)) +
-         al((size_t)B * H * sizeof(int)) + al((size_t)B * ncb * sizeof(double)) +
-         al((size_t)B * 2 * sizeof(double));
+bool pix_rot_size_ok(int H, int W) {
+  return pix_size_ok(H) && pix_size_ok(W) && pix_size_ok(std::min(H, W) / 2);
 }
 
-PixWs pix_ws_at(void *base, long B, long H, long W) {
+namespace {
+// Workspace parts in order: sa, sb, rowmax, rowarg, bmax, shift_px, then with rotation
+// mag [B][2][H][W/2 + 1], lp [2][B][H][min(H, W) / 2], yrot [B][H][W].
+template <typename F>
+void pix_parts(long B, long H, long W, bool rot, F &&take) {
   const long hw = W / 2 + 1;
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const long ncb = (hw + 1) / 2;
+  const long ncb = (hw + 1) / 2;             // strips of the narrowest kind (CW = 2)
+  take(0, (size_t)B * H * hw * sizeof(double2));
+  take(1, (size_t)B * H * hw * sizeof(double2));
+  take(2, (size_t)B * H * sizeof(double));
+  take(3, (size_t)B * H * sizeof(int));
+  take(4, (size_t)B * ncb * sizeof(double));
+  take(5, (size_t)B * 2 * sizeof(double));
+  if (rot) {
+    take(6, (size_t)B * 2 * H * hw * sizeof(double));
+    take(7, (size_t)B * 2 * H * (std::min(H, W) / 2) * sizeof(double));
+    take(8, (size_t)B * H * W * sizeof(double));
+  }
+}
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+}  // namespace
+
+size_t pix_ws_bytes(long B, long H, long W, bool rot) {
+  size_t n = 0;
+  pix_parts(B, H, W, rot, [&](int, size_t bytes) { n += al256(bytes); });
+  return n;
+}
+
+PixWs pix_ws_at(void *base, long B, long H, long W, bool rot) {
   unsigned char *p = static_cast<unsigned char *>(base);
   PixWs ws;
-  ws.sa = reinterpret_cast<double2 *>(p);
-  p += al((size_t)B * H * hw * sizeof(double2));
-  ws.sb = reinterpret_cast<double2 *>(p);
-  p += al((size_t)B * H * hw * sizeof(double2));
-  ws.rowmax = reinterpret_cast<double *>(p);
-  p += al((size_t)B * H * sizeof(double));
-  ws.rowarg = reinterpret_cast<int *>(p);
-  p += al((size_t)B * H * sizeof(int));
-  ws.bmax = reinterpret_cast<double *>(p);
-  p += al((size_t)B * ncb * sizeof(double));
-  ws.shift_px = reinterpret_cast<double *>(p);
+  pix_parts(B, H, W, rot, [&](int part, size_t bytes) {
+    switch (part) {
+      case 0: ws.sa = reinterpret_cast<double2 *>(p); break;
+      case 1: ws.sb = reinterpret_cast<double2 *>(p); break;
+      case 2: ws.rowmax = reinterpret_cast<double *>(p); break;
+      case 3: ws.rowarg = reinterpret_cast<int *>(p); break;
+      case 4: ws.bmax = reinterpret_cast<double *>(p); break;
+      case 5: ws.shift_px = reinterpret_cast<double *>(p); break;
+      case 6: ws.mag = reinterpret_cast<double *>(p); break;
+      case 7: ws.lp = reinterpret_cast<double *>(p); break;
+      case 8: ws.yrot = reinterpret_cast<double *>(p); break;
+    }
+    p += al256(bytes);
+  });
   return ws;
 }
 
-fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
-                          int B, int H, int W, double *shift_px, int32_t *peak, double *resp,
-                          int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st) {
-  if (!pix_size_ok(H) || !pix_size_ok(W))
-    return fail(FC_ERR_UNSUPPORTED, "pixel phase correlation: H=%d, W=%d must be 7 * 2^k, 14..%d",
-                H, W, kPcMaxN);
+namespace {
+// One phase correlation of B pairs of H x W inputs.  mag_only: the row transforms and
+// the forward column pass only, with the weighted magnitudes written to ws.mag.
+fc_status pc_run(fc_ctx *ctx, const PixWs &ws, PcIn in, int B, int H, int W, bool mag_only,
+                 double *shift_px, int32_t *peak, double *resp, int32_t *tok_shift, int tp,
+                 bool zero_shift, hipStream_t st) {
   // the response surface goes to the caller's buffer or over the current-frame
   // half-spectra, which the forward column pass has consumed by then
   double *r = resp ? resp : reinterpret_cast<double *>(ws.sb);
   {
     ProfScope ps(ctx, st, "fc_pc_rows");
-    hipLaunchKernelGGL(k_pc_rows, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, prev,
-                       cur, H, W, ws);
+    hipLaunchKernelGGL(k_pc_rows, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, in, H,
+                       W, ws);
     FC_LAUNCH_OK(st, "k_pc_rows");
   }
   {
     ProfScope ps(ctx, st, "fc_pc_cols");
+    double *mag = mag_only ? ws.mag : nullptr;
     if (H <= 224)
-      launch_cols<224, 8>(H, W, B, ws, st);
+      launch_cols<224, 8>(H, W, B, ws, mag, mag_only, st);
     else if (H <= 448)
-      launch_cols<448, 4>(H, W, B, ws, st);
+      launch_cols<448, 4>(H, W, B, ws, mag, mag_only, st);
     else
-      launch_cols<896, 2>(H, W, B, ws, st);
+      launch_cols<896, 2>(H, W, B, ws, mag, mag_only, st);
     FC_LAUNCH_OK(st, "k_pc_cols");
   }
+  if (mag_only) return FC_OK;
   {
     ProfScope ps(ctx, st, "fc_pc_rows_inv");
     hipLaunchKernelGGL(k_pc_rows_inv, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, H,
@@ -500,6 +633,50 @@ fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const
     FC_LAUNCH_OK(st, "k_pc_peak");
   }
   return FC_OK;
+}
+}  // namespace
+
+fc_status launch_pixel_pc(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
+                          int B, int H, int W, double *shift_px, int32_t *peak, double *resp,
+                          int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st) {
+  if (!pix_size_ok(H) || !pix_size_ok(W))
+    return fail(FC_ERR_UNSUPPORTED, "pixel phase correlation: H=%d, W=%d must be 7 * 2^k, 14..%d",
+                H, W, kPcMaxN);
+  return pc_run(ctx, ws, PcIn{prev, cur, nullptr, nullptr}, B, H, W, false, shift_px, peak, resp,
+                tok_shift, tp, zero_shift, st);
+}
+
+fc_status launch_pixel_pc_rot(fc_ctx *ctx, const PixWs &ws, const float *prev, const float *cur,
+                              int B, int H, int W, double *angle, double *shift_px,
+                              int32_t *tok_shift, int tp, bool zero_shift, hipStream_t st) {
+  if (!pix_rot_size_ok(H, W) || !ws.mag)
+    return fail(FC_ERR_UNSUPPORTED, "rotation phase correlation: H=%d, W=%d must be 7 * 2^k with "
+                "min(H, W) >= 28", H, W);
+  const int NT = H, NR = std::min(H, W) / 2;
+  fc_status s;
+  // 1. weighted magnitude spectra of both frames
+  if ((s = pc_run(ctx, ws, PcIn{prev, cur, nullptr, nullptr}, B, H, W, true, nullptr, nullptr,
+                  nullptr, nullptr, 1, false, st)) != FC_OK)
+    return s;
+  // 2. their log-polar samples, correlated: the angular offset of the peak
+  {
+    ProfScope ps(ctx, st, "fc_lp_sample");
+    hipLaunchKernelGGL(k_lp_sample, dim3((unsigned)NT, (unsigned)B), dim3(kPcThreads), 0, st,
+                       (const double *)ws.mag, H, W, NT, NR, ws.lp);
+    FC_LAUNCH_OK(st, "k_lp_sample");
+  }
+  if ((s = pc_run(ctx, ws, PcIn{nullptr, nullptr, ws.lp, ws.lp + (size_t)B * NT * NR}, B, NT, NR,
+                  false, ws.shift_px, nullptr, nullptr, nullptr, 1, false, st)) != FC_OK)
+    return s;
+  // 3. the current frame rotated back, then the displacement of the image centre
+  {
+    ProfScope ps(ctx, st, "fc_derotate");
+    hipLaunchKernelGGL(k_derotate, dim3((unsigned)H, (unsigned)B), dim3(kPcThreads), 0, st, cur, H,
+                       W, (const double *)ws.shift_px, NT, ws.yrot, angle);
+    FC_LAUNCH_OK(st, "k_derotate");
+  }
+  return pc_run(ctx, ws, PcIn{prev, nullptr, nullptr, ws.yrot}, B, H, W, false, shift_px, nullptr,
+                nullptr, tok_shift, tp, zero_shift, st);
 }
 
 }  // namespace fc

@@ -1040,8 +1040,11 @@ fc_status launch_select(fc_ctx *ctx, const SelectWs &ws, const fc_select_params 
   }
   if (prm.align_pixel) {
     // Module I at pixel resolution: the token shift of k_grid is replaced
-    fc_status s = launch_pixel_pc(ctx, ws.pix, prev, cur, B, H, W, nullptr, nullptr, nullptr,
-                                  out.shift, P * m, prm.no_align != 0, st);
+    fc_status s = prm.align_rotation
+                      ? launch_pixel_pc_rot(ctx, ws.pix, prev, cur, B, H, W, nullptr, nullptr,
+                                            out.shift, P * m, prm.no_align != 0, st)
+                      : launch_pixel_pc(ctx, ws.pix, prev, cur, B, H, W, nullptr, nullptr, nullptr,
+                                        out.shift, P * m, prm.no_align != 0, st);
     if (s != FC_OK) return s;
   }
   {
@@ -1106,7 +1109,8 @@ fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
                                 const float *cur, int B, int H, int W,
                                 const fc_select_out &out, hipStream_t st) {
   const SelectWsBytes sb = select_ws_bytes(B, H, W);
-  const size_t need = sb.total + (prm.align_pixel ? pix_ws_bytes(B, H, W) : 0);
+  const size_t need =
+      sb.total + (prm.align_pixel ? pix_ws_bytes(B, H, W, prm.align_rotation != 0) : 0);
   if (need > kNoAllocScratchBytes)
     return fail(FC_ERR_CAPACITY, "fc_select_noalloc: %zu bytes of scratch needed, %zu available",
                 need, kNoAllocScratchBytes);
@@ -1125,7 +1129,7 @@ fc_status launch_select_noalloc(const fc_select_params &prm, const float *prev,
   ws.cur = spectra_at(base + sb.spectra, B, H, W);
   ws.penergy = reinterpret_cast<double *>(base + 2 * sb.spectra);
   ws.pdot = reinterpret_cast<double *>(base + 2 * sb.spectra + sb.penergy);
-  if (prm.align_pixel) ws.pix = pix_ws_at(base + sb.total, B, H, W);
+  if (prm.align_pixel) ws.pix = pix_ws_at(base + sb.total, B, H, W, prm.align_rotation != 0);
   return launch_select(nullptr, ws, prm, prev, cur, B, H, W, out, st);
 }
 

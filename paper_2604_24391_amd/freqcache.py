@@ -31,7 +31,8 @@ FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
            "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
-           "fc_phase_correlate", "fc_slot_state_bytes", "fc_slot_map_init",
+           "fc_phase_correlate", "fc_phase_correlate_rotation", "fc_slot_state_bytes",
+           "fc_slot_map_init",
            "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
 
@@ -52,7 +53,7 @@ class fc_select_params(ctypes.Structure):
                 ("lambda_", c_double), ("alpha_min", c_double), ("alpha_max", c_double),
                 ("adaptive", c_int32), ("alpha_fixed", c_double), ("entropy_norm", c_int32),
                 ("tau_sim", c_double), ("no_align", c_int32), ("no_refresh", c_int32),
-                ("align_pixel", c_int32)]
+                ("align_pixel", c_int32), ("align_rotation", c_int32)]
 
 
 class fc_select_out(ctypes.Structure):
@@ -116,6 +117,8 @@ def lib() -> ctypes.CDLL:
                                              c_int32, c_void_p]
         L.fc_phase_correlate.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fc_phase_correlate_rotation.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
+                                                  c_int32, c_void_p, c_void_p, c_void_p]
         L.fc_slot_state_bytes.argtypes = [c_int32, c_int32]
         L.fc_slot_state_bytes.restype = ctypes.c_size_t
         L.fc_slot_map_init.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
@@ -128,7 +131,8 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(c_int64), c_int32]
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
                   "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward",
-                  "fc_layer_forward_trail", "fc_phase_correlate", "fc_slot_map_init",
+                  "fc_layer_forward_trail", "fc_phase_correlate", "fc_phase_correlate_rotation",
+                  "fc_slot_map_init",
                   "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
             getattr(L, n).restype = c_int32
@@ -243,6 +247,7 @@ class SelectParams:
     align: bool = True          # False: ablation "w/o Module I" (position-wise matching)
     refresh: bool = True        # False: ablation "w/o Module II" (no edge refresh)
     align_pixel: bool = False   # True: Module I's displacement from full-resolution luma
+    align_rotation: bool = False  # with align_pixel: the rotation found and undone first
 
     @classmethod
     def naive(cls, tau: float, merge: int = 1) -> "SelectParams":
@@ -258,7 +263,8 @@ class SelectParams:
         return fc_select_params(self.patch, self.merge, self.tau_mig, self.lam, self.alpha_min,
                                 self.alpha_max, int(self.adaptive), self.alpha_fixed,
                                 int(self.entropy_norm), self.tau_sim, int(not self.align),
-                                int(not self.refresh), int(self.align_pixel))
+                                int(not self.refresh), int(self.align_pixel),
+                                int(self.align_rotation))
 
 
 @dataclass
@@ -360,6 +366,28 @@ def fc_phase_correlate(ctx: Context, prev: torch.Tensor | None, cur: torch.Tenso
     pk = _ptr(peak, torch.int32, 2 * B, "peak") if peak is not None else c_void_p(0)
     rs = _ptr(response, torch.float64, B * H * W, "response") if response is not None else c_void_p(0)
     _check(lib().fc_phase_correlate(ctx.handle, pp, pc, B, H, W, sp, pk, rs, _stream(stream)))
+
+
+def fc_phase_correlate_rotation(ctx: Context, prev: torch.Tensor | None, cur: torch.Tensor,
+                                shift_px: torch.Tensor, angle: torch.Tensor | None = None,
+                                stream=None):
+    """Rotation of the current frames relative to the previous ones (angle [B] float64,
+    radians) and the displacement of the frame centre after undoing it (shift_px [B, 2]
+    float64)."""
+    if cur.dim() != 4 or cur.shape[1] != 3:
+        raise ValueError("cur must be [B, 3, H, W]")
+    B, _, H, W = cur.shape
+    pc = _ptr(cur, torch.float32, B * 3 * H * W, "cur")
+    if prev is not None:
+        if tuple(prev.shape) != tuple(cur.shape):
+            raise ValueError("prev and cur shapes differ")
+        pp = _ptr(prev, torch.float32, B * 3 * H * W, "prev")
+    else:
+        pp = c_void_p(0)
+    ang = _ptr(angle, torch.float64, B, "angle") if angle is not None else c_void_p(0)
+    _check(lib().fc_phase_correlate_rotation(ctx.handle, pp, pc, B, H, W, ang,
+                                             _ptr(shift_px, torch.float64, 2 * B, "shift_px"),
+                                             _stream(stream)))
 
 
 def select_state_bytes(B: int, H: int, W: int) -> int:

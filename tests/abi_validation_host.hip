@@ -188,6 +188,20 @@ int main() {
            FC_ERR_CAPACITY);
     EXPECT_DEVICE_FAIL(fc_phase_correlate(ctx, nullptr, f, 4, 448, 448, sp, nullptr, nullptr,
                                           nullptr));
+    EXPECT(fc_phase_correlate_rotation(nullptr, f, f, 1, 448, 448, sp, sp, nullptr),
+           FC_ERR_INVALID_ARG);
+    EXPECT(fc_phase_correlate_rotation(ctx, f, f, 1, 14, 448, sp, sp, nullptr), FC_ERR_UNSUPPORTED);
+    EXPECT(fc_phase_correlate_rotation(ctx, f, f, 1, 448, 448, sp, nullptr, nullptr),
+           FC_ERR_INVALID_ARG);
+    EXPECT(fc_phase_correlate_rotation(ctx, f, f, 5, 448, 448, sp, sp, nullptr), FC_ERR_CAPACITY);
+    EXPECT_DEVICE_FAIL(fc_phase_correlate_rotation(ctx, f, f, 2, 448, 224, nullptr, sp, nullptr));
+    q.align_rotation = 1;
+    EXPECT_DEVICE_FAIL(fc_select(ctx, &q, f, f, 1, 448, 448, &out, nullptr));
+    q.align_pixel = 0;
+    EXPECT(fc_select(ctx, &q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+    q.align_pixel = 1;
+    q.align_rotation = 2;
+    EXPECT(fc_select(ctx, &q, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
   }
 
   fc_layer_desc L = qwen_layer(h16);

@@ -163,4 +163,4 @@ def oracle_select_params(prm) -> osel.SelectParams:
                              adaptive=prm.adaptive, alpha_fixed=prm.alpha_fixed,
                              entropy_norm=prm.entropy_norm, tau_sim=prm.tau_sim,
                              align=prm.align, refresh=prm.refresh,
-                             align_pixel=prm.align_pixel)
+                             align_pixel=prm.align_pixel, align_rotation=prm.align_rotation)

@@ -157,3 +157,76 @@ def test_noalloc_with_pixel_alignment(fc):
     oa, ob = fcutil.select_out_np(a), fcutil.select_out_np(b)
     for k in oa:
         np.testing.assert_array_equal(oa[k], ob[k], err_msg=k)
+
+
+# ------------------------------------------------------ rotation (log-polar spectra)
+def rotated_pair(size, angle, roll):
+    """A shear-free trajectory frame and the same frame rotated by `angle` about its
+    centre (per channel, bilinear) and rolled by `roll` pixels."""
+    prev = fcdata.episode_frames(11, size=size, n_frames=1, shear=0.0)[0]
+    cur = np.stack([np.roll(osel.rotate_image(prev[c].astype(np.float64), -angle), roll,
+                            axis=(0, 1)) for c in range(3)]).astype(np.float32)
+    return prev, cur
+
+
+@pytest.mark.parametrize("size", [224, 448])
+def test_rotation_against_oracle(fc, size):
+    """fc_phase_correlate_rotation on pairs rotated by 0.0 / 0.06 / -0.12 rad and moved:
+    angle to 1e-8 rad and the centre's displacement to 1e-6 px of the oracle's."""
+    pairs = [rotated_pair(size, a, r) for a, r in ((0.0, (3, -7)), (0.06, (0, 0)),
+                                                   (-0.12, (-11, 5)))]
+    prev = np.stack([p for p, _ in pairs])
+    cur = np.stack([c for _, c in pairs])
+    B = len(pairs)
+    ctx = ctx_for(fc, B, size, size)
+    try:
+        sp = torch.empty(B, 2, dtype=torch.float64, device="cuda")
+        ang = torch.empty(B, dtype=torch.float64, device="cuda")
+        fc.fc_phase_correlate_rotation(ctx, torch.from_numpy(prev).cuda(),
+                                       torch.from_numpy(cur).cuda(), sp, ang)
+        torch.cuda.synchronize()
+        sp, ang = sp.cpu().numpy(), ang.cpu().numpy()
+    finally:
+        ctx.close()
+    for b in range(B):
+        a_o, d_o, _ = osel.rotation_phase_correlation(osel.luma(prev[b]), osel.luma(cur[b]))
+        assert abs(ang[b] - a_o) < 1e-8, (b, ang[b], a_o)
+        np.testing.assert_allclose(sp[b], d_o, rtol=0, atol=1e-6, err_msg=f"pair {b}")
+
+
+def test_selection_with_rotation(fc):
+    """fc_select with align_pixel and align_rotation on rotated-and-moved pairs and on
+    trajectory pairs, bit-exact against the oracle's selection (strict)."""
+    rot = [rotated_pair(224, a, r) for a, r in ((0.08, (28, 0)), (-0.05, (0, -30)))]
+    traj = fcdata.episode_frames(99, size=224, n_frames=3)
+    prev = np.concatenate([np.stack([p for p, _ in rot]), traj[:-1]])
+    cur = np.concatenate([np.stack([c for _, c in rot]), traj[1:]])
+    prm = fc.SelectParams(merge=2, align_pixel=True, align_rotation=True)
+    op = fcutil.oracle_select_params(prm)
+    B = prev.shape[0]
+    ctx = ctx_for(fc, B, 224, 224)
+    try:
+        out = fc.SelectOut.alloc(B, 64)
+        fc.fc_select(ctx, prm, torch.from_numpy(prev).cuda(), torch.from_numpy(cur).cuda(), out)
+        torch.cuda.synchronize()
+        o = fcutil.select_out_np(out)
+    finally:
+        ctx.close()
+    for b in range(B):
+        res = osel.select_item(prev[b], cur[b], op)
+        mg, esc = fcutil.check_select(o, res, op, b)
+        assert not esc, f"pair {b}: {esc}"
+
+
+def test_rotation_rejects_small_frames(fc):
+    ctx = ctx_for(fc, 1, 448, 448)
+    try:
+        sp = torch.empty(1, 2, dtype=torch.float64, device="cuda")
+        with pytest.raises(fc.FcError, match="UNSUPPORTED"):
+            fc.fc_phase_correlate_rotation(ctx, None, torch.zeros(1, 3, 14, 28, device="cuda"), sp)
+        out = fc.SelectOut.alloc(1, 4)
+        with pytest.raises(fc.FcError, match="INVALID_ARG"):
+            fc.fc_select(ctx, fc.SelectParams(merge=1, align_rotation=True), None,
+                         torch.zeros(1, 3, 28, 28, device="cuda"), out)
+    finally:
+        ctx.close()
