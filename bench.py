@@ -554,6 +554,10 @@ def bench_pixel_pc(fc, ctx, torch, prev, cur, out, base_p50):
     torch.cuda.synchronize()
     pc = timed_calls(torch, lambda: fc.fc_phase_correlate(ctx, prev, cur, shift_px))
     sel = timed_calls(torch, lambda: fc.fc_select(ctx, prm, prev, cur, out))
+    angle = torch.empty(B, dtype=torch.float64, device="cuda")
+    rot = timed_calls(torch, lambda: fc.fc_phase_correlate_rotation(ctx, prev, cur, shift_px, angle))
+    prm_rot = fc.SelectParams(align_pixel=True, align_rotation=True)
+    sel_rot = timed_calls(torch, lambda: fc.fc_select(ctx, prm_rot, prev, cur, out))
     fc.fc_profile_read(ctx, None, reset=True)
     fc.fc_profile_enable(ctx, True)
     for _ in range(20):
@@ -577,6 +581,7 @@ def bench_pixel_pc(fc, ctx, torch, prev, cur, out, base_p50):
     p50 = pc["p50"]
     return dict(workload="Eq. 4-1 on 448x448 luma (float64), 64 pairs",
                 phase_correlate_us=pc, select_align_pixel_us=sel,
+                phase_correlate_rotation_us=rot, select_align_rotation_us=sel_rot,
                 select_token_grid_p50_us=round(base_p50, 2), kernel_avg_us=kern,
                 frame_bytes=frames, workspace_bytes=int(ws),
                 frame_gbs_p50=round(frames / (p50 * 1e-6) / 1e9, 1),
