@@ -113,3 +113,37 @@ def token_embeddings(frames: np.ndarray, d: int, token_px: int, seed: int,
     px = np.asarray(frames, np.float32).reshape(nf, 3, gh, token_px, gw, token_px)
     px = px.transpose(0, 2, 4, 1, 3, 5).reshape(nf, gh * gw, 3 * token_px * token_px)
     return bf16_round(px @ proj)
+
+
+@dataclass(frozen=True)
+class VitShape:
+    """A vision-encoder block: hidden size, heads x head dim, MLP size."""
+    d: int
+    heads: int
+    hd: int
+    ffn: int
+    eps: float = 1e-6
+    theta: float = 10000.0
+
+
+QWEN_VIT = VitShape(d=1280, heads=16, hd=80, ffn=3420)     # Qwen2.5-VL vision block
+TINY_VIT = VitShape(d=160, heads=2, hd=80, ffn=192)
+
+
+def vit_weights(seed: int, shape: VitShape, std: float = 0.02) -> dict:
+    """Random-init weights of one vision block, bf16 bit patterns: linear weights and
+    biases N(0, std), RMSNorm gains 1 + N(0, 0.1).  Keys: w_qkv [3d, d] (rows q | k | v,
+    each head's dims contiguous), b_qkv [3d], w_o [d, d], b_o [d], w_gate / w_up [ffn, d],
+    b_gate / b_up [ffn], w_down [d, ffn], b_down [d], g1 [d], g2 [d]."""
+    rng = np.random.default_rng(seed)
+    d, f = shape.d, shape.ffn
+
+    def gain():
+        return bf16_round(1.0 + 0.1 * rng.standard_normal(d, dtype=np.float32))
+    return dict(
+        w_qkv=_normal_bf16(rng, (3 * d, d), std), b_qkv=_normal_bf16(rng, (3 * d,), std),
+        w_o=_normal_bf16(rng, (d, d), std), b_o=_normal_bf16(rng, (d,), std),
+        w_gate=_normal_bf16(rng, (f, d), std), b_gate=_normal_bf16(rng, (f,), std),
+        w_up=_normal_bf16(rng, (f, d), std), b_up=_normal_bf16(rng, (f,), std),
+        w_down=_normal_bf16(rng, (d, f), std), b_down=_normal_bf16(rng, (d,), std),
+        g1=gain(), g2=gain())
