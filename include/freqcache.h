@@ -177,6 +177,35 @@ typedef struct {
   int32_t *slot_map;
 } fc_kv_cache;
 
+/* One vision-encoder block (Qwen2.5-VL style; host struct, device bf16 pointers):
+ * pre-norm RMSNorm, q/k/v with bias, 2-D rotary positions, bidirectional attention,
+ * output projection with bias, SiLU-gated MLP with biases.
+ *   w_qkv [3 d][d] (rows q | k | v, each head's head_dim dims contiguous), b_qkv [3 d];
+ *   w_o [d][d], b_o [d]; w_gate_up [2 d_ffn][d] (gate rows, then up rows),
+ *   b_gate_up [2 d_ffn]; w_down [d][d_ffn], b_down [d]; g1, g2 [d] RMSNorm gains.
+ * d = n_heads head_dim; d and d_ffn multiples of 64 (pad the MLP with zero rows,
+ * columns and biases: exact); head_dim a multiple of 8 up to 128. */
+typedef struct {
+  int32_t d_model, n_heads, head_dim, d_ffn;
+  float rms_eps;            /* 1e-6 */
+  double rope_theta;        /* 1e4: frequencies theta^(-2 i / (head_dim / 2)), i < head_dim / 4 */
+  const uint16_t *w_qkv, *b_qkv, *w_o, *b_o, *w_gate_up, *b_gate_up, *w_down, *b_down;
+  const uint16_t *g1, *g2;
+} fc_vit_desc;
+
+/* The encoder's per-layer cache of one frame: raw (pre-rotary) keys and values of every
+ * patch, patches token-major: the merge x merge patches of merged token t = (I, J) are
+ * rows t merge^2 + a merge + c, at patch-grid position (I merge + a, J merge + c).
+ *   k, v: [B][grid_h grid_w merge^2][n_heads][head_dim] bf16 (device). */
+typedef struct {
+  uint16_t *k, *v;
+  int32_t grid_h, grid_w;   /* merged-token grid of the frame */
+  int32_t merge;            /* patches per merged token side (1 or 2) */
+  int32_t window;           /* attention window side in merged tokens (Qwen2.5-VL: 4,
+                               i.e. 112 px at 14-px patches and 2 x 2 merge); 0 = full
+                               attention over the frame */
+} fc_vit_cache;
+
 /* Library version string. */
 const char *fc_version(void);
 
@@ -305,6 +334,30 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
                            const uint16_t *x_cur, const int32_t *recompute_idx,
                            const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
                            void *stream);
+
+/* The vision-encoder side of the partial recompute (Sec. 4.1: flushed or refreshed
+ * tokens are recomputed by the visual encoder; reused ones keep their cached results),
+ * for one block.  The patches of the merged tokens recompute_idx[b][0 .. n_recompute[b])
+ * (the selection's ids, ascending) go through the block: their raw k, v are written to
+ * the cache, their queries attend to every key of their window (cached keys of reused
+ * patches, new ones of recomputed patches; keys rotated at their patch position), and
+ * their output rows are written to y.  Other rows of y and of the cache are untouched.
+ *   x, y: [B][grid_h grid_w merge^2][d_model] bf16 (device), token-major patch rows.
+ *   Capacity: the rows, B grid_h grid_w merge^2, use the layer workspace of the context
+ *   (each buffer's rows x width within max_batch max_tokens rows x its cap width);
+ *   patch grid sides up to 128.  Stream-ordered; allocates nothing. */
+fc_status fc_vit_block_forward(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
+                               const uint16_t *x, const int32_t *recompute_idx,
+                               const int32_t *n_recompute, uint16_t *y, int32_t B, void *stream);
+
+/* The encoder cache's preparation for a new frame (Sec. 4.1 / Eq. 4-2 at patch level):
+ * every reused merged token takes the merge^2 patch rows of K, V (from the cache, which
+ * holds the previous frame) and of the outputs (y_prev into y_cur) of its source token
+ * (I + di, J + dj).  shift [B][2], reuse_mask [B][grid_h grid_w]: from fc_select with
+ * the same merge.  y_prev, y_cur: [B][patches][d_model] bf16, distinct. */
+fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
+                              const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                              const uint8_t *reuse_mask, int32_t B, void *stream);
 
 /* Pixel-resolution phase correlation: Eq. 4-1 (Sec. 4.1) with the feature maps taken
  * as the frames' full-resolution BT.601 luma (float64).  The displacement is the first

@@ -15,7 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libfreqcache.so")
-SOURCES = ["abi.hip", "select.hip", "pixpc.hip", "layer.hip", "slotmap.hip"]
+SOURCES = ["abi.hip", "select.hip", "pixpc.hip", "layer.hip", "slotmap.hip", "vit.hip"]
 
 # gfx950 only.  Packed-FP32 instructions are disabled for all device code.
 FLAGS = [

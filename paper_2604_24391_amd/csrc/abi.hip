@@ -159,7 +159,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->spec, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
-                  c->krot, c->pix, c->vlog};
+                  c->krot, c->pix, c->vlog, c->vit_rows};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -256,6 +256,7 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
       (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||
       (st = dev_alloc(&ctx->stage, ctx->stage_elems, "stage")) != FC_OK ||
       (ctx->krot_elems && (st = dev_alloc(&ctx->krot, ctx->krot_elems, "rotated keys")) != FC_OK) ||
+      (st = dev_alloc(&ctx->vit_rows, B, "vision rows")) != FC_OK ||
       (st = fc::upload_select_tables()) != FC_OK) {
     free_ws(ctx);
     delete ctx;
@@ -556,6 +557,72 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
   if (st != FC_OK) return st;
   return fc::launch_cache_update_layers(ctx, *layer, n_layers, kvs, y_prev, y_cur, shift, reuse_mask,
                                         grid_w, B, reinterpret_cast<hipStream_t>(stream));
+}
+
+static fc_status check_vit(fc_ctx *ctx, const fc_vit_desc *L, const fc_vit_cache *c, int B,
+                           const char *who) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "%s: null context", who);
+  if (!L || !c) return fail(FC_ERR_INVALID_ARG, "%s: null layer or cache descriptor", who);
+  if (!c->k || !c->v) return fail(FC_ERR_INVALID_ARG, "%s: null K or V cache", who);
+  if (L->n_heads < 1 || L->head_dim < 8 || L->head_dim > 128 || L->head_dim % 8 ||
+      (long)L->n_heads * L->head_dim != L->d_model)
+    return fail(FC_ERR_INVALID_ARG, "%s: d_model %d must be n_heads %d x head_dim %d (head_dim a "
+                "multiple of 8 up to 128)", who, L->d_model, L->n_heads, L->head_dim);
+  if (L->d_model % fc::kGemmBK || L->d_model > 2048 || L->d_ffn < fc::kGemmBK ||
+      L->d_ffn % fc::kGemmBK || L->d_ffn > (1 << 20))
+    return fail(FC_ERR_SHAPE, "%s: d_model (<= 2048) and d_ffn must be multiples of %d", who,
+                fc::kGemmBK);
+  if (!(L->rms_eps > 0) || !(L->rope_theta > 1))
+    return fail(FC_ERR_INVALID_ARG, "%s: rms_eps must be > 0 and rope_theta > 1", who);
+  if (c->grid_h < 1 || c->grid_w < 1 || c->merge < 1 || c->merge > 4 || c->window < 0)
+    return fail(FC_ERR_INVALID_ARG, "%s: grid %dx%d, merge %d, window %d", who, c->grid_h,
+                c->grid_w, c->merge, c->window);
+  if ((long)c->grid_h * c->merge > 128 || (long)c->grid_w * c->merge > 128)
+    return fail(FC_ERR_UNSUPPORTED, "%s: patch grid sides up to 128", who);
+  if (B < 1) return fail(FC_ERR_SHAPE, "%s: B=%d", who, B);
+  const long N = (long)c->grid_h * c->grid_w;
+  const long slots = (long)B * N * c->merge * c->merge;
+  const fc_caps &cp = ctx->caps;
+  const long rows = (long)cp.max_batch * cp.max_tokens;
+  if (B > cp.max_batch || N > cp.max_tokens || slots * L->d_model > rows * cp.max_d_model ||
+      slots * L->d_model > rows * cp.max_qkv || slots * L->d_ffn > rows * cp.max_ffn)
+    return fail(FC_ERR_CAPACITY, "%s: B=%d x %ld patches of d=%d, ffn=%d exceed the context's "
+                "layer workspace", who, B, N * c->merge * c->merge, L->d_model, L->d_ffn);
+  return FC_OK;
+}
+
+fc_status fc_vit_block_forward(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
+                               const uint16_t *x, const int32_t *recompute_idx,
+                               const int32_t *n_recompute, uint16_t *y, int32_t B, void *stream) {
+  fc_status st = check_vit(ctx, layer, cache, B, "fc_vit_block_forward");
+  if (st != FC_OK) return st;
+  const fc_vit_desc &L = *layer;
+  if (!x || !recompute_idx || !n_recompute || !y)
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_block_forward: null activation or index buffer");
+  if (!L.w_qkv || !L.b_qkv || !L.w_o || !L.b_o || !L.w_gate_up || !L.b_gate_up || !L.w_down ||
+      !L.b_down || !L.g1 || !L.g2)
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_block_forward: null weight pointer");
+  if ((st = use_device(ctx)) != FC_OK) return st;
+  return fc::launch_vit_block(ctx, L, *cache, x, recompute_idx, n_recompute, y, B,
+                              reinterpret_cast<hipStream_t>(stream));
+}
+
+fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
+                              const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                              const uint8_t *reuse_mask, int32_t B, void *stream) {
+  fc_status st = check_vit(ctx, layer, cache, B, "fc_vit_cache_update");
+  if (st != FC_OK) return st;
+  if (!y_prev || !y_cur || !shift || !reuse_mask)
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: null buffer");
+  if (y_prev == y_cur) return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: y_prev and y_cur alias");
+  const long mm = (long)cache->merge * cache->merge;
+  // the in-place overwrite of the one frame slot stages the old K and V rows
+  if (2L * B * cache->grid_h * cache->grid_w * mm * layer->d_model > (long)ctx->stage_elems)
+    return fail(FC_ERR_CAPACITY, "fc_vit_cache_update: the frame's K/V rows exceed the context's "
+                "staging buffer");
+  if ((st = use_device(ctx)) != FC_OK) return st;
+  return fc::launch_vit_cache_update(ctx, *layer, *cache, y_prev, y_cur, shift, reuse_mask, B,
+                                     reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t fc_slot_state_bytes(int32_t B, int32_t S) { return fc::slot_state_bytes(B, S); }

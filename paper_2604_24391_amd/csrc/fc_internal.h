@@ -83,6 +83,7 @@ struct fc_ctx {
   size_t krot_elems = 0;
   unsigned char *pix = nullptr;  // pixel phase-correlation workspace, allocated at first use
   size_t pix_bytes = 0;
+  int32_t *vit_rows = nullptr;  // [max_batch] recomputed patch rows per item (vision block)
   uint16_t *vlog = nullptr;     // [B][S][kv row] values in row order (slot-mapped caches,
   size_t vlog_elems = 0;        // many-row layer calls only), allocated at first use
   // kernel timing
@@ -196,6 +197,21 @@ __device__ __forceinline__ int pool_row(const int32_t *map, int b, int S, int r)
   const int p = map[(long)b * S + r];
   return p < 0 ? 0 : (p >= S ? S - 1 : p);
 }
+
+// C[split][B N][Nout] = split-K partial sums of A[B N][K] W[Nout][K]^T over the first
+// nrec[b] rows of each item (the weight-streaming GEMM without an epilogue); K a multiple
+// of 64, Nout of 16.  *splits: the split count used.
+fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const uint16_t *A,
+                         const uint16_t *W, int K, int Nout, int N, const int32_t *nrec,
+                         float *part, int B, int *splits);
+
+// Vision-encoder block with partial recompute and its cache update (vit.hip).
+fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,
+                           const uint16_t *x, const int32_t *idx, const int32_t *nrec,
+                           uint16_t *y, int B, hipStream_t st);
+fc_status launch_vit_cache_update(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,
+                                  const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                                  const uint8_t *reuse, int B, hipStream_t st);
 
 // trail: recompute the text rows after the frames instead of the selected frame tokens
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,

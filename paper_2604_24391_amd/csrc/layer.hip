@@ -2169,6 +2169,18 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
   return FC_OK;
 }
 
+fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const uint16_t *A,
+                         const uint16_t *W, int K, int Nout, int N, const int32_t *nrec,
+                         float *part, int B, int *splits) {
+  WArgs g{};
+  g.A = A; g.W0 = W;
+  g.K = K; g.Nout = Nout; g.N = N; g.nrec = nrec;
+  g.part = part; g.rows = (long)B * N;
+  fc_status rc = run_wgemm<G_O>(ctx, st, name, g, B);
+  *splits = g.splits;
+  return rc;
+}
+
 fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                               const uint8_t *reuse, int grid_w, int B, hipStream_t st) {

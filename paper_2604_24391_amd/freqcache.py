@@ -31,7 +31,8 @@ FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
            "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
-           "fc_phase_correlate", "fc_phase_correlate_rotation", "fc_slot_state_bytes",
+           "fc_phase_correlate", "fc_phase_correlate_rotation", "fc_vit_block_forward",
+           "fc_vit_cache_update", "fc_slot_state_bytes",
            "fc_slot_map_init",
            "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
@@ -79,6 +80,18 @@ class fc_kv_cache(ctypes.Structure):
 _lib = None
 
 
+class fc_vit_desc(ctypes.Structure):
+    _fields_ = [("d_model", c_int32), ("n_heads", c_int32), ("head_dim", c_int32),
+                ("d_ffn", c_int32), ("rms_eps", ctypes.c_float), ("rope_theta", c_double)] + \
+        [(n, c_void_p) for n in ("w_qkv", "b_qkv", "w_o", "b_o", "w_gate_up", "b_gate_up",
+                                 "w_down", "b_down", "g1", "g2")]
+
+
+class fc_vit_cache(ctypes.Structure):
+    _fields_ = [("k", c_void_p), ("v", c_void_p), ("grid_h", c_int32), ("grid_w", c_int32),
+                ("merge", c_int32), ("window", c_int32)]
+
+
 def lib() -> ctypes.CDLL:
     """Load libfreqcache.so (fails loudly when it has not been built)."""
     global _lib
@@ -117,6 +130,12 @@ def lib() -> ctypes.CDLL:
                                              c_int32, c_void_p]
         L.fc_phase_correlate.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                          c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fc_vit_block_forward.argtypes = [c_void_p, ctypes.POINTER(fc_vit_desc),
+                                           ctypes.POINTER(fc_vit_cache), c_void_p, c_void_p,
+                                           c_void_p, c_void_p, c_int32, c_void_p]
+        L.fc_vit_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_vit_desc),
+                                          ctypes.POINTER(fc_vit_cache), c_void_p, c_void_p,
+                                          c_void_p, c_void_p, c_int32, c_void_p]
         L.fc_phase_correlate_rotation.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
                                                   c_int32, c_void_p, c_void_p, c_void_p]
         L.fc_slot_state_bytes.argtypes = [c_int32, c_int32]
@@ -132,6 +151,7 @@ def lib() -> ctypes.CDLL:
         for n in ("fc_create", "fc_destroy", "fc_select", "fc_select_noalloc", "fc_select_carry",
                   "fc_cache_update", "fc_cache_update_layers", "fc_layer_forward",
                   "fc_layer_forward_trail", "fc_phase_correlate", "fc_phase_correlate_rotation",
+                  "fc_vit_block_forward", "fc_vit_cache_update",
                   "fc_slot_map_init",
                   "fc_profile_enable",
                   "fc_profile_only", "fc_profile_read"):
@@ -555,6 +575,72 @@ def fc_cache_update_layers(ctx: Context, layer: LayerDesc, kvs, y_prevs, y_curs,
         ctx.handle, ctypes.byref(cl), n, cks, yp, yc,
         _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
+
+
+@dataclass
+class VitDesc:
+    """One vision-encoder block: bf16 device weights (w_gate_up stacks gate rows, then up
+    rows; d_ffn a multiple of 64, padded with zeros if needed)."""
+    d_model: int
+    n_heads: int
+    head_dim: int
+    d_ffn: int
+    w: dict
+    rms_eps: float = 1e-6
+    rope_theta: float = 10000.0
+
+    def c(self) -> fc_vit_desc:
+        d, f = self.d_model, self.d_ffn
+        sizes = dict(w_qkv=3 * d * d, b_qkv=3 * d, w_o=d * d, b_o=d, w_gate_up=2 * f * d,
+                     b_gate_up=2 * f, w_down=d * f, b_down=d, g1=d, g2=d)
+        ptrs = [_ptr(self.w[k], torch.bfloat16, n, k) for k, n in sizes.items()]
+        return fc_vit_desc(d, self.n_heads, self.head_dim, f, self.rms_eps, self.rope_theta, *ptrs)
+
+
+@dataclass
+class VitCache:
+    """One block's encoder cache: k, v [B, grid_h grid_w merge^2, n_heads, head_dim] bf16
+    (patch rows token-major); window: attention window side in merged tokens, 0 = full."""
+    k: torch.Tensor
+    v: torch.Tensor
+    grid_h: int
+    grid_w: int
+    merge: int = 2
+    window: int = 4
+
+    def c(self, B: int, d: int) -> fc_vit_cache:
+        n = B * self.grid_h * self.grid_w * self.merge * self.merge * d
+        return fc_vit_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
+                            self.grid_h, self.grid_w, self.merge, self.window)
+
+
+def fc_vit_block_forward(ctx: Context, layer: VitDesc, cache: VitCache, x: torch.Tensor,
+                         recompute_idx: torch.Tensor, n_recompute: torch.Tensor, y: torch.Tensor,
+                         stream=None):
+    """One vision block over the patches of the recomputed merged tokens (x, y:
+    [B, patches, d] bf16)."""
+    B = y.shape[0]
+    n = cache.grid_h * cache.grid_w
+    rows = B * n * cache.merge * cache.merge * layer.d_model
+    cl, cc = layer.c(), cache.c(B, layer.d_model)
+    _check(lib().fc_vit_block_forward(
+        ctx.handle, ctypes.byref(cl), ctypes.byref(cc), _ptr(x, torch.bfloat16, rows, "x"),
+        _ptr(recompute_idx, torch.int32, B * n, "recompute_idx"),
+        _ptr(n_recompute, torch.int32, B, "n_recompute"), _ptr(y, torch.bfloat16, rows, "y"), B,
+        _stream(stream)))
+
+
+def fc_vit_cache_update(ctx: Context, layer: VitDesc, cache: VitCache, y_prev: torch.Tensor,
+                        y_cur: torch.Tensor, shift: torch.Tensor, reuse_mask: torch.Tensor,
+                        stream=None):
+    B = y_cur.shape[0]
+    n = cache.grid_h * cache.grid_w
+    rows = B * n * cache.merge * cache.merge * layer.d_model
+    cl, cc = layer.c(), cache.c(B, layer.d_model)
+    _check(lib().fc_vit_cache_update(
+        ctx.handle, ctypes.byref(cl), ctypes.byref(cc), _ptr(y_prev, torch.bfloat16, rows, "y_prev"),
+        _ptr(y_cur, torch.bfloat16, rows, "y_cur"), _ptr(shift, torch.int32, 2 * B, "shift"),
+        _ptr(reuse_mask, torch.uint8, B * n, "reuse_mask"), B, _stream(stream)))
 
 
 def slot_state_bytes(B: int, S: int) -> int:

@@ -153,6 +153,7 @@ int main() {
   ctx->caps.max_d_model = 3584;
   ctx->caps.max_ffn = 18944;
   ctx->caps.max_qkv = 4608;
+  ctx->stage_elems = (size_t)4 * 256 * 4608;      // as fc_create sizes it for these caps
 
   EXPECT(fc_select(nullptr, &p, f, f, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
   EXPECT(fc_select(ctx, &p, f, f, 5, 448, 448, &out, nullptr), FC_ERR_CAPACITY);
@@ -346,6 +347,59 @@ int main() {
       ++g_fail;
     }
     (void)fc_slot_state_bytes(INT_MAX, INT_MAX);
+  }
+  {
+    // vision block
+    fc_vit_desc vd{};
+    vd.d_model = 1280;
+    vd.n_heads = 16;
+    vd.head_dim = 80;
+    vd.d_ffn = 3456;
+    vd.rms_eps = 1e-6f;
+    vd.rope_theta = 1e4;
+    vd.w_qkv = vd.b_qkv = vd.w_o = vd.b_o = vd.w_gate_up = vd.b_gate_up = vd.w_down = vd.b_down =
+        vd.g1 = vd.g2 = h16;
+    fc_vit_cache vc{};
+    vc.k = vc.v = h16;
+    vc.grid_h = vc.grid_w = 16;
+    vc.merge = 2;
+    vc.window = 4;
+    auto vfwd = [&](const fc_vit_desc &l, const fc_vit_cache &c, int B) {
+      return fc_vit_block_forward(ctx, &l, &c, h16, i32, i32, h16, B, nullptr);
+    };
+    EXPECT_DEVICE_FAIL(vfwd(vd, vc, 1));
+    EXPECT(fc_vit_block_forward(nullptr, &vd, &vc, h16, i32, i32, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_vit_block_forward(ctx, &vd, &vc, nullptr, i32, i32, h16, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(vfwd(vd, vc, 0), FC_ERR_SHAPE);
+    EXPECT(vfwd(vd, vc, 5), FC_ERR_CAPACITY);
+    fc_vit_desc l2 = vd;
+    l2.head_dim = 81;
+    EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);
+    l2 = vd;
+    l2.n_heads = INT_MAX;
+    EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);
+    l2 = vd;
+    l2.d_ffn = 3420;
+    EXPECT(vfwd(l2, vc, 1), FC_ERR_SHAPE);
+    l2 = vd;
+    l2.w_down = nullptr;
+    EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);
+    fc_vit_cache c2 = vc;
+    c2.grid_h = 65;
+    EXPECT(vfwd(vd, c2, 1), FC_ERR_UNSUPPORTED);
+    c2 = vc;
+    c2.grid_h = c2.grid_w = INT_MAX;
+    EXPECT(vfwd(vd, c2, 1), FC_ERR_UNSUPPORTED);
+    c2 = vc;
+    c2.window = -1;
+    EXPECT(vfwd(vd, c2, 1), FC_ERR_INVALID_ARG);
+    c2 = vc;
+    c2.k = nullptr;
+    EXPECT(vfwd(vd, c2, 1), FC_ERR_INVALID_ARG);
+    uint16_t *y2 = h16 + 8;
+    EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, i32, u8, 1, nullptr));
+    EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, h16, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, nullptr, u8, 1, nullptr), FC_ERR_INVALID_ARG);
   }
   EXPECT(fc_profile_enable(nullptr, 1), FC_ERR_INVALID_ARG);
   EXPECT(fc_profile_only(nullptr, "k"), FC_ERR_INVALID_ARG);
