@@ -72,6 +72,9 @@ def main():
     ap.add_argument("--layer-only", action="store_true",
                     help="run only the one-layer workload (reuse 0/25/50/75/90 %%) and print its "
                          "record (for profiling that workload on its own)")
+    ap.add_argument("--vit-only", action="store_true",
+                    help="run only the vision-block workload (windowed and full attention, "
+                         "reuse 0/25/50/75/90 %%) and print its record")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -106,6 +109,14 @@ def main():
     if args.layer_only:
         torch.cuda.set_device(0)
         rec = bench_layer_only(fc, torch)
+        if args.calib_mb > 0:
+            calib_copy(torch, args.calib_mb)
+        print(json.dumps(rec), flush=True)
+        return
+
+    if args.vit_only:
+        torch.cuda.set_device(0)
+        rec = bench_vit(fc, torch)
         if args.calib_mb > 0:
             calib_copy(torch, args.calib_mb)
         print(json.dumps(rec), flush=True)
@@ -284,6 +295,7 @@ def main():
         result["layer_ratios"] = bench_layer_ratios(fc, ctx, torch, layers[0], shape)
         result["tiny"] = bench_tiny(fc, torch)
         result["ablations"] = bench_ablations(fc, ctx, torch, frames, m, N)
+        result["vit"] = bench_vit(fc, torch)
         # the two targets of the hot path side by side: selection (64 pairs of 448x448)
         # against HBM peak, and the one-layer call against bf16 MFMA peak with its
         # roofline ceiling (compute time over the larger of compute and HBM time)
@@ -588,6 +600,94 @@ def bench_pixel_pc(fc, ctx, torch, prev, cur, out, base_p50):
                 frac_hbm_frames_p50=round(frames / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                 frac_hbm_with_workspace_p50=round((frames + ws) / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                 fp64_tflops_p50=round(flops / (p50 * 1e-6) / 1e12, 2))
+
+
+def bench_vit(fc, torch):
+    """One Qwen2.5-VL vision block (d 1280 = 16 heads x 80, SiLU MLP 3420 padded to 3456)
+    on a 448x448 frame (16x16 merged tokens of 2x2 patches, 1024 patch rows), windowed
+    (4x4 merged tokens) and full attention, at fixed random reuse ratios, B = 1."""
+    import fcdata
+    dev = torch.device("cuda:0")
+    sh = fcdata.QWEN_VIT
+    d, H, hd, fa = sh.d, sh.heads, sh.hd, sh.ffn
+    f = (fa + 63) // 64 * 64
+    gh = gw = 16
+    m = 2
+    N = gh * gw
+    Np = N * m * m
+    ctx = fc.Context(fc.Caps(max_batch=1, max_height=448, max_width=448, max_tokens=N,
+                             max_seq=64, max_d_model=4 * d, max_ffn=4 * f, max_qkv=4 * d))
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+
+    def randn(*shp, std=0.02):
+        return (torch.randn(*shp, device=dev, generator=g) * std).to(torch.bfloat16)
+    w_gu = randn(2 * f, d)
+    w_gu[fa:f].zero_()
+    w_gu[f + fa:].zero_()
+    w_dn = randn(d, f)
+    w_dn[:, fa:].zero_()
+    w = dict(w_qkv=randn(3 * d, d), b_qkv=randn(3 * d), w_o=randn(d, d), b_o=randn(d),
+             w_gate_up=w_gu, b_gate_up=torch.zeros(2 * f, device=dev, dtype=torch.bfloat16),
+             w_down=w_dn, b_down=randn(d), g1=torch.ones(d, device=dev, dtype=torch.bfloat16),
+             g2=torch.ones(d, device=dev, dtype=torch.bfloat16))
+    desc = fc.VitDesc(d, H, hd, f, w)
+    k = randn(1, Np, H, hd, std=1.0)
+    v = randn(1, Np, H, hd, std=1.0)
+    x = randn(1, Np, d, std=1.0)
+    y = randn(1, Np, d, std=1.0)
+    wbytes = 2 * (4 * d * d + 3 * f * d)
+    out = {}
+    for win in (4, 0):
+        cache = fc.VitCache(k, v, gh, gw, m, win)
+        keys = (win * win * m * m) if win else Np
+        rec = {}
+        for r in (0, 25, 50, 75, 90):
+            ids = fcdata.random_reuse_ids(200 + r, N, r)
+            n = len(ids)
+            idx = torch.full((1, N), -1, dtype=torch.int32)
+            idx[0, :n] = torch.from_numpy(ids)
+            idx = idx.cuda()
+            nrec = torch.tensor([n], dtype=torch.int32, device=dev)
+            dist = timed_calls(torch, lambda: fc.fc_vit_block_forward(ctx, desc, cache, x, idx,
+                                                                       nrec, y))
+            rows = n * m * m
+            flops = 2.0 * rows * (4 * d * d + 3 * fa * d) + 4.0 * rows * H * hd * keys
+            us = dist["p50"]
+            tf = flops / (us * 1e-6) / 1e12
+            gbs = wbytes / (us * 1e-6) / 1e9
+            rec[f"reuse{r}"] = dict(patch_rows=rows, us=dist, tflops_p50=round(tf, 1),
+                                    mfma_util_p50=round(tf / BF16_PEAK_TFLOPS, 4),
+                                    weight_gbs_p50=round(gbs, 1), flops=round(flops))
+        out["window4" if win else "full"] = rec
+    # per-kernel split of the windowed block at 50 % reuse
+    cache = fc.VitCache(k, v, gh, gw, m, 4)
+    ids = fcdata.random_reuse_ids(250, N, 50)
+    idx = torch.full((1, N), -1, dtype=torch.int32)
+    idx[0, :len(ids)] = torch.from_numpy(ids)
+    idx = idx.cuda()
+    nrec = torch.tensor([len(ids)], dtype=torch.int32, device=dev)
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    for _ in range(20):
+        fc.fc_vit_block_forward(ctx, desc, cache, x, idx, nrec, y)
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
+    kern = {}
+    for name in ("fc_vit_gather_norm", "fc_vit_gemm_qkv", "fc_vit_red_qkv", "fc_vit_attn",
+                 "fc_vit_gemm_o", "fc_vit_red_o", "fc_vit_gemm_gateup", "fc_vit_red_gu",
+                 "fc_vit_gemm_down", "fc_vit_red_down"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        kern[name] = round(tot * 1e3 / max(cnt, 1), 2)
+    fc.fc_profile_read(ctx, None, reset=True)
+    # the encoder of the deployed model: 32 blocks, full attention in 4 of them
+    enc = {f"reuse{r}": round((28 * out["window4"][f"reuse{r}"]["us"]["p50"]
+                              + 4 * out["full"][f"reuse{r}"]["us"]["p50"]) / 1e3, 3)
+           for r in (0, 25, 50, 75, 90)}
+    ctx.close()
+    return dict(workload="Qwen2.5-VL vision block, 448x448 frame, 1024 patch rows, B = 1",
+                blocks=out, kernel_avg_us_window4_reuse50=kern,
+                encoder_32_blocks_ms_est=enc, weight_bytes=wbytes)
 
 
 def bench_ablations(fc, ctx, torch, frames, m, N):

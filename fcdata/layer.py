@@ -147,3 +147,31 @@ def vit_weights(seed: int, shape: VitShape, std: float = 0.02) -> dict:
         w_up=_normal_bf16(rng, (f, d), std), b_up=_normal_bf16(rng, (f,), std),
         w_down=_normal_bf16(rng, (d, f), std), b_down=_normal_bf16(rng, (d,), std),
         g1=gain(), g2=gain())
+
+
+@dataclass(frozen=True)
+class MergerShape:
+    """The patch merger: per-patch hidden size d, merge side m, output size d_out."""
+    d: int
+    m: int
+    d_out: int
+    eps: float = 1e-6
+
+    @property
+    def hidden(self) -> int:
+        return self.m * self.m * self.d
+
+
+QWEN_MERGER = MergerShape(d=1280, m=2, d_out=3584)         # Qwen2.5-VL merger
+TINY_MERGER = MergerShape(d=160, m=2, d_out=256)
+
+
+def merger_weights(seed: int, shape: MergerShape, std: float = 0.02) -> dict:
+    """Random-init merger weights, bf16 bit patterns: g [d] = 1 + N(0, 0.1); w1 [hidden,
+    hidden], b1 [hidden], w2 [d_out, hidden], b2 [d_out] ~ N(0, std)."""
+    rng = np.random.default_rng(seed)
+    h = shape.hidden
+    return dict(g=bf16_round(1.0 + 0.1 * rng.standard_normal(shape.d, dtype=np.float32)),
+                w1=_normal_bf16(rng, (h, h), std), b1=_normal_bf16(rng, (h,), std),
+                w2=_normal_bf16(rng, (shape.d_out, h), std),
+                b2=_normal_bf16(rng, (shape.d_out,), std))

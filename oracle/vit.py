@@ -22,10 +22,17 @@ v from their input rows and attend, per block, to the keys of their window, the
 reused patches' keys and values coming from the cache (raw keys, rotated at their
 position in the current frame); their outputs replace the cached ones, and reused
 patches keep their cached outputs.
+
+The encoder ends in the 2 x 2 patch merger (Sec. 2.1: the visual tokens handed to the
+language model are merged patches): each patch row RMS-normalised, the m^2 rows of a
+merged token concatenated, then a two-layer MLP with biases and the exact (erf) GELU.
+It acts on each merged token alone, so only the recomputed tokens go through it.
 """
 from __future__ import annotations
 
 from dataclasses import dataclass
+
+import math
 
 import numpy as np
 
@@ -169,3 +176,37 @@ def vit_cache_update(k_cache, v_cache, y_prev, y_cur, shift, reuse_mask, gw: int
         vc[t * mm:(t + 1) * mm] = v_cache[s * mm:(s + 1) * mm]
         yc[t * mm:(t + 1) * mm] = y_prev[s * mm:(s + 1) * mm]
     return kc, vc, yc
+
+
+@dataclass(frozen=True)
+class MergerShape:
+    d: int = 1280          # vision hidden size (per patch)
+    m: int = 2             # merge side: m^2 patches per token
+    d_out: int = 3584      # language-model hidden size
+    eps: float = 1e-6
+
+    @property
+    def hidden(self) -> int:
+        return self.m * self.m * self.d
+
+
+def gelu(x: np.ndarray) -> np.ndarray:
+    """Exact GELU: x Phi(x) = x (1 + erf(x / sqrt 2)) / 2, erf in float64."""
+    xd = np.asarray(x, np.float64)
+    erf = np.vectorize(math.erf, otypes=[np.float64])
+    return (0.5 * xd * (1.0 + erf(xd / math.sqrt(2.0)))).astype(np.float32)
+
+
+def merger_rows(y_u16, tokens, wt_u16, shape: MergerShape) -> np.ndarray:
+    """The merger for the merged tokens `tokens` of one frame: y [Np, d] (the last
+    block's outputs, token-major patch rows); weights g [d] (per-patch RMSNorm gain),
+    w1 [hidden, hidden], b1 [hidden], w2 [d_out, hidden], b2 [d_out].  Returns
+    [len(tokens), d_out] float32."""
+    wt = {k: f32(v) for k, v in wt_u16.items()}
+    y = f32(y_u16)
+    mm = shape.m * shape.m
+    t = np.asarray(tokens, np.int64)
+    rows = (t[:, None] * mm + np.arange(mm)[None, :]).ravel()
+    xn = rmsnorm(y[rows], wt["g"], shape.eps).reshape(len(t), shape.hidden)
+    h = gelu(_lin(xn, wt["w1"], wt["b1"]))
+    return _lin(h, wt["w2"], wt["b2"]).astype(np.float32)

@@ -169,12 +169,13 @@ def test_vit_cache_update_matches_oracle(fc, ctx):
 
 
 def test_encoder_chain_driven_by_selection(fc, ctx):
-    """Three frames of a camera trajectory (224 x 224, 2 x 2 merge, 64 tokens): each step
+    """Four frames of a camera trajectory (224 x 224, 2 x 2 merge, 64 tokens; steps up to
+    30 px, so the shifts found are (-1, 0), (1, 0) and (4, 2) tokens): each step
     selects on the GPU, remaps the encoder cache and runs one vision block on the
     recomputed tokens; the oracle runs the same chain from the same start.  The
     selection must match bit for bit and the block's rows as in the single-call tests."""
     sh = SMALL
-    frames = fcdata.episode_frames(41, size=224, n_frames=3)
+    frames = fcdata.episode_frames(43, size=224, n_frames=4, max_step=30)
     m, gh, gw = 2, 8, 8
     mm = m * m
     np_ = gh * gw * mm
@@ -192,7 +193,7 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
     sel = fc.SelectOut.alloc(1, gh * gw)
     fr = torch.from_numpy(frames).cuda()
     cur = 0
-    for s in range(3):
+    for s in range(4):
         x = fcdata.bf16_round(rng.standard_normal((np_, sh.d), dtype=np.float32))
         nxt = 1 - cur
         fc.fc_select(ctx, prm, None if s == 0 else fr[s - 1:s], fr[s:s + 1], sel)

@@ -147,3 +147,54 @@ def test_vit_cache_update_moves_whole_tokens():
     np.testing.assert_array_equal(yc[0:4], y[4:8])
     np.testing.assert_array_equal(kc[8:], k[8:])
     assert not yc[8:].any()
+
+
+MSH = fcdata.TINY_MERGER
+OMSH = ov.MergerShape(d=MSH.d, m=MSH.m, d_out=MSH.d_out)
+
+
+def test_gelu_closed_forms():
+    """GELU(0) = 0; GELU(x) - GELU(-x) = x (Phi(x) + Phi(-x) = 1); GELU(1) = Phi(1) with
+    Phi(1) = 0.841344746068543 (normal table)."""
+    x = np.linspace(-4, 4, 33).astype(np.float32)
+    g = ov.gelu(x)
+    assert ov.gelu(np.float32(0.0)) == 0.0
+    np.testing.assert_allclose(g - ov.gelu(-x), x, atol=1e-6)
+    np.testing.assert_allclose(ov.gelu(np.float32(1.0)), 0.841344746068543, rtol=1e-7)
+
+
+def test_merger_matches_transformers():
+    """The merger of a few tokens against transformers' Qwen2.5-VL patch merger on the
+    same (bf16-valued) weights and inputs."""
+    from transformers.models.qwen2_5_vl.modeling_qwen2_5_vl import Qwen2_5_VLPatchMerger
+    wt = fcdata.merger_weights(40, MSH)
+    rng = np.random.default_rng(41)
+    n_tok = 12
+    y = fcdata.bf16_round(rng.standard_normal((n_tok * 4, MSH.d), dtype=np.float32))
+    toks = np.array([0, 3, 4, 11], np.int64)
+    got = ov.merger_rows(y, toks, wt, OMSH)
+    mod = Qwen2_5_VLPatchMerger(MSH.d_out, MSH.d, spatial_merge_size=2).float().eval()
+    t = {k: torch.from_numpy(fcdata.bf16_to_f32(v)) for k, v in wt.items()}
+    with torch.no_grad():
+        mod.ln_q.weight.copy_(t["g"])
+        mod.mlp[0].weight.copy_(t["w1"])
+        mod.mlp[0].bias.copy_(t["b1"])
+        mod.mlp[2].weight.copy_(t["w2"])
+        mod.mlp[2].bias.copy_(t["b2"])
+        want = mod(torch.from_numpy(fcdata.bf16_to_f32(y))).numpy()[toks]
+    np.testing.assert_allclose(got, want, rtol=2e-5, atol=2e-5)
+
+
+def test_merger_tokens_are_independent():
+    """A token's output depends only on its own m^2 patch rows: changing another token's
+    rows leaves it bit-identical, and the patch order inside the token matters."""
+    wt = fcdata.merger_weights(42, MSH)
+    rng = np.random.default_rng(43)
+    y = fcdata.bf16_round(rng.standard_normal((8 * 4, MSH.d), dtype=np.float32))
+    a = ov.merger_rows(y, [2], wt, OMSH)
+    y2 = y.copy()
+    y2[:8] = fcdata.bf16_round(rng.standard_normal((8, MSH.d), dtype=np.float32))
+    np.testing.assert_array_equal(ov.merger_rows(y2, [2], wt, OMSH), a)
+    y3 = y.copy()
+    y3[8:12] = y[[9, 8, 11, 10]]
+    assert not np.allclose(ov.merger_rows(y3, [2], wt, OMSH), a)
