@@ -680,13 +680,33 @@ def bench_vit(fc, torch):
         tot, cnt = fc.fc_profile_read(ctx, name)
         kern[name] = round(tot * 1e3 / max(cnt, 1), 2)
     fc.fc_profile_read(ctx, None, reset=True)
+    # the patch merger (1280 x 4 -> 5120 -> 3584) on the frame's 256 tokens
+    msh = fcdata.QWEN_MERGER
+    hid = msh.hidden
+    mw = dict(g=torch.ones(msh.d, device=dev, dtype=torch.bfloat16), w1=randn(hid, hid),
+              b1=randn(hid), w2=randn(msh.d_out, hid), b2=randn(msh.d_out))
+    mdesc = fc.MergerDesc(msh.d, msh.m, msh.d_out, mw)
+    xo = torch.empty(1, N, msh.d_out, device=dev, dtype=torch.bfloat16)
+    merger = {}
+    for r in (0, 50, 90):
+        ids = fcdata.random_reuse_ids(260 + r, N, r)
+        idx = torch.full((1, N), -1, dtype=torch.int32)
+        idx[0, :len(ids)] = torch.from_numpy(ids)
+        idx = idx.cuda()
+        nrec = torch.tensor([len(ids)], dtype=torch.int32, device=dev)
+        dist = timed_calls(torch, lambda: fc.fc_vit_merger_forward(ctx, mdesc, y, idx, nrec, xo))
+        flops = 2.0 * len(ids) * (hid * hid + hid * msh.d_out)
+        wb = 2 * (hid * hid + hid * msh.d_out)
+        merger[f"reuse{r}"] = dict(tokens=len(ids), us=dist,
+                                   tflops_p50=round(flops / (dist["p50"] * 1e-6) / 1e12, 1),
+                                   weight_gbs_p50=round(wb / (dist["p50"] * 1e-6) / 1e9, 1))
     # the encoder of the deployed model: 32 blocks, full attention in 4 of them
     enc = {f"reuse{r}": round((28 * out["window4"][f"reuse{r}"]["us"]["p50"]
                               + 4 * out["full"][f"reuse{r}"]["us"]["p50"]) / 1e3, 3)
            for r in (0, 25, 50, 75, 90)}
     ctx.close()
     return dict(workload="Qwen2.5-VL vision block, 448x448 frame, 1024 patch rows, B = 1",
-                blocks=out, kernel_avg_us_window4_reuse50=kern,
+                blocks=out, merger=merger, kernel_avg_us_window4_reuse50=kern,
                 encoder_32_blocks_ms_est=enc, weight_bytes=wbytes)
 
 

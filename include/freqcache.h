@@ -206,6 +206,18 @@ typedef struct {
                                attention over the frame */
 } fc_vit_cache;
 
+/* The encoder's patch merger (Qwen2.5-VL style; host struct, device bf16 pointers): each
+ * patch row RMS-normalised (gain g), the merge^2 patch rows of a merged token
+ * concatenated (hidden = merge^2 d_model), then hidden -> hidden with bias, exact (erf)
+ * GELU, hidden -> d_out with bias.
+ *   g [d_model]; w1 [hidden][hidden], b1 [hidden]; w2 [d_out][hidden], b2 [d_out].
+ * d_model a multiple of 64 up to 2048; d_out a multiple of 16. */
+typedef struct {
+  int32_t d_model, merge, d_out;
+  float rms_eps;            /* 1e-6 */
+  const uint16_t *g, *w1, *b1, *w2, *b2;
+} fc_merger_desc;
+
 /* Library version string. */
 const char *fc_version(void);
 
@@ -358,6 +370,20 @@ fc_status fc_vit_block_forward(fc_ctx *ctx, const fc_vit_desc *layer, const fc_v
 fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                               const uint8_t *reuse_mask, int32_t B, void *stream);
+
+/* The patch merger for the recomputed merged tokens only (it acts on each token alone;
+ * Sec. 2.1 merged visual tokens, Sec. 4.1 recompute): the language-model input rows
+ * x_out[b][recompute_idx[b][j]] for j < n_recompute[b]; other rows are untouched.
+ *   y:     [B][n_tokens merge^2][d_model] bf16, the last vision block's outputs
+ *          (token-major patch rows);
+ *   recompute_idx: [B][n_tokens], n_recompute: [B] (from fc_select with this merge);
+ *   x_out: [B][n_tokens][d_out] bf16.
+ *   Capacity: 2 B n_tokens hidden <= max_batch max_tokens max_ffn; the split-K
+ *   partials within the context's partial-sum workspace (FC_ERR_CAPACITY otherwise).
+ * Stream-ordered; allocates nothing. */
+fc_status fc_vit_merger_forward(fc_ctx *ctx, const fc_merger_desc *merger, const uint16_t *y,
+                                const int32_t *recompute_idx, const int32_t *n_recompute,
+                                uint16_t *x_out, int32_t n_tokens, int32_t B, void *stream);
 
 /* Pixel-resolution phase correlation: Eq. 4-1 (Sec. 4.1) with the feature maps taken
  * as the frames' full-resolution BT.601 luma (float64).  The displacement is the first

@@ -625,6 +625,37 @@ fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vi
                                      reinterpret_cast<hipStream_t>(stream));
 }
 
+fc_status fc_vit_merger_forward(fc_ctx *ctx, const fc_merger_desc *merger, const uint16_t *y,
+                                const int32_t *recompute_idx, const int32_t *n_recompute,
+                                uint16_t *x_out, int32_t n_tokens, int32_t B, void *stream) {
+  const char *who = "fc_vit_merger_forward";
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "%s: null context", who);
+  if (!merger) return fail(FC_ERR_INVALID_ARG, "%s: null merger descriptor", who);
+  const fc_merger_desc &M = *merger;
+  if (!y || !recompute_idx || !n_recompute || !x_out)
+    return fail(FC_ERR_INVALID_ARG, "%s: null activation or index buffer", who);
+  if (!M.g || !M.w1 || !M.b1 || !M.w2 || !M.b2)
+    return fail(FC_ERR_INVALID_ARG, "%s: null weight pointer", who);
+  if (M.merge < 1 || M.merge > 4)
+    return fail(FC_ERR_INVALID_ARG, "%s: merge %d (1 to 4)", who, M.merge);
+  if (M.d_model < fc::kGemmBK || M.d_model % fc::kGemmBK || M.d_model > 2048 || M.d_out < 16 ||
+      M.d_out % 16 || M.d_out > (1 << 16))
+    return fail(FC_ERR_SHAPE, "%s: d_model %d (a multiple of %d up to 2048) and d_out %d (a "
+                "multiple of 16)", who, M.d_model, fc::kGemmBK, M.d_out);
+  if (!(M.rms_eps > 0)) return fail(FC_ERR_INVALID_ARG, "%s: rms_eps must be > 0", who);
+  if (B < 1 || n_tokens < 1) return fail(FC_ERR_SHAPE, "%s: B=%d, n_tokens=%d", who, B, n_tokens);
+  const fc_caps &cp = ctx->caps;
+  const long hidden = (long)M.merge * M.merge * M.d_model;
+  const long rows = (long)cp.max_batch * cp.max_tokens;
+  if (B > cp.max_batch || n_tokens > cp.max_tokens || 2L * B * n_tokens * hidden > rows * cp.max_ffn)
+    return fail(FC_ERR_CAPACITY, "%s: B=%d x %d tokens of %ld merged features exceed the "
+                "context's MLP workspace", who, B, n_tokens, hidden);
+  fc_status st = use_device(ctx);
+  if (st != FC_OK) return st;
+  return fc::launch_vit_merger(ctx, M, y, recompute_idx, n_recompute, x_out, n_tokens, B,
+                               reinterpret_cast<hipStream_t>(stream));
+}
+
 size_t fc_slot_state_bytes(int32_t B, int32_t S) { return fc::slot_state_bytes(B, S); }
 
 fc_status fc_slot_map_init(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,

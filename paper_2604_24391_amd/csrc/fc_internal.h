@@ -212,6 +212,9 @@ fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache
 fc_status launch_vit_cache_update(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,
                                   const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                                   const uint8_t *reuse, int B, hipStream_t st);
+fc_status launch_vit_merger(fc_ctx *ctx, const fc_merger_desc &M, const uint16_t *y,
+                            const int32_t *idx, const int32_t *nrec, uint16_t *x_out, int N,
+                            int B, hipStream_t st);
 
 // trail: recompute the text rows after the frames instead of the selected frame tokens
 fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &kv,

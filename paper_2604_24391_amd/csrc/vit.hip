@@ -346,6 +346,64 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_down(
   }
 }
 
+// --------------------------------------------------------------------- patch merger
+// One workgroup per (item, recomputed token): the token's merge^2 patch rows, each
+// RMS-normalised with its own 1/rms, side by side as the token's bf16 GEMM row.
+__global__ __launch_bounds__(kVitThreads) void k_merge_norm(
+    const uint16_t *__restrict__ y, const uint16_t *__restrict__ gain,
+    const int32_t *__restrict__ idx, const int32_t *__restrict__ nrec, int N, int mm, int d,
+    float eps, uint16_t *__restrict__ hb) {
+  __shared__ float red[kVitThreads / 64];
+  const long s = blockIdx.x;
+  const int b = (int)(s / N), j = (int)(s - (long)b * N);
+  if (j >= min(max(nrec[b], 0), N)) return;
+  const int t = min(max(idx[s], 0), N - 1);
+  for (int a = 0; a < mm; ++a) {
+    const uint16_t *yr = y + (((long)b * N + t) * mm + a) * d;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) {
+      const float v = bf2f_v(yr[c]);
+      ss = fmaf(v, v, ss);
+    }
+    const float inv = 1.f / sqrtf(block_sum(ss, red) / (float)d + eps);
+    uint16_t *o = hb + (s * mm + a) * d;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) o[c] = f2bf_v(bf2f_v(yr[c]) * inv * bf2f_v(gain[c]));
+  }
+}
+
+// split-K sums + bias, then exact GELU (x Phi(x)), bf16
+__global__ __launch_bounds__(kVitThreads) void k_merge_red_gelu(
+    const float *__restrict__ part, int splits, const uint16_t *__restrict__ bias,
+    const int32_t *__restrict__ nrec, int N, int hidden, uint16_t *__restrict__ act) {
+  const long s = blockIdx.x;
+  const int b = (int)(s / N), j = (int)(s - (long)b * N);
+  if (j >= min(max(nrec[b], 0), N)) return;
+  const long rows = (long)gridDim.x;
+  for (int c = threadIdx.x; c < hidden; c += blockDim.x) {
+    float v = bf2f_v(bias[c]);
+    for (int sp = 0; sp < splits; ++sp) v += part[((long)sp * rows + s) * hidden + c];
+    act[s * hidden + c] = f2bf_v(0.5f * v * (1.f + erff(v * 0.70710678118654752f)));
+  }
+}
+
+// split-K sums + bias into the token's output row
+__global__ __launch_bounds__(kVitThreads) void k_merge_red_out(
+    const float *__restrict__ part, int splits, const uint16_t *__restrict__ bias,
+    const int32_t *__restrict__ idx, const int32_t *__restrict__ nrec, int N, int d_out,
+    uint16_t *__restrict__ x_out) {
+  const long s = blockIdx.x;
+  const int b = (int)(s / N), j = (int)(s - (long)b * N);
+  if (j >= min(max(nrec[b], 0), N)) return;
+  const int t = min(max(idx[s], 0), N - 1);
+  const long rows = (long)gridDim.x;
+  uint16_t *o = x_out + ((long)b * N + t) * d_out;
+  for (int c = threadIdx.x; c < d_out; c += blockDim.x) {
+    float v = bf2f_v(bias[c]);
+    for (int sp = 0; sp < splits; ++sp) v += part[((long)sp * rows + s) * d_out + c];
+    o[c] = f2bf_v(v);
+  }
+}
+
 }  // namespace
 
 fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,
@@ -444,6 +502,43 @@ fc_status launch_vit_cache_update(fc_ctx *ctx, const fc_vit_desc &L, const fc_vi
   kv.window = 1;
   kv.head = 0;
   return launch_cache_update(ctx, ld, kv, y_prev, y_cur, shift, reuse, c.grid_w, B, st);
+}
+
+fc_status launch_vit_merger(fc_ctx *ctx, const fc_merger_desc &M, const uint16_t *y,
+                            const int32_t *idx, const int32_t *nrec, uint16_t *x_out, int N,
+                            int B, hipStream_t st) {
+  const int mm = M.merge * M.merge;
+  const int hidden = mm * M.d_model;
+  const long slots = (long)B * N;
+  uint16_t *hb = ctx->act;                                   // normalised token rows
+  uint16_t *act = ctx->act + slots * hidden;                 // GELU outputs
+  int splits = 1;
+  fc_status rc;
+  {
+    ProfScope ps(ctx, st, "fc_merge_norm");
+    hipLaunchKernelGGL(k_merge_norm, dim3((unsigned)slots), dim3(kVitThreads), 0, st, y, M.g, idx,
+                       nrec, N, mm, M.d_model, M.rms_eps, hb);
+    FC_LAUNCH_OK(st, "k_merge_norm");
+  }
+  if ((rc = run_plain_gemm(ctx, st, "fc_merge_gemm1", hb, M.w1, hidden, hidden, N, nrec,
+                           ctx->part, B, &splits)) != FC_OK)
+    return rc;
+  {
+    ProfScope ps(ctx, st, "fc_merge_red_gelu");
+    hipLaunchKernelGGL(k_merge_red_gelu, dim3((unsigned)slots), dim3(kVitThreads), 0, st,
+                       (const float *)ctx->part, splits, M.b1, nrec, N, hidden, act);
+    FC_LAUNCH_OK(st, "k_merge_red_gelu");
+  }
+  if ((rc = run_plain_gemm(ctx, st, "fc_merge_gemm2", act, M.w2, hidden, M.d_out, N, nrec,
+                           ctx->part, B, &splits)) != FC_OK)
+    return rc;
+  {
+    ProfScope ps(ctx, st, "fc_merge_red_out");
+    hipLaunchKernelGGL(k_merge_red_out, dim3((unsigned)slots), dim3(kVitThreads), 0, st,
+                       (const float *)ctx->part, splits, M.b2, idx, nrec, N, M.d_out, x_out);
+    FC_LAUNCH_OK(st, "k_merge_red_out");
+  }
+  return FC_OK;
 }
 
 }  // namespace fc

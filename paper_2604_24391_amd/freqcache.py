@@ -32,7 +32,7 @@ EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select"
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
            "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
            "fc_phase_correlate", "fc_phase_correlate_rotation", "fc_vit_block_forward",
-           "fc_vit_cache_update", "fc_slot_state_bytes",
+           "fc_vit_cache_update", "fc_vit_merger_forward", "fc_slot_state_bytes",
            "fc_slot_map_init",
            "fc_profile_enable", "fc_profile_only", "fc_profile_read")
 
@@ -87,6 +87,11 @@ class fc_vit_desc(ctypes.Structure):
                                  "w_down", "b_down", "g1", "g2")]
 
 
+class fc_merger_desc(ctypes.Structure):
+    _fields_ = [("d_model", c_int32), ("merge", c_int32), ("d_out", c_int32),
+                ("rms_eps", ctypes.c_float)] + [(n, c_void_p) for n in ("g", "w1", "b1", "w2", "b2")]
+
+
 class fc_vit_cache(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("grid_h", c_int32), ("grid_w", c_int32),
                 ("merge", c_int32), ("window", c_int32)]
@@ -136,6 +141,9 @@ def lib() -> ctypes.CDLL:
         L.fc_vit_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_vit_desc),
                                           ctypes.POINTER(fc_vit_cache), c_void_p, c_void_p,
                                           c_void_p, c_void_p, c_int32, c_void_p]
+        L.fc_vit_merger_forward.argtypes = [c_void_p, ctypes.POINTER(fc_merger_desc), c_void_p,
+                                            c_void_p, c_void_p, c_void_p, c_int32, c_int32,
+                                            c_void_p]
         L.fc_phase_correlate_rotation.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
                                                   c_int32, c_void_p, c_void_p, c_void_p]
         L.fc_slot_state_bytes.argtypes = [c_int32, c_int32]
@@ -641,6 +649,38 @@ def fc_vit_cache_update(ctx: Context, layer: VitDesc, cache: VitCache, y_prev: t
         ctx.handle, ctypes.byref(cl), ctypes.byref(cc), _ptr(y_prev, torch.bfloat16, rows, "y_prev"),
         _ptr(y_cur, torch.bfloat16, rows, "y_cur"), _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * n, "reuse_mask"), B, _stream(stream)))
+
+
+@dataclass
+class MergerDesc:
+    """The patch merger: bf16 device weights g [d_model], w1 [hidden, hidden], b1 [hidden],
+    w2 [d_out, hidden], b2 [d_out] (hidden = merge^2 d_model)."""
+    d_model: int
+    merge: int
+    d_out: int
+    w: dict
+    rms_eps: float = 1e-6
+
+    def c(self) -> fc_merger_desc:
+        h = self.merge * self.merge * self.d_model
+        sizes = dict(g=self.d_model, w1=h * h, b1=h, w2=self.d_out * h, b2=self.d_out)
+        ptrs = [_ptr(self.w[k], torch.bfloat16, n, k) for k, n in sizes.items()]
+        return fc_merger_desc(self.d_model, self.merge, self.d_out, self.rms_eps, *ptrs)
+
+
+def fc_vit_merger_forward(ctx: Context, merger: MergerDesc, y: torch.Tensor,
+                          recompute_idx: torch.Tensor, n_recompute: torch.Tensor,
+                          x_out: torch.Tensor, stream=None):
+    """The merger for the recomputed tokens: y [B, tokens merge^2, d_model] bf16 ->
+    x_out [B, tokens, d_out] bf16 (rows of recompute_idx only)."""
+    B, n = recompute_idx.shape
+    mm = merger.merge * merger.merge
+    cm = merger.c()
+    _check(lib().fc_vit_merger_forward(
+        ctx.handle, ctypes.byref(cm), _ptr(y, torch.bfloat16, B * n * mm * merger.d_model, "y"),
+        _ptr(recompute_idx, torch.int32, B * n, "recompute_idx"),
+        _ptr(n_recompute, torch.int32, B, "n_recompute"),
+        _ptr(x_out, torch.bfloat16, B * n * merger.d_out, "x_out"), n, B, _stream(stream)))
 
 
 def slot_state_bytes(B: int, S: int) -> int:

@@ -401,6 +401,45 @@ int main() {
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, h16, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, nullptr, u8, 1, nullptr), FC_ERR_INVALID_ARG);
   }
+  {
+    // patch merger
+    fc_merger_desc md{};
+    md.d_model = 1280;
+    md.merge = 2;
+    md.d_out = 3584;
+    md.rms_eps = 1e-6f;
+    md.g = md.w1 = md.b1 = md.w2 = md.b2 = h16;
+    auto mfwd = [&](const fc_merger_desc &m, int n, int B) {
+      return fc_vit_merger_forward(ctx, &m, h16, i32, i32, h16, n, B, nullptr);
+    };
+    EXPECT_DEVICE_FAIL(mfwd(md, 256, 4));
+    EXPECT(fc_vit_merger_forward(nullptr, &md, h16, i32, i32, h16, 256, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_vit_merger_forward(ctx, nullptr, h16, i32, i32, h16, 256, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_vit_merger_forward(ctx, &md, h16, nullptr, i32, h16, 256, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(mfwd(md, 256, 0), FC_ERR_SHAPE);
+    EXPECT(mfwd(md, 0, 1), FC_ERR_SHAPE);
+    EXPECT(mfwd(md, 256, 5), FC_ERR_CAPACITY);
+    EXPECT(mfwd(md, 257, 1), FC_ERR_CAPACITY);
+    fc_merger_desc m2 = md;
+    m2.merge = 4;
+    m2.d_model = 2048;
+    EXPECT(mfwd(m2, 256, 4), FC_ERR_CAPACITY);
+    m2 = md;
+    m2.merge = 0;
+    EXPECT(mfwd(m2, 256, 1), FC_ERR_INVALID_ARG);
+    m2 = md;
+    m2.d_model = 1300;
+    EXPECT(mfwd(m2, 256, 1), FC_ERR_SHAPE);
+    m2 = md;
+    m2.d_out = 3580;
+    EXPECT(mfwd(m2, 256, 1), FC_ERR_SHAPE);
+    m2 = md;
+    m2.rms_eps = 0.f;
+    EXPECT(mfwd(m2, 256, 1), FC_ERR_INVALID_ARG);
+    m2 = md;
+    m2.w2 = nullptr;
+    EXPECT(mfwd(m2, 256, 1), FC_ERR_INVALID_ARG);
+  }
   EXPECT(fc_profile_enable(nullptr, 1), FC_ERR_INVALID_ARG);
   EXPECT(fc_profile_only(nullptr, "k"), FC_ERR_INVALID_ARG);
   {

@@ -86,7 +86,7 @@ def test_struct_layouts_match_the_header(fc, tmp_path):
     import subprocess
     structs = [fc.freqcache.fc_caps, fc.freqcache.fc_select_params, fc.freqcache.fc_select_out,
                fc.freqcache.fc_kv_cache, fc.freqcache.fc_layer_desc, fc.freqcache.fc_vit_desc,
-               fc.freqcache.fc_vit_cache]
+               fc.freqcache.fc_vit_cache, fc.freqcache.fc_merger_desc]
     cc = shutil.which("gcc") or shutil.which("cc")
     if cc is None:
         pytest.skip("no C compiler")

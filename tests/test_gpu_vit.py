@@ -14,6 +14,7 @@ from tests import fcutil
 pytestmark = pytest.mark.gpu
 
 SMALL = fcdata.VitShape(d=320, heads=4, hd=80, ffn=448)
+SMALL_MERGER = fcdata.MergerShape(d=320, m=2, d_out=256)
 
 
 @pytest.fixture(scope="module")
@@ -171,8 +172,9 @@ def test_vit_cache_update_matches_oracle(fc, ctx):
 def test_encoder_chain_driven_by_selection(fc, ctx):
     """Four frames of a camera trajectory (224 x 224, 2 x 2 merge, 64 tokens; steps up to
     30 px, so the shifts found are (-1, 0), (1, 0) and (4, 2) tokens): each step
-    selects on the GPU, remaps the encoder cache and runs one vision block on the
-    recomputed tokens; the oracle runs the same chain from the same start.  The
+    selects on the GPU, remaps the encoder cache, runs one vision block on the recomputed
+    tokens and the patch merger on their outputs; the oracle runs the same chain from
+    the same start.  The
     selection must match bit for bit and the block's rows as in the single-call tests."""
     sh = SMALL
     frames = fcdata.episode_frames(43, size=224, n_frames=4, max_step=30)
@@ -192,6 +194,9 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
     ko, vo, yo = ov.f32(k0), ov.f32(k0), [ov.f32(y0), ov.f32(y0)]
     sel = fc.SelectOut.alloc(1, gh * gw)
     fr = torch.from_numpy(frames).cuda()
+    mwt = fcdata.merger_weights(342, SMALL_MERGER)
+    mdesc = merger_desc(fc, mwt, SMALL_MERGER)
+    xo_g = torch.zeros(1, gh * gw, SMALL_MERGER.d_out, dtype=torch.bfloat16, device="cuda")
     cur = 0
     for s in range(4):
         x = fcdata.bf16_round(rng.standard_normal((np_, sh.d), dtype=np.float32))
@@ -215,5 +220,66 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
         assert fcutil.rel_l2(kgn, ko) <= fcutil.LAYER_RTOL, s
         if rows.size:
             assert fcutil.rel_l2(yg[rows], y[rows]) <= fcutil.LAYER_RTOL, s
+        # the merger on the block's outputs: the decoder's input rows of the recomputed tokens
+        fc.fc_vit_merger_forward(ctx, mdesc, ys[nxt], sel.recompute_idx, sel.n_recompute, xo_g)
+        torch.cuda.synchronize()
+        if res.n_recompute:
+            want = ov.merger_rows(y, res.recompute_idx, mwt, omerger(SMALL_MERGER))
+            got = fcdata.bf16_to_f32(fcutil.bf16_np(xo_g)[0][res.recompute_idx])
+            assert fcutil.rel_l2(got, want) <= fcutil.LAYER_RTOL, s
         print(f"step {s}: recomputed {res.n_recompute} tokens, shift {res.shift}")
         cur = nxt
+
+
+def merger_desc(fc, wt, sh):
+    return fc.MergerDesc(sh.d, sh.m, sh.d_out, {k: fcutil.bf16_gpu(v) for k, v in wt.items()})
+
+
+def omerger(sh):
+    return ov.MergerShape(d=sh.d, m=sh.m, d_out=sh.d_out)
+
+
+def check_merger(fc, ctx, sh, n_tokens, ids_per_item, seed):
+    B = len(ids_per_item)
+    mm = sh.m * sh.m
+    wt = fcdata.merger_weights(seed, sh)
+    rng = np.random.default_rng(seed + 1)
+    y = fcdata.bf16_round(rng.standard_normal((B, n_tokens * mm, sh.d), dtype=np.float32))
+    x0 = fcdata.bf16_round(rng.standard_normal((B, n_tokens, sh.d_out), dtype=np.float32))
+    idx = np.full((B, n_tokens), -1, np.int32)
+    nrec = np.zeros(B, np.int32)
+    for b, ids in enumerate(ids_per_item):
+        idx[b, :len(ids)] = ids
+        nrec[b] = len(ids)
+    xg = fcutil.bf16_gpu(x0)
+    fc.fc_vit_merger_forward(ctx, merger_desc(fc, wt, sh), fcutil.bf16_gpu(y),
+                             torch.from_numpy(idx).cuda(), torch.from_numpy(nrec).cuda(), xg)
+    torch.cuda.synchronize()
+    x = fcutil.bf16_np(xg)
+    worst = 0.0
+    for b, ids in enumerate(ids_per_item):
+        keep = np.setdiff1d(np.arange(n_tokens), ids)
+        np.testing.assert_array_equal(x[b][keep], x0[b][keep])
+        if len(ids) == 0:
+            continue
+        want = ov.merger_rows(y[b], ids, wt, omerger(sh))
+        err = fcutil.rel_l2(fcdata.bf16_to_f32(x[b][ids]), want)
+        print(f"merger item {b}: {len(ids)} tokens, rel-L2 {err:.2e}")
+        assert err <= fcutil.LAYER_RTOL
+        worst = max(worst, err)
+    return worst
+
+
+def test_merger_small_ragged_and_edges(fc, ctx):
+    """d 320, 2 x 2 merge (hidden 1280) -> 256, 64 tokens: items recomputing 30 %, none,
+    and all of their tokens."""
+    check_merger(fc, ctx, SMALL_MERGER, 64,
+                 [np.sort(fcdata.random_reuse_ids(350, 64, 70)), np.array([], np.int32)], 351)
+    check_merger(fc, ctx, SMALL_MERGER, 64, [np.arange(64, dtype=np.int32)], 352)
+
+
+def test_merger_qwen_shape(fc, ctx):
+    """The Qwen2.5-VL merger (1280 x 4 = 5120 -> 5120 -> 3584) on a 448 x 448 frame's 256
+    tokens, half of them recomputed."""
+    check_merger(fc, ctx, fcdata.QWEN_MERGER, 256,
+                 [np.sort(fcdata.random_reuse_ids(360, 256, 50))], 361)
