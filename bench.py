@@ -437,6 +437,35 @@ def timed_calls(torch, fn, reps=60, warm=5):
                 p90=round(float(np.percentile(us, 90)), 2), runs=reps)
 
 
+def graph_us(torch, fn, calls=10, reps=20):
+    """GPU time per call (us) of fn replayed from a HIP graph holding `calls` back-to-back
+    calls (the host launch cost of the individual kernels taken out), median of `reps`
+    replays, each bracketed by its own pair of HIP events."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(calls):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record()
+        graph.replay()
+        b.record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 / calls for a, b in evs])
+    del graph
+    return round(float(np.median(us)), 2)
+
+
 def observed_sclk_mhz():
     """Current shader clock of GPU 0: the level the driver marks current in its pp_dpm_sclk
     table (what rocm-smi --showclocks prints), found through the device's PCI bus id; None
@@ -651,14 +680,18 @@ def bench_vit(fc, torch):
             nrec = torch.tensor([n], dtype=torch.int32, device=dev)
             dist = timed_calls(torch, lambda: fc.fc_vit_block_forward(ctx, desc, cache, x, idx,
                                                                        nrec, y))
+            gus = graph_us(torch, lambda: fc.fc_vit_block_forward(ctx, desc, cache, x, idx, nrec,
+                                                                  y))
             rows = n * m * m
             flops = 2.0 * rows * (4 * d * d + 3 * fa * d) + 4.0 * rows * H * hd * keys
             us = dist["p50"]
             tf = flops / (us * 1e-6) / 1e12
+            tfg = flops / (gus * 1e-6) / 1e12
             gbs = wbytes / (us * 1e-6) / 1e9
             rec[f"reuse{r}"] = dict(patch_rows=rows, us=dist, tflops_p50=round(tf, 1),
                                     mfma_util_p50=round(tf / BF16_PEAK_TFLOPS, 4),
-                                    weight_gbs_p50=round(gbs, 1), flops=round(flops))
+                                    weight_gbs_p50=round(gbs, 1), flops=round(flops),
+                                    graph_us=gus, mfma_util_graph=round(tfg / BF16_PEAK_TFLOPS, 4))
         out["window4" if win else "full"] = rec
     # per-kernel split of the windowed block at 50 % reuse
     cache = fc.VitCache(k, v, gh, gw, m, 4)
@@ -695,18 +728,34 @@ def bench_vit(fc, torch):
         idx = idx.cuda()
         nrec = torch.tensor([len(ids)], dtype=torch.int32, device=dev)
         dist = timed_calls(torch, lambda: fc.fc_vit_merger_forward(ctx, mdesc, y, idx, nrec, xo))
+        gus = graph_us(torch, lambda: fc.fc_vit_merger_forward(ctx, mdesc, y, idx, nrec, xo))
         flops = 2.0 * len(ids) * (hid * hid + hid * msh.d_out)
         wb = 2 * (hid * hid + hid * msh.d_out)
         merger[f"reuse{r}"] = dict(tokens=len(ids), us=dist,
                                    tflops_p50=round(flops / (dist["p50"] * 1e-6) / 1e12, 1),
-                                   weight_gbs_p50=round(wb / (dist["p50"] * 1e-6) / 1e9, 1))
+                                   weight_gbs_p50=round(wb / (dist["p50"] * 1e-6) / 1e9, 1),
+                                   graph_us=gus,
+                                   weight_gbs_graph=round(wb / (gus * 1e-6) / 1e9, 1))
+    fc.fc_profile_read(ctx, None, reset=True)
+    fc.fc_profile_enable(ctx, True)
+    for _ in range(20):
+        fc.fc_vit_merger_forward(ctx, mdesc, y, idx, nrec, xo)
+    torch.cuda.synchronize()
+    fc.fc_profile_enable(ctx, False)
+    mkern = {}
+    for name in ("fc_merge_norm", "fc_merge_gemm1", "fc_merge_red_gelu", "fc_merge_gemm2",
+                 "fc_merge_red_out"):
+        tot, cnt = fc.fc_profile_read(ctx, name)
+        mkern[name] = round(tot * 1e3 / max(cnt, 1), 2)
+    fc.fc_profile_read(ctx, None, reset=True)
     # the encoder of the deployed model: 32 blocks, full attention in 4 of them
-    enc = {f"reuse{r}": round((28 * out["window4"][f"reuse{r}"]["us"]["p50"]
-                              + 4 * out["full"][f"reuse{r}"]["us"]["p50"]) / 1e3, 3)
+    enc = {f"reuse{r}": round((28 * out["window4"][f"reuse{r}"]["graph_us"]
+                              + 4 * out["full"][f"reuse{r}"]["graph_us"]) / 1e3, 3)
            for r in (0, 25, 50, 75, 90)}
     ctx.close()
     return dict(workload="Qwen2.5-VL vision block, 448x448 frame, 1024 patch rows, B = 1",
                 blocks=out, merger=merger, kernel_avg_us_window4_reuse50=kern,
+                merger_kernel_avg_us_reuse90=mkern,
                 encoder_32_blocks_ms_est=enc, weight_bytes=wbytes)
 
 

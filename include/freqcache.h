@@ -184,7 +184,7 @@ typedef struct {
  *   w_o [d][d], b_o [d]; w_gate_up [2 d_ffn][d] (gate rows, then up rows),
  *   b_gate_up [2 d_ffn]; w_down [d][d_ffn], b_down [d]; g1, g2 [d] RMSNorm gains.
  * d = n_heads head_dim; d and d_ffn multiples of 64 (pad the MLP with zero rows,
- * columns and biases: exact); head_dim a multiple of 8 up to 128. */
+ * columns and biases: exact); head_dim a multiple of 16 up to 128. */
 typedef struct {
   int32_t d_model, n_heads, head_dim, d_ffn;
   float rms_eps;            /* 1e-6 */

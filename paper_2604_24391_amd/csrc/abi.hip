@@ -159,7 +159,7 @@ fc_status dev_alloc(T **p, size_t count, const char *what) {
 void free_ws(fc_ctx *c) {
   void *ptrs[] = {c->spec, c->penergy, c->pdot, c->qbuf, c->attn,
                   c->h1,  c->hb,    c->act,     c->part,    c->rope, c->stage, c->ssq,
-                  c->krot, c->pix, c->vlog, c->vit_rows};
+                  c->krot, c->pix, c->vlog, c->vit_rows, c->vit_rope};
   for (void *p : ptrs)
     if (p) hipFree(p);
   for (auto &r : c->recs) {
@@ -256,7 +256,8 @@ fc_status fc_create(fc_ctx **out, int32_t device, const fc_caps *caps) {
       (st = dev_alloc(&ctx->rope, (size_t)c.max_seq * 64, "rope")) != FC_OK ||
       (st = dev_alloc(&ctx->stage, ctx->stage_elems, "stage")) != FC_OK ||
       (ctx->krot_elems && (st = dev_alloc(&ctx->krot, ctx->krot_elems, "rotated keys")) != FC_OK) ||
-      (st = dev_alloc(&ctx->vit_rows, B, "vision rows")) != FC_OK ||
+      (st = dev_alloc(&ctx->vit_rows, B + 1, "vision rows")) != FC_OK ||
+      (st = dev_alloc(&ctx->vit_rope, (size_t)128 * 32, "vision rotary table")) != FC_OK ||
       (st = fc::upload_select_tables()) != FC_OK) {
     free_ws(ctx);
     delete ctx;
@@ -564,10 +565,10 @@ static fc_status check_vit(fc_ctx *ctx, const fc_vit_desc *L, const fc_vit_cache
   if (!ctx) return fail(FC_ERR_INVALID_ARG, "%s: null context", who);
   if (!L || !c) return fail(FC_ERR_INVALID_ARG, "%s: null layer or cache descriptor", who);
   if (!c->k || !c->v) return fail(FC_ERR_INVALID_ARG, "%s: null K or V cache", who);
-  if (L->n_heads < 1 || L->head_dim < 8 || L->head_dim > 128 || L->head_dim % 8 ||
+  if (L->n_heads < 1 || L->head_dim < 16 || L->head_dim > 128 || L->head_dim % 16 ||
       (long)L->n_heads * L->head_dim != L->d_model)
     return fail(FC_ERR_INVALID_ARG, "%s: d_model %d must be n_heads %d x head_dim %d (head_dim a "
-                "multiple of 8 up to 128)", who, L->d_model, L->n_heads, L->head_dim);
+                "multiple of 16 up to 128)", who, L->d_model, L->n_heads, L->head_dim);
   if (L->d_model % fc::kGemmBK || L->d_model > 2048 || L->d_ffn < fc::kGemmBK ||
       L->d_ffn % fc::kGemmBK || L->d_ffn > (1 << 20))
     return fail(FC_ERR_SHAPE, "%s: d_model (<= 2048) and d_ffn must be multiples of %d", who,
@@ -584,8 +585,11 @@ static fc_status check_vit(fc_ctx *ctx, const fc_vit_desc *L, const fc_vit_cache
   const long slots = (long)B * N * c->merge * c->merge;
   const fc_caps &cp = ctx->caps;
   const long rows = (long)cp.max_batch * cp.max_tokens;
+  // the O reduction's sums of squares: one per slot and 1024-column chunk
+  const long ssq_cap = rows * std::max<long>(8, (cp.max_d_model + 127) / 128);
   if (B > cp.max_batch || N > cp.max_tokens || slots * L->d_model > rows * cp.max_d_model ||
-      slots * L->d_model > rows * cp.max_qkv || slots * L->d_ffn > rows * cp.max_ffn)
+      slots * L->d_model > rows * cp.max_qkv || slots * L->d_ffn > rows * cp.max_ffn ||
+      slots * ((L->d_model + 1023) / 1024) > ssq_cap)
     return fail(FC_ERR_CAPACITY, "%s: B=%d x %ld patches of d=%d, ffn=%d exceed the context's "
                 "layer workspace", who, B, N * c->merge * c->merge, L->d_model, L->d_ffn);
   return FC_OK;

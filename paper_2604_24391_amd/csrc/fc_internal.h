@@ -47,6 +47,7 @@ constexpr int kMaxSplits = 16;
 // Layer calls with at least this many token slots (B * N) run the large-M path:
 // square MFMA tiles with fused epilogues and keys rotated once per call.
 constexpr long kBigRows = 2048;
+constexpr long kPlainBigRows = 512;  // rows from which run_plain_gemm takes the 256 x 256 tiles
 
 // ----------------------------------------------------------------------------- context
 struct ProfRec {
@@ -83,7 +84,9 @@ struct fc_ctx {
   size_t krot_elems = 0;
   unsigned char *pix = nullptr;  // pixel phase-correlation workspace, allocated at first use
   size_t pix_bytes = 0;
-  int32_t *vit_rows = nullptr;  // [max_batch] recomputed patch rows per item (vision block)
+  int32_t *vit_rows = nullptr;  // [max_batch + 1] recomputed patch rows per item (vision
+                                // block), then the split count of the last many-row GEMM
+  float2 *vit_rope = nullptr;   // [128][32] vision rotary (cos, sin) by position, frequency
   uint16_t *vlog = nullptr;     // [B][S][kv row] values in row order (slot-mapped caches,
   size_t vlog_elems = 0;        // many-row layer calls only), allocated at first use
   // kernel timing
@@ -198,12 +201,18 @@ __device__ __forceinline__ int pool_row(const int32_t *map, int b, int S, int r)
   return p < 0 ? 0 : (p >= S ? S - 1 : p);
 }
 
-// C[split][B N][Nout] = split-K partial sums of A[B N][K] W[Nout][K]^T over the first
-// nrec[b] rows of each item (the weight-streaming GEMM without an epilogue); K a multiple
-// of 64, Nout of 16.  *splits: the split count used.
+// Split-K partial sums of A[B N][K] W[Nout][K]^T over the first nrec[b] rows of each
+// item, no epilogue; K a multiple of 64, Nout of 16.  Few rows: the weight-streaming GEMM,
+// part = C[split][B N][Nout], *splits = its split count, *dsplits_used = null, *tiles = 0.
+// Many rows (and dsplits given): the 256 x 256-tile GEMM over the rows packed across
+// items (item b's rows after those of items < b), part = [split][*tiles] tiles of
+// [256 packed rows][256 columns] (tile mt ceil(Nout / 256) + nt); its split count (at
+// most 4) is decided on the device and written to *dsplits; *splits = 4 and
+// *dsplits_used = dsplits.
 fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const uint16_t *A,
                          const uint16_t *W, int K, int Nout, int N, const int32_t *nrec,
-                         float *part, int B, int *splits);
+                         float *part, int B, int *splits, int *dsplits,
+                         const int **dsplits_used, int *tiles);
 
 // Vision-encoder block with partial recompute and its cache update (vit.hip).
 fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,

@@ -107,7 +107,7 @@ __device__ __forceinline__ int rope_pos(const MRope &m, int seqpos, int k) {
 // Split-K partial sums go to a float32 buffer [split][rows][cols] that the k_red_*
 // kernels reduce; the SwiGLU mode applies the MLP RMSNorm and SiLU(g) * u in its own
 // epilogue.
-enum { G_QKV = 0, G_O = 1, G_GU = 2, G_DOWN = 3 };
+enum { G_QKV = 0, G_O = 1, G_GU = 2, G_DOWN = 3, G_PLAIN = 4 };   // PLAIN: fp32 sums only (k_mgemm)
 constexpr int KS = kGemmBK;                 // 64 K values per step
 constexpr int RB = KS * 2;                  // bytes per staged operand row
 constexpr int MT = 256;                     // rows per M tile
@@ -682,8 +682,23 @@ struct MArgs {
   int cus;                        // workgroup slots: one resident workgroup per CU
   int part_units;                 // 256 x 256 fp32 tiles the partial buffer holds
   float *part;                    // K-range partial tiles of the split tail
+  float *out;                     // G_PLAIN output: [ks][mtiles][ntn] tiles of 256 x 256 fp32
+  int *ks_out;                    // G_PLAIN: the K-range part count ks, written by workgroup 0
   RedArgs r;                      // epilogue operands (as the reductions use them)
 };
+
+// G_PLAIN: when the tiles fill at most half the CUs, every tile runs as ks K-range parts
+// (at most 4, at least 4 K steps each), written as separate sums that the consumer adds.
+__host__ __device__ inline int plain_split(int tiles, int cus, int nk) {
+  int ks = 1;
+  if (tiles > 0 && 2 * tiles <= cus) {
+    ks = cus / tiles;
+    ks = ks < 4 ? ks : 4;
+    ks = ks < nk / 4 ? ks : nk / 4;
+    ks = ks > 1 ? ks : 1;
+  }
+  return ks;
+}
 
 // With one workgroup per CU, tiles run in rounds of `cus`.  When there are few rounds
 // and the last is at most half full, its `tail` tiles run as `ks` parts over K ranges
@@ -785,7 +800,7 @@ __device__ __forceinline__ void mg_epi_rows8(const MArgs &a, const int *pre, Row
     rv[it] = rows(it) < nvalid;
     bi[it] = 0;
     slot[it] = rv[it] ? packed_slot(pre, a.B, a.N, row0 + rows(it), bi[it]) : 0;
-    tok[it] = (MODE != G_GU && rv[it]) ? tok_of(r.idx, slot[it], a.N) : 0;
+    tok[it] = (MODE != G_GU && MODE != G_PLAIN && rv[it]) ? tok_of(r.idx, slot[it], a.N) : 0;
   }
   // residual inputs: x rows for O, h1 rows for down
   uint2 xin[MODE == G_O ? 8 : 1];
@@ -886,19 +901,32 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   // tiles as K-range parts
   const int V = (pre[a.B] + MB - 1) / MB;
   const int nk = a.K / KS;
-  int F, tail, ks;
-  mtail_split(V * a.ntn, a.cus, a.part_units, nk, F, tail, ks);
   const int bid = blockIdx.x;
-  if (bid >= F + tail * ks) return;
+  int split = 0;
   int mt, nt, kb = 0, ke = nk, unit = -1;
-  if (bid < F) {
-    mtile_of(V, a.ntn, bid, mt, nt);
+  if (MODE == G_PLAIN) {
+    // every tile as ks K-range parts, part p of tile i at workgroup p V ntn + i
+    const int T = V * a.ntn;
+    const int ks = plain_split(T, a.cus, nk);
+    if (bid == 0 && t == 0) *a.ks_out = ks;
+    if (bid >= T * ks) return;
+    split = bid / T;
+    mtile_of(V, a.ntn, bid - split * T, mt, nt);
+    kb = split * nk / ks;
+    ke = (split + 1) * nk / ks;
   } else {
-    const int u = bid - F, ti = u % tail, kp = u / tail;
-    mtile_of(V, a.ntn, F + ti, mt, nt);
-    kb = kp * nk / ks;
-    ke = (kp + 1) * nk / ks;
-    unit = ti * ks + kp;
+    int F, tail, ks;
+    mtail_split(V * a.ntn, a.cus, a.part_units, nk, F, tail, ks);
+    if (bid >= F + tail * ks) return;
+    if (bid < F) {
+      mtile_of(V, a.ntn, bid, mt, nt);
+    } else {
+      const int u = bid - F, ti = u % tail, kp = u / tail;
+      mtile_of(V, a.ntn, F + ti, mt, nt);
+      kb = kp * nk / ks;
+      ke = (kp + 1) * nk / ks;
+      unit = ti * ks + kp;
+    }
   }
   const int row0 = mt * MB;
   const int nvalid = min(MB, pre[a.B] - row0);
@@ -990,6 +1018,22 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   }
   lds_barrier();                                               // the stages are free
 
+  if (MODE == G_PLAIN) {
+    // the raw K-range sums straight from the accumulators, tile-contiguous: part `split`
+    // of tile (mt, nt) is the [256 packed rows][256 columns] block at
+    // ((split mtiles + mt) ntn + nt) 256^2 (rows past the packed rows are not stored)
+    float *ob = a.out + (((long)split * a.mtiles + mt) * a.ntn + nt) * (MB * MB);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int rr = wm * 128 + i * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
+        if (rr >= nvalid) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) ob[rr * MB + wn * 64 + j * 32 + l32] = acc[i][j][e];
+      }
+    return;
+  }
   if (unit >= 0) {
     // a part of a tail tile: the raw fp32 accumulators, [256 rows][256 staged columns]
     float *pt = a.part + (long)unit * (MB * MB);
@@ -1904,8 +1948,10 @@ fc_status run_mgemm(fc_ctx *ctx, hipStream_t st, const char *name, MArgs &g, int
   const int tn = MODE == G_GU ? MB / 2 : MB;
   g.ntn = (g.Nout + tn - 1) / tn;
   g.cus = std::max(ctx->num_cus, 1);
-  g.part = ctx->part;
-  g.part_units = (int)std::min<size_t>(ctx->part_elems / ((size_t)MB * MB), 1 << 20);
+  if (!g.part) {
+    g.part = ctx->part;
+    g.part_units = (int)std::min<size_t>(ctx->part_elems / ((size_t)MB * MB), 1 << 20);
+  }
   // whole tiles plus the extra parts of a split tail (fewer than one round)
   const long total = (long)g.mtiles * g.ntn + g.cus;
   if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
@@ -2171,7 +2217,35 @@ fc_status launch_layer(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_cache &k
 
 fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const uint16_t *A,
                          const uint16_t *W, int K, int Nout, int N, const int32_t *nrec,
-                         float *part, int B, int *splits) {
+                         float *part, int B, int *splits, int *dsplits, const int **dsplits_used,
+                         int *tiles) {
+  *dsplits_used = nullptr;
+  // many rows: the 256 x 256-tile GEMM, each tile as up to 4 K-range parts whose sums go
+  // to part as 256 x 256 tiles over the packed rows; the part count is decided on the
+  // device (it depends on the row counts there) and written to *dsplits for the consumer
+  const long mtiles = ((long)B * N + MB - 1) / MB, ntn = (Nout + MB - 1) / MB;
+  *tiles = 0;
+  if (dsplits && (long)B * N >= kPlainBigRows && B <= kMMaxItems && K % KS == 0 &&
+      Nout % 16 == 0 && (size_t)4 * mtiles * ntn * MB * MB <= ctx->part_elems) {
+    MArgs m{};
+    m.A = A; m.W0 = W;
+    m.K = K; m.Nout = Nout; m.N = N; m.B = B;
+    m.r.nrec = nrec;
+    m.out = part;
+    m.ks_out = dsplits;
+    m.mtiles = (int)(((long)B * N + MB - 1) / MB);
+    m.ntn = (Nout + MB - 1) / MB;
+    m.cus = std::max(ctx->num_cus, 1);
+    const long total = (long)m.mtiles * m.ntn * 4;
+    if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
+    ProfScope ps(ctx, st, name);
+    hipLaunchKernelGGL(k_mgemm<G_PLAIN>, dim3((unsigned)total), dim3(512), 0, st, m);
+    FC_LAUNCH_OK(st, "k_mgemm");
+    *splits = 4;
+    *dsplits_used = dsplits;
+    *tiles = (int)(mtiles * ntn);
+    return FC_OK;
+  }
   WArgs g{};
   g.A = A; g.W0 = W;
   g.K = K; g.Nout = Nout; g.N = N; g.nrec = nrec;

@@ -375,6 +375,9 @@ int main() {
     fc_vit_desc l2 = vd;
     l2.head_dim = 81;
     EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);
+    l2.head_dim = 40;                  // a multiple of 8 but not of 16
+    l2.n_heads = 32;
+    EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);
     l2 = vd;
     l2.n_heads = INT_MAX;
     EXPECT(vfwd(l2, vc, 1), FC_ERR_INVALID_ARG);

@@ -283,3 +283,58 @@ def test_merger_qwen_shape(fc, ctx):
     tokens, half of them recomputed."""
     check_merger(fc, ctx, fcdata.QWEN_MERGER, 256,
                  [np.sort(fcdata.random_reuse_ids(360, 256, 50))], 361)
+
+
+def test_block_and_merger_replay_from_graph(fc, ctx):
+    """The vision block and the merger captured in a HIP graph (they launch kernels only:
+    no allocation, memset or host synchronisation); every replay reproduces the eager
+    bytes, with eager calls in between."""
+    c = VitCase(SMALL, 8, 8, 2, 4, 1, seed=370)
+    ids = np.sort(fcdata.random_reuse_ids(371, 64, 50))
+    idx = torch.full((1, 64), -1, dtype=torch.int32)
+    idx[0, :len(ids)] = torch.from_numpy(ids)
+    idx, nrec = idx.cuda(), torch.tensor([len(ids)], dtype=torch.int32, device="cuda")
+    desc = gpu_desc(fc, c.wt, SMALL)
+    mwt = fcdata.merger_weights(372, SMALL_MERGER)
+    mdesc = merger_desc(fc, mwt, SMALL_MERGER)
+    k0, v0, y0 = fcutil.bf16_gpu(c.k), fcutil.bf16_gpu(c.v), fcutil.bf16_gpu(c.y)
+    kc, vc, y = k0.clone(), v0.clone(), y0.clone()
+    x = fcutil.bf16_gpu(c.x)
+    xo = torch.zeros(1, 64, SMALL_MERGER.d_out, dtype=torch.bfloat16, device="cuda")
+    cache = fc.VitCache(kc, vc, 8, 8, 2, 4)
+
+    def restore():
+        kc.copy_(k0)
+        vc.copy_(v0)
+        y.copy_(y0)
+        xo.zero_()
+
+    def call():
+        fc.fc_vit_block_forward(ctx, desc, cache, x, idx, nrec, y)
+        fc.fc_vit_merger_forward(ctx, mdesc, y, idx, nrec, xo)
+
+    def snap():
+        torch.cuda.synchronize()
+        return [fcutil.bf16_np(t) for t in (kc, vc, y, xo)]
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        restore()
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    want = snap()
+    graph = torch.cuda.CUDAGraph()
+    restore()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        call()
+    for rep in range(3):
+        restore()
+        graph.replay()
+        for a, b in zip(snap(), want):
+            np.testing.assert_array_equal(a, b, err_msg=f"replay {rep}")
+        restore()
+        call()
+        for a, b in zip(snap(), want):
+            np.testing.assert_array_equal(a, b, err_msg=f"eager call after replay {rep}")
