@@ -205,10 +205,10 @@ __device__ __forceinline__ int pool_row(const int32_t *map, int b, int S, int r)
 // item, no epilogue; K a multiple of 64, Nout of 16.  Few rows: the weight-streaming GEMM,
 // part = C[split][B N][Nout], *splits = its split count, *dsplits_used = null, *tiles = 0.
 // Many rows (and dsplits given): the 256 x 256-tile GEMM over the rows packed across
-// items (item b's rows after those of items < b), part = [split][*tiles] tiles of
-// [256 packed rows][256 columns] (tile mt ceil(Nout / 256) + nt); its split count (at
-// most 4) is decided on the device and written to *dsplits; *splits = 4 and
-// *dsplits_used = dsplits.
+// items (item b's rows after those of items < b), part = [split][V][ceil(Nout / 256)]
+// tiles of [256 packed rows][256 columns], V = ceil(packed rows / 256); its split count
+// (at most 8) is decided on the device and written to *dsplits; *splits = 8,
+// *dsplits_used = dsplits and *tiles = 1.
 fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const uint16_t *A,
                          const uint16_t *W, int K, int Nout, int N, const int32_t *nrec,
                          float *part, int B, int *splits, int *dsplits,

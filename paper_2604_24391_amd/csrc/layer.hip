@@ -682,18 +682,20 @@ struct MArgs {
   int cus;                        // workgroup slots: one resident workgroup per CU
   int part_units;                 // 256 x 256 fp32 tiles the partial buffer holds
   float *part;                    // K-range partial tiles of the split tail
-  float *out;                     // G_PLAIN output: [ks][mtiles][ntn] tiles of 256 x 256 fp32
+  float *out;                     // G_PLAIN output: [ks][V][ntn] tiles of 256 x 256 fp32
   int *ks_out;                    // G_PLAIN: the K-range part count ks, written by workgroup 0
   RedArgs r;                      // epilogue operands (as the reductions use them)
 };
 
 // G_PLAIN: when the tiles fill at most half the CUs, every tile runs as ks K-range parts
-// (at most 4, at least 4 K steps each), written as separate sums that the consumer adds.
+// (at most kPlainMaxParts, at least 4 K steps each), written as separate sums that the
+// consumer adds.
+constexpr int kPlainMaxParts = 8;
 __host__ __device__ inline int plain_split(int tiles, int cus, int nk) {
   int ks = 1;
   if (tiles > 0 && 2 * tiles <= cus) {
     ks = cus / tiles;
-    ks = ks < 4 ? ks : 4;
+    ks = ks < kPlainMaxParts ? ks : kPlainMaxParts;
     ks = ks < nk / 4 ? ks : nk / 4;
     ks = ks > 1 ? ks : 1;
   }
@@ -1021,8 +1023,9 @@ __global__ __launch_bounds__(512) void k_mgemm(MArgs a) {
   if (MODE == G_PLAIN) {
     // the raw K-range sums straight from the accumulators, tile-contiguous: part `split`
     // of tile (mt, nt) is the [256 packed rows][256 columns] block at
-    // ((split mtiles + mt) ntn + nt) 256^2 (rows past the packed rows are not stored)
-    float *ob = a.out + (((long)split * a.mtiles + mt) * a.ntn + nt) * (MB * MB);
+    // ((split V + mt) ntn + nt) 256^2, V the valid M tiles (rows past the packed rows are
+    // not stored)
+    float *ob = a.out + (((long)split * V + mt) * a.ntn + nt) * (MB * MB);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -2220,13 +2223,18 @@ fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const ui
                          float *part, int B, int *splits, int *dsplits, const int **dsplits_used,
                          int *tiles) {
   *dsplits_used = nullptr;
-  // many rows: the 256 x 256-tile GEMM, each tile as up to 4 K-range parts whose sums go
+  // many rows: the 256 x 256-tile GEMM, each tile as up to 8 K-range parts whose sums go
   // to part as 256 x 256 tiles over the packed rows; the part count is decided on the
   // device (it depends on the row counts there) and written to *dsplits for the consumer
   const long mtiles = ((long)B * N + MB - 1) / MB, ntn = (Nout + MB - 1) / MB;
+  const int cus = std::max(ctx->num_cus, 1);
+  // the most tiles any row count can store: V ntn ks(V) over V <= mtiles
+  long most = 0;
+  for (long V = 1; V <= mtiles && V * ntn <= INT32_MAX; ++V)
+    most = std::max(most, V * ntn * plain_split((int)(V * ntn), cus, K / KS));
   *tiles = 0;
   if (dsplits && (long)B * N >= kPlainBigRows && B <= kMMaxItems && K % KS == 0 &&
-      Nout % 16 == 0 && (size_t)4 * mtiles * ntn * MB * MB <= ctx->part_elems) {
+      Nout % 16 == 0 && most > 0 && (size_t)most * MB * MB <= ctx->part_elems) {
     MArgs m{};
     m.A = A; m.W0 = W;
     m.K = K; m.Nout = Nout; m.N = N; m.B = B;
@@ -2235,15 +2243,15 @@ fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const ui
     m.ks_out = dsplits;
     m.mtiles = (int)(((long)B * N + MB - 1) / MB);
     m.ntn = (Nout + MB - 1) / MB;
-    m.cus = std::max(ctx->num_cus, 1);
-    const long total = (long)m.mtiles * m.ntn * 4;
+    m.cus = cus;
+    const long total = (long)m.mtiles * m.ntn * kPlainMaxParts;
     if (total > INT32_MAX) return fail(FC_ERR_CAPACITY, "%s: too many tiles", name);
     ProfScope ps(ctx, st, name);
     hipLaunchKernelGGL(k_mgemm<G_PLAIN>, dim3((unsigned)total), dim3(512), 0, st, m);
     FC_LAUNCH_OK(st, "k_mgemm");
-    *splits = 4;
+    *splits = kPlainMaxParts;
     *dsplits_used = dsplits;
-    *tiles = (int)(mtiles * ntn);
+    *tiles = 1;
     return FC_OK;
   }
   WArgs g{};

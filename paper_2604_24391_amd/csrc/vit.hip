@@ -85,53 +85,51 @@ __device__ float block_sum(float v, float *red) {
 // Split-K sums of columns c .. c + 3 of row s (partials [split][rows][nc]): all SPL
 // 16-byte loads issued first (indices past the last split re-read it), then summed in
 // split order with the extra ones masked out.
+// Sum over the splits of the float4 at p0 + sp stride, in split order, loads issued in
+// groups of up to 4 (a group past the last split is skipped; `splits` is uniform).
 template <int SPL>
-__device__ __forceinline__ float4 sum_parts4(const float *__restrict__ part, int splits, long rows,
-                                             long s, int nc, int c) {
-  float4 u[SPL];
-#pragma unroll
-  for (int sp = 0; sp < SPL; ++sp)
-    u[sp] = *reinterpret_cast<const float4 *>(part + ((long)min(sp, splits - 1) * rows + s) * nc + c);
+__device__ __forceinline__ float4 sum_splits4(const float *__restrict__ p0, long stride, int splits) {
+  constexpr int G = SPL < 4 ? SPL : 4;
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int sp = 0; sp < SPL; ++sp) {
-    const bool in = sp < splits;
-    a.x += in ? u[sp].x : 0.f;
-    a.y += in ? u[sp].y : 0.f;
-    a.z += in ? u[sp].z : 0.f;
-    a.w += in ? u[sp].w : 0.f;
+  for (int g0 = 0; g0 < SPL; g0 += G) {
+    if (g0 > 0 && g0 >= splits) break;
+    float4 u[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      u[i] = *reinterpret_cast<const float4 *>(p0 + (long)min(g0 + i, splits - 1) * stride);
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const bool in = g0 + i < splits;
+      a.x += in ? u[i].x : 0.f;
+      a.y += in ? u[i].y : 0.f;
+      a.z += in ? u[i].z : 0.f;
+      a.w += in ? u[i].w : 0.f;
+    }
   }
   return a;
 }
-// The split-K sums a reduction reads: [split][rows][nc] rows (tiles = 0), or, from the
-// many-row GEMM, [split][tiles] tiles of [256 packed rows][256 columns] with the split
-// count on the device.
+template <int SPL>
+__device__ __forceinline__ float4 sum_parts4(const float *__restrict__ part, int splits, long rows,
+                                             long s, int nc, int c) {
+  return sum_splits4<SPL>(part + s * nc + c, rows * nc, splits);
+}
+// The split-K sums a reduction reads: [split][rows][nc] rows (tiled = 0), or, from the
+// many-row GEMM, [split][V][ceil(nc / 256)] tiles of [256 packed rows][256 columns] with
+// the split count on the device (V: 256-row tiles of the packed rows).
 struct PartIn {
   const float *part;
   int splits;          // split count (an upper bound when dsp is set)
   const int *dsp;      // device split count, or null
-  int tiles;           // tiles per split (0: row layout)
+  int tiled;           // 1: tile layout
 };
 template <int SPL>
 __device__ __forceinline__ float4 part_sum(const PartIn &P, int splits, long rows, long s, int prow,
-                                           int nc, int c) {
-  if (P.tiles == 0) return sum_parts4<SPL>(P.part, splits, rows, s, nc, c);
+                                           int V, int nc, int c) {
+  if (!P.tiled) return sum_parts4<SPL>(P.part, splits, rows, s, nc, c);
   const int ntn = (nc + 255) >> 8;
   const float *p0 = P.part + ((long)((prow >> 8) * ntn + (c >> 8)) << 16) + ((prow & 255) << 8) + (c & 255);
-  const long stride = (long)P.tiles << 16;
-  float4 u[SPL];
-#pragma unroll
-  for (int sp = 0; sp < SPL; ++sp) u[sp] = *reinterpret_cast<const float4 *>(p0 + min(sp, splits - 1) * stride);
-  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-  for (int sp = 0; sp < SPL; ++sp) {
-    const bool in = sp < splits;
-    a.x += in ? u[sp].x : 0.f;
-    a.y += in ? u[sp].y : 0.f;
-    a.z += in ? u[sp].z : 0.f;
-    a.w += in ? u[sp].w : 0.f;
-  }
-  return a;
+  return sum_splits4<SPL>(p0, (long)V * ntn << 16, splits);
 }
 
 __device__ __forceinline__ float4 bf4(const uint16_t *p) {
@@ -223,12 +221,13 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_qkv(
   const int b = (int)(s / g.Np), j = (int)(s - (long)b * g.Np);
   if (j >= n_rows(nrec, g, b)) return;
   const int prow = packed_row(nrec, g, b, j);
+  const int V = (packed_row(nrec, g, (int)(gridDim.x / g.Np), 0) + 255) >> 8;
   const int d = g.d, nc = 3 * d;
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   if (c >= nc) return;
   const long rows = (long)gridDim.x;
   const int p = slot_patch(idx, g, b, j);
-  float4 v = part_sum<SPL>(P, splits, rows, s, prow, nc, c);
+  float4 v = part_sum<SPL>(P, splits, rows, s, prow, V, nc, c);
   const float4 bb = bf4(bias + c);
   v = make_float4(v.x + bb.x, v.y + bb.y, v.z + bb.z, v.w + bb.w);
   if (c >= d) {
@@ -239,7 +238,7 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_qkv(
   const int half = g.hd / 2, quarter = g.hd / 4;
   const int hd_i = c % g.hd;
   const int pcol = hd_i < half ? c + half : c - half;          // 4 partner columns
-  float4 pv = part_sum<SPL>(P, splits, rows, s, prow, nc, pcol);
+  float4 pv = part_sum<SPL>(P, splits, rows, s, prow, V, nc, pcol);
   const float4 pb = bf4(bias + pcol);
   const float sg = hd_i < half ? -1.f : 1.f;
   const float pp[4] = {sg * (pv.x + pb.x), sg * (pv.y + pb.y), sg * (pv.z + pb.z), sg * (pv.w + pb.w)};
@@ -316,12 +315,13 @@ typedef float vf32x4 __attribute__((ext_vector_type(4)));
 
 // Grid: x = window * chunks_per_window + chunk, y = head, z = item; 4 waves of 16
 // queries.  Per key block of 64 the workgroup stages the keys (rotated at their patch
-// position, head dims zero-padded to HDP) row-major and the values transposed in LDS.
+// position, head dims zero-padded to HDP) row-major and the values transposed in LDS,
+// two blocks in flight: the next block's loads are issued before this block's MFMAs.
 // Each wave computes S^T = K Q^T with 16x16x32 bf16 MFMAs, so a lane's accumulators
 // all belong to one query (keys 4 (lane / 16) + e of each 16-key tile) and the online
 // softmax needs two cross-lane steps; P then feeds O^T = V^T P^T straight from the
 // registers, the values being read from LDS in the same key order.
-template <int HDP>
+template <int HDP, bool PIPE>
 __global__ __launch_bounds__(kVitThreads) void k_vit_attn(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kc,
     const uint16_t *__restrict__ vc, const int32_t *__restrict__ idx,
@@ -329,8 +329,9 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_attn(
     uint16_t *__restrict__ out) {
   constexpr int KP = HDP + 8;          // key row pitch (bf16)
   constexpr int VP = kVitK + 8;        // transposed value row pitch (bf16)
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kVitK * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HDP * VP];
+  constexpr int NB = PIPE ? 2 : 1;     // key blocks in flight
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[NB][kVitK * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[NB][HDP * VP];
   __shared__ int qslot[kVitQ];
   __shared__ int wcnt[kVitThreads / 64];
   __shared__ int nq_s;
@@ -343,9 +344,12 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_attn(
   // padded head dims stay zero for the whole kernel
   for (int e = t; e < kVitK * (HDP - hd); e += blockDim.x) {
     const int r = e / (HDP - hd);
-    Ks[r * KP + hd + (e - r * (HDP - hd))] = 0;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) Ks[nb][r * KP + hd + (e - r * (HDP - hd))] = 0;
   }
-  for (int e = t; e < (HDP - hd) * VP; e += blockDim.x) Vt[hd * VP + e] = 0;
+  for (int e = t; e < (HDP - hd) * VP; e += blockDim.x)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) Vt[nb][hd * VP + e] = 0;
   // this lane's query (column l16 of the wave's 16) as the B operand, dims 32 s + 8 gq..
   const int qi = wv * 16 + l16;
   const bool qv = qi < nq;
@@ -366,48 +370,68 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_attn(
   const float scale = 1.f / sqrtf((float)hd);
   const int nk = window_keys(g, w);
   const int cpr = hd / 8;                                  // 8-dim chunks per row
-  for (int k0 = 0; k0 < nk; k0 += kVitK) {
+  // Staging of a key block: task e (< 64 cpr) is key e / cpr, dims 8 (e % cpr) ..; the
+  // raw loads of block k + 1 are issued into registers before block k's MFMAs and go
+  // to the other LDS buffer (rotated) after them.
+  constexpr int TASKS = (kVitK * (HDP / 8) + kVitThreads - 1) / kVitThreads;
+  uint4 rk[TASKS], rp[TASKS], rv[TASKS];
+  int rpatch[TASKS];
+  auto load_block = [&](int k0) {
     const int kn = min(kVitK, nk - k0);
-    __syncthreads();                                       // the previous block is consumed
-    for (int e = t; e < kVitK * cpr; e += blockDim.x) {
+#pragma unroll
+    for (int i = 0; i < TASKS; ++i) {
+      const int e = t + i * kVitThreads;
       const int ki = e / cpr, c0 = (e - ki * cpr) * 8;
-      uint16_t kr[8], vr[8];
-      if (ki < kn) {
+      rpatch[i] = -1;
+      if (e < kVitK * cpr && ki < kn) {
         const int p = key_patch(g, w, k0 + ki);
         const long base = (((long)b * g.Np + p) * g.H + h) * hd;
-        const uint4 kx = *reinterpret_cast<const uint4 *>(kc + base + c0);
-        const uint4 kp = *reinterpret_cast<const uint4 *>(kc + base + (c0 < half ? c0 + half : c0 - half));
-        const uint4 vx = *reinterpret_cast<const uint4 *>(vc + base + c0);
-        const uint16_t *xs = reinterpret_cast<const uint16_t *>(&kx);
-        const uint16_t *ps = reinterpret_cast<const uint16_t *>(&kp);
-        const uint16_t *vs = reinterpret_cast<const uint16_t *>(&vx);
-        int pr, pc;
-        patch_pos(g, p, pr, pc);
+        rk[i] = *reinterpret_cast<const uint4 *>(kc + base + c0);
+        rp[i] = *reinterpret_cast<const uint4 *>(kc + base + (c0 < half ? c0 + half : c0 - half));
+        rv[i] = *reinterpret_cast<const uint4 *>(vc + base + c0);
+        rpatch[i] = p;
+      }
+    }
+  };
+  auto store_block = [&](int buf) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int c = c0 + i, pair = c % half;
+    for (int i = 0; i < TASKS; ++i) {
+      const int e = t + i * kVitThreads;
+      if (e >= kVitK * cpr) continue;
+      const int ki = e / cpr, c0 = (e - ki * cpr) * 8;
+      uint16_t kr[8], vr[8];
+      if (rpatch[i] >= 0) {
+        const uint16_t *xs = reinterpret_cast<const uint16_t *>(&rk[i]);
+        const uint16_t *ps = reinterpret_cast<const uint16_t *>(&rp[i]);
+        const uint16_t *vs = reinterpret_cast<const uint16_t *>(&rv[i]);
+        int pr, pc;
+        patch_pos(g, rpatch[i], pr, pc);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int c = c0 + q, pair = c % half;
           const float2 cs = rope[(pair < quarter ? pr : pc) * 32 + (pair < quarter ? pair : pair - quarter)];
-          const float partner = c < half ? -bf2f_v(ps[i]) : bf2f_v(ps[i]);
-          kr[i] = f2bf_v(bf2f_v(xs[i]) * cs.x + partner * cs.y);
-          vr[i] = vs[i];
+          const float partner = c < half ? -bf2f_v(ps[q]) : bf2f_v(ps[q]);
+          kr[q] = f2bf_v(bf2f_v(xs[q]) * cs.x + partner * cs.y);
+          vr[q] = vs[q];
         }
       } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) kr[i] = vr[i] = 0;
+        for (int q = 0; q < 8; ++q) kr[q] = vr[q] = 0;
       }
-      *reinterpret_cast<uint4 *>(Ks + ki * KP + c0) = *reinterpret_cast<const uint4 *>(kr);
+      *reinterpret_cast<uint4 *>(Ks[buf] + ki * KP + c0) = *reinterpret_cast<const uint4 *>(kr);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) Vt[(c0 + i) * VP + ki] = vr[i];
+      for (int q = 0; q < 8; ++q) Vt[buf][(c0 + q) * VP + ki] = vr[q];
     }
-    __syncthreads();
-    if (!wact) continue;
+  };
+  // one key block from LDS buffer buf (kn valid keys): S^T, the online softmax, O^T
+  auto compute = [&](int buf, int kn) {
     vf32x4 sa[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       sa[kt] = vf32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < HDP / 32; ++s) {
-        const vbf16x8 ka = *reinterpret_cast<const vbf16x8 *>(Ks + (16 * kt + l16) * KP + 32 * s + 8 * gq);
+        const vbf16x8 ka = *reinterpret_cast<const vbf16x8 *>(Ks[buf] + (16 * kt + l16) * KP + 32 * s + 8 * gq);
         sa[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[s], sa[kt], 0, 0, 0);
       }
     }
@@ -447,12 +471,34 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_attn(
       }
 #pragma unroll
       for (int dt = 0; dt < HDP / 16; ++dt) {
-        const uint16_t *vrow = Vt + (16 * dt + l16) * VP + 32 * ks + 4 * gq;
+        const uint16_t *vrow = Vt[buf] + (16 * dt + l16) * VP + 32 * ks + 4 * gq;
         const uint2 lo = *reinterpret_cast<const uint2 *>(vrow);
         const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 16);
         const vbf16x8 va = __builtin_bit_cast(vbf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[dt], 0, 0, 0);
       }
+    }
+  };
+  const int nblk = (nk + kVitK - 1) / kVitK;
+  if (PIPE) {
+    load_block(0);
+    store_block(0);
+    for (int kb = 0; kb < nblk; ++kb) {
+      const int k0 = kb * kVitK, buf = kb & 1;
+      // block kb is in buffer buf; every reader of the other buffer (block kb - 1) is done
+      __syncthreads();
+      if (kb + 1 < nblk) load_block(k0 + kVitK);
+      if (wact) compute(buf, min(kVitK, nk - k0));
+      if (kb + 1 < nblk) store_block(buf ^ 1);
+    }
+  } else {
+    for (int kb = 0; kb < nblk; ++kb) {
+      const int k0 = kb * kVitK;
+      __syncthreads();                                   // the previous block is consumed
+      load_block(k0);
+      store_block(0);
+      __syncthreads();
+      if (wact) compute(0, min(kVitK, nk - k0));
     }
   }
   if (!wact) return;
@@ -490,12 +536,13 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_o(
   const int b = (int)(s / g.Np), j = (int)(s - (long)b * g.Np);
   if (j >= n_rows(nrec, g, b)) return;
   const int prow = packed_row(nrec, g, b, j);
+  const int V = (packed_row(nrec, g, (int)(gridDim.x / g.Np), 0) + 255) >> 8;
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   const long rows = (long)gridDim.x;
   float ss = 0.f;
   if (c < g.d) {
     const uint16_t *xr = x + ((long)b * g.Np + slot_patch(idx, g, b, j)) * g.d;
-    const float4 v = part_sum<SPL>(P, splits, rows, s, prow, g.d, c);
+    const float4 v = part_sum<SPL>(P, splits, rows, s, prow, V, g.d, c);
     const float4 bb = bf4(bias + c), xv = bf4(xr + c), gn = bf4(g2 + c);
     const float4 h = make_float4(xv.x + (v.x + bb.x), xv.y + (v.y + bb.y), xv.z + (v.z + bb.z),
                                  xv.w + (v.w + bb.w));
@@ -519,14 +566,15 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_gu(
   const int b = (int)(s / g.Np), j = (int)(s - (long)b * g.Np);
   if (j >= n_rows(nrec, g, b)) return;
   const int prow = packed_row(nrec, g, b, j);
+  const int V = (packed_row(nrec, g, (int)(gridDim.x / g.Np), 0) + 255) >> 8;
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   if (c >= f) return;
   float sq = 0.f;
   for (int i = 0; i < nch; ++i) sq += ssq[s * nch + i];
   const float inv = 1.f / sqrtf(sq / (float)g.d + eps);
   const long rows = (long)gridDim.x;
-  const float4 gs = part_sum<SPL>(P, splits, rows, s, prow, 2 * f, c);
-  const float4 us = part_sum<SPL>(P, splits, rows, s, prow, 2 * f, f + c);
+  const float4 gs = part_sum<SPL>(P, splits, rows, s, prow, V, 2 * f, c);
+  const float4 us = part_sum<SPL>(P, splits, rows, s, prow, V, 2 * f, f + c);
   const float4 gb = bf4(bias + c), ub = bf4(bias + f + c);
   const float g0 = gs.x * inv + gb.x, g1 = gs.y * inv + gb.y, g2 = gs.z * inv + gb.z,
               g3 = gs.w * inv + gb.w;
@@ -546,11 +594,12 @@ __global__ __launch_bounds__(kVitThreads) void k_vit_red_down(
   const int b = (int)(s / g.Np), j = (int)(s - (long)b * g.Np);
   if (j >= n_rows(nrec, g, b)) return;
   const int prow = packed_row(nrec, g, b, j);
+  const int V = (packed_row(nrec, g, (int)(gridDim.x / g.Np), 0) + 255) >> 8;
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   if (c >= g.d) return;
   uint16_t *yr = y + ((long)b * g.Np + slot_patch(idx, g, b, j)) * g.d;
   const long rows = (long)gridDim.x;
-  const float4 v = part_sum<SPL>(P, splits, rows, s, prow, g.d, c);
+  const float4 v = part_sum<SPL>(P, splits, rows, s, prow, V, g.d, c);
   const float4 bb = bf4(bias + c);
   const float4 h = *reinterpret_cast<const float4 *>(h1 + s * g.d + c);
   st_bf4(yr + c, h.x + (v.x + bb.x), h.y + (v.y + bb.y), h.z + (v.z + bb.z), h.w + (v.w + bb.w));
@@ -586,7 +635,7 @@ __global__ __launch_bounds__(kVitThreads) void k_merge_red_gelu(
   if (j >= min(max(nrec[b], 0), N)) return;
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   if (c >= hidden) return;
-  const float4 v = part_sum<SPL>(P, splits, (long)gridDim.x, s, 0, hidden, c);
+  const float4 v = part_sum<SPL>(P, splits, (long)gridDim.x, s, 0, 0, hidden, c);
   const float4 bb = bf4(bias + c);
   st_bf4(act + s * hidden + c, gelu_erf(bb.x + v.x), gelu_erf(bb.y + v.y), gelu_erf(bb.z + v.z),
          gelu_erf(bb.w + v.w));
@@ -605,7 +654,7 @@ __global__ __launch_bounds__(kVitThreads) void k_merge_red_out(
   const int c = 4 * (blockIdx.y * kVitThreads + threadIdx.x);
   if (c >= d_out) return;
   const int t = min(max(idx[s], 0), N - 1);
-  const float4 v = part_sum<SPL>(P, splits, (long)gridDim.x, s, 0, d_out, c);
+  const float4 v = part_sum<SPL>(P, splits, (long)gridDim.x, s, 0, 0, d_out, c);
   const float4 bb = bf4(bias + c);
   st_bf4(x_out + ((long)b * N + t) * d_out + c, bb.x + v.x, bb.y + v.y, bb.z + v.z, bb.w + v.w);
 }
@@ -670,14 +719,20 @@ fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache
     const uint16_t *qb = ctx->qbuf, *kb = c.k, *vb = c.v;
     const float2 *rp = ctx->vit_rope;
     ProfScope ps(ctx, st, "fc_vit_attn");
-    if (g.hd <= 32)
-      hipLaunchKernelGGL(k_vit_attn<32>, grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn);
-    else if (g.hd <= 64)
-      hipLaunchKernelGGL(k_vit_attn<64>, grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn);
-    else if (g.hd <= 96)
-      hipLaunchKernelGGL(k_vit_attn<96>, grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn);
-    else
-      hipLaunchKernelGGL(k_vit_attn<128>, grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn);
+    // more than one key block per workgroup: two blocks in flight
+    const bool pipe = wkeys > kVitK;
+#define FC_VIT_ATTN(HDP)                                                                      \
+  do {                                                                                        \
+    if (pipe)                                                                                 \
+      hipLaunchKernelGGL((k_vit_attn<HDP, true>), grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn); \
+    else                                                                                      \
+      hipLaunchKernelGGL((k_vit_attn<HDP, false>), grid, dim3(kVitThreads), 0, st, qb, kb, vb, idx, nrec, g, rp, chunks, ctx->attn); \
+  } while (0)
+    if (g.hd <= 32) FC_VIT_ATTN(32);
+    else if (g.hd <= 64) FC_VIT_ATTN(64);
+    else if (g.hd <= 96) FC_VIT_ATTN(96);
+    else FC_VIT_ATTN(128);
+#undef FC_VIT_ATTN
     FC_LAUNCH_OK(st, "k_vit_attn");
   }
   if ((rc = run_plain_gemm(ctx, st, "fc_vit_gemm_o", ctx->attn, L.w_o, g.d, g.d, g.Np,
