@@ -75,6 +75,9 @@ def main():
     ap.add_argument("--vit-only", action="store_true",
                     help="run only the vision-block workload (windowed and full attention, "
                          "reuse 0/25/50/75/90 %%) and print its record")
+    ap.add_argument("--full-model-only", action="store_true",
+                    help="run only the whole-model step (FreqCache and flush-every-step) after "
+                         "the episode inputs are built, and print its record (for profiling)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="after the measurement, run an elementwise negation over this many "
                          "MiB of float32 (reads and writes exactly that many bytes): the "
@@ -179,6 +182,11 @@ def main():
     ctx = fc.Context(fc.Caps(max_batch=64, max_height=size, max_width=size, max_tokens=1024,
                              max_seq=S, max_d_model=shape.d, max_ffn=shape.ffn,
                              max_qkv=shape.qkv))
+    if args.full_model_only:
+        rec = bench_full_model(fc, ctx, torch, frames, layers, shape, T, N, gw, size)
+        ctx.close()
+        print(json.dumps(rec), flush=True)
+        return
     prm = fc.SelectParams(merge=m)
     sel = fc.SelectOut.alloc(1, N)
     # the previous frame's spectra are carried from step to step (two state buffers)
@@ -296,6 +304,8 @@ def main():
         result["tiny"] = bench_tiny(fc, torch)
         result["ablations"] = bench_ablations(fc, ctx, torch, frames, m, N)
         result["vit"] = bench_vit(fc, torch)
+        result["full_model"] = bench_full_model(fc, ctx, torch, frames, layers, shape, T, N,
+                                                gw, size)
         # the two targets of the hot path side by side: selection (64 pairs of 448x448)
         # against HBM peak, and the one-layer call against bf16 MFMA peak with its
         # roofline ceiling (compute time over the larger of compute and HBM time)
@@ -757,6 +767,113 @@ def bench_vit(fc, torch):
                 blocks=out, merger=merger, kernel_avg_us_window4_reuse50=kern,
                 merger_kernel_avg_us_reuse90=mkern,
                 encoder_32_blocks_ms_est=enc, weight_bytes=wbytes)
+
+
+def bench_full_model(fc, ctx, torch, frames, layers, shape, T, N, gw, size, steps=10, warmup=3):
+    """The whole model per frame, as the paper times it (Table 2: a step with and without
+    the cache): selection (carried spectra), then for each of the 32 Qwen2.5-VL vision
+    blocks (windows of 4 x 4 tokens, full attention in blocks 7, 15, 23, 31) the encoder
+    cache's remap and the block over the recomputed patches, the 2 x 2 merger for the
+    recomputed tokens, the decoder's window advance and remap in one launch and its 28
+    layers.  Timed with FreqCache and with a flush at every step (the selection without
+    a previous frame: every token recomputed by encoder and decoder), same frames,
+    weights and caches.  The patch embedding is a stand-in computed before the timed
+    region: a fixed linear map of each 14x14x3 patch to the vision width."""
+    import fcdata
+    dev = torch.device("cuda:0")
+    vs = fcdata.QWEN_VIT
+    d, H, hd = vs.d, vs.heads, vs.hd
+    f = (vs.ffn + 63) // 64 * 64
+    m = 2
+    gh = size // (14 * m)
+    Np = N * m * m
+    nb_vit, full_idx = 32, (7, 15, 23, 31)
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+
+    def randn(*shp, std=0.02):
+        return (torch.randn(*shp, device=dev, generator=g) * std).to(torch.bfloat16)
+    n_frames = frames.shape[0]
+    px = frames.unfold(2, 14, 14).unfold(3, 14, 14)                  # [F,3,32,32,14,14]
+    px = px.permute(0, 2, 3, 1, 4, 5).reshape(n_frames, gh, m, gw, m, 3 * 14 * 14)
+    px = px.permute(0, 1, 3, 2, 4, 5).reshape(n_frames, Np, 3 * 14 * 14)
+    emb = (px.to(torch.bfloat16) @ randn(3 * 14 * 14, d)).contiguous()  # [F, Np, d]
+    del px
+    blocks = []
+    for li in range(nb_vit):
+        w_gu = randn(2 * f, d)
+        w_gu[vs.ffn:f].zero_()
+        w_gu[f + vs.ffn:].zero_()
+        w_dn = randn(d, f)
+        w_dn[:, vs.ffn:].zero_()
+        w = dict(w_qkv=randn(3 * d, d), b_qkv=randn(3 * d), w_o=randn(d, d), b_o=randn(d),
+                 w_gate_up=w_gu, b_gate_up=randn(2 * f), w_down=w_dn, b_down=randn(d),
+                 g1=torch.ones(d, device=dev, dtype=torch.bfloat16),
+                 g2=torch.ones(d, device=dev, dtype=torch.bfloat16))
+        blocks.append(dict(desc=fc.VitDesc(d, H, hd, f, w),
+                           cache=fc.VitCache(randn(1, Np, H, hd, std=1.0),
+                                             randn(1, Np, H, hd, std=1.0), gh, gw, m,
+                                             0 if li in full_idx else 4),
+                           y=[randn(1, Np, d, std=1.0), randn(1, Np, d, std=1.0)]))
+    msh = fcdata.QWEN_MERGER
+    hid = msh.hidden
+    mdesc = fc.MergerDesc(msh.d, msh.m, msh.d_out,
+                          dict(g=torch.ones(msh.d, device=dev, dtype=torch.bfloat16),
+                               w1=randn(hid, hid), b1=randn(hid), w2=randn(msh.d_out, hid),
+                               b2=randn(msh.d_out)))
+    x_llm = randn(1, N, shape.d, std=1.0)
+    prm = fc.SelectParams(merge=m)
+    sel = fc.SelectOut.alloc(1, N)
+    states = [fc.select_state_alloc(1, size, size), fc.select_state_alloc(1, size, size)]
+    cur = [0]
+
+    def step(s, flush):
+        fi = s % n_frames
+        prev = None if (flush or fi == 0) else states[(s - 1) % 2]
+        fc.fc_select_carry(ctx, prm, prev, frames[fi:fi + 1], states[s % 2], sel)
+        c, nxt = cur[0], 1 - cur[0]
+        x = emb[fi:fi + 1]
+        for blk in blocks:
+            fc.fc_vit_cache_update(ctx, blk["desc"], blk["cache"], blk["y"][c], blk["y"][nxt],
+                                   sel.shift, sel.reuse_mask)
+            fc.fc_vit_block_forward(ctx, blk["desc"], blk["cache"], x, sel.recompute_idx,
+                                    sel.n_recompute, blk["y"][nxt])
+            x = blk["y"][nxt]
+        fc.fc_vit_merger_forward(ctx, mdesc, x, sel.recompute_idx, sel.n_recompute, x_llm)
+        for lay in layers:
+            lay["kv"].advance()
+        fc.fc_cache_update_layers(ctx, layers[0]["desc"], [lay["kv"] for lay in layers],
+                                  [lay["y"][c] for lay in layers],
+                                  [lay["y"][nxt] for lay in layers], sel.shift, sel.reuse_mask,
+                                  gw)
+        h = x_llm
+        for lay in layers:
+            fc.fc_layer_forward(ctx, lay["desc"], lay["kv"], h, sel.recompute_idx,
+                                sel.n_recompute, lay["y"][nxt])
+            h = lay["y"][nxt]
+        cur[0] = nxt
+
+    out = {}
+    s0 = 0
+    for name, flush in (("freqcache", False), ("flush_every_step", True)):
+        for k in range(warmup):
+            step(s0 + k, flush)
+        torch.cuda.synchronize()
+        n_hist = torch.zeros(steps, dtype=torch.int32, device=dev)
+        t1 = time.perf_counter()
+        for k in range(steps):
+            step(s0 + warmup + k, flush)
+            n_hist[k:k + 1].copy_(sel.n_recompute)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t1) * 1e3 / steps
+        out[name] = dict(ms_per_step=round(ms, 3), frames_per_s=round(1e3 / ms, 2),
+                         mean_recomputed_tokens=round(float(n_hist.float().mean()), 1))
+        s0 += warmup + steps
+    out["speedup"] = round(out["flush_every_step"]["ms_per_step"] / out["freqcache"]["ms_per_step"], 3)
+    del blocks, emb
+    return dict(workload="whole model per 448x448 frame: selection + 32 Qwen2.5-VL vision "
+                         "blocks (1024 patch rows) + 2x2 merger + 28 Qwen2.5-VL-7B-shaped "
+                         "decoder layers over 2176 cached positions, batch 1", **out)
 
 
 def bench_ablations(fc, ctx, torch, frames, m, N):
