@@ -810,11 +810,15 @@ def bench_full_model(fc, ctx, torch, frames, layers, shape, T, N, gw, size, step
                  w_gate_up=w_gu, b_gate_up=randn(2 * f), w_down=w_dn, b_down=randn(d),
                  g1=torch.ones(d, device=dev, dtype=torch.bfloat16),
                  g2=torch.ones(d, device=dev, dtype=torch.bfloat16))
+        # two caches per block, alternating: the remap copies the reused rows from the
+        # previous frame's (no staging); one output buffer (only recomputed rows are read)
+        win = 0 if li in full_idx else 4
+        kv = [(randn(1, Np, H, hd, std=1.0), randn(1, Np, H, hd, std=1.0)) for _ in range(2)]
         blocks.append(dict(desc=fc.VitDesc(d, H, hd, f, w),
-                           cache=fc.VitCache(randn(1, Np, H, hd, std=1.0),
-                                             randn(1, Np, H, hd, std=1.0), gh, gw, m,
-                                             0 if li in full_idx else 4),
-                           y=[randn(1, Np, d, std=1.0), randn(1, Np, d, std=1.0)]))
+                           caches=[fc.VitCache(kv[j][0], kv[j][1], gh, gw, m, win,
+                                               k_prev=kv[1 - j][0], v_prev=kv[1 - j][1])
+                                   for j in range(2)],
+                           y=randn(1, Np, d, std=1.0)))
     msh = fcdata.QWEN_MERGER
     hid = msh.hidden
     mdesc = fc.MergerDesc(msh.d, msh.m, msh.d_out,
@@ -834,11 +838,11 @@ def bench_full_model(fc, ctx, torch, frames, layers, shape, T, N, gw, size, step
         c, nxt = cur[0], 1 - cur[0]
         x = emb[fi:fi + 1]
         for blk in blocks:
-            fc.fc_vit_cache_update(ctx, blk["desc"], blk["cache"], blk["y"][c], blk["y"][nxt],
-                                   sel.shift, sel.reuse_mask)
-            fc.fc_vit_block_forward(ctx, blk["desc"], blk["cache"], x, sel.recompute_idx,
-                                    sel.n_recompute, blk["y"][nxt])
-            x = blk["y"][nxt]
+            fc.fc_vit_cache_update(ctx, blk["desc"], blk["caches"][nxt], None, None, sel.shift,
+                                   sel.reuse_mask)
+            fc.fc_vit_block_forward(ctx, blk["desc"], blk["caches"][nxt], x, sel.recompute_idx,
+                                    sel.n_recompute, blk["y"])
+            x = blk["y"]
         fc.fc_vit_merger_forward(ctx, mdesc, x, sel.recompute_idx, sel.n_recompute, x_llm)
         for lay in layers:
             lay["kv"].advance()

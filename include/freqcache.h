@@ -204,6 +204,11 @@ typedef struct {
   int32_t window;           /* attention window side in merged tokens (Qwen2.5-VL: 4,
                                i.e. 112 px at 14-px patches and 2 x 2 merge); 0 = full
                                attention over the frame */
+  /* fc_vit_cache_update only: NULL, NULL = k, v hold the previous frame and are remapped
+     in place (the frame's old rows staged first); otherwise the previous frame's k, v
+     (same layout, distinct buffers), from which the reused rows are copied into k, v
+     (callers alternate two caches per block; no staging) */
+  const uint16_t *k_prev, *v_prev;
 } fc_vit_cache;
 
 /* The encoder's patch merger (Qwen2.5-VL style; host struct, device bf16 pointers): each
@@ -364,9 +369,11 @@ fc_status fc_vit_block_forward(fc_ctx *ctx, const fc_vit_desc *layer, const fc_v
 
 /* The encoder cache's preparation for a new frame (Sec. 4.1 / Eq. 4-2 at patch level):
  * every reused merged token takes the merge^2 patch rows of K, V (from the cache, which
- * holds the previous frame) and of the outputs (y_prev into y_cur) of its source token
- * (I + di, J + dj).  shift [B][2], reuse_mask [B][grid_h grid_w]: from fc_select with
- * the same merge.  y_prev, y_cur: [B][patches][d_model] bf16, distinct. */
+ * holds the previous frame, or from cache->k_prev / v_prev) and of the outputs (y_prev
+ * into y_cur) of its source token (I + di, J + dj).  shift [B][2], reuse_mask
+ * [B][grid_h grid_w]: from fc_select with the same merge.  y_prev, y_cur:
+ * [B][patches][d_model] bf16, distinct, or both NULL (no output rows are moved: a block
+ * reads only the recomputed rows of its input, the merger only the recomputed tokens). */
 fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                               const uint8_t *reuse_mask, int32_t B, void *stream);

@@ -616,12 +616,19 @@ fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vi
                               const uint8_t *reuse_mask, int32_t B, void *stream) {
   fc_status st = check_vit(ctx, layer, cache, B, "fc_vit_cache_update");
   if (st != FC_OK) return st;
-  if (!y_prev || !y_cur || !shift || !reuse_mask)
-    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: null buffer");
-  if (y_prev == y_cur) return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: y_prev and y_cur alias");
+  if (!shift || !reuse_mask || (!y_prev) != (!y_cur))
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: null shift or reuse mask, or only one of "
+                "y_prev and y_cur");
+  if (y_prev && y_prev == y_cur)
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: y_prev and y_cur alias");
+  if ((!cache->k_prev) != (!cache->v_prev) ||
+      (cache->k_prev && (cache->k_prev == cache->k || cache->v_prev == cache->v)))
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: k_prev and v_prev must both be given, "
+                "apart from k and v, or both be NULL");
   const long mm = (long)cache->merge * cache->merge;
   // the in-place overwrite of the one frame slot stages the old K and V rows
-  if (2L * B * cache->grid_h * cache->grid_w * mm * layer->d_model > (long)ctx->stage_elems)
+  if (!cache->k_prev &&
+      2L * B * cache->grid_h * cache->grid_w * mm * layer->d_model > (long)ctx->stage_elems)
     return fail(FC_ERR_CAPACITY, "fc_vit_cache_update: the frame's K/V rows exceed the context's "
                 "staging buffer");
   if ((st = use_device(ctx)) != FC_OK) return st;

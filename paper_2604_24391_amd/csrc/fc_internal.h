@@ -215,6 +215,13 @@ fc_status run_plain_gemm(fc_ctx *ctx, hipStream_t st, const char *name, const ui
                          const int **dsplits_used, int *tiles);
 
 // Vision-encoder block with partial recompute and its cache update (vit.hip).
+// Reused tokens' K/V rows (and output rows, when y_prev is given) copied from a previous
+// frame's cache [B][N][kvw] into a distinct current one, token (I, J) from (I + di, J + dj)
+// (the layer remap with source and destination in separate buffers: no staging).
+fc_status launch_remap_copy(fc_ctx *ctx, const uint16_t *ksrc, const uint16_t *vsrc, uint16_t *kdst,
+                            uint16_t *vdst, const uint16_t *y_prev, uint16_t *y_cur, int N, int kvw,
+                            int d, int grid_w, const int32_t *shift, const uint8_t *reuse, int B,
+                            hipStream_t st);
 fc_status launch_vit_block(fc_ctx *ctx, const fc_vit_desc &L, const fc_vit_cache &c,
                            const uint16_t *x, const int32_t *idx, const int32_t *nrec,
                            uint16_t *y, int B, hipStream_t st);

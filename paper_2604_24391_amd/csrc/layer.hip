@@ -2320,6 +2320,37 @@ fc_status launch_cache_update(fc_ctx *ctx, const fc_layer_desc &L, const fc_kv_c
   return FC_OK;
 }
 
+fc_status launch_remap_copy(fc_ctx *ctx, const uint16_t *ksrc, const uint16_t *vsrc, uint16_t *kdst,
+                            uint16_t *vdst, const uint16_t *y_prev, uint16_t *y_cur, int N, int kvw,
+                            int d, int grid_w, const int32_t *shift, const uint8_t *reuse, int B,
+                            hipStream_t st) {
+  CacheArgs c{};
+  c.kc = kdst;
+  c.vc = vdst;
+  c.ksrc = ksrc;
+  c.vsrc = vsrc;
+  c.src_bstride = (long)N * kvw;
+  c.src_row0 = 0;
+  c.y_prev = y_prev;
+  c.y_cur = y_cur;
+  c.shift = shift;
+  c.reuse = reuse;
+  c.N = N;
+  c.S = N;
+  c.kvw = kvw;
+  c.d = d;
+  c.gw = grid_w;
+  c.gh = N / grid_w;
+  c.cur_row0 = 0;
+  c.kv_copy = 1;
+  c.y_copy = y_prev != nullptr;
+  ProfScope ps(ctx, st, "fc_cache_update");
+  const long chunks = (long)N * cache_chunks(c);
+  hipLaunchKernelGGL(k_cache_update, dim3((unsigned)((chunks + 255) / 256), B), dim3(256), 0, st, c);
+  FC_LAUNCH_OK(st, "k_cache_update");
+  return FC_OK;
+}
+
 fc_status launch_cache_update_layers(fc_ctx *ctx, const fc_layer_desc &L, int n_layers,
                                      const fc_kv_cache *kvs, const uint16_t *const *y_prev,
                                      uint16_t *const *y_cur, const int32_t *shift,

@@ -770,8 +770,13 @@ fc_status launch_vit_cache_update(fc_ctx *ctx, const fc_vit_desc &L, const fc_vi
                                   const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                                   const uint8_t *reuse, int B, hipStream_t st) {
   // a merged token's patch rows are contiguous: the token-level remap with rows of
-  // m^2 patches (one frame slot, whose in-place overwrite stages the old rows)
+  // m^2 patches, from a separate previous-frame cache, or in place in the one frame
+  // slot (whose overwrite stages the old rows)
   const int mm = c.merge * c.merge;
+  if (c.k_prev)
+    return launch_remap_copy(ctx, c.k_prev, c.v_prev, c.k, c.v, y_prev, y_cur,
+                             c.grid_h * c.grid_w, mm * L.d_model, mm * L.d_model, c.grid_w,
+                             shift, reuse, B, st);
   fc_layer_desc ld{};
   ld.d_model = mm * L.d_model;
   ld.n_heads = mm * L.n_heads;

@@ -94,7 +94,8 @@ class fc_merger_desc(ctypes.Structure):
 
 class fc_vit_cache(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("grid_h", c_int32), ("grid_w", c_int32),
-                ("merge", c_int32), ("window", c_int32)]
+                ("merge", c_int32), ("window", c_int32), ("k_prev", c_void_p),
+                ("v_prev", c_void_p)]
 
 
 def lib() -> ctypes.CDLL:
@@ -608,18 +609,24 @@ class VitDesc:
 @dataclass
 class VitCache:
     """One block's encoder cache: k, v [B, grid_h grid_w merge^2, n_heads, head_dim] bf16
-    (patch rows token-major); window: attention window side in merged tokens, 0 = full."""
+    (patch rows token-major); window: attention window side in merged tokens, 0 = full.
+    k_prev, v_prev (fc_vit_cache_update only): the previous frame's cache in separate
+    buffers, or None (k, v hold it and are remapped in place)."""
     k: torch.Tensor
     v: torch.Tensor
     grid_h: int
     grid_w: int
     merge: int = 2
     window: int = 4
+    k_prev: torch.Tensor | None = None
+    v_prev: torch.Tensor | None = None
 
     def c(self, B: int, d: int) -> fc_vit_cache:
         n = B * self.grid_h * self.grid_w * self.merge * self.merge * d
+        kp = _ptr(self.k_prev, torch.bfloat16, n, "k_prev") if self.k_prev is not None else c_void_p(0)
+        vp = _ptr(self.v_prev, torch.bfloat16, n, "v_prev") if self.v_prev is not None else c_void_p(0)
         return fc_vit_cache(_ptr(self.k, torch.bfloat16, n, "k"), _ptr(self.v, torch.bfloat16, n, "v"),
-                            self.grid_h, self.grid_w, self.merge, self.window)
+                            self.grid_h, self.grid_w, self.merge, self.window, kp, vp)
 
 
 def fc_vit_block_forward(ctx: Context, layer: VitDesc, cache: VitCache, x: torch.Tensor,
@@ -638,16 +645,19 @@ def fc_vit_block_forward(ctx: Context, layer: VitDesc, cache: VitCache, x: torch
         _stream(stream)))
 
 
-def fc_vit_cache_update(ctx: Context, layer: VitDesc, cache: VitCache, y_prev: torch.Tensor,
-                        y_cur: torch.Tensor, shift: torch.Tensor, reuse_mask: torch.Tensor,
-                        stream=None):
-    B = y_cur.shape[0]
+def fc_vit_cache_update(ctx: Context, layer: VitDesc, cache: VitCache,
+                        y_prev: torch.Tensor | None, y_cur: torch.Tensor | None,
+                        shift: torch.Tensor, reuse_mask: torch.Tensor, stream=None):
+    """The encoder cache's remap (y_prev = y_cur = None: no output rows moved)."""
+    B = shift.shape[0]
     n = cache.grid_h * cache.grid_w
     rows = B * n * cache.merge * cache.merge * layer.d_model
     cl, cc = layer.c(), cache.c(B, layer.d_model)
+    yp = _ptr(y_prev, torch.bfloat16, rows, "y_prev") if y_prev is not None else c_void_p(0)
+    yc = _ptr(y_cur, torch.bfloat16, rows, "y_cur") if y_cur is not None else c_void_p(0)
     _check(lib().fc_vit_cache_update(
-        ctx.handle, ctypes.byref(cl), ctypes.byref(cc), _ptr(y_prev, torch.bfloat16, rows, "y_prev"),
-        _ptr(y_cur, torch.bfloat16, rows, "y_cur"), _ptr(shift, torch.int32, 2 * B, "shift"),
+        ctx.handle, ctypes.byref(cl), ctypes.byref(cc), yp, yc,
+        _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * n, "reuse_mask"), B, _stream(stream)))
 
 

@@ -403,6 +403,23 @@ int main() {
     EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, i32, u8, 1, nullptr));
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, h16, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, nullptr, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &vc, nullptr, nullptr, i32, u8, 1, nullptr));
+    fc_vit_cache c3 = vc;
+    c3.k_prev = y2;                    // k_prev without v_prev
+    EXPECT(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    c3.v_prev = h16;                   // v_prev is v itself
+    EXPECT(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    c3.v_prev = y2;
+    EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr));
+    // separate buffers need no staging: with a one-element staging buffer only the
+    // in-place remap is refused
+    fc_vit_cache c4 = vc;
+    const size_t stage_keep = ctx->stage_elems;
+    ctx->stage_elems = 1;
+    EXPECT(fc_vit_cache_update(ctx, &vd, &c4, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_CAPACITY);
+    EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr));
+    ctx->stage_elems = stage_keep;
   }
   {
     // patch merger

@@ -142,7 +142,11 @@ def test_qwen_vit_block(fc, ctx):
     print(f"worst rel-L2 {worst:.2e}")
 
 
-def test_vit_cache_update_matches_oracle(fc, ctx):
+@pytest.mark.parametrize("mode", ["in_place", "separate", "separate_no_y"])
+def test_vit_cache_update_matches_oracle(fc, ctx, mode):
+    """in_place: the cache holds the previous frame and is remapped in place; separate:
+    the reused rows are copied from a previous-frame cache into a distinct one, whose
+    other rows stay as they were; separate_no_y: the same without the output rows."""
     sh = SMALL
     gh, gw, m, B = 8, 8, 2, 2
     rng = np.random.default_rng(330)
@@ -156,26 +160,45 @@ def test_vit_cache_update_matches_oracle(fc, ctx):
     for b in range(B):
         al = osel.align_mask(gh, gw, *shifts[b]).ravel()
         reuse[b] = al & (rng.random(gh * gw) < 0.6)
-    kg, vg = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v)
-    ypg, ycg = fcutil.bf16_gpu(yp), fcutil.bf16_gpu(yc)
     wt = fcdata.vit_weights(331, sh)
-    fc.fc_vit_cache_update(ctx, gpu_desc(fc, wt, sh), fc.VitCache(kg, vg, gh, gw, m, 4), ypg, ycg,
-                           torch.from_numpy(shifts).cuda(), torch.from_numpy(reuse).cuda())
+    # the destination of the separate modes: stale rows from an older frame
+    k_old = fcdata.bf16_round(rng.standard_normal(k.shape, dtype=np.float32))
+    v_old = fcdata.bf16_round(rng.standard_normal(v.shape, dtype=np.float32))
+    if mode == "in_place":
+        kg, vg = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v)
+        cache = fc.VitCache(kg, vg, gh, gw, m, 4)
+    else:
+        kg, vg = fcutil.bf16_gpu(k_old), fcutil.bf16_gpu(v_old)
+        cache = fc.VitCache(kg, vg, gh, gw, m, 4, k_prev=fcutil.bf16_gpu(k), v_prev=fcutil.bf16_gpu(v))
+    ypg, ycg = fcutil.bf16_gpu(yp), fcutil.bf16_gpu(yc)
+    no_y = mode == "separate_no_y"
+    fc.fc_vit_cache_update(ctx, gpu_desc(fc, wt, sh), cache, None if no_y else ypg,
+                           None if no_y else ycg, torch.from_numpy(shifts).cuda(),
+                           torch.from_numpy(reuse).cuda())
     torch.cuda.synchronize()
+    mm = m * m
     for b in range(B):
         ko, vo, yo = ov.vit_cache_update(k[b], v[b], yp[b], yc[b], tuple(shifts[b]), reuse[b], gw, m)
+        if mode != "in_place":
+            moved = np.repeat(reuse[b] != 0, mm)
+            ko = np.where(moved[:, None, None], ko, k_old[b])
+            vo = np.where(moved[:, None, None], vo, v_old[b])
         np.testing.assert_array_equal(fcutil.bf16_np(kg)[b], ko)
         np.testing.assert_array_equal(fcutil.bf16_np(vg)[b], vo)
-        np.testing.assert_array_equal(fcutil.bf16_np(ycg)[b], yo)
+        np.testing.assert_array_equal(fcutil.bf16_np(ycg)[b], yc[b] if no_y else yo)
 
 
-def test_encoder_chain_driven_by_selection(fc, ctx):
+@pytest.mark.parametrize("two_caches", [False, True])
+def test_encoder_chain_driven_by_selection(fc, ctx, two_caches):
     """Four frames of a camera trajectory (224 x 224, 2 x 2 merge, 64 tokens; steps up to
     30 px, so the shifts found are (-1, 0), (1, 0) and (4, 2) tokens): each step
     selects on the GPU, remaps the encoder cache, runs one vision block on the recomputed
     tokens and the patch merger on their outputs; the oracle runs the same chain from
     the same start.  The
-    selection must match bit for bit and the block's rows as in the single-call tests."""
+    selection must match bit for bit and the block's rows as in the single-call tests.
+    two_caches: the encoder cache alternates between two buffers (the remap copies the
+    reused rows from the previous one, no staging) and no output rows are remapped (a
+    block reads only the recomputed rows of its input), so y is compared on those rows."""
     sh = SMALL
     frames = fcdata.episode_frames(43, size=224, n_frames=4, max_step=30)
     m, gh, gw = 2, 8, 8
@@ -188,9 +211,9 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
     rng = np.random.default_rng(341)
     k0 = fcdata.bf16_round(rng.standard_normal((np_, sh.heads, sh.hd), dtype=np.float32))
     y0 = fcdata.bf16_round(rng.standard_normal((np_, sh.d), dtype=np.float32))
-    kg, vg = fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(k0[None])
+    kvs = [(fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(k0[None])),
+           (fcutil.bf16_gpu(k0[None]), fcutil.bf16_gpu(k0[None]))]
     ys = [fcutil.bf16_gpu(y0[None]), fcutil.bf16_gpu(y0[None])]
-    cache = fc.VitCache(kg, vg, gh, gw, m, 4)
     ko, vo, yo = ov.f32(k0), ov.f32(k0), [ov.f32(y0), ov.f32(y0)]
     sel = fc.SelectOut.alloc(1, gh * gw)
     fr = torch.from_numpy(frames).cuda()
@@ -202,7 +225,14 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
         x = fcdata.bf16_round(rng.standard_normal((np_, sh.d), dtype=np.float32))
         nxt = 1 - cur
         fc.fc_select(ctx, prm, None if s == 0 else fr[s - 1:s], fr[s:s + 1], sel)
-        fc.fc_vit_cache_update(ctx, desc, cache, ys[cur], ys[nxt], sel.shift, sel.reuse_mask)
+        if two_caches:
+            kg, vg = kvs[nxt]
+            cache = fc.VitCache(kg, vg, gh, gw, m, 4, k_prev=kvs[cur][0], v_prev=kvs[cur][1])
+            fc.fc_vit_cache_update(ctx, desc, cache, None, None, sel.shift, sel.reuse_mask)
+        else:
+            kg, vg = kvs[0]
+            cache = fc.VitCache(kg, vg, gh, gw, m, 4)
+            fc.fc_vit_cache_update(ctx, desc, cache, ys[cur], ys[nxt], sel.shift, sel.reuse_mask)
         fc.fc_vit_block_forward(ctx, desc, cache, fcutil.bf16_gpu(x[None]), sel.recompute_idx,
                                 sel.n_recompute, ys[nxt])
         torch.cuda.synchronize()
@@ -216,8 +246,10 @@ def test_encoder_chain_driven_by_selection(fc, ctx):
         rows = (res.recompute_idx[:, None].astype(np.int64) * mm + np.arange(mm)).ravel()
         yg = ov.f32(fcutil.bf16_np(ys[nxt])[0])
         kgn = ov.f32(fcutil.bf16_np(kg)[0])
-        assert fcutil.rel_l2(yg, y) <= fcutil.LAYER_RTOL, s
+        if not two_caches:
+            assert fcutil.rel_l2(yg, y) <= fcutil.LAYER_RTOL, s
         assert fcutil.rel_l2(kgn, ko) <= fcutil.LAYER_RTOL, s
+        assert fcutil.rel_l2(ov.f32(fcutil.bf16_np(vg)[0]), vo) <= fcutil.LAYER_RTOL, s
         if rows.size:
             assert fcutil.rel_l2(yg[rows], y[rows]) <= fcutil.LAYER_RTOL, s
         # the merger on the block's outputs: the decoder's input rows of the recomputed tokens
