@@ -1182,6 +1182,7 @@ def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
         that step's mask, extrapolated to a whole step (select + 28 layers);
       * the one-layer workload at every reuse ratio (one call each);
       * selection of 448x448 pairs and the tiny configuration;
+      * one vision block at 50 % reuse and the merger on its recomputed tokens;
       * a single-core leg: this thread pinned to one core with one BLAS thread, for the
         selection of one pair and one layer call at 0 % reuse.
     cores = the CPUs this process may run on (all-core figures)."""
@@ -1229,6 +1230,25 @@ def cpu_baseline(fc, torch, frames_np, lay, shape, sel, prm, T, N, Wn, L, gw):
     ol.layer_partial(tx, tres.recompute_idx, tk, tk, tx, ol.Layout(T=32, N=256, W=1, head=0),
                      twt, tshape)
     other["tiny_select_plus_layer_ms"] = round((time.perf_counter() - t0) * 1e3, 2)
+    # the vision path: one Qwen2.5-VL vision block (windows of 4 tokens) at 50 % reuse on a
+    # 448x448 frame, and the merger on the recomputed tokens
+    from oracle import vit as ov
+    vs = fcdata.QWEN_VIT
+    vwt = fcdata.vit_weights(21, vs)
+    vsh = ov.VitShape(d=vs.d, heads=vs.heads, hd=vs.hd, ffn=vs.ffn)
+    np_v = 1024
+    vx = fcdata.bf16_round(rng.standard_normal((np_v, vs.d), dtype=np.float32))
+    vk = fcdata.bf16_round(rng.standard_normal((np_v, vs.heads, vs.hd), dtype=np.float32))
+    vids = fcdata.random_reuse_ids(250, 256, 50)
+    t0 = time.perf_counter()
+    vy, _, _ = ov.vit_block_partial(vx, vids, vk, vk, vx, vwt, vsh, 16, 16, 2, 4)
+    other["vit_block_reuse50_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+    msh = fcdata.QWEN_MERGER
+    mwt = fcdata.merger_weights(22, msh)
+    t0 = time.perf_counter()
+    ov.merger_rows(fcdata.bf16_round(vy), vids, mwt,
+                   ov.MergerShape(d=msh.d, m=msh.m, d_out=msh.d_out))
+    other["merger_reuse50_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
     # single core: this thread on one CPU, one BLAS thread
     single = None
     try:
