@@ -338,7 +338,23 @@ size_t fc_slot_state_bytes(int32_t B, int32_t S);
 fc_status fc_slot_map_init(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
                            int32_t B, void *stream);
 
-/* The partial-recompute decoder layer for B batch items.
+/* fc_cache_step flags */
+#define FC_ADVANCE_WINDOW 1  /* kv->head = (kv->head + 1) mod window before anything else */
+#define FC_REMAP 2           /* then fc_cache_update on the (advanced) layout */
+
+/* The step's cache preparation for one layer with the window advance done by the library
+ * (Sec. 4.1: the frame window moves on, reused tokens take their aligned sources' rows):
+ * flags FC_ADVANCE_WINDOW and/or FC_REMAP.  kv->head is written on the host (the descriptor
+ * is the caller's); the arguments of FC_REMAP are those of fc_cache_update (shift,
+ * reuse_mask, y_prev, y_cur and grid_w are not read without it).  Flags outside the two
+ * bits, or none, are FC_ERR_INVALID_ARG.  A failing remap leaves the head advanced. */
+fc_status fc_cache_step(fc_ctx *ctx, const fc_layer_desc *layer, fc_kv_cache *kv,
+                        const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                        const uint8_t *reuse_mask, int32_t grid_w, int32_t flags, int32_t B,
+                        void *stream);
+
+/* The partial-recompute decoder layer for B batch items (Sec. 4.1: the tokens that are
+ * not reused are recomputed; the per-step computation flow of Sec. 5.2).
  *   x_cur:         [B][N][d_model] bf16 layer input of the current frame's tokens;
  *                  only rows listed in recompute_idx are read;
  *   recompute_idx: [B][N] ascending token ids, n_recompute: [B] (from fc_select);

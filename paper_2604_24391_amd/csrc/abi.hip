@@ -523,6 +523,20 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
                                  reinterpret_cast<hipStream_t>(stream));
 }
 
+fc_status fc_cache_step(fc_ctx *ctx, const fc_layer_desc *layer, fc_kv_cache *kv,
+                        const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
+                        const uint8_t *reuse_mask, int32_t grid_w, int32_t flags, int32_t B,
+                        void *stream) {
+  if (!ctx) return fail(FC_ERR_INVALID_ARG, "fc_cache_step: null context");
+  if (!kv) return fail(FC_ERR_INVALID_ARG, "fc_cache_step: null cache descriptor");
+  if (flags <= 0 || (flags & ~(FC_ADVANCE_WINDOW | FC_REMAP)))
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_step: flags %d (FC_ADVANCE_WINDOW | FC_REMAP)", flags);
+  if (kv->window < 1) return fail(FC_ERR_SHAPE, "fc_cache_step: window %d", kv->window);
+  if (flags & FC_ADVANCE_WINDOW) kv->head = (kv->head + 1) % kv->window;
+  if (!(flags & FC_REMAP)) return FC_OK;
+  return fc_cache_update(ctx, layer, kv, y_prev, y_cur, shift, reuse_mask, grid_w, B, stream);
+}
+
 fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_t n_layers,
                                  const fc_kv_cache *kvs, const uint16_t *const *y_prev,
                                  uint16_t *const *y_cur, const int32_t *shift,

@@ -30,7 +30,7 @@ FLAG_ALIGNED, FLAG_FRESH, FLAG_CAND = 1, 2, 4
 
 EXPORTS = ("fc_version", "fc_last_error", "fc_create", "fc_destroy", "fc_select",
            "fc_select_noalloc", "fc_select_state_bytes", "fc_select_carry", "fc_cache_update",
-           "fc_cache_update_layers", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
+           "fc_cache_update_layers", "fc_cache_step", "fc_layer_forward", "fc_layer_forward_trail", "fc_debug",
            "fc_phase_correlate", "fc_phase_correlate_rotation", "fc_vit_block_forward",
            "fc_vit_cache_update", "fc_vit_merger_forward", "fc_slot_state_bytes",
            "fc_slot_map_init",
@@ -124,6 +124,9 @@ def lib() -> ctypes.CDLL:
         L.fc_cache_update.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
                                       ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
                                       c_void_p, c_int32, c_int32, c_void_p]
+        L.fc_cache_step.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc),
+                                    ctypes.POINTER(fc_kv_cache), c_void_p, c_void_p, c_void_p,
+                                    c_void_p, c_int32, c_int32, c_int32, c_void_p]
         L.fc_cache_update_layers.argtypes = [c_void_p, ctypes.POINTER(fc_layer_desc), c_int32,
                                              ctypes.POINTER(fc_kv_cache), ctypes.POINTER(c_void_p),
                                              ctypes.POINTER(c_void_p), c_void_p, c_void_p, c_int32,
@@ -556,6 +559,27 @@ def fc_cache_update(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev: torch.T
         _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur"),
         _ptr(shift, torch.int32, 2 * B, "shift"),
         _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask"), grid_w, B, _stream(stream)))
+
+
+FC_ADVANCE_WINDOW, FC_REMAP = 1, 2
+
+
+def fc_cache_step(ctx: Context, layer: LayerDesc, kv: KVCache, y_prev, y_cur, shift, reuse_mask,
+                  grid_w: int, flags: int, B: int = 1, stream=None):
+    """fc_cache_update with the window advance done by the library (FC_ADVANCE_WINDOW,
+    FC_REMAP); the head the library writes is copied back into kv."""
+    N, d = kv.frame_tokens, layer.d_model
+    cl = layer.c()
+    ck = kv.c(B, layer.n_kv_heads * layer.head_dim)
+    remap = bool(flags & FC_REMAP)
+    _check(lib().fc_cache_step(
+        ctx.handle, ctypes.byref(cl), ctypes.byref(ck),
+        _ptr(y_prev, torch.bfloat16, B * N * d, "y_prev") if remap else c_void_p(0),
+        _ptr(y_cur, torch.bfloat16, B * N * d, "y_cur") if remap else c_void_p(0),
+        _ptr(shift, torch.int32, 2 * B, "shift") if remap else c_void_p(0),
+        _ptr(reuse_mask, torch.uint8, B * N, "reuse_mask") if remap else c_void_p(0),
+        grid_w, flags, B, _stream(stream)))
+    kv.head = int(ck.head)
 
 
 def fc_cache_update_layers(ctx: Context, layer: LayerDesc, kvs, y_prevs, y_curs,

@@ -299,6 +299,22 @@ int main() {
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, h16, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 15, 1, nullptr), FC_ERR_SHAPE);
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, nullptr, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
+    {
+      fc_kv_cache ks = kv;
+      const int h0 = ks.head;
+      EXPECT(fc_cache_step(ctx, &L, &ks, h16, y2, i32, u8, 16, 0, 1, nullptr), FC_ERR_INVALID_ARG);
+      EXPECT(fc_cache_step(ctx, &L, &ks, h16, y2, i32, u8, 16, 4, 1, nullptr), FC_ERR_INVALID_ARG);
+      EXPECT(fc_cache_step(nullptr, &L, &ks, h16, y2, i32, u8, 16, FC_REMAP, 1, nullptr), FC_ERR_INVALID_ARG);
+      EXPECT(fc_cache_step(ctx, &L, nullptr, h16, y2, i32, u8, 16, FC_REMAP, 1, nullptr), FC_ERR_INVALID_ARG);
+      EXPECT(fc_cache_step(ctx, &L, &ks, nullptr, nullptr, nullptr, nullptr, 16, FC_ADVANCE_WINDOW, 1, nullptr), FC_OK);
+      if (ks.head != (h0 + 1) % ks.window) {
+        std::printf("FAIL: fc_cache_step did not advance the head\n");
+        ++g_fail;
+      }
+      EXPECT(fc_cache_step(ctx, &L, &ks, h16, y2, nullptr, u8, 16, FC_ADVANCE_WINDOW | FC_REMAP, 1, nullptr),
+             FC_ERR_INVALID_ARG);
+      EXPECT_DEVICE_FAIL(fc_cache_step(ctx, &L, &ks, h16, y2, i32, u8, 16, FC_REMAP, 1, nullptr));
+    }
     EXPECT_DEVICE_FAIL(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 16, 1, nullptr));
     fc_kv_cache kvs[3] = {kv, kv, kv};
     const uint16_t *yp[3] = {h16, h16, h16};

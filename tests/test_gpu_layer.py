@@ -240,6 +240,51 @@ def test_cache_update_matches_oracle(fc, ctx, W, head, B):
         assert mask[b].sum() > 0
 
 
+@pytest.mark.parametrize("W,head", [(1, 0), (3, 2)])
+def test_cache_step_advances_and_remaps(fc, ctx, W, head):
+    """fc_cache_step(FC_ADVANCE_WINDOW | FC_REMAP) = the head advanced by one slot, then
+    fc_cache_update: the descriptor's head and every byte of K, V and the output cache
+    equal the oracle's remap on the advanced layout."""
+    shape = GQA_SMALL
+    N, gw, T, B = 64, 8, 16, 2
+    rng = np.random.default_rng(7100 + W)
+    kvw = shape.n_kv * shape.hd
+    nxt = (head + 1) % W
+    lay = ol.Layout(T=T, N=N, W=W, head=nxt)
+    k = rng.integers(0, 1 << 16, size=(B, lay.S, shape.n_kv, shape.hd), dtype=np.uint16)
+    v = rng.integers(0, 1 << 16, size=k.shape, dtype=np.uint16)
+    y_prev = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+    y_cur = rng.integers(0, 1 << 16, size=(B, N, shape.d), dtype=np.uint16)
+    shifts = np.array([[1, -2], [-3, 1]], np.int32)
+    mask = np.zeros((B, N), np.uint8)
+    for b in range(B):
+        I, J = np.divmod(np.arange(N), gw)
+        si, sj = I + shifts[b, 0], J + shifts[b, 1]
+        mask[b] = (si >= 0) & (si < N // gw) & (sj >= 0) & (sj < gw) & (rng.random(N) < 0.6)
+    kc, vc = fcutil.bf16_gpu(k), fcutil.bf16_gpu(v)
+    yp, yc = fcutil.bf16_gpu(y_prev), fcutil.bf16_gpu(y_cur)
+    desc = fcutil.layer_desc(shape, fcutil.weights_gpu(fcdata.layer_weights(0, shape)))
+    kv = fc.KVCache(kc, vc, T, N, W, head)
+    fc.fc_cache_step(ctx, desc, kv, yp, yc, torch.from_numpy(shifts).cuda(),
+                     torch.from_numpy(mask).cuda(), gw, fc.FC_ADVANCE_WINDOW | fc.FC_REMAP, B)
+    torch.cuda.synchronize()
+    assert kv.head == nxt
+    kg, vg, yg = fcutil.bf16_np(kc), fcutil.bf16_np(vc), fcutil.bf16_np(yc)
+    for b in range(B):
+        ko, vo, yo = ol.cache_update(k[b].reshape(lay.S, kvw), v[b].reshape(lay.S, kvw),
+                                     y_prev[b], y_cur[b], tuple(shifts[b]), mask[b], gw, lay)
+        np.testing.assert_array_equal(kg[b].reshape(lay.S, kvw), ko)
+        np.testing.assert_array_equal(vg[b].reshape(lay.S, kvw), vo)
+        np.testing.assert_array_equal(yg[b], yo)
+    # the advance alone moves no byte
+    before = [fcutil.bf16_np(t) for t in (kc, vc, yc)]
+    fc.fc_cache_step(ctx, desc, kv, None, None, None, None, gw, fc.FC_ADVANCE_WINDOW, B)
+    torch.cuda.synchronize()
+    assert kv.head == (nxt + 1) % W
+    for a, t in zip(before, (kc, vc, yc)):
+        np.testing.assert_array_equal(fcutil.bf16_np(t), a)
+
+
 @pytest.mark.parametrize("W,head,n_layers", [(1, 0, 3), (3, 2, 4), (2, 1, 35)])
 def test_cache_update_layers_matches_oracle(fc, ctx, W, head, n_layers):
     """fc_cache_update_layers (one launch for many layers' caches) against the oracle's
