@@ -26,7 +26,7 @@ def fc():
 
 @pytest.fixture(scope="module")
 def ctx(fc):
-    c = fc.Context(fc.Caps(max_batch=2, max_height=448, max_width=448, max_tokens=1024,
+    c = fc.Context(fc.Caps(max_batch=3, max_height=448, max_width=448, max_tokens=1024,
                            max_seq=64, max_d_model=3584, max_ffn=18944, max_qkv=4608))
     yield c
     c.close()
@@ -370,3 +370,21 @@ def test_block_and_merger_replay_from_graph(fc, ctx):
         call()
         for a, b in zip(snap(), want):
             np.testing.assert_array_equal(a, b, err_msg=f"eager call after replay {rep}")
+
+
+@pytest.mark.parametrize("d,heads,hd,ffn,gh,gw,m,window,B", [
+    (256, 4, 64, 512, 8, 8, 2, 8, 3),     # head dim 64; one window of 256 keys (4 key blocks);
+                                          # 768 slots: the large-tile GEMM over 3 packed items
+    (256, 2, 128, 320, 16, 16, 1, 4, 2),  # head dim 128, merge 1 (a patch per token)
+    (384, 6, 64, 448, 6, 9, 2, 0, 1),     # full attention over 216 patches (ragged key block)
+])
+def test_block_variants(fc, ctx, d, heads, hd, ffn, gh, gw, m, window, B):
+    """Shapes beyond the Qwen block: other head dims (attention instantiations), windows
+    of several key blocks, merge 1, and items packed across tile borders; ragged
+    recompute sets per item (one of them empty when B = 3)."""
+    sh = fcdata.VitShape(d=d, heads=heads, hd=hd, ffn=ffn)
+    c = VitCase(sh, gh, gw, m, window, B, seed=400 + d + gh + window)
+    n = gh * gw
+    pct = [60, 15, 100][:B]
+    ids = [np.sort(fcdata.random_reuse_ids(401 + b, n, p)) for b, p in enumerate(pct)]
+    c.check(fc, ctx, ids)
