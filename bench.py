@@ -316,7 +316,7 @@ def main():
             t_c = v["flops"] / (BF16_PEAK_TFLOPS * 1e12)
             t_m = lb / (HBM_PEAK_GBS * 1e9)
             ceil[k] = round(t_c / max(t_c, t_m), 4)
-        result["north_star"] = dict(
+        result["targets"] = dict(
             selection_frac_hbm=result["select_batch"]["frac_hbm"], selection_target=0.60,
             layer_mfma_util={k: v["mfma_util"] for k, v in result["layer_ratios"].items()},
             layer_mfma_ceiling=ceil, layer_target=0.50)
