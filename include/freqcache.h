@@ -368,8 +368,8 @@ fc_status fc_layer_forward(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
                            const int32_t *n_recompute, uint16_t *y_cur, int32_t B,
                            void *stream);
 
-/* The vision-encoder side of the partial recompute (Sec. 4.1: flushed or refreshed
- * tokens are recomputed by the visual encoder; reused ones keep their cached results),
+/* The vision-encoder side of the partial recompute (Sec. 4.1: a flushed or refreshed
+ * token goes through the vision encoder again; a reused one keeps its cached results),
  * for one block.  The patches of the merged tokens recompute_idx[b][0 .. n_recompute[b])
  * (the selection's ids, ascending) go through the block: their raw k, v are written to
  * the cache, their queries attend to every key of their window (cached keys of reused

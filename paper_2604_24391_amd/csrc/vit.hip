@@ -1,6 +1,6 @@
 // Vision-encoder side of the partial recompute on gfx950: one Qwen2.5-VL-style vision
-// block over the patches of the recomputed merged tokens (Sec. 4.1: tokens that are not
-// reused are recomputed by the visual encoder), with the reused patches' keys and values
+// block over the patches of the recomputed merged tokens (Sec. 4.1: a token that is not
+// reused goes through the vision encoder again), with the reused patches' keys and values
 // taken from the encoder's per-layer cache.
 //
 // Rows: the recomputed patches of item b are slots b Np + j, j < n_recompute[b] m^2,
