@@ -548,43 +548,74 @@ __global__ __launch_bounds__(256) void k_red_qkv(RedArgs r) {
   const int c0 = blockIdx.y * 1024;
   const int c = c0 + threadIdx.x * 4;
   const int tok = tok_of(r.idx, slot, r.N);
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (c < r.ncols) v = sum_parts<SPL>(r, slot, c);
-  // 1/rms of the token's input row (d <= 8192: at most 4 chunks of 8 a thread)
+  const bool incol = c < r.ncols;
+  const bool rot = c < r.qw;                      // query columns are rotated
+  const int half = r.hd / 2;
+  // Every load that depends only on the token goes out before the first use, so the
+  // workgroup waits one memory round trip instead of three: the split partials and
+  // the bias of the thread's 4 columns, its chunks of the input row (for 1/rms; d <=
+  // 8192: at most 4 chunks of 8 a thread) and the rotary pairs of its query dims.
+  // Threads past the columns or the row read an in-range element and never use it.
+  const float *pp = r.part + slot * r.ncols + (incol ? c : 0);
+  const long stride = r.rows * r.ncols;
+  float4 u[SPL];
+#pragma unroll
+  for (int s = 0; s < SPL; ++s)
+    u[s] = *reinterpret_cast<const float4 *>(pp + min(s, r.splits - 1) * stride);
+  const uint2 bb = *reinterpret_cast<const uint2 *>(r.bias + (incol ? c : 0));
   const uint16_t *xr = r.x + ((long)b * r.N + tok) * r.d;
-  float ss = 0.f;
+  U16x8 xv[4];
 #pragma unroll
   for (int it = 0; it < 4; ++it) {
     const int cx = (it * 256 + threadIdx.x) * 8;
-    if (cx < r.d) {
-      const U16x8 xv = *reinterpret_cast<const U16x8 *>(xr + cx);
+    xv[it] = *reinterpret_cast<const U16x8 *>(xr + (cx < r.d ? cx : 0));
+  }
+  float2 cs[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss = fmaf(bf2f(xv.v[e]), bf2f(xv.v[e]), ss);
+  for (int e = 0; e < 4; ++e) {
+    const int k = ((c + e) % r.hd) % half;       // rotary frequency pair
+    cs[e] = r.rope[rot ? (long)rope_pos(r.mr, r.qpos0 + tok, k) * half + k : 0L];
+  }
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s = 0; s < SPL; ++s) {
+    const bool in = s < r.splits;
+    v.x += in ? u[s].x : 0.f;
+    v.y += in ? u[s].y : 0.f;
+    v.z += in ? u[s].z : 0.f;
+    v.w += in ? u[s].w : 0.f;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    if ((it * 256 + (int)threadIdx.x) * 8 < r.d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(bf2f(xv[it].v[e]), bf2f(xv[it].v[e]), ss);
     }
   }
   const float inv = 1.f / sqrtf(block_sum256(ss, qs) / (float)r.d + r.eps);
   float vv[4] = {0.f, 0.f, 0.f, 0.f};
-  if (c < r.ncols) {
+  if (incol) {
+    const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xFFFF0000u),
+                           __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xFFFF0000u)};
     vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) vv[e] = fmaf(vv[e], inv, bf2f(r.bias[c + e]));
+    for (int e = 0; e < 4; ++e) vv[e] = fmaf(vv[e], inv, bias[e]);
   }
   if (c0 < r.qw) {   // uniform: the block's query columns are rotated
     *reinterpret_cast<float4 *>(&qs[threadIdx.x * 4]) = make_float4(vv[0], vv[1], vv[2], vv[3]);
     __syncthreads();
-    if (c < r.qw) {
-      const int half = r.hd / 2;
+    if (rot) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int d = (c + e) % r.hd;                 // dim within the head
         const int lc = threadIdx.x * 4 + e;           // column within the block
-        const int k = d % half;                       // rotary frequency pair
-        const float2 cs = r.rope[(long)rope_pos(r.mr, r.qpos0 + tok, k) * half + k];
-        vv[e] = d < half ? vv[e] * cs.x - qs[lc + half] * cs.y : vv[e] * cs.x + qs[lc - half] * cs.y;
+        vv[e] = d < half ? vv[e] * cs[e].x - qs[lc + half] * cs[e].y
+                         : vv[e] * cs[e].x + qs[lc - half] * cs[e].y;
       }
     }
   }
-  if (c >= r.ncols) return;
+  if (!incol) return;
   uint16_t o[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) o[e] = f2bf(vv[e]);
