@@ -532,3 +532,30 @@ def test_batched_episode_qwen_layer_sampled(fc, ctx_episodes):
         for e in (ey, ek, ev):
             assert e <= fcutil.LAYER_RTOL
         assert np.linalg.norm(ys - yo) <= fcutil.LAYER_RTOL * np.linalg.norm(yo - xs) + 2 * rnd
+
+
+# The remaining head groupings the attention kernels are built for: MHA at head_dim 128,
+# two query heads per kv head at head_dim 64, four per kv head at head_dim 128.
+GROUPINGS = {
+    "mha_hd128": fcdata.LayerShape(d=512, n_heads=4, n_kv=4, hd=128, ffn=1024),
+    "gqa2_hd64": fcdata.LayerShape(d=512, n_heads=8, n_kv=4, hd=64, ffn=1024),
+    "gqa4_hd128": fcdata.LayerShape(d=512, n_heads=8, n_kv=2, hd=128, ffn=1024),
+}
+
+
+@pytest.mark.parametrize("name", sorted(GROUPINGS))
+def test_other_head_groupings(fc, ctx, name):
+    """Few-row path: two ragged items (30 % and 75 % reuse) on a ring of two frames."""
+    c = Case(GROUPINGS[name], T=64, N=256, W=2, head=1, B=2, seed=80)
+    worst = c.check(fc, ctx, [fcdata.random_reuse_ids(81, 256, 30),
+                              fcdata.random_reuse_ids(82, 256, 75)])
+    print(f"{name}: worst rel-L2 {worst:.2e}")
+
+
+@pytest.mark.parametrize("name", sorted(GROUPINGS))
+def test_batch_path_other_head_groupings(fc, ctx_big, name):
+    """Large-M path (2 x 1024 token slots): two ragged items at 20 % and 60 % reuse."""
+    c = Case(GROUPINGS[name], T=64, N=1024, W=1, head=0, B=2, seed=85)
+    worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(86, 1024, 20),
+                                  fcdata.random_reuse_ids(87, 1024, 60)])
+    print(f"{name}: worst rel-L2 {worst:.2e}")
