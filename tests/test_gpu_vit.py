@@ -310,6 +310,15 @@ def test_merger_small_ragged_and_edges(fc, ctx):
     check_merger(fc, ctx, SMALL_MERGER, 64, [np.arange(64, dtype=np.int32)], 352)
 
 
+@pytest.mark.parametrize("m", [1, 3, 4])
+def test_merger_other_merge_factors(fc, ctx, m):
+    """d 320 with 1 x 1, 3 x 3 and 4 x 4 merges (hidden 320, 2880, 5120) -> 256, 36
+    tokens: one item recomputing 60 % of them, one all of them."""
+    sh = fcdata.MergerShape(d=320, m=m, d_out=256)
+    check_merger(fc, ctx, sh, 36, [np.sort(fcdata.random_reuse_ids(370 + m, 36, 40)),
+                                   np.arange(36, dtype=np.int32)], 375 + m)
+
+
 def test_merger_qwen_shape(fc, ctx):
     """The Qwen2.5-VL merger (1280 x 4 = 5120 -> 5120 -> 3584) on a 448 x 448 frame's 256
     tokens, half of them recomputed."""
@@ -377,6 +386,9 @@ def test_block_and_merger_replay_from_graph(fc, ctx):
                                           # 768 slots: the large-tile GEMM over 3 packed items
     (256, 2, 128, 320, 16, 16, 1, 4, 2),  # head dim 128, merge 1 (a patch per token)
     (384, 6, 64, 448, 6, 9, 2, 0, 1),     # full attention over 216 patches (ragged key block)
+    (320, 4, 80, 448, 5, 6, 3, 2, 2),     # merge 3: windows of 2 x 2 tokens (36 keys), ragged
+                                          # last window row; 540 slots on the large tiles
+    (256, 4, 64, 512, 4, 4, 4, 0, 1),     # merge 4: full attention over 16 x 16 patches
 ])
 def test_block_variants(fc, ctx, d, heads, hd, ffn, gh, gw, m, window, B):
     """Shapes beyond the Qwen block: other head dims (attention instantiations), windows
