@@ -347,7 +347,8 @@ fc_status fc_slot_map_init(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_
  * flags FC_ADVANCE_WINDOW and/or FC_REMAP.  kv->head is written on the host (the descriptor
  * is the caller's); the arguments of FC_REMAP are those of fc_cache_update (shift,
  * reuse_mask, y_prev, y_cur and grid_w are not read without it).  Flags outside the two
- * bits, or none, are FC_ERR_INVALID_ARG.  A failing remap leaves the head advanced. */
+ * bits, or none, and a head outside [0, window) are FC_ERR_INVALID_ARG.  On any error
+ * kv->head is left as it was: it is written only once the remap has been launched. */
 fc_status fc_cache_step(fc_ctx *ctx, const fc_layer_desc *layer, fc_kv_cache *kv,
                         const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
                         const uint8_t *reuse_mask, int32_t grid_w, int32_t flags, int32_t B,

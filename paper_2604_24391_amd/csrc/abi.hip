@@ -532,9 +532,19 @@ fc_status fc_cache_step(fc_ctx *ctx, const fc_layer_desc *layer, fc_kv_cache *kv
   if (flags <= 0 || (flags & ~(FC_ADVANCE_WINDOW | FC_REMAP)))
     return fail(FC_ERR_INVALID_ARG, "fc_cache_step: flags %d (FC_ADVANCE_WINDOW | FC_REMAP)", flags);
   if (kv->window < 1) return fail(FC_ERR_SHAPE, "fc_cache_step: window %d", kv->window);
-  if (flags & FC_ADVANCE_WINDOW) kv->head = (kv->head + 1) % kv->window;
-  if (!(flags & FC_REMAP)) return FC_OK;
-  return fc_cache_update(ctx, layer, kv, y_prev, y_cur, shift, reuse_mask, grid_w, B, stream);
+  if (kv->head < 0 || kv->head >= kv->window)
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_step: head %d outside the window of %d frames",
+                kv->head, kv->window);
+  // the remap runs on the advanced layout; the caller's head changes only on success
+  fc_kv_cache next = *kv;
+  if (flags & FC_ADVANCE_WINDOW) next.head = (next.head + 1) % next.window;
+  if (flags & FC_REMAP) {
+    const fc_status st =
+        fc_cache_update(ctx, layer, &next, y_prev, y_cur, shift, reuse_mask, grid_w, B, stream);
+    if (st != FC_OK) return st;
+  }
+  kv->head = next.head;
+  return FC_OK;
 }
 
 fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_t n_layers,

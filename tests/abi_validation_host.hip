@@ -311,8 +311,20 @@ int main() {
         std::printf("FAIL: fc_cache_step did not advance the head\n");
         ++g_fail;
       }
+      const int h1 = ks.head;
       EXPECT(fc_cache_step(ctx, &L, &ks, h16, y2, nullptr, u8, 16, FC_ADVANCE_WINDOW | FC_REMAP, 1, nullptr),
              FC_ERR_INVALID_ARG);
+      if (ks.head != h1) {
+        std::printf("FAIL: a failing fc_cache_step moved the head\n");
+        ++g_fail;
+      }
+      {
+        fc_kv_cache kb = ks;
+        kb.head = kb.window;
+        EXPECT(fc_cache_step(ctx, &L, &kb, nullptr, nullptr, nullptr, nullptr, 16, FC_ADVANCE_WINDOW, 1,
+                             nullptr),
+               FC_ERR_INVALID_ARG);
+      }
       EXPECT_DEVICE_FAIL(fc_cache_step(ctx, &L, &ks, h16, y2, i32, u8, 16, FC_REMAP, 1, nullptr));
     }
     EXPECT_DEVICE_FAIL(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 16, 1, nullptr));
