@@ -200,13 +200,14 @@ typedef struct {
 typedef struct {
   uint16_t *k, *v;
   int32_t grid_h, grid_w;   /* merged-token grid of the frame */
-  int32_t merge;            /* patches per merged token side (1 or 2) */
+  int32_t merge;            /* patches per merged token side (1 to 4; Qwen2.5-VL: 2) */
   int32_t window;           /* attention window side in merged tokens (Qwen2.5-VL: 4,
                                i.e. 112 px at 14-px patches and 2 x 2 merge); 0 = full
                                attention over the frame */
   /* fc_vit_cache_update only: NULL, NULL = k, v hold the previous frame and are remapped
      in place (the frame's old rows staged first); otherwise the previous frame's k, v
-     (same layout, distinct buffers), from which the reused rows are copied into k, v
+     (same layout, buffers overlapping neither k nor v), from which the reused rows are
+     copied into k, v
      (callers alternate two caches per block; no staging) */
   const uint16_t *k_prev, *v_prev;
 } fc_vit_cache;
@@ -298,7 +299,7 @@ fc_status fc_layer_forward_trail(fc_ctx *ctx, const fc_layer_desc *layer, const 
  * y_cur[b][t] are copied from source token s = (I + di) grid_w + (J + dj) of the
  * previous frame (K/V) and of y_prev.  Other rows are left untouched (the layer
  * call rewrites them).
- *   y_prev, y_cur: [B][N][d_model] bf16, distinct buffers;
+ *   y_prev, y_cur: [B][N][d_model] bf16, non-overlapping (else FC_ERR_INVALID_ARG);
  *   shift [B][2], reuse_mask [B][N]: from fc_select; grid_w: token-grid width. */
 fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_cache *kv,
                           const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,
@@ -309,7 +310,8 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
  * pointers inside) are layer l's cache and output buffers.  The layers share `layer`'s
  * dimensions and the caches' text_tokens, frame_tokens, window, head and trail_tokens
  * (all advanced to the same step); otherwise FC_ERR_SHAPE.  No two layers' K, V or
- * output buffers may overlap (not checked): the layers are copied concurrently.
+ * output buffers may overlap: the layers are copied concurrently (checked for the output
+ * buffers: a y_cur overlapping any y_prev or another layer's y_cur is FC_ERR_INVALID_ARG).
  *   y_prev, y_cur: both NULL moves no output rows (the layer calls read only the
  *     recomputed rows of their inputs; skip them when the reused tokens' outputs are
  *     not consumed), else as in fc_cache_update.
@@ -389,7 +391,7 @@ fc_status fc_vit_block_forward(fc_ctx *ctx, const fc_vit_desc *layer, const fc_v
  * holds the previous frame, or from cache->k_prev / v_prev) and of the outputs (y_prev
  * into y_cur) of its source token (I + di, J + dj).  shift [B][2], reuse_mask
  * [B][grid_h grid_w]: from fc_select with the same merge.  y_prev, y_cur:
- * [B][patches][d_model] bf16, distinct, or both NULL (no output rows are moved: a block
+ * [B][patches][d_model] bf16, non-overlapping, or both NULL (no output rows are moved: a block
  * reads only the recomputed rows of its input, the merger only the recomputed tokens). */
 fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vit_cache *cache,
                               const uint16_t *y_prev, uint16_t *y_cur, const int32_t *shift,

@@ -33,6 +33,13 @@ fc_status fail(fc_status st, const char *fmt, ...) {
   return st;
 }
 
+// Whether the byte ranges [a, a + n) and [b, b + n) share a byte (both given): a remap
+// that reads one while writing the other would race.
+static bool overlap(const void *a, const void *b, size_t n) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return a && b && x < y + n && y < x + n;
+}
+
 // Debug mode: FC_DEBUG set to anything but "" or "0" when the library loads, or fc_debug.
 static std::atomic<int> g_debug{[] {
   const char *e = std::getenv("FC_DEBUG");
@@ -511,7 +518,8 @@ fc_status fc_cache_update(fc_ctx *ctx, const fc_layer_desc *layer, const fc_kv_c
   if (kv->slot_map)
     return fail(FC_ERR_INVALID_ARG, "fc_cache_update: a slot-mapped cache is remapped once for all "
                 "layers by fc_cache_update_layers");
-  if (y_prev == y_cur) return fail(FC_ERR_INVALID_ARG, "fc_cache_update: y_prev and y_cur alias");
+  if (fc::overlap(y_prev, y_cur, (size_t)B * kv->frame_tokens * layer->d_model * 2))
+    return fail(FC_ERR_INVALID_ARG, "fc_cache_update: y_prev and y_cur overlap");
   if (grid_w < 1 || kv->frame_tokens % grid_w)
     return fail(FC_ERR_SHAPE, "fc_cache_update: grid_w %d does not divide N=%d", grid_w,
                 kv->frame_tokens);
@@ -563,8 +571,8 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
   for (int l = 0; l < n_layers; ++l) {
     fc_status st = check_layer(ctx, layer, &kvs[l], B, "fc_cache_update_layers");
     if (st != FC_OK) return st;
-    if (y_prev && (!y_prev[l] || !y_cur[l] || y_prev[l] == y_cur[l]))
-      return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d: null or aliased outputs", l);
+    if (y_prev && (!y_prev[l] || !y_cur[l]))
+      return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d: null output buffer", l);
     if (kvs[l].text_tokens != kvs[0].text_tokens || kvs[l].frame_tokens != kvs[0].frame_tokens ||
         kvs[l].window != kvs[0].window || kvs[l].head != kvs[0].head ||
         kvs[l].trail_tokens != kvs[0].trail_tokens)
@@ -572,6 +580,16 @@ fc_status fc_cache_update_layers(fc_ctx *ctx, const fc_layer_desc *layer, int32_
     if (kvs[l].slot_map != kvs[0].slot_map)
       return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: layer %d's slot map differs from "
                   "layer 0's (one map serves all layers)", l);
+  }
+  if (y_prev) {
+    // one launch remaps every layer: no layer's output rows may overlap any layer's input
+    // rows or another layer's output rows
+    const size_t yb = (size_t)B * kvs[0].frame_tokens * layer->d_model * 2;
+    for (int l = 0; l < n_layers; ++l)
+      for (int m = 0; m < n_layers; ++m)
+        if (fc::overlap(y_prev[l], y_cur[m], yb) || (m != l && fc::overlap(y_cur[l], y_cur[m], yb)))
+          return fail(FC_ERR_INVALID_ARG, "fc_cache_update_layers: the output buffer of layer %d "
+                      "overlaps an input or output buffer of layer %d", m, l);
   }
   if (grid_w < 1 || kvs[0].frame_tokens % grid_w)
     return fail(FC_ERR_SHAPE, "fc_cache_update_layers: grid_w %d does not divide N=%d", grid_w,
@@ -643,13 +661,15 @@ fc_status fc_vit_cache_update(fc_ctx *ctx, const fc_vit_desc *layer, const fc_vi
   if (!shift || !reuse_mask || (!y_prev) != (!y_cur))
     return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: null shift or reuse mask, or only one of "
                 "y_prev and y_cur");
-  if (y_prev && y_prev == y_cur)
-    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: y_prev and y_cur alias");
-  if ((!cache->k_prev) != (!cache->v_prev) ||
-      (cache->k_prev && (cache->k_prev == cache->k || cache->v_prev == cache->v)))
-    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: k_prev and v_prev must both be given, "
-                "apart from k and v, or both be NULL");
   const long mm = (long)cache->merge * cache->merge;
+  const size_t rb = (size_t)B * cache->grid_h * cache->grid_w * mm * layer->d_model * 2;
+  if (fc::overlap(y_prev, y_cur, rb))
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: y_prev and y_cur overlap");
+  if ((!cache->k_prev) != (!cache->v_prev) ||
+      (cache->k_prev && (fc::overlap(cache->k_prev, cache->k, rb) || fc::overlap(cache->v_prev, cache->v, rb) ||
+                         fc::overlap(cache->k_prev, cache->v, rb) || fc::overlap(cache->v_prev, cache->k, rb))))
+    return fail(FC_ERR_INVALID_ARG, "fc_vit_cache_update: k_prev and v_prev must both be given, "
+                "apart from k and v (no overlap), or both be NULL");
   // the in-place overwrite of the one frame slot stages the old K and V rows
   if (!cache->k_prev &&
       2L * B * cache->grid_h * cache->grid_w * mm * layer->d_model > (long)ctx->stage_elems)

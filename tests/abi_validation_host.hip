@@ -81,6 +81,9 @@ int main() {
   uint16_t *h16 = reinterpret_cast<uint16_t *>(host);
   int32_t *i32 = reinterpret_cast<int32_t *>(host);
   uint8_t *u8 = host;
+  // buffers that a remap reads and writes at once must not overlap: stand-ins for
+  // distinct allocations, 1 TiB apart (never dereferenced either)
+  auto far16 = [](int i) { return reinterpret_cast<uint16_t *>((uintptr_t)(i + 1) << 40); };
 
   fc_select_out out{};
   out.sim = f;
@@ -295,8 +298,10 @@ int main() {
     EXPECT(fc_layer_forward_trail(ctx, &L, &c, h16, h16, 1, nullptr), FC_ERR_CAPACITY);
   }
   {
-    uint16_t *y2 = h16 + 8;
+    uint16_t *y2 = far16(0);
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, h16, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
+    // a partial overlap: 8 elements apart
+    EXPECT(fc_cache_update(ctx, &L, &kv, h16, h16 + 8, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 15, 1, nullptr), FC_ERR_SHAPE);
     EXPECT(fc_cache_update(ctx, &L, &kv, h16, y2, nullptr, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
     {
@@ -330,8 +335,12 @@ int main() {
     EXPECT_DEVICE_FAIL(fc_cache_update(ctx, &L, &kv, h16, y2, i32, u8, 16, 1, nullptr));
     fc_kv_cache kvs[3] = {kv, kv, kv};
     const uint16_t *yp[3] = {h16, h16, h16};
-    uint16_t *yc[3] = {y2, y2, y2};
+    uint16_t *yc[3] = {far16(1), far16(2), far16(3)};
     EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr));
+    yc[2] = yc[1] + 8;                 // two layers' outputs overlap
+    EXPECT(fc_cache_update_layers(ctx, &L, 3, kvs, yp, yc, i32, u8, 16, 1, nullptr),
+           FC_ERR_INVALID_ARG);
+    yc[2] = far16(3);
     EXPECT(fc_cache_update_layers(ctx, &L, 0, kvs, yp, yc, i32, u8, 16, 1, nullptr),
            FC_ERR_INVALID_ARG);
     EXPECT(fc_cache_update_layers(ctx, &L, INT_MIN, kvs, yp, yc, i32, u8, 16, 1, nullptr),
@@ -348,11 +357,11 @@ int main() {
     int32_t *smap = i32;
     fc_kv_cache mk = kv;
     mk.slot_map = smap;
-    uint16_t *y2 = h16 + 8;
+    uint16_t *y2 = far16(0);
     EXPECT(fc_cache_update(ctx, &L, &mk, h16, y2, i32, u8, 16, 1, nullptr), FC_ERR_INVALID_ARG);
     fc_kv_cache kvs[2] = {mk, mk};
     const uint16_t *yp[2] = {h16, h16};
-    uint16_t *yc[2] = {y2, y2};
+    uint16_t *yc[2] = {far16(1), far16(2)};
     EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 2, kvs, yp, yc, i32, u8, 16, 1, nullptr));
     EXPECT_DEVICE_FAIL(fc_cache_update_layers(ctx, &L, 2, kvs, nullptr, nullptr, i32, u8, 16, 1,
                                               nullptr));
@@ -427,8 +436,9 @@ int main() {
     c2 = vc;
     c2.k = nullptr;
     EXPECT(vfwd(vd, c2, 1), FC_ERR_INVALID_ARG);
-    uint16_t *y2 = h16 + 8;
+    uint16_t *y2 = far16(0);
     EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, i32, u8, 1, nullptr));
+    EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, h16 + 8, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, h16, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, y2, nullptr, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     EXPECT(fc_vit_cache_update(ctx, &vd, &vc, h16, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
@@ -437,6 +447,8 @@ int main() {
     c3.k_prev = y2;                    // k_prev without v_prev
     EXPECT(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     c3.v_prev = h16;                   // v_prev is v itself
+    EXPECT(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
+    c3.v_prev = h16 + 64;              // v_prev overlaps v in part
     EXPECT(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr), FC_ERR_INVALID_ARG);
     c3.v_prev = y2;
     EXPECT_DEVICE_FAIL(fc_vit_cache_update(ctx, &vd, &c3, nullptr, nullptr, i32, u8, 1, nullptr));
