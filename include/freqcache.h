@@ -258,7 +258,7 @@ size_t fc_select_state_bytes(int32_t B, int32_t H, int32_t W);
  *               or NULL at the first step (no previous frame: flushed, as fc_select
  *               with frames_prev = NULL);
  *   state_cur:  receives this frame's spectra; fc_select_state_bytes(B, H, W) bytes,
- *               not aliasing state_prev (callers alternate two buffers).
+ *               not overlapping state_prev (callers alternate two buffers).
  * Outputs are byte-identical to fc_select on the pixels of both frames.  The states
  * hold no meaning for other sizes or parameters of P (not checked). */
 fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *state_prev,

@@ -322,8 +322,8 @@ fc_status fc_select_carry(fc_ctx *ctx, const fc_select_params *prm, const void *
   if (prm->align_pixel)
     return fail(FC_ERR_UNSUPPORTED, "fc_select_carry: align_pixel needs the previous frame's "
                 "pixels; use fc_select");
-  if (state_cur == state_prev)
-    return fail(FC_ERR_INVALID_ARG, "fc_select_carry: state_prev and state_cur alias");
+  if (state_cur == state_prev || fc::overlap(state_prev, state_cur, fc_select_state_bytes(B, H, W)))
+    return fail(FC_ERR_INVALID_ARG, "fc_select_carry: state_prev and state_cur overlap");
   const int tp = prm->patch * prm->merge;
   const int M = (H / tp) * (W / tp);
   if (B > ctx->caps.max_batch || H > ctx->caps.max_height || W > ctx->caps.max_width ||

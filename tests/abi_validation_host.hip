@@ -163,6 +163,9 @@ int main() {
   EXPECT(fc_select(ctx, &p, f, f, 1, 896, 448, &out, nullptr), FC_ERR_CAPACITY);
   EXPECT_DEVICE_FAIL(fc_select(ctx, &p, f, f, 4, 448, 448, &out, nullptr));
   EXPECT(fc_select_carry(ctx, &p, host, f, host, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT(fc_select_carry(ctx, &p, host, f, host + 64, 1, 448, 448, &out, nullptr), FC_ERR_INVALID_ARG);
+  EXPECT_DEVICE_FAIL(fc_select_carry(ctx, &p, reinterpret_cast<unsigned char *>(far16(5)), f, host, 1,
+                                     448, 448, &out, nullptr));
   EXPECT(fc_select_carry(ctx, &p, nullptr, f, nullptr, 1, 448, 448, &out, nullptr),
          FC_ERR_INVALID_ARG);
   EXPECT(fc_select_carry(ctx, &p, nullptr, f, host, INT_MAX, 448, 448, &out, nullptr),
