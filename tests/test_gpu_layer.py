@@ -559,3 +559,14 @@ def test_batch_path_other_head_groupings(fc, ctx_big, name):
     worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(86, 1024, 20),
                                   fcdata.random_reuse_ids(87, 1024, 60)])
     print(f"{name}: worst rel-L2 {worst:.2e}")
+
+
+@pytest.mark.parametrize("slots", [False, True])
+def test_long_cache_few_rows(fc, ctx_big, slots):
+    """The few-row path (one item, 1024 tokens per frame) over a window of 4 frames plus
+    128 text rows, 4224 cached positions: twice the key blocks per split of the
+    benchmark's cache; on copied rows and on a slot-mapped cache."""
+    c = Case(GQA_SMALL, T=128, N=1024, W=4, head=2, B=1, seed=90,
+             slot_seed=91 if slots else None)
+    worst = c.check(fc, ctx_big, [fcdata.random_reuse_ids(92, 1024, 84)])
+    print(f"worst rel-L2 {worst:.2e}")
