@@ -185,3 +185,66 @@ def test_vision_outputs(fc):
             g.check()
     finally:
         ctx.close()
+
+
+def test_layers_remap_trail_slot_map_and_noalloc_outputs(fc):
+    """fc_cache_update_layers over three layers (with and without output rows),
+    fc_layer_forward_trail, fc_slot_map_init and the slot-mapped per-step update, and
+    fc_select_noalloc."""
+    shape = fcdata.LayerShape(d=512, n_heads=7, n_kv=1, hd=128, ffn=1024)
+    T, N, W, U, gw, B = 16, 64, 2, 24, 8, 2
+    S = T + W * N + U
+    ctx = fc.Context(fc.Caps(max_batch=B, max_height=224, max_width=224, max_tokens=N,
+                             max_seq=S, max_d_model=shape.d, max_ffn=shape.ffn,
+                             max_qkv=shape.qkv))
+    try:
+        rng = np.random.default_rng(12)
+        desc = fcutil.layer_desc(shape, fcutil.weights_gpu(fcdata.layer_weights(2, shape)))
+
+        def rnd(*shp):
+            return fcutil.bf16_gpu(fcdata.bf16_round(rng.standard_normal(shp, dtype=np.float32)))
+        g = Guarded()
+        shift = torch.tensor([[1, 0], [0, -1]], dtype=torch.int32, device="cuda")
+        reuse = torch.zeros(B, N, dtype=torch.uint8)
+        reuse[0, :40] = 1
+        reuse[1, 1::2] = 1
+        reuse = reuse.cuda()
+        kvs, yps, ycs = [], [], []
+        for _ in range(3):
+            k = g.new((B, S, shape.n_kv, shape.hd), torch.bfloat16, rnd(B, S, shape.n_kv, shape.hd))
+            v = g.new((B, S, shape.n_kv, shape.hd), torch.bfloat16, rnd(B, S, shape.n_kv, shape.hd))
+            kvs.append(fc.KVCache(k, v, T, N, W, head=1, trail_tokens=U))
+            yps.append(g.new((B, N, shape.d), torch.bfloat16, rnd(B, N, shape.d)))
+            ycs.append(g.new((B, N, shape.d), torch.bfloat16, rnd(B, N, shape.d)))
+        fc.fc_cache_update_layers(ctx, desc, kvs, yps, ycs, shift, reuse, gw)
+        fc.fc_cache_update_layers(ctx, desc, kvs, None, None, shift, reuse, gw)
+        g.check()
+        ids = np.sort(fcdata.random_reuse_ids(13, N, 40))
+        idx = torch.full((B, N), -1, dtype=torch.int32)
+        idx[:, :len(ids)] = torch.from_numpy(ids)
+        nrec = torch.tensor([len(ids), 5], dtype=torch.int32, device="cuda")
+        yt = g.new((B, U, shape.d), torch.bfloat16, rnd(B, U, shape.d))
+        fc.fc_layer_forward(ctx, desc, kvs[0], rnd(B, N, shape.d), idx.cuda(), nrec, ycs[0])
+        fc.fc_layer_forward_trail(ctx, desc, kvs[0], rnd(B, U, shape.d), yt)
+        g.check()
+        state = g.new((fc.slot_state_bytes(B, S) // 4,), torch.int32)
+        kvm = [fc.KVCache(kvs[i].k, kvs[i].v, T, N, W, head=1, trail_tokens=U, slot_map=state)
+               for i in range(2)]
+        fc.fc_slot_map_init(ctx, desc, kvm[0], B)
+        fc.fc_cache_update_layers(ctx, desc, kvm, None, None, shift, reuse, gw)
+        g.check()
+    finally:
+        ctx.close()
+    prev, cur, _ = fcdata.sel_pairs(3, batch=2, size=224)
+    g = Guarded()
+    B, N = 2, 64
+    out = fc.SelectOut(
+        sim=g.new((B, N), torch.float32), energy=g.new((B, N), torch.float64),
+        reuse_mask=g.new((B, N), torch.uint8), recompute_idx=g.new((B, N), torch.int32),
+        n_recompute=g.new((B,), torch.int32), shift=g.new((B, 2), torch.int32),
+        scalars=g.new((B, fc.freqcache.NSCALARS), torch.float64),
+        counts=g.new((B, fc.freqcache.NCOUNTS), torch.int32),
+        flags=g.new((B, N), torch.uint8))
+    fc.fc_select_noalloc(fc.SelectParams(merge=2), torch.from_numpy(prev).cuda(),
+                         torch.from_numpy(cur).cuda(), out)
+    g.check()
