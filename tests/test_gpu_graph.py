@@ -87,3 +87,52 @@ def test_captured_step_replays_match_eager(fc):
         for a, b in zip(snapshot(), want):
             np.testing.assert_array_equal(a, b, err_msg=f"eager step after replay {rep}")
     ctx.close()
+
+
+def test_captured_batch_selection_replays_match_eager(fc):
+    """fc_select on 64 pairs (the batch the selection benchmark times) captured into a
+    graph: every replay, after eager calls on other frames have overwritten the
+    outputs, must give the eager result byte for byte."""
+    B = 64
+    ctx = fc.Context(fc.Caps(max_batch=B, max_height=448, max_width=448, max_tokens=1024,
+                             max_seq=64, max_d_model=64, max_ffn=64, max_qkv=64))
+    try:
+        prev, cur, _ = fcdata.sel_pairs(1)
+        prev2, cur2, _ = fcdata.sel_pairs(2)
+        fp, fcur = torch.from_numpy(prev).cuda(), torch.from_numpy(cur).cuda()
+        gp, gcur = torch.from_numpy(prev2).cuda(), torch.from_numpy(cur2).cuda()
+        prm = fc.SelectParams()
+        out = fc.SelectOut.alloc(B, 1024)
+        keys = ("sim", "energy", "reuse_mask", "recompute_idx", "n_recompute", "shift", "scalars",
+                "counts", "flags")
+
+        def snap():
+            torch.cuda.synchronize()
+            return {k: getattr(out, k).cpu().numpy().copy() for k in keys}
+
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fc.fc_select(ctx, prm, fp, fcur, out)
+        torch.cuda.current_stream().wait_stream(side)
+        want = snap()
+        with torch.cuda.stream(side):
+            fc.fc_select(ctx, prm, gp, gcur, out)
+        torch.cuda.current_stream().wait_stream(side)
+        other = snap()
+        assert not np.array_equal(other["reuse_mask"], want["reuse_mask"])
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            fc.fc_select(ctx, prm, fp, fcur, out)
+        for rep in range(3):
+            fc.fc_select(ctx, prm, gp, gcur, out)            # eager, other frames
+            got = snap()
+            for k in keys:
+                np.testing.assert_array_equal(got[k], other[k], err_msg=f"eager {k}, round {rep}")
+            graph.replay()
+            got = snap()
+            for k in keys:
+                np.testing.assert_array_equal(got[k], want[k], err_msg=f"replay {k}, round {rep}")
+    finally:
+        ctx.close()

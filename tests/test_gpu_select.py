@@ -77,6 +77,14 @@ def test_selection_at_scale_all_pairs(fc, ctx):
           "min shift margin", min(m["shift"] for m in margins))
 
 
+def test_odd_batch_with_and_without_previous_frames(fc, ctx):
+    """19 pairs at 448x448 (an odd batch, not a power of two), every pair against the
+    oracle; then the same current frames with the previous frames missing (all-zero)."""
+    prev, cur, _ = fcdata.sel_pairs(17, batch=19)
+    compare(fc, ctx, fc.SelectParams(), prev, cur)
+    compare(fc, ctx, fc.SelectParams(), None, cur)
+
+
 def test_budget_clamped_to_candidates(fc, ctx):
     """Algorithm 1 takes K_final = min(K_reuse, |C|): with a 100 % budget on a pair
     rolled by one token (one row and one column unaligned, edge tokens refreshed)
